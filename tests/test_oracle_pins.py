@@ -1,0 +1,386 @@
+"""Pins of the CPU oracle against facts fixed outside it.
+
+Each check below is chosen so that a plausible slip in the oracle (a dropped
+term, a wrong sign or index, a transposed operand, the wrong rounding mode,
+the wrong branch of the SwiGLU) fails at least one of them:
+
+* IEEE fp16 rounding against Python's own half-precision packer (``struct``),
+* hand-derived quantisation / packing / routing examples (tests/golden),
+* exhaustive dequantisation against exact rational products,
+* GEMV / GEMM against exact rational brute force, integer grids with
+  closed-form answers and one-hot inputs,
+* routing against an independent repeated-argmax selection and the softmax's
+  closed-form ratios, bucketing against Python's stable ``sorted``,
+* the MoE layer against dense evaluation, a top-1 special case, identical
+  experts and a hand-computed scalar example; SiLU against its identities.
+"""
+
+import math
+import os
+import struct
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import qmatmul_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.txt")
+
+
+def _half_bits_struct(x: float) -> int:
+    return struct.unpack("<H", struct.pack("<e", x))[0]
+
+
+def _half_value_struct(bits: int) -> float:
+    return struct.unpack("<e", struct.pack("<H", bits))[0]
+
+
+def _golden_lines(kind):
+    out = []
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line.split()[0] == kind:
+                out.append([p.strip() for p in line.split("|")])
+    return out
+
+
+# --------------------------------------------------------------- fp16 rounding
+
+def test_fp16_rounding_matches_struct_packer():
+    rng = np.random.default_rng(1)
+    vals = np.concatenate([
+        rng.standard_normal(4000).astype(np.float32) * 0.01,
+        rng.standard_normal(2000).astype(np.float32) * 1e-6,        # subnormal fp16
+        np.array([0.0, 65504.0, 6.1035156e-05, 5.9604645e-08, 2.9802322e-08,
+                  1.0 + 2.0 ** -11, 1.0 + 3 * 2.0 ** -11], dtype=np.float32),  # ties
+    ])
+    got = O.fp16_bits(vals)
+    want = np.array([_half_bits_struct(float(v)) for v in vals], dtype=np.uint16)
+    assert np.array_equal(got, want)
+    # values back
+    assert np.array_equal(O.fp16_value(want),
+                          np.array([_half_value_struct(int(b)) for b in want], dtype=np.float32))
+
+
+# ------------------------------------------------------------- worked examples
+
+@pytest.mark.parametrize("row", _golden_lines("quant"))
+def test_quantise_worked_examples(row):
+    head, w_s, s_hex, q_s, dq_s = row
+    fmt = O.Q4 if head.split()[1] == "Q4" else O.Q8
+    wv = [float(t) for t in w_s.split()]
+    w = np.zeros((1, 32), np.float32)
+    w[0, :len(wv)] = wv
+    q, s16 = O.quantise(w, fmt)
+    qv = [int(t) for t in q_s.split()]
+    assert s16.shape == (1, 1) and int(s16[0, 0]) == int(s_hex, 16)
+    assert q[0, :len(qv)].tolist() == qv
+    assert not q[0, len(qv):].any()
+    if dq_s != "-":
+        dq = O.dequantise(O.pack(q, fmt), s16, fmt)
+        want = [float(t) for t in dq_s.split()]
+        assert dq[0, :len(want)].tolist() == want
+
+
+def test_pack_worked_example():
+    (row,) = _golden_lines("pack")
+    q = np.array([[int(t) for t in row[1].split()]], np.int8)
+    want = [int(t, 16) for t in row[2].split()]
+    assert O.pack(q, O.Q4)[0].tolist() == want
+    assert O.unpack(O.pack(q, O.Q4), O.Q4).tolist() == q.tolist()
+
+
+def test_route_and_bucket_worked_example():
+    (row,) = _golden_lines("route")
+    e, k = (int(t) for t in row[0].split()[1:3])
+    logits = np.array([[float(t) for t in r.split()] for r in row[1].split(";")], np.float32)
+    ids, gates = O.moe_route(logits, k)
+    assert ids.tolist() == [[int(t) for t in r.split()] for r in row[2].split(";")]
+    want_g = np.array([[float(t) for t in r.split()] for r in row[3].split(";")])
+    assert np.allclose(gates, want_g, rtol=0, atol=1e-15)
+    (b,) = _golden_lines("bucket")
+    counts, offsets, srt = O.moe_bucket(ids, e)
+    assert counts.tolist() == [int(t) for t in b[2].split()[1:]]
+    assert offsets.tolist() == [int(t) for t in b[3].split()[1:]]
+    assert srt.tolist() == [int(t) for t in b[4].split()[1:]]
+
+
+# ------------------------------------------------------------------ invariants
+
+@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+def test_quantise_invariants_random_groups(fmt):
+    rng = np.random.default_rng(7 + fmt)
+    w = (rng.standard_normal((625, 1024)).astype(np.float32) * np.float32(0.02))
+    q, s16 = O.quantise(w, fmt)
+    s = O.fp16_value(s16).astype(np.float64)
+    qg = q.reshape(625, 32, 32).astype(np.int64)
+    # every normal-range group reaches +-qmax exactly and never -8 for Q4
+    assert np.all(np.abs(qg).max(axis=2) == O.QMAX[fmt])
+    assert q.min() >= -O.QMAX[fmt]
+    # reconstruction error within half a step (plus the fp32 division's rounding)
+    dq = O.dequantise(O.pack(q, fmt), s16, fmt).astype(np.float64)
+    err = np.abs(dq - w.astype(np.float64)).reshape(625, 32, 32)
+    assert np.all(err <= (s[:, :, None] / 2) * (1 + 2.0 ** -20))
+    # re-quantising the dequantised matrix reproduces the codes and scales
+    q2, s2 = O.quantise(dq.astype(np.float32), fmt)
+    assert np.array_equal(q2, q) and np.array_equal(s2, s16)
+
+
+def test_quantise_scale_is_fp16_of_fp32_quotient():
+    """Scale = fp16_RNE(fp32(max|w| / qmax)), checked with Python floats:
+    the fp32 quotient is the double quotient rounded once to fp32."""
+    rng = np.random.default_rng(3)
+    w = rng.standard_normal((64, 64)).astype(np.float32) * np.float32(0.02)
+    for fmt in (O.Q4, O.Q8):
+        _, s16 = O.quantise(w, fmt)
+        for n in range(64):
+            for g in range(2):
+                m = max(abs(float(v)) for v in w[n, 32 * g:32 * g + 32])
+                q32 = struct.unpack("<f", struct.pack("<f", m / O.QMAX[fmt]))[0]
+                assert int(s16[n, g]) == _half_bits_struct(q32)
+
+
+@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+def test_pack_roundtrip_all_codes(fmt):
+    lo, hi = O.QLO[fmt], O.QHI[fmt]
+    codes = np.arange(lo, hi + 1)
+    rng = np.random.default_rng(11)
+    q = rng.choice(codes, size=(37, 256)).astype(np.int8)
+    b = O.pack(q, fmt)
+    assert b.shape == ((37, 128) if fmt == O.Q4 else (37, 256))
+    assert np.array_equal(O.unpack(b, fmt), q)
+
+
+@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+def test_dequantise_exhaustive_against_exact_products(fmt):
+    lo, hi = O.QLO[fmt], O.QHI[fmt]
+    codes = list(range(lo, hi + 1))
+    scale_bits = [0x0000, 0x0001, 0x0002, 0x03FF, 0x0400, 0x1C63, 0x1DDA, 0x0D29,
+                  0x2E66, 0x3C00, 0x5140, 0x7BFF]
+    n = len(scale_bits)
+    reps = -(-32 // len(codes))
+    row = (codes * reps)[:32] if len(codes) < 32 else codes
+    k = (len(row) + 31) // 32 * 32
+    q = np.zeros((n, k), np.int8)
+    for i in range(n):
+        q[i, :len(row)] = row
+    s16 = np.array([[b] * (k // 32) for b in scale_bits], np.uint16)
+    dq = O.dequantise(O.pack(q, fmt), s16, fmt)
+    for i, bits in enumerate(scale_bits):
+        sv = Fraction(_half_value_struct(bits))
+        for kk in range(k):
+            assert Fraction(float(dq[i, kk])) == sv * int(q[i, kk])
+
+
+def test_f16_tile_value_is_one_rounding_of_exact_product():
+    q = np.zeros((1, 32), np.int8)
+    q[0, 0] = 7
+    s16 = np.array([[0x1DDA]], np.uint16)    # s = 0.00571441650390625
+    bits = O.dequantise_f16_tile_value(O.pack(q, O.Q4), s16, O.Q4)
+    # exact 7*s = 0.04000091552734375 is not an fp16; nearest fp16 is 0.0400085...
+    assert int(bits[0, 0]) == _half_bits_struct(0.04000091552734375)
+    assert _half_value_struct(int(bits[0, 0])) != 0.04000091552734375
+
+
+# ------------------------------------------------------------------ GEMV/GEMM
+
+def _exact_decode(qbytes, s16, fmt, n, k):
+    """Independent pure-Python decode of the canonical bytes into Fractions."""
+    rows = []
+    for r in range(n):
+        row = []
+        for kk in range(k):
+            if fmt == O.Q4:
+                byte = int(qbytes[r, kk // 2])
+                nib = (byte >> (4 * (kk % 2))) & 0xF
+                code = nib - 16 if nib >= 8 else nib
+            else:
+                byte = int(qbytes[r, kk])
+                code = byte - 256 if byte >= 128 else byte
+            row.append(Fraction(_half_value_struct(int(s16[r, kk // 32]))) * code)
+        rows.append(row)
+    return rows
+
+
+@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+def test_gemv_gemm_against_exact_rationals(fmt):
+    rng = np.random.default_rng(21 + fmt)
+    n, k, m = 5, 96, 3                            # non-square: catches a transpose
+    w = rng.standard_normal((n, k)).astype(np.float32) * np.float32(0.02)
+    q, s16 = O.quantise(w, fmt)
+    qb = O.pack(q, fmt)
+    x = rng.standard_normal((m, k)).astype(np.float16)
+    wf = _exact_decode(qb, s16, fmt, n, k)
+    xf = [[Fraction(float(v)) for v in row] for row in x]
+    exact = [[sum(wf[j][kk] * xf[i][kk] for kk in range(k)) for j in range(n)] for i in range(m)]
+    y = O.gemm(qb, s16, fmt, x)
+    assert y.shape == (m, n)
+    for i in range(m):
+        yv = O.gemv(qb, s16, fmt, x[i])
+        for j in range(n):
+            e = float(exact[i][j])
+            assert abs(y[i, j] - e) <= 1e-14 * max(1.0, abs(e))
+            assert abs(yv[j] - e) <= 1e-14 * max(1.0, abs(e))
+
+
+@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+def test_gemv_integer_grid_is_exact(fmt):
+    """Integer weights with a +-qmax in every group quantise with scale 1, so
+    y is the exact integer sum (computed here with Python ints)."""
+    rng = np.random.default_rng(5)
+    qm = O.QMAX[fmt]
+    n, k = 48, 160
+    wi = rng.integers(-qm, qm + 1, size=(n, k))
+    wi[:, ::32] = qm * rng.choice([-1, 1], size=(n, k // 32))
+    q, s16 = O.quantise(wi.astype(np.float32), fmt)
+    assert np.all(s16 == 0x3C00) and np.array_equal(q, wi)
+    xi = rng.integers(-4, 5, size=(3, k))
+    y = O.gemm(O.pack(q, fmt), s16, fmt, xi.astype(np.float16))
+    want = [[sum(int(wi[j, kk]) * int(xi[i, kk]) for kk in range(k)) for j in range(n)] for i in range(3)]
+    assert y.tolist() == want
+
+
+def test_gemv_one_hot_returns_dequantised_column():
+    rng = np.random.default_rng(9)
+    w = rng.standard_normal((70, 128)).astype(np.float32) * np.float32(0.02)
+    q, s16 = O.quantise(w, O.Q4)
+    qb = O.pack(q, O.Q4)
+    dq = O.dequantise(qb, s16, O.Q4)
+    for kk in (0, 31, 32, 77, 127):
+        x = np.zeros(128, np.float16)
+        x[kk] = 1.0
+        assert np.array_equal(O.gemv(qb, s16, O.Q4, x), dq[:, kk].astype(np.float64))
+
+
+# ------------------------------------------------------------------------ MoE
+
+def test_route_matches_repeated_argmax_and_softmax_ratios():
+    rng = np.random.default_rng(13)
+    logits = rng.standard_normal((64, 128)).astype(np.float32)
+    logits[:8, 5] = logits[:8, 9] = 3.0            # forced ties inside the top set
+    logits[8, :] = 0.0                              # all equal
+    ids, gates = O.moe_route(logits, 8)
+    for t in range(64):
+        work = logits[t].astype(np.float64).copy()
+        pick = []
+        for _ in range(8):
+            j = int(np.argmax(work))               # first maximum = lower index
+            pick.append(j)
+            work[j] = -np.inf
+        assert ids[t].tolist() == pick
+        assert abs(gates[t].sum() - 1.0) < 1e-15
+        for a in range(8):
+            for b in range(8):
+                want = math.exp(float(logits[t, pick[a]]) - float(logits[t, pick[b]]))
+                assert abs(gates[t, a] / gates[t, b] - want) <= 1e-13 * want
+    assert ids[8].tolist() == list(range(8))
+
+
+def test_bucket_matches_stable_sorted():
+    rng = np.random.default_rng(17)
+    for ids in (rng.integers(0, 128, size=(100, 8)),
+                np.tile(np.arange(8), (50, 1)),                 # 120 empty experts
+                np.full((3, 1), 127)):
+        e = 128
+        counts, offsets, srt = O.moe_bucket(ids, e)
+        flat = ids.reshape(-1).tolist()
+        assert counts.tolist() == np.bincount(flat, minlength=e).tolist()
+        assert offsets[0] == 0 and offsets[-1] == len(flat)
+        assert np.array_equal(np.diff(offsets), counts)
+        assert srt.tolist() == sorted(range(len(flat)), key=lambda a: (flat[a], a))
+
+
+def test_silu_identities():
+    z = np.linspace(-30, 30, 601)
+    s = O.silu(z)
+    assert np.allclose(s - O.silu(-z), z, rtol=0, atol=1e-13)       # silu(z)-silu(-z)=z
+    assert O.silu(np.array([0.0]))[0] == 0.0
+    assert abs(O.silu(np.array([1.0]))[0] - 1.0 / (1.0 + math.exp(-1.0))) < 1e-16
+
+
+def _grid_expert(rng, n, k):
+    w = rng.integers(-7, 8, size=(n, k))
+    w[:, ::32] = 7
+    q, s16 = O.quantise(w.astype(np.float32), O.Q4)
+    return O.pack(q, O.Q4), s16, w
+
+
+def test_expert_ffn_hand_example():
+    """x = e_0, integer grid weights (scale 1): a_i = Wg[i][0], b_i = Wu[i][0],
+    y_n = sum_i Wd[n][i] * silu(a_i) * b_i.  Evaluated with scalar math.exp."""
+    rng = np.random.default_rng(23)
+    h, inter = 32, 64
+    gq, gs, wg = _grid_expert(rng, inter, h)
+    uq, us, wu = _grid_expert(rng, inter, h)
+    dq_, ds, wd = _grid_expert(rng, h, inter)
+    x = np.zeros((1, h), np.float16)
+    x[0, 0] = 1.0
+    logits = np.zeros((1, 1), np.float32)
+    out, *_ = O.moe_layer(x, logits, 1, gq[None], gs[None], uq[None], us[None], dq_[None], ds[None])
+    for n in range(h):
+        want = 0.0
+        for i in range(inter):
+            a = float(wg[i, 0])
+            want += float(wd[n, i]) * (a / (1.0 + math.exp(-a))) * float(wu[i, 0])
+        assert abs(out[0, n] - want) <= 1e-12 * max(1.0, abs(want))
+
+
+def _random_experts(rng, e, h, inter):
+    def mk(n, k):
+        w = rng.standard_normal((e, n, k)).astype(np.float32) * np.float32(0.02)
+        qs = [O.quantise(w[i], O.Q4) for i in range(e)]
+        return np.stack([O.pack(q, O.Q4) for q, _ in qs]), np.stack([s for _, s in qs])
+    return mk(inter, h) + mk(inter, h) + mk(h, inter)
+
+
+def test_moe_layer_equals_dense_gate_evaluation():
+    rng = np.random.default_rng(29)
+    e, h, inter, m, k = 16, 64, 96, 40, 4
+    gq, gs, uq, us, dq_, ds = _random_experts(rng, e, h, inter)
+    x = rng.standard_normal((m, h)).astype(np.float16)
+    logits = rng.standard_normal((m, e)).astype(np.float32)
+    out, ids, gates, *_ = O.moe_layer(x, logits, k, gq, gs, uq, us, dq_, ds)
+    # dense: every expert on every token, gate matrix zero off the top-k
+    x64 = x.astype(np.float64)
+    dense_gate = np.zeros((m, e))
+    for t in range(m):
+        for j in range(k):
+            dense_gate[t, ids[t, j]] = gates[t, j]
+    ref = np.zeros((m, h))
+    for ex in range(e):
+        wg = O.dequantise(gq[ex], gs[ex], O.Q4).astype(np.float64)
+        wu = O.dequantise(uq[ex], us[ex], O.Q4).astype(np.float64)
+        wd = O.dequantise(dq_[ex], ds[ex], O.Q4).astype(np.float64)
+        for t in range(m):
+            a = wg @ x64[t]
+            b = wu @ x64[t]
+            hh = (a / (1 + np.exp(-a))) * b
+            ref[t] += dense_gate[t, ex] * (wd @ hh)
+    assert np.allclose(out, ref, rtol=0, atol=1e-12 * np.abs(ref).max())
+
+
+def test_moe_top1_and_identical_experts():
+    rng = np.random.default_rng(31)
+    e, h, inter, m = 8, 32, 64, 12
+    gq, gs, uq, us, dq_, ds = _random_experts(rng, e, h, inter)
+    x = rng.standard_normal((m, h)).astype(np.float16)
+    logits = rng.standard_normal((m, e)).astype(np.float32)
+    out1, ids1, g1, *_ = O.moe_layer(x, logits, 1, gq, gs, uq, us, dq_, ds)
+    assert np.all(g1 == 1.0)
+    for t in range(m):
+        ex = int(np.argmax(logits[t]))
+        assert ids1[t, 0] == ex
+        single, *_ = O.moe_layer(x[t:t + 1], np.zeros((1, 1), np.float32), 1,
+                                 gq[ex:ex + 1], gs[ex:ex + 1], uq[ex:ex + 1], us[ex:ex + 1],
+                                 dq_[ex:ex + 1], ds[ex:ex + 1])
+        assert np.allclose(out1[t], single[0], rtol=0, atol=1e-14 * np.abs(single).max())
+    # identical experts: the gates sum to one, so the layer is that expert's FFN
+    rep = lambda a: np.repeat(a[:1], e, axis=0)
+    outs, *_ = O.moe_layer(x, logits, 4, rep(gq), rep(gs), rep(uq), rep(us), rep(dq_), rep(ds))
+    one, *_ = O.moe_layer(x, np.zeros((m, 1), np.float32), 1, gq[:1], gs[:1], uq[:1], us[:1],
+                          dq_[:1], ds[:1])
+    assert np.allclose(outs, one, rtol=0, atol=1e-13 * np.abs(one).max())
