@@ -1,0 +1,183 @@
+/*
+ * qmatmul.h -- C ABI of the MI355X (gfx950) weight-only-quantised matmul library.
+ *
+ * The library implements the matrix products of LLM decode and prefill with
+ * quantised weights: a fused dequantise+GEMV for batch-1 decode, a
+ * dequantise-into-LDS + fp16 MFMA GEMM for prefill, and the top-k-routed
+ * grouped expert GEMM of a mixture-of-experts layer (BaseRT, Sec. 3.3
+ * "Kernel Fusion and Specialisation": one GEMV (M = 1) and one GEMM (M > 1)
+ * kernel per quantisation format, dequantisation inside the inner loop and
+ * never materialised; Sec. 3.4 "Prefill": tiled GEMM for prompts, bounded
+ * chunks; Sec. 4.1: Q4 / Q8 formats and the MoE models).
+ *
+ * Conventions shared by every entry point
+ *  - Pointers named d_* / device buffers are HIP device pointers; the caller
+ *    owns every buffer.  The library never allocates, frees or retains memory
+ *    (Sec. 3.2, "Zero-Allocation Decode Loop").
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    QM_OK means "validated and enqueued on stream"; nothing is synchronised.
+ *  - Arguments are validated on the host before anything is enqueued.  On an
+ *    error nothing is enqueued, outputs are untouched and a message is left in
+ *    a thread-local buffer read by qm_last_error() (Sec. 3.2: error handling
+ *    through a static thread-local buffer).
+ *  - A launch failure reported by the HIP runtime maps to QM_EDEVICE.
+ *  - Calls that share output or workspace buffers and overlap on one device
+ *    race; the library holds no state besides an immutable per-device
+ *    configuration table.
+ *
+ * Weight format (group-32 symmetric, one fp16 scale per 32 weights along K)
+ *  For row n and group g = k / 32 of a weight matrix W [N][K]:
+ *    m = max |w| over the group (fp32), s32 = m / qmax (fp32, correctly
+ *    rounded), s16 = fp16_RNE(s32), s = value(s16);
+ *    q = 0 if s == 0, else clamp(rint_half_even(w / s), lo, hi)  (fp32 division);
+ *    Q4 (QM_Q4_G32): qmax = 7,   [lo, hi] = [-8, 7];
+ *    Q8 (QM_Q8_G32): qmax = 127, [lo, hi] = [-127, 127].
+ *  The dequantised weight is w' = s * q, exact in fp32.
+ *
+ *  CANONICAL layout (QM_LAYOUT_CANONICAL):
+ *    Q4 codes: uint8 [N][K/2], byte j = (q[2j] & 0xF) | ((q[2j+1] & 0xF) << 4)
+ *              (even k in the low nibble, two's complement nibbles);
+ *    Q8 codes: int8 [N][K], two's complement;
+ *    scales:   uint16 [N][K/32], fp16 bit patterns.
+ *
+ *  DEVICE layout (QM_LAYOUT_DEVICE), the one the matmul kernels read: rows
+ *  are grouped into panels of 64 (N is padded up to a multiple of 64 with
+ *  zero bytes), and the 32 codes of one (row, group) form a "chunk".
+ *    Q4: chunk = 16 bytes at byte ((p*G + g)*64 + r)*16, p = n/64, r = n%64,
+ *        G = K/32.  Dword j of the chunk covers k = 32g + 8j .. 32g + 8j + 7;
+ *        its nibble t (bits 4t..4t+3) holds the offset-binary code q + 8 of
+ *        k-offset 2t (t < 4) or 2(t-4)+1 (t >= 4).
+ *    Q8: chunk = 32 bytes split in two 16-byte halves h = 0, 1 (k = 32g + 16h
+ *        .. +15); half h of row r sits at byte ((p*G + g)*2 + h)*1024 + r*16,
+ *        each byte the offset-binary code q + 128.
+ *    scales: uint16 at element (p*G + g)*64 + r.
+ *  Stacked matrices (batch > 1, e.g. the experts of a MoE layer) place
+ *  matrix b at b * (bytes of one matrix) in both buffers, in both layouts.
+ *  Every 64-lane wavefront load of one chunk index over a panel reads 1 KiB
+ *  (Q4) of contiguous bytes, so the weight stream is fully coalesced.
+ */
+#ifndef QMATMUL_H
+#define QMATMUL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  QM_OK = 0,
+  QM_EINVAL = 1,      /* null pointer, bad enum, negative size            */
+  QM_ESHAPE = 2,      /* K % 32 != 0, mismatched shapes, size limits      */
+  QM_EALIGN = 3,      /* a device pointer is not 16-byte aligned          */
+  QM_EFORMAT = 4,     /* unsupported format for this entry point          */
+  QM_ELAYOUT = 5,     /* wrong layout for this entry point                */
+  QM_EWORKSPACE = 6,  /* workspace missing or smaller than required       */
+  QM_EDEVICE = 7      /* the HIP runtime reported an error                */
+} qm_status;
+
+enum { QM_Q4_G32 = 1, QM_Q8_G32 = 2 };
+enum { QM_LAYOUT_CANONICAL = 0, QM_LAYOUT_DEVICE = 1 };
+
+/* Non-owning view of a quantised weight tensor [batch][n][k].
+ * qdata: device codes in `layout`; scales: device fp16 bits.  k % 32 == 0.
+ * Both pointers must be 16-byte aligned; the buffers must hold at least the
+ * sizes qm_weight_bytes() returns for (format, layout, batch, n, k). */
+typedef struct {
+  int32_t format;
+  int32_t layout;
+  int64_t batch;
+  int64_t n;
+  int64_t k;
+  void* qdata;
+  uint16_t* scales;
+} qm_qweight;
+
+/* Text of the last error on the calling thread ("" if none yet).  The
+ * pointer stays valid until the next failing call on the same thread. */
+const char* qm_last_error(void);
+
+/* Host-only: bytes of the code buffer and of the scale buffer for a tensor
+ * [batch][n][k] in the given format and layout (DEVICE pads n to 64). */
+qm_status qm_weight_bytes(int32_t format, int32_t layout, int64_t batch, int64_t n,
+                          int64_t k, size_t* qbytes, size_t* sbytes);
+
+/* Quantise fp32 weights w [batch][n][k] (device, row-major) into `out`, which
+ * must be in CANONICAL layout with out->format set.  Bit-exact with the
+ * format definition above (one thread per group, IEEE fp32 division,
+ * round-half-even, fp16 round-to-nearest-even).  Weights must be finite and
+ * every group's max|w| / qmax must be <= 65504 (not scanned). */
+qm_status qm_quantise(int32_t format, const float* w, const qm_qweight* out, void* stream);
+
+/* Dequantise w (either layout) into fp32 out [batch][n][k] (device):
+ * out = s * q, exact. */
+qm_status qm_dequantise(const qm_qweight* w, float* out, void* stream);
+
+/* Reorder codes and scales between layouts (CANONICAL <-> DEVICE).  src and
+ * dst must agree in format, batch, n, k and differ in layout; the map is a
+ * bijection on the real rows, and DEVICE padding rows are written as zero.
+ * src and dst buffers must not overlap. */
+qm_status qm_repack(const qm_qweight* src, const qm_qweight* dst, void* stream);
+
+/* Decode GEMV (Sec. 3.3, M = 1): y[n] = sum_k s[n][k/32] * q[n][k] * x[k].
+ * w: DEVICE layout, batch 1, Q4 or Q8.  x: fp16 [k] (device).  y: fp32 [n]
+ * (device).  Dequantisation happens in registers; products and sums in fp32.
+ * Single kernel launch, no workspace, deterministic. */
+qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* stream);
+
+/* Prefill GEMM (Sec. 3.3, Sec. 3.4, M > 1): Y[m][n] = sum_k X[m][k] * w'[n][k].
+ * w: DEVICE layout, batch 1, Q4.  X: fp16 [m][k] row-major; Y: fp32 [m][n].
+ * Weight tiles are dequantised to fp16 (value fp16_RNE(s*q)) in LDS and fed
+ * to fp16 MFMA with fp32 accumulation.  m >= 1 (m == 1 runs the GEMV);
+ * m <= 65536 per call (chunk larger prompts).  Deterministic. */
+qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream);
+
+/* Host-only: workspace bytes qmoe_grouped_gemm needs for m tokens. */
+qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden,
+                               int64_t inter, size_t* bytes);
+
+/* MoE routing and bucketing (device in/out; all int32/fp32):
+ *  logits [m][n_experts] fp32 -> topk_ids [m][top_k]: per token the top_k
+ *  experts by logit, descending, equal logits -> lower expert first;
+ *  topk_w [m][top_k]: softmax over those top_k logits (fp32);
+ *  counts [n_experts], offsets [n_experts + 1] (exclusive prefix sum,
+ *  offsets[E] = m*top_k) and sorted_assign [m*top_k]: the flat assignment
+ *  ids a = t*top_k + j grouped by expert, ascending a inside each expert
+ *  (stable counting sort).  n_experts <= 1024, 1 <= top_k <= min(16, n_experts),
+ *  m <= 65536.  Ids, counts, offsets and sorted_assign are deterministic. */
+qm_status qmoe_route(const float* logits, int64_t m, int32_t n_experts, int32_t top_k,
+                     int32_t* topk_ids, float* topk_w, int32_t* counts, int32_t* offsets,
+                     int32_t* sorted_assign, void* stream);
+
+/* Routed SwiGLU expert layer (grouped GEMMs + weighted combine):
+ *  for every assignment a = t*top_k + j, with e the expert whose bucket
+ *  [offsets[e], offsets[e+1]) of sorted_assign holds a:
+ *    h_a = silu(Wg_e x_t) * (Wu_e x_t),  y_a = Wd_e h_a,
+ *  y[t] = sum_j topk_w[t][j] * y_{t*top_k+j}, summed in slot order j.
+ *  w_gate, w_up: DEVICE layout Q4, batch E, [E][inter][hidden];
+ *  w_down: DEVICE layout Q4, batch E, [E][hidden][inter];
+ *  x: fp16 [m][hidden]; y: fp32 [m][hidden]; topk_w [m][top_k], counts,
+ *  offsets and sorted_assign come from qmoe_route (sorted_assign must be a
+ *  permutation of 0 .. m*top_k-1 consistent with counts/offsets).  hidden % 32 == 0 and inter % 32 == 0.  h is held in fp16;
+ *  all GEMMs use fp16 MFMA with fp32 accumulation.  The workspace (device,
+ *  16-byte aligned, >= qmoe_workspace_bytes) holds h and the per-assignment
+ *  outputs; no host synchronisation: per-expert row counts stay on the
+ *  device.  Deterministic. */
+qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up,
+                            const qm_qweight* w_down, const uint16_t* x, int64_t m,
+                            int32_t top_k, const float* topk_w,
+                            const int32_t* counts, const int32_t* offsets,
+                            const int32_t* sorted_assign, float* y, void* workspace,
+                            size_t ws_bytes, void* stream);
+
+/* Writes a one-line description of the per-chip launch table chosen for the
+ * current device (arch, CU count, tile choices) into buf (Sec. 3.3: kernel
+ * geometry from a per-chip configuration). */
+qm_status qm_device_config(char* buf, size_t len);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QMATMUL_H */

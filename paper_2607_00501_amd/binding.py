@@ -1,0 +1,228 @@
+"""Thin ctypes binding of libqmatmul.so.
+
+Only argument marshalling lives here: torch supplies device memory (for the
+outputs it allocates) and the current HIP stream; every step of the
+quantised matmul runs in the library's HIP kernels.  The functions carry the
+C ABI's names.  If the library has not been built, every call raises: there
+is no fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+Q4_G32, Q8_G32 = 1, 2
+LAYOUT_CANONICAL, LAYOUT_DEVICE = 0, 1
+
+STATUS = {0: "QM_OK", 1: "QM_EINVAL", 2: "QM_ESHAPE", 3: "QM_EALIGN", 4: "QM_EFORMAT",
+          5: "QM_ELAYOUT", 6: "QM_EWORKSPACE", 7: "QM_EDEVICE"}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqmatmul.so")
+
+EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "qm_repack",
+           "qmatmul_gemv", "qmatmul_gemm", "qmoe_workspace_bytes", "qmoe_route",
+           "qmoe_grouped_gemm", "qm_device_config")
+
+
+class QmError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class CQWeight(ctypes.Structure):
+    _fields_ = [("format", ctypes.c_int32), ("layout", ctypes.c_int32), ("batch", ctypes.c_int64),
+                ("n", ctypes.c_int64), ("k", ctypes.c_int64), ("qdata", ctypes.c_void_p),
+                ("scales", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Loads libqmatmul.so (raises if it was never built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2607_00501_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        W = ctypes.POINTER(CQWeight)
+        L.qm_last_error.restype = ctypes.c_char_p
+        L.qm_last_error.argtypes = []
+        sig = {
+            "qm_weight_bytes": [i32, i32, i64, i64, i64, ctypes.POINTER(sz), ctypes.POINTER(sz)],
+            "qm_quantise": [i32, vp, W, vp],
+            "qm_dequantise": [W, vp, vp],
+            "qm_repack": [W, W, vp],
+            "qmatmul_gemv": [W, vp, vp, vp],
+            "qmatmul_gemm": [W, vp, i64, vp, vp],
+            "qmoe_workspace_bytes": [i64, i32, i32, i64, i64, ctypes.POINTER(sz)],
+            "qmoe_route": [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp],
+            "qmoe_grouped_gemm": [W, W, W, vp, i64, i32, vp, vp, vp, vp, vp, vp, sz, vp],
+            "qm_device_config": [ctypes.c_char_p, sz],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise QmError(status, lib().qm_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+@dataclass
+class QWeight:
+    """A quantised tensor [batch][n][k]: codes and fp16 scale bits in torch
+    uint8 / int16 buffers, in CANONICAL or DEVICE layout."""
+    format: int
+    layout: int
+    batch: int
+    n: int
+    k: int
+    qdata: torch.Tensor
+    scales: torch.Tensor
+
+    def c(self) -> CQWeight:
+        return CQWeight(self.format, self.layout, self.batch, self.n, self.k,
+                        self.qdata.data_ptr(), self.scales.data_ptr())
+
+    @property
+    def nbytes(self) -> int:
+        return self.qdata.numel() + 2 * self.scales.numel()
+
+
+def qm_last_error() -> str:
+    return lib().qm_last_error().decode()
+
+
+def qm_weight_bytes(fmt: int, layout: int, batch: int, n: int, k: int):
+    qb, sb = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().qm_weight_bytes(fmt, layout, batch, n, k, ctypes.byref(qb), ctypes.byref(sb)))
+    return qb.value, sb.value
+
+
+def empty_qweight(fmt: int, layout: int, batch: int, n: int, k: int, device="cuda") -> QWeight:
+    qb, sb = qm_weight_bytes(fmt, layout, batch, n, k)
+    return QWeight(fmt, layout, batch, n, k,
+                   torch.empty(max(qb, 16), dtype=torch.uint8, device=device),
+                   torch.empty(max(sb // 2, 8), dtype=torch.int16, device=device))
+
+
+def qm_quantise(w: torch.Tensor, fmt: int, out: Optional[QWeight] = None, stream=None) -> QWeight:
+    """w: fp32 [n][k] or [batch][n][k] on the GPU -> CANONICAL QWeight."""
+    if w.dim() == 2:
+        batch, (n, k) = 1, w.shape
+    else:
+        batch, n, k = w.shape
+    assert w.dtype == torch.float32 and w.is_contiguous()
+    if out is None:
+        out = empty_qweight(fmt, LAYOUT_CANONICAL, batch, n, k, w.device)
+    _check(lib().qm_quantise(fmt, _ptr(w), ctypes.byref(out.c()), _stream(stream)))
+    return out
+
+
+def qm_dequantise(w: QWeight, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    if out is None:
+        out = torch.empty((w.batch, w.n, w.k), dtype=torch.float32, device=w.qdata.device)
+    _check(lib().qm_dequantise(ctypes.byref(w.c()), _ptr(out), _stream(stream)))
+    return out
+
+
+def qm_repack(src: QWeight, layout: int, out: Optional[QWeight] = None, stream=None) -> QWeight:
+    if out is None:
+        out = empty_qweight(src.format, layout, src.batch, src.n, src.k, src.qdata.device)
+    _check(lib().qm_repack(ctypes.byref(src.c()), ctypes.byref(out.c()), _stream(stream)))
+    return out
+
+
+def qmatmul_gemv(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """x: fp16 [k] -> fp32 [n]."""
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.numel() == w.k
+    if out is None:
+        out = torch.empty(w.n, dtype=torch.float32, device=x.device)
+    _check(lib().qmatmul_gemv(ctypes.byref(w.c()), _ptr(x), _ptr(out), _stream(stream)))
+    return out
+
+
+def qmatmul_gemm(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """X: fp16 [m][k] -> fp32 [m][n]."""
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.dim() == 2 and x.shape[1] == w.k
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, w.n), dtype=torch.float32, device=x.device)
+    _check(lib().qmatmul_gemm(ctypes.byref(w.c()), _ptr(x), m, _ptr(out), _stream(stream)))
+    return out
+
+
+def qmoe_workspace_bytes(m: int, n_experts: int, top_k: int, hidden: int, inter: int) -> int:
+    b = ctypes.c_size_t()
+    _check(lib().qmoe_workspace_bytes(m, n_experts, top_k, hidden, inter, ctypes.byref(b)))
+    return b.value
+
+
+@dataclass
+class Routing:
+    ids: torch.Tensor            # int32 [m][top_k]
+    gates: torch.Tensor          # fp32 [m][top_k]
+    counts: torch.Tensor         # int32 [E]
+    offsets: torch.Tensor        # int32 [E+1]
+    sorted_assign: torch.Tensor  # int32 [m*top_k]
+    top_k: int
+
+
+def qmoe_route(logits: torch.Tensor, top_k: int, out: Optional[Routing] = None, stream=None) -> Routing:
+    m, e = logits.shape
+    assert logits.dtype == torch.float32 and logits.is_contiguous()
+    dev = logits.device
+    if out is None:
+        out = Routing(torch.empty((m, top_k), dtype=torch.int32, device=dev),
+                      torch.empty((m, top_k), dtype=torch.float32, device=dev),
+                      torch.empty(e, dtype=torch.int32, device=dev),
+                      torch.empty(e + 1, dtype=torch.int32, device=dev),
+                      torch.empty(max(m * top_k, 1), dtype=torch.int32, device=dev), top_k)
+    _check(lib().qmoe_route(_ptr(logits), m, e, top_k, _ptr(out.ids), _ptr(out.gates), _ptr(out.counts),
+                            _ptr(out.offsets), _ptr(out.sorted_assign), _stream(stream)))
+    return out
+
+
+def qmoe_grouped_gemm(w_gate: QWeight, w_up: QWeight, w_down: QWeight, x: torch.Tensor, r: Routing,
+                      out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                      stream=None) -> torch.Tensor:
+    m, hidden = x.shape
+    assert x.dtype == torch.float16 and x.is_contiguous()
+    if out is None:
+        out = torch.empty((m, hidden), dtype=torch.float32, device=x.device)
+    if workspace is None:
+        nb = qmoe_workspace_bytes(m, w_gate.batch, r.top_k, hidden, w_gate.n)
+        workspace = torch.empty(max(nb, 16), dtype=torch.uint8, device=x.device)
+    _check(lib().qmoe_grouped_gemm(ctypes.byref(w_gate.c()), ctypes.byref(w_up.c()), ctypes.byref(w_down.c()),
+                                   _ptr(x), m, r.top_k, _ptr(r.gates), _ptr(r.counts), _ptr(r.offsets),
+                                   _ptr(r.sorted_assign), _ptr(out), _ptr(workspace), workspace.numel(),
+                                   _stream(stream)))
+    return out
+
+
+def qm_device_config() -> str:
+    buf = ctypes.create_string_buffer(512)
+    _check(lib().qm_device_config(buf, 512))
+    return buf.value.decode()

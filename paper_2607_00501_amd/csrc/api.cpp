@@ -1,0 +1,298 @@
+// C ABI entry points: argument validation (nothing is enqueued on error),
+// the thread-local error buffer, the per-device configuration and dispatch
+// to the kernel launchers.
+//
+// The library allocates nothing and keeps no per-call state (BaseRT Sec. 3.2:
+// the decode loop allocates zero bytes and errors go through a static
+// thread-local buffer); the only shared state is an immutable per-device
+// table (CU count, architecture) built once per device.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+
+#include "qm_internal.h"
+
+namespace qm {
+namespace {
+
+thread_local char g_err[512] = "";
+
+struct DeviceInfo {
+  int cu_count = 0;
+  char arch[64] = "";
+  hipError_t status = hipSuccess;
+};
+
+constexpr int kMaxDevices = 64;
+DeviceInfo g_dev[kMaxDevices];
+std::once_flag g_dev_once[kMaxDevices];
+
+qm_status device_info(const DeviceInfo** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(QM_EDEVICE, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(QM_EDEVICE, "device index %d out of range", dev);
+  std::call_once(g_dev_once[dev], [dev]() {
+    DeviceInfo& d = g_dev[dev];
+    hipDeviceProp_t prop;
+    d.status = hipGetDeviceProperties(&prop, dev);
+    if (d.status == hipSuccess) {
+      d.cu_count = prop.multiProcessorCount;
+      std::snprintf(d.arch, sizeof(d.arch), "%s", prop.gcnArchName);
+    }
+  });
+  const DeviceInfo& d = g_dev[dev];
+  if (d.status != hipSuccess)
+    return fail(QM_EDEVICE, "hipGetDeviceProperties failed: %s", hipGetErrorString(d.status));
+  if (std::strncmp(d.arch, "gfx950", 6) != 0)
+    return fail(QM_EDEVICE, "device %d is %s; this library is built for gfx950 only", dev, d.arch);
+  *out = &d;
+  return QM_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+qm_status check_weight(const qm_qweight* w, const char* name) {
+  if (!w) return fail(QM_EINVAL, "%s: null weight descriptor", name);
+  if (w->format != QM_Q4_G32 && w->format != QM_Q8_G32)
+    return fail(QM_EFORMAT, "%s: unknown format %d", name, w->format);
+  if (w->layout != QM_LAYOUT_CANONICAL && w->layout != QM_LAYOUT_DEVICE)
+    return fail(QM_ELAYOUT, "%s: unknown layout %d", name, w->layout);
+  if (w->batch < 1 || w->n < 0 || w->k < 0)
+    return fail(QM_ESHAPE, "%s: bad shape batch=%lld n=%lld k=%lld", name, (long long)w->batch,
+                (long long)w->n, (long long)w->k);
+  if (w->k % kGroup != 0 || w->k == 0)
+    return fail(QM_ESHAPE, "%s: k=%lld must be a positive multiple of 32", name, (long long)w->k);
+  if (w->n >= (int64_t(1) << 31) || w->k >= (int64_t(1) << 31))
+    return fail(QM_ESHAPE, "%s: n and k must be < 2^31", name);
+  if (w->n > 0 && (!w->qdata || !w->scales)) return fail(QM_EINVAL, "%s: null data pointer", name);
+  if (!aligned16(w->qdata) || !aligned16(w->scales))
+    return fail(QM_EALIGN, "%s: qdata and scales must be 16-byte aligned", name);
+  return QM_OK;
+}
+
+}  // namespace
+
+qm_status fail(qm_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+qm_status check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(QM_EDEVICE, "%s: launch failed: %s", what, hipGetErrorString(e));
+  return QM_OK;
+}
+
+static qm_status launched(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(QM_EDEVICE, "%s: launch failed: %s", what, hipGetErrorString(e));
+  return QM_OK;
+}
+
+}  // namespace qm
+
+using namespace qm;
+
+extern "C" {
+
+const char* qm_last_error(void) { return g_err; }
+
+qm_status qm_weight_bytes(int32_t format, int32_t layout, int64_t batch, int64_t n, int64_t k,
+                          size_t* qbytes, size_t* sbytes) {
+  if (!qbytes || !sbytes) return fail(QM_EINVAL, "qm_weight_bytes: null output pointer");
+  if (format != QM_Q4_G32 && format != QM_Q8_G32)
+    return fail(QM_EFORMAT, "qm_weight_bytes: unknown format %d", format);
+  if (layout != QM_LAYOUT_CANONICAL && layout != QM_LAYOUT_DEVICE)
+    return fail(QM_ELAYOUT, "qm_weight_bytes: unknown layout %d", layout);
+  if (batch < 1 || n < 0 || k <= 0 || k % kGroup != 0)
+    return fail(QM_ESHAPE, "qm_weight_bytes: bad shape batch=%lld n=%lld k=%lld", (long long)batch,
+                (long long)n, (long long)k);
+  const int64_t rows = batch * matrix_rows(layout, n);
+  *qbytes = static_cast<size_t>(rows * row_code_bytes(format, k));
+  *sbytes = static_cast<size_t>(rows * (k / kGroup) * 2);
+  return QM_OK;
+}
+
+qm_status qm_quantise(int32_t format, const float* w, const qm_qweight* out, void* stream) {
+  qm_status st = check_weight(out, "qm_quantise(out)");
+  if (st != QM_OK) return st;
+  if (out->format != format)
+    return fail(QM_EFORMAT, "qm_quantise: out->format %d != format %d", out->format, format);
+  if (out->layout != QM_LAYOUT_CANONICAL)
+    return fail(QM_ELAYOUT, "qm_quantise: output must be in CANONICAL layout");
+  if (out->n > 0 && !w) return fail(QM_EINVAL, "qm_quantise: null input");
+  if (!aligned16(w)) return fail(QM_EALIGN, "qm_quantise: w must be 16-byte aligned");
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_quantise(format, w, static_cast<uint8_t*>(out->qdata), out->scales, out->batch,
+                                  out->n, out->k, static_cast<hipStream_t>(stream)),
+                  "qm_quantise");
+}
+
+qm_status qm_dequantise(const qm_qweight* w, float* out, void* stream) {
+  qm_status st = check_weight(w, "qm_dequantise(w)");
+  if (st != QM_OK) return st;
+  if (w->n > 0 && !out) return fail(QM_EINVAL, "qm_dequantise: null output");
+  if (!aligned16(out)) return fail(QM_EALIGN, "qm_dequantise: out must be 16-byte aligned");
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_dequantise(w->format, w->layout, static_cast<const uint8_t*>(w->qdata),
+                                    w->scales, out, w->batch, w->n, w->k,
+                                    static_cast<hipStream_t>(stream)),
+                  "qm_dequantise");
+}
+
+qm_status qm_repack(const qm_qweight* src, const qm_qweight* dst, void* stream) {
+  qm_status st = check_weight(src, "qm_repack(src)");
+  if (st != QM_OK) return st;
+  if ((st = check_weight(dst, "qm_repack(dst)")) != QM_OK) return st;
+  if (src->format != dst->format) return fail(QM_EFORMAT, "qm_repack: formats differ");
+  if (src->layout == dst->layout) return fail(QM_ELAYOUT, "qm_repack: src and dst layouts are equal");
+  if (src->batch != dst->batch || src->n != dst->n || src->k != dst->k)
+    return fail(QM_ESHAPE, "qm_repack: shapes differ");
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_repack(src->format, src->layout, static_cast<const uint8_t*>(src->qdata),
+                                src->scales, static_cast<uint8_t*>(dst->qdata), dst->scales, src->batch,
+                                src->n, src->k, static_cast<hipStream_t>(stream)),
+                  "qm_repack");
+}
+
+qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* stream) {
+  qm_status st = check_weight(w, "qmatmul_gemv(w)");
+  if (st != QM_OK) return st;
+  if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "qmatmul_gemv: weights must be in DEVICE layout");
+  if (w->batch != 1) return fail(QM_ESHAPE, "qmatmul_gemv: batch must be 1");
+  if (w->n > 0 && (!x || !y)) return fail(QM_EINVAL, "qmatmul_gemv: null x or y");
+  if (!aligned16(x)) return fail(QM_EALIGN, "qmatmul_gemv: x must be 16-byte aligned");
+  if (!aligned4(y)) return fail(QM_EALIGN, "qmatmul_gemv: y must be 4-byte aligned");
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_gemv(w->format, static_cast<const uint8_t*>(w->qdata), w->scales, x, y, w->n,
+                              w->k, d->cu_count, static_cast<hipStream_t>(stream)),
+                  "qmatmul_gemv");
+}
+
+qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream) {
+  qm_status st = check_weight(w, "qmatmul_gemm(w)");
+  if (st != QM_OK) return st;
+  if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "qmatmul_gemm: weights must be in DEVICE layout");
+  if (w->batch != 1) return fail(QM_ESHAPE, "qmatmul_gemm: batch must be 1");
+  if (m < 1 || m > 65536) return fail(QM_ESHAPE, "qmatmul_gemm: m=%lld must be in [1, 65536]", (long long)m);
+  if (m > 1 && w->format != QM_Q4_G32)
+    return fail(QM_EFORMAT, "qmatmul_gemm: the MFMA GEMM supports Q4 only (m > 1)");
+  if (w->n > 0 && (!x || !y)) return fail(QM_EINVAL, "qmatmul_gemm: null x or y");
+  if (!aligned16(x)) return fail(QM_EALIGN, "qmatmul_gemm: x must be 16-byte aligned");
+  if (!aligned4(y)) return fail(QM_EALIGN, "qmatmul_gemm: y must be 4-byte aligned");
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (m == 1)
+    return launched(launch_gemv(w->format, static_cast<const uint8_t*>(w->qdata), w->scales, x, y, w->n,
+                                w->k, d->cu_count, s),
+                    "qmatmul_gemm(m=1)");
+  return launched(launch_gemm(static_cast<const uint8_t*>(w->qdata), w->scales, x, y, m, w->n, w->k,
+                              d->cu_count, s),
+                  "qmatmul_gemm");
+}
+
+qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden, int64_t inter,
+                               size_t* bytes) {
+  if (!bytes) return fail(QM_EINVAL, "qmoe_workspace_bytes: null output pointer");
+  if (m < 0 || m > 65536 || n_experts < 1 || top_k < 1 || top_k > n_experts || top_k > 16 ||
+      hidden <= 0 || inter <= 0 || hidden % kGroup || inter % kGroup)
+    return fail(QM_ESHAPE, "qmoe_workspace_bytes: bad sizes");
+  *bytes = moe_workspace_bytes(m, top_k, hidden, inter);
+  return QM_OK;
+}
+
+qm_status qmoe_route(const float* logits, int64_t m, int32_t n_experts, int32_t top_k, int32_t* topk_ids,
+                     float* topk_w, int32_t* counts, int32_t* offsets, int32_t* sorted_assign,
+                     void* stream) {
+  if (n_experts < 1 || n_experts > 1024)
+    return fail(QM_ESHAPE, "qmoe_route: n_experts=%d must be in [1, 1024]", n_experts);
+  if (top_k < 1 || top_k > 16 || top_k > n_experts)
+    return fail(QM_ESHAPE, "qmoe_route: top_k=%d must be in [1, min(16, n_experts)]", top_k);
+  if (m < 0 || m > 65536) return fail(QM_ESHAPE, "qmoe_route: m=%lld must be in [0, 65536]", (long long)m);
+  if (!counts || !offsets) return fail(QM_EINVAL, "qmoe_route: null counts/offsets");
+  if (m > 0 && (!logits || !topk_ids || !topk_w || !sorted_assign))
+    return fail(QM_EINVAL, "qmoe_route: null pointer");
+  if (!aligned4(logits) || !aligned4(topk_ids) || !aligned4(topk_w) || !aligned4(counts) ||
+      !aligned4(offsets) || !aligned4(sorted_assign))
+    return fail(QM_EALIGN, "qmoe_route: pointers must be 4-byte aligned");
+  const DeviceInfo* d;
+  qm_status st;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_route(logits, m, n_experts, top_k, topk_ids, topk_w, counts, offsets,
+                               sorted_assign, static_cast<hipStream_t>(stream)),
+                  "qmoe_route");
+}
+
+qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up, const qm_qweight* w_down,
+                            const uint16_t* x, int64_t m, int32_t top_k, const float* topk_w, const int32_t* counts, const int32_t* offsets,
+                            const int32_t* sorted_assign, float* y, void* workspace, size_t ws_bytes,
+                            void* stream) {
+  qm_status st;
+  if ((st = check_weight(w_gate, "qmoe_grouped_gemm(w_gate)")) != QM_OK) return st;
+  if ((st = check_weight(w_up, "qmoe_grouped_gemm(w_up)")) != QM_OK) return st;
+  if ((st = check_weight(w_down, "qmoe_grouped_gemm(w_down)")) != QM_OK) return st;
+  const qm_qweight* ws[3] = {w_gate, w_up, w_down};
+  for (const qm_qweight* w : ws) {
+    if (w->format != QM_Q4_G32) return fail(QM_EFORMAT, "qmoe_grouped_gemm: experts must be Q4");
+    if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "qmoe_grouped_gemm: experts must be in DEVICE layout");
+  }
+  const int64_t E = w_gate->batch, inter = w_gate->n, hidden = w_gate->k;
+  if (w_up->batch != E || w_up->n != inter || w_up->k != hidden || w_down->batch != E ||
+      w_down->n != hidden || w_down->k != inter)
+    return fail(QM_ESHAPE, "qmoe_grouped_gemm: expert shapes disagree (gate/up [E][inter][hidden], down [E][hidden][inter])");
+  if (E > 1024) return fail(QM_ESHAPE, "qmoe_grouped_gemm: at most 1024 experts");
+  if (inter == 0 || hidden == 0) return fail(QM_ESHAPE, "qmoe_grouped_gemm: empty expert matrices");
+  if (top_k < 1 || top_k > 16 || top_k > E)
+    return fail(QM_ESHAPE, "qmoe_grouped_gemm: top_k=%d must be in [1, min(16, E)]", top_k);
+  if (m < 0 || m > 65536) return fail(QM_ESHAPE, "qmoe_grouped_gemm: m must be in [0, 65536]");
+  if (m == 0) return QM_OK;
+  if (!x || !topk_w || !counts || !offsets || !sorted_assign || !y)
+    return fail(QM_EINVAL, "qmoe_grouped_gemm: null pointer");
+  if (!aligned16(x) || !aligned16(y)) return fail(QM_EALIGN, "qmoe_grouped_gemm: x and y must be 16-byte aligned");
+  const size_t need = moe_workspace_bytes(m, top_k, hidden, inter);
+  if (!workspace || ws_bytes < need)
+    return fail(QM_EWORKSPACE, "qmoe_grouped_gemm: workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  if (!aligned16(workspace)) return fail(QM_EALIGN, "qmoe_grouped_gemm: workspace must be 16-byte aligned");
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  MoeArgs a;
+  a.gq = static_cast<const uint8_t*>(w_gate->qdata); a.gs = w_gate->scales;
+  a.uq = static_cast<const uint8_t*>(w_up->qdata); a.us = w_up->scales;
+  a.dq = static_cast<const uint8_t*>(w_down->qdata); a.ds = w_down->scales;
+  a.x = x; a.counts = counts; a.offsets = offsets; a.sorted_assign = sorted_assign; a.topk_w = topk_w;
+  a.y = y;
+  const size_t h_bytes = (static_cast<size_t>(m * top_k * inter) * 2 + 255) / 256 * 256;
+  a.h = static_cast<uint16_t*>(workspace);
+  a.yp = reinterpret_cast<float*>(static_cast<char*>(workspace) + h_bytes);
+  a.m = m; a.hidden = hidden; a.inter = inter;
+  a.n_experts = static_cast<int32_t>(E); a.top_k = top_k;
+  return launched(launch_moe(a, d->cu_count, static_cast<hipStream_t>(stream)), "qmoe_grouped_gemm");
+}
+
+qm_status qm_device_config(char* buf, size_t len) {
+  if (!buf || len == 0) return fail(QM_EINVAL, "qm_device_config: null buffer");
+  const DeviceInfo* d;
+  qm_status st;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  std::snprintf(buf, len,
+                "arch=%s cu=%d gemv_waves(1024x1024)=%d gemv_waves(lm_head 151936x1024)=%d "
+                "gemm_tile(m=512,n=2048)=%s moe_tile(rows/expert=8)=%s moe_tile(rows/expert=128)=%s",
+                d->arch, d->cu_count, gemv_waves_per_block(16, 32, d->cu_count),
+                gemv_waves_per_block(2374, 32, d->cu_count), gemm_tile_name(512, 2048),
+                moe_tile_name(8), moe_tile_name(128));
+  return QM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,194 @@
+// Decode GEMV with dequantisation fused into the inner loop (BaseRT Sec. 3.3:
+// one GEMV kernel per quantisation format for M = 1, weights never
+// materialised in dequantised form, traffic cut by the compression ratio).
+//
+// Mapping on gfx950
+//  * one workgroup owns one 64-row panel of the device layout; lane r of
+//    every wavefront owns row 64p + r, so one chunk index over the panel is a
+//    contiguous 1 KiB (Q4) / 2 KiB (Q8) load: dwordx4 per lane, fully
+//    coalesced, no cross-lane reduction inside a wavefront;
+//  * the WAVES wavefronts of the workgroup split the K groups of the panel;
+//    their per-row partial sums meet once in LDS and wavefront 0 adds them in
+//    a fixed order (deterministic, single pass, no workspace, no atomics);
+//  * the 32 activations of a group are wavefront-uniform, so they arrive
+//    through scalar loads into SGPRs and feed v_dot2_f32_f16 directly;
+//  * dequantisation in registers: one v_and_or_b32 turns two offset-binary
+//    nibbles u = q + 8 into the fp16 pair 1024 + u (or 1024 + 16u for the
+//    nibbles at bits 4-7), one packed fp16 subtraction gives the exact
+//    integers q (or 16q), one v_dot2_f32_f16 folds two weights into the
+//    fp32 group sum, and the fp16 group scale multiplies the group sum once
+//    (about 1.7 VALU operations per Q4 weight).  Q8 builds 0x64|u bytes with
+//    v_perm_b32 and subtracts 1152.
+#include "qm_internal.h"
+
+#include <hip/hip_fp16.h>
+
+namespace qm {
+namespace {
+
+constexpr int kUnroll = 4;   // chunks in flight per lane
+
+// v_and_or_b32 with the mask in a VGPR and the OR constant in an SGPR (gfx9
+// VOP3 takes no literal and at most one SGPR).
+__device__ inline uint32_t and_or(uint32_t a, uint32_t mask_v, uint32_t or_s) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(mask_v), "s"(or_s));
+  return r;
+}
+
+// Sum over one Q4 group of q[k] * x[k] (fp32).  Dword j of the chunk holds
+// the offset-binary nibbles of k = 8j + {0,2,4,6} in bits 0-15 and of
+// k = 8j + {1,3,5,7} in bits 16-31, so (dword & 0x000F000F) | 0x6400_6400 is
+// the fp16 pair (1024 + u[8j], 1024 + u[8j+1]); the nibbles at bits 4-7 /
+// 20-23 land in mantissa bits 4-7 and give (1024 + 16u), i.e. 16*q after
+// subtracting 1152.  Those pairs accumulate separately and are scaled by
+// 1/16 (exact) at the end of the group.
+__device__ inline float dot_q4_chunk(const uint4 w, const uint32_t* xs, uint32_t m0, uint32_t m1) {
+  const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+  const half2v b1 = {(_Float16)1032.0f, (_Float16)1032.0f};
+  const half2v b16 = {(_Float16)1152.0f, (_Float16)1152.0f};
+  const uint32_t magic = 0x64006400u;
+  float acc1 = 0.0f, acc16 = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t d = wd[j];
+    const uint32_t d8 = d >> 8;
+    const half2v q01 = __builtin_bit_cast(half2v, and_or(d, m0, magic)) - b1;     // k 0,1
+    const half2v q23 = __builtin_bit_cast(half2v, and_or(d, m1, magic)) - b16;    // k 2,3 (x16)
+    const half2v q45 = __builtin_bit_cast(half2v, and_or(d8, m0, magic)) - b1;    // k 4,5
+    const half2v q67 = __builtin_bit_cast(half2v, and_or(d8, m1, magic)) - b16;   // k 6,7 (x16)
+    acc1 = __builtin_amdgcn_fdot2(q01, __builtin_bit_cast(half2v, xs[4 * j + 0]), acc1, false);
+    acc16 = __builtin_amdgcn_fdot2(q23, __builtin_bit_cast(half2v, xs[4 * j + 1]), acc16, false);
+    acc1 = __builtin_amdgcn_fdot2(q45, __builtin_bit_cast(half2v, xs[4 * j + 2]), acc1, false);
+    acc16 = __builtin_amdgcn_fdot2(q67, __builtin_bit_cast(half2v, xs[4 * j + 3]), acc16, false);
+  }
+  return fmaf(acc16, 0.0625f, acc1);
+}
+
+// Sum over 16 Q8 codes (one half chunk, offset-binary bytes) of q * x.
+__device__ inline float dot_q8_half(const uint4 w, const uint32_t* xs) {
+  const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+  const half2v bias = {(_Float16)1152.0f, (_Float16)1152.0f};
+  float acc = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t lo = __builtin_amdgcn_perm(0x64646464u, wd[j], 0x04010400u);  // bytes 0,1
+    const uint32_t hi = __builtin_amdgcn_perm(0x64646464u, wd[j], 0x04030402u);  // bytes 2,3
+    const half2v q0 = __builtin_bit_cast(half2v, lo) - bias;
+    const half2v q1 = __builtin_bit_cast(half2v, hi) - bias;
+    acc = __builtin_amdgcn_fdot2(q0, __builtin_bit_cast(half2v, xs[2 * j]), acc, false);
+    acc = __builtin_amdgcn_fdot2(q1, __builtin_bit_cast(half2v, xs[2 * j + 1]), acc, false);
+  }
+  return acc;
+}
+
+// U chunks starting at chunk c (all in range): issue every load, then reduce.
+template <int FMT, int U>
+__device__ inline float gemv_chunks(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
+                                    const uint32_t* __restrict__ xw, int64_t ch0, int c, int lane,
+                                    uint32_t m0, uint32_t m1) {
+  constexpr int NW = FMT == QM_Q4_G32 ? 1 : 2;
+  uint4 wv[U][NW];
+  uint32_t sv[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t ch = ch0 + c + u;
+    if (FMT == QM_Q4_G32) {
+      wv[u][0] = *reinterpret_cast<const uint4*>(q + (ch * 64 + lane) * 16);
+    } else {
+      const uint8_t* base = q + ch * 2048 + lane * 16;
+      wv[u][0] = *reinterpret_cast<const uint4*>(base);
+      wv[u][NW - 1] = *reinterpret_cast<const uint4*>(base + 1024);
+    }
+    sv[u] = s[ch * 64 + lane];
+  }
+  float acc = 0.0f;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const uint32_t* xs = xw + (c + u) * 16;   // wavefront-uniform: scalar loads
+    float d;
+    if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][0], xs, m0, m1);
+    else d = dot_q8_half(wv[u][0], xs) + dot_q8_half(wv[u][NW - 1], xs + 8);
+    acc = fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sv[u]))), d, acc);
+  }
+  return acc;
+}
+
+template <int FMT, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restrict__ q,
+                                                          const uint16_t* __restrict__ s,
+                                                          const uint16_t* __restrict__ x,
+                                                          float* __restrict__ y, int n_rows,
+                                                          int groups, int chunks_per_wave) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t panel = blockIdx.x;
+  const int c0 = wave * chunks_per_wave;
+  const int c1 = min(groups, c0 + chunks_per_wave);
+  const int64_t ch0 = panel * groups;                 // first (panel, group) chunk index
+  const uint32_t* xw = reinterpret_cast<const uint32_t*>(x);
+  // Loop-invariant masks (the asm constraint keeps them in VGPRs).
+  const uint32_t m0 = 0x000F000Fu;
+  const uint32_t m1 = 0x00F000F0u;
+
+  float acc = 0.0f;
+  int c = c0;
+  for (; c + kUnroll <= c1; c += kUnroll) acc += gemv_chunks<FMT, kUnroll>(q, s, xw, ch0, c, lane, m0, m1);
+  for (; c < c1; ++c) acc += gemv_chunks<FMT, 1>(q, s, xw, ch0, c, lane, m0, m1);
+
+  if (WAVES == 1) {
+    const int64_t n = panel * 64 + lane;
+    if (n < n_rows) y[n] = acc;
+    return;
+  }
+  __shared__ float part[WAVES][64];
+  part[wave][lane] = acc;
+  __syncthreads();
+  if (wave == 0) {
+    float t = part[0][lane];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) t += part[w][lane];
+    const int64_t n = panel * 64 + lane;
+    if (n < n_rows) y[n] = t;
+  }
+}
+
+template <int FMT>
+hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t n,
+                      int64_t k, int cu_count, hipStream_t st) {
+  const int64_t panels = padded_rows(n) / kPanel;
+  const int64_t groups = k / kGroup;
+  const int waves = gemv_waves_per_block(panels, groups, cu_count);
+  const int cpw = static_cast<int>((groups + waves - 1) / waves);
+  const dim3 grid(static_cast<unsigned>(panels));
+  const int ni = static_cast<int>(n), gi = static_cast<int>(groups);
+  switch (waves) {
+    case 1: hipLaunchKernelGGL((gemv_kernel<FMT, 1>), grid, dim3(64), 0, st, q, s, x, y, ni, gi, cpw); break;
+    case 2: hipLaunchKernelGGL((gemv_kernel<FMT, 2>), grid, dim3(128), 0, st, q, s, x, y, ni, gi, cpw); break;
+    case 4: hipLaunchKernelGGL((gemv_kernel<FMT, 4>), grid, dim3(256), 0, st, q, s, x, y, ni, gi, cpw); break;
+    case 8: hipLaunchKernelGGL((gemv_kernel<FMT, 8>), grid, dim3(512), 0, st, q, s, x, y, ni, gi, cpw); break;
+    default: hipLaunchKernelGGL((gemv_kernel<FMT, 16>), grid, dim3(1024), 0, st, q, s, x, y, ni, gi, cpw); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Per-chip choice of wavefronts per panel: enough wavefronts in the grid to
+// keep every CU's memory pipeline busy (>= 8 per CU), never more wavefronts
+// than groups, at most 16 (1024 threads).
+int gemv_waves_per_block(int64_t panels, int64_t groups, int cu_count) {
+  const int64_t want = static_cast<int64_t>(cu_count) * 8;
+  int w = 1;
+  while (w < 16 && panels * w < want && w * 2 <= groups) w *= 2;
+  return w;
+}
+
+hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
+                       int64_t n, int64_t k, int cu_count, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  return fmt == QM_Q4_G32 ? launch_fmt<QM_Q4_G32>(q, s, x, y, n, k, cu_count, st)
+                          : launch_fmt<QM_Q8_G32>(q, s, x, y, n, k, cu_count, st);
+}
+
+}  // namespace qm

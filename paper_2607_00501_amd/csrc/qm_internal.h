@@ -1,0 +1,75 @@
+// Internal declarations shared by the HIP translation units of libqmatmul.
+// Only gfx950 (CDNA4) is targeted: 64-lane wavefronts, fp16 MFMA with fp32
+// accumulation, 160 KiB of LDS per CU.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/qmatmul.h"
+
+namespace qm {
+
+constexpr int kGroup = 32;   // weights per scale (group along K)
+constexpr int kPanel = 64;   // rows per device-layout panel (one row per lane)
+
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef _Float16 half8v __attribute__((ext_vector_type(8)));
+typedef float float16v __attribute__((ext_vector_type(16)));
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+__host__ __device__ inline int64_t padded_rows(int64_t n) { return (n + kPanel - 1) / kPanel * kPanel; }
+
+// Bytes of codes per row of one matrix (canonical and device layouts agree).
+__host__ __device__ inline int64_t row_code_bytes(int32_t fmt, int64_t k) { return fmt == QM_Q4_G32 ? k / 2 : k; }
+
+// Per-matrix sizes for a layout.
+__host__ __device__ inline int64_t matrix_rows(int32_t layout, int64_t n) {
+  return layout == QM_LAYOUT_DEVICE ? padded_rows(n) : n;
+}
+
+// Error reporting into the thread-local buffer; returns the status.
+qm_status fail(qm_status st, const char* fmt, ...);
+qm_status check_launch(const char* what);
+
+// Launchers (validated arguments only).
+hipError_t launch_quantise(int32_t fmt, const float* w, uint8_t* q, uint16_t* s, int64_t batch,
+                           int64_t n, int64_t k, hipStream_t st);
+hipError_t launch_dequantise(int32_t fmt, int32_t layout, const uint8_t* q, const uint16_t* s,
+                             float* out, int64_t batch, int64_t n, int64_t k, hipStream_t st);
+hipError_t launch_repack(int32_t fmt, int32_t src_layout, const uint8_t* sq, const uint16_t* ss,
+                         uint8_t* dq, uint16_t* ds, int64_t batch, int64_t n, int64_t k,
+                         hipStream_t st);
+hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
+                       int64_t n, int64_t k, int cu_count, hipStream_t st);
+hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
+                       int64_t n, int64_t k, int cu_count, hipStream_t st);
+
+struct MoeArgs {
+  const uint8_t* gq; const uint16_t* gs;   // gate [E][inter][hidden], device layout
+  const uint8_t* uq; const uint16_t* us;   // up   [E][inter][hidden]
+  const uint8_t* dq; const uint16_t* ds;   // down [E][hidden][inter]
+  const uint16_t* x;                       // [m][hidden] fp16
+  const int32_t* counts;                   // [E]
+  const int32_t* offsets;                  // [E+1]
+  const int32_t* sorted_assign;            // [m*top_k]
+  const float* topk_w;                     // [m*top_k]
+  float* y;                                // [m][hidden]
+  uint16_t* h;                             // workspace: [m*top_k][inter] fp16
+  float* yp;                               // workspace: [m*top_k][hidden] fp32
+  int64_t m, hidden, inter;
+  int32_t n_experts, top_k;
+};
+size_t moe_workspace_bytes(int64_t m, int32_t top_k, int64_t hidden, int64_t inter);
+hipError_t launch_moe(const MoeArgs& a, int cu_count, hipStream_t st);
+hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, int32_t* ids,
+                        float* w, int32_t* counts, int32_t* offsets, int32_t* sorted_assign,
+                        hipStream_t st);
+
+// Per-chip choices (Sec. 3.3: per-chip configuration table).
+int gemv_waves_per_block(int64_t panels, int64_t groups, int cu_count);
+const char* gemm_tile_name(int64_t m, int64_t n);
+const char* moe_tile_name(int64_t rows_per_expert);
+
+}  // namespace qm

@@ -1,0 +1,142 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads and
+exports every function include/qmatmul.h declares, the pure host functions
+return the documented sizes, and invalid arguments are rejected before any
+device work with the documented status and a message."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_00501_amd import binding as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "qmatmul.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(q\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert len(names) >= 11, names
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B.EXPORTS)
+
+
+@pytest.mark.parametrize("fmt,layout,batch,n,k,want", [
+    (B.Q4_G32, B.LAYOUT_CANONICAL, 1, 3, 64, (3 * 32, 3 * 2 * 2)),
+    (B.Q4_G32, B.LAYOUT_DEVICE, 1, 3, 64, (64 * 32, 64 * 2 * 2)),
+    (B.Q8_G32, B.LAYOUT_DEVICE, 2, 65, 32, (2 * 128 * 32, 2 * 128 * 2)),
+    (B.Q4_G32, B.LAYOUT_DEVICE, 1, 151936, 1024, (151936 * 512, 151936 * 32 * 2)),
+    (B.Q8_G32, B.LAYOUT_CANONICAL, 128, 768, 2048, (128 * 768 * 2048, 128 * 768 * 64 * 2)),
+])
+def test_weight_bytes(fmt, layout, batch, n, k, want):
+    assert B.qm_weight_bytes(fmt, layout, batch, n, k) == want
+
+
+@pytest.mark.parametrize("args,status", [
+    ((3, 0, 1, 4, 64), 4),          # bad format
+    ((1, 7, 1, 4, 64), 5),          # bad layout
+    ((1, 0, 1, 4, 48), 2),          # k % 32
+    ((1, 0, 0, 4, 64), 2),          # batch 0
+])
+def test_weight_bytes_errors(args, status):
+    with pytest.raises(B.QmError) as e:
+        B.qm_weight_bytes(*args)
+    assert e.value.status == status
+    assert B.qm_last_error()
+
+
+def _fake_weight(fmt=1, layout=1, batch=1, n=64, k=64, qdata=0x10000, scales=0x20000):
+    return B.CQWeight(fmt, layout, batch, n, k, qdata, scales)
+
+
+def _call(name, *args):
+    return getattr(B.lib(), name)(*args)
+
+
+def test_gemv_validation_before_device_work():
+    L = B.lib()
+    x, y = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x40000)
+    cases = [
+        (None, 1),                                          # null descriptor
+        (_fake_weight(layout=0), 5),                        # canonical layout
+        (_fake_weight(k=48), 2),                            # k % 32
+        (_fake_weight(batch=2), 2),                         # batched GEMV
+        (_fake_weight(fmt=9), 4),                           # unknown format
+        (_fake_weight(qdata=0x10008), 3),                   # misaligned
+        (_fake_weight(qdata=0), 1),                         # null codes
+    ]
+    for w, status in cases:
+        st = L.qmatmul_gemv(ctypes.byref(w) if w is not None else None, x, y, None)
+        assert st == status, (w and (w.format, w.layout, w.k, w.batch), st)
+        assert B.qm_last_error()
+    w = _fake_weight()
+    assert L.qmatmul_gemv(ctypes.byref(w), ctypes.c_void_p(0x30004), y, None) == 3   # x misaligned
+    assert L.qmatmul_gemv(ctypes.byref(w), None, y, None) == 1
+
+
+def test_gemm_and_moe_validation():
+    L = B.lib()
+    w = _fake_weight()
+    x, y = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x40000)
+    assert L.qmatmul_gemm(ctypes.byref(w), x, 0, y, None) == 2          # m = 0
+    assert L.qmatmul_gemm(ctypes.byref(w), x, 70000, y, None) == 2      # m too large
+    w8 = _fake_weight(fmt=2)
+    assert L.qmatmul_gemm(ctypes.byref(w8), x, 16, y, None) == 4        # Q8 GEMM not offered
+    p = ctypes.c_void_p(0x50000)
+    assert L.qmoe_route(p, 16, 2000, 8, p, p, p, p, p, None) == 2       # too many experts
+    assert L.qmoe_route(p, 16, 128, 17, p, p, p, p, p, None) == 2       # top_k > 16
+    assert L.qmoe_route(p, 16, 4, 8, p, p, p, p, p, None) == 2          # top_k > E
+    assert L.qmoe_route(p, 16, 128, 8, p, p, None, p, p, None) == 1     # null counts
+    g = _fake_weight(batch=8, n=96, k=64)
+    d = _fake_weight(batch=8, n=64, k=96)
+    bad = _fake_weight(batch=8, n=64, k=64)
+    ws = ctypes.c_void_p(0x60000)
+    args = lambda wg, wu, wd, nbytes: L.qmoe_grouped_gemm(
+        ctypes.byref(wg), ctypes.byref(wu), ctypes.byref(wd), x, 16, 2, p, p, p, p, y, ws, nbytes, None)
+    need = B.qmoe_workspace_bytes(16, 8, 2, 64, 96)
+    assert need == 16 * 2 * 96 * 2 + 16 * 2 * 64 * 4
+    assert args(g, g, bad, need) == 2                                  # down shape mismatch
+    assert args(g, g, d, need - 1) == 6                                # workspace too small
+    g8 = _fake_weight(fmt=2, batch=8, n=96, k=64)
+    assert args(g8, g, d, need) == 4                                   # experts must be Q4
+
+
+def test_quantise_repack_validation():
+    L = B.lib()
+    w = _fake_weight(layout=1)
+    p = ctypes.c_void_p(0x70000)
+    assert L.qm_quantise(1, p, ctypes.byref(w), None) == 5            # must write canonical
+    wc = _fake_weight(layout=0)
+    assert L.qm_quantise(2, p, ctypes.byref(wc), None) == 4           # format mismatch
+    assert L.qm_quantise(1, ctypes.c_void_p(0x70004), ctypes.byref(wc), None) == 3
+    assert L.qm_repack(ctypes.byref(wc), ctypes.byref(wc), None) == 5  # same layout
+    other = _fake_weight(layout=1, n=65)
+    assert L.qm_repack(ctypes.byref(wc), ctypes.byref(other), None) == 2
+
+
+def test_error_text_is_thread_local():
+    import threading
+    L = B.lib()
+    L.qm_weight_bytes(9, 0, 1, 1, 32, ctypes.byref(ctypes.c_size_t()), ctypes.byref(ctypes.c_size_t()))
+    main_msg = B.qm_last_error()
+    seen = {}
+
+    def other():
+        seen["before"] = B.qm_last_error()
+        L.qm_weight_bytes(1, 9, 1, 1, 32, ctypes.byref(ctypes.c_size_t()), ctypes.byref(ctypes.c_size_t()))
+        seen["after"] = B.qm_last_error()
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen["before"] == ""
+    assert "layout" in seen["after"]
+    assert B.qm_last_error() == main_msg and "format" in main_msg

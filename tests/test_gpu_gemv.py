@@ -1,0 +1,117 @@
+"""GPU parity of the fused dequantise+GEMV (qmatmul_gemv) with the oracle."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import qmatmul_oracle as O
+from paper_2607_00501_amd import binding as B
+from paper_2607_00501_amd import inputs, workloads
+from tests.helpers import GEMV_TOL, rel_err
+
+pytestmark = pytest.mark.gpu
+
+FMTS = [(O.Q4, B.Q4_G32), (O.Q8, B.Q8_G32)]
+
+
+def _device_weight(w_np, bfmt):
+    w = torch.from_numpy(np.ascontiguousarray(w_np)).cuda()
+    return B.qm_repack(B.qm_quantise(w, bfmt), B.LAYOUT_DEVICE)
+
+
+@pytest.mark.parametrize("ofmt,bfmt", FMTS)
+@pytest.mark.parametrize("n,k", [(1, 32), (63, 64), (65, 96), (200, 1024), (1024, 1024),
+                                 (130, 3072), (1000, 2048), (64, 8192)])
+def test_gemv_parity(ofmt, bfmt, n, k):
+    w = inputs.weights_np(inputs.seed_for(0, n, "q"), (n, k))
+    x = inputs.activations_np(inputs.seed_for(0, n, "x"), (k,))
+    wd = _device_weight(w, bfmt)
+    y = B.qmatmul_gemv(wd, torch.from_numpy(x).cuda()).cpu().numpy()
+    q, s = O.quantise(w, ofmt)
+    ref = O.gemv(O.pack(q, ofmt), s, ofmt, x)
+    assert rel_err(y, ref) <= GEMV_TOL
+    assert rel_err(y, ref) <= 1e-5          # fp32 accumulation in practice
+
+
+@pytest.mark.parametrize("ofmt,bfmt", FMTS)
+def test_gemv_integer_grid_exact(ofmt, bfmt):
+    """Scale-1 integer weights and small integer x: every partial sum is an
+    integer below 2^24, so the fp32 result must equal the oracle exactly."""
+    rng = np.random.default_rng(3)
+    qm = O.QMAX[ofmt]
+    n, k = 300, 1536
+    w = rng.integers(-qm, qm + 1, size=(n, k))
+    w[:, ::32] = qm
+    x = rng.integers(-3, 4, size=k).astype(np.float16)
+    wd = _device_weight(w.astype(np.float32), bfmt)
+    y = B.qmatmul_gemv(wd, torch.from_numpy(x).cuda()).cpu().numpy()
+    q, s = O.quantise(w.astype(np.float32), ofmt)
+    ref = O.gemv(O.pack(q, ofmt), s, ofmt, x)
+    assert np.array_equal(y.astype(np.float64), ref)
+
+
+def test_gemv_one_hot_x_gives_column():
+    n, k = 150, 512
+    w = inputs.weights_np(11, (n, k))
+    wd = _device_weight(w, B.Q4_G32)
+    q, s = O.quantise(w, O.Q4)
+    col = O.dequantise(O.pack(q, O.Q4), s, O.Q4)
+    for kk in (0, 33, 511):
+        x = np.zeros(k, np.float16)
+        x[kk] = 1.0
+        y = B.qmatmul_gemv(wd, torch.from_numpy(x).cuda()).cpu().numpy()
+        assert np.array_equal(y, col[:, kk])
+
+
+def test_gemv_deterministic_and_config0():
+    """Config 0: single Q4 GEMV 1024x1024; repeated calls are bitwise equal."""
+    cfg = workloads.SINGLE_GEMV
+    w = inputs.weights_np(inputs.seed_for(0, 0, "q"), (cfg["n"], cfg["k"]))
+    x = inputs.activations_np(inputs.seed_for(0, 0, "x"), (cfg["k"],))
+    wd = _device_weight(w, B.Q4_G32)
+    xt = torch.from_numpy(x).cuda()
+    y1 = B.qmatmul_gemv(wd, xt)
+    y2 = B.qmatmul_gemv(wd, xt)
+    assert torch.equal(y1, y2)
+    q, s = O.quantise(w, O.Q4)
+    assert rel_err(y1.cpu().numpy(), O.gemv(O.pack(q, O.Q4), s, O.Q4, x)) <= GEMV_TOL
+
+
+def test_gemv_empty_is_noop():
+    wd = B.empty_qweight(B.Q4_G32, B.LAYOUT_DEVICE, 1, 0, 64)
+    x = torch.zeros(64, dtype=torch.float16, device="cuda")
+    y = torch.full((4,), 7.0, device="cuda")
+    B.qmatmul_gemv(wd, x, out=y)
+    assert torch.all(y == 7.0)
+
+
+@pytest.mark.parametrize("ofmt,bfmt,model", [(O.Q4, B.Q4_G32, "qwen"), (O.Q8, B.Q8_G32, "llama3b"),
+                                             (O.Q4, B.Q4_G32, "llama3b")])
+def test_full_size_lm_head_sampled_rows(ofmt, bfmt, model):
+    """Full-size lm_heads (Qwen3-0.6B 1024->151936, Llama-3.2-3B 3072->128256)
+    in the bench's launch configuration; the oracle recomputes sampled rows."""
+    cfgn, m = (1, workloads.QWEN3_06B) if model == "qwen" else (2, workloads.LLAMA32_3B)
+    k, n = m["lm_head"]
+    w = inputs.weights_dev(inputs.seed_for(cfgn, m["layers"], "lm_head"), (n, k))
+    x = inputs.activations_dev(inputs.seed_for(cfgn, m["layers"], "x"), (k,))
+    wd = B.qm_repack(B.qm_quantise(w, bfmt), B.LAYOUT_DEVICE)
+    y = B.qmatmul_gemv(wd, x).cpu().numpy()
+    rows = np.unique(np.concatenate([np.arange(0, n, 997), [n - 1]]))
+    w_rows = w[torch.from_numpy(rows).cuda()].cpu().numpy()
+    del w
+    q, s = O.quantise(w_rows, ofmt)
+    ref = O.gemv(O.pack(q, ofmt), s, ofmt, x.cpu().numpy())
+    assert rel_err(y[rows], ref) <= GEMV_TOL
+
+
+@pytest.mark.parametrize("cfgn,model", [(1, workloads.QWEN3_06B), (2, workloads.LLAMA32_3B)])
+def test_decode_stack_layer_shapes(cfgn, model):
+    """One layer of each decode stack, every projection, full size."""
+    for li, (name, k, n) in enumerate(model["layer"]):
+        w = inputs.weights_np(inputs.seed_for(cfgn, 0, name), (n, k))
+        x = inputs.activations_np(inputs.seed_for(cfgn, 0, "x", li), (k,))
+        for ofmt, bfmt in FMTS:
+            wd = _device_weight(w, bfmt)
+            y = B.qmatmul_gemv(wd, torch.from_numpy(x).cuda()).cpu().numpy()
+            q, s = O.quantise(w, ofmt)
+            assert rel_err(y, O.gemv(O.pack(q, ofmt), s, ofmt, x)) <= GEMV_TOL, (name, ofmt)
