@@ -1,0 +1,376 @@
+"""Benchmark of the quantised-matmul hot path on one MI355X.
+
+Default workload (the JSON line's `value`): one decode step of a
+Qwen3-0.6B-shaped stack at batch 1 with Q4 group-32 weights -- 28 layers x
+{q 1024->2048, k/v 1024->1024, o 2048->1024, gate/up 1024->3072,
+down 3072->1024} plus the lm_head 1024->151936, i.e. 197 GEMV calls, each
+with its own fp16 activation vector.  All weights (335,241,216 bytes of Q4
+codes and scales) sit in HBM in the device layout before timing; the 197
+calls of a step are captured once in a HIP graph and replayed.
+
+value = Q4 weight bytes streamed per step x steps / elapsed (GB/s).
+
+The line also carries
+  roofline:     the dominant kernel's achieved weight GB/s (algorithmic bytes
+                per launch / its mean launch duration, timed with HIP events
+                on the launch stream) against the 8 TB/s HBM peak;
+  cpu_baseline: the CPU oracle timed on a bounded sample of the same step;
+  extra:        the other workloads (single 1024x1024 GEMV, Llama-3.2-3B Q4 and
+                Q8 decode stacks, Llama-3.2-1B prefill GEMM stacks and the
+                Qwen3-30B-A3B MoE layer at M = 128 / 512 / 2048), each timed
+                the same way (omit with --extra none).
+
+Run: python bench.py [--gpus 1] [--steps K] [--warmup W] [--extra all|none]
+"""
+
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 FLOP/clk (dense fp16)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# --------------------------------------------------------------- helpers
+
+class GemvCall:
+    """One pre-marshalled qmatmul_gemv call (descriptor kept alive)."""
+
+    def __init__(self, lib, wd, x, y):
+        self.lib, self.wd, self.x, self.y = lib, wd, x, y
+        self.desc = wd.c()
+        self.ref = ctypes.byref(self.desc)
+        self.xp = ctypes.c_void_p(x.data_ptr())
+        self.yp = ctypes.c_void_p(y.data_ptr())
+
+    def __call__(self, stream):
+        st = self.lib.qmatmul_gemv(self.ref, self.xp, self.yp, stream)
+        if st != 0:
+            raise RuntimeError(self.lib.qm_last_error().decode())
+
+
+def build_decode_stack(model, cfg_id, fmt, torch, B, inputs, workloads, want_fp32=False):
+    """Quantise + repack every projection of a decode stack on the GPU."""
+    lib = B.lib()
+    calls, nbytes = [], 0
+    for ci, (layer, name, k, n) in enumerate(workloads.stack_calls(model)):
+        w = inputs.weights_dev(inputs.seed_for(cfg_id, layer, name), (n, k))
+        wd = B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE)
+        del w
+        x = inputs.activations_dev(inputs.seed_for(cfg_id, layer, "x", ci), (k,))
+        y = torch.empty(n, dtype=torch.float32, device="cuda")
+        calls.append(GemvCall(lib, wd, x, y))
+        nbytes += workloads.q4_bytes(k, n) if fmt == B.Q4_G32 else workloads.q8_bytes(k, n)
+    torch.cuda.synchronize()
+    return calls, nbytes
+
+
+def capture(torch, fn):
+    """Capture fn(stream_ptr) into a graph on a side stream; returns the graph."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for _ in range(2):                       # eager warm-up outside capture
+            fn(ctypes.c_void_p(s.cuda_stream))
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn(ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    return g
+
+
+def time_graph(torch, g, steps, warmup):
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(st)
+    for _ in range(steps):
+        g.replay()
+    e1.record(st)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return e0.elapsed_time(e1) / 1e3, wall      # seconds (events), seconds (wall)
+
+
+def per_launch_ms(torch, calls, passes=5):
+    """Mean duration of each call, timed with an event pair around every
+    launch on the launch stream (eager, not captured)."""
+    st = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(st.cuda_stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in calls]
+    tot = [0.0] * len(calls)
+    for _ in range(passes):
+        for c, (a, b) in zip(calls, ev):
+            a.record(st)
+            c(sp)
+            b.record(st)
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(ev):
+            tot[i] += a.elapsed_time(b)
+    return [t / passes for t in tot]
+
+
+# --------------------------------------------------------- CPU baseline
+
+def cpu_baseline(budget_s: float):
+    """The CPU oracle on a bounded sample of the default workload: whole
+    layers of the Qwen3-0.6B Q4 decode step, then a slice of the lm_head,
+    until about budget_s seconds of oracle time have been spent."""
+    import numpy as np
+    from oracle import qmatmul_oracle as O
+    from paper_2607_00501_amd import inputs, workloads
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = 1
+    model = workloads.QWEN3_06B
+    spent, nbytes, ncalls, layers = 0.0, 0, 0, 0
+    wall0 = time.perf_counter()
+    for layer in range(model["layers"]):
+        for ci, (name, k, n) in enumerate(model["layer"]):
+            w = inputs.weights_np(inputs.seed_for(1, layer, name), (n, k))
+            x = inputs.activations_np(inputs.seed_for(1, layer, "x", ci), (k,))
+            q, s = O.quantise(w, O.Q4)
+            qb = O.pack(q, O.Q4)
+            t0 = time.perf_counter()
+            O.gemv(qb, s, O.Q4, x)
+            spent += time.perf_counter() - t0
+            nbytes += workloads.q4_bytes(k, n)
+            ncalls += 1
+        layers += 1
+        if spent > budget_s * 0.6 or time.perf_counter() - wall0 > budget_s * 2:
+            break
+    k, n_full = model["lm_head"]
+    rows = min(n_full, 16384)
+    w = inputs.weights_np(inputs.seed_for(1, model["layers"], "lm_head"), (rows, k))
+    x = inputs.activations_np(inputs.seed_for(1, model["layers"], "x"), (k,))
+    q, s = O.quantise(w, O.Q4)
+    qb = O.pack(q, O.Q4)
+    t0 = time.perf_counter()
+    O.gemv(qb, s, O.Q4, x)
+    spent += time.perf_counter() - t0
+    nbytes += workloads.q4_bytes(k, rows)
+    return {"value": round(nbytes / spent / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{ncalls} GEMVs (layers 0-{layers - 1}, all 7 projections) + lm_head rows "
+                      f"0-{rows - 1} of the Qwen3-0.6B Q4 decode step; {nbytes} weight bytes in "
+                      f"{spent:.2f} s of oracle time (numpy fp64; BLAS threads={threads})"}
+
+
+# ------------------------------------------------------------ extras
+
+def extra_workloads(torch, B, inputs, workloads, steps, warmup):
+    out = {}
+    lib = B.lib()
+
+    # single Q4 GEMV 1024 x 1024
+    cfg = workloads.SINGLE_GEMV
+    w = inputs.weights_dev(inputs.seed_for(0, 0, "q"), (cfg["n"], cfg["k"]))
+    wd = B.qm_repack(B.qm_quantise(w, B.Q4_G32), B.LAYOUT_DEVICE)
+    x = inputs.activations_dev(inputs.seed_for(0, 0, "x"), (cfg["k"],))
+    y = torch.empty(cfg["n"], device="cuda")
+    call = GemvCall(lib, wd, x, y)
+    reps = 100
+    g = capture(torch, lambda s: [call(s) for _ in range(reps)])
+    t, _ = time_graph(torch, g, max(steps // 5, 5), warmup)
+    us = t / (max(steps // 5, 5) * reps) * 1e6
+    ms = per_launch_ms(torch, [call], passes=20)[0]
+    out["single_gemv_1024x1024_q4"] = {"us_per_call_graph": round(us, 3), "us_per_launch_events": round(ms * 1e3, 3),
+                                       "weight_GBps_graph": round(workloads.q4_bytes(1024, 1024) / us / 1e3, 2)}
+    log(f"config single gemv: {us:.2f} us/call")
+    del g
+
+    # Llama-3.2-3B decode stacks, Q4 and Q8
+    for fmt, tag in ((B.Q4_G32, "q4"), (B.Q8_G32, "q8")):
+        calls, nbytes = build_decode_stack(workloads.LLAMA32_3B, 2, fmt, torch, B, inputs, workloads)
+        g = capture(torch, lambda s: [c(s) for c in calls])
+        t, _ = time_graph(torch, g, steps, warmup)
+        per = per_launch_ms(torch, calls, passes=3)
+        head_ms = per[-1]
+        kh, nh = workloads.LLAMA32_3B["lm_head"]
+        head_bytes = workloads.q4_bytes(kh, nh) if fmt == B.Q4_G32 else workloads.q8_bytes(kh, nh)
+        out[f"llama3.2-3b_decode_{tag}"] = {
+            "tokens_per_s": round(steps / t, 2), "ms_per_token": round(t / steps * 1e3, 4),
+            "weight_GBps": round(nbytes * steps / t / 1e9, 2),
+            "frac_hbm_peak": round(nbytes * steps / t / 1e9 / HBM_PEAK_GBS, 4),
+            "lm_head_GBps_events": round(head_bytes / (head_ms * 1e-3) / 1e9, 2),
+            "lm_head_frac_hbm_peak": round(head_bytes / (head_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"llama3b {tag}: {out[f'llama3.2-3b_decode_{tag}']}")
+        del g, calls
+        torch.cuda.empty_cache()
+
+    # Llama-3.2-1B prefill GEMM stacks
+    model = workloads.LLAMA32_1B_PREFILL
+    wds = []
+    for layer in range(model["layers"]):
+        for name, k, n in model["layer"]:
+            w = inputs.weights_dev(inputs.seed_for(3, layer, name), (n, k))
+            wds.append((B.qm_repack(B.qm_quantise(w, B.Q4_G32), B.LAYOUT_DEVICE), k, n))
+            del w
+    for m in model["m_sweep"]:
+        xs = {k: inputs.activations_dev(inputs.seed_for(3, 0, "x", k), (m, k)) for k in {k for _, k, _ in wds}}
+        ys = [torch.empty((m, n), device="cuda") for _, _, n in wds]
+        descs = [wd.c() for wd, _, _ in wds]
+        def run(s, xs=xs, ys=ys, descs=descs, m=m):
+            for d, (wd, k, n), yv in zip(descs, wds, ys):
+                st = lib.qmatmul_gemm(ctypes.byref(d), ctypes.c_void_p(xs[k].data_ptr()), m,
+                                      ctypes.c_void_p(yv.data_ptr()), s)
+                if st:
+                    raise RuntimeError(lib.qm_last_error().decode())
+        g = capture(torch, run)
+        t, _ = time_graph(torch, g, max(steps // 2, 5), warmup)
+        flops = 2.0 * m * sum(k * n for _, k, n in wds)
+        tf = flops * max(steps // 2, 5) / t / 1e12
+        out[f"llama3.2-1b_prefill_m{m}"] = {"tokens_per_s": round(m * max(steps // 2, 5) / t, 1),
+                                            "stack_TFLOPs": round(tf, 2),
+                                            "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4)}
+        log(f"prefill m={m}: {out[f'llama3.2-1b_prefill_m{m}']}")
+        del g, ys, xs
+    del wds
+    torch.cuda.empty_cache()
+
+    # Qwen3-30B-A3B MoE layer
+    cfg = workloads.QWEN3_30B_A3B_MOE
+    E, K, H, I = cfg["experts"], cfg["top_k"], cfg["hidden"], cfg["inter"]
+    mk = lambda t, sh: B.qm_repack(B.qm_quantise(inputs.weights_dev(inputs.seed_for(4, 0, t), sh), B.Q4_G32),
+                                   B.LAYOUT_DEVICE)
+    wg, wu, wdn = mk("gate", (E, I, H)), mk("up", (E, I, H)), mk("down", (E, H, I))
+    wbytes = 3 * E * workloads.q4_bytes(H, I)
+    for m in cfg["m_sweep"]:
+        x = inputs.activations_dev(inputs.seed_for(4, m, "x"), (m, H))
+        lg = inputs.logits_dev(inputs.seed_for(4, m, "logits"), (m, E))
+        r = B.qmoe_route(lg, K)
+        yv = torch.empty((m, H), device="cuda")
+        ws = torch.empty(B.qmoe_workspace_bytes(m, E, K, H, I), dtype=torch.uint8, device="cuda")
+        def run(s, x=x, lg=lg, r=r, yv=yv, ws=ws):
+            B.qmoe_route(lg, K, out=r, stream=_Raw(s))
+            B.qmoe_grouped_gemm(wg, wu, wdn, x, r, out=yv, workspace=ws, stream=_Raw(s))
+        g = capture(torch, run)
+        t, _ = time_graph(torch, g, max(steps // 2, 5), warmup)
+        n = max(steps // 2, 5)
+        flops = 2.0 * m * K * 3 * H * I
+        tf = flops * n / t / 1e12
+        ai = flops / wbytes
+        attainable = min(MFMA_F16_PEAK_TFLOPS, ai * HBM_PEAK_GBS / 1e3)
+        out[f"qwen3-30b-a3b_moe_m{m}"] = {"tokens_per_s": round(m * n / t, 1), "layer_us": round(t / n * 1e6, 2),
+                                          "TFLOPs": round(tf, 2), "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4),
+                                          "frac_attainable": round(tf / attainable, 4),
+                                          "weight_GBps": round(wbytes * n / t / 1e9, 1)}
+        log(f"moe m={m}: {out[f'qwen3-30b-a3b_moe_m{m}']}")
+        del g
+    return out
+
+
+class _Raw:
+    """Adapter so binding functions accept a raw stream pointer."""
+
+    def __init__(self, ptr):
+        self.cuda_stream = ptr.value
+
+
+# ---------------------------------------------------------------- main
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--extra", choices=["all", "none"], default="all")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the quantised matmul path "
+                                   "has no multi-GPU component; run with --gpus 1"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2607_00501_amd import binding as B
+    from paper_2607_00501_amd import inputs, workloads
+
+    B.lib()                                   # raises if the HIP library is missing
+    torch.cuda.set_device(0)
+    log(f"device config: {B.qm_device_config()}")
+
+    # copy kernel of known size, for scaling the HBM byte counters
+    a = torch.empty(64 << 20, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    del a, b
+
+    model = workloads.QWEN3_06B
+    calls, nbytes = build_decode_stack(model, 1, B.Q4_G32, torch, B, inputs, workloads)
+    log(f"qwen3-0.6b stack ready: {len(calls)} GEMVs, {nbytes} weight bytes")
+    g = capture(torch, lambda s: [c(s) for c in calls])
+    secs, wall = time_graph(torch, g, args.steps, args.warmup)
+    gbs = nbytes * args.steps / secs / 1e9
+    log(f"step: {secs / args.steps * 1e3:.4f} ms, {gbs:.1f} GB/s (wall {wall:.3f} s)")
+
+    # dominant kernel: mean launch duration per kernel instance, event-timed
+    per = per_launch_ms(torch, calls, passes=10)
+    groups = {"gemv_kernel<Q4, 16 waves> (196 layer projections)": (per[:-1], nbytes - workloads.q4_bytes(*model["lm_head"])),
+              "gemv_kernel<Q4, 4 waves> (lm_head 1024->151936)": (per[-1:], workloads.q4_bytes(*model["lm_head"]))}
+    totals = {k: sum(v[0]) for k, v in groups.items()}
+    dom = max(totals, key=totals.get)
+    launches, dom_bytes = groups[dom]
+    mean_ms = sum(launches) / len(launches)
+    bytes_per_launch = dom_bytes / len(launches)
+    achieved = bytes_per_launch / (mean_ms * 1e-3) / 1e9
+    lm_name = "gemv_kernel<Q4, 4 waves> (lm_head 1024->151936)"
+    lm_ms = groups[lm_name][0][0]
+    lm_gbs = groups[lm_name][1] / (lm_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom,
+                "launches_per_step": len(launches), "mean_launch_us": round(mean_ms * 1e3, 3),
+                "algorithmic_bytes_per_launch": int(bytes_per_launch),
+                "lm_head_launch_us": round(lm_ms * 1e3, 3), "lm_head_GBps": round(lm_gbs, 1),
+                "lm_head_frac": round(lm_gbs / HBM_PEAK_GBS, 4)}
+    log(f"roofline: {roofline}")
+    del g
+
+    extra = {}
+    if args.extra == "all":
+        del calls
+        torch.cuda.empty_cache()
+        extra = extra_workloads(torch, B, inputs, workloads, args.steps, args.warmup)
+
+    cpu = cpu_baseline(args.cpu_seconds)
+    log(f"cpu baseline: {cpu}")
+
+    line = {
+        "metric": "Q4 decode GEMV weight GB/s (% of HBM peak); prefill/MoE GEMM TFLOP/s",
+        "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(secs / args.steps * 1e3, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f16 (Q4 weights dequantised in registers, fp32 accumulation)",
+        "data": "synthetic (seeded N(0,0.02^2) weights quantised on the GPU, N(0,1) fp16 activations)",
+        "config": {"workload": "qwen3-0.6b decode stack, batch 1, Q4 group-32: 28 layers x 7 GEMVs + "
+                               "lm_head 1024->151936 (197 GEMV calls per token)",
+                   "weight_bytes_per_step": nbytes, "tokens_per_s": round(args.steps / secs, 2),
+                   "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4), "timing": "hip graph replay, HIP events"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "extra": extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -124,8 +124,8 @@ def qm_weight_bytes(fmt: int, layout: int, batch: int, n: int, k: int):
 def empty_qweight(fmt: int, layout: int, batch: int, n: int, k: int, device="cuda") -> QWeight:
     qb, sb = qm_weight_bytes(fmt, layout, batch, n, k)
     return QWeight(fmt, layout, batch, n, k,
-                   torch.empty(max(qb, 16), dtype=torch.uint8, device=device),
-                   torch.empty(max(sb // 2, 8), dtype=torch.int16, device=device))
+                   torch.empty(max(qb, 1), dtype=torch.uint8, device=device),
+                   torch.empty(max(sb // 2, 1), dtype=torch.int16, device=device))
 
 
 def qm_quantise(w: torch.Tensor, fmt: int, out: Optional[QWeight] = None, stream=None) -> QWeight:

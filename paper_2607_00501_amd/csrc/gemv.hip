@@ -175,10 +175,10 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
 }  // namespace
 
 // Per-chip choice of wavefronts per panel: enough wavefronts in the grid to
-// keep every CU's memory pipeline busy (>= 8 per CU), never more wavefronts
-// than groups, at most 16 (1024 threads).
+// keep every CU's memory pipeline busy (>= 32 per CU, i.e. 8 per SIMD), never
+// more wavefronts than groups, at most 16 (1024 threads).
 int gemv_waves_per_block(int64_t panels, int64_t groups, int cu_count) {
-  const int64_t want = static_cast<int64_t>(cu_count) * 8;
+  const int64_t want = static_cast<int64_t>(cu_count) * 32;
   int w = 1;
   while (w < 16 && panels * w < want && w * 2 <= groups) w *= 2;
   return w;
