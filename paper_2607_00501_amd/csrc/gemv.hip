@@ -23,10 +23,27 @@
 
 #include <hip/hip_fp16.h>
 
+#include <cstdio>
+#include <cstdlib>
+
 namespace qm {
 namespace {
 
 constexpr int kUnroll = 4;   // chunks in flight per lane
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// In the large-matrix kernel weights and scales are streamed once per call:
+// nontemporal loads raise the sustained read rate (measured +12% on a plain
+// streaming read).  The small-matrix kernel keeps ordinary loads, whose
+// first-access latency measured lower.
+__device__ inline uint4 stream_load16(const uint8_t* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ inline uint32_t stream_load_u16(const uint16_t* p) {
+  return __builtin_nontemporal_load(p);
+}
 
 // v_and_or_b32 with the mask in a VGPR and the OR constant in an SGPR (gfx9
 // VOP3 takes no literal and at most one SGPR).
@@ -94,13 +111,13 @@ __device__ inline float gemv_chunks(const uint8_t* __restrict__ q, const uint16_
   for (int u = 0; u < U; ++u) {
     const int64_t ch = ch0 + c + u;
     if (FMT == QM_Q4_G32) {
-      wv[u][0] = *reinterpret_cast<const uint4*>(q + (ch * 64 + lane) * 16);
+      wv[u][0] = stream_load16(q + (ch * 64 + lane) * 16);
     } else {
       const uint8_t* base = q + ch * 2048 + lane * 16;
-      wv[u][0] = *reinterpret_cast<const uint4*>(base);
-      wv[u][NW - 1] = *reinterpret_cast<const uint4*>(base + 1024);
+      wv[u][0] = stream_load16(base);
+      wv[u][NW - 1] = stream_load16(base + 1024);
     }
-    sv[u] = s[ch * 64 + lane];
+    sv[u] = stream_load_u16(s + ch * 64 + lane);
   }
   float acc = 0.0f;
 #pragma unroll
@@ -153,12 +170,147 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
   }
 }
 
+// Sub-panel variant for matrices with fewer 64-row panels than CUs: a
+// workgroup owns SUBR rows of one panel (lane = (row r, chunk lane cl), CL =
+// 64/SUBR chunk lanes per wavefront), so N/SUBR workgroups spread the VALU
+// dequantisation and the loads over many CUs.  One wavefront load reads CL
+// contiguous segments of SUBR*16 bytes.  Every lane issues all of its (at
+// most kSubU per pass) chunk loads before the first use, so a small GEMV
+// costs one memory round trip.  Lanes of a wavefront see different groups,
+// so activations come either from an LDS copy of x made once per workgroup
+// (XLDS) or straight from global memory (four 16-byte loads per chunk,
+// served by the L1/L2 broadcast).  Per-row sums: butterfly over the chunk
+// lanes, then a fixed-order sum over wavefronts in LDS.
+constexpr int kSubU = 8;
+
+template <int FMT, int SUBR, int WAVES, bool XLDS>
+__global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(const uint8_t* __restrict__ q,
+                                                              const uint16_t* __restrict__ s,
+                                                              const uint16_t* __restrict__ x,
+                                                              float* __restrict__ y, int n_rows,
+                                                              int groups) {
+  constexpr int CL = 64 / SUBR;
+  constexpr int NW = FMT == QM_Q4_G32 ? 1 : 2;
+  constexpr int U = kSubU;
+  extern __shared__ uint4 xs[];                       // groups * 4 uint4 (K halves) if XLDS
+  __shared__ float part[WAVES][SUBR];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r = lane % SUBR, cl = lane / SUBR;
+  const int64_t panel = blockIdx.x / CL;
+  const int row = (blockIdx.x % CL) * SUBR + r;       // row inside the panel
+  const int64_t ch0 = panel * groups;
+  const int stride = WAVES * CL;
+  const int first = wave * CL + cl;
+  const int iters = (groups + U * stride - 1) / (U * stride);
+  const uint32_t m0 = 0x000F000Fu, m1 = 0x00F000F0u;
+  const uint4* xg = reinterpret_cast<const uint4*>(x);
+
+  float acc = 0.0f;
+  for (int it = 0; it < iters; ++it) {
+    uint4 wv[U][NW];
+    uint32_t sv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = first + (it * U + u) * stride;
+      if (c < groups) {
+        const int64_t ch = ch0 + c;
+        if (FMT == QM_Q4_G32) {
+          wv[u][0] = *reinterpret_cast<const uint4*>(q + (ch * 64 + row) * 16);
+        } else {
+          const uint8_t* base = q + ch * 2048 + row * 16;
+          wv[u][0] = *reinterpret_cast<const uint4*>(base);
+          wv[u][NW - 1] = *reinterpret_cast<const uint4*>(base + 1024);
+        }
+        sv[u] = s[ch * 64 + row];
+      }
+    }
+    if (XLDS && it == 0) {
+      for (int i = threadIdx.x; i < groups * 4; i += WAVES * 64) xs[i] = xg[i];
+      __syncthreads();
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = first + (it * U + u) * stride;
+      if (c < groups) {
+        uint32_t xv[16];
+        if (XLDS) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint4 t = xs[c * 4 + i];
+            xv[4 * i] = t.x; xv[4 * i + 1] = t.y; xv[4 * i + 2] = t.z; xv[4 * i + 3] = t.w;
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint4 t = xg[c * 4 + i];
+            xv[4 * i] = t.x; xv[4 * i + 1] = t.y; xv[4 * i + 2] = t.z; xv[4 * i + 3] = t.w;
+          }
+        }
+        float d;
+        if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][0], xv, m0, m1);
+        else d = dot_q8_half(wv[u][0], xv) + dot_q8_half(wv[u][NW - 1], xv + 8);
+        acc = fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sv[u]))), d, acc);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = SUBR; off < 64; off <<= 1) acc += __shfl_xor(acc, off);
+  if (WAVES == 1) {
+    if (lane < SUBR) {
+      const int64_t n = panel * 64 + row;
+      if (n < n_rows) y[n] = acc;
+    }
+    return;
+  }
+  if (cl == 0) part[wave][r] = acc;
+  __syncthreads();
+  if (wave == 0 && lane < SUBR) {
+    float t = part[0][lane];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) t += part[w][lane];
+    const int64_t n = panel * 64 + row;
+    if (n < n_rows) y[n] = t;
+  }
+}
+
+template <int FMT, int SUBR, bool XLDS>
+hipError_t launch_sub_waves(int waves, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
+                            int64_t n, int64_t groups, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(padded_rows(n) / SUBR));
+  const size_t lds = XLDS ? static_cast<size_t>(groups) * 64 : 0;
+  const int ni = static_cast<int>(n), gi = static_cast<int>(groups);
+  switch (waves) {
+    case 1: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 1, XLDS>), grid, dim3(64), lds, st, q, s, x, y, ni, gi); break;
+    case 2: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 2, XLDS>), grid, dim3(128), lds, st, q, s, x, y, ni, gi); break;
+    case 4: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 4, XLDS>), grid, dim3(256), lds, st, q, s, x, y, ni, gi); break;
+    default: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, q, s, x, y, ni, gi); break;
+  }
+  return hipGetLastError();
+}
+
+template <int FMT, bool XLDS>
+hipError_t launch_sub(const GemvPlan& plan, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
+                      int64_t n, int64_t groups, hipStream_t st) {
+  switch (plan.subr) {
+    case 4: return launch_sub_waves<FMT, 4, XLDS>(plan.waves, q, s, x, y, n, groups, st);
+    case 8: return launch_sub_waves<FMT, 8, XLDS>(plan.waves, q, s, x, y, n, groups, st);
+    case 16: return launch_sub_waves<FMT, 16, XLDS>(plan.waves, q, s, x, y, n, groups, st);
+    default: return launch_sub_waves<FMT, 32, XLDS>(plan.waves, q, s, x, y, n, groups, st);
+  }
+}
+
 template <int FMT>
 hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t n,
                       int64_t k, int cu_count, hipStream_t st) {
   const int64_t panels = padded_rows(n) / kPanel;
   const int64_t groups = k / kGroup;
-  const int waves = gemv_waves_per_block(panels, groups, cu_count);
+  const GemvPlan plan = gemv_plan(n, k, cu_count);
+  if (plan.subr < kPanel) {
+    return plan.xlds ? launch_sub<FMT, true>(plan, q, s, x, y, n, groups, st)
+                     : launch_sub<FMT, false>(plan, q, s, x, y, n, groups, st);
+  }
+  const int waves = plan.waves;
   const int cpw = static_cast<int>((groups + waves - 1) / waves);
   const dim3 grid(static_cast<unsigned>(panels));
   const int ni = static_cast<int>(n), gi = static_cast<int>(groups);
@@ -174,14 +326,44 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
 
 }  // namespace
 
-// Per-chip choice of wavefronts per panel: enough wavefronts in the grid to
-// keep every CU's memory pipeline busy (>= 32 per CU, i.e. 8 per SIMD), never
-// more wavefronts than groups, at most 16 (1024 threads).
-int gemv_waves_per_block(int64_t panels, int64_t groups, int cu_count) {
-  const int64_t want = static_cast<int64_t>(cu_count) * 32;
-  int w = 1;
-  while (w < 16 && panels * w < want && w * 2 <= groups) w *= 2;
-  return w;
+// Per-chip launch plan, from a cold per-shape sweep on MI355X (256 CUs).
+// Matrices with at least one 64-row panel per CU use the panel kernel with 8
+// wavefronts per panel (fewer only if there are fewer groups).  Smaller matrices use the sub-panel
+// kernel with 8 wavefronts per workgroup and the smallest row count (8, 16
+// or 32) that keeps the grid at <= 2 workgroups per CU; activations are
+// staged in LDS for K <= 4096 and read from global memory beyond.
+GemvPlan gemv_plan(int64_t n, int64_t k, int cu_count) {
+  // Tuning sweeps only: QM_GEMV_PLAN="rows,waves,x_in_lds" forces the plan.
+  static const GemvPlan forced = [] {
+    GemvPlan f{0, 0, 1};
+    if (const char* e = std::getenv("QM_GEMV_PLAN")) std::sscanf(e, "%d,%d,%d", &f.subr, &f.waves, &f.xlds);
+    return f;
+  }();
+  if (forced.subr == 4 || forced.subr == 8 || forced.subr == 16 || forced.subr == 32 || forced.subr == 64) {
+    GemvPlan f = forced;
+    if (f.subr < kPanel && k > 16384) f.xlds = 0;
+    if (f.waves < 1) f.waves = 1;
+    if (f.waves > (f.subr == kPanel ? 16 : 8)) f.waves = f.subr == kPanel ? 16 : 8;
+    return f;
+  }
+  const int64_t npad = padded_rows(n);
+  const int64_t panels = npad / kPanel;
+  const int64_t groups = k / kGroup;
+  GemvPlan p;
+  if (panels >= cu_count) {
+    int w = 1;
+    while (w < 8 && w * 2 <= groups) w *= 2;
+    p.subr = kPanel;
+    p.waves = w;
+    p.xlds = 0;
+    return p;
+  }
+  int subr = 8;
+  while (subr < 32 && npad / subr > 2 * cu_count) subr *= 2;
+  p.subr = subr;
+  p.waves = 8;
+  p.xlds = k <= 4096 ? 1 : 0;
+  return p;
 }
 
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,

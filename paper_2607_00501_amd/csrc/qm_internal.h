@@ -68,7 +68,10 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
                         hipStream_t st);
 
 // Per-chip choices (Sec. 3.3: per-chip configuration table).
-int gemv_waves_per_block(int64_t panels, int64_t groups, int cu_count);
+// GEMV launch plan: rows per workgroup (64 = whole panel), wavefronts per
+// workgroup, and whether activations are staged in LDS (sub-panel kernel).
+struct GemvPlan { int subr; int waves; int xlds; };
+GemvPlan gemv_plan(int64_t n, int64_t k, int cu_count);
 const char* gemm_tile_name(int64_t m, int64_t n);
 const char* moe_tile_name(int64_t rows_per_expert);
 

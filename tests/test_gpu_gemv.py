@@ -21,7 +21,8 @@ def _device_weight(w_np, bfmt):
 
 @pytest.mark.parametrize("ofmt,bfmt", FMTS)
 @pytest.mark.parametrize("n,k", [(1, 32), (63, 64), (65, 96), (200, 1024), (1024, 1024),
-                                 (130, 3072), (1000, 2048), (64, 8192)])
+                                 (130, 3072), (1000, 2048), (64, 8192), (70, 20000),
+                                 (4100, 1024), (20000, 64)])
 def test_gemv_parity(ofmt, bfmt, n, k):
     w = inputs.weights_np(inputs.seed_for(0, n, "q"), (n, k))
     x = inputs.activations_np(inputs.seed_for(0, n, "x"), (k,))
