@@ -10,7 +10,7 @@
 // workgroup finds its (expert, row tile) from the counts itself.
 #include <hip/hip_fp16.h>
 
-#include "mfma_tile.h"
+#include "qgemm.h"
 
 namespace qm {
 namespace {
@@ -154,153 +154,6 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   }
 }
 
-// ------------------------------------------------------- tile scheduling
-
-// Wavefront 0 maps the workgroup's linear tile index to (expert, row tile)
-// in expert order, with ceil(count / BM) tiles per expert.  Returns expert
-// -1 when the index lies beyond the last tile.
-__device__ inline void find_tile(const int32_t* counts, int E, int BM, int bx, int* sh_e, int* sh_tile) {
-  if (threadIdx.x == 0) *sh_e = -1;
-  __syncthreads();
-  if ((threadIdx.x >> 6) == 0) {
-    const int lane = threadIdx.x & 63;
-    int running = 0;
-    for (int b0 = 0; b0 < E; b0 += 64) {
-      const int e = b0 + lane;
-      const int t = e < E ? (counts[e] + BM - 1) / BM : 0;
-      int incl = t;
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const int o = __shfl_up(incl, d);
-        if (lane >= d) incl += o;
-      }
-      const int excl = running + incl - t;
-      if (t > 0 && bx >= excl && bx < excl + t) {
-        *sh_e = e;
-        *sh_tile = bx - excl;
-      }
-      running += __shfl(incl, 63);
-    }
-  }
-  __syncthreads();
-}
-
-// ------------------------------------------------- grouped GEMM 1: gate/up
-
-template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(WM * WN * 64) void moe_gateup_kernel(MoeArgs p) {
-  using T = MfmaTile<BM, BN, WM, WN, true>;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[T::kLdsBytes / 2];
-  __shared__ int sh_e, sh_tile;
-  find_tile(p.counts, p.n_experts, BM, blockIdx.x, &sh_e, &sh_tile);
-  const int e = sh_e;
-  if (e < 0) return;
-  const int64_t row0 = p.offsets[e] + static_cast<int64_t>(sh_tile) * BM;
-  const int rows = static_cast<int>(min<int64_t>(BM, p.offsets[e + 1] - row0));
-  constexpr int BNh = T::kBNh;
-  const int64_t n0 = static_cast<int64_t>(blockIdx.y) * BNh;
-  const int64_t G = p.hidden / kGroup;
-  const int64_t ipad = padded_rows(p.inter);
-  const uint8_t* gq = p.gq + e * ipad * (p.hidden / 2);
-  const uint8_t* uq = p.uq + e * ipad * (p.hidden / 2);
-  const uint16_t* gs = p.gs + e * ipad * G;
-  const uint16_t* us = p.us + e * ipad * G;
-
-  const uint16_t* a_rows[T::kALoads];
-#pragma unroll
-  for (int i = 0; i < T::kALoads; ++i) {
-    const int lr = T::a_row(i);
-    if (lr < rows) {
-      const int64_t tok = p.sorted_assign[row0 + lr] / p.top_k;
-      a_rows[i] = p.x + tok * p.hidden;
-    } else {
-      a_rows[i] = nullptr;
-    }
-  }
-  const uint8_t* b_q[T::kBLoads];
-  const uint16_t* b_s[T::kBLoads];
-#pragma unroll
-  for (int i = 0; i < T::kBLoads; ++i) {
-    const int br = T::b_row(i);
-    const bool up = br >= BNh;
-    const int64_t n = n0 + (up ? br - BNh : br);
-    b_q[i] = n < ipad ? q4_row_chunk0(up ? uq : gq, n, G) : nullptr;
-    b_s[i] = n < ipad ? q4_row_scale0(up ? us : gs, n, G) : nullptr;
-  }
-  float16v acc[T::kTM][T::kTN];
-  T::run(a_rows, b_q, b_s, static_cast<int>(p.hidden), lds, acc);
-
-  constexpr int half_tiles = T::kTN / 2;
-#pragma unroll
-  for (int a = 0; a < T::kTM; ++a)
-#pragma unroll
-    for (int b = 0; b < half_tiles; ++b) {
-      const int64_t n = n0 + T::out_col(b);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int lr = T::out_row(a, r);
-        if (lr < rows && n < p.inter) {
-          const float g = acc[a][b][r];
-          const float u = acc[a][b + half_tiles][r];
-          const float h = g / (1.0f + expf(-g)) * u;
-          p.h[(row0 + lr) * p.inter + n] = __half_as_ushort(__float2half_rn(h));
-        }
-      }
-    }
-}
-
-// --------------------------------------------------- grouped GEMM 2: down
-
-template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(WM * WN * 64) void moe_down_kernel(MoeArgs p) {
-  using T = MfmaTile<BM, BN, WM, WN, false>;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[T::kLdsBytes / 2];
-  __shared__ int sh_e, sh_tile;
-  find_tile(p.counts, p.n_experts, BM, blockIdx.x, &sh_e, &sh_tile);
-  const int e = sh_e;
-  if (e < 0) return;
-  const int64_t row0 = p.offsets[e] + static_cast<int64_t>(sh_tile) * BM;
-  const int rows = static_cast<int>(min<int64_t>(BM, p.offsets[e + 1] - row0));
-  const int64_t n0 = static_cast<int64_t>(blockIdx.y) * BN;
-  const int64_t G = p.inter / kGroup;
-  const int64_t hpad = padded_rows(p.hidden);
-  const uint8_t* dq = p.dq + e * hpad * (p.inter / 2);
-  const uint16_t* ds = p.ds + e * hpad * G;
-
-  const uint16_t* a_rows[T::kALoads];
-#pragma unroll
-  for (int i = 0; i < T::kALoads; ++i) {
-    const int lr = T::a_row(i);
-    a_rows[i] = lr < rows ? p.h + (row0 + lr) * p.inter : nullptr;
-  }
-  const uint8_t* b_q[T::kBLoads];
-  const uint16_t* b_s[T::kBLoads];
-#pragma unroll
-  for (int i = 0; i < T::kBLoads; ++i) {
-    const int64_t n = n0 + T::b_row(i);
-    b_q[i] = n < hpad ? q4_row_chunk0(dq, n, G) : nullptr;
-    b_s[i] = n < hpad ? q4_row_scale0(ds, n, G) : nullptr;
-  }
-  float16v acc[T::kTM][T::kTN];
-  T::run(a_rows, b_q, b_s, static_cast<int>(p.inter), lds, acc);
-
-#pragma unroll
-  for (int a = 0; a < T::kTM; ++a) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int lr = T::out_row(a, r);
-      if (lr >= rows) continue;
-      const int64_t asg = p.sorted_assign[row0 + lr];
-      const float gw = p.topk_w[asg];
-#pragma unroll
-      for (int b = 0; b < T::kTN; ++b) {
-        const int64_t n = n0 + T::out_col(b);
-        if (n < p.hidden) p.yp[asg * p.hidden + n] = gw * acc[a][b][r];
-      }
-    }
-  }
-}
-
 // ---------------------------------------------------------------- combine
 
 // y[t][n] = sum over slots j (in order) of the gate-weighted expert outputs.
@@ -318,16 +171,25 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   reinterpret_cast<float4*>(y + t * hidden)[c] = s;
 }
 
-template <int BM, int BN1, int WM1, int WN1, int BN2, int WM2, int WN2>
+template <int BM, int WN>
 hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
   const int64_t A = a.m * a.top_k;
+  // Upper bound on the number of (expert, row tile) pairs: sum of
+  // ceil(count_e / BM) <= A / BM + E.  Workgroups past the last tile exit.
   const unsigned tiles = static_cast<unsigned>((A + BM - 1) / BM + a.n_experts);
-  const unsigned ny1 = static_cast<unsigned>((a.inter + BN1 / 2 - 1) / (BN1 / 2));
-  hipLaunchKernelGGL((moe_gateup_kernel<BM, BN1, WM1, WN1>), dim3(tiles, ny1), dim3(WM1 * WN1 * 64), 0, st, a);
+  QgemmArgs g{};
+  g.counts = a.counts; g.offsets = a.offsets; g.sorted_assign = a.sorted_assign; g.topk_w = a.topk_w;
+  g.n_experts = a.n_experts; g.top_k = a.top_k; g.M = A;
+  // gate/up + SwiGLU: A = x rows gathered per assignment, N = inter, K = hidden
+  g.q = a.gq; g.s = a.gs; g.q2 = a.uq; g.s2 = a.us; g.a = a.x; g.h = a.h; g.N = a.inter; g.K = a.hidden;
+  const unsigned ny1 = static_cast<unsigned>((a.inter + 64 * WN - 1) / (64 * WN));
+  hipLaunchKernelGGL((qgemm_kernel<BM, WN, 1, QgMode::kMoeGateUp>), dim3(tiles, ny1), dim3(WN * 64), 0, st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const unsigned ny2 = static_cast<unsigned>((a.hidden + BN2 - 1) / BN2);
-  hipLaunchKernelGGL((moe_down_kernel<BM, BN2, WM2, WN2>), dim3(tiles, ny2), dim3(WM2 * WN2 * 64), 0, st, a);
+  // down, scaled by the gate weight and scattered to the assignment slot
+  g.q = a.dq; g.s = a.ds; g.q2 = nullptr; g.s2 = nullptr; g.a = a.h; g.yp = a.yp; g.N = a.hidden; g.K = a.inter;
+  const unsigned ny2 = static_cast<unsigned>((a.hidden + 64 * WN - 1) / (64 * WN));
+  hipLaunchKernelGGL((qgemm_kernel<BM, WN, 1, QgMode::kMoeDown>), dim3(tiles, ny2), dim3(WN * 64), 0, st, g);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t n4 = a.m * (a.hidden / 4);
@@ -346,9 +208,7 @@ size_t moe_workspace_bytes(int64_t m, int32_t top_k, int64_t hidden, int64_t int
 }
 
 const char* moe_tile_name(int64_t rows_per_expert) {
-  if (rows_per_expert <= 24) return "BM32(gate/up 32x(64+64), down 32x128)";
-  if (rows_per_expert <= 80) return "BM64(gate/up 64x(64+64), down 64x128)";
-  return "BM128(gate/up 128x(64+64), down 128x128)";
+  return rows_per_expert <= 24 ? "32-row bucket tiles x 4 panels" : "64-row bucket tiles x 4 panels";
 }
 
 hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, int32_t* ids, float* w,
@@ -366,10 +226,11 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
 
 hipError_t launch_moe(const MoeArgs& a, int cu_count, hipStream_t st) {
   (void)cu_count;
+  // Per-chip tile choice by rows per expert: 32-row tiles when buckets are
+  // small (decode-like prefill chunks), 64-row tiles otherwise.
   const int64_t rpe = a.m * a.top_k / a.n_experts;
-  if (rpe <= 24) return launch_moe_tiles<32, 128, 1, 2, 128, 1, 2>(a, st);
-  if (rpe <= 80) return launch_moe_tiles<64, 128, 2, 2, 128, 2, 2>(a, st);
-  return launch_moe_tiles<128, 128, 2, 2, 128, 2, 2>(a, st);
+  if (rpe <= 24) return launch_moe_tiles<32, 4>(a, st);
+  return launch_moe_tiles<64, 4>(a, st);
 }
 
 }  // namespace qm

@@ -1,0 +1,360 @@
+// Q4 MFMA GEMM core shared by the prefill GEMM and the MoE grouped GEMMs.
+//
+// Y = A * W'^T with W' the group-32 Q4 weights dequantised inside the
+// kernel (BaseRT Sec. 3.3: dequantisation in the matmul inner loop; Sec.
+// 3.4: tiled GEMM for prefill).  Mapping on gfx950 (64-lane wavefronts,
+// v_mfma_f32_32x32x16_f16):
+//  * a workgroup has WN x WK wavefronts; wavefront (wn, wk) owns the BM x 64
+//    output block whose 64 columns are one device-layout panel, over the
+//    wk-th slice of the K steps (WK > 1: split-K inside the workgroup, the
+//    partial sums meet in LDS in a fixed order).  One 64-deep K step of its
+//    weights is two 1 KiB contiguous chunk rows: one dwordx4 per lane per
+//    chunk, fully coalesced;
+//  * the weights never pass through LDS: each wavefront dequantises its own
+//    B fragments in registers.  One v_permlane32_swap per dword pair moves
+//    the codes of panel rows 32..63 / 0..31 into the MFMA B-operand lane
+//    layout (lane l holds 8 consecutive k of column l%32); v_and_or_b32 +
+//    v_pk_add_f16 + v_pk_mul_f16 then give fp16_RNE(s*q) exactly;
+//  * the activation tile of each K slice (BM x 64 fp16) is double-buffered
+//    in LDS (one barrier per K step) and shared by the WN wavefronts of the
+//    slice; A fragments of the next substep are read while the current
+//    MFMAs run;
+//  * global loads run two K steps ahead of the MFMAs.  Out-of-range rows,
+//    columns and K steps read clamped (valid) addresses with their scales
+//    forced to zero, so the loads carry no branches;
+//  * modes: kDense (rows m0.., plain row-major A and Y); kMoeGateUp (rows of
+//    one expert's bucket, A rows gathered through the assignment
+//    permutation, each wavefront streams the gate and the up panel of the
+//    same columns and the epilogue writes fp16 silu(gate) * up); kMoeDown
+//    (A = the fp16 h rows of the bucket, the epilogue scales by the
+//    assignment's gate weight and scatters the row to its assignment slot).
+//    MoE workgroups find their (expert, row tile) from the per-expert counts
+//    on the device, so no host synchronisation is needed.
+#pragma once
+
+#include <type_traits>
+
+#include "qm_internal.h"
+
+namespace qm {
+
+enum class QgMode { kDense = 0, kMoeGateUp = 1, kMoeDown = 2 };
+
+struct QgemmArgs {
+  const uint8_t* q;  const uint16_t* s;    // dense weights; MoE gate or down experts
+  const uint8_t* q2; const uint16_t* s2;   // MoE up experts (kMoeGateUp)
+  const uint16_t* a;                       // A rows: X (dense, gate/up) or h (down)
+  float* y;                                // dense output [M][N]
+  int64_t M, N, K;                         // MoE: M = number of assignments
+  const int32_t* counts;
+  const int32_t* offsets;
+  const int32_t* sorted_assign;
+  const float* topk_w;
+  uint16_t* h;                             // kMoeGateUp output [M][N] fp16 (bucket order)
+  float* yp;                               // kMoeDown output [M][N] (assignment order)
+  int32_t n_experts, top_k;
+};
+
+namespace qg {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBK = 64;                 // K per step (two quantisation groups)
+constexpr int kRow = kBK + 8;           // LDS row stride in halves (16-byte pad)
+
+__device__ inline uint32_t and_or_v(uint32_t a, uint32_t mask_v, uint32_t or_s) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(mask_v), "s"(or_s));
+  return r;
+}
+
+// 8 offset-binary nibbles of one device-layout dword (k order 0,2,4,6 |
+// 1,3,5,7) -> 8 fp16 fp16_RNE(s*q) in natural k order.
+__device__ inline half8v dequant_dword(uint32_t d, half2v s2) {
+  const half2v bias = {(_Float16)1032.0f, (_Float16)1032.0f};
+  const uint32_t m0 = 0x000F000Fu, magic = 0x64006400u;
+  half8v out;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const half2v q = __builtin_bit_cast(half2v, and_or_v(d >> (4 * i), m0, magic)) - bias;
+    const half2v v = q * s2;
+    out[2 * i] = v[0];
+    out[2 * i + 1] = v[1];
+  }
+  return out;
+}
+
+// Wavefront 0 maps the workgroup's linear tile index to (expert, row tile)
+// in expert order, with ceil(count / BM) tiles per expert.  Expert -1 when
+// the index lies beyond the last tile.
+__device__ inline void find_tile(const int32_t* counts, int E, int BM, int bx, int* sh_e, int* sh_tile) {
+  if (threadIdx.x == 0) *sh_e = -1;
+  __syncthreads();
+  if ((threadIdx.x >> 6) == 0) {
+    const int lane = threadIdx.x & 63;
+    int running = 0;
+    for (int b0 = 0; b0 < E; b0 += 64) {
+      const int e = b0 + lane;
+      const int t = e < E ? (counts[e] + BM - 1) / BM : 0;
+      int incl = t;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int o = __shfl_up(incl, d);
+        if (lane >= d) incl += o;
+      }
+      const int excl = running + incl - t;
+      if (t > 0 && bx >= excl && bx < excl + t) {
+        *sh_e = e;
+        *sh_tile = bx - excl;
+      }
+      running += __shfl(incl, 63);
+    }
+  }
+  __syncthreads();
+}
+
+template <int BM, int WN, int WK, QgMode MODE>
+struct Cfg {
+  static constexpr bool kDual = MODE == QgMode::kMoeGateUp;
+  static constexpr int kNB = kDual ? 2 : 1;                      // weight matrices per wavefront
+  static constexpr int kThreads = WN * WK * 64;
+  static constexpr int kSliceThreads = WN * 64;
+  static constexpr int kTM = BM / 32;
+  static constexpr int kALoads = BM * (kBK / 8) / kSliceThreads;
+  static constexpr int kStage = BM * kRow;                        // halves per A stage
+  static_assert(kALoads >= 1 && BM * (kBK / 8) % kSliceThreads == 0, "A tile split");
+  static_assert(WK == 1 || MODE == QgMode::kDense, "split-K only for the dense GEMM");
+  static_assert(WK == 1 || (WK - 1) * WN * BM * 64 * 4 <= 2 * WK * kStage * 2, "reduction fits in LDS");
+};
+
+template <int BM, int WN, int WK, QgMode MODE>
+__device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
+  using C = Cfg<BM, WN, WK, MODE>;
+  constexpr int NB = C::kNB;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * WK * C::kStage];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wk = wave / WN, wn = wave % WN;
+  const int stid = tid - wk * C::kSliceThreads;          // thread index inside the K slice
+  const int64_t K = p.K, N = p.N;
+  const int G = static_cast<int>(K / kGroup);
+  const int KT = (G + 1) / 2;
+  const int KTs = (KT + WK - 1) / WK;                      // K steps per slice
+  const int kt0 = wk * KTs;
+  const int64_t npad = padded_rows(N);
+
+  // Rows of this workgroup.
+  int64_t row0 = 0;
+  int rows = 0;
+  int expert = 0;
+  int64_t col_block;
+  if constexpr (MODE == QgMode::kDense) {
+    row0 = static_cast<int64_t>(blockIdx.y) * BM;
+    rows = static_cast<int>(min<int64_t>(BM, p.M - row0));
+    col_block = blockIdx.x;
+  } else {
+    __shared__ int sh_e, sh_tile;
+    find_tile(p.counts, p.n_experts, BM, blockIdx.x, &sh_e, &sh_tile);
+    expert = sh_e;
+    if (expert < 0) return;
+    row0 = p.offsets[expert] + static_cast<int64_t>(sh_tile) * BM;
+    rows = static_cast<int>(min<int64_t>(BM, p.offsets[expert + 1] - row0));
+    col_block = blockIdx.y;
+  }
+  const int64_t n_wave = col_block * (64 * WN) + 64 * wn;
+  const bool cols_ok = n_wave < npad;
+
+  // A: this thread's rows/cols of the slice's BM x 64 tile (rows clamped).
+  const uint16_t* a_src[C::kALoads];
+  int a_lds[C::kALoads], a_col[C::kALoads];
+#pragma unroll
+  for (int i = 0; i < C::kALoads; ++i) {
+    const int idx = stid + i * C::kSliceThreads;
+    const int row = idx >> 3;
+    a_col[i] = (idx & 7) * 8;
+    a_lds[i] = row * kRow + a_col[i];
+    const int64_t r = row0 + min(row, rows - 1);
+    int64_t src_row = r;
+    if constexpr (MODE == QgMode::kMoeGateUp) src_row = p.sorted_assign[r] / p.top_k;
+    a_src[i] = p.a + src_row * K;
+  }
+  // B: lane l streams row l of the wavefront's panel(s) (clamped to a real panel).
+  const int64_t panel = (cols_ok ? n_wave : npad - kPanel) / kPanel;
+  const int64_t mat_q = npad * (K / 2), mat_s = npad * G;   // bytes / scales of one matrix
+  const uint8_t* b_q[NB];
+  const uint16_t* b_s[NB];
+  b_q[0] = p.q + expert * mat_q + (panel * G * kPanel + lane) * 16;
+  b_s[0] = p.s + expert * mat_s + panel * G * kPanel + lane;
+  if constexpr (NB == 2) {
+    b_q[1] = p.q2 + expert * mat_q + (panel * G * kPanel + lane) * 16;
+    b_s[1] = p.s2 + expert * mat_s + panel * G * kPanel + lane;
+  }
+
+  // Two register sets of raw step operands, always indexed by constants.
+  u32x4 ra[2][C::kALoads];
+  u32x4 rb[2][NB][2];
+  uint32_t rs[2][NB][2];
+  auto load = [&](auto slot, int step) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot)::value;
+    const int kt = kt0 + step;
+#pragma unroll
+    for (int i = 0; i < C::kALoads; ++i) {
+      const int k = min(kt * kBK + a_col[i], static_cast<int>(K) - 8);
+      ra[sl][i] = *reinterpret_cast<const u32x4*>(a_src[i] + k);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int g = 2 * kt + c;
+        const int gc = min(g, G - 1);
+        rb[sl][j][c] = *reinterpret_cast<const u32x4*>(b_q[j] + static_cast<int64_t>(gc) * kPanel * 16);
+        const uint32_t sv = b_s[j][static_cast<int64_t>(gc) * kPanel];
+        rs[sl][j][c] = (cols_ok && g < G && step < KTs && kt < KT) ? sv : 0u;
+      }
+  };
+  auto store_a = [&](auto slot, int buf) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot)::value;
+    uint16_t* dst = lds + (buf * WK + wk) * C::kStage;
+#pragma unroll
+    for (int i = 0; i < C::kALoads; ++i) *reinterpret_cast<u32x4*>(dst + a_lds[i]) = ra[sl][i];
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+
+  float16v acc[C::kTM][2 * NB];
+#pragma unroll
+  for (int a = 0; a < C::kTM; ++a)
+#pragma unroll
+    for (int b = 0; b < 2 * NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+
+  // One K step t: register slot sl holds step t's raw operands (its A tile is
+  // already in LDS buffer t&1), slot 1-sl step t+1's.  The B codes of slot sl
+  // move to registers in MFMA layout, then slot sl is refilled with step t+2;
+  // step t+1's A tile goes to the other LDS buffer after the MFMAs.
+  auto step = [&](auto slot, int t) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot)::value;
+    using Next = std::integral_constant<int, 1 - sl>;
+    const int buf = t & 1;
+    uint32_t bd[NB][2][4];                                 // [matrix][column half][substep]
+    half2v sc[NB][2][2];                                   // [matrix][chunk][column half]
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(rs[sl][j][c], rs[sl][j][c], false, false);
+        const _Float16 lo = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[0]));
+        const _Float16 hi = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[1]));
+        sc[j][c][0] = half2v{lo, lo};
+        sc[j][c][1] = half2v{hi, hi};
+        const uint32_t d[4] = {rb[sl][j][c][0], rb[sl][j][c][1], rb[sl][j][c][2], rb[sl][j][c][3]};
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const auto pr = __builtin_amdgcn_permlane32_swap(d[2 * i], d[2 * i + 1], false, false);
+          bd[j][0][2 * c + i] = pr[0];                     // panel rows 0..31
+          bd[j][1][2 * c + i] = pr[1];                     // panel rows 32..63
+        }
+      }
+    load(slot, t + 2);                                     // two steps ahead
+    __builtin_amdgcn_sched_barrier(0);                     // keep the loads at the top
+    const uint16_t* At = lds + (buf * WK + wk) * C::kStage + (lane & 31) * kRow + 8 * (lane >> 5);
+    half8v af[2][C::kTM];
+#pragma unroll
+    for (int a = 0; a < C::kTM; ++a) af[0][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      if (ks + 1 < kBK / 16) {
+#pragma unroll
+        for (int a = 0; a < C::kTM; ++a)
+          af[(ks + 1) & 1][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow + (ks + 1) * 16);
+      }
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const half8v b0 = dequant_dword(bd[j][0][ks], sc[j][ks >> 1][0]);
+        const half8v b1 = dequant_dword(bd[j][1][ks], sc[j][ks >> 1][1]);
+#pragma unroll
+        for (int a = 0; a < C::kTM; ++a) {
+          acc[a][2 * j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[ks & 1][a], b0, acc[a][2 * j], 0, 0, 0);
+          acc[a][2 * j + 1] =
+              __builtin_amdgcn_mfma_f32_32x32x16_f16(af[ks & 1][a], b1, acc[a][2 * j + 1], 0, 0, 0);
+        }
+      }
+    }
+    if (t + 1 < KTs) store_a(Next{}, buf ^ 1);
+    __syncthreads();
+  };
+
+  load(S0{}, 0);
+  load(S1{}, 1);
+  store_a(S0{}, 0);
+  __syncthreads();
+  int t = 0;
+  for (; t + 2 <= KTs; t += 2) {
+    step(S0{}, t);
+    step(S1{}, t + 1);
+  }
+  if (t < KTs) step(S0{}, t);
+
+  if constexpr (WK > 1) {
+    // Partial sums of slices 1..WK-1 go through LDS; slice 0 adds them in order.
+    float* red = reinterpret_cast<float*>(lds);
+    constexpr int per_wave = C::kTM * 2 * 16 * 64;
+    if (wk > 0) {
+      float* dst = red + ((wk - 1) * WN + wn) * per_wave;
+#pragma unroll
+      for (int a = 0; a < C::kTM; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[((a * 2 + b) * 16 + r) * 64 + lane] = acc[a][b][r];
+    }
+    __syncthreads();
+    if (wk > 0) return;
+    for (int j = 1; j < WK; ++j) {
+      const float* src = red + ((j - 1) * WN + wn) * per_wave;
+#pragma unroll
+      for (int a = 0; a < C::kTM; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[a][b][r] += src[((a * 2 + b) * 16 + r) * 64 + lane];
+    }
+  }
+
+  // Epilogue: lane l, register r of a 32x32 tile holds
+  // row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+#pragma unroll
+  for (int a = 0; a < C::kTM; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int64_t col = n_wave + 32 * b + (lane & 31);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int lr = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (lr >= rows || col >= N) continue;
+        if constexpr (MODE == QgMode::kDense) {
+          p.y[(row0 + lr) * N + col] = acc[a][b][r];
+        } else if constexpr (MODE == QgMode::kMoeGateUp) {
+          const float g = acc[a][b][r];
+          const float u = acc[a][2 + b][r];
+          const float hv = g / (1.0f + expf(-g)) * u;
+          p.h[(row0 + lr) * N + col] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hv));
+        } else {
+          const int64_t asg = p.sorted_assign[row0 + lr];
+          p.yp[asg * N + col] = p.topk_w[asg] * acc[a][b][r];
+        }
+      }
+    }
+}
+
+}  // namespace qg
+
+template <int BM, int WN, int WK, QgMode MODE>
+__global__ __launch_bounds__(WN * WK * 64, 2) void qgemm_kernel(QgemmArgs p) {
+  qg::qgemm_body<BM, WN, WK, MODE>(p);
+}
+
+}  // namespace qm
