@@ -20,6 +20,41 @@ namespace {
 constexpr int kRouteThreads = 256;   // one wavefront per token
 constexpr int kMaxPerLane = 16;      // n_experts <= 1024
 
+// (value, index) order used by the router: larger value first, lower index
+// on equal values.
+__device__ inline void take_better(float& bv, int& be, float ov, int oe) {
+  const bool better = ov > bv || (ov == bv && oe < be);
+  bv = better ? ov : bv;
+  be = better ? oe : be;
+}
+
+template <int CTRL>
+__device__ inline void dpp_step(float& bv, int& be) {
+  const float ov = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, bv), CTRL, 0xF, 0xF, false));
+  const int oe = __builtin_amdgcn_mov_dpp(be, CTRL, 0xF, 0xF, false);
+  take_better(bv, be, ov, oe);
+}
+
+// Every lane ends with the wavefront's best (value, index): DPP exchanges
+// within each row of 16 lanes, then the four row winners are read out as
+// wave-uniform values and compared in a fixed order.
+__device__ inline void wave_argmax(float& bv, int& be) {
+  dpp_step<0xB1>(bv, be);    // quad_perm [1,0,3,2]
+  dpp_step<0x4E>(bv, be);    // quad_perm [2,3,0,1]
+  dpp_step<0x124>(bv, be);   // row_ror:4
+  dpp_step<0x128>(bv, be);   // row_ror:8
+  float v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bv), 0));
+  int e = __builtin_amdgcn_readlane(be, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) {
+    const float ov = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bv), 16 * r));
+    const int oe = __builtin_amdgcn_readlane(be, 16 * r);
+    take_better(v, e, ov, oe);
+  }
+  bv = v;
+  be = e;
+}
+
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(const float* __restrict__ logits,
                                                               int64_t m, int E, int K,
                                                               int32_t* __restrict__ ids,
@@ -36,8 +71,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(const float* __res
     v[i] = (i < per_lane && e < E) ? row[e] : -INFINITY;
   }
   uint32_t taken = 0;   // bit i: item i of this lane already selected
-  float top_v[16];
-  int top_e[16];
+  float my_v = -INFINITY;   // lane j < K ends up holding the j-th selected logit
+  int my_e = 0;
   for (int j = 0; j < K; ++j) {
     // Lane-local best: highest value, lowest expert index on ties.
     float bv = -INFINITY;
@@ -50,26 +85,20 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(const float* __res
       }
     }
     // Wavefront argmax with the same order.
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      const float ov = __shfl_xor(bv, off);
-      const int oe = __shfl_xor(be, off);
-      if (ov > bv || (ov == bv && oe < be)) { bv = ov; be = oe; }
-    }
-    top_v[j] = bv;
-    top_e[j] = be;
+    wave_argmax(bv, be);
+    if (lane == j) { my_v = bv; my_e = be; }
     if ((be & 63) == lane) taken |= 1u << (be >> 6);
   }
-  // Softmax over the selected logits, relative to the largest.
-  float denom = 0.0f;
-  for (int j = 0; j < K; ++j) denom += expf(top_v[j] - top_v[0]);
+  // Softmax over the selected logits, relative to the largest (slot 0);
+  // the denominator is a fixed-order butterfly sum over the lanes.
+  const float vmax = __shfl(my_v, 0);
+  const float ex = lane < K ? expf(my_v - vmax) : 0.0f;
+  float denom = ex;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) denom += __shfl_xor(denom, off);
   if (lane < K) {
-    float val = 0.0f;
-    int ex = 0;
-    for (int j = 0; j < K; ++j)
-      if (j == lane) { val = top_v[j]; ex = top_e[j]; }
-    ids[t * K + lane] = ex;
-    gates[t * K + lane] = expf(val - top_v[0]) / denom;
+    ids[t * K + lane] = my_e;
+    gates[t * K + lane] = ex / denom;
   }
 }
 
@@ -77,80 +106,105 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(const float* __res
 
 constexpr int kBucketThreads = 1024;
 constexpr int kBucketWaves = kBucketThreads / 64;
+constexpr int kBucketUnroll = 8;
 
-// One workgroup: histogram, exclusive scan, then a stable scatter that walks
-// the assignments in order, 1024 at a time.  Inside a wavefront the lanes
-// holding the same expert are found with ten ballots (one per bit of the
-// expert id); their rank is the population count of the lower matching lanes,
-// and lower wavefronts' counts for that expert come from LDS.
+// Lanes of the wavefront that hold the same expert id (ten ballots, one per
+// bit of the id), restricted to the valid lanes.
+__device__ inline uint64_t match_expert(int e, bool valid) {
+  uint64_t mask = __ballot(valid);
+#pragma unroll
+  for (int bit = 0; bit < 10; ++bit) {
+    const bool set = (e >> bit) & 1;
+    const uint64_t b = __ballot(valid && set);
+    mask &= set ? b : ~b;
+  }
+  return mask;
+}
+
+// One workgroup of 16 wavefronts; wavefront w owns the contiguous range
+// [w*R, (w+1)*R) of assignments.  Pass 1 counts each wavefront's
+// assignments per expert (64 at a time: the leader of each group of equal
+// experts adds the group size); then one pass over the experts turns the
+// per-wavefront counts into exclusive bases (expert offset + earlier
+// wavefronts' counts) and writes counts and offsets; pass 2 walks the range
+// again and places each assignment at base + rank among equal experts of
+// its group of 64, the leader advancing the base.  The result is the stable
+// counting sort by (expert, assignment id).  Two barriers in total.
 __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* __restrict__ ids,
                                                                 int64_t A, int E,
                                                                 int32_t* __restrict__ counts,
                                                                 int32_t* __restrict__ offsets,
                                                                 int32_t* __restrict__ sorted_assign) {
-  __shared__ int cnt[1024];
-  __shared__ int off[1024];
-  __shared__ int running[1024];
+  __shared__ int base[kBucketWaves][1024];   // per-wavefront counts, then bases
   __shared__ int wsum[kBucketWaves];
-  __shared__ uint8_t wave_cnt[kBucketWaves][1024];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  cnt[tid] = 0;
-  running[tid] = 0;
-  for (int w = 0; w < kBucketWaves; ++w) wave_cnt[w][tid] = 0;
+  for (int w = 0; w < kBucketWaves; ++w) base[w][tid] = 0;
   __syncthreads();
-  for (int64_t a = tid; a < A; a += kBucketThreads) atomicAdd(&cnt[ids[a]], 1);
-  __syncthreads();
-  // Exclusive scan of cnt[0..1023] (entries >= E are zero).
-  {
-    const int c = cnt[tid];
-    int incl = c;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const int o = __shfl_up(incl, d);
-      if (lane >= d) incl += o;
-    }
-    if (lane == 63) wsum[wave] = incl;
-    __syncthreads();
-    int base = 0;
-    for (int w = 0; w < wave; ++w) base += wsum[w];
-    off[tid] = base + incl - c;
-    __syncthreads();
-    if (tid < E) {
-      counts[tid] = c;
-      offsets[tid] = off[tid];
-    }
-    if (tid == 0) offsets[E] = static_cast<int32_t>(A);
-  }
+  const int64_t R = ((A + kBucketWaves - 1) / kBucketWaves + 63) / 64 * 64;
+  const int64_t lo = min<int64_t>(A, wave * R), hi = min<int64_t>(A, lo + R);
   const uint64_t lower = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int64_t base = 0; base < A; base += kBucketThreads) {
-    const int64_t a = base + tid;
-    const bool valid = a < A;
-    const int e = valid ? ids[a] : 0;
-    uint64_t mask = __ballot(valid);
+  // 8 groups of 64 per round: all eight id loads are issued before use.
+  for (int64_t b0 = lo; b0 < hi; b0 += 64 * kBucketUnroll) {
+    int ev[kBucketUnroll];
 #pragma unroll
-    for (int bit = 0; bit < 10; ++bit) {
-      const bool set = (e >> bit) & 1;
-      const uint64_t b = __ballot(valid && set);
-      mask &= set ? b : ~b;
+    for (int u = 0; u < kBucketUnroll; ++u) {
+      const int64_t a = b0 + u * 64 + lane;
+      ev[u] = a < hi ? ids[a] : 0;
     }
-    const int rank = __popcll(mask & lower);
-    const int wcount = __popcll(mask);
-    const bool leader = valid && rank == 0;
-    if (leader) wave_cnt[wave][e] = static_cast<uint8_t>(wcount);
-    __syncthreads();
-    if (valid) {
-      int pre = 0;
-      for (int w = 0; w < wave; ++w) pre += wave_cnt[w][e];
-      sorted_assign[off[e] + running[e] + pre + rank] = static_cast<int32_t>(a);
+#pragma unroll
+    for (int u = 0; u < kBucketUnroll; ++u) {
+      const bool valid = b0 + u * 64 + lane < hi;
+      const uint64_t mask = match_expert(ev[u], valid);
+      if (valid && __popcll(mask & lower) == 0) base[wave][ev[u]] += __popcll(mask);
     }
-    __syncthreads();
-    if (leader) {
-      wave_cnt[wave][e] = 0;
-      atomicAdd(&running[e], wcount);
+  }
+  __syncthreads();
+  // Thread e: total count, per-wavefront exclusive prefix; then the
+  // exclusive scan of the totals over experts.
+  const int e = tid;
+  int total = 0;
+  for (int w = 0; w < kBucketWaves; ++w) {
+    const int c = base[w][e];
+    base[w][e] = total;
+    total += c;
+  }
+  int incl = total;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int o = __shfl_up(incl, d);
+    if (lane >= d) incl += o;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int off = incl - total;
+  for (int w = 0; w < wave; ++w) off += wsum[w];
+  for (int w = 0; w < kBucketWaves; ++w) base[w][e] += off;
+  if (e < E) {
+    counts[e] = total;
+    offsets[e] = off;
+  }
+  if (e == 0) offsets[E] = static_cast<int32_t>(A);
+  __syncthreads();
+  for (int64_t b0 = lo; b0 < hi; b0 += 64 * kBucketUnroll) {
+    int ev[kBucketUnroll];
+#pragma unroll
+    for (int u = 0; u < kBucketUnroll; ++u) {
+      const int64_t a = b0 + u * 64 + lane;
+      ev[u] = a < hi ? ids[a] : 0;
     }
-    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kBucketUnroll; ++u) {
+      const int64_t a = b0 + u * 64 + lane;
+      const bool valid = a < hi;
+      const uint64_t mask = match_expert(ev[u], valid);
+      const int rank = __popcll(mask & lower);
+      if (valid) sorted_assign[base[wave][ev[u]] + rank] = static_cast<int32_t>(a);
+      // every lane read its base before the leader advances it (same
+      // wavefront, program order); the update is visible to the next group
+      if (valid && rank == 0) base[wave][ev[u]] += __popcll(mask);
+    }
   }
 }
 

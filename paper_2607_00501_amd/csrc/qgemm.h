@@ -164,6 +164,17 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   }
   const int64_t n_wave = col_block * (64 * WN) + 64 * wn;
   const bool cols_ok = n_wave < npad;
+  // kMoeDown: assignment id and gate weight of each row of the tile, staged
+  // once in LDS for the epilogue (visible after the first barrier below).
+  __shared__ int64_t row_asg[MODE == QgMode::kMoeDown ? BM : 1];
+  __shared__ float row_w[MODE == QgMode::kMoeDown ? BM : 1];
+  if constexpr (MODE == QgMode::kMoeDown) {
+    for (int r = tid; r < BM; r += C::kThreads) {
+      const int64_t asg = p.sorted_assign[row0 + min(r, rows - 1)];
+      row_asg[r] = asg;
+      row_w[r] = p.topk_w[asg];
+    }
+  }
 
   // A: this thread's rows/cols of the slice's BM x 64 tile (rows clamped).
   const uint16_t* a_src[C::kALoads];
@@ -343,8 +354,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
           const float hv = g / (1.0f + expf(-g)) * u;
           p.h[(row0 + lr) * N + col] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hv));
         } else {
-          const int64_t asg = p.sorted_assign[row0 + lr];
-          p.yp[asg * N + col] = p.topk_w[asg] * acc[a][b][r];
+          p.yp[row_asg[lr] * N + col] = row_w[lr] * acc[a][b][r];
         }
       }
     }
