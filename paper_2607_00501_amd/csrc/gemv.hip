@@ -197,8 +197,12 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(const uint8_t* __r
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = lane % SUBR, cl = lane / SUBR;
-  const int64_t panel = blockIdx.x / CL;
-  const int row = (blockIdx.x % CL) * SUBR + r;       // row inside the panel
+  // The CL workgroups of one panel share the 128-byte lines of its scales
+  // (and of x): keep them on one XCD so each line is fetched once.
+  int64_t panel;
+  int sub;
+  xcd_group_member(blockIdx.x, gridDim.x / CL, CL, &panel, &sub);
+  const int row = sub * SUBR + r;                     // row inside the panel
   const int64_t ch0 = panel * groups;
   const int stride = WAVES * CL;
   const int first = wave * CL + cl;

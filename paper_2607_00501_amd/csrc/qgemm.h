@@ -221,9 +221,14 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         const int g = 2 * kt + c;
         const int gc = min(g, G - 1);
         rb[sl][j][c] = *reinterpret_cast<const u32x4*>(b_q[j] + static_cast<int64_t>(gc) * kPanel * 16);
-        const uint32_t sv = b_s[j][static_cast<int64_t>(gc) * kPanel];
-        rs[sl][j][c] = (cols_ok && g < G && step < KTs && kt < KT) ? sv : 0u;
+        rs[sl][j][c] = b_s[j][static_cast<int64_t>(gc) * kPanel];
       }
+  };
+  // Scale validity of step t's chunk c, applied when the step is consumed
+  // (a select at load time would wait for the load to land).
+  auto scale_ok = [&](int t, int c) __attribute__((always_inline)) {
+    const int kt = kt0 + t;
+    return cols_ok && 2 * kt + c < G && kt < KT;
   };
   auto store_a = [&](auto slot, int buf) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot)::value;
@@ -256,7 +261,8 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     for (int j = 0; j < NB; ++j)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const auto sw = __builtin_amdgcn_permlane32_swap(rs[sl][j][c], rs[sl][j][c], false, false);
+        const uint32_t sv = scale_ok(t, c) ? rs[sl][j][c] : 0u;
+        const auto sw = __builtin_amdgcn_permlane32_swap(sv, sv, false, false);
         const _Float16 lo = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[0]));
         const _Float16 hi = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[1]));
         sc[j][c][0] = half2v{lo, lo};

@@ -21,6 +21,28 @@ typedef float float4v __attribute__((ext_vector_type(4)));
 
 __host__ __device__ inline int64_t padded_rows(int64_t n) { return (n + kPanel - 1) / kPanel * kPanel; }
 
+// Workgroups are dealt to the 8 XCDs of an MI355X round-robin by linear
+// index, and each XCD has its own L2.  For a grid of `groups` x `per`
+// workgroups where the `per` members of a group share cache lines, this maps
+// the linear index i to (group, member) so that all members of a group run on
+// the same XCD (index i lands on XCD i % 8; members are consecutive among the
+// indices of that XCD).  The trailing groups that do not fill all 8 XCDs keep
+// the plain mapping.  A bijection on [0, groups * per).
+constexpr int kXcds = 8;
+__host__ __device__ inline void xcd_group_member(int64_t i, int64_t groups, int per, int64_t* group,
+                                                 int* member) {
+  const int64_t full = groups / kXcds * kXcds;           // groups in complete sets of 8
+  if (i < full * per) {
+    const int64_t xcd = i % kXcds, j = i / kXcds;        // j: position among this XCD's indices
+    *group = (j / per) * kXcds + xcd;
+    *member = static_cast<int>(j % per);
+  } else {
+    const int64_t r = i - full * per;
+    *group = full + r / per;
+    *member = static_cast<int>(r % per);
+  }
+}
+
 // Bytes of codes per row of one matrix (canonical and device layouts agree).
 __host__ __device__ inline int64_t row_code_bytes(int32_t fmt, int64_t k) { return fmt == QM_Q4_G32 ? k / 2 : k; }
 
