@@ -110,6 +110,27 @@ def time_graph(torch, g, steps, warmup):
     return e0.elapsed_time(e1) / 1e3, wall      # seconds (events), seconds (wall)
 
 
+def steady_launch_us(torch, B, call, copies, reps=24, passes=5):
+    """Per-launch time of one GEMV run back to back in a graph (reps launches
+    cycling over `copies` copies of the weights, so that the bytes of one
+    cycle exceed the 256 MB MALL and every launch streams from HBM)."""
+    lib = B.lib()
+    wd = call.wd
+    ws = [wd] + [B.QWeight(wd.format, wd.layout, wd.batch, wd.n, wd.k, wd.qdata.clone(), wd.scales.clone())
+                 for _ in range(copies - 1)]
+    descs = [w.c() for w in ws]
+
+    def run(s):
+        for r in range(reps):
+            st = lib.qmatmul_gemv(ctypes.byref(descs[r % copies]), call.xp, call.yp, s)
+            if st != 0:
+                raise RuntimeError(lib.qm_last_error().decode())
+    g = capture(torch, run)
+    t, _ = time_graph(torch, g, passes, 1)
+    del g, ws
+    return t / passes / reps * 1e6
+
+
 def per_launch_ms(torch, calls, passes=5):
     """Mean duration of each call, timed with an event pair around every
     launch on the launch stream (eager, not captured)."""
@@ -207,12 +228,16 @@ def extra_workloads(torch, B, inputs, workloads, steps, warmup):
         head_ms = per[-1]
         kh, nh = workloads.LLAMA32_3B["lm_head"]
         head_bytes = workloads.q4_bytes(kh, nh) if fmt == B.Q4_G32 else workloads.q8_bytes(kh, nh)
+        head_us = steady_launch_us(torch, B, calls[-1], copies=2 if fmt == B.Q4_G32 else 1, reps=12)
         out[f"llama3.2-3b_decode_{tag}"] = {
             "tokens_per_s": round(steps / t, 2), "ms_per_token": round(t / steps * 1e3, 4),
             "weight_GBps": round(nbytes * steps / t / 1e9, 2),
             "frac_hbm_peak": round(nbytes * steps / t / 1e9 / HBM_PEAK_GBS, 4),
             "lm_head_GBps_events": round(head_bytes / (head_ms * 1e-3) / 1e9, 2),
-            "lm_head_frac_hbm_peak": round(head_bytes / (head_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            "lm_head_frac_hbm_peak": round(head_bytes / (head_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "lm_head_steady_us": round(head_us, 3),
+            "lm_head_steady_GBps": round(head_bytes / head_us / 1e3, 2),
+            "lm_head_steady_frac": round(head_bytes / head_us / 1e3 / HBM_PEAK_GBS, 4)}
         log(f"llama3b {tag}: {out[f'llama3.2-3b_decode_{tag}']}")
         del g, calls
         torch.cuda.empty_cache()
@@ -358,10 +383,11 @@ def main():
     gbs = nbytes * args.steps / secs / 1e9
     log(f"step: {secs / args.steps * 1e3:.4f} ms, {gbs:.1f} GB/s (wall {wall:.3f} s)")
 
-    # Dominant kernel: every launch of the step is the fused GEMV kernel
-    # (196 projections with 16 wavefronts per panel, the lm_head with 4).  In a
-    # graph replay the launches run back to back, so the mean launch duration
-    # is the step time over the launch count (HIP events on the launch stream).
+    # Dominant kernel: every launch of the step is the fused GEMV kernel (the
+    # 196 projections on the sub-panel plan, the lm_head on the panel plan).
+    # In a graph replay the launches run back to back, so the mean launch
+    # duration is the step time over the launch count (HIP events on the
+    # launch stream).
     mean_us = secs / args.steps / len(calls) * 1e6
     bytes_per_launch = nbytes / len(calls)
     achieved = bytes_per_launch / (mean_us * 1e-6) / 1e9
@@ -377,6 +403,11 @@ def main():
                 "algorithmic_bytes_per_launch": int(bytes_per_launch),
                 "lm_head_event_us": round(per[-1] * 1e3, 3), "lm_head_GBps": round(lm_gbs, 1),
                 "lm_head_frac": round(lm_gbs / HBM_PEAK_GBS, 4)}
+    # The lm_head back to back (4 copies = 350 MB per cycle, beyond the MALL).
+    lm_us = steady_launch_us(torch, B, calls[-1], copies=4)
+    roofline.update({"lm_head_steady_us": round(lm_us, 3),
+                     "lm_head_steady_GBps": round(lm_bytes / lm_us / 1e3, 1),
+                     "lm_head_steady_frac": round(lm_bytes / lm_us / 1e3 / HBM_PEAK_GBS, 4)})
     log(f"roofline: {roofline}")
     del g
 

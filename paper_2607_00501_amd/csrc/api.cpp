@@ -290,10 +290,10 @@ qm_status qm_device_config(char* buf, size_t len) {
                 "arch=%s cu=%d gemv(1024x1024: rows/wg=%d waves=%d) gemv(3072->1024: rows/wg=%d waves=%d) "
                 "gemv(lm_head 1024->151936: rows/wg=%d waves=%d) "
                 "gemm_tile(m=512,n=2048)=%s moe_tile(rows/expert=8)=%s moe_tile(rows/expert=128)=%s",
-                d->arch, d->cu_count, gemv_plan(1024, 1024, d->cu_count).subr,
-                gemv_plan(1024, 1024, d->cu_count).waves, gemv_plan(1024, 3072, d->cu_count).subr,
-                gemv_plan(1024, 3072, d->cu_count).waves, gemv_plan(151936, 1024, d->cu_count).subr,
-                gemv_plan(151936, 1024, d->cu_count).waves, gemm_tile_name(512, 2048),
+                d->arch, d->cu_count, gemv_plan(QM_Q4_G32, 1024, 1024, d->cu_count).subr,
+                gemv_plan(QM_Q4_G32, 1024, 1024, d->cu_count).waves, gemv_plan(QM_Q4_G32, 1024, 3072, d->cu_count).subr,
+                gemv_plan(QM_Q4_G32, 1024, 3072, d->cu_count).waves, gemv_plan(QM_Q4_G32, 151936, 1024, d->cu_count).subr,
+                gemv_plan(QM_Q4_G32, 151936, 1024, d->cu_count).waves, gemm_tile_name(512, 2048),
                 moe_tile_name(8), moe_tile_name(128));
   return QM_OK;
 }

@@ -29,7 +29,10 @@
 namespace qm {
 namespace {
 
-constexpr int kUnroll = 4;   // chunks in flight per lane
+// Chunks in flight per lane in the panel kernel: 8 Q4 chunks (128 B) or 4
+// Q8 chunks (two 16-B halves each), from a per-shape sweep of the lm_head
+// sizes on MI355X.
+template <int FMT> constexpr int kPanelUnroll = FMT == QM_Q4_G32 ? 8 : 4;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -131,7 +134,7 @@ __device__ inline float gemv_chunks(const uint8_t* __restrict__ q, const uint16_
   return acc;
 }
 
-template <int FMT, int WAVES>
+template <int FMT, int WAVES, int U>
 __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restrict__ q,
                                                           const uint16_t* __restrict__ s,
                                                           const uint16_t* __restrict__ x,
@@ -150,7 +153,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
 
   float acc = 0.0f;
   int c = c0;
-  for (; c + kUnroll <= c1; c += kUnroll) acc += gemv_chunks<FMT, kUnroll>(q, s, xw, ch0, c, lane, m0, m1);
+  for (; c + U <= c1; c += U) acc += gemv_chunks<FMT, U>(q, s, xw, ch0, c, lane, m0, m1);
   for (; c < c1; ++c) acc += gemv_chunks<FMT, 1>(q, s, xw, ch0, c, lane, m0, m1);
 
   if (WAVES == 1) {
@@ -309,7 +312,7 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
                       int64_t k, int cu_count, hipStream_t st) {
   const int64_t panels = padded_rows(n) / kPanel;
   const int64_t groups = k / kGroup;
-  const GemvPlan plan = gemv_plan(n, k, cu_count);
+  const GemvPlan plan = gemv_plan(FMT, n, k, cu_count);
   if (plan.subr < kPanel) {
     return plan.xlds ? launch_sub<FMT, true>(plan, q, s, x, y, n, groups, st)
                      : launch_sub<FMT, false>(plan, q, s, x, y, n, groups, st);
@@ -318,25 +321,29 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
   const int cpw = static_cast<int>((groups + waves - 1) / waves);
   const dim3 grid(static_cast<unsigned>(panels));
   const int ni = static_cast<int>(n), gi = static_cast<int>(groups);
+  constexpr int U = kPanelUnroll<FMT>;
   switch (waves) {
-    case 1: hipLaunchKernelGGL((gemv_kernel<FMT, 1>), grid, dim3(64), 0, st, q, s, x, y, ni, gi, cpw); break;
-    case 2: hipLaunchKernelGGL((gemv_kernel<FMT, 2>), grid, dim3(128), 0, st, q, s, x, y, ni, gi, cpw); break;
-    case 4: hipLaunchKernelGGL((gemv_kernel<FMT, 4>), grid, dim3(256), 0, st, q, s, x, y, ni, gi, cpw); break;
-    case 8: hipLaunchKernelGGL((gemv_kernel<FMT, 8>), grid, dim3(512), 0, st, q, s, x, y, ni, gi, cpw); break;
-    default: hipLaunchKernelGGL((gemv_kernel<FMT, 16>), grid, dim3(1024), 0, st, q, s, x, y, ni, gi, cpw); break;
+    case 1: hipLaunchKernelGGL((gemv_kernel<FMT, 1, U>), grid, dim3(64), 0, st, q, s, x, y, ni, gi, cpw); break;
+    case 2: hipLaunchKernelGGL((gemv_kernel<FMT, 2, U>), grid, dim3(128), 0, st, q, s, x, y, ni, gi, cpw); break;
+    case 4: hipLaunchKernelGGL((gemv_kernel<FMT, 4, U>), grid, dim3(256), 0, st, q, s, x, y, ni, gi, cpw); break;
+    case 8: hipLaunchKernelGGL((gemv_kernel<FMT, 8, U>), grid, dim3(512), 0, st, q, s, x, y, ni, gi, cpw); break;
+    case 12: hipLaunchKernelGGL((gemv_kernel<FMT, 12, U>), grid, dim3(768), 0, st, q, s, x, y, ni, gi, cpw); break;
+    default: hipLaunchKernelGGL((gemv_kernel<FMT, 16, U>), grid, dim3(1024), 0, st, q, s, x, y, ni, gi, cpw); break;
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Per-chip launch plan, from a cold per-shape sweep on MI355X (256 CUs).
-// Matrices with at least one 64-row panel per CU use the panel kernel with 8
-// wavefronts per panel (fewer only if there are fewer groups).  Smaller matrices use the sub-panel
-// kernel with 8 wavefronts per workgroup and the smallest row count (8, 16
-// or 32) that keeps the grid at <= 2 workgroups per CU; activations are
-// staged in LDS for K <= 4096 and read from global memory beyond.
-GemvPlan gemv_plan(int64_t n, int64_t k, int cu_count) {
+// Per-chip launch plan, from per-shape sweeps on MI355X (256 CUs).
+// Matrices with at least one 64-row panel per CU use the panel kernel.  Q4:
+// enough wavefronts per panel for one pass of 8 chunks each (4 at K = 1024,
+// 12 at K = 3072), at most 16; Q8: 8 wavefronts (fewer only if there are
+// fewer groups).  Smaller matrices use the sub-panel kernel with 8
+// wavefronts per workgroup and the smallest row count (8, 16 or 32) that
+// keeps the grid at <= 2 workgroups per CU; activations are staged in LDS
+// for K <= 4096 and read from global memory beyond.
+GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count) {
   // Tuning sweeps only: QM_GEMV_PLAN="rows,waves,x_in_lds" forces the plan.
   static const GemvPlan forced = [] {
     GemvPlan f{0, 0, 1};
@@ -346,8 +353,13 @@ GemvPlan gemv_plan(int64_t n, int64_t k, int cu_count) {
   if (forced.subr == 4 || forced.subr == 8 || forced.subr == 16 || forced.subr == 32 || forced.subr == 64) {
     GemvPlan f = forced;
     if (f.subr < kPanel && k > 16384) f.xlds = 0;
-    if (f.waves < 1) f.waves = 1;
-    if (f.waves > (f.subr == kPanel ? 16 : 8)) f.waves = f.subr == kPanel ? 16 : 8;
+    if (f.subr == kPanel) {
+      int w = 1;
+      while (w < 16 && w < f.waves) w = w == 8 ? 12 : (w == 12 ? 16 : 2 * w);
+      f.waves = w;
+    } else {
+      f.waves = f.waves <= 1 ? 1 : f.waves <= 2 ? 2 : f.waves <= 4 ? 4 : 8;
+    }
     return f;
   }
   const int64_t npad = padded_rows(n);
@@ -356,7 +368,12 @@ GemvPlan gemv_plan(int64_t n, int64_t k, int cu_count) {
   GemvPlan p;
   if (panels >= cu_count) {
     int w = 1;
-    while (w < 8 && w * 2 <= groups) w *= 2;
+    if (fmt == QM_Q4_G32) {
+      const int64_t want = (groups + kPanelUnroll<QM_Q4_G32> - 1) / kPanelUnroll<QM_Q4_G32>;
+      while (w < 16 && w < want) w = w == 8 ? 12 : (w == 12 ? 16 : 2 * w);
+    } else {
+      while (w < 8 && w * 2 <= groups) w *= 2;
+    }
     p.subr = kPanel;
     p.waves = w;
     p.xlds = 0;

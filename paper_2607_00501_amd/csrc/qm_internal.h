@@ -93,7 +93,7 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
 // GEMV launch plan: rows per workgroup (64 = whole panel), wavefronts per
 // workgroup, and whether activations are staged in LDS (sub-panel kernel).
 struct GemvPlan { int subr; int waves; int xlds; };
-GemvPlan gemv_plan(int64_t n, int64_t k, int cu_count);
+GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count);
 struct GemmPlan { int bm; int wn; int wk; };   // rows per tile, panels (wavefronts) per K slice, K slices
 GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count);
 const char* gemm_tile_name(int64_t m, int64_t n);
