@@ -19,7 +19,7 @@
 //    in LDS (one barrier per K step) and shared by the WN wavefronts of the
 //    slice; A fragments of the next substep are read while the current
 //    MFMAs run;
-//  * global loads run two K steps ahead of the MFMAs.  Out-of-range rows,
+//  * global loads run DEPTH (2-4) K steps ahead of the MFMAs.  Out-of-range rows,
 //    columns and K steps read clamped (valid) addresses with their scales
 //    forced to zero, so the loads carry no branches;
 //  * modes: kDense (rows m0.., plain row-major A and Y); kMoeGateUp (rows of
@@ -33,6 +33,7 @@
 #pragma once
 
 #include <type_traits>
+#include <utility>
 
 #include "qm_internal.h"
 
@@ -113,7 +114,7 @@ __device__ inline void find_tile(const int32_t* counts, int E, int BM, int bx, i
   __syncthreads();
 }
 
-template <int BM, int WN, int WK, QgMode MODE>
+template <int BM, int WN, int WK, QgMode MODE, int DEPTH>
 struct Cfg {
   static constexpr bool kDual = MODE == QgMode::kMoeGateUp;
   static constexpr int kNB = kDual ? 2 : 1;                      // weight matrices per wavefront
@@ -124,12 +125,13 @@ struct Cfg {
   static constexpr int kStage = BM * kRow;                        // halves per A stage
   static_assert(kALoads >= 1 && BM * (kBK / 8) % kSliceThreads == 0, "A tile split");
   static_assert(WK == 1 || MODE == QgMode::kDense, "split-K only for the dense GEMM");
+  static_assert(DEPTH >= 2 && DEPTH <= 4, "register slots of K steps in flight");
   static_assert(WK == 1 || (WK - 1) * WN * BM * 64 * 4 <= 2 * WK * kStage * 2, "reduction fits in LDS");
 };
 
-template <int BM, int WN, int WK, QgMode MODE>
+template <int BM, int WN, int WK, QgMode MODE, int DEPTH>
 __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
-  using C = Cfg<BM, WN, WK, MODE>;
+  using C = Cfg<BM, WN, WK, MODE, DEPTH>;
   constexpr int NB = C::kNB;
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * WK * C::kStage];
   const int tid = threadIdx.x;
@@ -202,10 +204,11 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     b_s[1] = p.s2 + expert * mat_s + panel * G * kPanel + lane;
   }
 
-  // Two register sets of raw step operands, always indexed by constants.
-  u32x4 ra[2][C::kALoads];
-  u32x4 rb[2][NB][2];
-  uint32_t rs[2][NB][2];
+  // DEPTH register sets of raw step operands (step t lives in slot t % DEPTH),
+  // always indexed by constants.
+  u32x4 ra[DEPTH][C::kALoads];
+  u32x4 rb[DEPTH][NB][2];
+  uint32_t rs[DEPTH][NB][2];
   auto load = [&](auto slot, int step) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot)::value;
     const int kt = kt0 + step;
@@ -236,8 +239,6 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 #pragma unroll
     for (int i = 0; i < C::kALoads; ++i) *reinterpret_cast<u32x4*>(dst + a_lds[i]) = ra[sl][i];
   };
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, 1>;
 
   float16v acc[C::kTM][2 * NB];
 #pragma unroll
@@ -247,13 +248,14 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
 
-  // One K step t: register slot sl holds step t's raw operands (its A tile is
-  // already in LDS buffer t&1), slot 1-sl step t+1's.  The B codes of slot sl
-  // move to registers in MFMA layout, then slot sl is refilled with step t+2;
-  // step t+1's A tile goes to the other LDS buffer after the MFMAs.
+  // One K step t: register slot sl = t % DEPTH holds step t's raw operands
+  // (its A tile is already in LDS buffer t&1), the other slots steps t+1 ..
+  // t+DEPTH-1.  The B codes of slot sl move to registers in MFMA layout, then
+  // slot sl is refilled with step t+DEPTH; step t+1's A tile goes to the other
+  // LDS buffer after the MFMAs.
   auto step = [&](auto slot, int t) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot)::value;
-    using Next = std::integral_constant<int, 1 - sl>;
+    using Next = std::integral_constant<int, (sl + 1) % DEPTH>;
     const int buf = t & 1;
     uint32_t bd[NB][2][4];                                 // [matrix][column half][substep]
     half2v sc[NB][2][2];                                   // [matrix][chunk][column half]
@@ -275,28 +277,41 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
           bd[j][1][2 * c + i] = pr[1];                     // panel rows 32..63
         }
       }
-    load(slot, t + 2);                                     // two steps ahead
+    load(slot, t + DEPTH);                                 // DEPTH steps ahead
     __builtin_amdgcn_sched_barrier(0);                     // keep the loads at the top
     const uint16_t* At = lds + (buf * WK + wk) * C::kStage + (lane & 31) * kRow + 8 * (lane >> 5);
+    // Software pipeline over the four 16-deep substeps: the A fragments and
+    // the dequantised B fragments of substep ks+1 are produced while the
+    // MFMAs of substep ks run.
     half8v af[2][C::kTM];
+    half8v bq[2][NB][2];
 #pragma unroll
     for (int a = 0; a < C::kTM; ++a) af[0][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow);
 #pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      bq[0][j][0] = dequant_dword(bd[j][0][0], sc[j][0][0]);
+      bq[0][j][1] = dequant_dword(bd[j][1][0], sc[j][0][1]);
+    }
+#pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
+      const int cur = ks & 1, nxt = cur ^ 1;
       if (ks + 1 < kBK / 16) {
 #pragma unroll
         for (int a = 0; a < C::kTM; ++a)
-          af[(ks + 1) & 1][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow + (ks + 1) * 16);
+          af[nxt][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow + (ks + 1) * 16);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          bq[nxt][j][0] = dequant_dword(bd[j][0][ks + 1], sc[j][(ks + 1) >> 1][0]);
+          bq[nxt][j][1] = dequant_dword(bd[j][1][ks + 1], sc[j][(ks + 1) >> 1][1]);
+        }
       }
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
-        const half8v b0 = dequant_dword(bd[j][0][ks], sc[j][ks >> 1][0]);
-        const half8v b1 = dequant_dword(bd[j][1][ks], sc[j][ks >> 1][1]);
 #pragma unroll
         for (int a = 0; a < C::kTM; ++a) {
-          acc[a][2 * j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[ks & 1][a], b0, acc[a][2 * j], 0, 0, 0);
+          acc[a][2 * j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][a], bq[cur][j][0], acc[a][2 * j], 0, 0, 0);
           acc[a][2 * j + 1] =
-              __builtin_amdgcn_mfma_f32_32x32x16_f16(af[ks & 1][a], b1, acc[a][2 * j + 1], 0, 0, 0);
+              __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][a], bq[cur][j][1], acc[a][2 * j + 1], 0, 0, 0);
         }
       }
     }
@@ -304,16 +319,21 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     __syncthreads();
   };
 
-  load(S0{}, 0);
-  load(S1{}, 1);
-  store_a(S0{}, 0);
+  using Slots = std::make_integer_sequence<int, DEPTH>;
+  [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
+    (load(std::integral_constant<int, I>{}, I), ...);
+  }(Slots{});
+  store_a(std::integral_constant<int, 0>{}, 0);
   __syncthreads();
   int t = 0;
-  for (; t + 2 <= KTs; t += 2) {
-    step(S0{}, t);
-    step(S1{}, t + 1);
+  for (; t + DEPTH <= KTs; t += DEPTH) {
+    [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
+      (step(std::integral_constant<int, I>{}, t + I), ...);
+    }(Slots{});
   }
-  if (t < KTs) step(S0{}, t);
+  [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
+    ((t + I < KTs ? step(std::integral_constant<int, I>{}, t + I) : void()), ...);
+  }(Slots{});
 
   if constexpr (WK > 1) {
     // Partial sums of slices 1..WK-1 go through LDS; slice 0 adds them in order.
@@ -368,9 +388,9 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 
 }  // namespace qg
 
-template <int BM, int WN, int WK, QgMode MODE>
+template <int BM, int WN, int WK, QgMode MODE, int DEPTH = 2>
 __global__ __launch_bounds__(WN * WK * 64, 2) void qgemm_kernel(QgemmArgs p) {
-  qg::qgemm_body<BM, WN, WK, MODE>(p);
+  qg::qgemm_body<BM, WN, WK, MODE, DEPTH>(p);
 }
 
 }  // namespace qm
