@@ -159,7 +159,9 @@ qm_status qmoe_route(const float* logits, int64_t m, int32_t n_experts, int32_t 
  *  w_down: DEVICE layout Q4, batch E, [E][hidden][inter];
  *  x: fp16 [m][hidden]; y: fp32 [m][hidden]; topk_w [m][top_k], counts,
  *  offsets and sorted_assign come from qmoe_route (sorted_assign must be a
- *  permutation of 0 .. m*top_k-1 consistent with counts/offsets).  hidden % 32 == 0 and inter % 32 == 0.  h is held in fp16;
+ *  permutation of 0 .. m*top_k-1 consistent with counts/offsets).
+ *  hidden % 32 == 0 and inter % 32 == 0.  h and the gate-weighted
+ *  per-assignment outputs topk_w * y_a are held in fp16 (summed in fp32);
  *  all GEMMs use fp16 MFMA with fp32 accumulation.  The workspace (device,
  *  16-byte aligned, >= qmoe_workspace_bytes) holds h and the per-assignment
  *  outputs; no host synchronisation: per-expert row counts stay on the

@@ -275,7 +275,7 @@ qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up, co
   a.y = y;
   const size_t h_bytes = (static_cast<size_t>(m * top_k * inter) * 2 + 255) / 256 * 256;
   a.h = static_cast<uint16_t*>(workspace);
-  a.yp = reinterpret_cast<float*>(static_cast<char*>(workspace) + h_bytes);
+  a.yp = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + h_bytes);
   a.m = m; a.hidden = hidden; a.inter = inter;
   a.n_experts = static_cast<int32_t>(E); a.top_k = top_k;
   return launched(launch_moe(a, d->cu_count, static_cast<hipStream_t>(stream)), "qmoe_grouped_gemm");

@@ -18,7 +18,6 @@ namespace {
 // ------------------------------------------------------------------ route
 
 constexpr int kRouteThreads = 256;   // one wavefront per token
-constexpr int kMaxPerLane = 16;      // n_experts <= 1024
 
 // (value, index) order used by the router: larger value first, lower index
 // on equal values.
@@ -55,6 +54,8 @@ __device__ inline void wave_argmax(float& bv, int& be) {
   be = e;
 }
 
+// PER = logits per lane (n_experts <= 64 * PER), a power of two.
+template <int PER>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(const float* __restrict__ logits,
                                                               int64_t m, int E, int K,
                                                               int32_t* __restrict__ ids,
@@ -63,26 +64,26 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(const float* __res
   const int64_t t = static_cast<int64_t>(blockIdx.x) * (kRouteThreads / 64) + (threadIdx.x >> 6);
   if (t >= m) return;
   const float* row = logits + t * E;
-  float v[kMaxPerLane];
-  const int per_lane = (E + 63) / 64;
+  float v[PER];
 #pragma unroll
-  for (int i = 0; i < kMaxPerLane; ++i) {
+  for (int i = 0; i < PER; ++i) {
     const int e = i * 64 + lane;
-    v[i] = (i < per_lane && e < E) ? row[e] : -INFINITY;
+    v[i] = e < E ? row[e] : -INFINITY;
   }
-  uint32_t taken = 0;   // bit i: item i of this lane already selected
-  float my_v = -INFINITY;   // lane j < K ends up holding the j-th selected logit
+  uint32_t taken = 0;         // bit i: item i of this lane already selected
+  float my_v = -INFINITY;     // lane j < K ends up holding the j-th selected logit
   int my_e = 0;
   for (int j = 0; j < K; ++j) {
     // Lane-local best: highest value, lowest expert index on ties.
     float bv = -INFINITY;
     int be = 0x7FFFFFFF;
 #pragma unroll
-    for (int i = 0; i < kMaxPerLane; ++i) {
+    for (int i = 0; i < PER; ++i) {
       const int e = i * 64 + lane;
-      if (i < per_lane && e < E && !(taken >> i & 1u)) {
-        if (v[i] > bv || (v[i] == bv && e < be)) { bv = v[i]; be = e; }
-      }
+      const bool ok = e < E && !((taken >> i) & 1u);
+      const bool better = ok && (v[i] > bv || (v[i] == bv && e < be));
+      bv = better ? v[i] : bv;
+      be = better ? e : be;
     }
     // Wavefront argmax with the same order.
     wave_argmax(bv, be);
@@ -108,12 +109,12 @@ constexpr int kBucketThreads = 1024;
 constexpr int kBucketWaves = kBucketThreads / 64;
 constexpr int kBucketUnroll = 8;
 
-// Lanes of the wavefront that hold the same expert id (ten ballots, one per
-// bit of the id), restricted to the valid lanes.
-__device__ inline uint64_t match_expert(int e, bool valid) {
+// Lanes of the wavefront that hold the same expert id (one ballot per bit of
+// the id, `bits` = bits needed for n_experts - 1), restricted to the valid
+// lanes.
+__device__ inline uint64_t match_expert(int e, bool valid, int bits) {
   uint64_t mask = __ballot(valid);
-#pragma unroll
-  for (int bit = 0; bit < 10; ++bit) {
+  for (int bit = 0; bit < bits; ++bit) {
     const bool set = (e >> bit) & 1;
     const uint64_t b = __ballot(valid && set);
     mask &= set ? b : ~b;
@@ -123,13 +124,14 @@ __device__ inline uint64_t match_expert(int e, bool valid) {
 
 // One workgroup of 16 wavefronts; wavefront w owns the contiguous range
 // [w*R, (w+1)*R) of assignments.  Pass 1 counts each wavefront's
-// assignments per expert (64 at a time: the leader of each group of equal
-// experts adds the group size); then one pass over the experts turns the
+// assignments per expert (LDS integer atomics: the counts do not depend on
+// the order of the adds); then one pass over the experts turns the
 // per-wavefront counts into exclusive bases (expert offset + earlier
 // wavefronts' counts) and writes counts and offsets; pass 2 walks the range
 // again and places each assignment at base + rank among equal experts of
-// its group of 64, the leader advancing the base.  The result is the stable
-// counting sort by (expert, assignment id).  Two barriers in total.
+// its group of 64 lanes, the group's leader advancing the base.  The result
+// is the stable counting sort by (expert, assignment id).  Groups past the
+// end of a wavefront's range are skipped (wavefront-uniform test).
 __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* __restrict__ ids,
                                                                 int64_t A, int E,
                                                                 int32_t* __restrict__ counts,
@@ -140,12 +142,14 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  int bits = 0;
+  while ((1 << bits) < E) ++bits;
   for (int w = 0; w < kBucketWaves; ++w) base[w][tid] = 0;
   __syncthreads();
   const int64_t R = ((A + kBucketWaves - 1) / kBucketWaves + 63) / 64 * 64;
   const int64_t lo = min<int64_t>(A, wave * R), hi = min<int64_t>(A, lo + R);
   const uint64_t lower = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  // 8 groups of 64 per round: all eight id loads are issued before use.
+  // kBucketUnroll groups of 64 per round: all their id loads are issued first.
   for (int64_t b0 = lo; b0 < hi; b0 += 64 * kBucketUnroll) {
     int ev[kBucketUnroll];
 #pragma unroll
@@ -154,11 +158,8 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
       ev[u] = a < hi ? ids[a] : 0;
     }
 #pragma unroll
-    for (int u = 0; u < kBucketUnroll; ++u) {
-      const bool valid = b0 + u * 64 + lane < hi;
-      const uint64_t mask = match_expert(ev[u], valid);
-      if (valid && __popcll(mask & lower) == 0) base[wave][ev[u]] += __popcll(mask);
-    }
+    for (int u = 0; u < kBucketUnroll; ++u)
+      if (b0 + u * 64 + lane < hi) atomicAdd(&base[wave][ev[u]], 1);
   }
   __syncthreads();
   // Thread e: total count, per-wavefront exclusive prefix; then the
@@ -196,9 +197,10 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
     }
 #pragma unroll
     for (int u = 0; u < kBucketUnroll; ++u) {
+      if (b0 + u * 64 >= hi) break;                      // wavefront-uniform
       const int64_t a = b0 + u * 64 + lane;
       const bool valid = a < hi;
-      const uint64_t mask = match_expert(ev[u], valid);
+      const uint64_t mask = match_expert(ev[u], valid, bits);
       const int rank = __popcll(mask & lower);
       if (valid) sorted_assign[base[wave][ev[u]] + rank] = static_cast<int32_t>(a);
       // every lane read its base before the leader advances it (same
@@ -210,19 +212,23 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
 
 // ---------------------------------------------------------------- combine
 
-// y[t][n] = sum over slots j (in order) of the gate-weighted expert outputs.
-__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ yp, float* __restrict__ y,
+// y[t][n] = sum over slots j (in order) of the gate-weighted expert outputs
+// (fp16 in the workspace, summed in fp32).  One thread per 8 outputs.
+__global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict__ yp, float* __restrict__ y,
                                                       int64_t m, int64_t hidden, int K) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;   // float4 index
-  const int64_t h4 = hidden / 4;
-  if (i >= m * h4) return;
-  const int64_t t = i / h4, c = i % h4;
-  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;   // 8-output index
+  const int64_t h8 = hidden / 8;
+  if (i >= m * h8) return;
+  const int64_t t = i / h8, c = i % h8;
+  float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int j = 0; j < K; ++j) {
-    const float4 v = reinterpret_cast<const float4*>(yp + (t * K + j) * hidden)[c];
-    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    const half8v v = reinterpret_cast<const half8v*>(yp + (t * K + j) * hidden)[c];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) s[r] += static_cast<float>(v[r]);
   }
-  reinterpret_cast<float4*>(y + t * hidden)[c] = s;
+  float4* dst = reinterpret_cast<float4*>(y + t * hidden) + 2 * c;
+  dst[0] = make_float4(s[0], s[1], s[2], s[3]);
+  dst[1] = make_float4(s[4], s[5], s[6], s[7]);
 }
 
 template <int BM, int WN>
@@ -246,8 +252,8 @@ hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((qgemm_kernel<BM, WN, 1, QgMode::kMoeDown>), dim3(tiles, ny2), dim3(WN * 64), 0, st, g);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t n4 = a.m * (a.hidden / 4);
-  hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((n4 + 255) / 256)), dim3(256), 0, st, a.yp,
+  const int64_t n8 = a.m * (a.hidden / 8);
+  hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((n8 + 255) / 256)), dim3(256), 0, st, a.yp,
                      a.y, a.m, a.hidden, a.top_k);
   return hipGetLastError();
 }
@@ -257,7 +263,7 @@ hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
 size_t moe_workspace_bytes(int64_t m, int32_t top_k, int64_t hidden, int64_t inter) {
   const size_t A = static_cast<size_t>(m) * top_k;
   const size_t h_bytes = (A * inter * 2 + 255) / 256 * 256;
-  const size_t yp_bytes = (A * hidden * 4 + 255) / 256 * 256;
+  const size_t yp_bytes = (A * hidden * 2 + 255) / 256 * 256;
   return h_bytes + yp_bytes;
 }
 
@@ -269,7 +275,12 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
                         int32_t* counts, int32_t* offsets, int32_t* sorted_assign, hipStream_t st) {
   if (m > 0) {
     const unsigned blocks = static_cast<unsigned>((m + 3) / 4);
-    hipLaunchKernelGGL(route_kernel, dim3(blocks), dim3(kRouteThreads), 0, st, logits, m, e, k, ids, w);
+    const dim3 g(blocks), b(kRouteThreads);
+    if (e <= 64) hipLaunchKernelGGL(route_kernel<1>, g, b, 0, st, logits, m, e, k, ids, w);
+    else if (e <= 128) hipLaunchKernelGGL(route_kernel<2>, g, b, 0, st, logits, m, e, k, ids, w);
+    else if (e <= 256) hipLaunchKernelGGL(route_kernel<4>, g, b, 0, st, logits, m, e, k, ids, w);
+    else if (e <= 512) hipLaunchKernelGGL(route_kernel<8>, g, b, 0, st, logits, m, e, k, ids, w);
+    else hipLaunchKernelGGL(route_kernel<16>, g, b, 0, st, logits, m, e, k, ids, w);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
   }

@@ -27,7 +27,8 @@
 //    permutation, each wavefront streams the gate and the up panel of the
 //    same columns and the epilogue writes fp16 silu(gate) * up); kMoeDown
 //    (A = the fp16 h rows of the bucket, the epilogue scales by the
-//    assignment's gate weight and scatters the row to its assignment slot).
+//    assignment's gate weight and scatters the row, in fp16, to its
+//    assignment slot).
 //    MoE workgroups find their (expert, row tile) from the per-expert counts
 //    on the device, so no host synchronisation is needed.
 #pragma once
@@ -52,7 +53,7 @@ struct QgemmArgs {
   const int32_t* sorted_assign;
   const float* topk_w;
   uint16_t* h;                             // kMoeGateUp output [M][N] fp16 (bucket order)
-  float* yp;                               // kMoeDown output [M][N] (assignment order)
+  uint16_t* yp;                            // kMoeDown output [M][N] fp16 (assignment order)
   int32_t n_experts, top_k;
 };
 
@@ -380,7 +381,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
           const float hv = g / (1.0f + expf(-g)) * u;
           p.h[(row0 + lr) * N + col] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(hv));
         } else {
-          p.yp[row_asg[lr] * N + col] = row_w[lr] * acc[a][b][r];
+          p.yp[row_asg[lr] * N + col] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(row_w[lr] * acc[a][b][r]));
         }
       }
     }

@@ -79,7 +79,7 @@ struct MoeArgs {
   const float* topk_w;                     // [m*top_k]
   float* y;                                // [m][hidden]
   uint16_t* h;                             // workspace: [m*top_k][inter] fp16
-  float* yp;                               // workspace: [m*top_k][hidden] fp32
+  uint16_t* yp;                            // workspace: [m*top_k][hidden] fp16
   int64_t m, hidden, inter;
   int32_t n_experts, top_k;
 };
