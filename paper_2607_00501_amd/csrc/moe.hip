@@ -10,6 +10,11 @@
 // workgroup finds its (expert, row tile) from the counts itself.
 #include <hip/hip_fp16.h>
 
+#include <cstdio>
+#include <cstdlib>
+#include <array>
+#include <utility>
+
 #include "qgemm.h"
 
 namespace qm {
@@ -231,25 +236,27 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict
   dst[1] = make_float4(s[4], s[5], s[6], s[7]);
 }
 
-template <int BM, int WN>
+template <int BMG, int WKG, int BMD, int WKD, int WN, int DG = 2, int DD = 2>
 hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
   const int64_t A = a.m * a.top_k;
   // Upper bound on the number of (expert, row tile) pairs: sum of
   // ceil(count_e / BM) <= A / BM + E.  Workgroups past the last tile exit.
-  const unsigned tiles = static_cast<unsigned>((A + BM - 1) / BM + a.n_experts);
+  auto tiles = [&](int bm) { return static_cast<unsigned>((A + bm - 1) / bm + a.n_experts); };
   QgemmArgs g{};
   g.counts = a.counts; g.offsets = a.offsets; g.sorted_assign = a.sorted_assign; g.topk_w = a.topk_w;
   g.n_experts = a.n_experts; g.top_k = a.top_k; g.M = A;
   // gate/up + SwiGLU: A = x rows gathered per assignment, N = inter, K = hidden
   g.q = a.gq; g.s = a.gs; g.q2 = a.uq; g.s2 = a.us; g.a = a.x; g.h = a.h; g.N = a.inter; g.K = a.hidden;
   const unsigned ny1 = static_cast<unsigned>((a.inter + 64 * WN - 1) / (64 * WN));
-  hipLaunchKernelGGL((qgemm_kernel<BM, WN, 1, QgMode::kMoeGateUp>), dim3(tiles, ny1), dim3(WN * 64), 0, st, g);
+  hipLaunchKernelGGL((qgemm_kernel<BMG, WN, WKG, QgMode::kMoeGateUp, DG>), dim3(tiles(BMG), ny1), dim3(WN * WKG * 64), 0,
+                     st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // down, scaled by the gate weight and scattered to the assignment slot
   g.q = a.dq; g.s = a.ds; g.q2 = nullptr; g.s2 = nullptr; g.a = a.h; g.yp = a.yp; g.N = a.hidden; g.K = a.inter;
   const unsigned ny2 = static_cast<unsigned>((a.hidden + 64 * WN - 1) / (64 * WN));
-  hipLaunchKernelGGL((qgemm_kernel<BM, WN, 1, QgMode::kMoeDown>), dim3(tiles, ny2), dim3(WN * 64), 0, st, g);
+  hipLaunchKernelGGL((qgemm_kernel<BMD, WN, WKD, QgMode::kMoeDown, DD>), dim3(tiles(BMD), ny2), dim3(WN * WKD * 64), 0,
+                     st, g);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t n8 = a.m * (a.hidden / 8);
@@ -291,11 +298,24 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
 
 hipError_t launch_moe(const MoeArgs& a, int cu_count, hipStream_t st) {
   (void)cu_count;
+  // Tuning sweeps only: QM_MOE_PLAN="bm_gate_up,wk_gate_up,bm_down,wk_down,
+  // depth_gate_up,depth_down".
+  static const std::array<int, 6> forced = [] {
+    std::array<int, 6> f{0, 0, 0, 0, 2, 2};
+    if (const char* e = std::getenv("QM_MOE_PLAN"))
+      std::sscanf(e, "%d,%d,%d,%d,%d,%d", &f[0], &f[1], &f[2], &f[3], &f[4], &f[5]);
+    return f;
+  }();
+  using P = std::array<int, 6>;
+  if (forced == P{32, 1, 32, 1, 2, 2}) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2>(a, st);
+  if (forced == P{64, 1, 64, 1, 2, 2}) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2>(a, st);
+  if (forced == P{32, 2, 32, 1, 2, 2}) return launch_moe_tiles<32, 2, 32, 1, 4, 2, 2>(a, st);
+  if (forced == P{64, 1, 128, 1, 2, 2}) return launch_moe_tiles<64, 1, 128, 1, 4, 2, 2>(a, st);
   // Per-chip tile choice by rows per expert: 32-row tiles when buckets are
   // small (decode-like prefill chunks), 64-row tiles otherwise.
   const int64_t rpe = a.m * a.top_k / a.n_experts;
-  if (rpe <= 24) return launch_moe_tiles<32, 4>(a, st);
-  return launch_moe_tiles<64, 4>(a, st);
+  if (rpe <= 24) return launch_moe_tiles<32, 1, 32, 1, 4>(a, st);
+  return launch_moe_tiles<64, 1, 64, 1, 4>(a, st);
 }
 
 }  // namespace qm

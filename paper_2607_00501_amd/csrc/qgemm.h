@@ -6,10 +6,10 @@
 // v_mfma_f32_32x32x16_f16):
 //  * a workgroup has WN x WK wavefronts; wavefront (wn, wk) owns the BM x 64
 //    output block whose 64 columns are one device-layout panel, over the
-//    wk-th slice of the K steps (WK > 1: split-K inside the workgroup, the
-//    partial sums meet in LDS in a fixed order).  One 64-deep K step of its
-//    weights is two 1 KiB contiguous chunk rows: one dwordx4 per lane per
-//    chunk, fully coalesced;
+//    wk-th slice of the K steps (WK > 1: split-K inside the workgroup, in
+//    every mode; the partial sums meet in LDS in a fixed order).  One 64-deep
+//    K step of its weights is two 1 KiB contiguous chunk rows: one dwordx4
+//    per lane per chunk, fully coalesced;
 //  * the weights never pass through LDS: each wavefront dequantises its own
 //    B fragments in registers.  One v_permlane32_swap per dword pair moves
 //    the codes of panel rows 32..63 / 0..31 into the MFMA B-operand lane
@@ -125,16 +125,17 @@ struct Cfg {
   static constexpr int kALoads = BM * (kBK / 8) / kSliceThreads;
   static constexpr int kStage = BM * kRow;                        // halves per A stage
   static_assert(kALoads >= 1 && BM * (kBK / 8) % kSliceThreads == 0, "A tile split");
-  static_assert(WK == 1 || MODE == QgMode::kDense, "split-K only for the dense GEMM");
   static_assert(DEPTH >= 2 && DEPTH <= 4, "register slots of K steps in flight");
-  static_assert(WK == 1 || (WK - 1) * WN * BM * 64 * 4 <= 2 * WK * kStage * 2, "reduction fits in LDS");
+  // Split-K partial sums of slices 1..WK-1, in halves (fp32 = 2 halves).
+  static constexpr int kRedHalves = (WK - 1) * WN * kTM * 2 * kNB * 16 * 64 * 2;
+  static constexpr int kLdsHalves = 2 * WK * kStage > kRedHalves ? 2 * WK * kStage : kRedHalves;
 };
 
 template <int BM, int WN, int WK, QgMode MODE, int DEPTH>
 __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   using C = Cfg<BM, WN, WK, MODE, DEPTH>;
   constexpr int NB = C::kNB;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * WK * C::kStage];
+  __shared__ __attribute__((aligned(16))) uint16_t lds[C::kLdsHalves];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -339,15 +340,15 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   if constexpr (WK > 1) {
     // Partial sums of slices 1..WK-1 go through LDS; slice 0 adds them in order.
     float* red = reinterpret_cast<float*>(lds);
-    constexpr int per_wave = C::kTM * 2 * 16 * 64;
+    constexpr int per_wave = C::kTM * 2 * NB * 16 * 64;
     if (wk > 0) {
       float* dst = red + ((wk - 1) * WN + wn) * per_wave;
 #pragma unroll
       for (int a = 0; a < C::kTM; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < 2 * NB; ++b)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) dst[((a * 2 + b) * 16 + r) * 64 + lane] = acc[a][b][r];
+          for (int r = 0; r < 16; ++r) dst[((a * 2 * NB + b) * 16 + r) * 64 + lane] = acc[a][b][r];
     }
     __syncthreads();
     if (wk > 0) return;
@@ -356,9 +357,9 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 #pragma unroll
       for (int a = 0; a < C::kTM; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < 2 * NB; ++b)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) acc[a][b][r] += src[((a * 2 + b) * 16 + r) * 64 + lane];
+          for (int r = 0; r < 16; ++r) acc[a][b][r] += src[((a * 2 * NB + b) * 16 + r) * 64 + lane];
     }
   }
 
