@@ -126,11 +126,28 @@ qm_status qm_repack(const qm_qweight* src, const qm_qweight* dst, void* stream);
  * Single kernel launch, no workspace, deterministic. */
 qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* stream);
 
+/* Grouped decode GEMV (Sec. 3.3: fusing a sequence of operators removes a
+ * launch each, which matters most in decode; e.g. the q/k/v projections of
+ * a layer, which share x, or its gate and up projections):
+ *   y_i[n] = sum_k s_i[n][k/32] * q_i[n][k] * x_i[k]   for i < count,
+ * in one launch when the group's total rows stay below 64 rows per CU (else
+ * one launch per matrix).  w: host array of `count` descriptors, all DEVICE
+ * layout, batch 1, one format and one k; n_i may differ.  x, y: host arrays
+ * of `count` device pointers; x_i fp16 [k], 16-byte aligned, and may be
+ * shared between entries; y_i fp32 [n_i], 4-byte aligned, must not overlap
+ * each other or any x_i.  1 <= count <= 8 (QM_GEMV_GROUP_MAX).  Same
+ * arithmetic as qmatmul_gemv (the summation order may differ, since the
+ * launch plan follows the group's total rows).  No workspace, deterministic. */
+#define QM_GEMV_GROUP_MAX 8
+qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_t* const* x,
+                               float* const* y, void* stream);
+
 /* Prefill GEMM (Sec. 3.3, Sec. 3.4, M > 1): Y[m][n] = sum_k X[m][k] * w'[n][k].
  * w: DEVICE layout, batch 1, Q4.  X: fp16 [m][k] row-major; Y: fp32 [m][n].
- * Weight tiles are dequantised to fp16 (value fp16_RNE(s*q)) in LDS and fed
- * to fp16 MFMA with fp32 accumulation.  m >= 1 (m == 1 runs the GEMV);
- * m <= 65536 per call (chunk larger prompts).  Deterministic. */
+ * Weight tiles are dequantised to fp16 (value fp16_RNE(s*q)) in registers
+ * and fed to fp16 MFMA with fp32 accumulation; X tiles go through LDS.
+ * m >= 1 (m == 1 runs the GEMV); m <= 65536 per call (chunk larger
+ * prompts).  Deterministic. */
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream);
 
 /* Host-only: workspace bytes qmoe_grouped_gemm needs for m tokens. */

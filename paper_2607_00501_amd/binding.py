@@ -25,7 +25,7 @@ STATUS = {0: "QM_OK", 1: "QM_EINVAL", 2: "QM_ESHAPE", 3: "QM_EALIGN", 4: "QM_EFO
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqmatmul.so")
 
 EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "qm_repack",
-           "qmatmul_gemv", "qmatmul_gemm", "qmoe_workspace_bytes", "qmoe_route",
+           "qmatmul_gemv", "qmatmul_gemv_grouped", "qmatmul_gemm", "qmoe_workspace_bytes", "qmoe_route",
            "qmoe_grouped_gemm", "qm_device_config")
 
 
@@ -61,6 +61,7 @@ def lib() -> ctypes.CDLL:
             "qm_dequantise": [W, vp, vp],
             "qm_repack": [W, W, vp],
             "qmatmul_gemv": [W, vp, vp, vp],
+            "qmatmul_gemv_grouped": [i32, W, ctypes.POINTER(vp), ctypes.POINTER(vp), vp],
             "qmatmul_gemm": [W, vp, i64, vp, vp],
             "qmoe_workspace_bytes": [i64, i32, i32, i64, i64, ctypes.POINTER(sz)],
             "qmoe_route": [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp],
@@ -162,6 +163,32 @@ def qmatmul_gemv(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None
         out = torch.empty(w.n, dtype=torch.float32, device=x.device)
     _check(lib().qmatmul_gemv(ctypes.byref(w.c()), _ptr(x), _ptr(out), _stream(stream)))
     return out
+
+
+GEMV_GROUP_MAX = 8
+
+
+def gemv_group_args(ws, xs, outs):
+    """Marshals a grouped GEMV call: (count, descriptor array, x pointer
+    array, y pointer array); keep the returned tuple alive while in use."""
+    n = len(ws)
+    descs = (CQWeight * n)(*[w.c() for w in ws])
+    xp = (ctypes.c_void_p * n)(*[t.data_ptr() for t in xs])
+    yp = (ctypes.c_void_p * n)(*[t.data_ptr() for t in outs])
+    return n, descs, xp, yp
+
+
+def qmatmul_gemv_grouped(ws, xs, outs=None, stream=None):
+    """Independent GEMVs y_i = W_i' x_i with one k, in one launch; xs may repeat
+    a tensor (shared input).  Returns the list of fp32 outputs."""
+    assert len(ws) == len(xs)
+    for w, x in zip(ws, xs):
+        assert x.dtype == torch.float16 and x.is_contiguous() and x.numel() == w.k
+    if outs is None:
+        outs = [torch.empty(w.n, dtype=torch.float32, device=x.device) for w, x in zip(ws, xs)]
+    n, descs, xp, yp = gemv_group_args(ws, xs, outs)
+    _check(lib().qmatmul_gemv_grouped(n, descs, xp, yp, _stream(stream)))
+    return outs
 
 
 def qmatmul_gemm(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):

@@ -180,6 +180,39 @@ qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* s
                   "qmatmul_gemv");
 }
 
+qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_t* const* x, float* const* y,
+                               void* stream) {
+  static_assert(QM_GEMV_GROUP_MAX == kGemvGroupMax, "group size");
+  if (count < 1 || count > QM_GEMV_GROUP_MAX)
+    return fail(QM_ESHAPE, "qmatmul_gemv_grouped: count=%d must be in [1, %d]", count, QM_GEMV_GROUP_MAX);
+  if (!w || !x || !y) return fail(QM_EINVAL, "qmatmul_gemv_grouped: null array");
+  GemvGroup g{};
+  g.count = count;
+  for (int i = 0; i < count; ++i) {
+    qm_status st = check_weight(&w[i], "qmatmul_gemv_grouped(w[i])");
+    if (st != QM_OK) return st;
+    if (w[i].layout != QM_LAYOUT_DEVICE)
+      return fail(QM_ELAYOUT, "qmatmul_gemv_grouped: w[%d] must be in DEVICE layout", i);
+    if (w[i].batch != 1) return fail(QM_ESHAPE, "qmatmul_gemv_grouped: w[%d] batch must be 1", i);
+    if (w[i].format != w[0].format) return fail(QM_EFORMAT, "qmatmul_gemv_grouped: formats differ");
+    if (w[i].k != w[0].k) return fail(QM_ESHAPE, "qmatmul_gemv_grouped: k differs between entries");
+    if (w[i].n > INT32_MAX / 2) return fail(QM_ESHAPE, "qmatmul_gemv_grouped: n too large");
+    if (w[i].n > 0 && (!x[i] || !y[i])) return fail(QM_EINVAL, "qmatmul_gemv_grouped: null x[%d] or y[%d]", i, i);
+    if (!aligned16(x[i])) return fail(QM_EALIGN, "qmatmul_gemv_grouped: x[%d] must be 16-byte aligned", i);
+    if (!aligned4(y[i])) return fail(QM_EALIGN, "qmatmul_gemv_grouped: y[%d] must be 4-byte aligned", i);
+    g.q[i] = static_cast<const uint8_t*>(w[i].qdata);
+    g.s[i] = w[i].scales;
+    g.x[i] = x[i];
+    g.y[i] = y[i];
+    g.n[i] = static_cast<int>(w[i].n);
+  }
+  const DeviceInfo* d;
+  qm_status st;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_gemv_group(w[0].format, g, w[0].k, d->cu_count, static_cast<hipStream_t>(stream)),
+                  "qmatmul_gemv_grouped");
+}
+
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream) {
   qm_status st = check_weight(w, "qmatmul_gemm(w)");
   if (st != QM_OK) return st;

@@ -186,12 +186,11 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
 // lanes, then a fixed-order sum over wavefronts in LDS.
 constexpr int kSubU = 8;
 
+// One workgroup's share of one matrix: `block` of `nblocks` = N/SUBR.
 template <int FMT, int SUBR, int WAVES, bool XLDS>
-__global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(const uint8_t* __restrict__ q,
-                                                              const uint16_t* __restrict__ s,
-                                                              const uint16_t* __restrict__ x,
-                                                              float* __restrict__ y, int n_rows,
-                                                              int groups) {
+__device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
+                                              const uint16_t* __restrict__ x, float* __restrict__ y, int n_rows,
+                                              int groups, int64_t block, int64_t nblocks) {
   constexpr int CL = 64 / SUBR;
   constexpr int NW = FMT == QM_Q4_G32 ? 1 : 2;
   constexpr int U = kSubU;
@@ -204,7 +203,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(const uint8_t* __r
   // (and of x): keep them on one XCD so each line is fetched once.
   int64_t panel;
   int sub;
-  xcd_group_member(blockIdx.x, gridDim.x / CL, CL, &panel, &sub);
+  xcd_group_member(block, nblocks / CL, CL, &panel, &sub);
   const int row = sub * SUBR + r;                     // row inside the panel
   const int64_t ch0 = panel * groups;
   const int stride = WAVES * CL;
@@ -281,29 +280,47 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(const uint8_t* __r
   }
 }
 
+// A group of independent GEMVs with one K in one launch: the workgroup
+// ranges of the matrices follow each other (each but the last rounded up to
+// a multiple of 8, so every matrix starts on XCD 0 and keeps the XCD
+// grouping of its panels); a workgroup finds its matrix by a uniform scan.
+template <int FMT, int SUBR, int WAVES, bool XLDS>
+__global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(GemvGroup g) {
+  int i = 0;
+  while (i + 1 < g.count && static_cast<int>(blockIdx.x) >= g.start[i + 1]) ++i;
+  const int64_t local = static_cast<int64_t>(blockIdx.x) - g.start[i];
+  const int64_t nb = padded_rows(g.n[i]) / SUBR;
+  if (local >= nb) return;                             // padding workgroup (whole group exits)
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(g.q[i], g.s[i], g.x[i], g.y[i], g.n[i], g.groups, local, nb);
+}
+
 template <int FMT, int SUBR, bool XLDS>
-hipError_t launch_sub_waves(int waves, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
-                            int64_t n, int64_t groups, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>(padded_rows(n) / SUBR));
-  const size_t lds = XLDS ? static_cast<size_t>(groups) * 64 : 0;
-  const int ni = static_cast<int>(n), gi = static_cast<int>(groups);
+hipError_t launch_sub_waves(int waves, const GemvGroup& g, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(g.start[g.count]));
+  const size_t lds = XLDS ? static_cast<size_t>(g.groups) * 64 : 0;
   switch (waves) {
-    case 1: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 1, XLDS>), grid, dim3(64), lds, st, q, s, x, y, ni, gi); break;
-    case 2: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 2, XLDS>), grid, dim3(128), lds, st, q, s, x, y, ni, gi); break;
-    case 4: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 4, XLDS>), grid, dim3(256), lds, st, q, s, x, y, ni, gi); break;
-    default: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, q, s, x, y, ni, gi); break;
+    case 1: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 1, XLDS>), grid, dim3(64), lds, st, g); break;
+    case 2: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 2, XLDS>), grid, dim3(128), lds, st, g); break;
+    case 4: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 4, XLDS>), grid, dim3(256), lds, st, g); break;
+    default: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, g); break;
   }
   return hipGetLastError();
 }
 
 template <int FMT, bool XLDS>
-hipError_t launch_sub(const GemvPlan& plan, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
-                      int64_t n, int64_t groups, hipStream_t st) {
+hipError_t launch_sub(const GemvPlan& plan, GemvGroup& g, hipStream_t st) {
+  int start = 0;
+  for (int i = 0; i < g.count; ++i) {
+    g.start[i] = start;
+    const int nb = static_cast<int>(padded_rows(g.n[i]) / plan.subr);
+    start += i + 1 < g.count ? (nb + kXcds - 1) / kXcds * kXcds : nb;
+  }
+  g.start[g.count] = start;
   switch (plan.subr) {
-    case 4: return launch_sub_waves<FMT, 4, XLDS>(plan.waves, q, s, x, y, n, groups, st);
-    case 8: return launch_sub_waves<FMT, 8, XLDS>(plan.waves, q, s, x, y, n, groups, st);
-    case 16: return launch_sub_waves<FMT, 16, XLDS>(plan.waves, q, s, x, y, n, groups, st);
-    default: return launch_sub_waves<FMT, 32, XLDS>(plan.waves, q, s, x, y, n, groups, st);
+    case 4: return launch_sub_waves<FMT, 4, XLDS>(plan.waves, g, st);
+    case 8: return launch_sub_waves<FMT, 8, XLDS>(plan.waves, g, st);
+    case 16: return launch_sub_waves<FMT, 16, XLDS>(plan.waves, g, st);
+    default: return launch_sub_waves<FMT, 32, XLDS>(plan.waves, g, st);
   }
 }
 
@@ -314,8 +331,10 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
   const int64_t groups = k / kGroup;
   const GemvPlan plan = gemv_plan(FMT, n, k, cu_count);
   if (plan.subr < kPanel) {
-    return plan.xlds ? launch_sub<FMT, true>(plan, q, s, x, y, n, groups, st)
-                     : launch_sub<FMT, false>(plan, q, s, x, y, n, groups, st);
+    GemvGroup g{};
+    g.q[0] = q; g.s[0] = s; g.x[0] = x; g.y[0] = y;
+    g.n[0] = static_cast<int>(n); g.count = 1; g.groups = static_cast<int>(groups);
+    return plan.xlds ? launch_sub<FMT, true>(plan, g, st) : launch_sub<FMT, false>(plan, g, st);
   }
   const int waves = plan.waves;
   const int cpw = static_cast<int>((groups + waves - 1) / waves);
@@ -385,6 +404,25 @@ GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count) {
   p.waves = 8;
   p.xlds = k <= 4096 ? 1 : 0;
   return p;
+}
+
+hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count, hipStream_t st) {
+  int64_t rows = 0;
+  for (int i = 0; i < g.count; ++i) rows += padded_rows(g.n[i]);
+  if (rows == 0) return hipSuccess;
+  const GemvPlan plan = gemv_plan(fmt, rows, k, cu_count);
+  if (plan.subr == kPanel) {
+    // Enough rows for the panel kernel: one launch per matrix.
+    for (int i = 0; i < g.count; ++i) {
+      const hipError_t e = launch_gemv(fmt, g.q[i], g.s[i], g.x[i], g.y[i], g.n[i], k, cu_count, st);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  g.groups = static_cast<int>(k / kGroup);
+  if (fmt == QM_Q4_G32)
+    return plan.xlds ? launch_sub<QM_Q4_G32, true>(plan, g, st) : launch_sub<QM_Q4_G32, false>(plan, g, st);
+  return plan.xlds ? launch_sub<QM_Q8_G32, true>(plan, g, st) : launch_sub<QM_Q8_G32, false>(plan, g, st);
 }
 
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,

@@ -63,6 +63,19 @@ hipError_t launch_dequantise(int32_t fmt, int32_t layout, const uint8_t* q, cons
 hipError_t launch_repack(int32_t fmt, int32_t src_layout, const uint8_t* sq, const uint16_t* ss,
                          uint8_t* dq, uint16_t* ds, int64_t batch, int64_t n, int64_t k,
                          hipStream_t st);
+// Up to kGemvGroupMax independent GEMVs with one K and one format.
+constexpr int kGemvGroupMax = 8;
+struct GemvGroup {
+  const uint8_t* q[kGemvGroupMax];
+  const uint16_t* s[kGemvGroupMax];
+  const uint16_t* x[kGemvGroupMax];
+  float* y[kGemvGroupMax];
+  int n[kGemvGroupMax];
+  int start[kGemvGroupMax + 1];   // first workgroup of each matrix (set by the launcher)
+  int count;
+  int groups;                     // K / 32
+};
+hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count, hipStream_t st);
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
                        int64_t n, int64_t k, int cu_count, hipStream_t st);
 hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,

@@ -140,3 +140,30 @@ def test_error_text_is_thread_local():
     assert seen["before"] == ""
     assert "layout" in seen["after"]
     assert B.qm_last_error() == main_msg and "format" in main_msg
+
+
+def test_gemv_grouped_validation():
+    L = B.lib()
+    x0, y0 = 0x30000, 0x40000
+
+    def call(ws, xs=None, ys=None, count=None):
+        n = len(ws)
+        descs = (B.CQWeight * max(n, 1))(*ws)
+        xs = xs if xs is not None else [x0] * n
+        ys = ys if ys is not None else [y0 + 0x1000 * i for i in range(n)]
+        xp = (ctypes.c_void_p * max(n, 1))(*xs)
+        yp = (ctypes.c_void_p * max(n, 1))(*ys)
+        return L.qmatmul_gemv_grouped(n if count is None else count, descs, xp, yp, None)
+
+    w = _fake_weight()
+    assert call([w], count=0) == 2                                     # count < 1
+    assert call([w] * 9) == 2                                          # count > 8
+    assert L.qmatmul_gemv_grouped(1, None, None, None, None) == 1      # null arrays
+    assert call([w, _fake_weight(fmt=2)]) == 4                         # formats differ
+    assert call([w, _fake_weight(k=96)]) == 2                          # k differs
+    assert call([w, _fake_weight(layout=0)]) == 5                      # not DEVICE layout
+    assert call([w, _fake_weight(batch=2)]) == 2                       # batch != 1
+    assert call([w, w], xs=[x0, x0 + 4]) == 3                          # x[1] misaligned
+    assert call([w, w], ys=[y0, y0 + 2]) == 3                          # y[1] misaligned
+    assert call([w, w], xs=[x0, 0]) == 1                               # null x[1]
+    assert B.qm_last_error()
