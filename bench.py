@@ -78,6 +78,53 @@ def build_decode_stack(model, cfg_id, fmt, torch, B, inputs, workloads, want_fp3
     return calls, nbytes
 
 
+class GroupCall:
+    """One pre-marshalled qmatmul_gemv_grouped call."""
+
+    def __init__(self, lib, B, wds, xs, ys):
+        self.lib, self.keep = lib, (wds, xs, ys)
+        self.args = B.gemv_group_args(wds, xs, ys)
+
+    def __call__(self, stream):
+        n, descs, xp, yp = self.args
+        st = self.lib.qmatmul_gemv_grouped(n, descs, xp, yp, stream)
+        if st != 0:
+            raise RuntimeError(self.lib.qm_last_error().decode())
+
+
+GROUPS = (("q", "k", "v"), ("o",), ("gate", "up"), ("down",))
+
+
+def build_grouped_stack(model, cfg_id, fmt, torch, B, inputs, workloads):
+    """The same decode step with one launch per group of projections that
+    read the same input (q/k/v, o, gate/up, down per layer; the lm_head)."""
+    lib = B.lib()
+    shapes = {name: (k, n) for name, k, n in model["layer"]}
+    calls, nbytes = [], 0
+    for layer in range(model["layers"]):
+        for gi, group in enumerate(GROUPS):
+            k = shapes[group[0]][0]
+            x = inputs.activations_dev(inputs.seed_for(cfg_id, layer, "x", 100 + gi), (k,))
+            wds, ys = [], []
+            for name in group:
+                kk, n = shapes[name]
+                w = inputs.weights_dev(inputs.seed_for(cfg_id, layer, name), (n, kk))
+                wds.append(B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE))
+                del w
+                ys.append(torch.empty(n, dtype=torch.float32, device="cuda"))
+                nbytes += workloads.q4_bytes(kk, n) if fmt == B.Q4_G32 else workloads.q8_bytes(kk, n)
+            calls.append(GroupCall(lib, B, wds, [x] * len(group), ys))
+    k, n = model["lm_head"]
+    w = inputs.weights_dev(inputs.seed_for(cfg_id, model["layers"], "lm_head"), (n, k))
+    wd = B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE)
+    del w
+    x = inputs.activations_dev(inputs.seed_for(cfg_id, model["layers"], "x"), (k,))
+    calls.append(GemvCall(lib, wd, x, torch.empty(n, dtype=torch.float32, device="cuda")))
+    nbytes += workloads.q4_bytes(k, n) if fmt == B.Q4_G32 else workloads.q8_bytes(k, n)
+    torch.cuda.synchronize()
+    return calls, nbytes
+
+
 def capture(torch, fn):
     """Capture fn(stream_ptr) into a graph on a side stream; returns the graph."""
     s = torch.cuda.Stream()
@@ -218,6 +265,20 @@ def extra_workloads(torch, B, inputs, workloads, steps, warmup):
                                        "weight_GBps_graph": round(workloads.q4_bytes(1024, 1024) / us / 1e3, 2)}
     log(f"config single gemv: {us:.2f} us/call")
     del g
+
+    # Grouped dispatch (qmatmul_gemv_grouped): the Qwen3-0.6B and Llama-3.2-3B
+    # Q4 steps with q/k/v and gate/up each in one launch (113 launches/token).
+    for model, cfg_id, tag in ((workloads.QWEN3_06B, 1, "qwen3-0.6b"), (workloads.LLAMA32_3B, 2, "llama3.2-3b")):
+        calls, nbytes = build_grouped_stack(model, cfg_id, B.Q4_G32, torch, B, inputs, workloads)
+        g = capture(torch, lambda s: [c(s) for c in calls])
+        t, _ = time_graph(torch, g, steps, warmup)
+        out[f"{tag}_decode_q4_grouped_dispatch"] = {
+            "launches_per_token": len(calls), "tokens_per_s": round(steps / t, 2),
+            "ms_per_token": round(t / steps * 1e3, 4), "weight_GBps": round(nbytes * steps / t / 1e9, 2),
+            "frac_hbm_peak": round(nbytes * steps / t / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"{tag} grouped dispatch: {out[f'{tag}_decode_q4_grouped_dispatch']}")
+        del g, calls
+        torch.cuda.empty_cache()
 
     # Llama-3.2-3B decode stacks, Q4 and Q8
     for fmt, tag in ((B.Q4_G32, "q4"), (B.Q8_G32, "q8")):

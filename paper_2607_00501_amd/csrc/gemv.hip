@@ -280,29 +280,71 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
   }
 }
 
+template <int FMT, int SUBR, int WAVES, bool XLDS>
+__global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(const uint8_t* __restrict__ q,
+                                                              const uint16_t* __restrict__ s,
+                                                              const uint16_t* __restrict__ x,
+                                                              float* __restrict__ y, int n_rows,
+                                                              int groups) {
+  // All kernel arguments in one batch of scalar loads (one round trip).
+  asm volatile("" ::"s"(q), "s"(s), "s"(x), "s"(y), "s"(n_rows), "s"(groups));
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, x, y, n_rows, groups, blockIdx.x, gridDim.x);
+}
+
 // A group of independent GEMVs with one K in one launch: the workgroup
 // ranges of the matrices follow each other (each but the last rounded up to
 // a multiple of 8, so every matrix starts on XCD 0 and keeps the XCD
-// grouping of its panels); a workgroup finds its matrix by a uniform scan.
+// grouping of its panels).  Every field of the group is read with
+// independent scalar loads and the workgroup's entry is picked by selects,
+// so the kernel arguments cost one memory round trip, as for one matrix.
 template <int FMT, int SUBR, int WAVES, bool XLDS>
-__global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(GemvGroup g) {
-  int i = 0;
-  while (i + 1 < g.count && static_cast<int>(blockIdx.x) >= g.start[i + 1]) ++i;
-  const int64_t local = static_cast<int64_t>(blockIdx.x) - g.start[i];
-  const int64_t nb = padded_rows(g.n[i]) / SUBR;
+__global__ __launch_bounds__(WAVES * 64) void gemv_sub_group_kernel(GemvGroup g) {
+  const int b = static_cast<int>(blockIdx.x);
+  const uint8_t* q = g.q[0];
+  const uint16_t* s = g.s[0];
+  const uint16_t* x = g.x[0];
+  float* y = g.y[0];
+  int n = g.n[0], first = 0;
+#pragma unroll
+  for (int j = 1; j < kGemvGroupMax; ++j) {
+    const bool in = j < g.count && b >= g.start[j];
+    q = in ? g.q[j] : q;
+    s = in ? g.s[j] : s;
+    x = in ? g.x[j] : x;
+    y = in ? g.y[j] : y;
+    n = in ? g.n[j] : n;
+    first = in ? g.start[j] : first;
+  }
+  int groups = g.groups;
+  // Pin every selected field before the branch below, so that the compiler
+  // cannot sink their loads past it (one round trip instead of three).
+  asm volatile("" ::"s"(q), "s"(s), "s"(x), "s"(y), "s"(n), "s"(first), "s"(groups));
+  const int64_t local = b - first;
+  const int64_t nb = padded_rows(n) / SUBR;
   if (local >= nb) return;                             // padding workgroup (whole group exits)
-  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(g.q[i], g.s[i], g.x[i], g.y[i], g.n[i], g.groups, local, nb);
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, x, y, n, groups, local, nb);
 }
 
 template <int FMT, int SUBR, bool XLDS>
 hipError_t launch_sub_waves(int waves, const GemvGroup& g, hipStream_t st) {
   const dim3 grid(static_cast<unsigned>(g.start[g.count]));
   const size_t lds = XLDS ? static_cast<size_t>(g.groups) * 64 : 0;
+  if (g.count == 1) {
+    const auto q = g.q[0]; const auto s = g.s[0]; const auto x = g.x[0]; const auto y = g.y[0];
+    const int n = g.n[0], gi = g.groups;
+    switch (waves) {
+      case 1: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 1, XLDS>), grid, dim3(64), lds, st, q, s, x, y, n, gi); break;
+      case 2: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 2, XLDS>), grid, dim3(128), lds, st, q, s, x, y, n, gi); break;
+      case 4: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 4, XLDS>), grid, dim3(256), lds, st, q, s, x, y, n, gi); break;
+      default: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, q, s, x, y, n, gi); break;
+    }
+    return hipGetLastError();
+  }
   switch (waves) {
-    case 1: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 1, XLDS>), grid, dim3(64), lds, st, g); break;
-    case 2: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 2, XLDS>), grid, dim3(128), lds, st, g); break;
-    case 4: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 4, XLDS>), grid, dim3(256), lds, st, g); break;
-    default: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, g); break;
+    case 1: hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 1, XLDS>), grid, dim3(64), lds, st, g); break;
+    case 2: hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 2, XLDS>), grid, dim3(128), lds, st, g); break;
+    case 4: hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 4, XLDS>), grid, dim3(256), lds, st, g); break;
+    default: hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, g); break;
   }
   return hipGetLastError();
 }
