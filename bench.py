@@ -245,9 +245,20 @@ def cpu_baseline(budget_s: float):
 
 # ------------------------------------------------------------ extras
 
-def extra_workloads(torch, B, inputs, workloads, steps, warmup):
+def extra_workloads(torch, B, inputs, workloads, steps, warmup, which="all"):
     out = {}
     lib = B.lib()
+    if which in ("all", "decode"):
+        out.update(extra_decode(torch, B, inputs, workloads, steps, warmup, lib))
+    if which in ("all", "prefill"):
+        out.update(extra_prefill(torch, B, inputs, workloads, steps, warmup, lib))
+    if which in ("all", "moe"):
+        out.update(extra_moe(torch, B, inputs, workloads, steps, warmup, lib))
+    return out
+
+
+def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
+    out = {}
 
     # single Q4 GEMV 1024 x 1024
     cfg = workloads.SINGLE_GEMV
@@ -303,6 +314,11 @@ def extra_workloads(torch, B, inputs, workloads, steps, warmup):
         del g, calls
         torch.cuda.empty_cache()
 
+    return out
+
+
+def extra_prefill(torch, B, inputs, workloads, steps, warmup, lib):
+    out = {}
     # Llama-3.2-1B prefill GEMM stacks
     model = workloads.LLAMA32_1B_PREFILL
     wds = []
@@ -333,6 +349,11 @@ def extra_workloads(torch, B, inputs, workloads, steps, warmup):
     del wds
     torch.cuda.empty_cache()
 
+    return out
+
+
+def extra_moe(torch, B, inputs, workloads, steps, warmup, lib):
+    out = {}
     # Qwen3-30B-A3B MoE layer
     cfg = workloads.QWEN3_30B_A3B_MOE
     E, K, H, I = cfg["experts"], cfg["top_k"], cfg["hidden"], cfg["inter"]
@@ -413,7 +434,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--extra", choices=["all", "none"], default="all")
+    ap.add_argument("--extra", choices=["all", "none", "decode", "prefill", "moe"], default="all",
+                    help="other workloads to time after the headline step (subsets for profiling)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -473,10 +495,10 @@ def main():
     del g
 
     extra = {}
-    if args.extra == "all":
+    if args.extra != "none":
         del calls
         torch.cuda.empty_cache()
-        extra = extra_workloads(torch, B, inputs, workloads, args.steps, args.warmup)
+        extra = extra_workloads(torch, B, inputs, workloads, args.steps, args.warmup, args.extra)
 
     cpu = cpu_baseline(args.cpu_seconds)
     log(f"cpu baseline: {cpu}")
