@@ -247,15 +247,23 @@ hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
   g.n_experts = a.n_experts; g.top_k = a.top_k; g.M = A;
   // gate/up + SwiGLU: A = x rows gathered per assignment, N = inter, K = hidden
   g.q = a.gq; g.s = a.gs; g.q2 = a.uq; g.s2 = a.us; g.a = a.x; g.h = a.h; g.N = a.inter; g.K = a.hidden;
-  const unsigned ny1 = static_cast<unsigned>((a.inter + 64 * WN - 1) / (64 * WN));
-  hipLaunchKernelGGL((qgemm_kernel<BMG, WN, WKG, QgMode::kMoeGateUp, DG>), dim3(tiles(BMG), ny1), dim3(WN * WKG * 64), 0,
+  // 1-D grids over (row tile, column block) units, rounded up to whole
+  // rounds of XCD chunks (the XCD mapping is done in the kernel).
+  auto grid = [&](int bm, int64_t n) {
+    const int64_t ny = (padded_rows(n) + 64 * WN - 1) / (64 * WN);
+    const int64_t round = static_cast<int64_t>(kXcds) * qg::kMoeChunkTiles * ny;
+    const int64_t units = static_cast<int64_t>(tiles(bm)) * ny;
+    return dim3(static_cast<unsigned>((units + round - 1) / round * round));
+  };
+  g.tiles = tiles(BMG);
+  hipLaunchKernelGGL((qgemm_kernel<BMG, WN, WKG, QgMode::kMoeGateUp, DG>), grid(BMG, a.inter), dim3(WN * WKG * 64), 0,
                      st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // down, scaled by the gate weight and scattered to the assignment slot
   g.q = a.dq; g.s = a.ds; g.q2 = nullptr; g.s2 = nullptr; g.a = a.h; g.yp = a.yp; g.N = a.hidden; g.K = a.inter;
-  const unsigned ny2 = static_cast<unsigned>((a.hidden + 64 * WN - 1) / (64 * WN));
-  hipLaunchKernelGGL((qgemm_kernel<BMD, WN, WKD, QgMode::kMoeDown, DD>), dim3(tiles(BMD), ny2), dim3(WN * WKD * 64), 0,
+  g.tiles = tiles(BMD);
+  hipLaunchKernelGGL((qgemm_kernel<BMD, WN, WKD, QgMode::kMoeDown, DD>), grid(BMD, a.hidden), dim3(WN * WKD * 64), 0,
                      st, g);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

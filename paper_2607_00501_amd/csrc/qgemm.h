@@ -55,6 +55,7 @@ struct QgemmArgs {
   uint16_t* h;                             // kMoeGateUp output [M][N] fp16 (bucket order)
   uint16_t* yp;                            // kMoeDown output [M][N] fp16 (assignment order)
   int32_t n_experts, top_k;
+  int64_t tiles;                           // MoE: bound on the number of (expert, row tile) pairs
 };
 
 namespace qg {
@@ -62,6 +63,7 @@ namespace qg {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBK = 64;                 // K per step (two quantisation groups)
+constexpr int kMoeChunkTiles = 4;       // MoE row tiles per XCD chunk
 constexpr int kRow = kBK + 8;           // LDS row stride in halves (16-byte pad)
 
 __device__ inline uint32_t and_or_v(uint32_t a, uint32_t mask_v, uint32_t or_s) {
@@ -158,13 +160,20 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     rows = static_cast<int>(min<int64_t>(BM, p.M - row0));
     col_block = blockIdx.x;
   } else {
+    // 1-D grid over (row tile, column block) units, row-tile major, dealt to
+    // the XCDs in chunks of kMoeChunkTiles row tiles: the row tiles of one
+    // expert (same weight panels) and the column blocks of one tile (same A
+    // rows) mostly share an L2.
+    const int64_t ny = (npad + 64 * WN - 1) / (64 * WN);
+    const int64_t u = xcd_chunked(blockIdx.x, kMoeChunkTiles * ny);
+    if (u >= p.tiles * ny) return;                        // whole workgroup, before any barrier
     __shared__ int sh_e, sh_tile;
-    find_tile(p.counts, p.n_experts, BM, blockIdx.x, &sh_e, &sh_tile);
+    find_tile(p.counts, p.n_experts, BM, static_cast<int>(u / ny), &sh_e, &sh_tile);
     expert = sh_e;
     if (expert < 0) return;
     row0 = p.offsets[expert] + static_cast<int64_t>(sh_tile) * BM;
     rows = static_cast<int>(min<int64_t>(BM, p.offsets[expert + 1] - row0));
-    col_block = blockIdx.y;
+    col_block = u % ny;
   }
   const int64_t n_wave = col_block * (64 * WN) + 64 * wn;
   const bool cols_ok = n_wave < npad;

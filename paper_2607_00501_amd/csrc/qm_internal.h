@@ -63,6 +63,16 @@ hipError_t launch_dequantise(int32_t fmt, int32_t layout, const uint8_t* q, cons
 hipError_t launch_repack(int32_t fmt, int32_t src_layout, const uint8_t* sq, const uint16_t* ss,
                          uint8_t* dq, uint16_t* ds, int64_t batch, int64_t n, int64_t k,
                          hipStream_t st);
+// Linear workgroup index i (XCD i % 8) -> work unit u, dealing chunks of
+// `chunk` consecutive units to the XCDs in turn: the units of one chunk
+// (which share operands) run on one XCD, in order, and share its L2, while
+// the chunks, and any tail of empty units, spread evenly over the XCDs.  A
+// bijection on [0, n) for n a multiple of 8 * chunk.
+__host__ __device__ inline int64_t xcd_chunked(int64_t i, int64_t chunk) {
+  const int64_t xcd = i % kXcds, j = i / kXcds;
+  return ((j / chunk) * kXcds + xcd) * chunk + j % chunk;
+}
+
 // Up to kGemvGroupMax independent GEMVs with one K and one format.
 constexpr int kGemvGroupMax = 8;
 struct GemvGroup {
