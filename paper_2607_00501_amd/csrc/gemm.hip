@@ -28,8 +28,10 @@ hipError_t launch_tile(const uint8_t* q, const uint16_t* s, const uint16_t* x, f
 // Per-chip tile choice by M regime (Sec. 3.4: tiles tuned to sequence
 // length), fitted to a per-shape sweep on MI355X (256 CUs): the 128 x 256
 // tile when it gives at least two workgroups per CU, else the 64 x 256 tile
-// when it gives one per CU, else one panel per workgroup with split-K over
-// up to 4 wavefronts (at least 8 K steps per slice).
+// when it gives one per CU; else one 64-column panel per K slice with
+// split-K over as many one-wavefront slices as keep >= 8 K steps each (at
+// most 8), in 64-row tiles if that gives 8 wavefronts per CU, else 32-row
+// tiles.
 GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count) {
   // Tuning sweeps only: QM_GEMM_PLAN="bm,wn,wk" forces the plan.
   static const GemmPlan forced = [] {
@@ -37,19 +39,20 @@ GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count) {
     if (const char* e = std::getenv("QM_GEMM_PLAN")) std::sscanf(e, "%d,%d,%d", &f.bm, &f.wn, &f.wk);
     return f;
   }();
-  if ((forced.bm == 64 || forced.bm == 128) && (forced.wn == 1 || forced.wn == 2 || forced.wn == 4) &&
-      (forced.wk == 1 || forced.wk == 2 || forced.wk == 4)) {
+  if ((forced.bm == 32 || forced.bm == 64 || forced.bm == 128) && (forced.wn == 1 || forced.wn == 2 || forced.wn == 4) &&
+      (forced.wk == 1 || forced.wk == 2 || forced.wk == 4 || forced.wk == 8)) {
     GemmPlan f = forced;
-    if (f.wk > 1) { f.bm = 64; f.wn = 1; }
+    if (f.wk > 1 || f.bm == 32) { f.wn = 1; if (f.bm == 128) f.bm = 64; }
     return f;
   }
   auto blocks = [&](int bm, int wn) { return ((n + 64 * wn - 1) / (64 * wn)) * ((m + bm - 1) / bm); };
   if (blocks(128, 4) >= 2 * cu_count) return GemmPlan{128, 4, 1};
   if (blocks(64, 4) >= cu_count) return GemmPlan{64, 4, 1};
-  GemmPlan p{64, 1, 1};
   const int64_t kt = (k / kGroup + 1) / 2;
-  while (p.wk < 4 && blocks(64, 1) * p.wk < 4 * cu_count && kt / (2 * p.wk) >= 8) p.wk *= 2;
-  return p;
+  int wk = 1;
+  while (wk < 8 && kt / (2 * wk) >= 8) wk *= 2;
+  if (blocks(64, 1) * wk >= 8 * static_cast<int64_t>(cu_count)) return GemmPlan{64, 1, wk};
+  return GemmPlan{32, 1, wk};
 }
 
 const char* gemm_tile_name(int64_t m, int64_t n) {
@@ -63,17 +66,25 @@ hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, f
                        int64_t n, int64_t k, int cu_count, hipStream_t st) {
   if (n == 0) return hipSuccess;
   const GemmPlan p = gemm_plan(m, n, k, cu_count);
-  if (p.wk == 1) {
-    if (p.bm == 128) {
-      if (p.wn == 4) return launch_tile<128, 4, 1>(q, s, x, y, m, n, k, st);
-      return launch_tile<128, 2, 1>(q, s, x, y, m, n, k, st);
-    }
-    if (p.wn == 4) return launch_tile<64, 4, 1>(q, s, x, y, m, n, k, st);
-    if (p.wn == 2) return launch_tile<64, 2, 1>(q, s, x, y, m, n, k, st);
-    return launch_tile<64, 1, 1>(q, s, x, y, m, n, k, st);
+  if (p.wn == 4) {
+    if (p.bm == 128) return launch_tile<128, 4, 1>(q, s, x, y, m, n, k, st);
+    return launch_tile<64, 4, 1>(q, s, x, y, m, n, k, st);
   }
-  if (p.wk == 2) return launch_tile<64, 1, 2>(q, s, x, y, m, n, k, st);
-  return launch_tile<64, 1, 4>(q, s, x, y, m, n, k, st);
+  if (p.wn == 2) return launch_tile<64, 2, 1>(q, s, x, y, m, n, k, st);
+  if (p.bm == 64) {
+    switch (p.wk) {
+      case 1: return launch_tile<64, 1, 1>(q, s, x, y, m, n, k, st);
+      case 2: return launch_tile<64, 1, 2>(q, s, x, y, m, n, k, st);
+      case 4: return launch_tile<64, 1, 4>(q, s, x, y, m, n, k, st);
+      default: return launch_tile<64, 1, 8>(q, s, x, y, m, n, k, st);
+    }
+  }
+  switch (p.wk) {
+    case 1: return launch_tile<32, 1, 1>(q, s, x, y, m, n, k, st);
+    case 2: return launch_tile<32, 1, 2>(q, s, x, y, m, n, k, st);
+    case 4: return launch_tile<32, 1, 4>(q, s, x, y, m, n, k, st);
+    default: return launch_tile<32, 1, 8>(q, s, x, y, m, n, k, st);
+  }
 }
 
 }  // namespace qm

@@ -251,6 +251,14 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     for (int i = 0; i < C::kALoads; ++i) *reinterpret_cast<u32x4*>(dst + a_lds[i]) = ra[sl][i];
   };
 
+  // The A buffers of a K slice are written and read only by the slice's WN
+  // wavefronts.  A one-wavefront slice needs no workgroup barrier: the LDS
+  // instructions of one wavefront execute in order.
+  auto slice_sync = [&]() __attribute__((always_inline)) {
+    if constexpr (WN == 1) __builtin_amdgcn_wave_barrier();
+    else __syncthreads();
+  };
+
   float16v acc[C::kTM][2 * NB];
 #pragma unroll
   for (int a = 0; a < C::kTM; ++a)
@@ -327,7 +335,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
       }
     }
     if (t + 1 < KTs) store_a(Next{}, buf ^ 1);
-    __syncthreads();
+    slice_sync();
   };
 
   using Slots = std::make_integer_sequence<int, DEPTH>;
@@ -335,7 +343,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     (load(std::integral_constant<int, I>{}, I), ...);
   }(Slots{});
   store_a(std::integral_constant<int, 0>{}, 0);
-  __syncthreads();
+  slice_sync();
   int t = 0;
   for (; t + DEPTH <= KTs; t += DEPTH) {
     [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
@@ -348,6 +356,9 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 
   if constexpr (WK > 1) {
     // Partial sums of slices 1..WK-1 go through LDS; slice 0 adds them in order.
+    // The buffer overlaps the A tiles, which slices no longer synchronise on
+    // per K step: wait until every slice is done with them.
+    __syncthreads();
     float* red = reinterpret_cast<float*>(lds);
     constexpr int per_wave = C::kTM * 2 * NB * 16 * 64;
     if (wk > 0) {
@@ -361,6 +372,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     }
     __syncthreads();
     if (wk > 0) return;
+#pragma unroll 1
     for (int j = 1; j < WK; ++j) {
       const float* src = red + ((j - 1) * WN + wn) * per_wave;
 #pragma unroll
@@ -399,8 +411,10 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 
 }  // namespace qg
 
+// Two workgroups per CU (up to 256 VGPRs per lane) for up to 4 wavefronts
+// per workgroup, one beyond.
 template <int BM, int WN, int WK, QgMode MODE, int DEPTH = 2>
-__global__ __launch_bounds__(WN * WK * 64, 2) void qgemm_kernel(QgemmArgs p) {
+__global__ __launch_bounds__(WN * WK * 64, WN * WK <= 4 ? 2 : 1) void qgemm_kernel(QgemmArgs p) {
   qg::qgemm_body<BM, WN, WK, MODE, DEPTH>(p);
 }
 

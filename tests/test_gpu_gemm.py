@@ -19,7 +19,8 @@ def _device_weight(w_np):
 
 @pytest.mark.parametrize("m,n,k", [(2, 64, 32), (5, 65, 96), (127, 130, 160), (129, 64, 64),
                                    (64, 256, 1024), (300, 200, 2048), (513, 384, 256),
-                                   (128, 512, 2048), (33, 1000, 8192)])
+                                   (128, 512, 2048), (33, 1000, 8192),
+                                   (70, 640, 8224), (200, 4096, 4128)])   # 8-way split-K, ragged K slices
 def test_gemm_parity(m, n, k):
     w = inputs.weights_np(inputs.seed_for(3, n, "gate"), (n, k))
     x = inputs.activations_np(inputs.seed_for(3, m, "x"), (m, k))
