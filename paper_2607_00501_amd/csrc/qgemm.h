@@ -66,21 +66,26 @@ constexpr int kBK = 64;                 // K per step (two quantisation groups)
 constexpr int kMoeChunkTiles = 4;       // MoE row tiles per XCD chunk
 constexpr int kRow = kBK + 8;           // LDS row stride in halves (16-byte pad)
 
-__device__ inline uint32_t and_or_v(uint32_t a, uint32_t mask_v, uint32_t or_s) {
-  uint32_t r;
-  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(mask_v), "s"(or_s));
-  return r;
-}
+// Dequantisation constants held in registers: the 0x000F000F mask in a VGPR
+// and the fp16 magic 0x6400_6400 in an SGPR, so that (d & mask) | magic
+// selects to one v_and_or_b32 (gfx9 VOP3 takes no literal operand).  The
+// empty asm makes the values opaque once, outside the loops.
+struct DequantRegs {
+  uint32_t mask_v, magic_s;
+  __device__ DequantRegs() : mask_v(0x000F000Fu), magic_s(0x64006400u) {
+    asm volatile("" : "+v"(mask_v));
+    asm volatile("" : "+s"(magic_s));
+  }
+};
 
 // 8 offset-binary nibbles of one device-layout dword (k order 0,2,4,6 |
 // 1,3,5,7) -> 8 fp16 fp16_RNE(s*q) in natural k order.
-__device__ inline half8v dequant_dword(uint32_t d, half2v s2) {
+__device__ inline half8v dequant_dword(uint32_t d, half2v s2, const DequantRegs& c) {
   const half2v bias = {(_Float16)1032.0f, (_Float16)1032.0f};
-  const uint32_t m0 = 0x000F000Fu, magic = 0x64006400u;
   half8v out;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const half2v q = __builtin_bit_cast(half2v, and_or_v(d >> (4 * i), m0, magic)) - bias;
+    const half2v q = __builtin_bit_cast(half2v, ((d >> (4 * i)) & c.mask_v) | c.magic_s) - bias;
     const half2v v = q * s2;
     out[2 * i] = v[0];
     out[2 * i + 1] = v[1];
@@ -259,6 +264,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     else __syncthreads();
   };
 
+  const DequantRegs dq;
   float16v acc[C::kTM][2 * NB];
 #pragma unroll
   for (int a = 0; a < C::kTM; ++a)
@@ -308,8 +314,8 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     for (int a = 0; a < C::kTM; ++a) af[0][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow);
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      bq[0][j][0] = dequant_dword(bd[j][0][0], sc[j][0][0]);
-      bq[0][j][1] = dequant_dword(bd[j][1][0], sc[j][0][1]);
+      bq[0][j][0] = dequant_dword(bd[j][0][0], sc[j][0][0], dq);
+      bq[0][j][1] = dequant_dword(bd[j][1][0], sc[j][0][1], dq);
     }
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
@@ -320,8 +326,8 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
           af[nxt][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow + (ks + 1) * 16);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
-          bq[nxt][j][0] = dequant_dword(bd[j][0][ks + 1], sc[j][(ks + 1) >> 1][0]);
-          bq[nxt][j][1] = dequant_dword(bd[j][1][ks + 1], sc[j][(ks + 1) >> 1][1]);
+          bq[nxt][j][0] = dequant_dword(bd[j][0][ks + 1], sc[j][(ks + 1) >> 1][0], dq);
+          bq[nxt][j][1] = dequant_dword(bd[j][1][ks + 1], sc[j][(ks + 1) >> 1][1], dq);
         }
       }
 #pragma unroll
