@@ -402,7 +402,8 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         const int lr = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         if (lr >= rows || col >= N) continue;
         if constexpr (MODE == QgMode::kDense) {
-          p.y[(row0 + lr) * N + col] = acc[a][b][r];
+          // Y is not read again by this kernel: stream it past the caches.
+          __builtin_nontemporal_store(acc[a][b][r], p.y + (row0 + lr) * N + col);
         } else if constexpr (MODE == QgMode::kMoeGateUp) {
           const float g = acc[a][b][r];
           const float u = acc[a][2 + b][r];
