@@ -48,13 +48,18 @@ __device__ inline uint32_t stream_load_u16(const uint16_t* p) {
   return __builtin_nontemporal_load(p);
 }
 
-// v_and_or_b32 with the mask in a VGPR and the OR constant in an SGPR (gfx9
-// VOP3 takes no literal and at most one SGPR).
-__device__ inline uint32_t and_or(uint32_t a, uint32_t mask_v, uint32_t or_s) {
-  uint32_t r;
-  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(mask_v), "s"(or_s));
-  return r;
-}
+// (a & mask) | magic as one v_and_or_b32: the masks live in VGPRs and the
+// magic in an SGPR (gfx9 VOP3 takes no literal operand), made opaque once
+// per kernel by DequantConsts.
+__device__ inline uint32_t and_or(uint32_t a, uint32_t mask_v, uint32_t or_s) { return (a & mask_v) | or_s; }
+
+struct DequantConsts {
+  uint32_t m0, m1, magic;
+  __device__ DequantConsts() : m0(0x000F000Fu), m1(0x00F000F0u), magic(0x64006400u) {
+    asm volatile("" : "+v"(m0), "+v"(m1));
+    asm volatile("" : "+s"(magic));
+  }
+};
 
 // Sum over one Q4 group of q[k] * x[k] (fp32).  Dword j of the chunk holds
 // the offset-binary nibbles of k = 8j + {0,2,4,6} in bits 0-15 and of
@@ -63,11 +68,11 @@ __device__ inline uint32_t and_or(uint32_t a, uint32_t mask_v, uint32_t or_s) {
 // 20-23 land in mantissa bits 4-7 and give (1024 + 16u), i.e. 16*q after
 // subtracting 1152.  Those pairs accumulate separately and are scaled by
 // 1/16 (exact) at the end of the group.
-__device__ inline float dot_q4_chunk(const uint4 w, const uint32_t* xs, uint32_t m0, uint32_t m1) {
+__device__ inline float dot_q4_chunk(const uint4 w, const uint32_t* xs, const DequantConsts& k) {
   const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
   const half2v b1 = {(_Float16)1032.0f, (_Float16)1032.0f};
   const half2v b16 = {(_Float16)1152.0f, (_Float16)1152.0f};
-  const uint32_t magic = 0x64006400u;
+  const uint32_t m0 = k.m0, m1 = k.m1, magic = k.magic;
   float acc1 = 0.0f, acc16 = 0.0f;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -106,7 +111,7 @@ __device__ inline float dot_q8_half(const uint4 w, const uint32_t* xs) {
 template <int FMT, int U>
 __device__ inline float gemv_chunks(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
                                     const uint32_t* __restrict__ xw, int64_t ch0, int c, int lane,
-                                    uint32_t m0, uint32_t m1) {
+                                    const DequantConsts& k) {
   constexpr int NW = FMT == QM_Q4_G32 ? 1 : 2;
   uint4 wv[U][NW];
   uint32_t sv[U];
@@ -127,7 +132,7 @@ __device__ inline float gemv_chunks(const uint8_t* __restrict__ q, const uint16_
   for (int u = 0; u < U; ++u) {
     const uint32_t* xs = xw + (c + u) * 16;   // wavefront-uniform: scalar loads
     float d;
-    if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][0], xs, m0, m1);
+    if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][0], xs, k);
     else d = dot_q8_half(wv[u][0], xs) + dot_q8_half(wv[u][NW - 1], xs + 8);
     acc = fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sv[u]))), d, acc);
   }
@@ -147,14 +152,12 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
   const int c1 = min(groups, c0 + chunks_per_wave);
   const int64_t ch0 = panel * groups;                 // first (panel, group) chunk index
   const uint32_t* xw = reinterpret_cast<const uint32_t*>(x);
-  // Loop-invariant masks (the asm constraint keeps them in VGPRs).
-  const uint32_t m0 = 0x000F000Fu;
-  const uint32_t m1 = 0x00F000F0u;
+  const DequantConsts dk;
 
   float acc = 0.0f;
   int c = c0;
-  for (; c + U <= c1; c += U) acc += gemv_chunks<FMT, U>(q, s, xw, ch0, c, lane, m0, m1);
-  for (; c < c1; ++c) acc += gemv_chunks<FMT, 1>(q, s, xw, ch0, c, lane, m0, m1);
+  for (; c + U <= c1; c += U) acc += gemv_chunks<FMT, U>(q, s, xw, ch0, c, lane, dk);
+  for (; c < c1; ++c) acc += gemv_chunks<FMT, 1>(q, s, xw, ch0, c, lane, dk);
 
   if (WAVES == 1) {
     const int64_t n = panel * 64 + lane;
@@ -209,7 +212,7 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
   const int stride = WAVES * CL;
   const int first = wave * CL + cl;
   const int iters = (groups + U * stride - 1) / (U * stride);
-  const uint32_t m0 = 0x000F000Fu, m1 = 0x00F000F0u;
+  const DequantConsts dk;
   const uint4* xg = reinterpret_cast<const uint4*>(x);
 
   float acc = 0.0f;
@@ -254,7 +257,7 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
           }
         }
         float d;
-        if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][0], xv, m0, m1);
+        if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][0], xv, dk);
         else d = dot_q8_half(wv[u][0], xv) + dot_q8_half(wv[u][NW - 1], xv + 8);
         acc = fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sv[u]))), d, acc);
       }
