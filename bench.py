@@ -507,12 +507,13 @@ def main():
         "metric": "Q4 decode GEMV weight GB/s (% of HBM peak); prefill/MoE GEMM TFLOP/s",
         "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(secs / args.steps * 1e3, 5), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f16 (Q4 weights dequantised in registers, fp32 accumulation)",
+        "vs_baseline": None, "dtype": "f16",
         "data": "synthetic (seeded N(0,0.02^2) weights quantised on the GPU, N(0,1) fp16 activations)",
         "config": {"workload": "qwen3-0.6b decode stack, batch 1, Q4 group-32: 28 layers x 7 GEMVs + "
                                "lm_head 1024->151936 (197 GEMV calls per token)",
                    "weight_bytes_per_step": nbytes, "tokens_per_s": round(args.steps / secs, 2),
-                   "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4), "timing": "hip graph replay, HIP events"},
+                   "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4), "timing": "hip graph replay, HIP events",
+                   "arithmetic": "Q4 codes dequantised to fp16 in registers, fp16 products, fp32 accumulation"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "extra": extra,
