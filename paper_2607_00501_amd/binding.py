@@ -25,7 +25,8 @@ STATUS = {0: "QM_OK", 1: "QM_EINVAL", 2: "QM_ESHAPE", 3: "QM_EALIGN", 4: "QM_EFO
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqmatmul.so")
 
 EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "qm_repack",
-           "qmatmul_gemv", "qmatmul_gemv_grouped", "qmatmul_gemm", "qmoe_workspace_bytes", "qmoe_route",
+           "qmatmul_gemv", "qmatmul_gemv_grouped", "qmatmul_gemm", "qmatmul_gemm_grouped",
+           "qmoe_workspace_bytes", "qmoe_route",
            "qmoe_grouped_gemm", "qm_device_config")
 
 
@@ -63,6 +64,7 @@ def lib() -> ctypes.CDLL:
             "qmatmul_gemv": [W, vp, vp, vp],
             "qmatmul_gemv_grouped": [i32, W, ctypes.POINTER(vp), ctypes.POINTER(vp), vp],
             "qmatmul_gemm": [W, vp, i64, vp, vp],
+            "qmatmul_gemm_grouped": [i32, W, vp, i64, ctypes.POINTER(vp), vp],
             "qmoe_workspace_bytes": [i64, i32, i32, i64, i64, ctypes.POINTER(sz)],
             "qmoe_route": [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp],
             "qmoe_grouped_gemm": [W, W, W, vp, i64, i32, vp, vp, vp, vp, vp, vp, sz, vp],
@@ -199,6 +201,28 @@ def qmatmul_gemm(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None
         out = torch.empty((m, w.n), dtype=torch.float32, device=x.device)
     _check(lib().qmatmul_gemm(ctypes.byref(w.c()), _ptr(x), m, _ptr(out), _stream(stream)))
     return out
+
+
+def gemm_group_args(ws, outs):
+    """Marshals a grouped GEMM call: (count, descriptor array, y pointer
+    array); keep the returned tuple alive while in use."""
+    n = len(ws)
+    descs = (CQWeight * n)(*[w.c() for w in ws])
+    yp = (ctypes.c_void_p * n)(*[t.data_ptr() for t in outs])
+    return n, descs, yp
+
+
+def qmatmul_gemm_grouped(ws, x: torch.Tensor, outs=None, stream=None):
+    """Y_i = X W_i'^T for matrices with one k sharing X, in one launch."""
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.dim() == 2
+    m = x.shape[0]
+    for w in ws:
+        assert x.shape[1] == w.k
+    if outs is None:
+        outs = [torch.empty((m, w.n), dtype=torch.float32, device=x.device) for w in ws]
+    n, descs, yp = gemm_group_args(ws, outs)
+    _check(lib().qmatmul_gemm_grouped(n, descs, _ptr(x), m, yp, _stream(stream)))
+    return outs
 
 
 def qmoe_workspace_bytes(m: int, n_experts: int, top_k: int, hidden: int, inter: int) -> int:

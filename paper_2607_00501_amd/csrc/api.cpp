@@ -213,6 +213,54 @@ qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_
                   "qmatmul_gemv_grouped");
 }
 
+qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_t* x, int64_t m, float* const* y,
+                               void* stream) {
+  static_assert(QM_GEMM_GROUP_MAX == kGemmGroupMax, "group size");
+  if (count < 1 || count > QM_GEMM_GROUP_MAX)
+    return fail(QM_ESHAPE, "qmatmul_gemm_grouped: count=%d must be in [1, %d]", count, QM_GEMM_GROUP_MAX);
+  if (!w || !y) return fail(QM_EINVAL, "qmatmul_gemm_grouped: null array");
+  if (m < 1 || m > 65536) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: m=%lld must be in [1, 65536]", (long long)m);
+  int64_t rows = 0;
+  for (int i = 0; i < count; ++i) {
+    qm_status st = check_weight(&w[i], "qmatmul_gemm_grouped(w[i])");
+    if (st != QM_OK) return st;
+    if (w[i].layout != QM_LAYOUT_DEVICE)
+      return fail(QM_ELAYOUT, "qmatmul_gemm_grouped: w[%d] must be in DEVICE layout", i);
+    if (w[i].batch != 1) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: w[%d] batch must be 1", i);
+    if (w[i].format != w[0].format) return fail(QM_EFORMAT, "qmatmul_gemm_grouped: formats differ");
+    if (m > 1 && w[i].format != QM_Q4_G32)
+      return fail(QM_EFORMAT, "qmatmul_gemm_grouped: the MFMA GEMM supports Q4 only (m > 1)");
+    if (w[i].k != w[0].k) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: k differs between entries");
+    if (w[i].n > 0 && !y[i]) return fail(QM_EINVAL, "qmatmul_gemm_grouped: null y[%d]", i);
+    if (!aligned4(y[i])) return fail(QM_EALIGN, "qmatmul_gemm_grouped: y[%d] must be 4-byte aligned", i);
+    rows += padded_rows(w[i].n);
+  }
+  if (rows > (int64_t(1) << 30)) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: too many rows in the group");
+  if (rows > 0 && !x) return fail(QM_EINVAL, "qmatmul_gemm_grouped: null x");
+  if (!aligned16(x)) return fail(QM_EALIGN, "qmatmul_gemm_grouped: x must be 16-byte aligned");
+  const DeviceInfo* d;
+  qm_status st;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (m == 1) {
+    GemvGroup g{};
+    g.count = count;
+    for (int i = 0; i < count; ++i) {
+      g.q[i] = static_cast<const uint8_t*>(w[i].qdata); g.s[i] = w[i].scales;
+      g.x[i] = x; g.y[i] = y[i]; g.n[i] = static_cast<int>(w[i].n);
+    }
+    return launched(launch_gemv_group(w[0].format, g, w[0].k, d->cu_count, s), "qmatmul_gemm_grouped(m=1)");
+  }
+  const uint8_t* qs[kGemmGroupMax];
+  const uint16_t* ss[kGemmGroupMax];
+  float* ys[kGemmGroupMax];
+  int64_t ns[kGemmGroupMax];
+  for (int i = 0; i < count; ++i) {
+    qs[i] = static_cast<const uint8_t*>(w[i].qdata); ss[i] = w[i].scales; ys[i] = y[i]; ns[i] = w[i].n;
+  }
+  return launched(launch_gemm_group(count, qs, ss, ys, ns, x, m, w[0].k, d->cu_count, s), "qmatmul_gemm_grouped");
+}
+
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream) {
   qm_status st = check_weight(w, "qmatmul_gemm(w)");
   if (st != QM_OK) return st;

@@ -13,12 +13,9 @@ namespace qm {
 namespace {
 
 template <int BM, int WN, int WK>
-hipError_t launch_tile(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
-                       int64_t n, int64_t k, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>((n + 64 * WN - 1) / (64 * WN)),
-                  static_cast<unsigned>((m + BM - 1) / BM));
-  QgemmArgs a{};
-  a.q = q; a.s = s; a.a = x; a.y = y; a.M = m; a.N = n; a.K = k;
+hipError_t launch_tile(const QgemmArgs& a, hipStream_t st) {
+  const int64_t panels = a.gpanel[a.gcount];
+  const dim3 grid(static_cast<unsigned>((panels + WN - 1) / WN), static_cast<unsigned>((a.M + BM - 1) / BM));
   hipLaunchKernelGGL((qgemm_kernel<BM, WN, WK, QgMode::kDense>), grid, dim3(WN * WK * 64), 0, st, a);
   return hipGetLastError();
 }
@@ -62,29 +59,57 @@ const char* gemm_tile_name(int64_t m, int64_t n) {
   return buf;
 }
 
-hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
-                       int64_t n, int64_t k, int cu_count, hipStream_t st) {
-  if (n == 0) return hipSuccess;
-  const GemmPlan p = gemm_plan(m, n, k, cu_count);
+namespace {
+
+hipError_t launch_args(const QgemmArgs& a, int cu_count, hipStream_t st) {
+  const int64_t panels = a.gpanel[a.gcount];
+  if (panels == 0) return hipSuccess;
+  const GemmPlan p = gemm_plan(a.M, panels * kPanel, a.K, cu_count);
   if (p.wn == 4) {
-    if (p.bm == 128) return launch_tile<128, 4, 1>(q, s, x, y, m, n, k, st);
-    return launch_tile<64, 4, 1>(q, s, x, y, m, n, k, st);
+    if (p.bm == 128) return launch_tile<128, 4, 1>(a, st);
+    return launch_tile<64, 4, 1>(a, st);
   }
-  if (p.wn == 2) return launch_tile<64, 2, 1>(q, s, x, y, m, n, k, st);
+  if (p.wn == 2) return launch_tile<64, 2, 1>(a, st);
   if (p.bm == 64) {
     switch (p.wk) {
-      case 1: return launch_tile<64, 1, 1>(q, s, x, y, m, n, k, st);
-      case 2: return launch_tile<64, 1, 2>(q, s, x, y, m, n, k, st);
-      case 4: return launch_tile<64, 1, 4>(q, s, x, y, m, n, k, st);
-      default: return launch_tile<64, 1, 8>(q, s, x, y, m, n, k, st);
+      case 1: return launch_tile<64, 1, 1>(a, st);
+      case 2: return launch_tile<64, 1, 2>(a, st);
+      case 4: return launch_tile<64, 1, 4>(a, st);
+      default: return launch_tile<64, 1, 8>(a, st);
     }
   }
   switch (p.wk) {
-    case 1: return launch_tile<32, 1, 1>(q, s, x, y, m, n, k, st);
-    case 2: return launch_tile<32, 1, 2>(q, s, x, y, m, n, k, st);
-    case 4: return launch_tile<32, 1, 4>(q, s, x, y, m, n, k, st);
-    default: return launch_tile<32, 1, 8>(q, s, x, y, m, n, k, st);
+    case 1: return launch_tile<32, 1, 1>(a, st);
+    case 2: return launch_tile<32, 1, 2>(a, st);
+    case 4: return launch_tile<32, 1, 4>(a, st);
+    default: return launch_tile<32, 1, 8>(a, st);
   }
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
+                       int64_t n, int64_t k, int cu_count, hipStream_t st) {
+  const uint8_t* qs[1] = {q};
+  const uint16_t* ss[1] = {s};
+  float* ys[1] = {y};
+  const int64_t ns[1] = {n};
+  return launch_gemm_group(1, qs, ss, ys, ns, x, m, k, cu_count, st);
+}
+
+hipError_t launch_gemm_group(int count, const uint8_t* const* q, const uint16_t* const* s, float* const* y,
+                             const int64_t* n, const uint16_t* x, int64_t m, int64_t k, int cu_count,
+                             hipStream_t st) {
+  QgemmArgs a{};
+  a.a = x; a.M = m; a.K = k;
+  a.q = q[0]; a.s = s[0]; a.y = y[0]; a.N = n[0];
+  a.gcount = count;
+  a.gpanel[0] = 0;
+  for (int i = 0; i < count; ++i) {
+    a.gq[i] = q[i]; a.gs[i] = s[i]; a.gy[i] = y[i]; a.gn[i] = n[i];
+    a.gpanel[i + 1] = a.gpanel[i] + static_cast<int32_t>(padded_rows(n[i]) / kPanel);
+  }
+  return launch_args(a, cu_count, st);
 }
 
 }  // namespace qm

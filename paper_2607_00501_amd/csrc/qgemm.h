@@ -56,6 +56,15 @@ struct QgemmArgs {
   uint16_t* yp;                            // kMoeDown output [M][N] fp16 (assignment order)
   int32_t n_experts, top_k;
   int64_t tiles;                           // MoE: bound on the number of (expert, row tile) pairs
+  // kDense: gcount matrices with one K and a shared A, side by side in the
+  // panel index space (matrix i owns panels [gpanel[i], gpanel[i+1]));
+  // each wavefront picks its matrix.  A single GEMM is a group of one.
+  int32_t gcount;
+  int32_t gpanel[kGemmGroupMax + 1];
+  const uint8_t* gq[kGemmGroupMax];
+  const uint16_t* gs[kGemmGroupMax];
+  float* gy[kGemmGroupMax];
+  int64_t gn[kGemmGroupMax];
 };
 
 namespace qg {
@@ -180,8 +189,30 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     rows = static_cast<int>(min<int64_t>(BM, p.offsets[expert + 1] - row0));
     col_block = u % ny;
   }
-  const int64_t n_wave = col_block * (64 * WN) + 64 * wn;
-  const bool cols_ok = n_wave < npad;
+  // The wavefront's matrix (kDense groups) and its first output column.
+  const uint8_t* mq = p.q;
+  const uint16_t* ms = p.s;
+  float* my = p.y;
+  int64_t mN = N;
+  int64_t n_wave = col_block * (64 * WN) + 64 * wn;
+  bool cols_ok = n_wave < npad;
+  if constexpr (MODE == QgMode::kDense) {
+    const int gp = static_cast<int>(col_block * WN + wn);  // panel in the group's index space
+    mq = p.gq[0]; ms = p.gs[0]; my = p.gy[0]; mN = p.gn[0];
+    int first = 0;
+#pragma unroll
+    for (int j = 1; j < kGemmGroupMax; ++j) {
+      const bool in = j < p.gcount && gp >= p.gpanel[j];
+      mq = in ? p.gq[j] : mq;
+      ms = in ? p.gs[j] : ms;
+      my = in ? p.gy[j] : my;
+      mN = in ? p.gn[j] : mN;
+      first = in ? p.gpanel[j] : first;
+    }
+    n_wave = static_cast<int64_t>(gp - first) * kPanel;
+    cols_ok = gp < p.gpanel[p.gcount];
+  }
+  const int64_t mnpad = padded_rows(mN);
   // kMoeDown: assignment id and gate weight of each row of the tile, staged
   // once in LDS for the epilogue (visible after the first barrier below).
   __shared__ int64_t row_asg[MODE == QgMode::kMoeDown ? BM : 1];
@@ -209,12 +240,12 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     a_src[i] = p.a + src_row * K;
   }
   // B: lane l streams row l of the wavefront's panel(s) (clamped to a real panel).
-  const int64_t panel = (cols_ok ? n_wave : npad - kPanel) / kPanel;
+  const int64_t panel = (cols_ok ? n_wave : mnpad - kPanel) / kPanel;
   const int64_t mat_q = npad * (K / 2), mat_s = npad * G;   // bytes / scales of one matrix
   const uint8_t* b_q[NB];
   const uint16_t* b_s[NB];
-  b_q[0] = p.q + expert * mat_q + (panel * G * kPanel + lane) * 16;
-  b_s[0] = p.s + expert * mat_s + panel * G * kPanel + lane;
+  b_q[0] = mq + expert * mat_q + (panel * G * kPanel + lane) * 16;
+  b_s[0] = ms + expert * mat_s + panel * G * kPanel + lane;
   if constexpr (NB == 2) {
     b_q[1] = p.q2 + expert * mat_q + (panel * G * kPanel + lane) * 16;
     b_s[1] = p.s2 + expert * mat_s + panel * G * kPanel + lane;
@@ -400,10 +431,10 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int lr = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (lr >= rows || col >= N) continue;
+        if (lr >= rows || col >= mN) continue;
         if constexpr (MODE == QgMode::kDense) {
           // Y is not read again by this kernel: stream it past the caches.
-          __builtin_nontemporal_store(acc[a][b][r], p.y + (row0 + lr) * N + col);
+          __builtin_nontemporal_store(acc[a][b][r], my + (row0 + lr) * mN + col);
         } else if constexpr (MODE == QgMode::kMoeGateUp) {
           const float g = acc[a][b][r];
           const float u = acc[a][2 + b][r];

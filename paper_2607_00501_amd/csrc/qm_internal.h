@@ -73,6 +73,9 @@ __host__ __device__ inline int64_t xcd_chunked(int64_t i, int64_t chunk) {
   return ((j / chunk) * kXcds + xcd) * chunk + j % chunk;
 }
 
+// Up to kGemmGroupMax matrices with one K sharing A in one grouped GEMM.
+constexpr int kGemmGroupMax = 4;
+
 // Up to kGemvGroupMax independent GEMVs with one K and one format.
 constexpr int kGemvGroupMax = 8;
 struct GemvGroup {
@@ -90,6 +93,9 @@ hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const u
                        int64_t n, int64_t k, int cu_count, hipStream_t st);
 hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
                        int64_t n, int64_t k, int cu_count, hipStream_t st);
+hipError_t launch_gemm_group(int count, const uint8_t* const* q, const uint16_t* const* s, float* const* y,
+                             const int64_t* n, const uint16_t* x, int64_t m, int64_t k, int cu_count,
+                             hipStream_t st);
 
 struct MoeArgs {
   const uint8_t* gq; const uint16_t* gs;   // gate [E][inter][hidden], device layout

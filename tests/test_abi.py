@@ -167,3 +167,29 @@ def test_gemv_grouped_validation():
     assert call([w, w], ys=[y0, y0 + 2]) == 3                          # y[1] misaligned
     assert call([w, w], xs=[x0, 0]) == 1                               # null x[1]
     assert B.qm_last_error()
+
+
+def test_gemm_grouped_validation():
+    L = B.lib()
+    x = ctypes.c_void_p(0x30000)
+
+    def call(ws, ys=None, m=16, xp=x, count=None):
+        n = len(ws)
+        descs = (B.CQWeight * max(n, 1))(*ws)
+        ys = ys if ys is not None else [0x40000 + 0x1000 * i for i in range(n)]
+        yp = (ctypes.c_void_p * max(n, 1))(*ys)
+        return L.qmatmul_gemm_grouped(n if count is None else count, descs, xp, m, yp, None)
+
+    w = _fake_weight()
+    assert call([w], count=0) == 2                                     # count < 1
+    assert call([w] * 5) == 2                                          # count > 4
+    assert L.qmatmul_gemm_grouped(1, None, x, 16, None, None) == 1     # null arrays
+    assert call([w], m=0) == 2                                         # m < 1
+    assert call([w, _fake_weight(fmt=2)]) == 4                         # formats differ
+    assert call([_fake_weight(fmt=2)] * 2) == 4                        # Q8 with m > 1
+    assert call([w, _fake_weight(k=96)]) == 2                          # k differs
+    assert call([w, _fake_weight(layout=0)]) == 5                      # not DEVICE layout
+    assert call([w, w], ys=[0x40000, 0x40002]) == 3                    # y[1] misaligned
+    assert call([w], xp=ctypes.c_void_p(0x30004)) == 3                 # x misaligned
+    assert call([w], xp=None) == 1                                     # null x
+    assert B.qm_last_error()
