@@ -345,7 +345,34 @@ def extra_prefill(torch, B, inputs, workloads, steps, warmup, lib):
                                             "stack_TFLOPs": round(tf, 2),
                                             "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4)}
         log(f"prefill m={m}: {out[f'llama3.2-1b_prefill_m{m}']}")
-        del g, ys, xs
+        del g
+
+        # Grouped dispatch (qmatmul_gemm_grouped): q/k/v and gate/up of a layer
+        # each in one launch (64 launches for the 16 layers).
+        per_layer = len(model["layer"])
+        names = [name for name, _, _ in model["layer"]]
+        calls = []
+        for layer in range(model["layers"]):
+            base = layer * per_layer
+            for group in GROUPS:
+                idx = [base + names.index(nm) for nm in group]
+                k = wds[idx[0]][1]
+                n_, descs_g, yp = B.gemm_group_args([wds[i][0] for i in idx], [ys[i] for i in idx])
+                calls.append((n_, descs_g, ctypes.c_void_p(xs[k].data_ptr()), yp))
+
+        def run_g(s, calls=calls, m=m):
+            for n_, descs_g, xp, yp in calls:
+                st = lib.qmatmul_gemm_grouped(n_, descs_g, xp, m, yp, s)
+                if st:
+                    raise RuntimeError(lib.qm_last_error().decode())
+        g = capture(torch, run_g)
+        t, _ = time_graph(torch, g, max(steps // 2, 5), warmup)
+        tf = flops * max(steps // 2, 5) / t / 1e12
+        out[f"llama3.2-1b_prefill_m{m}_grouped_dispatch"] = {
+            "launches_per_stack": len(calls), "tokens_per_s": round(m * max(steps // 2, 5) / t, 1),
+            "stack_TFLOPs": round(tf, 2), "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4)}
+        log(f"prefill m={m} grouped: {out[f'llama3.2-1b_prefill_m{m}_grouped_dispatch']}")
+        del g, calls, ys, xs
     del wds
     torch.cuda.empty_cache()
 
