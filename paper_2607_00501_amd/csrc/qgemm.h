@@ -11,15 +11,21 @@
 //    K step of its weights is two 1 KiB contiguous chunk rows: one dwordx4
 //    per lane per chunk, fully coalesced;
 //  * the weights never pass through LDS: each wavefront dequantises its own
-//    B fragments in registers.  One v_permlane32_swap per dword pair moves
-//    the codes of panel rows 32..63 / 0..31 into the MFMA B-operand lane
-//    layout (lane l holds 8 consecutive k of column l%32); v_and_or_b32 +
-//    v_pk_add_f16 + v_pk_mul_f16 then give fp16_RNE(s*q) exactly;
+//    B fragments in registers.  The 16-deep k block an MFMA lane half
+//    covers is relabelled (A and B agree, so the sum is unchanged): in the
+//    substep s of group c, lane half h takes k = 32c + 16h + 8s + 0..7.  Lane
+//    l then needs two consecutive dwords of row l%32 (column half 0) and of
+//    row 32 + l%32 (column half 1), one dwordx2 each: the two loads of a
+//    wavefront read the 1 KiB chunk row exactly once, with no cross-lane
+//    permute.  v_and_or_b32 + one packed fp16 add (or fma for the nibbles at
+//    bits 4-7) + v_pk_mul_f16 then give fp16_RNE(s*q) exactly;
 //  * the activation tile of each K slice (BM x 64 fp16) is double-buffered
 //    in LDS (one barrier per K step) and shared by the WN wavefronts of the
 //    slice; A fragments of the next substep are read while the current
 //    MFMAs run;
-//  * global loads run DEPTH (2-4) K steps ahead of the MFMAs.  Out-of-range rows,
+//  * global loads run DEPTH (2-3) K steps ahead of the MFMAs, into DEPTH + 1
+//    register slots, so a load always targets a slot whose step is already
+//    consumed (no loop-carried register copies).  Out-of-range rows,
 //    columns and K steps read clamped (valid) addresses with their scales
 //    forced to zero, so the loads carry no branches;
 //  * modes: kDense (rows m0.., plain row-major A and Y); kMoeGateUp (rows of
@@ -70,36 +76,40 @@ struct QgemmArgs {
 namespace qg {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBK = 64;                 // K per step (two quantisation groups)
 constexpr int kMoeChunkTiles = 4;       // MoE row tiles per XCD chunk
 constexpr int kRow = kBK + 8;           // LDS row stride in halves (16-byte pad)
 
-// Dequantisation constants held in registers: the 0x000F000F mask in a VGPR
-// and the fp16 magic 0x6400_6400 in an SGPR, so that (d & mask) | magic
-// selects to one v_and_or_b32 (gfx9 VOP3 takes no literal operand).  The
-// empty asm makes the values opaque once, outside the loops.
+// Dequantisation constants held in registers: the masks 0x000F000F and
+// 0x00F000F0 in VGPRs and the fp16 magic 0x6400_6400 in an SGPR, so that
+// (d & mask) | magic selects to one v_and_or_b32 (gfx9 VOP3 takes no literal
+// operand).  The empty asm makes the values opaque once, outside the loops.
 struct DequantRegs {
-  uint32_t mask_v, magic_s;
-  __device__ DequantRegs() : mask_v(0x000F000Fu), magic_s(0x64006400u) {
-    asm volatile("" : "+v"(mask_v));
+  uint32_t m0, m1, magic_s;
+  __device__ DequantRegs() : m0(0x000F000Fu), m1(0x00F000F0u), magic_s(0x64006400u) {
+    asm volatile("" : "+v"(m0), "+v"(m1));
     asm volatile("" : "+s"(magic_s));
   }
 };
 
 // 8 offset-binary nibbles of one device-layout dword (k order 0,2,4,6 |
-// 1,3,5,7) -> 8 fp16 fp16_RNE(s*q) in natural k order.
+// 1,3,5,7) -> 8 fp16 fp16_RNE(s*q) in natural k order.  Nibbles at bits 0-3
+// (and 16-19) give the fp16 1024 + u, so q = x - 1032; nibbles at bits 4-7
+// (20-23) give 1024 + 16u, so q = x/16 - 72, one exact fma (x/16 is exact
+// and q is a small integer).  Bits 8-15 take one shift and the same steps.
 __device__ inline half8v dequant_dword(uint32_t d, half2v s2, const DequantRegs& c) {
-  const half2v bias = {(_Float16)1032.0f, (_Float16)1032.0f};
-  half8v out;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const half2v q = __builtin_bit_cast(half2v, ((d >> (4 * i)) & c.mask_v) | c.magic_s) - bias;
-    const half2v v = q * s2;
-    out[2 * i] = v[0];
-    out[2 * i + 1] = v[1];
-  }
-  return out;
+  const half2v b1 = {(_Float16)1032.0f, (_Float16)1032.0f};
+  const half2v r16 = {(_Float16)0.0625f, (_Float16)0.0625f};
+  const half2v b16 = {(_Float16)-72.0f, (_Float16)-72.0f};
+  const uint32_t d8 = d >> 8;
+  const half2v q01 = __builtin_bit_cast(half2v, (d & c.m0) | c.magic_s) - b1;
+  const half2v q23 = __builtin_elementwise_fma(__builtin_bit_cast(half2v, (d & c.m1) | c.magic_s), r16, b16);
+  const half2v q45 = __builtin_bit_cast(half2v, (d8 & c.m0) | c.magic_s) - b1;
+  const half2v q67 = __builtin_elementwise_fma(__builtin_bit_cast(half2v, (d8 & c.m1) | c.magic_s), r16, b16);
+  const half2v v0 = q01 * s2, v1 = q23 * s2, v2 = q45 * s2, v3 = q67 * s2;
+  return half8v{v0[0], v0[1], v1[0], v1[1], v2[0], v2[1], v3[0], v3[1]};
 }
 
 // Wavefront 0 maps the workgroup's linear tile index to (expert, row tile)
@@ -141,7 +151,13 @@ struct Cfg {
   static constexpr int kALoads = BM * (kBK / 8) / kSliceThreads;
   static constexpr int kStage = BM * kRow;                        // halves per A stage
   static_assert(kALoads >= 1 && BM * (kBK / 8) % kSliceThreads == 0, "A tile split");
-  static_assert(DEPTH >= 2 && DEPTH <= 4, "register slots of K steps in flight");
+  static_assert(DEPTH >= 2 && DEPTH <= 3, "K steps of loads in flight");
+  static constexpr int kSlots = DEPTH + 1;                       // register slots of raw B operands
+  // A tiles are loaded kADist steps ahead: one step (one register set, loaded
+  // at the top of the step before and stored to LDS at its end) for the
+  // register-heavy 128-row tiles, else DEPTH steps like B.
+  static constexpr int kADist = BM >= 128 ? 1 : DEPTH;
+  static constexpr int kASlots = kADist == 1 ? 1 : kSlots;
   // Split-K partial sums of slices 1..WK-1, in halves (fp32 = 2 halves).
   static constexpr int kRedHalves = (WK - 1) * WN * kTM * 2 * kNB * 16 * 64 * 2;
   static constexpr int kLdsHalves = 2 * WK * kStage > kRedHalves ? 2 * WK * kStage : kRedHalves;
@@ -154,7 +170,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[C::kLdsHalves];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform (SGPR)
   const int wk = wave / WN, wn = wave % WN;
   const int stid = tid - wk * C::kSliceThreads;          // thread index inside the K slice
   const int64_t K = p.K, N = p.N;
@@ -183,9 +199,9 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     if (u >= p.tiles * ny) return;                        // whole workgroup, before any barrier
     __shared__ int sh_e, sh_tile;
     find_tile(p.counts, p.n_experts, BM, static_cast<int>(u / ny), &sh_e, &sh_tile);
-    expert = sh_e;
+    expert = __builtin_amdgcn_readfirstlane(sh_e);
     if (expert < 0) return;
-    row0 = p.offsets[expert] + static_cast<int64_t>(sh_tile) * BM;
+    row0 = p.offsets[expert] + static_cast<int64_t>(__builtin_amdgcn_readfirstlane(sh_tile)) * BM;
     rows = static_cast<int>(min<int64_t>(BM, p.offsets[expert + 1] - row0));
     col_block = u % ny;
   }
@@ -239,24 +255,30 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     if constexpr (MODE == QgMode::kMoeGateUp) src_row = p.sorted_assign[r] / p.top_k;
     a_src[i] = p.a + src_row * K;
   }
-  // B: lane l streams row l of the wavefront's panel(s) (clamped to a real panel).
+  // B: lane l reads dwords 2(l/32), 2(l/32)+1 of panel rows l%32 and
+  // 32 + l%32 (clamped to a real panel).  The matrix, expert and panel bases
+  // are wavefront-uniform; the lane part is a 32-bit offset.
   const int64_t panel = (cols_ok ? n_wave : mnpad - kPanel) / kPanel;
   const int64_t mat_q = npad * (K / 2), mat_s = npad * G;   // bytes / scales of one matrix
   const uint8_t* b_q[NB];
   const uint16_t* b_s[NB];
-  b_q[0] = mq + expert * mat_q + (panel * G * kPanel + lane) * 16;
-  b_s[0] = ms + expert * mat_s + panel * G * kPanel + lane;
+  b_q[0] = mq + expert * mat_q + panel * G * kPanel * 16;
+  b_s[0] = ms + expert * mat_s + panel * G * kPanel;
   if constexpr (NB == 2) {
-    b_q[1] = p.q2 + expert * mat_q + (panel * G * kPanel + lane) * 16;
-    b_s[1] = p.s2 + expert * mat_s + panel * G * kPanel + lane;
+    b_q[1] = p.q2 + expert * mat_q + panel * G * kPanel * 16;
+    b_s[1] = p.s2 + expert * mat_s + panel * G * kPanel;
   }
+  const uint32_t bq_lane = (lane & 31) * 16 + (lane >> 5) * 8;
+  const uint32_t bs_lane = lane & 31;
 
-  // DEPTH register sets of raw step operands (step t lives in slot t % DEPTH),
-  // always indexed by constants.
-  u32x4 ra[DEPTH][C::kALoads];
-  u32x4 rb[DEPTH][NB][2];
-  uint32_t rs[DEPTH][NB][2];
-  auto load = [&](auto slot, int step) __attribute__((always_inline)) {
+  // DEPTH + 1 register sets of raw B operands (step t lives in slot
+  // t % (DEPTH + 1)), always indexed by constants; A has kASlots sets.
+  constexpr int NS = C::kSlots;
+  constexpr int AD = C::kADist;
+  u32x4 ra[C::kASlots][C::kALoads];
+  u32x2 rb[NS][NB][2][2];                                  // [slot][matrix][chunk][column half]
+  uint32_t rs[NS][NB][2][2];
+  auto load_a = [&](auto slot, int step) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot)::value;
     const int kt = kt0 + step;
 #pragma unroll
@@ -264,14 +286,22 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
       const int k = min(kt * kBK + a_col[i], static_cast<int>(K) - 8);
       ra[sl][i] = *reinterpret_cast<const u32x4*>(a_src[i] + k);
     }
+  };
+  auto load_b = [&](auto slot, int step) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot)::value;
+    const int kt = kt0 + step;
 #pragma unroll
     for (int j = 0; j < NB; ++j)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const int g = 2 * kt + c;
-        const int gc = min(g, G - 1);
-        rb[sl][j][c] = *reinterpret_cast<const u32x4*>(b_q[j] + static_cast<int64_t>(gc) * kPanel * 16);
-        rs[sl][j][c] = b_s[j][static_cast<int64_t>(gc) * kPanel];
+        const int gc = min(2 * kt + c, G - 1);
+        const uint8_t* bq = b_q[j] + static_cast<int64_t>(gc) * kPanel * 16;
+        const uint16_t* bs = b_s[j] + static_cast<int64_t>(gc) * kPanel;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          rb[sl][j][c][h] = *reinterpret_cast<const u32x2*>(bq + bq_lane + h * 512);
+          rs[sl][j][c][h] = bs[bs_lane + 32 * h];
+        }
       }
   };
   // Scale validity of step t's chunk c, applied when the step is consumed
@@ -304,14 +334,16 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
 
-  // One K step t: register slot sl = t % DEPTH holds step t's raw operands
-  // (its A tile is already in LDS buffer t&1), the other slots steps t+1 ..
-  // t+DEPTH-1.  The B codes of slot sl move to registers in MFMA layout, then
-  // slot sl is refilled with step t+DEPTH; step t+1's A tile goes to the other
-  // LDS buffer after the MFMAs.
+  // One K step t: register slot sl = t % (DEPTH + 1) holds step t's raw
+  // operands (its A tile is already in LDS buffer t&1), the slots of steps
+  // t+1 .. t+DEPTH-1 are in flight, and the slot of step t-1 (consumed) is
+  // refilled with step t+DEPTH; step t+1's A tile goes to the other LDS
+  // buffer after the MFMAs.
   auto step = [&](auto slot, int t) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot)::value;
-    using Next = std::integral_constant<int, (sl + 1) % DEPTH>;
+    using Refill = std::integral_constant<int, (sl + DEPTH) % NS>;
+    using ANext = std::integral_constant<int, AD == 1 ? 0 : (sl + 1) % NS>;
+    using ARefill = std::integral_constant<int, AD == 1 ? 0 : (sl + DEPTH) % NS>;
     const int buf = t & 1;
     uint32_t bd[NB][2][4];                                 // [matrix][column half][substep]
     half2v sc[NB][2][2];                                   // [matrix][chunk][column half]
@@ -319,23 +351,20 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     for (int j = 0; j < NB; ++j)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const uint32_t sv = scale_ok(t, c) ? rs[sl][j][c] : 0u;
-        const auto sw = __builtin_amdgcn_permlane32_swap(sv, sv, false, false);
-        const _Float16 lo = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[0]));
-        const _Float16 hi = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[1]));
-        sc[j][c][0] = half2v{lo, lo};
-        sc[j][c][1] = half2v{hi, hi};
-        const uint32_t d[4] = {rb[sl][j][c][0], rb[sl][j][c][1], rb[sl][j][c][2], rb[sl][j][c][3]};
+        const bool ok = scale_ok(t, c);
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const auto pr = __builtin_amdgcn_permlane32_swap(d[2 * i], d[2 * i + 1], false, false);
-          bd[j][0][2 * c + i] = pr[0];                     // panel rows 0..31
-          bd[j][1][2 * c + i] = pr[1];                     // panel rows 32..63
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t sv = ok ? rs[sl][j][c][h] : 0u;
+          const _Float16 f = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sv));
+          sc[j][c][h] = half2v{f, f};
+          bd[j][h][2 * c] = rb[sl][j][c][h][0];
+          bd[j][h][2 * c + 1] = rb[sl][j][c][h][1];
         }
       }
-    load(slot, t + DEPTH);                                 // DEPTH steps ahead
+    load_a(ARefill{}, t + AD);                             // kADist steps ahead
+    load_b(Refill{}, t + DEPTH);                           // DEPTH steps ahead
     __builtin_amdgcn_sched_barrier(0);                     // keep the loads at the top
-    const uint16_t* At = lds + (buf * WK + wk) * C::kStage + (lane & 31) * kRow + 8 * (lane >> 5);
+    const uint16_t* At = lds + (buf * WK + wk) * C::kStage + (lane & 31) * kRow + 16 * (lane >> 5);
     // Software pipeline over the four 16-deep substeps: the A fragments and
     // the dequantised B fragments of substep ks+1 are produced while the
     // MFMAs of substep ks run.
@@ -354,7 +383,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
       if (ks + 1 < kBK / 16) {
 #pragma unroll
         for (int a = 0; a < C::kTM; ++a)
-          af[nxt][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow + (ks + 1) * 16);
+          af[nxt][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow + 32 * ((ks + 1) >> 1) + 8 * ((ks + 1) & 1));
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
           bq[nxt][j][0] = dequant_dword(bd[j][0][ks + 1], sc[j][(ks + 1) >> 1][0], dq);
@@ -371,18 +400,24 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         }
       }
     }
-    if (t + 1 < KTs) store_a(Next{}, buf ^ 1);
+    if (t + 1 < KTs) store_a(ANext{}, buf ^ 1);
     slice_sync();
   };
 
-  using Slots = std::make_integer_sequence<int, DEPTH>;
   [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
-    (load(std::integral_constant<int, I>{}, I), ...);
-  }(Slots{});
+    (load_b(std::integral_constant<int, I>{}, I), ...);
+    (load_a(std::integral_constant<int, AD == 1 ? 0 : I>{}, I), ...);
+  }(std::make_integer_sequence<int, AD == 1 ? 1 : DEPTH>{});
+  if constexpr (AD == 1) {
+    [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
+      (load_b(std::integral_constant<int, I + 1>{}, I + 1), ...);
+    }(std::make_integer_sequence<int, DEPTH - 1>{});
+  }
   store_a(std::integral_constant<int, 0>{}, 0);
   slice_sync();
+  using Slots = std::make_integer_sequence<int, NS>;
   int t = 0;
-  for (; t + DEPTH <= KTs; t += DEPTH) {
+  for (; t + NS <= KTs; t += NS) {
     [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
       (step(std::integral_constant<int, I>{}, t + I), ...);
     }(Slots{});
