@@ -236,7 +236,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict
   dst[1] = make_float4(s[4], s[5], s[6], s[7]);
 }
 
-template <int BMG, int WKG, int BMD, int WKD, int WN, int DG = 2, int DD = 2>
+template <int BMG, int WKG, int BMD, int WKD, int WN, int DG = 2, int DD = 2, bool NT = false>
 hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
   const int64_t A = a.m * a.top_k;
   // Upper bound on the number of (expert, row tile) pairs: sum of
@@ -256,14 +256,14 @@ hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
     return dim3(static_cast<unsigned>((units + round - 1) / round * round));
   };
   g.tiles = tiles(BMG);
-  hipLaunchKernelGGL((qgemm_kernel<BMG, WN, WKG, QgMode::kMoeGateUp, DG>), grid(BMG, a.inter), dim3(WN * WKG * 64), 0,
+  hipLaunchKernelGGL((qgemm_kernel<BMG, WN, WKG, QgMode::kMoeGateUp, DG, NT>), grid(BMG, a.inter), dim3(WN * WKG * 64), 0,
                      st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // down, scaled by the gate weight and scattered to the assignment slot
   g.q = a.dq; g.s = a.ds; g.q2 = nullptr; g.s2 = nullptr; g.a = a.h; g.yp = a.yp; g.N = a.hidden; g.K = a.inter;
   g.tiles = tiles(BMD);
-  hipLaunchKernelGGL((qgemm_kernel<BMD, WN, WKD, QgMode::kMoeDown, DD>), grid(BMD, a.hidden), dim3(WN * WKD * 64), 0,
+  hipLaunchKernelGGL((qgemm_kernel<BMD, WN, WKD, QgMode::kMoeDown, DD, NT>), grid(BMD, a.hidden), dim3(WN * WKD * 64), 0,
                      st, g);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -307,22 +307,27 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
 hipError_t launch_moe(const MoeArgs& a, int cu_count, hipStream_t st) {
   (void)cu_count;
   // Tuning sweeps only: QM_MOE_PLAN="bm_gate_up,wk_gate_up,bm_down,wk_down,
-  // depth_gate_up,depth_down".
-  static const std::array<int, 6> forced = [] {
-    std::array<int, 6> f{0, 0, 0, 0, 2, 2};
+  // depth_gate_up,depth_down,nontemporal".
+  static const std::array<int, 7> forced = [] {
+    std::array<int, 7> f{0, 0, 0, 0, 2, 2, 0};
     if (const char* e = std::getenv("QM_MOE_PLAN"))
-      std::sscanf(e, "%d,%d,%d,%d,%d,%d", &f[0], &f[1], &f[2], &f[3], &f[4], &f[5]);
+      std::sscanf(e, "%d,%d,%d,%d,%d,%d,%d", &f[0], &f[1], &f[2], &f[3], &f[4], &f[5], &f[6]);
     return f;
   }();
-  using P = std::array<int, 6>;
-  if (forced == P{32, 1, 32, 1, 2, 2}) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2>(a, st);
-  if (forced == P{64, 1, 64, 1, 2, 2}) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2>(a, st);
-  if (forced == P{32, 2, 32, 1, 2, 2}) return launch_moe_tiles<32, 2, 32, 1, 4, 2, 2>(a, st);
-  if (forced == P{64, 1, 128, 1, 2, 2}) return launch_moe_tiles<64, 1, 128, 1, 4, 2, 2>(a, st);
+  using P = std::array<int, 7>;
+  if (forced == P{32, 1, 32, 1, 2, 2, 0}) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2>(a, st);
+  if (forced == P{64, 1, 64, 1, 2, 2, 0}) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2>(a, st);
+  if (forced == P{32, 1, 32, 1, 2, 2, 1}) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2, true>(a, st);
+  if (forced == P{64, 1, 64, 1, 2, 2, 1}) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2, true>(a, st);
   // Per-chip tile choice by rows per expert: 32-row tiles when buckets are
-  // small (decode-like prefill chunks), 64-row tiles otherwise.
+  // small (decode-like prefill chunks), 64-row tiles otherwise.  While an
+  // expert's rows fit one row tile, each weight panel is read by exactly one
+  // workgroup: nontemporal weight loads (measured on MI355X with cold caches:
+  // 132 -> 102 us at 8 rows per expert, 157 -> 143 us at 32; with several
+  // row tiles per expert they lose the L2 reuse between tiles).
   const int64_t rpe = a.m * a.top_k / a.n_experts;
-  if (rpe <= 24) return launch_moe_tiles<32, 1, 32, 1, 4>(a, st);
+  if (rpe <= 24) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2, true>(a, st);
+  if (rpe <= 64) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2, true>(a, st);
   return launch_moe_tiles<64, 1, 64, 1, 4>(a, st);
 }
 

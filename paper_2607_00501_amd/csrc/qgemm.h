@@ -163,7 +163,7 @@ struct Cfg {
   static constexpr int kLdsHalves = 2 * WK * kStage > kRedHalves ? 2 * WK * kStage : kRedHalves;
 };
 
-template <int BM, int WN, int WK, QgMode MODE, int DEPTH>
+template <int BM, int WN, int WK, QgMode MODE, int DEPTH, bool NT>
 __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   using C = Cfg<BM, WN, WK, MODE, DEPTH>;
   constexpr int NB = C::kNB;
@@ -299,8 +299,15 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         const uint16_t* bs = b_s[j] + static_cast<int64_t>(gc) * kPanel;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          rb[sl][j][c][h] = *reinterpret_cast<const u32x2*>(bq + bq_lane + h * 512);
-          rs[sl][j][c][h] = bs[bs_lane + 32 * h];
+          const u32x2* qa = reinterpret_cast<const u32x2*>(bq + bq_lane + h * 512);
+          const uint16_t* sa = bs + bs_lane + 32 * h;
+          if constexpr (NT) {
+            rb[sl][j][c][h] = __builtin_nontemporal_load(qa);
+            rs[sl][j][c][h] = __builtin_nontemporal_load(sa);
+          } else {
+            rb[sl][j][c][h] = *qa;
+            rs[sl][j][c][h] = *sa;
+          }
         }
       }
   };
@@ -485,10 +492,12 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 }  // namespace qg
 
 // Two workgroups per CU (up to 256 VGPRs per lane) for up to 4 wavefronts
-// per workgroup, one beyond.
-template <int BM, int WN, int WK, QgMode MODE, int DEPTH = 2>
+// per workgroup, one beyond.  NT: weights and scales are read with
+// nontemporal loads (for weights each workgroup streams once and no other
+// workgroup re-reads soon).
+template <int BM, int WN, int WK, QgMode MODE, int DEPTH = 2, bool NT = false>
 __global__ __launch_bounds__(WN * WK * 64, WN * WK <= 4 ? 2 : 1) void qgemm_kernel(QgemmArgs p) {
-  qg::qgemm_body<BM, WN, WK, MODE, DEPTH>(p);
+  qg::qgemm_body<BM, WN, WK, MODE, DEPTH, NT>(p);
 }
 
 }  // namespace qm
