@@ -19,13 +19,18 @@
 //    wavefront read the 1 KiB chunk row exactly once, with no cross-lane
 //    permute.  v_and_or_b32 + one packed fp16 add (or fma for the nibbles at
 //    bits 4-7) + v_pk_mul_f16 then give fp16_RNE(s*q) exactly;
-//  * the activation tile of each K slice (BM x 64 fp16) is double-buffered
-//    in LDS (one barrier per K step) and shared by the WN wavefronts of the
-//    slice; A fragments of the next substep are read while the current
-//    MFMAs run;
-//  * global loads run DEPTH (2-3) K steps ahead of the MFMAs, into DEPTH + 1
-//    register slots, so a load always targets a slot whose step is already
-//    consumed (no loop-carried register copies).  Out-of-range rows,
+//  * the activation tile of each K slice (BM x 64 fp16) goes from global
+//    memory straight into LDS (global_load_lds_dwordx4: lane l of an
+//    instruction lands at M0 + 16 l, one 1 KiB row group per instruction),
+//    in DEPTH + 1 stages, and is shared by the WN wavefronts of the slice.
+//    LDS rows are 128 B; 16-byte chunk c of row r sits at position
+//    c ^ ((r >> 1) & 7), so the A-fragment reads of 16 consecutive rows
+//    touch all 64 banks.  A fragments of the next substep are read while the
+//    current MFMAs run;
+//  * global loads run DEPTH (2-3) K steps ahead of the MFMAs, B into DEPTH + 1
+//    register slots and A into DEPTH + 1 LDS stages, so a load always
+//    targets a slot whose step is already consumed (no loop-carried register
+//    copies, one barrier per K step).  Out-of-range rows,
 //    columns and K steps read clamped (valid) addresses with their scales
 //    forced to zero, so the loads carry no branches;
 //  * modes: kDense (rows m0.., plain row-major A and Y); kMoeGateUp (rows of
@@ -80,7 +85,28 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBK = 64;                 // K per step (two quantisation groups)
 constexpr int kMoeChunkTiles = 4;       // MoE row tiles per XCD chunk
-constexpr int kRow = kBK + 8;           // LDS row stride in halves (16-byte pad)
+
+// s_waitcnt vmcnt(N) with expcnt and lgkmcnt left free (gfx9 encoding:
+// vmcnt[3:0] in bits 3:0 and vmcnt[5:4] in bits 15:14).
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N <= 63, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// 16 bytes per lane from global memory straight into LDS: lane l of the
+// wavefront writes lds_addr + 16 l (lds_addr is wavefront-uniform and goes
+// to M0).  Issued as inline asm so that the compiler's wait-count tracking
+// does not see it: with an LDS DMA pending, that tracking would wait for
+// every outstanding load (vmcnt 0) before the next use of any loaded
+// register.  The hardware still counts it in vmcnt; the kernel waits for it
+// explicitly (vm_wait), and every later wait the compiler computes stays
+// conservative.
+__device__ __forceinline__ void lds_dma16(const void* src, const void* lds_dst) {
+  const uint32_t lds_addr =
+      static_cast<uint32_t>(reinterpret_cast<size_t>((const void __attribute__((address_space(3)))*)lds_dst));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_addr) : "memory", "m0");
+}
 
 // Dequantisation constants held in registers: the masks 0x000F000F and
 // 0x00F000F0 in VGPRs and the fp16 magic 0x6400_6400 in an SGPR, so that
@@ -149,18 +175,22 @@ struct Cfg {
   static constexpr int kSliceThreads = WN * 64;
   static constexpr int kTM = BM / 32;
   static constexpr int kALoads = BM * (kBK / 8) / kSliceThreads;
-  static constexpr int kStage = BM * kRow;                        // halves per A stage
+  static constexpr int kStage = BM * kBK;                         // halves per A stage (128-B rows)
   static_assert(kALoads >= 1 && BM * (kBK / 8) % kSliceThreads == 0, "A tile split");
   static_assert(DEPTH >= 2 && DEPTH <= 3, "K steps of loads in flight");
-  static constexpr int kSlots = DEPTH + 1;                       // register slots of raw B operands
-  // A tiles are loaded kADist steps ahead: one step (one register set, loaded
-  // at the top of the step before and stored to LDS at its end) for the
-  // register-heavy 128-row tiles, else DEPTH steps like B.
-  static constexpr int kADist = BM >= 128 ? 1 : DEPTH;
-  static constexpr int kASlots = kADist == 1 ? 1 : kSlots;
+  static constexpr int kSlots = DEPTH + 1;                       // B register slots
+  // A LDS stages: DEPTH + 1 (A loaded DEPTH steps ahead, like B) when they
+  // fit in 48 KiB, else 2 (A loaded one step ahead), so that two or more
+  // workgroups share a CU.
+  static constexpr int kAStages = kSlots * WK * kStage * 2 <= 48 * 1024 ? kSlots : 2;
+  static constexpr int kADist = kAStages - 1;
+  // Global loads of one K step issued by one wavefront: A row groups, then
+  // per weight matrix 2 chunks x 2 column halves of codes and of scales.
+  static constexpr int kBLoads = kNB * 2 * 2 * 2;
   // Split-K partial sums of slices 1..WK-1, in halves (fp32 = 2 halves).
   static constexpr int kRedHalves = (WK - 1) * WN * kTM * 2 * kNB * 16 * 64 * 2;
-  static constexpr int kLdsHalves = 2 * WK * kStage > kRedHalves ? 2 * WK * kStage : kRedHalves;
+  static constexpr int kLdsHalves = kAStages * WK * kStage > kRedHalves ? kAStages * WK * kStage : kRedHalves;
+  static_assert(kAStages == kSlots || (kAStages == 2 && DEPTH == 2), "A stage schedule");
 };
 
 template <int BM, int WN, int WK, QgMode MODE, int DEPTH, bool NT>
@@ -230,7 +260,8 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   }
   const int64_t mnpad = padded_rows(mN);
   // kMoeDown: assignment id and gate weight of each row of the tile, staged
-  // once in LDS for the epilogue (visible after the first barrier below).
+  // once in LDS for the epilogue (published by the barrier before the first
+  // loads).
   __shared__ int64_t row_asg[MODE == QgMode::kMoeDown ? BM : 1];
   __shared__ float row_w[MODE == QgMode::kMoeDown ? BM : 1];
   if constexpr (MODE == QgMode::kMoeDown) {
@@ -241,15 +272,16 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     }
   }
 
-  // A: this thread's rows/cols of the slice's BM x 64 tile (rows clamped).
+  // A: instruction i of wavefront wn fills LDS row group g = i * WN + wn
+  // (rows 8g .. 8g+7 of the stage); lane l lands at row 8g + l/8, position
+  // l%8, i.e. it fetches logical chunk (l%8) ^ ((row >> 1) & 7) of that row
+  // (rows clamped to the tile).
   const uint16_t* a_src[C::kALoads];
-  int a_lds[C::kALoads], a_col[C::kALoads];
+  int a_col[C::kALoads];
 #pragma unroll
   for (int i = 0; i < C::kALoads; ++i) {
-    const int idx = stid + i * C::kSliceThreads;
-    const int row = idx >> 3;
-    a_col[i] = (idx & 7) * 8;
-    a_lds[i] = row * kRow + a_col[i];
+    const int row = 8 * (i * WN + wn) + (lane >> 3);
+    a_col[i] = ((lane & 7) ^ ((row >> 1) & 7)) * 8;
     const int64_t r = row0 + min(row, rows - 1);
     int64_t src_row = r;
     if constexpr (MODE == QgMode::kMoeGateUp) src_row = p.sorted_assign[r] / p.top_k;
@@ -271,20 +303,18 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   const uint32_t bq_lane = (lane & 31) * 16 + (lane >> 5) * 8;
   const uint32_t bs_lane = lane & 31;
 
-  // DEPTH + 1 register sets of raw B operands (step t lives in slot
-  // t % (DEPTH + 1)), always indexed by constants; A has kASlots sets.
+  // DEPTH + 1 register sets of raw B operands and LDS stages of A (step t
+  // lives in slot t % (DEPTH + 1)), always indexed by constants.
   constexpr int NS = C::kSlots;
-  constexpr int AD = C::kADist;
-  u32x4 ra[C::kASlots][C::kALoads];
   u32x2 rb[NS][NB][2][2];                                  // [slot][matrix][chunk][column half]
   uint32_t rs[NS][NB][2][2];
-  auto load_a = [&](auto slot, int step) __attribute__((always_inline)) {
-    constexpr int sl = decltype(slot)::value;
+  auto load_a = [&](int st, int step) __attribute__((always_inline)) {
     const int kt = kt0 + step;
+    uint16_t* stage = lds + (st * WK + wk) * C::kStage;
 #pragma unroll
     for (int i = 0; i < C::kALoads; ++i) {
       const int k = min(kt * kBK + a_col[i], static_cast<int>(K) - 8);
-      ra[sl][i] = *reinterpret_cast<const u32x4*>(a_src[i] + k);
+      lds_dma16(a_src[i] + k, stage + (i * WN + wn) * 8 * kBK);
     }
   };
   auto load_b = [&](auto slot, int step) __attribute__((always_inline)) {
@@ -317,19 +347,17 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     const int kt = kt0 + t;
     return cols_ok && 2 * kt + c < G && kt < KT;
   };
-  auto store_a = [&](auto slot, int buf) __attribute__((always_inline)) {
-    constexpr int sl = decltype(slot)::value;
-    uint16_t* dst = lds + (buf * WK + wk) * C::kStage;
-#pragma unroll
-    for (int i = 0; i < C::kALoads; ++i) *reinterpret_cast<u32x4*>(dst + a_lds[i]) = ra[sl][i];
-  };
-
-  // The A buffers of a K slice are written and read only by the slice's WN
-  // wavefronts.  A one-wavefront slice needs no workgroup barrier: the LDS
-  // instructions of one wavefront execute in order.
+  // The A stages of a K slice are written (by LDS DMA) and read only by the
+  // slice's WN wavefronts.  Each wavefront first waits for its own DMA of the
+  // step (wait_a); a plain s_barrier then publishes every wavefront's part.
+  // No memory fence: a workgroup fence would also wait for the loads of the
+  // later steps still in flight.  The empty asm statements keep the compiler
+  // from moving LDS accesses across the barrier.  A one-wavefront slice
+  // needs no barrier.
   auto slice_sync = [&]() __attribute__((always_inline)) {
-    if constexpr (WN == 1) __builtin_amdgcn_wave_barrier();
-    else __syncthreads();
+    asm volatile("" ::: "memory");
+    if constexpr (WN > 1) __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   };
 
   const DequantRegs dq;
@@ -341,17 +369,47 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
 
-  // One K step t: register slot sl = t % (DEPTH + 1) holds step t's raw
-  // operands (its A tile is already in LDS buffer t&1), the slots of steps
-  // t+1 .. t+DEPTH-1 are in flight, and the slot of step t-1 (consumed) is
-  // refilled with step t+DEPTH; step t+1's A tile goes to the other LDS
-  // buffer after the MFMAs.
+  // Issue order: the prologue takes A of steps 0 .. AD-1 and B of steps
+  // 0 .. DEPTH-1 (step q's A before its B); step s then issues A of step
+  // s + AD and B of step s + DEPTH, A first, also past the last step
+  // (clamped addresses, zero scales, stages never read), so the count of
+  // loads issued after A of step t is the same at every step.
+  constexpr int kNA = C::kALoads, kNBl = C::kBLoads, AD = C::kADist, NSA = C::kAStages;
+  static_assert(kNBl + (DEPTH - 1) * (kNA + kNBl) <= 63 && 2 * kNBl <= 63, "vmcnt range");
+  auto wait_a = [&](int t) __attribute__((always_inline)) {
+    if constexpr (AD == DEPTH) {
+      // after A(t): B(t), then A and B of steps t+1 .. t+DEPTH-1
+      vm_wait<kNBl + (DEPTH - 1) * (kNA + kNBl)>();
+    } else {
+      // AD = 1, DEPTH = 2: after A(0): B(0), B(1); after A(t), t >= 1
+      // (issued by step t-1): B(t+1)
+      if (t == 0) vm_wait<2 * kNBl>();
+      else vm_wait<kNBl>();
+    }
+  };
+  auto a_stage = [&](auto slot, int t) __attribute__((always_inline)) {
+    if constexpr (NSA == NS) return static_cast<int>(decltype(slot)::value);
+    else return t & 1;
+  };
+  // Lane byte offsets of the A fragments of substep ks inside a stage (row
+  // a*32 + l%32 adds a * 4 KiB): logical chunk 4(ks/2) + 2(l/32) + ks%2 at
+  // its swizzled position.
+  int a_off[kBK / 16];
+#pragma unroll
+  for (int ks = 0; ks < kBK / 16; ++ks) {
+    const int cl = ((ks >> 1) << 2) | ((lane >> 5) << 1) | (ks & 1);
+    a_off[ks] = (lane & 31) * (2 * kBK) + 16 * (cl ^ ((lane >> 1) & 7));
+  }
+
+  // One K step t: register slot / LDS stage sl = t % (DEPTH + 1) holds step
+  // t's operands, the slots of steps t+1 .. t+DEPTH-1 are in flight, and the
+  // slot of step t-1 is refilled with step t+DEPTH once every wavefront of
+  // the slice is past step t-1 (the barrier at the top of the step).
   auto step = [&](auto slot, int t) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot)::value;
     using Refill = std::integral_constant<int, (sl + DEPTH) % NS>;
-    using ANext = std::integral_constant<int, AD == 1 ? 0 : (sl + 1) % NS>;
-    using ARefill = std::integral_constant<int, AD == 1 ? 0 : (sl + DEPTH) % NS>;
-    const int buf = t & 1;
+    wait_a(t);
+    slice_sync();
     uint32_t bd[NB][2][4];                                 // [matrix][column half][substep]
     half2v sc[NB][2][2];                                   // [matrix][chunk][column half]
 #pragma unroll
@@ -368,17 +426,18 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
           bd[j][h][2 * c + 1] = rb[sl][j][c][h][1];
         }
       }
-    load_a(ARefill{}, t + AD);                             // kADist steps ahead
-    load_b(Refill{}, t + DEPTH);                           // DEPTH steps ahead
-    __builtin_amdgcn_sched_barrier(0);                     // keep the loads at the top
-    const uint16_t* At = lds + (buf * WK + wk) * C::kStage + (lane & 31) * kRow + 16 * (lane >> 5);
+    load_a(a_stage(Refill{}, t + AD), t + AD);             // A, AD steps ahead
+    __builtin_amdgcn_sched_barrier(0);
+    load_b(Refill{}, t + DEPTH);                           // B, DEPTH steps ahead
+    __builtin_amdgcn_sched_barrier(0);                               // keep the loads at the top
+    const char* At = reinterpret_cast<const char*>(lds + (a_stage(slot, t) * WK + wk) * C::kStage);
     // Software pipeline over the four 16-deep substeps: the A fragments and
     // the dequantised B fragments of substep ks+1 are produced while the
     // MFMAs of substep ks run.
     half8v af[2][C::kTM];
     half8v bq[2][NB][2];
 #pragma unroll
-    for (int a = 0; a < C::kTM; ++a) af[0][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow);
+    for (int a = 0; a < C::kTM; ++a) af[0][a] = *reinterpret_cast<const half8v*>(At + a_off[0] + a * 32 * 2 * kBK);
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       bq[0][j][0] = dequant_dword(bd[j][0][0], sc[j][0][0], dq);
@@ -390,7 +449,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
       if (ks + 1 < kBK / 16) {
 #pragma unroll
         for (int a = 0; a < C::kTM; ++a)
-          af[nxt][a] = *reinterpret_cast<const half8v*>(At + a * 32 * kRow + 32 * ((ks + 1) >> 1) + 8 * ((ks + 1) & 1));
+          af[nxt][a] = *reinterpret_cast<const half8v*>(At + a_off[ks + 1] + a * 32 * 2 * kBK);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
           bq[nxt][j][0] = dequant_dword(bd[j][0][ks + 1], sc[j][(ks + 1) >> 1][0], dq);
@@ -407,21 +466,18 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         }
       }
     }
-    if (t + 1 < KTs) store_a(ANext{}, buf ^ 1);
-    slice_sync();
   };
 
+  // The kMoeDown row table (and any other LDS written above) is complete and
+  // visible before the first DMA is issued (no DMA in flight: the fence
+  // costs nothing here).
+  if constexpr (MODE == QgMode::kMoeDown) __syncthreads();
   [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
-    (load_b(std::integral_constant<int, I>{}, I), ...);
-    (load_a(std::integral_constant<int, AD == 1 ? 0 : I>{}, I), ...);
-  }(std::make_integer_sequence<int, AD == 1 ? 1 : DEPTH>{});
-  if constexpr (AD == 1) {
-    [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
-      (load_b(std::integral_constant<int, I + 1>{}, I + 1), ...);
-    }(std::make_integer_sequence<int, DEPTH - 1>{});
-  }
-  store_a(std::integral_constant<int, 0>{}, 0);
-  slice_sync();
+    ((I < AD ? load_a(I, I) : void(),
+      __builtin_amdgcn_sched_barrier(0),
+      load_b(std::integral_constant<int, I>{}, I),
+      __builtin_amdgcn_sched_barrier(0)), ...);
+  }(std::make_integer_sequence<int, DEPTH>{});
   using Slots = std::make_integer_sequence<int, NS>;
   int t = 0;
   for (; t + NS <= KTs; t += NS) {
@@ -432,6 +488,9 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
     ((t + I < KTs ? step(std::integral_constant<int, I>{}, t + I) : void()), ...);
   }(Slots{});
+  // No LDS DMA may still be in flight when the LDS is reused or the
+  // workgroup ends (the prefetches past the last step included).
+  vm_wait<0>();
 
   if constexpr (WK > 1) {
     // Partial sums of slices 1..WK-1 go through LDS; slice 0 adds them in order.
