@@ -95,17 +95,34 @@ __device__ __forceinline__ void vm_wait() {
 }
 
 // 16 bytes per lane from global memory straight into LDS: lane l of the
-// wavefront writes lds_addr + 16 l (lds_addr is wavefront-uniform and goes
+// wavefront writes lds_dst + 16 l (lds_dst is wavefront-uniform and goes
 // to M0).  Issued as inline asm so that the compiler's wait-count tracking
 // does not see it: with an LDS DMA pending, that tracking would wait for
 // every outstanding load (vmcnt 0) before the next use of any loaded
 // register.  The hardware still counts it in vmcnt; the kernel waits for it
 // explicitly (vm_wait), and every later wait the compiler computes stays
 // conservative.
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<size_t>((const void __attribute__((address_space(3)))*)p));
+}
+template <bool NT = false>
 __device__ __forceinline__ void lds_dma16(const void* src, const void* lds_dst) {
-  const uint32_t lds_addr =
-      static_cast<uint32_t>(reinterpret_cast<size_t>((const void __attribute__((address_space(3)))*)lds_dst));
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_addr) : "memory", "m0");
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" : : "v"(src), "s"(lds_address(lds_dst))
+                 : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_address(lds_dst))
+                 : "memory", "m0");
+}
+// 4 bytes per lane, lane l to lds_dst + 4 l.
+template <bool NT = false>
+__device__ __forceinline__ void lds_dma4(const void* src, const void* lds_dst) {
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off nt" : : "v"(src), "s"(lds_address(lds_dst))
+                 : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" : : "v"(src), "s"(lds_address(lds_dst))
+                 : "memory", "m0");
 }
 
 // Dequantisation constants held in registers: the masks 0x000F000F and
@@ -175,21 +192,32 @@ struct Cfg {
   static constexpr int kSliceThreads = WN * 64;
   static constexpr int kTM = BM / 32;
   static constexpr int kALoads = BM * (kBK / 8) / kSliceThreads;
-  static constexpr int kStage = BM * kBK;                         // halves per A stage (128-B rows)
   static_assert(kALoads >= 1 && BM * (kBK / 8) % kSliceThreads == 0, "A tile split");
   static_assert(DEPTH >= 2 && DEPTH <= 3, "K steps of loads in flight");
   static constexpr int kSlots = DEPTH + 1;                       // B register slots
+  // LDS stage: the A tiles of the WK slices (BM rows x 128 B each), then,
+  // when B also goes through LDS, per wavefront and weight matrix the two
+  // 1 KiB code chunks and their 2 x 64 scales (2304 B).  B goes through LDS
+  // for multi-wavefront slices whose DEPTH + 1 = 3 stages fit in 80 KiB (two
+  // workgroups per CU); otherwise B is loaded into registers.
+  static constexpr int kAStageBytes = WK * BM * kBK * 2;
+  static constexpr int kBWaveBytes = kNB * 2304;
+  static constexpr bool kBLds =
+      WN > 1 && DEPTH == 2 && 3 * (kAStageBytes + WN * WK * kBWaveBytes) <= 80 * 1024;
+  static constexpr int kStageBytes = kAStageBytes + (kBLds ? WN * WK * kBWaveBytes : 0);
   // A LDS stages: DEPTH + 1 (A loaded DEPTH steps ahead, like B) when they
-  // fit in 48 KiB, else 2 (A loaded one step ahead), so that two or more
-  // workgroups share a CU.
-  static constexpr int kAStages = kSlots * WK * kStage * 2 <= 48 * 1024 ? kSlots : 2;
+  // fit in 48 KiB or B goes through LDS, else 2 (A loaded one step ahead),
+  // so that two or more workgroups share a CU.
+  static constexpr int kAStages = (kBLds || kSlots * kAStageBytes <= 48 * 1024) ? kSlots : 2;
   static constexpr int kADist = kAStages - 1;
   // Global loads of one K step issued by one wavefront: A row groups, then
-  // per weight matrix 2 chunks x 2 column halves of codes and of scales.
-  static constexpr int kBLoads = kNB * 2 * 2 * 2;
+  // per weight matrix either 2 code chunks + 1 scale block (LDS DMA) or
+  // 2 chunks x 2 column halves of codes and of scales (registers).
+  static constexpr int kBLoads = kBLds ? kNB * 3 : kNB * 2 * 2 * 2;
   // Split-K partial sums of slices 1..WK-1, in halves (fp32 = 2 halves).
   static constexpr int kRedHalves = (WK - 1) * WN * kTM * 2 * kNB * 16 * 64 * 2;
-  static constexpr int kLdsHalves = kAStages * WK * kStage > kRedHalves ? kAStages * WK * kStage : kRedHalves;
+  static constexpr int kLdsHalves =
+      kAStages * kStageBytes / 2 > kRedHalves ? kAStages * kStageBytes / 2 : kRedHalves;
   static_assert(kAStages == kSlots || (kAStages == 2 && DEPTH == 2), "A stage schedule");
 };
 
@@ -308,18 +336,40 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   constexpr int NS = C::kSlots;
   u32x2 rb[NS][NB][2][2];                                  // [slot][matrix][chunk][column half]
   uint32_t rs[NS][NB][2][2];
+  char* const lds_b = reinterpret_cast<char*>(lds);
+  // A tile of this slice in stage st; B region of this wavefront in stage st.
+  auto a_tile = [&](int st) __attribute__((always_inline)) { return lds_b + st * C::kStageBytes + wk * BM * 2 * kBK; };
+  auto b_region = [&](int st) __attribute__((always_inline)) {
+    return lds_b + st * C::kStageBytes + C::kAStageBytes + wave * C::kBWaveBytes;
+  };
   auto load_a = [&](int st, int step) __attribute__((always_inline)) {
     const int kt = kt0 + step;
-    uint16_t* stage = lds + (st * WK + wk) * C::kStage;
+    char* tile = a_tile(st);
 #pragma unroll
     for (int i = 0; i < C::kALoads; ++i) {
       const int k = min(kt * kBK + a_col[i], static_cast<int>(K) - 8);
-      lds_dma16(a_src[i] + k, stage + (i * WN + wn) * 8 * kBK);
+      lds_dma16(a_src[i] + k, tile + (i * WN + wn) * 1024);
     }
   };
   auto load_b = [&](auto slot, int step) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot)::value;
     const int kt = kt0 + step;
+    if constexpr (C::kBLds) {
+      // Per matrix: the two 1 KiB chunk rows verbatim, then their scales
+      // (lanes 0-31: chunk 0, lanes 32-63: chunk 1; 4 B = 2 scales a lane).
+      char* reg = b_region(sl);
+      const int gs1 = min(2 * kt + (lane >> 5), G - 1);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const int gc = min(2 * kt + c, G - 1);
+          lds_dma16<NT>(b_q[j] + static_cast<int64_t>(gc) * kPanel * 16 + lane * 16, reg + j * 2304 + c * 1024);
+        }
+        lds_dma4<NT>(b_s[j] + static_cast<int64_t>(gs1) * kPanel + 2 * (lane & 31), reg + j * 2304 + 2048);
+      }
+      return;
+    }
 #pragma unroll
     for (int j = 0; j < NB; ++j)
 #pragma unroll
@@ -377,7 +427,10 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   constexpr int kNA = C::kALoads, kNBl = C::kBLoads, AD = C::kADist, NSA = C::kAStages;
   static_assert(kNBl + (DEPTH - 1) * (kNA + kNBl) <= 63 && 2 * kNBl <= 63, "vmcnt range");
   auto wait_a = [&](int t) __attribute__((always_inline)) {
-    if constexpr (AD == DEPTH) {
+    if constexpr (C::kBLds) {
+      // all of step t (A and B): the groups of steps t+1 .. t+DEPTH-1 may remain
+      vm_wait<(DEPTH - 1) * (kNA + kNBl)>();
+    } else if constexpr (AD == DEPTH) {
       // after A(t): B(t), then A and B of steps t+1 .. t+DEPTH-1
       vm_wait<kNBl + (DEPTH - 1) * (kNA + kNBl)>();
     } else {
@@ -412,6 +465,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     slice_sync();
     uint32_t bd[NB][2][4];                                 // [matrix][column half][substep]
     half2v sc[NB][2][2];                                   // [matrix][chunk][column half]
+    const char* breg = b_region(sl);
 #pragma unroll
     for (int j = 0; j < NB; ++j)
 #pragma unroll
@@ -419,18 +473,28 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         const bool ok = scale_ok(t, c);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const uint32_t sv = ok ? rs[sl][j][c][h] : 0u;
+          u32x2 d;
+          uint32_t sv;
+          if constexpr (C::kBLds) {
+            const int row = 32 * h + (lane & 31);
+            d = *reinterpret_cast<const u32x2*>(breg + j * 2304 + c * 1024 + row * 16 + 8 * (lane >> 5));
+            sv = *reinterpret_cast<const uint16_t*>(breg + j * 2304 + 2048 + c * 128 + row * 2);
+          } else {
+            d = rb[sl][j][c][h];
+            sv = rs[sl][j][c][h];
+          }
+          sv = ok ? sv : 0u;
           const _Float16 f = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sv));
           sc[j][c][h] = half2v{f, f};
-          bd[j][h][2 * c] = rb[sl][j][c][h][0];
-          bd[j][h][2 * c + 1] = rb[sl][j][c][h][1];
+          bd[j][h][2 * c] = d[0];
+          bd[j][h][2 * c + 1] = d[1];
         }
       }
     load_a(a_stage(Refill{}, t + AD), t + AD);             // A, AD steps ahead
     __builtin_amdgcn_sched_barrier(0);
     load_b(Refill{}, t + DEPTH);                           // B, DEPTH steps ahead
     __builtin_amdgcn_sched_barrier(0);                               // keep the loads at the top
-    const char* At = reinterpret_cast<const char*>(lds + (a_stage(slot, t) * WK + wk) * C::kStage);
+    const char* At = a_tile(a_stage(slot, t));
     // Software pipeline over the four 16-deep substeps: the A fragments and
     // the dequantised B fragments of substep ks+1 are produced while the
     // MFMAs of substep ks run.
