@@ -33,6 +33,24 @@ def test_gemm_parity(m, n, k):
     assert err <= 2e-3, err                  # fp16 weight rounding only: ~3e-4 expected
 
 
+def test_gemm_large_ragged_sampled():
+    """A large shape (the 128 x 256 tile at two workgroups per CU), ragged in
+    every dimension: 2000 rows, 8000 columns, K = 96 (a half-empty last K
+    step).  The oracle recomputes sampled rows and columns, including both
+    sides of tile boundaries."""
+    m, n, k = 2000, 8000, 96
+    w = inputs.weights_np(inputs.seed_for(3, n, "gate", 256), (n, k))
+    x = inputs.activations_np(inputs.seed_for(3, m, "x", 256), (m, k))
+    wd = _device_weight(w)
+    y = B.qmatmul_gemm(wd, torch.from_numpy(x).cuda()).cpu().numpy()
+    rng = np.random.default_rng(256)
+    rows = np.unique(np.concatenate([rng.choice(m, 40, replace=False), [0, 127, 128, 1919, 1920, m - 1]]))
+    cols = np.unique(np.concatenate([rng.choice(n, 300, replace=False), [0, 255, 256, 7935, 7936, n - 1]]))
+    q, s = O.quantise(w[cols], O.Q4)
+    ref = O.gemm(O.pack(q, O.Q4), s, O.Q4, x[rows])
+    assert rel_err(y[np.ix_(rows, cols)], ref) <= MFMA_TOL
+
+
 def test_gemm_integer_grid_exact():
     """Integer weights with scale 1 are exact in fp16, products and sums of
     small integers are exact in the fp32 MFMA accumulator."""
