@@ -159,8 +159,9 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
 
 /* Prefill GEMM (Sec. 3.3, Sec. 3.4, M > 1): Y[m][n] = sum_k X[m][k] * w'[n][k].
  * w: DEVICE layout, batch 1, Q4.  X: fp16 [m][k] row-major; Y: fp32 [m][n].
- * Weight tiles are dequantised to fp16 (value fp16_RNE(s*q)) in registers
- * and fed to fp16 MFMA with fp32 accumulation; X tiles go through LDS.
+ * X tiles and (for most tile shapes) the raw weight chunks are copied into
+ * LDS by DMA; weights are dequantised to fp16 (value fp16_RNE(s*q)) in
+ * registers and fed to fp16 MFMA with fp32 accumulation.
  * m >= 1 (m == 1 runs the GEMV); m <= 65536 per call (chunk larger
  * prompts).  Deterministic. */
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream);

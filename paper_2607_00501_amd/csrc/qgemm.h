@@ -8,31 +8,32 @@
 //    output block whose 64 columns are one device-layout panel, over the
 //    wk-th slice of the K steps (WK > 1: split-K inside the workgroup, in
 //    every mode; the partial sums meet in LDS in a fixed order).  One 64-deep
-//    K step of its weights is two 1 KiB contiguous chunk rows: one dwordx4
-//    per lane per chunk, fully coalesced;
-//  * the weights never pass through LDS: each wavefront dequantises its own
-//    B fragments in registers.  The 16-deep k block an MFMA lane half
-//    covers is relabelled (A and B agree, so the sum is unchanged): in the
-//    substep s of group c, lane half h takes k = 32c + 16h + 8s + 0..7.  Lane
-//    l then needs two consecutive dwords of row l%32 (column half 0) and of
-//    row 32 + l%32 (column half 1), one dwordx2 each: the two loads of a
-//    wavefront read the 1 KiB chunk row exactly once, with no cross-lane
-//    permute.  v_and_or_b32 + one packed fp16 add (or fma for the nibbles at
-//    bits 4-7) + v_pk_mul_f16 then give fp16_RNE(s*q) exactly;
-//  * the activation tile of each K slice (BM x 64 fp16) goes from global
-//    memory straight into LDS (global_load_lds_dwordx4: lane l of an
-//    instruction lands at M0 + 16 l, one 1 KiB row group per instruction),
-//    in DEPTH + 1 stages, and is shared by the WN wavefronts of the slice.
-//    LDS rows are 128 B; 16-byte chunk c of row r sits at position
-//    c ^ ((r >> 1) & 7), so the A-fragment reads of 16 consecutive rows
-//    touch all 64 banks.  A fragments of the next substep are read while the
-//    current MFMAs run;
-//  * global loads run DEPTH (2-3) K steps ahead of the MFMAs, B into DEPTH + 1
-//    register slots and A into DEPTH + 1 LDS stages, so a load always
+//    K step of its weights is two 1 KiB contiguous chunk rows;
+//  * loads go global -> LDS by DMA (global_load_lds_dwordx4: lane l of an
+//    instruction lands at M0 + 16 l, 1 KiB per instruction), with no staging
+//    registers: the activation tile of each K slice (BM x 64 fp16, shared by
+//    the WN wavefronts of the slice) and, for multi-wavefront tiles whose
+//    stages fit, each wavefront's two chunk rows verbatim plus their scales.
+//    One-wavefront split-K tiles load the weights into registers instead.
+//    LDS activation rows are 128 B; 16-byte chunk c of row r sits at
+//    position c ^ ((r >> 1) & 7), so the A-fragment reads of 16 consecutive
+//    rows touch all 64 banks;
+//  * each wavefront dequantises its own B fragments in registers, once per
+//    workgroup.  The 16-deep k block an MFMA lane half covers is relabelled
+//    (A and B agree, so the sum is unchanged): in substep s of group c, lane
+//    half h takes k = 32c + 16h + 8s + 0..7.  Lane l then needs two
+//    consecutive dwords of row l%32 (column half 0) and of row 32 + l%32
+//    (column half 1): no cross-lane permute.  v_and_or_b32 + one packed fp16
+//    add (or an exact fma for the nibbles at bits 4-7) + v_pk_mul_f16 give
+//    fp16_RNE(s*q) exactly.  A fragments and dequantised B of the next
+//    substep are produced while the current MFMAs run;
+//  * loads run DEPTH (2-3) K steps ahead into DEPTH + 1 LDS stages / register
+//    slots (2 stages, one step ahead, where LDS is short), so a load always
 //    targets a slot whose step is already consumed (no loop-carried register
-//    copies, one barrier per K step).  Out-of-range rows,
-//    columns and K steps read clamped (valid) addresses with their scales
-//    forced to zero, so the loads carry no branches;
+//    copies).  Each K step waits for exactly its own loads and then passes
+//    one barrier.  Out-of-range rows, columns and K steps (also the
+//    prefetches past the last step) read clamped (valid) addresses with
+//    their scales forced to zero, so the loads carry no branches;
 //  * modes: kDense (rows m0.., plain row-major A and Y); kMoeGateUp (rows of
 //    one expert's bucket, A rows gathered through the assignment
 //    permutation, each wavefront streams the gate and the up panel of the
