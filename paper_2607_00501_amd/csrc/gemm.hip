@@ -23,32 +23,33 @@ hipError_t launch_tile(const QgemmArgs& a, hipStream_t st) {
 }  // namespace
 
 // Per-chip tile choice by M regime (Sec. 3.4: tiles tuned to sequence
-// length), fitted to a per-shape sweep on MI355X (256 CUs): the 128 x 256
-// tile when it gives at least two workgroups per CU, else the 64 x 256 tile
-// when it gives one per CU; else one 64-column panel per K slice with
-// split-K over as many one-wavefront slices as keep >= 8 K steps each (at
-// most 8), in 64-row tiles if that gives 8 wavefronts per CU, else 32-row
-// tiles.
+// length), fitted to a per-shape sweep on MI355X (256 CUs) over the
+// Llama-3.2-1B shapes and their grouped widths at M = 128, 512, 2048:
+//  * 128 x 256 tiles when they give at least 3/4 workgroup per CU;
+//  * else 64 x 256 tiles when they give at least one per CU;
+//  * else 64 x 128 tiles with 2-way split-K when those give at least 3/4
+//    workgroup per CU and K has >= 32 steps;
+//  * else one 64-column panel per K slice with split-K over as many
+//    one-wavefront slices as keep >= 8 K steps each (at most 8), in 64-row
+//    tiles if that gives 4 wavefronts per CU, else 32-row tiles.
 GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count) {
-  // Tuning sweeps only: QM_GEMM_PLAN="bm,wn,wk" forces the plan.
+  // Tuning sweeps only: QM_GEMM_PLAN="bm,wn,wk" forces the plan (one of the
+  // instantiated tiles, see launch_args).
   static const GemmPlan forced = [] {
     GemmPlan f{0, 0, 0};
     if (const char* e = std::getenv("QM_GEMM_PLAN")) std::sscanf(e, "%d,%d,%d", &f.bm, &f.wn, &f.wk);
     return f;
   }();
-  if ((forced.bm == 32 || forced.bm == 64 || forced.bm == 128) && (forced.wn == 1 || forced.wn == 2 || forced.wn == 4) &&
-      (forced.wk == 1 || forced.wk == 2 || forced.wk == 4 || forced.wk == 8)) {
-    GemmPlan f = forced;
-    if (f.wk > 1 || f.bm == 32) { f.wn = 1; if (f.bm == 128) f.bm = 64; }
-    return f;
-  }
+  if (forced.bm != 0 && gemm_plan_instantiated(forced)) return forced;
   auto blocks = [&](int bm, int wn) { return ((n + 64 * wn - 1) / (64 * wn)) * ((m + bm - 1) / bm); };
-  if (blocks(128, 4) >= 2 * cu_count) return GemmPlan{128, 4, 1};
-  if (blocks(64, 4) >= cu_count) return GemmPlan{64, 4, 1};
+  const int64_t cu = cu_count;
   const int64_t kt = (k / kGroup + 1) / 2;
+  if (4 * blocks(128, 4) >= 3 * cu) return GemmPlan{128, 4, 1};
+  if (blocks(64, 4) >= cu) return GemmPlan{64, 4, 1};
+  if (4 * blocks(64, 2) >= 3 * cu && kt >= 32) return GemmPlan{64, 2, 2};
   int wk = 1;
   while (wk < 8 && kt / (2 * wk) >= 8) wk *= 2;
-  if (blocks(64, 1) * wk >= 8 * static_cast<int64_t>(cu_count)) return GemmPlan{64, 1, wk};
+  if (blocks(64, 1) * wk >= 4 * cu) return GemmPlan{64, 1, wk};
   return GemmPlan{32, 1, wk};
 }
 
@@ -61,31 +62,32 @@ const char* gemm_tile_name(int64_t m, int64_t n) {
 
 namespace {
 
+#define QM_GEMM_TILES(X) \
+  X(128, 4, 1) X(64, 4, 1) X(64, 4, 2) X(64, 2, 1) X(64, 2, 2) X(32, 4, 1) X(32, 4, 2) \
+  X(64, 1, 1) X(64, 1, 2) X(64, 1, 4) X(64, 1, 8) X(32, 1, 1) X(32, 1, 2) X(32, 1, 4) X(32, 1, 8)
+
 hipError_t launch_args(const QgemmArgs& a, int cu_count, hipStream_t st) {
   const int64_t panels = a.gpanel[a.gcount];
   if (panels == 0) return hipSuccess;
   const GemmPlan p = gemm_plan(a.M, panels * kPanel, a.K, cu_count);
-  if (p.wn == 4) {
-    if (p.bm == 128) return launch_tile<128, 4, 1>(a, st);
-    return launch_tile<64, 4, 1>(a, st);
-  }
-  if (p.wn == 2) return launch_tile<64, 2, 1>(a, st);
-  if (p.bm == 64) {
-    switch (p.wk) {
-      case 1: return launch_tile<64, 1, 1>(a, st);
-      case 2: return launch_tile<64, 1, 2>(a, st);
-      case 4: return launch_tile<64, 1, 4>(a, st);
-      default: return launch_tile<64, 1, 8>(a, st);
-    }
-  }
-  switch (p.wk) {
-    case 1: return launch_tile<32, 1, 1>(a, st);
-    case 2: return launch_tile<32, 1, 2>(a, st);
-    case 4: return launch_tile<32, 1, 4>(a, st);
-    default: return launch_tile<32, 1, 8>(a, st);
-  }
+#define QM_LAUNCH(BM, WN, WK) \
+  if (p.bm == BM && p.wn == WN && p.wk == WK) return launch_tile<BM, WN, WK>(a, st);
+  QM_GEMM_TILES(QM_LAUNCH)
+#undef QM_LAUNCH
+  return hipErrorInvalidConfiguration;
 }
 
+}  // namespace
+
+bool gemm_plan_instantiated(const GemmPlan& p) {
+#define QM_HAS(BM, WN, WK) \
+  if (p.bm == BM && p.wn == WN && p.wk == WK) return true;
+  QM_GEMM_TILES(QM_HAS)
+#undef QM_HAS
+  return false;
+}
+
+namespace {
 }  // namespace
 
 hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,

@@ -199,12 +199,11 @@ struct Cfg {
   // LDS stage: the A tiles of the WK slices (BM rows x 128 B each), then,
   // when B also goes through LDS, per wavefront and weight matrix the two
   // 1 KiB code chunks and their 2 x 64 scales (2304 B).  B goes through LDS
-  // for multi-wavefront slices whose DEPTH + 1 = 3 stages fit in 80 KiB (two
+  // for multi-wavefront slices whose DEPTH + 1 stages fit in 80 KiB (two
   // workgroups per CU); otherwise B is loaded into registers.
   static constexpr int kAStageBytes = WK * BM * kBK * 2;
   static constexpr int kBWaveBytes = kNB * 2304;
-  static constexpr bool kBLds =
-      WN > 1 && DEPTH == 2 && 3 * (kAStageBytes + WN * WK * kBWaveBytes) <= 80 * 1024;
+  static constexpr bool kBLds = WN > 1 && kSlots * (kAStageBytes + WN * WK * kBWaveBytes) <= 80 * 1024;
   static constexpr int kStageBytes = kAStageBytes + (kBLds ? WN * WK * kBWaveBytes : 0);
   // A LDS stages: DEPTH + 1 (A loaded DEPTH steps ahead, like B) when they
   // fit in 48 KiB or B goes through LDS, else 2 (A loaded one step ahead),

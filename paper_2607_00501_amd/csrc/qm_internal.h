@@ -125,6 +125,7 @@ struct GemvPlan { int subr; int waves; int xlds; };
 GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count);
 struct GemmPlan { int bm; int wn; int wk; };   // rows per tile, panels (wavefronts) per K slice, K slices
 GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count);
+bool gemm_plan_instantiated(const GemmPlan& p);   // a prefill GEMM tile exists for p
 const char* gemm_tile_name(int64_t m, int64_t n);
 const char* moe_tile_name(int64_t rows_per_expert);
 

@@ -51,6 +51,23 @@ def test_gemm_large_ragged_sampled():
     assert rel_err(y[np.ix_(rows, cols)], ref) <= MFMA_TOL
 
 
+def test_gemm_two_panel_split_k_ragged_sampled():
+    """A shape the 64 x 128 two-way split-K tile takes: 500 rows, 3000
+    columns (a half-filled last panel pair), K = 2080 (33 K steps: the second
+    slice has one step past the end).  Sampled rows and columns."""
+    m, n, k = 500, 3000, 2080
+    w = inputs.weights_np(inputs.seed_for(3, n, "up", 2), (n, k))
+    x = inputs.activations_np(inputs.seed_for(3, m, "x", 2), (m, k))
+    wd = _device_weight(w)
+    y = B.qmatmul_gemm(wd, torch.from_numpy(x).cuda()).cpu().numpy()
+    rng = np.random.default_rng(22)
+    rows = np.unique(np.concatenate([rng.choice(m, 30, replace=False), [0, 63, 64, 447, 448, m - 1]]))
+    cols = np.unique(np.concatenate([rng.choice(n, 200, replace=False), [0, 127, 128, 2943, 2944, n - 1]]))
+    q, s = O.quantise(w[cols], O.Q4)
+    ref = O.gemm(O.pack(q, O.Q4), s, O.Q4, x[rows])
+    assert rel_err(y[np.ix_(rows, cols)], ref) <= MFMA_TOL
+
+
 def test_gemm_integer_grid_exact():
     """Integer weights with scale 1 are exact in fp16, products and sums of
     small integers are exact in the fp32 MFMA accumulator."""
