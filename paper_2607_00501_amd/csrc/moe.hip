@@ -12,6 +12,7 @@
 
 #include <cstdio>
 #include <cstdlib>
+#include <algorithm>
 #include <array>
 #include <utility>
 
@@ -113,6 +114,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(const float* __res
 constexpr int kBucketThreads = 1024;
 constexpr int kBucketWaves = kBucketThreads / 64;
 constexpr int kBucketUnroll = 8;
+// Workgroups: each scatters a contiguous slice of about kBucketSlice
+// assignments (two groups of 64 per wavefront), at most kBucketMaxGroups.
+constexpr int64_t kBucketSlice = 2048;
+constexpr int kBucketMaxGroups = 16;
 
 // Lanes of the wavefront that hold the same expert id (one ballot per bit of
 // the id, `bits` = bits needed for n_experts - 1), restricted to the valid
@@ -127,22 +132,27 @@ __device__ inline uint64_t match_expert(int e, bool valid, int bits) {
   return mask;
 }
 
-// One workgroup of 16 wavefronts; wavefront w owns the contiguous range
-// [w*R, (w+1)*R) of assignments.  Pass 1 counts each wavefront's
-// assignments per expert (LDS integer atomics: the counts do not depend on
-// the order of the adds); then one pass over the experts turns the
-// per-wavefront counts into exclusive bases (expert offset + earlier
-// wavefronts' counts) and writes counts and offsets; pass 2 walks the range
-// again and places each assignment at base + rank among equal experts of
-// its group of 64 lanes, the group's leader advancing the base.  The result
-// is the stable counting sort by (expert, assignment id).  Groups past the
-// end of a wavefront's range are skipped (wavefront-uniform test).
+// G workgroups of 16 wavefronts; workgroup g owns the contiguous slice
+// [g*S, (g+1)*S) of the assignments and wavefront w of it the contiguous
+// part [w*R, (w+1)*R) of that slice.  Pass 1: every workgroup counts all
+// assignments per expert, its own per wavefront and the others split into
+// those before and after its slice (LDS integer atomics: the counts do not
+// depend on the order of the adds).  One pass over the experts then turns
+// them into the expert offsets (written by workgroup 0 with the counts) and
+// each wavefront's exclusive base: expert offset + assignments of the
+// expert before the slice + those of earlier wavefronts in the slice.
+// Pass 2 walks the wavefront's part again and places each assignment at
+// base + rank among equal experts of its group of 64 lanes, the group's
+// leader advancing the base.  The result is the stable counting sort by
+// (expert, assignment id), the same for any G.  Groups past the end of a
+// range are skipped (wavefront-uniform test).
 __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* __restrict__ ids,
                                                                 int64_t A, int E,
                                                                 int32_t* __restrict__ counts,
                                                                 int32_t* __restrict__ offsets,
                                                                 int32_t* __restrict__ sorted_assign) {
   __shared__ int base[kBucketWaves][1024];   // per-wavefront counts, then bases
+  __shared__ int before[1024], after[1024];  // assignments outside the slice
   __shared__ int wsum[kBucketWaves];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -150,9 +160,13 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   int bits = 0;
   while ((1 << bits) < E) ++bits;
   for (int w = 0; w < kBucketWaves; ++w) base[w][tid] = 0;
+  before[tid] = 0;
+  after[tid] = 0;
   __syncthreads();
-  const int64_t R = ((A + kBucketWaves - 1) / kBucketWaves + 63) / 64 * 64;
-  const int64_t lo = min<int64_t>(A, wave * R), hi = min<int64_t>(A, lo + R);
+  const int64_t S = (A + gridDim.x - 1) / gridDim.x;
+  const int64_t slo = min<int64_t>(A, blockIdx.x * S), shi = min<int64_t>(A, slo + S);
+  const int64_t R = ((shi - slo + kBucketWaves - 1) / kBucketWaves + 63) / 64 * 64;
+  const int64_t lo = min<int64_t>(shi, slo + wave * R), hi = min<int64_t>(shi, lo + R);
   const uint64_t lower = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   // kBucketUnroll groups of 64 per round: all their id loads are issued first.
   for (int64_t b0 = lo; b0 < hi; b0 += 64 * kBucketUnroll) {
@@ -166,14 +180,30 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
     for (int u = 0; u < kBucketUnroll; ++u)
       if (b0 + u * 64 + lane < hi) atomicAdd(&base[wave][ev[u]], 1);
   }
+  // The assignments outside the slice, strided over all threads.
+  auto count_range = [&](int64_t rlo, int64_t rhi, int* dst) {
+    for (int64_t b0 = rlo; b0 < rhi; b0 += static_cast<int64_t>(kBucketThreads) * kBucketUnroll) {
+      int ev[kBucketUnroll];
+#pragma unroll
+      for (int u = 0; u < kBucketUnroll; ++u) {
+        const int64_t a = b0 + u * kBucketThreads + tid;
+        ev[u] = a < rhi ? ids[a] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < kBucketUnroll; ++u)
+        if (b0 + u * kBucketThreads + tid < rhi) atomicAdd(&dst[ev[u]], 1);
+    }
+  };
+  count_range(0, slo, before);
+  count_range(shi, A, after);
   __syncthreads();
-  // Thread e: total count, per-wavefront exclusive prefix; then the
-  // exclusive scan of the totals over experts.
+  // Thread e: total count, per-wavefront exclusive prefix inside the slice;
+  // then the exclusive scan of the totals over experts.
   const int e = tid;
-  int total = 0;
+  int total = before[e] + after[e];
   for (int w = 0; w < kBucketWaves; ++w) {
     const int c = base[w][e];
-    base[w][e] = total;
+    base[w][e] = total - after[e];           // before[e] + earlier wavefronts
     total += c;
   }
   int incl = total;
@@ -187,11 +217,11 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_kernel(const int32_t* _
   int off = incl - total;
   for (int w = 0; w < wave; ++w) off += wsum[w];
   for (int w = 0; w < kBucketWaves; ++w) base[w][e] += off;
-  if (e < E) {
+  if (blockIdx.x == 0 && e < E) {
     counts[e] = total;
     offsets[e] = off;
   }
-  if (e == 0) offsets[E] = static_cast<int32_t>(A);
+  if (blockIdx.x == 0 && e == 0) offsets[E] = static_cast<int32_t>(A);
   __syncthreads();
   for (int64_t b0 = lo; b0 < hi; b0 += 64 * kBucketUnroll) {
     int ev[kBucketUnroll];
@@ -299,7 +329,10 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
-  hipLaunchKernelGGL(bucket_kernel, dim3(1), dim3(kBucketThreads), 0, st, ids, m * k, e, counts, offsets,
+  const int64_t A = m * k;
+  const unsigned groups = static_cast<unsigned>(
+      std::min<int64_t>(kBucketMaxGroups, std::max<int64_t>(1, (A + kBucketSlice - 1) / kBucketSlice)));
+  hipLaunchKernelGGL(bucket_kernel, dim3(groups), dim3(kBucketThreads), 0, st, ids, A, e, counts, offsets,
                      sorted_assign);
   return hipGetLastError();
 }

@@ -27,7 +27,9 @@ def _route_check(logits, top_k):
 
 
 @pytest.mark.parametrize("m,e,k", [(1, 128, 8), (37, 128, 8), (300, 100, 4), (1000, 1024, 16),
-                                   (64, 8, 8), (50, 3, 1), (2048, 128, 8)])
+                                   (64, 8, 8), (50, 3, 1), (2048, 128, 8),
+                                   (256, 128, 8), (257, 128, 8),     # one / two bucketing workgroups
+                                   (5000, 64, 8)])                   # 16 workgroups, 2500-id slices
 def test_route_bit_exact(m, e, k):
     logits = inputs.logits_np(inputs.seed_for(4, m, "logits"), (m, e))
     _route_check(logits, k)
@@ -43,6 +45,16 @@ def test_route_ties_and_adversarial():
     logits = np.full((m, e), -1.0, np.float32)
     logits[:, 127] = 5.0                                 # one hot expert, others tied
     logits[::2, 0] = -0.0
+    _route_check(logits, 8)
+
+
+def test_bucket_skewed_across_workgroup_slices():
+    """All 4096 tokens tie and pick experts 0..7: every expert's 4096
+    assignments span all 16 bucketing slices, so each slice's base must count
+    the earlier slices exactly."""
+    _route_check(np.zeros((4096, 128), np.float32), 8)
+    logits = np.zeros((4096, 128), np.float32)
+    logits[1::2, 100:108] = 1.0                           # odd tokens: experts 100..107
     _route_check(logits, 8)
 
 
