@@ -256,10 +256,19 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict
   if (i >= m * h8) return;
   const int64_t t = i / h8, c = i % h8;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int j = 0; j < K; ++j) {
-    const half8v v = reinterpret_cast<const half8v*>(yp + (t * K + j) * hidden)[c];
+  // Slots in batches of 8: all loads of a batch are in flight before the
+  // first add (Yp is read once: nontemporal); the adds keep slot order.
+  for (int j0 = 0; j0 < K; j0 += 8) {
+    half8v v[8];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) s[r] += static_cast<float>(v[r]);
+    for (int u = 0; u < 8; ++u)
+      if (j0 + u < K)
+        v[u] = __builtin_nontemporal_load(reinterpret_cast<const half8v*>(yp + (t * K + j0 + u) * hidden) + c);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (j0 + u < K)
+#pragma unroll
+        for (int r = 0; r < 8; ++r) s[r] += static_cast<float>(v[u][r]);
   }
   float4* dst = reinterpret_cast<float4*>(y + t * hidden) + 2 * c;
   dst[0] = make_float4(s[0], s[1], s[2], s[3]);
