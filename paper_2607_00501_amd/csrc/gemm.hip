@@ -62,8 +62,9 @@ const char* gemm_tile_name(int64_t m, int64_t n) {
 
 namespace {
 
+// The tiles gemm_plan() can choose (QM_GEMM_PLAN may force any of them).
 #define QM_GEMM_TILES(X) \
-  X(128, 4, 1) X(64, 4, 1) X(64, 4, 2) X(64, 2, 1) X(64, 2, 2) X(32, 4, 1) X(32, 4, 2) \
+  X(128, 4, 1) X(64, 4, 1) X(64, 2, 2) \
   X(64, 1, 1) X(64, 1, 2) X(64, 1, 4) X(64, 1, 8) X(32, 1, 1) X(32, 1, 2) X(32, 1, 4) X(32, 1, 8)
 
 hipError_t launch_args(const QgemmArgs& a, int cu_count, hipStream_t st) {
