@@ -41,23 +41,31 @@ __device__ inline void dpp_step(float& bv, int& be) {
 }
 
 // Every lane ends with the wavefront's best (value, index): DPP exchanges
-// within each row of 16 lanes, then the four row winners are read out as
-// wave-uniform values and compared in a fixed order.
+// within each row of 16 lanes, then cross-row lane swaps between adjacent
+// rows and between the two halves.
 __device__ inline void wave_argmax(float& bv, int& be) {
   dpp_step<0xB1>(bv, be);    // quad_perm [1,0,3,2]
   dpp_step<0x4E>(bv, be);    // quad_perm [2,3,0,1]
   dpp_step<0x124>(bv, be);   // row_ror:4
   dpp_step<0x128>(bv, be);   // row_ror:8
-  float v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bv), 0));
-  int e = __builtin_amdgcn_readlane(be, 0);
-#pragma unroll
-  for (int r = 1; r < 4; ++r) {
-    const float ov = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, bv), 16 * r));
-    const int oe = __builtin_amdgcn_readlane(be, 16 * r);
-    take_better(v, e, ov, oe);
+  // Every lane now holds its 16-lane row's best.  v_permlane16_swap of a
+  // value with itself gives each lane the pair {its row's, the adjacent
+  // row's}; v_permlane32_swap the same across the two halves.  The order is
+  // symmetric, so the better of each pair is the same in every lane.
+  {
+    const auto v = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(int, bv), __builtin_bit_cast(int, bv), false, false);
+    const auto e = __builtin_amdgcn_permlane16_swap(be, be, false, false);
+    bv = __builtin_bit_cast(float, static_cast<int>(v[0]));
+    be = static_cast<int>(e[0]);
+    take_better(bv, be, __builtin_bit_cast(float, static_cast<int>(v[1])), static_cast<int>(e[1]));
   }
-  bv = v;
-  be = e;
+  {
+    const auto v = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(int, bv), __builtin_bit_cast(int, bv), false, false);
+    const auto e = __builtin_amdgcn_permlane32_swap(be, be, false, false);
+    bv = __builtin_bit_cast(float, static_cast<int>(v[0]));
+    be = static_cast<int>(e[0]);
+    take_better(bv, be, __builtin_bit_cast(float, static_cast<int>(v[1])), static_cast<int>(e[1]));
+  }
 }
 
 // PER = logits per lane (n_experts <= 64 * PER), a power of two.
