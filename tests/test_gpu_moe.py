@@ -29,7 +29,8 @@ def _route_check(logits, top_k):
 @pytest.mark.parametrize("m,e,k", [(1, 128, 8), (37, 128, 8), (300, 100, 4), (1000, 1024, 16),
                                    (64, 8, 8), (50, 3, 1), (2048, 128, 8),
                                    (256, 128, 8), (257, 128, 8),     # one / two bucketing workgroups
-                                   (5000, 64, 8)])                   # 16 workgroups, 2500-id slices
+                                   (5000, 64, 8),                    # 16 bucketing workgroups
+                                   (120, 256, 16), (90, 200, 6)])    # 4 logits per lane
 def test_route_bit_exact(m, e, k):
     logits = inputs.logits_np(inputs.seed_for(4, m, "logits"), (m, e))
     _route_check(logits, k)
