@@ -195,7 +195,7 @@ struct Cfg {
   static constexpr int kALoads = BM * (kBK / 8) / kSliceThreads;
   static_assert(kALoads >= 1 && BM * (kBK / 8) % kSliceThreads == 0, "A tile split");
   static_assert(DEPTH >= 2 && DEPTH <= 3, "K steps of loads in flight");
-  static constexpr int kSlots = DEPTH + 1;                       // B register slots
+  static constexpr int kSlots = DEPTH + 1;                       // slots of B (registers or LDS)
   // LDS stage: the A tiles of the WK slices (BM rows x 128 B each), then,
   // when B also goes through LDS, per wavefront and weight matrix the two
   // 1 KiB code chunks and their 2 x 64 scales (2304 B).  B goes through LDS
@@ -331,8 +331,10 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   const uint32_t bq_lane = (lane & 31) * 16 + (lane >> 5) * 8;
   const uint32_t bs_lane = lane & 31;
 
-  // DEPTH + 1 register sets of raw B operands and LDS stages of A (step t
-  // lives in slot t % (DEPTH + 1)), always indexed by constants.
+  // DEPTH + 1 slots of raw B operands (registers, or LDS stages when B
+  // goes through LDS) and kAStages LDS stages of A; step t lives in slot
+  // t % (DEPTH + 1), always indexed by constants.  rb / rs are used only
+  // when B is loaded into registers.
   constexpr int NS = C::kSlots;
   u32x2 rb[NS][NB][2][2];                                  // [slot][matrix][chunk][column half]
   uint32_t rs[NS][NB][2][2];
