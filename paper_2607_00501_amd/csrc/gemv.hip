@@ -404,9 +404,10 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
 // enough wavefronts per panel for one pass of 8 chunks each (4 at K = 1024,
 // 12 at K = 3072), at most 16; Q8: 8 wavefronts (fewer only if there are
 // fewer groups).  Smaller matrices use the sub-panel kernel with 8
-// wavefronts per workgroup and the smallest row count (8, 16 or 32) that
-// keeps the grid at <= 2 workgroups per CU; activations are staged in LDS
-// for K <= 4096 and read from global memory beyond.
+// wavefronts per workgroup and the smallest row count (8, 16 or 32; from 4
+// for N <= 1024 with K >= 2048) that keeps the grid at <= 2 workgroups per
+// CU; activations are staged in LDS for K <= 4096 and read from global
+// memory beyond.
 GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count) {
   // Tuning sweeps only: QM_GEMV_PLAN="rows,waves,x_in_lds" forces the plan.
   static const GemvPlan forced = [] {
@@ -443,7 +444,7 @@ GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count) {
     p.xlds = 0;
     return p;
   }
-  int subr = 8;
+  int subr = (npad <= 1024 && k >= 2048) ? 4 : 8;
   while (subr < 32 && npad / subr > 2 * cu_count) subr *= 2;
   p.subr = subr;
   p.waves = 8;
