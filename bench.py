@@ -92,12 +92,28 @@ class GroupCall:
             raise RuntimeError(self.lib.qm_last_error().decode())
 
 
+class SwigluCall:
+    """One pre-marshalled qmatmul_gemv_swiglu call (gate/up pair, h out)."""
+
+    def __init__(self, lib, wg, wu, x, h):
+        self.lib, self.keep = lib, (wg, wu, x, h)
+        self.dg, self.du = wg.c(), wu.c()
+        self.xp, self.hp = ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(h.data_ptr())
+
+    def __call__(self, stream):
+        st = self.lib.qmatmul_gemv_swiglu(ctypes.byref(self.dg), ctypes.byref(self.du), self.xp, self.hp, stream)
+        if st != 0:
+            raise RuntimeError(self.lib.qm_last_error().decode())
+
+
 GROUPS = (("q", "k", "v"), ("o",), ("gate", "up"), ("down",))
 
 
-def build_grouped_stack(model, cfg_id, fmt, torch, B, inputs, workloads):
+def build_grouped_stack(model, cfg_id, fmt, torch, B, inputs, workloads, swiglu=False):
     """The same decode step with one launch per group of projections that
-    read the same input (q/k/v, o, gate/up, down per layer; the lm_head)."""
+    read the same input (q/k/v, o, gate/up, down per layer; the lm_head).
+    swiglu: the gate/up pair runs as qmatmul_gemv_swiglu, writing
+    silu(gate) * up instead of the two projections."""
     lib = B.lib()
     shapes = {name: (k, n) for name, k, n in model["layer"]}
     calls, nbytes = [], 0
@@ -113,7 +129,10 @@ def build_grouped_stack(model, cfg_id, fmt, torch, B, inputs, workloads):
                 del w
                 ys.append(torch.empty(n, dtype=torch.float32, device="cuda"))
                 nbytes += workloads.q4_bytes(kk, n) if fmt == B.Q4_G32 else workloads.q8_bytes(kk, n)
-            calls.append(GroupCall(lib, B, wds, [x] * len(group), ys))
+            if swiglu and group == ("gate", "up"):
+                calls.append(SwigluCall(lib, wds[0], wds[1], x, ys[0]))
+            else:
+                calls.append(GroupCall(lib, B, wds, [x] * len(group), ys))
     k, n = model["lm_head"]
     w = inputs.weights_dev(inputs.seed_for(cfg_id, model["layers"], "lm_head"), (n, k))
     wd = B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE)
@@ -278,18 +297,20 @@ def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
     del g
 
     # Grouped dispatch (qmatmul_gemv_grouped): the Qwen3-0.6B and Llama-3.2-3B
-    # Q4 steps with q/k/v and gate/up each in one launch (113 launches/token).
+    # Q4 steps with q/k/v and gate/up each in one launch (113 launches/token);
+    # and the same with gate/up as the fused SwiGLU pair.
     for model, cfg_id, tag in ((workloads.QWEN3_06B, 1, "qwen3-0.6b"), (workloads.LLAMA32_3B, 2, "llama3.2-3b")):
-        calls, nbytes = build_grouped_stack(model, cfg_id, B.Q4_G32, torch, B, inputs, workloads)
-        g = capture(torch, lambda s: [c(s) for c in calls])
-        t, _ = time_graph(torch, g, steps, warmup)
-        out[f"{tag}_decode_q4_grouped_dispatch"] = {
-            "launches_per_token": len(calls), "tokens_per_s": round(steps / t, 2),
-            "ms_per_token": round(t / steps * 1e3, 4), "weight_GBps": round(nbytes * steps / t / 1e9, 2),
-            "frac_hbm_peak": round(nbytes * steps / t / 1e9 / HBM_PEAK_GBS, 4)}
-        log(f"{tag} grouped dispatch: {out[f'{tag}_decode_q4_grouped_dispatch']}")
-        del g, calls
-        torch.cuda.empty_cache()
+        for swiglu, key in ((False, "grouped_dispatch"), (True, "grouped_swiglu")):
+            calls, nbytes = build_grouped_stack(model, cfg_id, B.Q4_G32, torch, B, inputs, workloads, swiglu)
+            g = capture(torch, lambda s: [c(s) for c in calls])
+            t, _ = time_graph(torch, g, steps, warmup)
+            out[f"{tag}_decode_q4_{key}"] = {
+                "launches_per_token": len(calls), "tokens_per_s": round(steps / t, 2),
+                "ms_per_token": round(t / steps * 1e3, 4), "weight_GBps": round(nbytes * steps / t / 1e9, 2),
+                "frac_hbm_peak": round(nbytes * steps / t / 1e9 / HBM_PEAK_GBS, 4)}
+            log(f"{tag} {key}: {out[f'{tag}_decode_q4_{key}']}")
+            del g, calls
+            torch.cuda.empty_cache()
 
     # Llama-3.2-3B decode stacks, Q4 and Q8
     for fmt, tag in ((B.Q4_G32, "q4"), (B.Q8_G32, "q8")):

@@ -126,6 +126,17 @@ qm_status qm_repack(const qm_qweight* src, const qm_qweight* dst, void* stream);
  * Single kernel launch, no workspace, deterministic. */
 qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* stream);
 
+/* SwiGLU front half of a feed-forward block at batch 1 (Sec. 3.3: the
+ * activation fused into the producing kernel, saving a launch and a
+ * global-memory round trip):
+ *   h[n] = silu(g[n]) * u[n],  g = Wg' x,  u = Wu' x,  silu(z) = z / (1 + e^-z).
+ * w_gate, w_up: DEVICE layout, batch 1, the same format (Q4 or Q8) and the
+ * same n and k.  x: fp16 [k] (16-byte aligned); h: fp32 [n].  g and u are
+ * accumulated as in qmatmul_gemv (fp32), in one pass over the same rows of
+ * both matrices.  Deterministic. */
+qm_status qmatmul_gemv_swiglu(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, float* h,
+                              void* stream);
+
 /* Grouped decode GEMV (Sec. 3.3: fusing a sequence of operators removes a
  * launch each, which matters most in decode; e.g. the q/k/v projections of
  * a layer, which share x, or its gate and up projections):

@@ -156,6 +156,13 @@ def gemv(qbytes, s16, fmt, x_f16) -> np.ndarray:
     return w @ x
 
 
+def gemv_swiglu(gq, gs16, uq, us16, fmt, x_f16) -> np.ndarray:
+    """h[n] = silu((Wg' x)[n]) * (Wu' x)[n]: the SwiGLU front half of a
+    feed-forward block at batch 1 (Sec. 3.3: fusing the activation into the
+    producing kernel), fp64."""
+    return silu(gemv(gq, gs16, fmt, x_f16)) * gemv(uq, us16, fmt, x_f16)
+
+
 def gemm(qbytes, s16, fmt, x_f16) -> np.ndarray:
     """Y[m][n] = sum_k X[m][k] * w'[n][k], in fp64 (fp64 result [M][N])."""
     w = dequantise(qbytes, s16, fmt).astype(np.float64)

@@ -25,7 +25,8 @@ STATUS = {0: "QM_OK", 1: "QM_EINVAL", 2: "QM_ESHAPE", 3: "QM_EALIGN", 4: "QM_EFO
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libqmatmul.so")
 
 EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "qm_repack",
-           "qmatmul_gemv", "qmatmul_gemv_grouped", "qmatmul_gemm", "qmatmul_gemm_grouped",
+           "qmatmul_gemv", "qmatmul_gemv_swiglu", "qmatmul_gemv_grouped", "qmatmul_gemm",
+           "qmatmul_gemm_grouped",
            "qmoe_workspace_bytes", "qmoe_route",
            "qmoe_grouped_gemm", "qm_device_config")
 
@@ -62,6 +63,7 @@ def lib() -> ctypes.CDLL:
             "qm_dequantise": [W, vp, vp],
             "qm_repack": [W, W, vp],
             "qmatmul_gemv": [W, vp, vp, vp],
+            "qmatmul_gemv_swiglu": [W, W, vp, vp, vp],
             "qmatmul_gemv_grouped": [i32, W, ctypes.POINTER(vp), ctypes.POINTER(vp), vp],
             "qmatmul_gemm": [W, vp, i64, vp, vp],
             "qmatmul_gemm_grouped": [i32, W, vp, i64, ctypes.POINTER(vp), vp],
@@ -164,6 +166,17 @@ def qmatmul_gemv(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None
     if out is None:
         out = torch.empty(w.n, dtype=torch.float32, device=x.device)
     _check(lib().qmatmul_gemv(ctypes.byref(w.c()), _ptr(x), _ptr(out), _stream(stream)))
+    return out
+
+
+def qmatmul_gemv_swiglu(w_gate: QWeight, w_up: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None,
+                        stream=None):
+    """x: fp16 [k] -> h = silu(Wg x) * (Wu x), fp32 [n]."""
+    assert x.dtype == torch.float16 and x.is_contiguous() and x.numel() == w_gate.k
+    if out is None:
+        out = torch.empty(w_gate.n, dtype=torch.float32, device=x.device)
+    _check(lib().qmatmul_gemv_swiglu(ctypes.byref(w_gate.c()), ctypes.byref(w_up.c()), _ptr(x), _ptr(out),
+                                     _stream(stream)))
     return out
 
 

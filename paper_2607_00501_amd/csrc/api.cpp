@@ -180,6 +180,29 @@ qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* s
                   "qmatmul_gemv");
 }
 
+qm_status qmatmul_gemv_swiglu(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, float* h,
+                              void* stream) {
+  qm_status st = check_weight(w_gate, "qmatmul_gemv_swiglu(w_gate)");
+  if (st != QM_OK) return st;
+  if ((st = check_weight(w_up, "qmatmul_gemv_swiglu(w_up)")) != QM_OK) return st;
+  if (w_gate->layout != QM_LAYOUT_DEVICE || w_up->layout != QM_LAYOUT_DEVICE)
+    return fail(QM_ELAYOUT, "qmatmul_gemv_swiglu: weights must be in DEVICE layout");
+  if (w_gate->batch != 1 || w_up->batch != 1) return fail(QM_ESHAPE, "qmatmul_gemv_swiglu: batch must be 1");
+  if (w_up->format != w_gate->format) return fail(QM_EFORMAT, "qmatmul_gemv_swiglu: formats differ");
+  if (w_up->n != w_gate->n || w_up->k != w_gate->k)
+    return fail(QM_ESHAPE, "qmatmul_gemv_swiglu: gate and up shapes differ");
+  if (w_gate->n > INT32_MAX / 2) return fail(QM_ESHAPE, "qmatmul_gemv_swiglu: n too large");
+  if (w_gate->n > 0 && (!x || !h)) return fail(QM_EINVAL, "qmatmul_gemv_swiglu: null x or h");
+  if (!aligned16(x)) return fail(QM_EALIGN, "qmatmul_gemv_swiglu: x must be 16-byte aligned");
+  if (!aligned4(h)) return fail(QM_EALIGN, "qmatmul_gemv_swiglu: h must be 4-byte aligned");
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_gemv_swiglu(w_gate->format, static_cast<const uint8_t*>(w_gate->qdata), w_gate->scales,
+                                     static_cast<const uint8_t*>(w_up->qdata), w_up->scales, x, h, w_gate->n,
+                                     w_gate->k, d->cu_count, static_cast<hipStream_t>(stream)),
+                  "qmatmul_gemv_swiglu");
+}
+
 qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_t* const* x, float* const* y,
                                void* stream) {
   static_assert(QM_GEMV_GROUP_MAX == kGemvGroupMax, "group size");

@@ -190,15 +190,20 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
 constexpr int kSubU = 8;
 
 // One workgroup's share of one matrix: `block` of `nblocks` = N/SUBR.
-template <int FMT, int SUBR, int WAVES, bool XLDS>
+// SWIGLU: the same rows of a second matrix (q2, s2) go through the same
+// loads-then-dots pass, and the workgroup writes silu(a) * b of the two
+// row sums a, b (the SwiGLU front half of a feed-forward block).
+template <int FMT, int SUBR, int WAVES, bool XLDS, bool SWIGLU = false>
 __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
+                                              const uint8_t* __restrict__ q2, const uint16_t* __restrict__ s2,
                                               const uint16_t* __restrict__ x, float* __restrict__ y, int n_rows,
                                               int groups, int64_t block, int64_t nblocks) {
   constexpr int CL = 64 / SUBR;
   constexpr int NW = FMT == QM_Q4_G32 ? 1 : 2;
+  constexpr int NM = SWIGLU ? 2 : 1;                  // matrices
   constexpr int U = kSubU;
   extern __shared__ uint4 xs[];                       // groups * 4 uint4 (K halves) if XLDS
-  __shared__ float part[WAVES][SUBR];
+  __shared__ float part[NM][WAVES][SUBR];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = lane % SUBR, cl = lane / SUBR;
@@ -215,23 +220,30 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
   const DequantConsts dk;
   const uint4* xg = reinterpret_cast<const uint4*>(x);
 
-  float acc = 0.0f;
+  float acc[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) acc[m] = 0.0f;
   for (int it = 0; it < iters; ++it) {
-    uint4 wv[U][NW];
-    uint32_t sv[U];
+    uint4 wv[U][NM][NW];
+    uint32_t sv[U][NM];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int c = first + (it * U + u) * stride;
       if (c < groups) {
         const int64_t ch = ch0 + c;
-        if (FMT == QM_Q4_G32) {
-          wv[u][0] = *reinterpret_cast<const uint4*>(q + (ch * 64 + row) * 16);
-        } else {
-          const uint8_t* base = q + ch * 2048 + row * 16;
-          wv[u][0] = *reinterpret_cast<const uint4*>(base);
-          wv[u][NW - 1] = *reinterpret_cast<const uint4*>(base + 1024);
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+          const uint8_t* qm = m == 0 ? q : q2;
+          const uint16_t* sm = m == 0 ? s : s2;
+          if (FMT == QM_Q4_G32) {
+            wv[u][m][0] = *reinterpret_cast<const uint4*>(qm + (ch * 64 + row) * 16);
+          } else {
+            const uint8_t* base = qm + ch * 2048 + row * 16;
+            wv[u][m][0] = *reinterpret_cast<const uint4*>(base);
+            wv[u][m][NW - 1] = *reinterpret_cast<const uint4*>(base + 1024);
+          }
+          sv[u][m] = sm[ch * 64 + row];
         }
-        sv[u] = s[ch * 64 + row];
       }
     }
     if (XLDS && it == 0) {
@@ -256,30 +268,43 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
             xv[4 * i] = t.x; xv[4 * i + 1] = t.y; xv[4 * i + 2] = t.z; xv[4 * i + 3] = t.w;
           }
         }
-        float d;
-        if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][0], xv, dk);
-        else d = dot_q8_half(wv[u][0], xv) + dot_q8_half(wv[u][NW - 1], xv + 8);
-        acc = fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sv[u]))), d, acc);
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+          float d;
+          if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][m][0], xv, dk);
+          else d = dot_q8_half(wv[u][m][0], xv) + dot_q8_half(wv[u][m][NW - 1], xv + 8);
+          acc[m] = fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sv[u][m]))), d, acc[m]);
+        }
       }
     }
   }
 #pragma unroll
-  for (int off = SUBR; off < 64; off <<= 1) acc += __shfl_xor(acc, off);
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int off = SUBR; off < 64; off <<= 1) acc[m] += __shfl_xor(acc[m], off);
+  auto out = [&](float a, float b) { return SWIGLU ? a / (1.0f + expf(-a)) * b : a; };
   if (WAVES == 1) {
     if (lane < SUBR) {
       const int64_t n = panel * 64 + row;
-      if (n < n_rows) y[n] = acc;
+      if (n < n_rows) y[n] = out(acc[0], acc[NM - 1]);
     }
     return;
   }
-  if (cl == 0) part[wave][r] = acc;
+  if (cl == 0) {
+#pragma unroll
+    for (int m = 0; m < NM; ++m) part[m][wave][r] = acc[m];
+  }
   __syncthreads();
   if (wave == 0 && lane < SUBR) {
-    float t = part[0][lane];
+    float t[NM];
 #pragma unroll
-    for (int w = 1; w < WAVES; ++w) t += part[w][lane];
+    for (int m = 0; m < NM; ++m) {
+      t[m] = part[m][0][lane];
+#pragma unroll
+      for (int w = 1; w < WAVES; ++w) t[m] += part[m][w][lane];
+    }
     const int64_t n = panel * 64 + row;
-    if (n < n_rows) y[n] = t;
+    if (n < n_rows) y[n] = out(t[0], t[NM - 1]);
   }
 }
 
@@ -291,7 +316,19 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(const uint8_t* __r
                                                               int groups) {
   // All kernel arguments in one batch of scalar loads (one round trip).
   asm volatile("" ::"s"(q), "s"(s), "s"(x), "s"(y), "s"(n_rows), "s"(groups));
-  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, x, y, n_rows, groups, blockIdx.x, gridDim.x);
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, nullptr, nullptr, x, y, n_rows, groups, blockIdx.x, gridDim.x);
+}
+
+// SwiGLU pair: h = silu(Wg' x) * (Wu' x) over the same rows, one launch.
+template <int FMT, int SUBR, int WAVES, bool XLDS>
+__global__ __launch_bounds__(WAVES * 64) void gemv_swiglu_kernel(const uint8_t* __restrict__ qg,
+                                                                 const uint16_t* __restrict__ sg,
+                                                                 const uint8_t* __restrict__ qu,
+                                                                 const uint16_t* __restrict__ su,
+                                                                 const uint16_t* __restrict__ x,
+                                                                 float* __restrict__ h, int n_rows, int groups) {
+  asm volatile("" ::"s"(qg), "s"(sg), "s"(qu), "s"(su), "s"(x), "s"(h), "s"(n_rows), "s"(groups));
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS, true>(qg, sg, qu, su, x, h, n_rows, groups, blockIdx.x, gridDim.x);
 }
 
 // A group of independent GEMVs with one K in one launch: the workgroup
@@ -325,7 +362,7 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_sub_group_kernel(GemvGroup g)
   const int64_t local = b - first;
   const int64_t nb = padded_rows(n) / SUBR;
   if (local >= nb) return;                             // padding workgroup (whole group exits)
-  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, x, y, n, groups, local, nb);
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, nullptr, nullptr, x, y, n, groups, local, nb);
 }
 
 template <int FMT, int SUBR, bool XLDS>
@@ -469,6 +506,53 @@ hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count,
   if (fmt == QM_Q4_G32)
     return plan.xlds ? launch_sub<QM_Q4_G32, true>(plan, g, st) : launch_sub<QM_Q4_G32, false>(plan, g, st);
   return plan.xlds ? launch_sub<QM_Q8_G32, true>(plan, g, st) : launch_sub<QM_Q8_G32, false>(plan, g, st);
+}
+
+namespace {
+
+template <int FMT, int SUBR, bool XLDS>
+hipError_t launch_swiglu_rows(const uint8_t* qg, const uint16_t* sg, const uint8_t* qu, const uint16_t* su,
+                              const uint16_t* x, float* h, int64_t n, int groups, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(padded_rows(n) / SUBR));
+  const size_t lds = XLDS ? static_cast<size_t>(groups) * 64 : 0;
+  hipLaunchKernelGGL((gemv_swiglu_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, qg, sg, qu, su, x, h,
+                     static_cast<int>(n), groups);
+  return hipGetLastError();
+}
+
+template <int FMT>
+hipError_t launch_swiglu_fmt(const GemvPlan& plan, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
+                             const uint16_t* su, const uint16_t* x, float* h, int64_t n, int groups,
+                             hipStream_t st) {
+  switch (plan.subr) {
+    case 4: return plan.xlds ? launch_swiglu_rows<FMT, 4, true>(qg, sg, qu, su, x, h, n, groups, st)
+                             : launch_swiglu_rows<FMT, 4, false>(qg, sg, qu, su, x, h, n, groups, st);
+    case 8: return plan.xlds ? launch_swiglu_rows<FMT, 8, true>(qg, sg, qu, su, x, h, n, groups, st)
+                             : launch_swiglu_rows<FMT, 8, false>(qg, sg, qu, su, x, h, n, groups, st);
+    case 16: return plan.xlds ? launch_swiglu_rows<FMT, 16, true>(qg, sg, qu, su, x, h, n, groups, st)
+                              : launch_swiglu_rows<FMT, 16, false>(qg, sg, qu, su, x, h, n, groups, st);
+    default: return plan.xlds ? launch_swiglu_rows<FMT, 32, true>(qg, sg, qu, su, x, h, n, groups, st)
+                              : launch_swiglu_rows<FMT, 32, false>(qg, sg, qu, su, x, h, n, groups, st);
+  }
+}
+
+}  // namespace
+
+// The sub-panel plan of one matrix of N rows (each workgroup covers its rows
+// of both matrices); matrices large enough for the panel kernel use 32-row
+// workgroups, 8 wavefronts.
+hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
+                              const uint16_t* su, const uint16_t* x, float* h, int64_t n, int64_t k,
+                              int cu_count, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  GemvPlan plan = gemv_plan(fmt, n, k, cu_count);
+  if (plan.subr == kPanel) {
+    plan.subr = 32;
+    plan.xlds = k <= 4096 ? 1 : 0;
+  }
+  const int groups = static_cast<int>(k / kGroup);
+  return fmt == QM_Q4_G32 ? launch_swiglu_fmt<QM_Q4_G32>(plan, qg, sg, qu, su, x, h, n, groups, st)
+                          : launch_swiglu_fmt<QM_Q8_G32>(plan, qg, sg, qu, su, x, h, n, groups, st);
 }
 
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,

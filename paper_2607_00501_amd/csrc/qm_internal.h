@@ -88,6 +88,9 @@ struct GemvGroup {
   int count;
   int groups;                     // K / 32
 };
+hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
+                              const uint16_t* su, const uint16_t* x, float* h, int64_t n, int64_t k,
+                              int cu_count, hipStream_t st);
 hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count, hipStream_t st);
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
                        int64_t n, int64_t k, int cu_count, hipStream_t st);

@@ -142,6 +142,23 @@ def test_error_text_is_thread_local():
     assert B.qm_last_error() == main_msg and "format" in main_msg
 
 
+def test_gemv_swiglu_validation():
+    L = B.lib()
+    x, h = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x40000)
+    w = _fake_weight()
+    call = lambda g, u, xp=x, hp=h: L.qmatmul_gemv_swiglu(ctypes.byref(g), ctypes.byref(u), xp, hp, None)
+    assert L.qmatmul_gemv_swiglu(None, ctypes.byref(w), x, h, None) == 1        # null descriptor
+    assert call(w, _fake_weight(fmt=2)) == 4                                     # formats differ
+    assert call(w, _fake_weight(n=65)) == 2                                      # n differs
+    assert call(w, _fake_weight(k=96)) == 2                                      # k differs
+    assert call(w, _fake_weight(layout=0)) == 5                                  # not DEVICE layout
+    assert call(w, _fake_weight(batch=2)) == 2                                   # batch != 1
+    assert call(w, w, xp=ctypes.c_void_p(0x30004)) == 3                          # x misaligned
+    assert call(w, w, hp=ctypes.c_void_p(0x40002)) == 3                          # h misaligned
+    assert call(w, w, xp=None) == 1                                              # null x
+    assert B.qm_last_error()
+
+
 def test_gemv_grouped_validation():
     L = B.lib()
     x0, y0 = 0x30000, 0x40000

@@ -302,6 +302,33 @@ def test_silu_identities():
     assert abs(O.silu(np.array([1.0]))[0] - 1.0 / (1.0 + math.exp(-1.0))) < 1e-16
 
 
+def test_gemv_swiglu_hand_example():
+    """x = e_0 over integer-grid weights (scale 1): (Wg x)[n] = Wg[n][0] and
+    (Wu x)[n] = Wu[n][0], so h[n] = silu(Wg[n][0]) * Wu[n][0], evaluated here
+    with scalar math.exp; and h equals the hidden vector of expert_ffn."""
+    rng = np.random.default_rng(29)
+    n, k = 48, 64
+    wg = rng.integers(-7, 8, size=(n, k)); wg[:, ::32] = 7
+    wu = rng.integers(-7, 8, size=(n, k)); wu[:, ::32] = 7
+    for fmt in (O.Q4, O.Q8):
+        gq, gs = O.quantise(wg.astype(np.float32), fmt)
+        uq, us = O.quantise(wu.astype(np.float32), fmt)
+        x = np.zeros(k, np.float16)
+        x[0] = 1.0
+        h = O.gemv_swiglu(O.pack(gq, fmt), gs, O.pack(uq, fmt), us, fmt, x)
+        dg = O.dequantise(O.pack(gq, fmt), gs, fmt).astype(np.float64)
+        du = O.dequantise(O.pack(uq, fmt), us, fmt).astype(np.float64)
+        for i in range(n):
+            a, b = float(dg[i, 0]), float(du[i, 0])
+            want = a / (1.0 + math.exp(-a)) * b
+            assert abs(h[i] - want) <= 1e-13 * max(1.0, abs(want))
+        if fmt == O.Q4:
+            assert np.array_equal(dg, wg) and np.array_equal(du, wu)        # scale 1: exact grid
+        # the same h as inside the SwiGLU expert (y = Wd h with Wd = identity)
+        y = O.expert_ffn(x.astype(np.float64)[None], dg, du, np.eye(n))
+        assert np.allclose(y[0], h, rtol=1e-15, atol=0)
+
+
 def _grid_expert(rng, n, k):
     w = rng.integers(-7, 8, size=(n, k))
     w[:, ::32] = 7
