@@ -340,62 +340,67 @@ def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
 
 def extra_prefill(torch, B, inputs, workloads, steps, warmup, lib):
     out = {}
-    # Llama-3.2-1B prefill GEMM stacks
+    # Llama-3.2-1B prefill GEMM stacks: Q4 with one launch per GEMM and with
+    # grouped dispatch; Q8 weights with grouped dispatch.
     model = workloads.LLAMA32_1B_PREFILL
-    wds = []
-    for layer in range(model["layers"]):
-        for name, k, n in model["layer"]:
-            w = inputs.weights_dev(inputs.seed_for(3, layer, name), (n, k))
-            wds.append((B.qm_repack(B.qm_quantise(w, B.Q4_G32), B.LAYOUT_DEVICE), k, n))
-            del w
-    for m in model["m_sweep"]:
-        xs = {k: inputs.activations_dev(inputs.seed_for(3, 0, "x", k), (m, k)) for k in {k for _, k, _ in wds}}
-        ys = [torch.empty((m, n), device="cuda") for _, _, n in wds]
-        descs = [wd.c() for wd, _, _ in wds]
-        def run(s, xs=xs, ys=ys, descs=descs, m=m):
-            for d, (wd, k, n), yv in zip(descs, wds, ys):
-                st = lib.qmatmul_gemm(ctypes.byref(d), ctypes.c_void_p(xs[k].data_ptr()), m,
-                                      ctypes.c_void_p(yv.data_ptr()), s)
-                if st:
-                    raise RuntimeError(lib.qm_last_error().decode())
-        g = capture(torch, run)
-        t, _ = time_graph(torch, g, max(steps // 2, 5), warmup)
-        flops = 2.0 * m * sum(k * n for _, k, n in wds)
-        tf = flops * max(steps // 2, 5) / t / 1e12
-        out[f"llama3.2-1b_prefill_m{m}"] = {"tokens_per_s": round(m * max(steps // 2, 5) / t, 1),
-                                            "stack_TFLOPs": round(tf, 2),
-                                            "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4)}
-        log(f"prefill m={m}: {out[f'llama3.2-1b_prefill_m{m}']}")
-        del g
-
-        # Grouped dispatch (qmatmul_gemm_grouped): q/k/v and gate/up of a layer
-        # each in one launch (64 launches for the 16 layers).
-        per_layer = len(model["layer"])
-        names = [name for name, _, _ in model["layer"]]
-        calls = []
+    reps = max(steps // 2, 5)
+    for fmt, tag in ((B.Q4_G32, ""), (B.Q8_G32, "_q8")):
+        wds = []
         for layer in range(model["layers"]):
-            base = layer * per_layer
-            for group in GROUPS:
-                idx = [base + names.index(nm) for nm in group]
-                k = wds[idx[0]][1]
-                n_, descs_g, yp = B.gemm_group_args([wds[i][0] for i in idx], [ys[i] for i in idx])
-                calls.append((n_, descs_g, ctypes.c_void_p(xs[k].data_ptr()), yp))
+            for name, k, n in model["layer"]:
+                w = inputs.weights_dev(inputs.seed_for(3, layer, name), (n, k))
+                wds.append((B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE), k, n))
+                del w
+        for m in model["m_sweep"]:
+            xs = {k: inputs.activations_dev(inputs.seed_for(3, 0, "x", k), (m, k)) for k in {k for _, k, _ in wds}}
+            ys = [torch.empty((m, n), device="cuda") for _, _, n in wds]
+            flops = 2.0 * m * sum(k * n for _, k, n in wds)
+            if fmt == B.Q4_G32:
+                descs = [wd.c() for wd, _, _ in wds]
 
-        def run_g(s, calls=calls, m=m):
-            for n_, descs_g, xp, yp in calls:
-                st = lib.qmatmul_gemm_grouped(n_, descs_g, xp, m, yp, s)
-                if st:
-                    raise RuntimeError(lib.qm_last_error().decode())
-        g = capture(torch, run_g)
-        t, _ = time_graph(torch, g, max(steps // 2, 5), warmup)
-        tf = flops * max(steps // 2, 5) / t / 1e12
-        out[f"llama3.2-1b_prefill_m{m}_grouped_dispatch"] = {
-            "launches_per_stack": len(calls), "tokens_per_s": round(m * max(steps // 2, 5) / t, 1),
-            "stack_TFLOPs": round(tf, 2), "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4)}
-        log(f"prefill m={m} grouped: {out[f'llama3.2-1b_prefill_m{m}_grouped_dispatch']}")
-        del g, calls, ys, xs
-    del wds
-    torch.cuda.empty_cache()
+                def run(s, xs=xs, ys=ys, descs=descs, m=m):
+                    for d, (wd, k, n), yv in zip(descs, wds, ys):
+                        st = lib.qmatmul_gemm(ctypes.byref(d), ctypes.c_void_p(xs[k].data_ptr()), m,
+                                              ctypes.c_void_p(yv.data_ptr()), s)
+                        if st:
+                            raise RuntimeError(lib.qm_last_error().decode())
+                g = capture(torch, run)
+                t, _ = time_graph(torch, g, reps, warmup)
+                tf = flops * reps / t / 1e12
+                out[f"llama3.2-1b_prefill_m{m}"] = {"tokens_per_s": round(m * reps / t, 1),
+                                                    "stack_TFLOPs": round(tf, 2),
+                                                    "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4)}
+                log(f"prefill m={m}: {out[f'llama3.2-1b_prefill_m{m}']}")
+                del g
+
+            # Grouped dispatch (qmatmul_gemm_grouped): q/k/v and gate/up of a
+            # layer each in one launch (64 launches for the 16 layers).
+            per_layer = len(model["layer"])
+            names = [name for name, _, _ in model["layer"]]
+            calls = []
+            for layer in range(model["layers"]):
+                base = layer * per_layer
+                for group in GROUPS:
+                    idx = [base + names.index(nm) for nm in group]
+                    k = wds[idx[0]][1]
+                    n_, descs_g, yp = B.gemm_group_args([wds[i][0] for i in idx], [ys[i] for i in idx])
+                    calls.append((n_, descs_g, ctypes.c_void_p(xs[k].data_ptr()), yp))
+
+            def run_g(s, calls=calls, m=m):
+                for n_, descs_g, xp, yp in calls:
+                    st = lib.qmatmul_gemm_grouped(n_, descs_g, xp, m, yp, s)
+                    if st:
+                        raise RuntimeError(lib.qm_last_error().decode())
+            g = capture(torch, run_g)
+            t, _ = time_graph(torch, g, reps, warmup)
+            tf = flops * reps / t / 1e12
+            key = f"llama3.2-1b_prefill{tag}_m{m}_grouped_dispatch"
+            out[key] = {"launches_per_stack": len(calls), "tokens_per_s": round(m * reps / t, 1),
+                        "stack_TFLOPs": round(tf, 2), "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4)}
+            log(f"prefill{tag} m={m} grouped: {out[key]}")
+            del g, calls, ys, xs
+        del wds
+        torch.cuda.empty_cache()
 
     return out
 

@@ -156,8 +156,8 @@ qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_
 /* Grouped prefill GEMM (Sec. 3.3: each fusion removes a launch; e.g. the
  * q/k/v projections of a layer, or its gate and up projections, which all
  * read the same X):  Y_i[m][n_i] = sum_k X[m][k] * w_i'[n_i][k]  for
- * i < count, in one launch.  w: host array of `count` descriptors, all Q4,
- * DEVICE layout, batch 1, one k; n_i may differ.  X: fp16 [m][k] row-major
+ * i < count, in one launch.  w: host array of `count` descriptors, all of
+ * one format (Q4 or Q8), DEVICE layout, batch 1, one k; n_i may differ.  X: fp16 [m][k] row-major
  * (device, 16-byte aligned), shared by all entries.  y: host array of
  * `count` device pointers to fp32 [m][n_i], 4-byte aligned, not
  * overlapping.  1 <= count <= 4 (QM_GEMM_GROUP_MAX); 1 <= m <= 65536 (m == 1
@@ -169,7 +169,9 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
                                float* const* y, void* stream);
 
 /* Prefill GEMM (Sec. 3.3, Sec. 3.4, M > 1): Y[m][n] = sum_k X[m][k] * w'[n][k].
- * w: DEVICE layout, batch 1, Q4.  X: fp16 [m][k] row-major; Y: fp32 [m][n].
+ * w: DEVICE layout, batch 1, Q4 or Q8 (Sec. 4.1: both formats; the MFMA
+ * path is the same, only the in-register unpacking differs).
+ * X: fp16 [m][k] row-major; Y: fp32 [m][n].
  * X tiles and (for most tile shapes) the raw weight chunks are copied into
  * LDS by DMA; weights are dequantised to fp16 (value fp16_RNE(s*q)) in
  * registers and fed to fp16 MFMA with fp32 accumulation.

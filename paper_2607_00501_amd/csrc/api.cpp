@@ -251,8 +251,6 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
       return fail(QM_ELAYOUT, "qmatmul_gemm_grouped: w[%d] must be in DEVICE layout", i);
     if (w[i].batch != 1) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: w[%d] batch must be 1", i);
     if (w[i].format != w[0].format) return fail(QM_EFORMAT, "qmatmul_gemm_grouped: formats differ");
-    if (m > 1 && w[i].format != QM_Q4_G32)
-      return fail(QM_EFORMAT, "qmatmul_gemm_grouped: the MFMA GEMM supports Q4 only (m > 1)");
     if (w[i].k != w[0].k) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: k differs between entries");
     if (w[i].n > 0 && !y[i]) return fail(QM_EINVAL, "qmatmul_gemm_grouped: null y[%d]", i);
     if (!aligned4(y[i])) return fail(QM_EALIGN, "qmatmul_gemm_grouped: y[%d] must be 4-byte aligned", i);
@@ -281,7 +279,8 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
   for (int i = 0; i < count; ++i) {
     qs[i] = static_cast<const uint8_t*>(w[i].qdata); ss[i] = w[i].scales; ys[i] = y[i]; ns[i] = w[i].n;
   }
-  return launched(launch_gemm_group(count, qs, ss, ys, ns, x, m, w[0].k, d->cu_count, s), "qmatmul_gemm_grouped");
+  return launched(launch_gemm_group(w[0].format, count, qs, ss, ys, ns, x, m, w[0].k, d->cu_count, s),
+                  "qmatmul_gemm_grouped");
 }
 
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream) {
@@ -290,8 +289,6 @@ qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float*
   if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "qmatmul_gemm: weights must be in DEVICE layout");
   if (w->batch != 1) return fail(QM_ESHAPE, "qmatmul_gemm: batch must be 1");
   if (m < 1 || m > 65536) return fail(QM_ESHAPE, "qmatmul_gemm: m=%lld must be in [1, 65536]", (long long)m);
-  if (m > 1 && w->format != QM_Q4_G32)
-    return fail(QM_EFORMAT, "qmatmul_gemm: the MFMA GEMM supports Q4 only (m > 1)");
   if (w->n > 0 && (!x || !y)) return fail(QM_EINVAL, "qmatmul_gemm: null x or y");
   if (!aligned16(x)) return fail(QM_EALIGN, "qmatmul_gemm: x must be 16-byte aligned");
   if (!aligned4(y)) return fail(QM_EALIGN, "qmatmul_gemm: y must be 4-byte aligned");
@@ -302,7 +299,7 @@ qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float*
     return launched(launch_gemv(w->format, static_cast<const uint8_t*>(w->qdata), w->scales, x, y, w->n,
                                 w->k, d->cu_count, s),
                     "qmatmul_gemm(m=1)");
-  return launched(launch_gemm(static_cast<const uint8_t*>(w->qdata), w->scales, x, y, m, w->n, w->k,
+  return launched(launch_gemm(w->format, static_cast<const uint8_t*>(w->qdata), w->scales, x, y, m, w->n, w->k,
                               d->cu_count, s),
                   "qmatmul_gemm");
 }

@@ -1,8 +1,8 @@
-// Prefill GEMM  Y[m][n] = sum_k X[m][k] * w'[n][k]  with Q4 weights
+// Prefill GEMM  Y[m][n] = sum_k X[m][k] * w'[n][k]  with Q4 or Q8 weights
 // dequantised inside the kernel and fp16 MFMA (BaseRT Sec. 3.4: tiled GEMM
 // for the prompt, tile geometry chosen by sequence-length regime; Sec. 3.3:
 // dequantisation lives inside the GEMM, weights are never materialised).
-// The kernel itself is the shared Q4 MFMA core in qgemm.h (dense mode);
+// The kernel itself is the shared MFMA core in qgemm.h (dense mode);
 // this file holds the per-chip tile plan and the launch.
 #include <cstdio>
 #include <cstdlib>
@@ -12,11 +12,12 @@
 namespace qm {
 namespace {
 
-template <int BM, int WN, int WK>
+template <int BM, int WN, int WK, int FMT>
 hipError_t launch_tile(const QgemmArgs& a, hipStream_t st) {
   const int64_t panels = a.gpanel[a.gcount];
   const dim3 grid(static_cast<unsigned>((panels + WN - 1) / WN), static_cast<unsigned>((a.M + BM - 1) / BM));
-  hipLaunchKernelGGL((qgemm_kernel<BM, WN, WK, QgMode::kDense>), grid, dim3(WN * WK * 64), 0, st, a);
+  hipLaunchKernelGGL((qgemm_kernel<BM, WN, WK, QgMode::kDense, 2, false, FMT>), grid, dim3(WN * WK * 64), 0, st,
+                     a);
   return hipGetLastError();
 }
 
@@ -32,6 +33,9 @@ hipError_t launch_tile(const QgemmArgs& a, hipStream_t st) {
 //  * else one 64-column panel per K slice with split-K over as many
 //    one-wavefront slices as keep >= 8 K steps each (at most 8), in 64-row
 //    tiles if that gives 4 wavefronts per CU, else 32-row tiles.
+// Q8 weights use the same plan: their 128 x 256 tile keeps the weights in
+// registers (twice the bytes do not fit in LDS beside 128-row A stages) and
+// still beats 64 x 256 tiles by 10-20% where the rule picks it.
 GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count) {
   // Tuning sweeps only: QM_GEMM_PLAN="bm,wn,wk" forces the plan (one of the
   // instantiated tiles, see launch_args).
@@ -63,18 +67,26 @@ const char* gemm_tile_name(int64_t m, int64_t n) {
 namespace {
 
 // The tiles gemm_plan() can choose (QM_GEMM_PLAN may force any of them).
+// Both formats instantiate the same tiles.
 #define QM_GEMM_TILES(X) \
   X(128, 4, 1) X(64, 4, 1) X(64, 2, 2) \
   X(64, 1, 1) X(64, 1, 2) X(64, 1, 4) X(64, 1, 8) X(32, 1, 1) X(32, 1, 2) X(32, 1, 4) X(32, 1, 8)
 
-hipError_t launch_args(const QgemmArgs& a, int cu_count, hipStream_t st) {
+hipError_t launch_args(const QgemmArgs& a, int32_t fmt, int cu_count, hipStream_t st) {
   const int64_t panels = a.gpanel[a.gcount];
   if (panels == 0) return hipSuccess;
   const GemmPlan p = gemm_plan(a.M, panels * kPanel, a.K, cu_count);
-#define QM_LAUNCH(BM, WN, WK) \
-  if (p.bm == BM && p.wn == WN && p.wk == WK) return launch_tile<BM, WN, WK>(a, st);
-  QM_GEMM_TILES(QM_LAUNCH)
-#undef QM_LAUNCH
+#define QM_LAUNCH4(BM, WN, WK) \
+  if (p.bm == BM && p.wn == WN && p.wk == WK) return launch_tile<BM, WN, WK, QM_Q4_G32>(a, st);
+#define QM_LAUNCH8(BM, WN, WK) \
+  if (p.bm == BM && p.wn == WN && p.wk == WK) return launch_tile<BM, WN, WK, QM_Q8_G32>(a, st);
+  if (fmt == QM_Q8_G32) {
+    QM_GEMM_TILES(QM_LAUNCH8)
+  } else {
+    QM_GEMM_TILES(QM_LAUNCH4)
+  }
+#undef QM_LAUNCH4
+#undef QM_LAUNCH8
   return hipErrorInvalidConfiguration;
 }
 
@@ -88,21 +100,18 @@ bool gemm_plan_instantiated(const GemmPlan& p) {
   return false;
 }
 
-namespace {
-}  // namespace
-
-hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
+hipError_t launch_gemm(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
                        int64_t n, int64_t k, int cu_count, hipStream_t st) {
   const uint8_t* qs[1] = {q};
   const uint16_t* ss[1] = {s};
   float* ys[1] = {y};
   const int64_t ns[1] = {n};
-  return launch_gemm_group(1, qs, ss, ys, ns, x, m, k, cu_count, st);
+  return launch_gemm_group(fmt, 1, qs, ss, ys, ns, x, m, k, cu_count, st);
 }
 
-hipError_t launch_gemm_group(int count, const uint8_t* const* q, const uint16_t* const* s, float* const* y,
-                             const int64_t* n, const uint16_t* x, int64_t m, int64_t k, int cu_count,
-                             hipStream_t st) {
+hipError_t launch_gemm_group(int32_t fmt, int count, const uint8_t* const* q, const uint16_t* const* s,
+                             float* const* y, const int64_t* n, const uint16_t* x, int64_t m, int64_t k,
+                             int cu_count, hipStream_t st) {
   QgemmArgs a{};
   a.a = x; a.M = m; a.K = k;
   a.q = q[0]; a.s = s[0]; a.y = y[0]; a.N = n[0];
@@ -112,7 +121,7 @@ hipError_t launch_gemm_group(int count, const uint8_t* const* q, const uint16_t*
     a.gq[i] = q[i]; a.gs[i] = s[i]; a.gy[i] = y[i]; a.gn[i] = n[i];
     a.gpanel[i + 1] = a.gpanel[i] + static_cast<int32_t>(padded_rows(n[i]) / kPanel);
   }
-  return launch_args(a, cu_count, st);
+  return launch_args(a, fmt, cu_count, st);
 }
 
 }  // namespace qm

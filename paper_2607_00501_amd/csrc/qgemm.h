@@ -1,14 +1,15 @@
-// Q4 MFMA GEMM core shared by the prefill GEMM and the MoE grouped GEMMs.
+// Q4/Q8 MFMA GEMM core shared by the prefill GEMM and the MoE grouped GEMMs.
 //
-// Y = A * W'^T with W' the group-32 Q4 weights dequantised inside the
-// kernel (BaseRT Sec. 3.3: dequantisation in the matmul inner loop; Sec.
+// Y = A * W'^T with W' the group-32 Q4 (or, for the dense GEMM, Q8) weights
+// dequantised inside the kernel (BaseRT Sec. 3.3: dequantisation in the matmul inner loop; Sec.
 // 3.4: tiled GEMM for prefill).  Mapping on gfx950 (64-lane wavefronts,
 // v_mfma_f32_32x32x16_f16):
 //  * a workgroup has WN x WK wavefronts; wavefront (wn, wk) owns the BM x 64
 //    output block whose 64 columns are one device-layout panel, over the
 //    wk-th slice of the K steps (WK > 1: split-K inside the workgroup, in
 //    every mode; the partial sums meet in LDS in a fixed order).  One 64-deep
-//    K step of its weights is two 1 KiB contiguous chunk rows;
+//    K step of its weights is two 1 KiB contiguous chunk rows (Q8: two
+//    2 KiB chunks, each two 1 KiB halves of 16 k);
 //  * loads go global -> LDS by DMA (global_load_lds_dwordx4: lane l of an
 //    instruction lands at M0 + 16 l, 1 KiB per instruction), with no staging
 //    registers: the activation tile of each K slice (BM x 64 fp16, shared by
@@ -23,10 +24,12 @@
 //    (A and B agree, so the sum is unchanged): in substep s of group c, lane
 //    half h takes k = 32c + 16h + 8s + 0..7.  Lane l then needs two
 //    consecutive dwords of row l%32 (column half 0) and of row 32 + l%32
-//    (column half 1): no cross-lane permute.  v_and_or_b32 + one packed fp16
-//    add (or an exact fma for the nibbles at bits 4-7) + v_pk_mul_f16 give
-//    fp16_RNE(s*q) exactly.  A fragments and dequantised B of the next
-//    substep are produced while the current MFMAs run;
+//    (column half 1) (Q8: 16 bytes, the row's half h): no cross-lane
+//    permute.  Q4: v_and_or_b32 + one packed fp16 add (or an exact fma for
+//    the nibbles at bits 4-7) + v_pk_mul_f16; Q8: v_perm_b32 + one packed
+//    add + v_pk_mul_f16; both give fp16_RNE(s*q) exactly.  A fragments and
+//    dequantised B of the next substep are produced while the current MFMAs
+//    run;
 //  * loads run DEPTH (2-3) K steps ahead into DEPTH + 1 LDS stages / register
 //    slots (2 stages, one step ahead, where LDS is short), so a load always
 //    targets a slot whose step is already consumed (no loop-carried register
@@ -156,6 +159,30 @@ __device__ inline half8v dequant_dword(uint32_t d, half2v s2, const DequantRegs&
   return half8v{v0[0], v0[1], v1[0], v1[1], v2[0], v2[1], v3[0], v3[1]};
 }
 
+// Q8 constants: v_perm_b32 selectors in VGPRs and the byte 0x64 repeated in
+// an SGPR (a VOP3 takes no literal and at most one scalar operand).
+struct DequantRegsQ8 {
+  uint32_t sel_lo, sel_hi, magic_s;
+  __device__ DequantRegsQ8() : sel_lo(0x04010400u), sel_hi(0x04030402u), magic_s(0x64646464u) {
+    asm volatile("" : "+v"(sel_lo), "+v"(sel_hi));
+    asm volatile("" : "+s"(magic_s));
+  }
+};
+
+// 8 offset-binary bytes u = q + 128 of the Q8 device layout (two dwords,
+// natural k order) -> 8 fp16 fp16_RNE(s*q).  v_perm_b32 puts bytes 0, 1
+// (or 2, 3) of a dword under the fp16 high byte 0x64, giving 1024 + u
+// exactly; one packed subtract of 1152 leaves q, and v_pk_mul_f16 scales.
+__device__ inline half8v dequant_q8(uint32_t d0, uint32_t d1, half2v s2, const DequantRegsQ8& c) {
+  const half2v b = {(_Float16)1152.0f, (_Float16)1152.0f};
+  const half2v q01 = __builtin_bit_cast(half2v, __builtin_amdgcn_perm(c.magic_s, d0, c.sel_lo)) - b;
+  const half2v q23 = __builtin_bit_cast(half2v, __builtin_amdgcn_perm(c.magic_s, d0, c.sel_hi)) - b;
+  const half2v q45 = __builtin_bit_cast(half2v, __builtin_amdgcn_perm(c.magic_s, d1, c.sel_lo)) - b;
+  const half2v q67 = __builtin_bit_cast(half2v, __builtin_amdgcn_perm(c.magic_s, d1, c.sel_hi)) - b;
+  const half2v v0 = q01 * s2, v1 = q23 * s2, v2 = q45 * s2, v3 = q67 * s2;
+  return half8v{v0[0], v0[1], v1[0], v1[1], v2[0], v2[1], v3[0], v3[1]};
+}
+
 // Wavefront 0 maps the workgroup's linear tile index to (expert, row tile)
 // in expert order, with ceil(count / BM) tiles per expert.  Expert -1 when
 // the index lies beyond the last tile.
@@ -185,8 +212,12 @@ __device__ inline void find_tile(const int32_t* counts, int E, int BM, int bx, i
   __syncthreads();
 }
 
-template <int BM, int WN, int WK, QgMode MODE, int DEPTH>
+template <int BM, int WN, int WK, QgMode MODE, int DEPTH, int FMT>
 struct Cfg {
+  static constexpr bool kQ8 = FMT == QM_Q8_G32;
+  static_assert(FMT == QM_Q4_G32 || (kQ8 && MODE == QgMode::kDense), "Q8 weights: dense GEMM only");
+  static constexpr int kChunkBytes = kQ8 ? 2048 : 1024;           // one group of a 64-row panel
+  static constexpr int kDwords = kQ8 ? 8 : 4;                     // B dwords per lane, column half and K step
   static constexpr bool kDual = MODE == QgMode::kMoeGateUp;
   static constexpr int kNB = kDual ? 2 : 1;                      // weight matrices per wavefront
   static constexpr int kThreads = WN * WK * 64;
@@ -198,11 +229,12 @@ struct Cfg {
   static constexpr int kSlots = DEPTH + 1;                       // slots of B (registers or LDS)
   // LDS stage: the A tiles of the WK slices (BM rows x 128 B each), then,
   // when B also goes through LDS, per wavefront and weight matrix the two
-  // 1 KiB code chunks and their 2 x 64 scales (2304 B).  B goes through LDS
+  // code chunks and their 2 x 64 scales (Q4 2304 B, Q8 4352 B).  B goes through LDS
   // for multi-wavefront slices whose DEPTH + 1 stages fit in 80 KiB (two
   // workgroups per CU); otherwise B is loaded into registers.
   static constexpr int kAStageBytes = WK * BM * kBK * 2;
-  static constexpr int kBWaveBytes = kNB * 2304;
+  static constexpr int kBMatBytes = 2 * kChunkBytes + 256;
+  static constexpr int kBWaveBytes = kNB * kBMatBytes;
   static constexpr bool kBLds = WN > 1 && kSlots * (kAStageBytes + WN * WK * kBWaveBytes) <= 80 * 1024;
   static constexpr int kStageBytes = kAStageBytes + (kBLds ? WN * WK * kBWaveBytes : 0);
   // A LDS stages: DEPTH + 1 (A loaded DEPTH steps ahead, like B) when they
@@ -211,9 +243,10 @@ struct Cfg {
   static constexpr int kAStages = (kBLds || kSlots * kAStageBytes <= 48 * 1024) ? kSlots : 2;
   static constexpr int kADist = kAStages - 1;
   // Global loads of one K step issued by one wavefront: A row groups, then
-  // per weight matrix either 2 code chunks + 1 scale block (LDS DMA) or
-  // 2 chunks x 2 column halves of codes and of scales (registers).
-  static constexpr int kBLoads = kBLds ? kNB * 3 : kNB * 2 * 2 * 2;
+  // per weight matrix either the code chunks in 1 KiB pieces + 1 scale
+  // block (LDS DMA) or 2 chunks x 2 column halves of codes and of scales
+  // (registers).
+  static constexpr int kBLoads = kBLds ? kNB * (2 * kChunkBytes / 1024 + 1) : kNB * 2 * 2 * 2;
   // Split-K partial sums of slices 1..WK-1, in halves (fp32 = 2 halves).
   static constexpr int kRedHalves = (WK - 1) * WN * kTM * 2 * kNB * 16 * 64 * 2;
   static constexpr int kLdsHalves =
@@ -221,16 +254,17 @@ struct Cfg {
   static_assert(kAStages == kSlots || (kAStages == 2 && DEPTH == 2), "A stage schedule");
 };
 
-template <int BM, int WN, int WK, QgMode MODE, int DEPTH, bool NT>
+template <int BM, int WN, int WK, QgMode MODE, int DEPTH, bool NT, int FMT>
 __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
-  using C = Cfg<BM, WN, WK, MODE, DEPTH>;
+  using C = Cfg<BM, WN, WK, MODE, DEPTH, FMT>;
+  constexpr bool Q8 = C::kQ8;
+  constexpr int CB = C::kChunkBytes, MB = C::kBMatBytes;
   constexpr int NB = C::kNB;
   __shared__ __attribute__((aligned(16))) uint16_t lds[C::kLdsHalves];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wavefront-uniform (SGPR)
   const int wk = wave / WN, wn = wave % WN;
-  const int stid = tid - wk * C::kSliceThreads;          // thread index inside the K slice
   const int64_t K = p.K, N = p.N;
   const int G = static_cast<int>(K / kGroup);
   const int KT = (G + 1) / 2;
@@ -316,19 +350,20 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     a_src[i] = p.a + src_row * K;
   }
   // B: lane l reads dwords 2(l/32), 2(l/32)+1 of panel rows l%32 and
-  // 32 + l%32 (clamped to a real panel).  The matrix, expert and panel bases
-  // are wavefront-uniform; the lane part is a 32-bit offset.
+  // 32 + l%32 (Q8: the 16 bytes of half l/32 of those rows), clamped to a
+  // real panel.  The matrix, expert and panel bases are wavefront-uniform;
+  // the lane part is a 32-bit offset.
   const int64_t panel = (cols_ok ? n_wave : mnpad - kPanel) / kPanel;
-  const int64_t mat_q = npad * (K / 2), mat_s = npad * G;   // bytes / scales of one matrix
+  const int64_t mat_q = npad * (K / 2), mat_s = npad * G;   // bytes / scales of one matrix (MoE, Q4)
   const uint8_t* b_q[NB];
   const uint16_t* b_s[NB];
-  b_q[0] = mq + expert * mat_q + panel * G * kPanel * 16;
+  b_q[0] = mq + expert * mat_q + panel * G * CB;
   b_s[0] = ms + expert * mat_s + panel * G * kPanel;
   if constexpr (NB == 2) {
-    b_q[1] = p.q2 + expert * mat_q + panel * G * kPanel * 16;
+    b_q[1] = p.q2 + expert * mat_q + panel * G * CB;
     b_s[1] = p.s2 + expert * mat_s + panel * G * kPanel;
   }
-  const uint32_t bq_lane = (lane & 31) * 16 + (lane >> 5) * 8;
+  const uint32_t bq_lane = Q8 ? (lane & 31) * 16 + (lane >> 5) * 1024 : (lane & 31) * 16 + (lane >> 5) * 8;
   const uint32_t bs_lane = lane & 31;
 
   // DEPTH + 1 slots of raw B operands (registers, or LDS stages when B
@@ -336,7 +371,8 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   // t % (DEPTH + 1), always indexed by constants.  rb / rs are used only
   // when B is loaded into registers.
   constexpr int NS = C::kSlots;
-  u32x2 rb[NS][NB][2][2];                                  // [slot][matrix][chunk][column half]
+  using BVec = std::conditional_t<Q8, u32x4, u32x2>;
+  BVec rb[NS][NB][2][2];                                   // [slot][matrix][chunk][column half]
   uint32_t rs[NS][NB][2][2];
   char* const lds_b = reinterpret_cast<char*>(lds);
   // A tile of this slice in stage st; B region of this wavefront in stage st.
@@ -357,8 +393,9 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     constexpr int sl = decltype(slot)::value;
     const int kt = kt0 + step;
     if constexpr (C::kBLds) {
-      // Per matrix: the two 1 KiB chunk rows verbatim, then their scales
-      // (lanes 0-31: chunk 0, lanes 32-63: chunk 1; 4 B = 2 scales a lane).
+      // Per matrix: the two code chunks verbatim in 1 KiB pieces, then
+      // their scales (lanes 0-31: chunk 0, lanes 32-63: chunk 1; 4 B = 2
+      // scales a lane).
       char* reg = b_region(sl);
       const int gs1 = min(2 * kt + (lane >> 5), G - 1);
 #pragma unroll
@@ -366,9 +403,12 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           const int gc = min(2 * kt + c, G - 1);
-          lds_dma16<NT>(b_q[j] + static_cast<int64_t>(gc) * kPanel * 16 + lane * 16, reg + j * 2304 + c * 1024);
+#pragma unroll
+          for (int piece = 0; piece < CB / 1024; ++piece)
+            lds_dma16<NT>(b_q[j] + static_cast<int64_t>(gc) * CB + piece * 1024 + lane * 16,
+                          reg + j * MB + c * CB + piece * 1024);
         }
-        lds_dma4<NT>(b_s[j] + static_cast<int64_t>(gs1) * kPanel + 2 * (lane & 31), reg + j * 2304 + 2048);
+        lds_dma4<NT>(b_s[j] + static_cast<int64_t>(gs1) * kPanel + 2 * (lane & 31), reg + j * MB + 2 * CB);
       }
       return;
     }
@@ -377,11 +417,11 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const int gc = min(2 * kt + c, G - 1);
-        const uint8_t* bq = b_q[j] + static_cast<int64_t>(gc) * kPanel * 16;
+        const uint8_t* bq = b_q[j] + static_cast<int64_t>(gc) * CB;
         const uint16_t* bs = b_s[j] + static_cast<int64_t>(gc) * kPanel;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const u32x2* qa = reinterpret_cast<const u32x2*>(bq + bq_lane + h * 512);
+          const BVec* qa = reinterpret_cast<const BVec*>(bq + bq_lane + h * 512);
           const uint16_t* sa = bs + bs_lane + 32 * h;
           if constexpr (NT) {
             rb[sl][j][c][h] = __builtin_nontemporal_load(qa);
@@ -412,7 +452,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     asm volatile("" ::: "memory");
   };
 
-  const DequantRegs dq;
+  const std::conditional_t<Q8, DequantRegsQ8, DequantRegs> dq;
   float16v acc[C::kTM][2 * NB];
 #pragma unroll
   for (int a = 0; a < C::kTM; ++a)
@@ -465,7 +505,10 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     using Refill = std::integral_constant<int, (sl + DEPTH) % NS>;
     wait_a(t);
     slice_sync();
-    uint32_t bd[NB][2][4];                                 // [matrix][column half][substep]
+    // [matrix][column half][dword]: substep ks takes dword ks (Q4) or
+    // dwords 2ks, 2ks+1 (Q8).
+    constexpr int DW = C::kDwords;
+    uint32_t bd[NB][2][DW];
     half2v sc[NB][2][2];                                   // [matrix][chunk][column half]
     const char* breg = b_region(sl);
 #pragma unroll
@@ -475,12 +518,13 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         const bool ok = scale_ok(t, c);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          u32x2 d;
+          BVec d;
           uint32_t sv;
           if constexpr (C::kBLds) {
             const int row = 32 * h + (lane & 31);
-            d = *reinterpret_cast<const u32x2*>(breg + j * 2304 + c * 1024 + row * 16 + 8 * (lane >> 5));
-            sv = *reinterpret_cast<const uint16_t*>(breg + j * 2304 + 2048 + c * 128 + row * 2);
+            const int in_chunk = Q8 ? row * 16 + 1024 * (lane >> 5) : row * 16 + 8 * (lane >> 5);
+            d = *reinterpret_cast<const BVec*>(breg + j * MB + c * CB + in_chunk);
+            sv = *reinterpret_cast<const uint16_t*>(breg + j * MB + 2 * CB + c * 128 + row * 2);
           } else {
             d = rb[sl][j][c][h];
             sv = rs[sl][j][c][h];
@@ -488,10 +532,14 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
           sv = ok ? sv : 0u;
           const _Float16 f = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sv));
           sc[j][c][h] = half2v{f, f};
-          bd[j][h][2 * c] = d[0];
-          bd[j][h][2 * c + 1] = d[1];
+#pragma unroll
+          for (int i = 0; i < DW / 2; ++i) bd[j][h][DW / 2 * c + i] = d[i];
         }
       }
+    auto dequant = [&](int j, int h, int ks) __attribute__((always_inline)) {
+      if constexpr (Q8) return dequant_q8(bd[j][h][2 * ks], bd[j][h][2 * ks + 1], sc[j][ks >> 1][h], dq);
+      else return dequant_dword(bd[j][h][ks], sc[j][ks >> 1][h], dq);
+    };
     load_a(a_stage(Refill{}, t + AD), t + AD);             // A, AD steps ahead
     __builtin_amdgcn_sched_barrier(0);
     load_b(Refill{}, t + DEPTH);                           // B, DEPTH steps ahead
@@ -506,8 +554,8 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     for (int a = 0; a < C::kTM; ++a) af[0][a] = *reinterpret_cast<const half8v*>(At + a_off[0] + a * 32 * 2 * kBK);
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      bq[0][j][0] = dequant_dword(bd[j][0][0], sc[j][0][0], dq);
-      bq[0][j][1] = dequant_dword(bd[j][1][0], sc[j][0][1], dq);
+      bq[0][j][0] = dequant(j, 0, 0);
+      bq[0][j][1] = dequant(j, 1, 0);
     }
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
@@ -518,8 +566,8 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
           af[nxt][a] = *reinterpret_cast<const half8v*>(At + a_off[ks + 1] + a * 32 * 2 * kBK);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
-          bq[nxt][j][0] = dequant_dword(bd[j][0][ks + 1], sc[j][(ks + 1) >> 1][0], dq);
-          bq[nxt][j][1] = dequant_dword(bd[j][1][ks + 1], sc[j][(ks + 1) >> 1][1], dq);
+          bq[nxt][j][0] = dequant(j, 0, ks + 1);
+          bq[nxt][j][1] = dequant(j, 1, ks + 1);
         }
       }
 #pragma unroll
@@ -619,10 +667,10 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 // Two workgroups per CU (up to 256 VGPRs per lane) for up to 4 wavefronts
 // per workgroup, one beyond.  NT: weights and scales are read with
 // nontemporal loads (for weights each workgroup streams once and no other
-// workgroup re-reads soon).
-template <int BM, int WN, int WK, QgMode MODE, int DEPTH = 2, bool NT = false>
+// workgroup re-reads soon).  FMT: QM_Q4_G32, or QM_Q8_G32 (dense mode).
+template <int BM, int WN, int WK, QgMode MODE, int DEPTH = 2, bool NT = false, int FMT = QM_Q4_G32>
 __global__ __launch_bounds__(WN * WK * 64, WN * WK <= 4 ? 2 : 1) void qgemm_kernel(QgemmArgs p) {
-  qg::qgemm_body<BM, WN, WK, MODE, DEPTH, NT>(p);
+  qg::qgemm_body<BM, WN, WK, MODE, DEPTH, NT, FMT>(p);
 }
 
 }  // namespace qm

@@ -94,11 +94,11 @@ hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg
 hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count, hipStream_t st);
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
                        int64_t n, int64_t k, int cu_count, hipStream_t st);
-hipError_t launch_gemm(const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
+hipError_t launch_gemm(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y, int64_t m,
                        int64_t n, int64_t k, int cu_count, hipStream_t st);
-hipError_t launch_gemm_group(int count, const uint8_t* const* q, const uint16_t* const* s, float* const* y,
-                             const int64_t* n, const uint16_t* x, int64_t m, int64_t k, int cu_count,
-                             hipStream_t st);
+hipError_t launch_gemm_group(int32_t fmt, int count, const uint8_t* const* q, const uint16_t* const* s,
+                             float* const* y, const int64_t* n, const uint16_t* x, int64_t m, int64_t k,
+                             int cu_count, hipStream_t st);
 
 struct MoeArgs {
   const uint8_t* gq; const uint16_t* gs;   // gate [E][inter][hidden], device layout

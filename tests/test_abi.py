@@ -88,8 +88,9 @@ def test_gemm_and_moe_validation():
     x, y = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x40000)
     assert L.qmatmul_gemm(ctypes.byref(w), x, 0, y, None) == 2          # m = 0
     assert L.qmatmul_gemm(ctypes.byref(w), x, 70000, y, None) == 2      # m too large
-    w8 = _fake_weight(fmt=2)
-    assert L.qmatmul_gemm(ctypes.byref(w8), x, 16, y, None) == 4        # Q8 GEMM not offered
+    w8 = _fake_weight(fmt=3)
+    assert L.qmatmul_gemm(ctypes.byref(w8), x, 16, y, None) == 4        # unknown format
+    assert L.qmatmul_gemm(ctypes.byref(_fake_weight(layout=0)), x, 16, y, None) == 5
     p = ctypes.c_void_p(0x50000)
     assert L.qmoe_route(p, 16, 2000, 8, p, p, p, p, p, None) == 2       # too many experts
     assert L.qmoe_route(p, 16, 128, 17, p, p, p, p, p, None) == 2       # top_k > 16
@@ -203,7 +204,7 @@ def test_gemm_grouped_validation():
     assert L.qmatmul_gemm_grouped(1, None, x, 16, None, None) == 1     # null arrays
     assert call([w], m=0) == 2                                         # m < 1
     assert call([w, _fake_weight(fmt=2)]) == 4                         # formats differ
-    assert call([_fake_weight(fmt=2)] * 2) == 4                        # Q8 with m > 1
+    assert call([_fake_weight(fmt=3)] * 2) == 4                        # unknown format
     assert call([w, _fake_weight(k=96)]) == 2                          # k differs
     assert call([w, _fake_weight(layout=0)]) == 5                      # not DEVICE layout
     assert call([w, w], ys=[0x40000, 0x40002]) == 3                    # y[1] misaligned
