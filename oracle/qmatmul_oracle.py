@@ -21,7 +21,11 @@ paper states no formula for the format, the routing or the expert FFN; the
 group-32 symmetric format, the top-8-then-softmax router and the SwiGLU
 experts follow the benchmark workload definitions, and each point the paper
 leaves open is resolved as listed in the module docstrings below (the same
-readings are collected in the design notes).
+readings are collected in the design notes).  The paper names eight weight
+formats (Sec. 4.1: Q2, Q3, Q4, Q5, Q6, Q8, BF16, FP16) without defining their
+encodings; Q2/Q3/Q5/Q6 here follow the same group-32 symmetric rule as Q4
+with qmax = 2^(b-1) - 1, and BF16/FP16 are plain round-to-nearest-even
+conversions of the weights.
 
 Pins: every function here is checked by ``tests/test_oracle_pins.py`` against
 values fixed by something other than this file (hand-derived IEEE bit
@@ -35,10 +39,13 @@ from __future__ import annotations
 import numpy as np
 
 GROUP = 32
-Q4, Q8 = 1, 2                      # format ids (same numbering as the C ABI)
-QMAX = {Q4: 7, Q8: 127}
-QLO = {Q4: -8, Q8: -127}
-QHI = {Q4: 7, Q8: 127}
+Q4, Q8, Q2, Q3, Q5, Q6, F16, BF16 = 1, 2, 3, 4, 5, 6, 7, 8    # format ids (same numbering as the C ABI)
+BITS = {Q2: 2, Q3: 3, Q4: 4, Q5: 5, Q6: 6, Q8: 8}             # integer formats
+FLOATS = (F16, BF16)
+QMAX = {f: (1 << (b - 1)) - 1 for f, b in BITS.items()}        # Q2 1, Q3 3, Q4 7, Q5 15, Q6 31, Q8 127
+QLO = {f: -(1 << (b - 1)) for f, b in BITS.items()}
+QLO[Q8] = -127                                                 # Q8 is symmetric
+QHI = dict(QMAX)
 
 
 # ---------------------------------------------------------------------------
@@ -55,6 +62,22 @@ def fp16_value(bits: np.ndarray) -> np.ndarray:
     return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float32)
 
 
+def bf16_bits(x32: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit pattern, round-to-nearest-even (finite inputs): the
+    upper 16 bits of the fp32 pattern, rounded on the lower 16."""
+    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    keep = u >> 16
+    rest = u & 0xFFFF
+    up = (rest > 0x8000) | ((rest == 0x8000) & (keep & 1 == 1))
+    return (keep + up).astype(np.uint16)
+
+
+def bf16_value(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit pattern -> its exact value as fp32 (the pattern in the upper
+    half of an fp32)."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
 def quantise(w: np.ndarray, fmt: int):
     """Symmetric group-32 quantisation of one weight matrix along K.
 
@@ -63,17 +86,25 @@ def quantise(w: np.ndarray, fmt: int):
       s32 = m / qmax                         (fp32, correctly rounded)
       s16 = fp16_RNE(s32),  s = value(s16)
       q   = 0 everywhere if s == 0, else clamp(rint_half_even(w / s), lo, hi)
-    with qmax = 7, [lo, hi] = [-8, 7] for Q4 and qmax = 127,
-    [lo, hi] = [-127, 127] for Q8.  The divisor is the fp16-rounded scale, so
+    with qmax = 2^(b-1) - 1 and [lo, hi] = [-2^(b-1), 2^(b-1) - 1] for the
+    b-bit formats (Q4: 7 and [-8, 7]), except Q8: qmax = 127,
+    [lo, hi] = [-127, 127].  The divisor is the fp16-rounded scale, so
     dequantisation lands within s/2 of w and re-quantising is idempotent.
 
-    Returns (q int8 [N][K], s16 uint16 [N][K/32]).
+    Returns (q int8 [N][K], s16 uint16 [N][K/32]).  F16 / BF16: returns
+    (bits uint16 [N][K], None), each weight rounded to nearest even.
     """
     w = np.asarray(w, dtype=np.float32)
     if w.ndim != 2 or w.shape[1] % GROUP:
         raise ValueError("w must be [N][K] with K a multiple of 32")
     if not np.all(np.isfinite(w)):
         raise ValueError("non-finite weights are outside the format's contract")
+    if fmt == F16:
+        if np.any(np.abs(w) >= np.float32(65520.0)):
+            raise ValueError("weight overflows fp16")
+        return fp16_bits(w), None
+    if fmt == BF16:
+        return bf16_bits(w), None
     n, k = w.shape
     g = w.reshape(n, k // GROUP, GROUP)
     m = np.max(np.abs(g), axis=2)                                  # fp32, exact
@@ -95,33 +126,34 @@ def quantise(w: np.ndarray, fmt: int):
 def pack(q: np.ndarray, fmt: int) -> np.ndarray:
     """Canonical byte packing of the codes of one [N][K] matrix.
 
-    Q4: uint8 [N][K/2], byte j = (q[2j] & 0xF) | ((q[2j+1] & 0xF) << 4),
-        i.e. the even k in the low nibble, each nibble two's complement.
-    Q8: uint8 [N][K] holding the int8 code in two's complement.
+    b-bit formats: per row a little-endian bit stream of K*b/8 bytes, code k
+    (b-bit two's complement) at bits b*k .. b*k + b - 1, bit i of the stream
+    being bit i%8 of byte i/8.  For Q4 that is byte j =
+    (q[2j] & 0xF) | ((q[2j+1] & 0xF) << 4); for Q8 the int8 code itself.
+    F16 / BF16: the uint16 bit patterns [N][K] unchanged.
     """
+    if fmt in FLOATS:
+        return np.asarray(q, dtype=np.uint16).copy()
+    b = BITS[fmt]
     q = np.asarray(q, dtype=np.int8)
-    if fmt == Q8:
-        return q.view(np.uint8).copy()
-    nib = q.astype(np.int16) & 0xF
-    lo = nib[:, 0::2]
-    hi = nib[:, 1::2]
-    return (lo | (hi << 4)).astype(np.uint8)
+    n, k = q.shape
+    u = q.astype(np.int16) & ((1 << b) - 1)                        # two's complement field
+    bits = ((u[:, :, None] >> np.arange(b)) & 1).astype(np.uint8)  # [N][K][b], LSB first
+    return np.packbits(bits.reshape(n, k * b), axis=1, bitorder="little")
 
 
 def unpack(qbytes: np.ndarray, fmt: int) -> np.ndarray:
-    """Inverse of ``pack``: canonical bytes -> int8 codes [N][K]."""
-    b = np.asarray(qbytes, dtype=np.uint8)
-    if fmt == Q8:
-        return b.view(np.int8).copy()
-    lo = (b & 0xF).astype(np.int16)
-    hi = (b >> 4).astype(np.int16)
-    lo = np.where(lo >= 8, lo - 16, lo)
-    hi = np.where(hi >= 8, hi - 16, hi)
-    n, half = b.shape
-    q = np.empty((n, 2 * half), dtype=np.int8)
-    q[:, 0::2] = lo
-    q[:, 1::2] = hi
-    return q
+    """Inverse of ``pack``: canonical bytes -> int8 codes [N][K] (F16/BF16:
+    the uint16 patterns)."""
+    if fmt in FLOATS:
+        return np.asarray(qbytes, dtype=np.uint16).copy()
+    b = BITS[fmt]
+    qb = np.asarray(qbytes, dtype=np.uint8)
+    n, nbytes = qb.shape
+    k = nbytes * 8 // b
+    bits = np.unpackbits(qb, axis=1, bitorder="little").reshape(n, k, b).astype(np.int16)
+    u = (bits << np.arange(b)).sum(axis=2)
+    return np.where(u >= (1 << (b - 1)), u - (1 << b), u).astype(np.int8)
 
 
 def dequantise(qbytes: np.ndarray, s16: np.ndarray, fmt: int) -> np.ndarray:
@@ -129,7 +161,12 @@ def dequantise(qbytes: np.ndarray, s16: np.ndarray, fmt: int) -> np.ndarray:
 
     The product of an 11-bit fp16 significand and an integer of at most
     8 bits fits in fp32's 24-bit significand, so this fp32 value is exact.
+    F16 / BF16: the value of the stored pattern (exact in fp32).
     """
+    if fmt == F16:
+        return fp16_value(qbytes)
+    if fmt == BF16:
+        return bf16_value(qbytes)
     q = unpack(qbytes, fmt).astype(np.float32)
     s = fp16_value(s16)
     n, k = q.shape
@@ -139,7 +176,8 @@ def dequantise(qbytes: np.ndarray, s16: np.ndarray, fmt: int) -> np.ndarray:
 def dequantise_f16_tile_value(qbytes: np.ndarray, s16: np.ndarray, fmt: int) -> np.ndarray:
     """The fp16 operand value fp16_RNE(s * q) a half-precision matrix unit
     consumes for one weight (bit pattern, uint16 [N][K]).  This rounding is
-    one step more than ``dequantise`` (7 * fp16(0.04/7) is not an fp16)."""
+    one step more than ``dequantise`` (7 * fp16(0.04/7) is not an fp16).
+    F16: the stored pattern itself; BF16: its value rounded to fp16."""
     return fp16_bits(dequantise(qbytes, s16, fmt))
 
 

@@ -38,3 +38,55 @@ def test_q8_device_halves_by_hand():
     assert b[off(0, 0, 0, 0)] == 128
     assert b[off(5, 0, 0, 0)] == 0          # padding row
     assert s[(0 * G + 1) * 64 + 1] == 1
+
+
+def _dword(b, off):
+    return int.from_bytes(b[off:off + 4].tobytes(), "little")
+
+
+def test_q5_planes_by_hand():
+    q = np.zeros((1, 32), np.int8)          # zero codes: u = 16 (nibble 0, bit 1)
+    q[0, 0], q[0, 1], q[0, 2], q[0, 17] = 15, -16, 1, -1
+    b, s = device_layout(q, np.array([[0x3C00]], np.uint16), O.Q5)
+    assert b.size == 1280
+    assert _dword(b, 0) == 0x1F             # k0 nibble 15 (slot 0), k2 nibble 1 (slot 1)
+    assert _dword(b, 8) == 0x000F0000       # k17 nibble 15: dword 2, slot 4
+    assert _dword(b, 1024) == 0xFEFEFFFF    # bit plane: k1 (bit 16) and k17 (bit 24) clear
+    assert not b[16:1024].any() and not b[1028:].any()     # padding rows
+
+
+def test_q3_planes_by_hand():
+    q = np.zeros((1, 32), np.int8)          # zero codes: u = 4 (crumb 0, bit 1)
+    q[0, 0], q[0, 1], q[0, 16] = 3, -4, -1
+    b, _ = device_layout(q, np.array([[0x3C00]], np.uint16), O.Q3)
+    assert b.size == 768
+    assert _dword(b, 0) == 0x3 and _dword(b, 4) == 0x3   # crumbs of k0 and k16
+    assert _dword(b, 512) == 0xFFFEFEFF     # bits: k16 (bit 8) and k1 (bit 16) clear
+
+
+def test_q6_planes_by_hand():
+    q = np.zeros((1, 32), np.int8)          # zero codes: u = 32 (nibble 0, crumb 2)
+    q[0, 0], q[0, 1] = 31, -32
+    b, _ = device_layout(q, np.array([[0x3C00]], np.uint16), O.Q6)
+    assert b.size == 1536
+    assert _dword(b, 0) == 0xF and not b[4:16].any()
+    assert _dword(b, 1024) == 0xAAA8AAAB and _dword(b, 1028) == 0xAAAAAAAA
+
+
+def test_q2_crumbs_by_hand():
+    q = np.zeros((1, 32), np.int8)          # zero codes: u = 2
+    q[0, 0], q[0, 1], q[0, 31] = 1, -2, -1
+    b, _ = device_layout(q, np.array([[0x3C00]], np.uint16), O.Q2)
+    assert b.size == 512
+    assert _dword(b, 0) == 0xAAA8AAAB and _dword(b, 4) == 0x6AAAAAAA
+
+
+def test_f16_quarters_by_hand():
+    v = np.zeros((2, 64), np.uint16)
+    v[1, 9] = 0x1234                        # row 1, group 0, quarter 1, position 1
+    v[0, 32 + 31] = 0xABCD                  # row 0, group 1, quarter 3, position 7
+    b, s = device_layout(v, None, O.F16)
+    assert s is None and b.size == 2 * 4096
+    assert int.from_bytes(b[1024 + 16 + 2:1024 + 16 + 4].tobytes(), "little") == 0x1234
+    assert int.from_bytes(b[4096 + 3 * 1024 + 14:4096 + 3 * 1024 + 16].tobytes(), "little") == 0xABCD
+    assert int(b.view(np.uint16).astype(np.int64).sum()) == 0x1234 + 0xABCD

@@ -26,6 +26,8 @@ import pytest
 from oracle import qmatmul_oracle as O
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.txt")
+FMT_NAMES = {"Q2": O.Q2, "Q3": O.Q3, "Q4": O.Q4, "Q5": O.Q5, "Q6": O.Q6, "Q8": O.Q8}
+INT_FMTS = [O.Q2, O.Q3, O.Q4, O.Q5, O.Q6, O.Q8]
 
 
 def _half_bits_struct(x: float) -> int:
@@ -71,7 +73,7 @@ def test_fp16_rounding_matches_struct_packer():
 @pytest.mark.parametrize("row", _golden_lines("quant"))
 def test_quantise_worked_examples(row):
     head, w_s, s_hex, q_s, dq_s = row
-    fmt = O.Q4 if head.split()[1] == "Q4" else O.Q8
+    fmt = FMT_NAMES[head.split()[1]]
     wv = [float(t) for t in w_s.split()]
     w = np.zeros((1, 32), np.float32)
     w[0, :len(wv)] = wv
@@ -86,12 +88,17 @@ def test_quantise_worked_examples(row):
         assert dq[0, :len(want)].tolist() == want
 
 
-def test_pack_worked_example():
-    (row,) = _golden_lines("pack")
-    q = np.array([[int(t) for t in row[1].split()]], np.int8)
+@pytest.mark.parametrize("row", _golden_lines("pack"))
+def test_pack_worked_example(row):
+    fmt = FMT_NAMES[row[0].split()[1]]
+    codes = [int(t) for t in row[1].split()]
+    q = np.zeros((1, 32), np.int8)
+    q[0, :len(codes)] = codes
     want = [int(t, 16) for t in row[2].split()]
-    assert O.pack(q, O.Q4)[0].tolist() == want
-    assert O.unpack(O.pack(q, O.Q4), O.Q4).tolist() == q.tolist()
+    b = O.pack(q, fmt)
+    assert b.shape == (1, 4 * O.BITS[fmt])
+    assert b[0, :len(want)].tolist() == want and not b[0, len(want):].any()
+    assert O.unpack(b, fmt).tolist() == q.tolist()
 
 
 def test_route_and_bucket_worked_example():
@@ -111,7 +118,7 @@ def test_route_and_bucket_worked_example():
 
 # ------------------------------------------------------------------ invariants
 
-@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+@pytest.mark.parametrize("fmt", INT_FMTS)
 def test_quantise_invariants_random_groups(fmt):
     rng = np.random.default_rng(7 + fmt)
     w = (rng.standard_normal((625, 1024)).astype(np.float32) * np.float32(0.02))
@@ -135,7 +142,7 @@ def test_quantise_scale_is_fp16_of_fp32_quotient():
     the fp32 quotient is the double quotient rounded once to fp32."""
     rng = np.random.default_rng(3)
     w = rng.standard_normal((64, 64)).astype(np.float32) * np.float32(0.02)
-    for fmt in (O.Q4, O.Q8):
+    for fmt in INT_FMTS:
         _, s16 = O.quantise(w, fmt)
         for n in range(64):
             for g in range(2):
@@ -144,18 +151,33 @@ def test_quantise_scale_is_fp16_of_fp32_quotient():
                 assert int(s16[n, g]) == _half_bits_struct(q32)
 
 
-@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+@pytest.mark.parametrize("fmt", INT_FMTS)
 def test_pack_roundtrip_all_codes(fmt):
     lo, hi = O.QLO[fmt], O.QHI[fmt]
     codes = np.arange(lo, hi + 1)
     rng = np.random.default_rng(11)
     q = rng.choice(codes, size=(37, 256)).astype(np.int8)
     b = O.pack(q, fmt)
-    assert b.shape == ((37, 128) if fmt == O.Q4 else (37, 256))
+    assert b.shape == (37, 256 * O.BITS[fmt] // 8)
     assert np.array_equal(O.unpack(b, fmt), q)
 
 
-@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+@pytest.mark.parametrize("fmt", INT_FMTS)
+def test_pack_bit_by_bit(fmt):
+    """Every code's bits at their stream positions, read back one bit at a
+    time with Python integers (little-endian stream)."""
+    rng = np.random.default_rng(31 + fmt)
+    nb = O.BITS[fmt]
+    q = rng.integers(O.QLO[fmt], O.QHI[fmt] + 1, size=(3, 64)).astype(np.int8)
+    b = O.pack(q, fmt)
+    for r in range(3):
+        stream = int.from_bytes(bytes(b[r].tolist()), "little")
+        for kk in range(64):
+            field = (stream >> (nb * kk)) & ((1 << nb) - 1)
+            assert field == int(q[r, kk]) % (1 << nb)
+
+
+@pytest.mark.parametrize("fmt", INT_FMTS)
 def test_dequantise_exhaustive_against_exact_products(fmt):
     lo, hi = O.QLO[fmt], O.QHI[fmt]
     codes = list(range(lo, hi + 1))
@@ -186,27 +208,83 @@ def test_f16_tile_value_is_one_rounding_of_exact_product():
     assert _half_value_struct(int(bits[0, 0])) != 0.04000091552734375
 
 
+# ---------------------------------------------------------- float formats
+
+def _bf16_nearest_exact(x: float) -> int:
+    """bf16 pattern nearest to x by exact rational comparison of the two
+    bf16 neighbours (truncation and the next pattern), ties to even."""
+    bits = struct.unpack("<I", struct.pack("<f", x))[0]
+    lo = bits >> 16
+    cand = [lo, lo + 1]
+    vals = [Fraction(struct.unpack("<f", struct.pack("<I", c << 16))[0]) for c in cand]
+    d = [abs(v - Fraction(x)) for v in vals]
+    if d[0] != d[1]:
+        return cand[0] if d[0] < d[1] else cand[1]
+    return cand[0] if cand[0] % 2 == 0 else cand[1]
+
+
+def test_bf16_rounding_hand_values_and_exact_neighbours():
+    f = lambda b: struct.unpack("<f", struct.pack("<I", b))[0]
+    hand = {0x3F800000: 0x3F80,          # 1.0
+            0x3F808000: 0x3F80,          # 1 + 2^-8: tie, keep even 0x3F80
+            0x3F818000: 0x3F82,          # 1 + 3*2^-8: tie, odd 0x3F81 rounds up
+            0x3F808001: 0x3F81,          # just above the tie
+            0xC0200000: 0xC020,          # -2.5
+            0x3CA3D70A: 0x3CA4,          # fp32(0.02): lower half 0xD70A > 0x8000
+            0x00000001: 0x0000}          # smallest fp32 subnormal
+    x = np.array([f(b) for b in hand], np.float32)
+    assert O.bf16_bits(x).tolist() == list(hand.values())
+    rng = np.random.default_rng(17)
+    vals = np.concatenate([rng.standard_normal(3000).astype(np.float32) * 0.02,
+                           rng.standard_normal(500).astype(np.float32) * 1e30,
+                           rng.standard_normal(500).astype(np.float32) * 1e-38])
+    got = O.bf16_bits(vals)
+    assert got.tolist() == [_bf16_nearest_exact(float(v)) for v in vals]
+    assert np.array_equal(O.bf16_value(got).view(np.uint32), got.astype(np.uint32) << 16)
+
+
+@pytest.mark.parametrize("fmt", [O.F16, O.BF16])
+def test_float_formats_quantise_is_one_rounding(fmt):
+    rng = np.random.default_rng(23)
+    w = rng.standard_normal((9, 64)).astype(np.float32) * np.float32(0.02)
+    bits, s = O.quantise(w, fmt)
+    assert s is None and bits.dtype == np.uint16
+    want = (O.fp16_bits(w) if fmt == O.F16 else np.vectorize(_bf16_nearest_exact)(w.astype(np.float64)))
+    assert np.array_equal(bits, want)
+    dq = O.dequantise(O.pack(bits, fmt), None, fmt)
+    assert np.array_equal(O.quantise(dq, fmt)[0], bits)              # idempotent
+    rel = 2.0 ** -11 if fmt == O.F16 else 2.0 ** -8
+    assert np.all(np.abs(dq.astype(np.float64) - w) <= rel * np.abs(w) + 2.0 ** -25)
+
+
 # ------------------------------------------------------------------ GEMV/GEMM
 
 def _exact_decode(qbytes, s16, fmt, n, k):
-    """Independent pure-Python decode of the canonical bytes into Fractions."""
+    """Independent pure-Python decode of the canonical bytes into Fractions
+    (F16 through struct's half-precision unpacker, BF16 as the upper half of
+    an fp32 pattern)."""
     rows = []
     for r in range(n):
         row = []
+        if fmt in O.FLOATS:
+            for kk in range(k):
+                bits = int(qbytes[r, kk])
+                v = (_half_value_struct(bits) if fmt == O.F16
+                     else struct.unpack("<f", struct.pack("<I", bits << 16))[0])
+                row.append(Fraction(v))
+            rows.append(row)
+            continue
+        nb = O.BITS[fmt]
+        stream = int.from_bytes(bytes(qbytes[r].tolist()), "little")
         for kk in range(k):
-            if fmt == O.Q4:
-                byte = int(qbytes[r, kk // 2])
-                nib = (byte >> (4 * (kk % 2))) & 0xF
-                code = nib - 16 if nib >= 8 else nib
-            else:
-                byte = int(qbytes[r, kk])
-                code = byte - 256 if byte >= 128 else byte
+            field = (stream >> (nb * kk)) & ((1 << nb) - 1)
+            code = field - (1 << nb) if field >= (1 << (nb - 1)) else field
             row.append(Fraction(_half_value_struct(int(s16[r, kk // 32]))) * code)
         rows.append(row)
     return rows
 
 
-@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+@pytest.mark.parametrize("fmt", INT_FMTS + [O.F16, O.BF16])
 def test_gemv_gemm_against_exact_rationals(fmt):
     rng = np.random.default_rng(21 + fmt)
     n, k, m = 5, 96, 3                            # non-square: catches a transpose
@@ -227,7 +305,7 @@ def test_gemv_gemm_against_exact_rationals(fmt):
             assert abs(yv[j] - e) <= 1e-14 * max(1.0, abs(e))
 
 
-@pytest.mark.parametrize("fmt", [O.Q4, O.Q8])
+@pytest.mark.parametrize("fmt", INT_FMTS)
 def test_gemv_integer_grid_is_exact(fmt):
     """Integer weights with a +-qmax in every group quantise with scale 1, so
     y is the exact integer sum (computed here with Python ints)."""
