@@ -335,6 +335,27 @@ def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
         del g, calls
         torch.cuda.empty_cache()
 
+    # The Llama-3.2-3B lm_head (3072 -> 128256) in every weight format, back
+    # to back over enough weight copies to stream from HBM every launch.
+    call = None
+    fm = {}
+    for fmt in (B.Q2_G32, B.Q3_G32, B.Q4_G32, B.Q5_G32, B.Q6_G32, B.Q8_G32, B.F16, B.BF16):
+        kh, nh = workloads.LLAMA32_3B["lm_head"]
+        w = inputs.weights_dev(inputs.seed_for(2, 28, "lm_head"), (nh, kh))
+        wd = B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE)
+        del w
+        x = inputs.activations_dev(inputs.seed_for(2, 28, "x"), (kh,))
+        call = GemvCall(lib, wd, x, torch.empty(nh, dtype=torch.float32, device="cuda"))
+        nbytes = workloads.weight_bytes(fmt, kh, nh)
+        copies = max(1, -(-600_000_000 // nbytes))
+        us = steady_launch_us(torch, B, call, copies=copies, reps=max(12, 2 * copies))
+        fm[workloads.FORMAT_NAMES[fmt]] = {"weight_MB": round(nbytes / 1e6, 1), "us": round(us, 3),
+                                           "GBps": round(nbytes / us / 1e3, 1),
+                                           "frac_hbm_peak": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)}
+        del call, wd
+        torch.cuda.empty_cache()
+    out["llama3.2-3b_lm_head_by_format"] = fm
+    log(f"lm_head by format: {fm}")
     return out
 
 

@@ -25,36 +25,56 @@
  *    race; the library holds no state besides an immutable per-device
  *    configuration table.
  *
- * Weight format (group-32 symmetric, one fp16 scale per 32 weights along K)
- *  For row n and group g = k / 32 of a weight matrix W [N][K]:
+ * Weight formats (Sec. 4.1: Q2, Q3, Q4, Q5, Q6, Q8, BF16 and FP16)
+ *  Integer formats Qb (b = 2, 3, 4, 5, 6, 8 bits), group-32 symmetric, one
+ *  fp16 scale per 32 weights along K.  For row n and group g = k / 32 of a
+ *  weight matrix W [N][K]:
  *    m = max |w| over the group (fp32), s32 = m / qmax (fp32, correctly
  *    rounded), s16 = fp16_RNE(s32), s = value(s16);
  *    q = 0 if s == 0, else clamp(rint_half_even(w / s), lo, hi)  (fp32 division);
- *    Q4 (QM_Q4_G32): qmax = 7,   [lo, hi] = [-8, 7];
- *    Q8 (QM_Q8_G32): qmax = 127, [lo, hi] = [-127, 127].
- *  The dequantised weight is w' = s * q, exact in fp32.
+ *    qmax = 2^(b-1) - 1 and [lo, hi] = [-2^(b-1), 2^(b-1) - 1], except Q8:
+ *    qmax = 127, [lo, hi] = [-127, 127].  (Q2: qmax 1, Q3: 3, Q4: 7, Q5: 15,
+ *    Q6: 31.)  The dequantised weight is w' = s * q, exact in fp32.
+ *  Float formats F16 and BF16: w is rounded to fp16 / bf16 (round to nearest
+ *  even; fp16 subnormals kept) and w' is that value; there are no scales
+ *  (the scale buffer has 0 bytes and `scales` may be NULL).
  *
  *  CANONICAL layout (QM_LAYOUT_CANONICAL):
- *    Q4 codes: uint8 [N][K/2], byte j = (q[2j] & 0xF) | ((q[2j+1] & 0xF) << 4)
- *              (even k in the low nibble, two's complement nibbles);
- *    Q8 codes: int8 [N][K], two's complement;
+ *    Qb codes: per row a little-endian bit stream of K*b/8 bytes; code k is
+ *              the b-bit two's complement of q at bits b*k .. b*k + b - 1
+ *              (bit i of the stream is bit i%8 of byte i/8).  So Q4 byte j =
+ *              (q[2j] & 0xF) | ((q[2j+1] & 0xF) << 4) and Q8 is int8 [N][K];
+ *    F16/BF16: uint16 [N][K] bit patterns;
  *    scales:   uint16 [N][K/32], fp16 bit patterns.
  *
  *  DEVICE layout (QM_LAYOUT_DEVICE), the one the matmul kernels read: rows
  *  are grouped into panels of 64 (N is padded up to a multiple of 64 with
- *  zero bytes), and the 32 codes of one (row, group) form a "chunk".
- *    Q4: chunk = 16 bytes at byte ((p*G + g)*64 + r)*16, p = n/64, r = n%64,
- *        G = K/32.  Dword j of the chunk covers k = 32g + 8j .. 32g + 8j + 7;
- *        its nibble t (bits 4t..4t+3) holds the offset-binary code q + 8 of
- *        k-offset 2t (t < 4) or 2(t-4)+1 (t >= 4).
- *    Q8: chunk = 32 bytes split in two 16-byte halves h = 0, 1 (k = 32g + 16h
- *        .. +15); half h of row r sits at byte ((p*G + g)*2 + h)*1024 + r*16,
- *        each byte the offset-binary code q + 128.
+ *  zero bytes), and the 32 codes of one (row, group) form a "chunk"; the
+ *  chunks of one (panel p = n/64, group g) lie together at byte
+ *  (p*G + g) * CB, G = K/32, r = n%64, CB the chunk block size below.
+ *  Integer codes are stored offset-binary, u = q + 2^(b-1) (Q8: q + 128).
+ *    Q4 (CB 1024): row r's 16 bytes at 16r.  Dword j covers k = 8j .. 8j+7
+ *        of the group; its nibble t (bits 4t..4t+3) holds u of k-offset 2t
+ *        (t < 4) or 2(t-4)+1 (t >= 4).
+ *    Q8 (CB 2048): two 16-byte halves h = 0, 1 (k = 16h .. 16h+15); half h of
+ *        row r at h*1024 + 16r, byte i = u of k = 16h + i.
+ *    Q2, Q3, Q5, Q6: u is split into bit planes, each plane 64 rows of equal
+ *        size, one after the other:
+ *          nibble plane (16 B a row, u & 15), order as Q4;
+ *          crumb plane (8 B a row): dword j, bits 2t..2t+1 hold k = 16j + 2t
+ *            and bits 16+2t..17+2t hold k = 16j + 2t + 1 (t = 0..7);
+ *          bit plane (4 B a row): bit t holds k = 2t, bit 16+t holds k = 2t+1.
+ *        Q2 (CB 512):  crumbs of u.
+ *        Q3 (CB 768):  crumbs of u & 3 (512 B), then bits of u >> 2 (256 B).
+ *        Q5 (CB 1280): nibbles of u & 15 (1024 B), then bits of u >> 4.
+ *        Q6 (CB 1536): nibbles of u & 15 (1024 B), then crumbs of u >> 4.
+ *    F16/BF16 (CB 4096): four 16-byte quarters j = 0..3 (k = 8j .. 8j+7, in
+ *        order); quarter j of row r at j*1024 + 16r.
  *    scales: uint16 at element (p*G + g)*64 + r.
  *  Stacked matrices (batch > 1, e.g. the experts of a MoE layer) place
  *  matrix b at b * (bytes of one matrix) in both buffers, in both layouts.
- *  Every 64-lane wavefront load of one chunk index over a panel reads 1 KiB
- *  (Q4) of contiguous bytes, so the weight stream is fully coalesced.
+ *  Every 64-lane wavefront load of one plane (or half, or quarter) of a chunk
+ *  block reads contiguous bytes, so the weight stream is fully coalesced.
  */
 #ifndef QMATMUL_H
 #define QMATMUL_H
@@ -77,13 +97,17 @@ typedef enum {
   QM_EDEVICE = 7      /* the HIP runtime reported an error                */
 } qm_status;
 
-enum { QM_Q4_G32 = 1, QM_Q8_G32 = 2 };
+enum {
+  QM_Q4_G32 = 1, QM_Q8_G32 = 2, QM_Q2_G32 = 3, QM_Q3_G32 = 4, QM_Q5_G32 = 5, QM_Q6_G32 = 6,
+  QM_F16 = 7, QM_BF16 = 8
+};
 enum { QM_LAYOUT_CANONICAL = 0, QM_LAYOUT_DEVICE = 1 };
 
 /* Non-owning view of a quantised weight tensor [batch][n][k].
- * qdata: device codes in `layout`; scales: device fp16 bits.  k % 32 == 0.
- * Both pointers must be 16-byte aligned; the buffers must hold at least the
- * sizes qm_weight_bytes() returns for (format, layout, batch, n, k). */
+ * qdata: device codes in `layout`; scales: device fp16 bits (unused, may be
+ * NULL, for F16/BF16).  k % 32 == 0.  Both pointers must be 16-byte aligned;
+ * the buffers must hold at least the sizes qm_weight_bytes() returns for
+ * (format, layout, batch, n, k). */
 typedef struct {
   int32_t format;
   int32_t layout;
@@ -106,8 +130,9 @@ qm_status qm_weight_bytes(int32_t format, int32_t layout, int64_t batch, int64_t
 /* Quantise fp32 weights w [batch][n][k] (device, row-major) into `out`, which
  * must be in CANONICAL layout with out->format set.  Bit-exact with the
  * format definition above (one thread per group, IEEE fp32 division,
- * round-half-even, fp16 round-to-nearest-even).  Weights must be finite and
- * every group's max|w| / qmax must be <= 65504 (not scanned). */
+ * round-half-even, fp16 round-to-nearest-even; F16/BF16: one rounding per
+ * weight).  Weights must be finite and every group's max|w| / qmax must be
+ * <= 65504 (F16: every |w| below 65520), not scanned. */
 qm_status qm_quantise(int32_t format, const float* w, const qm_qweight* out, void* stream);
 
 /* Dequantise w (either layout) into fp32 out [batch][n][k] (device):
@@ -120,9 +145,10 @@ qm_status qm_dequantise(const qm_qweight* w, float* out, void* stream);
  * src and dst buffers must not overlap. */
 qm_status qm_repack(const qm_qweight* src, const qm_qweight* dst, void* stream);
 
-/* Decode GEMV (Sec. 3.3, M = 1): y[n] = sum_k s[n][k/32] * q[n][k] * x[k].
- * w: DEVICE layout, batch 1, Q4 or Q8.  x: fp16 [k] (device).  y: fp32 [n]
- * (device).  Dequantisation happens in registers; products and sums in fp32.
+/* Decode GEMV (Sec. 3.3, M = 1): y[n] = sum_k w'[n][k] * x[k].
+ * w: DEVICE layout, batch 1, any format (one kernel per format).  x: fp16
+ * [k] (device).  y: fp32 [n] (device).  Dequantisation happens in
+ * registers; products and sums in fp32.
  * Single kernel launch, no workspace, deterministic. */
 qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* stream);
 
@@ -130,7 +156,7 @@ qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* s
  * activation fused into the producing kernel, saving a launch and a
  * global-memory round trip):
  *   h[n] = silu(g[n]) * u[n],  g = Wg' x,  u = Wu' x,  silu(z) = z / (1 + e^-z).
- * w_gate, w_up: DEVICE layout, batch 1, the same format (Q4 or Q8) and the
+ * w_gate, w_up: DEVICE layout, batch 1, the same format (any) and the
  * same n and k.  x: fp16 [k] (16-byte aligned); h: fp32 [n].  g and u are
  * accumulated as in qmatmul_gemv (fp32), in one pass over the same rows of
  * both matrices.  Deterministic. */
@@ -157,7 +183,8 @@ qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_
  * q/k/v projections of a layer, or its gate and up projections, which all
  * read the same X):  Y_i[m][n_i] = sum_k X[m][k] * w_i'[n_i][k]  for
  * i < count, in one launch.  w: host array of `count` descriptors, all of
- * one format (Q4 or Q8), DEVICE layout, batch 1, one k; n_i may differ.  X: fp16 [m][k] row-major
+ * one format (Q4 or Q8; any format when m == 1), DEVICE layout, batch 1,
+ * one k; n_i may differ.  X: fp16 [m][k] row-major
  * (device, 16-byte aligned), shared by all entries.  y: host array of
  * `count` device pointers to fp32 [m][n_i], 4-byte aligned, not
  * overlapping.  1 <= count <= 4 (QM_GEMM_GROUP_MAX); 1 <= m <= 65536 (m == 1
@@ -170,7 +197,8 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
 
 /* Prefill GEMM (Sec. 3.3, Sec. 3.4, M > 1): Y[m][n] = sum_k X[m][k] * w'[n][k].
  * w: DEVICE layout, batch 1, Q4 or Q8 (Sec. 4.1: both formats; the MFMA
- * path is the same, only the in-register unpacking differs).
+ * path is the same, only the in-register unpacking differs); any format
+ * when m == 1.  Other formats with m > 1: QM_EFORMAT.
  * X: fp16 [m][k] row-major; Y: fp32 [m][n].
  * X tiles and (for most tile shapes) the raw weight chunks are copied into
  * LDS by DMA; weights are dequantised to fp16 (value fp16_RNE(s*q)) in

@@ -16,7 +16,7 @@ from typing import Optional
 
 import torch
 
-Q4_G32, Q8_G32 = 1, 2
+Q4_G32, Q8_G32, Q2_G32, Q3_G32, Q5_G32, Q6_G32, F16, BF16 = 1, 2, 3, 4, 5, 6, 7, 8
 LAYOUT_CANONICAL, LAYOUT_DEVICE = 0, 1
 
 STATUS = {0: "QM_OK", 1: "QM_EINVAL", 2: "QM_ESHAPE", 3: "QM_EALIGN", 4: "QM_EFORMAT",
@@ -98,7 +98,8 @@ def _stream(stream=None):
 @dataclass
 class QWeight:
     """A quantised tensor [batch][n][k]: codes and fp16 scale bits in torch
-    uint8 / int16 buffers, in CANONICAL or DEVICE layout."""
+    uint8 / int16 buffers, in CANONICAL or DEVICE layout (F16/BF16: the
+    uint16 patterns as bytes; the scale buffer is a 1-element placeholder)."""
     format: int
     layout: int
     batch: int

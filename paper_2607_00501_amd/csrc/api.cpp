@@ -58,8 +58,7 @@ bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 
 qm_status check_weight(const qm_qweight* w, const char* name) {
   if (!w) return fail(QM_EINVAL, "%s: null weight descriptor", name);
-  if (w->format != QM_Q4_G32 && w->format != QM_Q8_G32)
-    return fail(QM_EFORMAT, "%s: unknown format %d", name, w->format);
+  if (!fmt_valid(w->format)) return fail(QM_EFORMAT, "%s: unknown format %d", name, w->format);
   if (w->layout != QM_LAYOUT_CANONICAL && w->layout != QM_LAYOUT_DEVICE)
     return fail(QM_ELAYOUT, "%s: unknown layout %d", name, w->layout);
   if (w->batch < 1 || w->n < 0 || w->k < 0)
@@ -69,8 +68,9 @@ qm_status check_weight(const qm_qweight* w, const char* name) {
     return fail(QM_ESHAPE, "%s: k=%lld must be a positive multiple of 32", name, (long long)w->k);
   if (w->n >= (int64_t(1) << 31) || w->k >= (int64_t(1) << 31))
     return fail(QM_ESHAPE, "%s: n and k must be < 2^31", name);
-  if (w->n > 0 && (!w->qdata || !w->scales)) return fail(QM_EINVAL, "%s: null data pointer", name);
-  if (!aligned16(w->qdata) || !aligned16(w->scales))
+  const bool scaled = !fmt_float(w->format);
+  if (w->n > 0 && (!w->qdata || (scaled && !w->scales))) return fail(QM_EINVAL, "%s: null data pointer", name);
+  if (!aligned16(w->qdata) || (scaled && !aligned16(w->scales)))
     return fail(QM_EALIGN, "%s: qdata and scales must be 16-byte aligned", name);
   return QM_OK;
 }
@@ -107,8 +107,7 @@ const char* qm_last_error(void) { return g_err; }
 qm_status qm_weight_bytes(int32_t format, int32_t layout, int64_t batch, int64_t n, int64_t k,
                           size_t* qbytes, size_t* sbytes) {
   if (!qbytes || !sbytes) return fail(QM_EINVAL, "qm_weight_bytes: null output pointer");
-  if (format != QM_Q4_G32 && format != QM_Q8_G32)
-    return fail(QM_EFORMAT, "qm_weight_bytes: unknown format %d", format);
+  if (!fmt_valid(format)) return fail(QM_EFORMAT, "qm_weight_bytes: unknown format %d", format);
   if (layout != QM_LAYOUT_CANONICAL && layout != QM_LAYOUT_DEVICE)
     return fail(QM_ELAYOUT, "qm_weight_bytes: unknown layout %d", layout);
   if (batch < 1 || n < 0 || k <= 0 || k % kGroup != 0)
@@ -116,7 +115,7 @@ qm_status qm_weight_bytes(int32_t format, int32_t layout, int64_t batch, int64_t
                 (long long)n, (long long)k);
   const int64_t rows = batch * matrix_rows(layout, n);
   *qbytes = static_cast<size_t>(rows * row_code_bytes(format, k));
-  *sbytes = static_cast<size_t>(rows * (k / kGroup) * 2);
+  *sbytes = static_cast<size_t>(rows * row_scales(format, k) * 2);
   return QM_OK;
 }
 
@@ -251,6 +250,8 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
       return fail(QM_ELAYOUT, "qmatmul_gemm_grouped: w[%d] must be in DEVICE layout", i);
     if (w[i].batch != 1) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: w[%d] batch must be 1", i);
     if (w[i].format != w[0].format) return fail(QM_EFORMAT, "qmatmul_gemm_grouped: formats differ");
+    if (m > 1 && w[i].format != QM_Q4_G32 && w[i].format != QM_Q8_G32)
+      return fail(QM_EFORMAT, "qmatmul_gemm_grouped: the MFMA GEMM takes Q4 or Q8 weights (m > 1)");
     if (w[i].k != w[0].k) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: k differs between entries");
     if (w[i].n > 0 && !y[i]) return fail(QM_EINVAL, "qmatmul_gemm_grouped: null y[%d]", i);
     if (!aligned4(y[i])) return fail(QM_EALIGN, "qmatmul_gemm_grouped: y[%d] must be 4-byte aligned", i);
@@ -289,6 +290,8 @@ qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float*
   if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "qmatmul_gemm: weights must be in DEVICE layout");
   if (w->batch != 1) return fail(QM_ESHAPE, "qmatmul_gemm: batch must be 1");
   if (m < 1 || m > 65536) return fail(QM_ESHAPE, "qmatmul_gemm: m=%lld must be in [1, 65536]", (long long)m);
+  if (m > 1 && w->format != QM_Q4_G32 && w->format != QM_Q8_G32)
+    return fail(QM_EFORMAT, "qmatmul_gemm: the MFMA GEMM takes Q4 or Q8 weights (m > 1)");
   if (w->n > 0 && (!x || !y)) return fail(QM_EINVAL, "qmatmul_gemm: null x or y");
   if (!aligned16(x)) return fail(QM_EALIGN, "qmatmul_gemm: x must be 16-byte aligned");
   if (!aligned4(y)) return fail(QM_EALIGN, "qmatmul_gemm: y must be 4-byte aligned");

@@ -18,46 +18,82 @@
 //    integers q (or 16q), one v_dot2_f32_f16 folds two weights into the
 //    fp32 group sum, and the fp16 group scale multiplies the group sum once
 //    (about 1.7 VALU operations per Q4 weight).  Q8 builds 0x64|u bytes with
-//    v_perm_b32 and subtracts 1152.
+//    v_perm_b32 and subtracts 1152.  Q5/Q6 add their high bit plane into the
+//    same fp16 lanes, Q2/Q3 mask crumbs in place with one fp32 sum per bit
+//    position, F16 feeds the stored pairs to v_dot2_f32_f16 and BF16 (the
+//    upper half of an fp32) goes through fp32 fma with the fp16 activation
+//    (Sec. 4.1: eight formats, one kernel each).
 #include "qm_internal.h"
 
 #include <hip/hip_fp16.h>
 
 #include <cstdio>
 #include <cstdlib>
+#include <type_traits>
 
 namespace qm {
 namespace {
 
+// fn(std::integral_constant<int, FMT>) for the runtime format (validated by
+// the caller).
+template <typename Fn>
+hipError_t with_format(int32_t fmt, Fn&& fn) {
+  switch (fmt) {
+    case QM_Q4_G32: return fn(std::integral_constant<int, QM_Q4_G32>{});
+    case QM_Q8_G32: return fn(std::integral_constant<int, QM_Q8_G32>{});
+    case QM_Q2_G32: return fn(std::integral_constant<int, QM_Q2_G32>{});
+    case QM_Q3_G32: return fn(std::integral_constant<int, QM_Q3_G32>{});
+    case QM_Q5_G32: return fn(std::integral_constant<int, QM_Q5_G32>{});
+    case QM_Q6_G32: return fn(std::integral_constant<int, QM_Q6_G32>{});
+    case QM_F16: return fn(std::integral_constant<int, QM_F16>{});
+    case QM_BF16: return fn(std::integral_constant<int, QM_BF16>{});
+    default: return hipErrorInvalidValue;
+  }
+}
+
 // Chunks in flight per lane in the panel kernel: 8 Q4 chunks (128 B) or 4
 // Q8 chunks (two 16-B halves each), from a per-shape sweep of the lm_head
-// sizes on MI355X.
-template <int FMT> constexpr int kPanelUnroll = FMT == QM_Q4_G32 ? 8 : 4;
+// sizes on MI355X; about 128 B for the other formats too.
+template <int FMT> constexpr int kPanelUnroll = FMT == QM_Q4_G32 ? 8 : FMT == QM_Q8_G32 ? 4
+                                              : FMT == QM_Q2_G32 ? 16 : FMT == QM_Q3_G32 ? 8
+                                              : FMT == QM_Q5_G32 ? 6 : FMT == QM_Q6_G32 ? 5 : 2;
+// Words (dwords) of one lane's chunk: 32 codes of b bits = b dwords.
+template <int FMT> constexpr int kWords = fmt_bits(FMT);
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 // In the large-matrix kernel weights and scales are streamed once per call:
 // nontemporal loads raise the sustained read rate (measured +12% on a plain
 // streaming read).  The small-matrix kernel keeps ordinary loads, whose
 // first-access latency measured lower.
-__device__ inline uint4 stream_load16(const uint8_t* p) {
+__device__ __forceinline__ uint4 stream_load16(const uint8_t* p) {
   const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
   return make_uint4(v.x, v.y, v.z, v.w);
 }
-__device__ inline uint32_t stream_load_u16(const uint16_t* p) {
+__device__ __forceinline__ uint32_t stream_load_u16(const uint16_t* p) {
   return __builtin_nontemporal_load(p);
 }
 
 // (a & mask) | magic as one v_and_or_b32: the masks live in VGPRs and the
 // magic in an SGPR (gfx9 VOP3 takes no literal operand), made opaque once
 // per kernel by DequantConsts.
-__device__ inline uint32_t and_or(uint32_t a, uint32_t mask_v, uint32_t or_s) { return (a & mask_v) | or_s; }
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t mask_v, uint32_t or_s) { return (a & mask_v) | or_s; }
 
+template <int FMT>
 struct DequantConsts {
   uint32_t m0, m1, magic;
+  uint32_t cm[4], bm[4];      // Q2/Q3: crumb masks 0x00030003 << 2s, Q3 bit masks 0x00040004 << 2s
   __device__ DequantConsts() : m0(0x000F000Fu), m1(0x00F000F0u), magic(0x64006400u) {
     asm volatile("" : "+v"(m0), "+v"(m1));
     asm volatile("" : "+s"(magic));
+#pragma unroll
+    for (int sc = 0; sc < 4; ++sc) {
+      cm[sc] = 0x00030003u << (2 * sc);
+      bm[sc] = 0x00040004u << (2 * sc);
+      if constexpr (FMT == QM_Q2_G32 || FMT == QM_Q3_G32) asm volatile("" : "+v"(cm[sc]));
+      if constexpr (FMT == QM_Q3_G32) asm volatile("" : "+v"(bm[sc]));
+    }
   }
 };
 
@@ -68,7 +104,8 @@ struct DequantConsts {
 // 20-23 land in mantissa bits 4-7 and give (1024 + 16u), i.e. 16*q after
 // subtracting 1152.  Those pairs accumulate separately and are scaled by
 // 1/16 (exact) at the end of the group.
-__device__ inline float dot_q4_chunk(const uint4 w, const uint32_t* xs, const DequantConsts& k) {
+template <class DC>
+__device__ __forceinline__ float dot_q4_chunk(const uint4 w, const uint32_t* xs, const DC& k) {
   const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
   const half2v b1 = {(_Float16)1032.0f, (_Float16)1032.0f};
   const half2v b16 = {(_Float16)1152.0f, (_Float16)1152.0f};
@@ -91,7 +128,7 @@ __device__ inline float dot_q4_chunk(const uint4 w, const uint32_t* xs, const De
 }
 
 // Sum over 16 Q8 codes (one half chunk, offset-binary bytes) of q * x.
-__device__ inline float dot_q8_half(const uint4 w, const uint32_t* xs) {
+__device__ __forceinline__ float dot_q8_half(const uint4 w, const uint32_t* xs) {
   const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
   const half2v bias = {(_Float16)1152.0f, (_Float16)1152.0f};
   float acc = 0.0f;
@@ -107,34 +144,189 @@ __device__ inline float dot_q8_half(const uint4 w, const uint32_t* xs) {
   return acc;
 }
 
+// Shift left by SH (right for negative SH); SH is a constant after unrolling.
+__device__ __forceinline__ uint32_t shift_by(uint32_t v, int sh) { return sh >= 0 ? v << sh : v >> -sh; }
+
+// Q5 / Q6: the nibble plane d[0..3] (u & 15, Q4 order) plus u >> 4 from the
+// bit plane d[4] (Q5) or the crumb plane d[4..5] (Q6).  As for Q4, the pairs
+// from nibble bits 0-3 give 1024 + u and those from bits 4-7 give
+// 1024 + 16u; the high part of u is moved to mantissa bit 4 (or 8) of the
+// same fp16 lanes with one shift and one v_and_or_b32.  16u <= 1008, so every
+// value stays in [1024, 2048), where fp16 is exact on the integers.
+template <int FMT>
+__device__ __forceinline__ float dot_nib_hi(const uint32_t* d, const uint32_t* xs, const DequantConsts<FMT>& k) {
+  constexpr int bias = FMT == QM_Q5_G32 ? 16 : 32;
+  const half2v b1 = {(_Float16)(1024 + bias), (_Float16)(1024 + bias)};
+  const half2v b16 = {(_Float16)(1024 + 16 * bias), (_Float16)(1024 + 16 * bias)};
+  float acc1 = 0.0f, acc16 = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t dj = d[j], dj8 = dj >> 8;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int i = 4 * j + t;                             // pair: codes 2i, 2i+1
+      const bool x16 = t & 1;
+      const int T = x16 ? 8 : 4;                           // target bit of the high part
+      const uint32_t base = and_or(t < 2 ? dj : dj8, x16 ? k.m1 : k.m0, k.magic);
+      uint32_t hi;
+      if constexpr (FMT == QM_Q5_G32) hi = shift_by(d[4], T - i) & ((1u << T) | (1u << (T + 16)));
+      else hi = shift_by(d[4 + i / 8], T - 2 * (i % 8)) & ((3u << T) | (3u << (T + 16)));
+      const half2v v = __builtin_bit_cast(half2v, base | hi) - (x16 ? b16 : b1);
+      if (x16) acc16 = __builtin_amdgcn_fdot2(v, __builtin_bit_cast(half2v, xs[i]), acc16, false);
+      else acc1 = __builtin_amdgcn_fdot2(v, __builtin_bit_cast(half2v, xs[i]), acc1, false);
+    }
+  }
+  return fmaf(acc16, 0.0625f, acc1);
+}
+
+// Q2 / Q3: the crumb plane d[0..1] (u & 3) plus, for Q3, u >> 2 from the bit
+// plane d[2].  The crumb pair of codes (2i, 2i+1) sits at bits 2t, 16 + 2t
+// of its dword (t = i % 8); masking it in place gives 1024 + 4^s u with
+// s = t % 4 (the upper four pairs after one shift by 8), the Q3 bit moves to
+// bit 2s + 2, and each power 4^s keeps its own fp32 sum, scaled at the end
+// (exactly).  4^3 * 7 = 448 keeps every value inside [1024, 2048).
+template <int FMT>
+__device__ __forceinline__ float dot_crumb(const uint32_t* d, const uint32_t* xs, const DequantConsts<FMT>& k) {
+  constexpr int bias = FMT == QM_Q2_G32 ? 2 : 4;
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int cd = 0; cd < 2; ++cd) {
+    const uint32_t c = d[cd], c8 = c >> 8;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int i = 8 * cd + t;
+      const int sc = t % 4;
+      uint32_t v = and_or(t < 4 ? c : c8, k.cm[sc], k.magic);      // masks in VGPRs: one v_and_or_b32
+      if constexpr (FMT == QM_Q3_G32) v = and_or(shift_by(d[2], 2 * sc + 2 - i), k.bm[sc], v);
+      const _Float16 bb = (_Float16)(1024 + (bias << (2 * sc)));
+      const half2v q = __builtin_bit_cast(half2v, v) - half2v{bb, bb};
+      acc[sc] = __builtin_amdgcn_fdot2(q, __builtin_bit_cast(half2v, xs[i]), acc[sc], false);
+    }
+  }
+  return acc[0] + acc[1] * 0.25f + acc[2] * 0.0625f + acc[3] * 0.015625f;
+}
+
+// F16: fp16 products straight from the stored pairs.  BF16: each bf16 is the
+// upper half of an fp32; fp32 fma with the fp16 activation.
+__device__ __forceinline__ float dot_f16(const uint32_t* d, const uint32_t* xs) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    acc = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, d[i]), __builtin_bit_cast(half2v, xs[i]), acc, false);
+  return acc;
+}
+__device__ __forceinline__ float dot_bf16(const uint32_t* d, const uint32_t* xs) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const half2v xh = __builtin_bit_cast(half2v, xs[i]);
+    acc = fmaf(__uint_as_float(d[i] << 16), static_cast<float>(xh[0]), acc);
+    acc = fmaf(__uint_as_float(d[i] & 0xFFFF0000u), static_cast<float>(xh[1]), acc);
+  }
+  return acc;
+}
+
+// Sum over one chunk (32 codes of one row and group) of w * x, before the
+// group scale (integer formats) or final (float formats).
+template <int FMT>
+__device__ __forceinline__ float dot_chunk(const uint32_t* d, const uint32_t* xs, const DequantConsts<FMT>& k) {
+  if constexpr (FMT == QM_Q4_G32) return dot_q4_chunk(make_uint4(d[0], d[1], d[2], d[3]), xs, k);
+  else if constexpr (FMT == QM_Q8_G32)
+    return dot_q8_half(make_uint4(d[0], d[1], d[2], d[3]), xs) + dot_q8_half(make_uint4(d[4], d[5], d[6], d[7]), xs + 8);
+  else if constexpr (FMT == QM_Q5_G32 || FMT == QM_Q6_G32) return dot_nib_hi<FMT>(d, xs, k);
+  else if constexpr (FMT == QM_Q2_G32 || FMT == QM_Q3_G32) return dot_crumb<FMT>(d, xs, k);
+  else if constexpr (FMT == QM_F16) return dot_f16(d, xs);
+  else return dot_bf16(d, xs);
+}
+
+// One lane's share of chunk block `blk` (panel row r): the planes, halves or
+// quarters of the device layout, each a coalesced wavefront load.
+template <int W, bool NT>
+__device__ __forceinline__ void load_words(const uint8_t* p, uint32_t* d) {
+  if constexpr (W == 4) {
+    const u32x4 v = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)) : *reinterpret_cast<const u32x4*>(p);
+    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+  } else if constexpr (W == 2) {
+    const u32x2 v = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p)) : *reinterpret_cast<const u32x2*>(p);
+    d[0] = v.x; d[1] = v.y;
+  } else {
+    d[0] = NT ? __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p)) : *reinterpret_cast<const uint32_t*>(p);
+  }
+}
+template <int FMT, bool NT>
+__device__ __forceinline__ void load_chunk(const uint8_t* blk, int r, uint32_t* d) {
+  if constexpr (FMT == QM_Q4_G32) {
+    load_words<4, NT>(blk + 16 * r, d);
+  } else if constexpr (FMT == QM_Q8_G32) {
+    load_words<4, NT>(blk + 16 * r, d);
+    load_words<4, NT>(blk + 1024 + 16 * r, d + 4);
+  } else if constexpr (FMT == QM_Q2_G32) {
+    load_words<2, NT>(blk + 8 * r, d);
+  } else if constexpr (FMT == QM_Q3_G32) {
+    load_words<2, NT>(blk + 8 * r, d);
+    load_words<1, NT>(blk + 512 + 4 * r, d + 2);
+  } else if constexpr (FMT == QM_Q5_G32) {
+    load_words<4, NT>(blk + 16 * r, d);
+    load_words<1, NT>(blk + 1024 + 4 * r, d + 4);
+  } else if constexpr (FMT == QM_Q6_G32) {
+    load_words<4, NT>(blk + 16 * r, d);
+    load_words<2, NT>(blk + 1024 + 8 * r, d + 4);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) load_words<4, NT>(blk + 1024 * j + 16 * r, d + 4 * j);
+  }
+}
+
+// Group sum -> contribution: times the fp16 group scale (integer formats).
+template <int FMT>
+__device__ __forceinline__ float scaled_add(uint32_t sbits, float d, float acc) {
+  if constexpr (fmt_float(FMT)) return acc + d;
+  else return fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sbits))), d, acc);
+}
+
 // U chunks starting at chunk c (all in range): issue every load, then reduce.
 template <int FMT, int U>
-__device__ inline float gemv_chunks(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
+__device__ __forceinline__ float gemv_chunks(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
                                     const uint32_t* __restrict__ xw, int64_t ch0, int c, int lane,
-                                    const DequantConsts& k) {
-  constexpr int NW = FMT == QM_Q4_G32 ? 1 : 2;
-  uint4 wv[U][NW];
+                                    const DequantConsts<FMT>& k) {
+  uint32_t wv[U][kWords<FMT>];
   uint32_t sv[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int64_t ch = ch0 + c + u;
-    if (FMT == QM_Q4_G32) {
-      wv[u][0] = stream_load16(q + (ch * 64 + lane) * 16);
-    } else {
-      const uint8_t* base = q + ch * 2048 + lane * 16;
-      wv[u][0] = stream_load16(base);
-      wv[u][NW - 1] = stream_load16(base + 1024);
-    }
-    sv[u] = stream_load_u16(s + ch * 64 + lane);
+    load_chunk<FMT, true>(q + ch * chunk_block_bytes(FMT), lane, wv[u]);
+    if constexpr (!fmt_float(FMT)) sv[u] = stream_load_u16(s + ch * 64 + lane);
+    else sv[u] = 0;
   }
   float acc = 0.0f;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const uint32_t* xs = xw + (c + u) * 16;   // wavefront-uniform: scalar loads
-    float d;
-    if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][0], xs, k);
-    else d = dot_q8_half(wv[u][0], xs) + dot_q8_half(wv[u][NW - 1], xs + 8);
-    acc = fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sv[u]))), d, acc);
+    acc = scaled_add<FMT>(sv[u], dot_chunk<FMT>(wv[u], xs, k), acc);
+  }
+  return acc;
+}
+
+// The last cnt < U chunks of a wavefront's range as one pass: indices past
+// the end re-read the last chunk (a valid, cached address) and are not
+// reduced, so all loads still go out before the first use.
+template <int FMT, int U>
+__device__ __forceinline__ float gemv_chunks_tail(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
+                                         const uint32_t* __restrict__ xw, int64_t ch0, int c, int cnt, int lane,
+                                         const DequantConsts<FMT>& k) {
+  uint32_t wv[U][kWords<FMT>];
+  uint32_t sv[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t ch = ch0 + c + min(u, cnt - 1);
+    load_chunk<FMT, true>(q + ch * chunk_block_bytes(FMT), lane, wv[u]);
+    if constexpr (!fmt_float(FMT)) sv[u] = stream_load_u16(s + ch * 64 + lane);
+    else sv[u] = 0;
+  }
+  float acc = 0.0f;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    if (u < cnt) acc = scaled_add<FMT>(sv[u], dot_chunk<FMT>(wv[u], xw + (c + u) * 16, k), acc);   // uniform branch
   }
   return acc;
 }
@@ -152,12 +344,16 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
   const int c1 = min(groups, c0 + chunks_per_wave);
   const int64_t ch0 = panel * groups;                 // first (panel, group) chunk index
   const uint32_t* xw = reinterpret_cast<const uint32_t*>(x);
-  const DequantConsts dk;
+  const DequantConsts<FMT> dk;
 
   float acc = 0.0f;
   int c = c0;
   for (; c + U <= c1; c += U) acc += gemv_chunks<FMT, U>(q, s, xw, ch0, c, lane, dk);
-  for (; c < c1; ++c) acc += gemv_chunks<FMT, 1>(q, s, xw, ch0, c, lane, dk);
+  if constexpr (FMT == QM_Q4_G32 || FMT == QM_Q8_G32) {
+    for (; c < c1; ++c) acc += gemv_chunks<FMT, 1>(q, s, xw, ch0, c, lane, dk);
+  } else if (c < c1) {
+    acc += gemv_chunks_tail<FMT, U>(q, s, xw, ch0, c, c1 - c, lane, dk);
+  }
 
   if (WAVES == 1) {
     const int64_t n = panel * 64 + lane;
@@ -187,7 +383,8 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
 // (XLDS) or straight from global memory (four 16-byte loads per chunk,
 // served by the L1/L2 broadcast).  Per-row sums: butterfly over the chunk
 // lanes, then a fixed-order sum over wavefronts in LDS.
-constexpr int kSubU = 8;
+// Chunks per lane per pass: 8 (F16/BF16: 4, 64 B each).
+template <int FMT> constexpr int kSubU = fmt_float(FMT) ? 4 : 8;
 
 // One workgroup's share of one matrix: `block` of `nblocks` = N/SUBR.
 // SWIGLU: the same rows of a second matrix (q2, s2) go through the same
@@ -199,9 +396,8 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
                                               const uint16_t* __restrict__ x, float* __restrict__ y, int n_rows,
                                               int groups, int64_t block, int64_t nblocks) {
   constexpr int CL = 64 / SUBR;
-  constexpr int NW = FMT == QM_Q4_G32 ? 1 : 2;
   constexpr int NM = SWIGLU ? 2 : 1;                  // matrices
-  constexpr int U = kSubU;
+  constexpr int U = kSubU<FMT>;
   extern __shared__ uint4 xs[];                       // groups * 4 uint4 (K halves) if XLDS
   __shared__ float part[NM][WAVES][SUBR];
   const int lane = threadIdx.x & 63;
@@ -217,14 +413,14 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
   const int stride = WAVES * CL;
   const int first = wave * CL + cl;
   const int iters = (groups + U * stride - 1) / (U * stride);
-  const DequantConsts dk;
+  const DequantConsts<FMT> dk;
   const uint4* xg = reinterpret_cast<const uint4*>(x);
 
   float acc[NM];
 #pragma unroll
   for (int m = 0; m < NM; ++m) acc[m] = 0.0f;
   for (int it = 0; it < iters; ++it) {
-    uint4 wv[U][NM][NW];
+    uint32_t wv[U][NM][kWords<FMT>];
     uint32_t sv[U][NM];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -235,14 +431,9 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
         for (int m = 0; m < NM; ++m) {
           const uint8_t* qm = m == 0 ? q : q2;
           const uint16_t* sm = m == 0 ? s : s2;
-          if (FMT == QM_Q4_G32) {
-            wv[u][m][0] = *reinterpret_cast<const uint4*>(qm + (ch * 64 + row) * 16);
-          } else {
-            const uint8_t* base = qm + ch * 2048 + row * 16;
-            wv[u][m][0] = *reinterpret_cast<const uint4*>(base);
-            wv[u][m][NW - 1] = *reinterpret_cast<const uint4*>(base + 1024);
-          }
-          sv[u][m] = sm[ch * 64 + row];
+          load_chunk<FMT, false>(qm + ch * chunk_block_bytes(FMT), row, wv[u][m]);
+          if constexpr (!fmt_float(FMT)) sv[u][m] = sm[ch * 64 + row];
+          else sv[u][m] = 0;
         }
       }
     }
@@ -269,12 +460,7 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
           }
         }
 #pragma unroll
-        for (int m = 0; m < NM; ++m) {
-          float d;
-          if (FMT == QM_Q4_G32) d = dot_q4_chunk(wv[u][m][0], xv, dk);
-          else d = dot_q8_half(wv[u][m][0], xv) + dot_q8_half(wv[u][m][NW - 1], xv + 8);
-          acc[m] = fmaf(__half2float(__ushort_as_half(static_cast<uint16_t>(sv[u][m]))), d, acc[m]);
-        }
+        for (int m = 0; m < NM; ++m) acc[m] = scaled_add<FMT>(sv[u][m], dot_chunk<FMT>(wv[u][m], xv, dk), acc[m]);
       }
     }
   }
@@ -369,6 +555,15 @@ template <int FMT, int SUBR, bool XLDS>
 hipError_t launch_sub_waves(int waves, const GemvGroup& g, hipStream_t st) {
   const dim3 grid(static_cast<unsigned>(g.start[g.count]));
   const size_t lds = XLDS ? static_cast<size_t>(g.groups) * 64 : 0;
+  if constexpr (FMT != QM_Q4_G32 && FMT != QM_Q8_G32) {
+    // The other formats use the plan's 8 wavefronts only.
+    if (g.count == 1)
+      hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, g.q[0], g.s[0], g.x[0],
+                         g.y[0], g.n[0], g.groups);
+    else
+      hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, g);
+    return hipGetLastError();
+  }
   if (g.count == 1) {
     const auto q = g.q[0]; const auto s = g.s[0]; const auto x = g.x[0]; const auto y = g.y[0];
     const int n = g.n[0], gi = g.groups;
@@ -427,9 +622,19 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
     case 1: hipLaunchKernelGGL((gemv_kernel<FMT, 1, U>), grid, dim3(64), 0, st, q, s, x, y, ni, gi, cpw); break;
     case 2: hipLaunchKernelGGL((gemv_kernel<FMT, 2, U>), grid, dim3(128), 0, st, q, s, x, y, ni, gi, cpw); break;
     case 4: hipLaunchKernelGGL((gemv_kernel<FMT, 4, U>), grid, dim3(256), 0, st, q, s, x, y, ni, gi, cpw); break;
-    case 8: hipLaunchKernelGGL((gemv_kernel<FMT, 8, U>), grid, dim3(512), 0, st, q, s, x, y, ni, gi, cpw); break;
-    case 12: hipLaunchKernelGGL((gemv_kernel<FMT, 12, U>), grid, dim3(768), 0, st, q, s, x, y, ni, gi, cpw); break;
-    default: hipLaunchKernelGGL((gemv_kernel<FMT, 16, U>), grid, dim3(1024), 0, st, q, s, x, y, ni, gi, cpw); break;
+    default:
+      if constexpr (FMT == QM_Q4_G32) {       // only the Q4 plan goes beyond 8 wavefronts
+        if (waves == 12) {
+          hipLaunchKernelGGL((gemv_kernel<FMT, 12, U>), grid, dim3(768), 0, st, q, s, x, y, ni, gi, cpw);
+          break;
+        }
+        if (waves == 16) {
+          hipLaunchKernelGGL((gemv_kernel<FMT, 16, U>), grid, dim3(1024), 0, st, q, s, x, y, ni, gi, cpw);
+          break;
+        }
+      }
+      hipLaunchKernelGGL((gemv_kernel<FMT, 8, U>), grid, dim3(512), 0, st, q, s, x, y, ni, gi, cpw);
+      break;
   }
   return hipGetLastError();
 }
@@ -439,8 +644,8 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
 // Per-chip launch plan, from per-shape sweeps on MI355X (256 CUs).
 // Matrices with at least one 64-row panel per CU use the panel kernel.  Q4:
 // enough wavefronts per panel for one pass of 8 chunks each (4 at K = 1024,
-// 12 at K = 3072), at most 16; Q8: 8 wavefronts (fewer only if there are
-// fewer groups).  Smaller matrices use the sub-panel kernel with 8
+// 12 at K = 3072), at most 16; other formats: 8 wavefronts (fewer only if
+// there are fewer groups).  Smaller matrices use the sub-panel kernel with 8
 // wavefronts per workgroup and the smallest row count (8, 16 or 32; from 4
 // for N <= 1024 with K >= 2048) that keeps the grid at <= 2 workgroups per
 // CU; activations are staged in LDS for K <= 4096 and read from global
@@ -503,9 +708,10 @@ hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count,
     return hipSuccess;
   }
   g.groups = static_cast<int>(k / kGroup);
-  if (fmt == QM_Q4_G32)
-    return plan.xlds ? launch_sub<QM_Q4_G32, true>(plan, g, st) : launch_sub<QM_Q4_G32, false>(plan, g, st);
-  return plan.xlds ? launch_sub<QM_Q8_G32, true>(plan, g, st) : launch_sub<QM_Q8_G32, false>(plan, g, st);
+  return with_format(fmt, [&](auto f) {
+    constexpr int F = decltype(f)::value;
+    return plan.xlds ? launch_sub<F, true>(plan, g, st) : launch_sub<F, false>(plan, g, st);
+  });
 }
 
 namespace {
@@ -551,15 +757,15 @@ hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg
     plan.xlds = k <= 4096 ? 1 : 0;
   }
   const int groups = static_cast<int>(k / kGroup);
-  return fmt == QM_Q4_G32 ? launch_swiglu_fmt<QM_Q4_G32>(plan, qg, sg, qu, su, x, h, n, groups, st)
-                          : launch_swiglu_fmt<QM_Q8_G32>(plan, qg, sg, qu, su, x, h, n, groups, st);
+  return with_format(fmt, [&](auto f) {
+    return launch_swiglu_fmt<decltype(f)::value>(plan, qg, sg, qu, su, x, h, n, groups, st);
+  });
 }
 
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
                        int64_t n, int64_t k, int cu_count, hipStream_t st) {
   if (n == 0) return hipSuccess;
-  return fmt == QM_Q4_G32 ? launch_fmt<QM_Q4_G32>(q, s, x, y, n, k, cu_count, st)
-                          : launch_fmt<QM_Q8_G32>(q, s, x, y, n, k, cu_count, st);
+  return with_format(fmt, [&](auto f) { return launch_fmt<decltype(f)::value>(q, s, x, y, n, k, cu_count, st); });
 }
 
 }  // namespace qm

@@ -43,8 +43,20 @@ __host__ __device__ inline void xcd_group_member(int64_t i, int64_t groups, int 
   }
 }
 
+// Weight formats: bits per weight, float (no scales) or integer, validity.
+__host__ __device__ constexpr int fmt_bits(int32_t fmt) {
+  return fmt == QM_Q2_G32 ? 2 : fmt == QM_Q3_G32 ? 3 : fmt == QM_Q4_G32 ? 4 : fmt == QM_Q5_G32 ? 5
+       : fmt == QM_Q6_G32 ? 6 : fmt == QM_Q8_G32 ? 8 : 16;
+}
+__host__ __device__ constexpr bool fmt_float(int32_t fmt) { return fmt == QM_F16 || fmt == QM_BF16; }
+__host__ __device__ constexpr bool fmt_valid(int32_t fmt) { return fmt >= QM_Q4_G32 && fmt <= QM_BF16; }
+// Bytes of one (panel, group) chunk block of the device layout: 64 rows x 32 codes.
+__host__ __device__ constexpr int chunk_block_bytes(int32_t fmt) { return 256 * fmt_bits(fmt); }
+
 // Bytes of codes per row of one matrix (canonical and device layouts agree).
-__host__ __device__ inline int64_t row_code_bytes(int32_t fmt, int64_t k) { return fmt == QM_Q4_G32 ? k / 2 : k; }
+__host__ __device__ inline int64_t row_code_bytes(int32_t fmt, int64_t k) { return k * fmt_bits(fmt) / 8; }
+// Scale elements per row (none for the float formats).
+__host__ __device__ inline int64_t row_scales(int32_t fmt, int64_t k) { return fmt_float(fmt) ? 0 : k / kGroup; }
 
 // Per-matrix sizes for a layout.
 __host__ __device__ inline int64_t matrix_rows(int32_t layout, int64_t n) {

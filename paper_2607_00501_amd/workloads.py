@@ -46,3 +46,14 @@ def q4_bytes(k: int, n: int) -> int:
 
 def q8_bytes(k: int, n: int) -> int:
     return n * k + n * (k // 32) * 2
+
+
+FORMAT_BITS = {1: 4, 2: 8, 3: 2, 4: 3, 5: 5, 6: 6, 7: 16, 8: 16}   # format id -> bits per weight
+FORMAT_NAMES = {1: "q4", 2: "q8", 3: "q2", 4: "q3", 5: "q5", 6: "q6", 7: "f16", 8: "bf16"}
+
+
+def weight_bytes(fmt: int, k: int, n: int) -> int:
+    """Algorithmic weight bytes of a K -> N matrix in any format: b/8 bytes
+    per code, plus a 2-byte scale per 32 codes for the integer formats."""
+    b = FORMAT_BITS[fmt]
+    return n * k * b // 8 + (0 if b == 16 else n * (k // 32) * 2)

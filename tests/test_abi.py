@@ -35,13 +35,20 @@ def test_library_exports_every_declared_symbol():
     (B.Q8_G32, B.LAYOUT_DEVICE, 2, 65, 32, (2 * 128 * 32, 2 * 128 * 2)),
     (B.Q4_G32, B.LAYOUT_DEVICE, 1, 151936, 1024, (151936 * 512, 151936 * 32 * 2)),
     (B.Q8_G32, B.LAYOUT_CANONICAL, 128, 768, 2048, (128 * 768 * 2048, 128 * 768 * 64 * 2)),
+    (B.Q2_G32, B.LAYOUT_DEVICE, 1, 3, 64, (64 * 64 * 2 // 8, 64 * 2 * 2)),
+    (B.Q3_G32, B.LAYOUT_CANONICAL, 2, 5, 96, (2 * 5 * 96 * 3 // 8, 2 * 5 * 3 * 2)),
+    (B.Q5_G32, B.LAYOUT_DEVICE, 1, 65, 32, (128 * 32 * 5 // 8, 128 * 1 * 2)),
+    (B.Q6_G32, B.LAYOUT_CANONICAL, 1, 7, 64, (7 * 64 * 6 // 8, 7 * 2 * 2)),
+    (B.F16, B.LAYOUT_DEVICE, 1, 65, 64, (128 * 64 * 2, 0)),
+    (B.BF16, B.LAYOUT_CANONICAL, 3, 5, 32, (3 * 5 * 32 * 2, 0)),
 ])
 def test_weight_bytes(fmt, layout, batch, n, k, want):
     assert B.qm_weight_bytes(fmt, layout, batch, n, k) == want
 
 
 @pytest.mark.parametrize("args,status", [
-    ((3, 0, 1, 4, 64), 4),          # bad format
+    ((9, 0, 1, 4, 64), 4),          # bad format
+    ((0, 0, 1, 4, 64), 4),          # bad format
     ((1, 7, 1, 4, 64), 5),          # bad layout
     ((1, 0, 1, 4, 48), 2),          # k % 32
     ((1, 0, 0, 4, 64), 2),          # batch 0
@@ -88,8 +95,9 @@ def test_gemm_and_moe_validation():
     x, y = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x40000)
     assert L.qmatmul_gemm(ctypes.byref(w), x, 0, y, None) == 2          # m = 0
     assert L.qmatmul_gemm(ctypes.byref(w), x, 70000, y, None) == 2      # m too large
-    w8 = _fake_weight(fmt=3)
-    assert L.qmatmul_gemm(ctypes.byref(w8), x, 16, y, None) == 4        # unknown format
+    assert L.qmatmul_gemm(ctypes.byref(_fake_weight(fmt=9)), x, 16, y, None) == 4   # unknown format
+    for f in (B.Q2_G32, B.Q3_G32, B.Q5_G32, B.Q6_G32, B.F16, B.BF16):
+        assert L.qmatmul_gemm(ctypes.byref(_fake_weight(fmt=f)), x, 16, y, None) == 4   # no MFMA GEMM
     assert L.qmatmul_gemm(ctypes.byref(_fake_weight(layout=0)), x, 16, y, None) == 5
     p = ctypes.c_void_p(0x50000)
     assert L.qmoe_route(p, 16, 2000, 8, p, p, p, p, p, None) == 2       # too many experts
@@ -141,6 +149,23 @@ def test_error_text_is_thread_local():
     assert seen["before"] == ""
     assert "layout" in seen["after"]
     assert B.qm_last_error() == main_msg and "format" in main_msg
+
+
+def test_float_formats_need_no_scales():
+    """F16/BF16 descriptors may carry a null scale pointer; the integer
+    formats may not."""
+    L = B.lib()
+    y = ctypes.c_void_p(0x40000)
+    for f in (B.F16, B.BF16):
+        w = _fake_weight(fmt=f, layout=0, scales=0)
+        # passes the descriptor checks and stops at the null output
+        assert L.qm_dequantise(ctypes.byref(w), None, None) == 1
+        assert "null output" in B.qm_last_error()
+    w = _fake_weight(fmt=B.Q5_G32, layout=0, scales=0)
+    assert L.qm_dequantise(ctypes.byref(w), None, None) == 1
+    assert "null data pointer" in B.qm_last_error()
+    w = _fake_weight(fmt=B.F16, scales=0x20008)                       # misaligned but unused
+    assert L.qmatmul_gemv(ctypes.byref(w), ctypes.c_void_p(0x30004), y, None) == 3   # x still checked
 
 
 def test_gemv_swiglu_validation():
@@ -204,7 +229,8 @@ def test_gemm_grouped_validation():
     assert L.qmatmul_gemm_grouped(1, None, x, 16, None, None) == 1     # null arrays
     assert call([w], m=0) == 2                                         # m < 1
     assert call([w, _fake_weight(fmt=2)]) == 4                         # formats differ
-    assert call([_fake_weight(fmt=3)] * 2) == 4                        # unknown format
+    assert call([_fake_weight(fmt=9)] * 2) == 4                        # unknown format
+    assert call([_fake_weight(fmt=B.Q5_G32)] * 2) == 4                 # no MFMA GEMM for Q5
     assert call([w, _fake_weight(k=96)]) == 2                          # k differs
     assert call([w, _fake_weight(layout=0)]) == 5                      # not DEVICE layout
     assert call([w, w], ys=[0x40000, 0x40002]) == 3                    # y[1] misaligned

@@ -1,0 +1,141 @@
+"""GPU parity of the Q2/Q3/Q5/Q6 and F16/BF16 weight formats: quantise,
+repack and dequantise bit-exact with the oracle and the device layout's
+definition, and the decode GEMV (single, grouped, SwiGLU pair) against the
+oracle."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import qmatmul_oracle as O
+from paper_2607_00501_amd import binding as B
+from paper_2607_00501_amd import inputs
+from tests.helpers import GEMV_TOL, device_layout, rel_err
+
+pytestmark = pytest.mark.gpu
+
+FMTS = [(O.Q2, B.Q2_G32), (O.Q3, B.Q3_G32), (O.Q5, B.Q5_G32), (O.Q6, B.Q6_G32),
+        (O.F16, B.F16), (O.BF16, B.BF16)]
+INT_FMTS = FMTS[:4]
+
+
+def _quantise(w_np, bfmt):
+    qw = B.qm_quantise(torch.from_numpy(np.ascontiguousarray(w_np)).cuda(), bfmt)
+    torch.cuda.synchronize()
+    return qw
+
+
+def _ref(w, ofmt):
+    q, s = O.quantise(w, ofmt)
+    return O.pack(q, ofmt), s
+
+
+@pytest.mark.parametrize("ofmt,bfmt", FMTS)
+@pytest.mark.parametrize("batch,n,k", [(1, 1, 32), (1, 65, 96), (3, 70, 64), (1, 200, 2048)])
+def test_quantise_repack_dequantise_bit_exact(ofmt, bfmt, batch, n, k):
+    w = inputs.weights_np(inputs.seed_for(4, n + batch, "up"), (batch, n, k))
+    qc = _quantise(w, bfmt)
+    qd = B.qm_repack(qc, B.LAYOUT_DEVICE)
+    back = B.qm_repack(qd, B.LAYOUT_CANONICAL)
+    dq_c, dq_d = B.qm_dequantise(qc), B.qm_dequantise(qd)
+    torch.cuda.synchronize()
+    qcb, qdb = qc.qdata.cpu().numpy(), qd.qdata.cpu().numpy()
+    per_c, per_d = qcb.size // batch, qdb.size // batch
+    for b in range(batch):
+        qbytes, s = _ref(w[b], ofmt)
+        assert np.array_equal(qcb[b * per_c:(b + 1) * per_c], np.ascontiguousarray(qbytes).view(np.uint8).reshape(-1))
+        q_codes = O.unpack(qbytes, ofmt) if ofmt not in O.FLOATS else qbytes
+        want_q, want_s = device_layout(q_codes, s, ofmt)
+        assert np.array_equal(qdb[b * per_d:(b + 1) * per_d], want_q)
+        if s is not None:
+            sc = qc.scales.cpu().numpy().view(np.uint16)
+            sd = qd.scales.cpu().numpy().view(np.uint16)
+            ps, pd = sc.size // batch, sd.size // batch
+            assert np.array_equal(sc[b * ps:(b + 1) * ps].reshape(n, k // 32), s)
+            assert np.array_equal(sd[b * pd:(b + 1) * pd], want_s)
+        ref = O.dequantise(qbytes, s, ofmt)
+        assert np.array_equal(dq_c[b].cpu().numpy().view(np.uint32), ref.view(np.uint32))
+        assert np.array_equal(dq_d[b].cpu().numpy().view(np.uint32), ref.view(np.uint32))
+    assert torch.equal(back.qdata, qc.qdata)
+    if ofmt not in O.FLOATS:
+        assert torch.equal(back.scales, qc.scales)
+
+
+@pytest.mark.parametrize("ofmt,bfmt", FMTS)
+def test_quantise_edge_groups_bit_exact(ofmt, bfmt):
+    """Ties, one-hot, all-zero, subnormal scales, tiny groups, large values,
+    fp16/bf16 rounding ties."""
+    def group(vals):
+        g = np.zeros(32, np.float32)
+        g[:len(vals)] = vals
+        return g
+    rows = [np.concatenate([group([7, -7, 2.5, 3.5, -2.5, -0.5, 0.5, 1.5]), group([0.03])]),
+            np.concatenate([group([1e-6, -5e-7]), group([-1e-6, 5e-7])]),
+            np.concatenate([group([]), group([1e-9, -3e-9])]),
+            np.concatenate([group([1000.0, -999.0, 0.1]), group([-127.0, 63.5, 64.5])]),
+            np.concatenate([group([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -11]),
+                            group([-(1.0 + 2.0 ** -11), 2.0 ** -24, 3 * 2.0 ** -25])])]
+    rng = np.random.default_rng(5)
+    rows.append((rng.standard_normal(64) * 1e-5).astype(np.float32))
+    w = np.stack(rows).astype(np.float32)
+    qc = _quantise(w, bfmt)
+    qbytes, s = _ref(w, ofmt)
+    assert np.array_equal(qc.qdata.cpu().numpy(), np.ascontiguousarray(qbytes).view(np.uint8).reshape(-1))
+    if s is not None:
+        assert np.array_equal(qc.scales.cpu().numpy().view(np.uint16).reshape(s.shape), s)
+
+
+def _device(w, bfmt):
+    return B.qm_repack(_quantise(w, bfmt), B.LAYOUT_DEVICE)
+
+
+# Panel kernel (N >= 16384), sub-panel kernel with 4/8/16/32-row workgroups,
+# x in LDS (K <= 4096) and from global memory, ragged N.
+@pytest.mark.parametrize("ofmt,bfmt", FMTS)
+@pytest.mark.parametrize("n,k", [(1, 32), (65, 96), (200, 1024), (1000, 2048), (130, 3072),
+                                 (64, 8192), (4100, 1024), (16448, 256)])
+def test_gemv_parity(ofmt, bfmt, n, k):
+    w = inputs.weights_np(inputs.seed_for(4, n, "q"), (n, k))
+    x = inputs.activations_np(inputs.seed_for(4, n, "x"), (k,))
+    y = B.qmatmul_gemv(_device(w, bfmt), torch.from_numpy(x).cuda()).cpu().numpy()
+    qbytes, s = _ref(w, ofmt)
+    ref = O.gemv(qbytes, s, ofmt, x)
+    assert rel_err(y, ref) <= GEMV_TOL
+    assert rel_err(y, ref) <= 1e-5
+
+
+@pytest.mark.parametrize("ofmt,bfmt", INT_FMTS)
+@pytest.mark.parametrize("n,k", [(300, 1536), (20000, 128)])
+def test_gemv_integer_grid_exact(ofmt, bfmt, n, k):
+    """Scale-1 integer weights covering every code in [-qmax, qmax] and
+    small integer x: the fp32 result is exact (sub-panel and panel
+    kernels)."""
+    rng = np.random.default_rng(3 + ofmt)
+    qm = O.QMAX[ofmt]
+    wi = rng.integers(-qm, qm + 1, size=(n, k))
+    wi[:, ::32] = qm
+    x = rng.integers(-3, 4, size=k).astype(np.float16)
+    w = wi.astype(np.float32)
+    y = B.qmatmul_gemv(_device(w, bfmt), torch.from_numpy(x).cuda()).cpu().numpy()
+    qbytes, s = _ref(w, ofmt)
+    assert np.array_equal(O.unpack(qbytes, ofmt), wi)
+    assert np.array_equal(y.astype(np.float64), O.gemv(qbytes, s, ofmt, x))
+
+
+@pytest.mark.parametrize("ofmt,bfmt", FMTS)
+def test_gemv_grouped_and_swiglu(ofmt, bfmt):
+    """q/k/v-like grouped GEMV and the SwiGLU pair in each format."""
+    k = 1024
+    ws = [inputs.weights_np(inputs.seed_for(4, i, "gate"), (n, k)) for i, n in enumerate([2048, 1024, 1000])]
+    x = inputs.activations_np(inputs.seed_for(4, 9, "x"), (k,))
+    xt = torch.from_numpy(x).cuda()
+    wd = [_device(w, bfmt) for w in ws]
+    ys = B.qmatmul_gemv_grouped(wd, [xt] * 3)
+    refs = []
+    for w, yv in zip(ws, ys):
+        qbytes, s = _ref(w, ofmt)
+        refs.append((qbytes, s))
+        assert rel_err(yv.cpu().numpy(), O.gemv(qbytes, s, ofmt, x)) <= 1e-5
+    h = B.qmatmul_gemv_swiglu(wd[0], wd[0], xt).cpu().numpy()          # gate = up = W_0
+    ref = O.gemv_swiglu(*refs[0], *refs[0], ofmt, x)
+    assert rel_err(h, ref) <= 1e-5
