@@ -1,4 +1,4 @@
-// Prefill GEMM  Y[m][n] = sum_k X[m][k] * w'[n][k]  with Q4 or Q8 weights
+// Prefill GEMM  Y[m][n] = sum_k X[m][k] * w'[n][k]  with Q2 .. Q8 weights
 // dequantised inside the kernel and fp16 MFMA (BaseRT Sec. 3.4: tiled GEMM
 // for the prompt, tile geometry chosen by sequence-length regime; Sec. 3.3:
 // dequantisation lives inside the GEMM, weights are never materialised).
@@ -33,9 +33,10 @@ hipError_t launch_tile(const QgemmArgs& a, hipStream_t st) {
 //  * else one 64-column panel per K slice with split-K over as many
 //    one-wavefront slices as keep >= 8 K steps each (at most 8), in 64-row
 //    tiles if that gives 4 wavefronts per CU, else 32-row tiles.
-// Q8 weights use the same plan: their 128 x 256 tile keeps the weights in
-// registers (twice the bytes do not fit in LDS beside 128-row A stages) and
-// still beats 64 x 256 tiles by 10-20% where the rule picks it.
+// The other formats use the same plan.  Where their weight stages do not fit
+// in LDS beside the A stages (Q8, Q5, Q6 at 128 x 256) the tile keeps the
+// weights in registers; for Q8 that still beats 64 x 256 tiles by 10-20%
+// where the rule picks it.
 GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count) {
   // Tuning sweeps only: QM_GEMM_PLAN="bm,wn,wk" forces the plan (one of the
   // instantiated tiles, see launch_args).
@@ -76,18 +77,40 @@ hipError_t launch_args(const QgemmArgs& a, int32_t fmt, int cu_count, hipStream_
   const int64_t panels = a.gpanel[a.gcount];
   if (panels == 0) return hipSuccess;
   const GemmPlan p = gemm_plan(a.M, panels * kPanel, a.K, cu_count);
-#define QM_LAUNCH4(BM, WN, WK) \
-  if (p.bm == BM && p.wn == WN && p.wk == WK) return launch_tile<BM, WN, WK, QM_Q4_G32>(a, st);
-#define QM_LAUNCH8(BM, WN, WK) \
-  if (p.bm == BM && p.wn == WN && p.wk == WK) return launch_tile<BM, WN, WK, QM_Q8_G32>(a, st);
-  if (fmt == QM_Q8_G32) {
-    QM_GEMM_TILES(QM_LAUNCH8)
-  } else {
-    QM_GEMM_TILES(QM_LAUNCH4)
+#define QM_LAUNCH_FMT(F) \
+  if (fmt == F) {                                                                            \
+    QM_GEMM_TILES(QM_LAUNCH_TILE)                                                            \
+    return hipErrorInvalidConfiguration;                                                     \
   }
-#undef QM_LAUNCH4
-#undef QM_LAUNCH8
-  return hipErrorInvalidConfiguration;
+#define QM_LAUNCH_TILE(BM, WN, WK) \
+  if (p.bm == BM && p.wn == WN && p.wk == WK) return launch_tile<BM, WN, WK, F_>(a, st);
+  {
+    constexpr int F_ = QM_Q4_G32;
+    QM_LAUNCH_FMT(QM_Q4_G32)
+  }
+  {
+    constexpr int F_ = QM_Q8_G32;
+    QM_LAUNCH_FMT(QM_Q8_G32)
+  }
+  {
+    constexpr int F_ = QM_Q2_G32;
+    QM_LAUNCH_FMT(QM_Q2_G32)
+  }
+  {
+    constexpr int F_ = QM_Q3_G32;
+    QM_LAUNCH_FMT(QM_Q3_G32)
+  }
+  {
+    constexpr int F_ = QM_Q5_G32;
+    QM_LAUNCH_FMT(QM_Q5_G32)
+  }
+  {
+    constexpr int F_ = QM_Q6_G32;
+    QM_LAUNCH_FMT(QM_Q6_G32)
+  }
+#undef QM_LAUNCH_TILE
+#undef QM_LAUNCH_FMT
+  return hipErrorInvalidValue;
 }
 
 }  // namespace

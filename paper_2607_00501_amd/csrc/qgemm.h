@@ -183,6 +183,58 @@ __device__ inline half8v dequant_q8(uint32_t d0, uint32_t d1, half2v s2, const D
   return half8v{v0[0], v0[1], v1[0], v1[1], v2[0], v2[1], v3[0], v3[1]};
 }
 
+// Shift left by SH (right for negative SH); SH is a constant after unrolling.
+__device__ __forceinline__ uint32_t shift_by(uint32_t v, int sh) { return sh >= 0 ? v << sh : v >> -sh; }
+
+// Bit-plane formats, substep s of a lane's 16 codes (k = 16h + 8s .. +7 of
+// the group, natural order) -> 8 fp16 fp16_RNE(s*q).
+//  Q5 / Q6: nibble dword nd (Q4 order) plus the high part of u: Q5 from the
+//  bit dword hb (already shifted right by 8h, so pair p of the 8 lies at
+//  bits p and 16 + p), Q6 from the crumb dword cw (pair p at 2p, 16 + 2p).
+//  The high bits join the Q4 fp16-magic lanes at mantissa bit 4 (lanes of
+//  1024 + u) or 8 (lanes of 1024 + 16u); both stay exact (16u <= 1008).
+template <int FMT>
+__device__ inline half8v dequant_nib_hi(uint32_t nd, uint32_t hi_w, int s, half2v s2, const DequantRegs& c) {
+  constexpr int bias = FMT == QM_Q5_G32 ? 16 : 32;
+  const half2v b1 = {(_Float16)(1024 + bias), (_Float16)(1024 + bias)};
+  const half2v r16 = {(_Float16)0.0625f, (_Float16)0.0625f};
+  const half2v b16 = {(_Float16)(-64 - bias), (_Float16)(-64 - bias)};
+  auto hi = [&](int pair, int T) __attribute__((always_inline)) {
+    if constexpr (FMT == QM_Q5_G32) return shift_by(hi_w, T - (4 * s + pair)) & ((1u << T) | (1u << (T + 16)));
+    else return shift_by(hi_w, T - 2 * (4 * s + pair)) & ((3u << T) | (3u << (T + 16)));
+  };
+  const uint32_t d8 = nd >> 8;
+  const half2v q01 = __builtin_bit_cast(half2v, ((nd & c.m0) | c.magic_s) | hi(0, 4)) - b1;
+  const half2v q23 = __builtin_elementwise_fma(__builtin_bit_cast(half2v, ((nd & c.m1) | c.magic_s) | hi(1, 8)), r16, b16);
+  const half2v q45 = __builtin_bit_cast(half2v, ((d8 & c.m0) | c.magic_s) | hi(2, 4)) - b1;
+  const half2v q67 = __builtin_elementwise_fma(__builtin_bit_cast(half2v, ((d8 & c.m1) | c.magic_s) | hi(3, 8)), r16, b16);
+  const half2v v0 = q01 * s2, v1 = q23 * s2, v2 = q45 * s2, v3 = q67 * s2;
+  return half8v{v0[0], v0[1], v1[0], v1[1], v2[0], v2[1], v3[0], v3[1]};
+}
+//  Q2 / Q3: crumb dword cw of the lane's 16 codes (pair p of substep s at
+//  bits 2(4s + p), 16 + 2(4s + p)); masked in place it gives 1024 + 4^p u
+//  (after a shift by 8 for s = 1), and one exact fma x * 4^-p - (1024 * 4^-p
+//  + bias) leaves q.  Q3 adds its bit (hb, shifted right by 8h) at bit
+//  2p + 2 of the same lanes (4^3 * 7 = 448 keeps the value in [1024, 2048)).
+template <int FMT>
+__device__ inline half8v dequant_crumb(uint32_t cw, uint32_t hb, int s, half2v s2, const DequantRegs& c) {
+  constexpr int bias = FMT == QM_Q2_G32 ? 2 : 4;
+  const uint32_t src = s ? cw >> 8 : cw;
+  half2v q[4];
+#pragma unroll
+  for (int pr = 0; pr < 4; ++pr) {
+    uint32_t x = (src & (0x00030003u << (2 * pr))) | c.magic_s;
+    if constexpr (FMT == QM_Q3_G32) {
+      const int T = 2 * pr + 2;
+      x |= shift_by(hb, T - (4 * s + pr)) & ((1u << T) | (1u << (T + 16)));
+    }
+    const _Float16 r = (_Float16)(1.0f / static_cast<float>(1 << (2 * pr)));
+    const _Float16 b = (_Float16)(-(1024.0f / static_cast<float>(1 << (2 * pr))) - bias);
+    q[pr] = __builtin_elementwise_fma(__builtin_bit_cast(half2v, x), half2v{r, r}, half2v{b, b}) * s2;
+  }
+  return half8v{q[0][0], q[0][1], q[1][0], q[1][1], q[2][0], q[2][1], q[3][0], q[3][1]};
+}
+
 // Wavefront 0 maps the workgroup's linear tile index to (expert, row tile)
 // in expert order, with ceil(count / BM) tiles per expert.  Expert -1 when
 // the index lies beyond the last tile.
@@ -215,9 +267,18 @@ __device__ inline void find_tile(const int32_t* counts, int E, int BM, int bx, i
 template <int BM, int WN, int WK, QgMode MODE, int DEPTH, int FMT>
 struct Cfg {
   static constexpr bool kQ8 = FMT == QM_Q8_G32;
-  static_assert(FMT == QM_Q4_G32 || (kQ8 && MODE == QgMode::kDense), "Q8 weights: dense GEMM only");
-  static constexpr int kChunkBytes = kQ8 ? 2048 : 1024;           // one group of a 64-row panel
-  static constexpr int kDwords = kQ8 ? 8 : 4;                     // B dwords per lane, column half and K step
+  static constexpr bool kPlanes = FMT == QM_Q2_G32 || FMT == QM_Q3_G32 || FMT == QM_Q5_G32 || FMT == QM_Q6_G32;
+  static_assert(FMT == QM_Q4_G32 || ((kQ8 || kPlanes) && MODE == QgMode::kDense),
+                "Q2/Q3/Q5/Q6/Q8 weights: dense GEMM only (no F16/BF16)");
+  static constexpr int kChunkBytes = chunk_block_bytes(FMT);      // one group of a 64-row panel
+  // B words a lane holds per group and column half: Q4 two nibble dwords,
+  // Q8 four byte dwords, Q5/Q6 two nibble dwords + one high-plane dword,
+  // Q3 one crumb + one bit dword, Q2 one crumb dword; and the global loads
+  // (planes) behind them.
+  static constexpr int kLW = FMT == QM_Q4_G32 ? 2 : kQ8 ? 4 : FMT == QM_Q2_G32 ? 1 : FMT == QM_Q3_G32 ? 2 : 3;
+  static constexpr int kPlaneLoads = FMT == QM_Q3_G32 || FMT == QM_Q5_G32 || FMT == QM_Q6_G32 ? 2 : 1;
+  static constexpr int kDwords = 2 * kLW;                         // B dwords per lane, column half and K step
+  static constexpr int kPieces16 = kChunkBytes / 1024, kPieces4 = kChunkBytes % 1024 / 256;
   static constexpr bool kDual = MODE == QgMode::kMoeGateUp;
   static constexpr int kNB = kDual ? 2 : 1;                      // weight matrices per wavefront
   static constexpr int kThreads = WN * WK * 64;
@@ -246,7 +307,7 @@ struct Cfg {
   // per weight matrix either the code chunks in 1 KiB pieces + 1 scale
   // block (LDS DMA) or 2 chunks x 2 column halves of codes and of scales
   // (registers).
-  static constexpr int kBLoads = kBLds ? kNB * (2 * kChunkBytes / 1024 + 1) : kNB * 2 * 2 * 2;
+  static constexpr int kBLoads = kBLds ? kNB * (2 * (kPieces16 + kPieces4) + 1) : kNB * 2 * 2 * (kPlaneLoads + 1);
   // Split-K partial sums of slices 1..WK-1, in halves (fp32 = 2 halves).
   static constexpr int kRedHalves = (WK - 1) * WN * kTM * 2 * kNB * 16 * 64 * 2;
   static constexpr int kLdsHalves =
@@ -257,8 +318,8 @@ struct Cfg {
 template <int BM, int WN, int WK, QgMode MODE, int DEPTH, bool NT, int FMT>
 __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   using C = Cfg<BM, WN, WK, MODE, DEPTH, FMT>;
-  constexpr bool Q8 = C::kQ8;
-  constexpr int CB = C::kChunkBytes, MB = C::kBMatBytes;
+  constexpr bool Q8 = C::kQ8, PL = C::kPlanes;
+  constexpr int CB = C::kChunkBytes, MB = C::kBMatBytes, LW = C::kLW;
   constexpr int NB = C::kNB;
   __shared__ __attribute__((aligned(16))) uint16_t lds[C::kLdsHalves];
   const int tid = threadIdx.x;
@@ -373,6 +434,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   constexpr int NS = C::kSlots;
   using BVec = std::conditional_t<Q8, u32x4, u32x2>;
   BVec rb[NS][NB][2][2];                                   // [slot][matrix][chunk][column half]
+  uint32_t rw[NS][NB][2][2][LW];                           // the same for the bit-plane formats
   uint32_t rs[NS][NB][2][2];
   char* const lds_b = reinterpret_cast<char*>(lds);
   // A tile of this slice in stage st; B region of this wavefront in stage st.
@@ -404,9 +466,13 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         for (int c = 0; c < 2; ++c) {
           const int gc = min(2 * kt + c, G - 1);
 #pragma unroll
-          for (int piece = 0; piece < CB / 1024; ++piece)
+          for (int piece = 0; piece < C::kPieces16; ++piece)
             lds_dma16<NT>(b_q[j] + static_cast<int64_t>(gc) * CB + piece * 1024 + lane * 16,
                           reg + j * MB + c * CB + piece * 1024);
+#pragma unroll
+          for (int piece = 0; piece < C::kPieces4; ++piece)          // 256-byte tails (bit-plane formats)
+            lds_dma4<NT>(b_q[j] + static_cast<int64_t>(gc) * CB + C::kPieces16 * 1024 + piece * 256 + lane * 4,
+                         reg + j * MB + c * CB + C::kPieces16 * 1024 + piece * 256);
         }
         lds_dma4<NT>(b_s[j] + static_cast<int64_t>(gs1) * kPanel + 2 * (lane & 31), reg + j * MB + 2 * CB);
       }
@@ -421,8 +487,25 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         const uint16_t* bs = b_s[j] + static_cast<int64_t>(gc) * kPanel;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const BVec* qa = reinterpret_cast<const BVec*>(bq + bq_lane + h * 512);
           const uint16_t* sa = bs + bs_lane + 32 * h;
+          if constexpr (PL) {
+            // Row 32h + l%32, lane half l/32: the planes of the bit-plane
+            // formats (plain loads; these tiles are not built with NT).
+            const int row = 32 * h + (lane & 31), lh = lane >> 5;
+            uint32_t* w = rw[sl][j][c][h];
+            if constexpr (FMT == QM_Q5_G32 || FMT == QM_Q6_G32) {
+              const u32x2 nb = *reinterpret_cast<const u32x2*>(bq + row * 16 + 8 * lh);
+              w[0] = nb.x; w[1] = nb.y;
+              w[2] = FMT == QM_Q5_G32 ? *reinterpret_cast<const uint32_t*>(bq + 1024 + row * 4)
+                                      : *reinterpret_cast<const uint32_t*>(bq + 1024 + row * 8 + 4 * lh);
+            } else {
+              w[0] = *reinterpret_cast<const uint32_t*>(bq + row * 8 + 4 * lh);
+              if constexpr (FMT == QM_Q3_G32) w[1] = *reinterpret_cast<const uint32_t*>(bq + 512 + row * 4);
+            }
+            rs[sl][j][c][h] = *sa;
+            continue;
+          }
+          const BVec* qa = reinterpret_cast<const BVec*>(bq + bq_lane + h * 512);
           if constexpr (NT) {
             rb[sl][j][c][h] = __builtin_nontemporal_load(qa);
             rs[sl][j][c][h] = __builtin_nontemporal_load(sa);
@@ -518,6 +601,37 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         const bool ok = scale_ok(t, c);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
+          if constexpr (PL) {
+            uint32_t w[LW];
+            uint32_t sv;
+            const int row = 32 * h + (lane & 31), lh = lane >> 5;
+            if constexpr (C::kBLds) {
+              const char* ch = breg + j * MB + c * CB;
+              if constexpr (FMT == QM_Q5_G32 || FMT == QM_Q6_G32) {
+                const u32x2 nb = *reinterpret_cast<const u32x2*>(ch + row * 16 + 8 * lh);
+                w[0] = nb.x; w[1] = nb.y;
+                w[2] = FMT == QM_Q5_G32 ? *reinterpret_cast<const uint32_t*>(ch + 1024 + row * 4)
+                                        : *reinterpret_cast<const uint32_t*>(ch + 1024 + row * 8 + 4 * lh);
+              } else {
+                w[0] = *reinterpret_cast<const uint32_t*>(ch + row * 8 + 4 * lh);
+                if constexpr (FMT == QM_Q3_G32) w[1] = *reinterpret_cast<const uint32_t*>(ch + 512 + row * 4);
+              }
+              sv = *reinterpret_cast<const uint16_t*>(breg + j * MB + 2 * CB + c * 128 + row * 2);
+            } else {
+#pragma unroll
+              for (int i = 0; i < LW; ++i) w[i] = rw[sl][j][c][h][i];
+              sv = rs[sl][j][c][h];
+            }
+            // Bit planes hold the lane's 16 codes at bits 8h.. and 16 + 8h..
+            if constexpr (FMT == QM_Q5_G32) w[2] >>= 8 * lh;
+            if constexpr (FMT == QM_Q3_G32) w[1] >>= 8 * lh;
+            sv = ok ? sv : 0u;
+            const _Float16 f = __builtin_bit_cast(_Float16, static_cast<uint16_t>(sv));
+            sc[j][c][h] = half2v{f, f};
+#pragma unroll
+            for (int i = 0; i < LW; ++i) bd[j][h][LW * c + i] = w[i];
+            continue;
+          }
           BVec d;
           uint32_t sv;
           if constexpr (C::kBLds) {
@@ -537,8 +651,14 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
         }
       }
     auto dequant = [&](int j, int h, int ks) __attribute__((always_inline)) {
-      if constexpr (Q8) return dequant_q8(bd[j][h][2 * ks], bd[j][h][2 * ks + 1], sc[j][ks >> 1][h], dq);
-      else return dequant_dword(bd[j][h][ks], sc[j][ks >> 1][h], dq);
+      const int c = ks >> 1, s = ks & 1;
+      if constexpr (Q8) return dequant_q8(bd[j][h][2 * ks], bd[j][h][2 * ks + 1], sc[j][c][h], dq);
+      else if constexpr (FMT == QM_Q5_G32 || FMT == QM_Q6_G32)
+        return dequant_nib_hi<FMT>(bd[j][h][LW * c + s], bd[j][h][LW * c + 2], s, sc[j][c][h], dq);
+      else if constexpr (FMT == QM_Q2_G32 || FMT == QM_Q3_G32)
+        return dequant_crumb<FMT>(bd[j][h][LW * c], FMT == QM_Q3_G32 ? bd[j][h][LW * c + LW - 1] : 0u, s,
+                                  sc[j][c][h], dq);
+      else return dequant_dword(bd[j][h][ks], sc[j][c][h], dq);
     };
     load_a(a_stage(Refill{}, t + AD), t + AD);             // A, AD steps ahead
     __builtin_amdgcn_sched_barrier(0);
