@@ -311,3 +311,60 @@ def moe_layer(x_f16, logits, top_k,
     for j in range(top_k):
         out += gates[:, j:j + 1] * y_assign[np.arange(m) * top_k + j]
     return out, ids, gates, counts, offsets, sorted_assign
+
+
+# ---------------------------------------------------------------------------
+# Attention over a KV cache                 (Sec. 3.2 KV cache; Sec. 3.4)
+# ---------------------------------------------------------------------------
+
+def attention_decode(q, k_cache, v_cache, length: int, scale: float) -> np.ndarray:
+    """One decode step of grouped-query attention, in fp64.
+
+    q: [Hq][D]; k_cache, v_cache: [Hkv][Tmax][D], rows t < length valid
+    (the cache is allocated to the maximum context length, Sec. 3.2).  Query
+    head h reads KV head h // (Hq / Hkv).  For each head:
+      s_t = scale * (q_h . k_t),  p = softmax(s) over t < length,
+      o_h = sum_t p_t v_t.
+    Returns o [Hq][D] (fp64).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k_cache, dtype=np.float64)
+    v = np.asarray(v_cache, dtype=np.float64)
+    hq, d = q.shape
+    hkv = k.shape[0]
+    if hq % hkv or k.shape != v.shape or k.shape[2] != d or not 1 <= length <= k.shape[1]:
+        raise ValueError("bad attention shapes")
+    group = hq // hkv
+    out = np.empty((hq, d))
+    for h in range(hq):
+        kk = k[h // group, :length]
+        vv = v[h // group, :length]
+        sc = scale * (kk @ q[h])
+        p = np.exp(sc - sc.max())
+        out[h] = (p / p.sum()) @ vv
+    return out
+
+
+def attention_prefill(q, k, v, scale: float) -> np.ndarray:
+    """Causal grouped-query attention over a prompt, in fp64.
+
+    q: [Hq][M][D]; k, v: [Hkv][M][D].  Row i of head h attends to rows
+    j <= i of KV head h // (Hq / Hkv) with softmax(scale * q_i . k_j).
+    Returns o [Hq][M][D] (fp64).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    hq, m, d = q.shape
+    hkv = k.shape[0]
+    if hq % hkv or k.shape != (hkv, m, d) or v.shape != k.shape:
+        raise ValueError("bad attention shapes")
+    group = hq // hkv
+    out = np.empty((hq, m, d))
+    mask = np.tril(np.ones((m, m), dtype=bool))
+    for h in range(hq):
+        sc = scale * (q[h] @ k[h // group].T)                  # [M][M]
+        sc = np.where(mask, sc, -np.inf)
+        p = np.exp(sc - sc.max(axis=1, keepdims=True))
+        out[h] = (p / p.sum(axis=1, keepdims=True)) @ v[h // group]
+    return out

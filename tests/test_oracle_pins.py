@@ -489,3 +489,65 @@ def test_moe_top1_and_identical_experts():
     one, *_ = O.moe_layer(x, np.zeros((m, 1), np.float32), 1, gq[:1], gs[:1], uq[:1], us[:1],
                           dq_[:1], ds[:1])
     assert np.allclose(outs, one, rtol=0, atol=1e-13 * np.abs(one).max())
+
+
+# ------------------------------------------------------------------ attention
+
+def test_attention_hand_example():
+    """Scores ln 3 and 0 give weights 3/4 and 1/4: o = 3/4 v0 + 1/4 v1."""
+    q = np.array([[1.0, 0.0]])
+    k = np.array([[[math.log(3.0), 5.0], [0.0, 7.0], [9.0, 9.0]]])     # row 2 is past the length
+    v = np.array([[[4.0, 0.0], [0.0, 8.0], [100.0, 100.0]]])
+    o = O.attention_decode(q, k, v, 2, 1.0)
+    assert np.allclose(o, [[3.0, 2.0]], rtol=0, atol=1e-15)
+    # causal prefill of the same two rows: row 0 sees only itself
+    op = O.attention_prefill(np.array([[[1.0, 0.0], [1.0, 0.0]]]), k[:, :2], v[:, :2], 1.0)
+    assert np.allclose(op[0, 0], v[0, 0]) and np.allclose(op[0, 1], [3.0, 2.0], atol=1e-15)
+
+
+def test_attention_closed_forms_and_gqa_mapping():
+    rng = np.random.default_rng(41)
+    hkv, tmax, d = 2, 9, 4
+    k = rng.standard_normal((hkv, tmax, d))
+    v = rng.standard_normal((hkv, tmax, d))
+    # length 1: the only value row, whatever the scores
+    q = rng.standard_normal((6, d))
+    assert np.allclose(O.attention_decode(q, k, v, 1, 0.7), v[np.arange(6) // 3, 0], atol=1e-15)
+    # zero query: uniform weights, the mean of the valid rows
+    z = np.zeros((6, d))
+    o = O.attention_decode(z, k, v, 7, 1.0)
+    assert np.allclose(o, v[np.arange(6) // 3, :7].mean(axis=1), atol=1e-14)
+    # a dominant key: e^-60 of the rest
+    kk = k.copy()
+    kk[1, 4] = 30.0 * np.ones(d)
+    qq = np.ones((6, d))
+    o = O.attention_decode(qq, kk, v, 9, 0.5)
+    assert np.allclose(o[3:], v[1, 4], atol=1e-20 + 1e-12)
+    # heads 0-2 read KV head 0 and heads 3-5 KV head 1: swapping the KV heads
+    # swaps the two halves of the output
+    o1 = O.attention_decode(q, k, v, 8, 0.3)
+    o2 = O.attention_decode(np.concatenate([q[3:], q[:3]]), k[::-1], v[::-1], 8, 0.3)
+    assert np.allclose(o1, np.concatenate([o2[3:], o2[:3]]), atol=1e-14)
+
+
+def test_attention_against_python_loops():
+    """Tiny case with math.exp and plain Python sums."""
+    rng = np.random.default_rng(42)
+    hq, hkv, t, d = 4, 2, 5, 3
+    q = rng.standard_normal((hq, d))
+    k = rng.standard_normal((hkv, t + 2, d))
+    v = rng.standard_normal((hkv, t + 2, d))
+    o = O.attention_decode(q, k, v, t, 0.9)
+    for h in range(hq):
+        g = h // 2
+        sc = [0.9 * sum(q[h][i] * k[g][j][i] for i in range(d)) for j in range(t)]
+        w = [math.exp(x) for x in sc]
+        tot = sum(w)
+        for i in range(d):
+            assert abs(o[h][i] - sum(w[j] * v[g][j][i] for j in range(t)) / tot) < 1e-13
+    qp = rng.standard_normal((hq, t, d))
+    op = O.attention_prefill(qp, k[:, :t], v[:, :t], 0.9)
+    for h in range(hq):
+        for r in range(t):
+            # row r of causal prefill = decode attention over the first r+1 rows
+            assert np.allclose(op[h, r], O.attention_decode(qp[:, r], k, v, r + 1, 0.9)[h], atol=1e-14)
