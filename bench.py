@@ -356,6 +356,42 @@ def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
         torch.cuda.empty_cache()
     out["llama3.2-3b_lm_head_by_format"] = fm
     log(f"lm_head by format: {fm}")
+
+    # Decode attention over the KV cache (one layer, one token): Qwen3-0.6B
+    # (16 query / 8 KV heads) and Llama-3.2-3B (24 / 8), head_dim 128, cycling
+    # over enough cache copies that every call streams K and V from HBM.
+    att = {}
+    for tag, hq, hkv in (("qwen3-0.6b", 16, 8), ("llama3.2-3b", 24, 8)):
+        for length in (1024, 4096, 16384, 65536):
+            d = 128
+            kv_bytes = 2 * hkv * length * d * 2
+            copies = max(1, -(-600_000_000 // kv_bytes))
+            g = torch.Generator(device="cuda").manual_seed(length)
+            q = torch.randn((hq, d), generator=g, device="cuda").half()
+            ks = [torch.randn((hkv, length, d), generator=g, device="cuda").half() for _ in range(copies)]
+            vs = [torch.randn((hkv, length, d), generator=g, device="cuda").half() for _ in range(copies)]
+            o = torch.empty((hq, d), dtype=torch.float32, device="cuda")
+            ws = torch.empty(B.qattn_decode_workspace_bytes(hq, d), dtype=torch.uint8, device="cuda")
+            reps = max(8, 2 * copies)
+
+            def run(st, ks=ks, vs=vs, q=q, o=o, ws=ws, hq=hq, hkv=hkv, length=length, reps=reps):
+                for r in range(reps):
+                    rc = lib.qattn_decode(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(ks[r % len(ks)].data_ptr()),
+                                          ctypes.c_void_p(vs[r % len(vs)].data_ptr()), hq, hkv, 128, length, length,
+                                          ctypes.c_float(1.0 / 128 ** 0.5), ctypes.c_void_p(o.data_ptr()),
+                                          ctypes.c_void_p(ws.data_ptr()), ws.numel(), st)
+                    if rc != 0:
+                        raise RuntimeError(lib.qm_last_error().decode())
+            gr = capture(torch, run)
+            t, _ = time_graph(torch, gr, 5, 1)
+            us = t / 5 / reps * 1e6
+            att[f"{tag}_len{length}"] = {"us_per_call": round(us, 3), "kv_MB": round(kv_bytes / 1e6, 2),
+                                         "GBps": round(kv_bytes / us / 1e3, 1),
+                                         "frac_hbm_peak": round(kv_bytes / us / 1e3 / HBM_PEAK_GBS, 4)}
+            del gr, ks, vs
+            torch.cuda.empty_cache()
+    out["decode_attention"] = att
+    log(f"decode attention: {att}")
     return out
 
 

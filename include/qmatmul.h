@@ -207,6 +207,28 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
  * prompts).  Deterministic. */
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream);
 
+/* Host-only: bytes of the decode-attention workspace for n_q_heads query
+ * heads of head_dim (64 or 128): per query head up to 256 slices of
+ * (head_dim + 2) floats. */
+qm_status qattn_decode_workspace_bytes(int32_t n_q_heads, int32_t head_dim, size_t* bytes);
+
+/* Decode attention over a pre-allocated KV cache (Sec. 3.2: the cache is
+ * allocated to the maximum context length, laid out for coalesced reads;
+ * grouped-query attention as in the Llama 3.2 and Qwen3 models):
+ *   o[h] = sum_t p_t v[g][t],  p = softmax_t(scale * q[h] . k[g][t]),
+ *   g = h / (n_q_heads / n_kv_heads),  t < len.
+ * q: fp16 [n_q_heads][head_dim]; k_cache, v_cache: fp16
+ * [n_kv_heads][max_len][head_dim] (rows t >= len are not read as data);
+ * o: fp32 [n_q_heads][head_dim].  head_dim 64 or 128; at most 8 query heads
+ * per KV head; 1 <= len <= max_len <= 262144; scale finite.  q, k_cache,
+ * v_cache, workspace 16-byte aligned; workspace of at least
+ * qattn_decode_workspace_bytes() bytes (caller-owned scratch, contents not
+ * preserved).  Scores and sums in fp32, split over the cache length and
+ * merged exactly as online softmax does.  Two kernel launches; deterministic. */
+qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                       int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale, float* o,
+                       void* workspace, size_t ws_bytes, void* stream);
+
 /* Host-only: workspace bytes qmoe_grouped_gemm needs for m tokens. */
 qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden,
                                int64_t inter, size_t* bytes);

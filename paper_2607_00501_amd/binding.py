@@ -28,7 +28,7 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmatmul_gemv", "qmatmul_gemv_swiglu", "qmatmul_gemv_grouped", "qmatmul_gemm",
            "qmatmul_gemm_grouped",
            "qmoe_workspace_bytes", "qmoe_route",
-           "qmoe_grouped_gemm", "qm_device_config")
+           "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode")
 
 
 class QmError(RuntimeError):
@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
             "qmoe_route": [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp],
             "qmoe_grouped_gemm": [W, W, W, vp, i64, i32, vp, vp, vp, vp, vp, vp, sz, vp],
             "qm_device_config": [ctypes.c_char_p, sz],
+            "qattn_decode_workspace_bytes": [i32, i32, ctypes.POINTER(sz)],
+            "qattn_decode": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -237,6 +239,30 @@ def qmatmul_gemm_grouped(ws, x: torch.Tensor, outs=None, stream=None):
     n, descs, yp = gemm_group_args(ws, outs)
     _check(lib().qmatmul_gemm_grouped(n, descs, _ptr(x), m, yp, _stream(stream)))
     return outs
+
+
+def qattn_decode_workspace_bytes(n_q_heads: int, head_dim: int) -> int:
+    b = ctypes.c_size_t()
+    _check(lib().qattn_decode_workspace_bytes(n_q_heads, head_dim, ctypes.byref(b)))
+    return b.value
+
+
+def qattn_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, length: int, scale: float,
+                 out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None, stream=None):
+    """q: fp16 [Hq][D]; k_cache, v_cache: fp16 [Hkv][max_len][D] -> fp32 [Hq][D]."""
+    hq, d = q.shape
+    hkv, max_len, d2 = k_cache.shape
+    assert d2 == d and v_cache.shape == k_cache.shape
+    assert q.dtype == k_cache.dtype == v_cache.dtype == torch.float16
+    assert q.is_contiguous() and k_cache.is_contiguous() and v_cache.is_contiguous()
+    if out is None:
+        out = torch.empty((hq, d), dtype=torch.float32, device=q.device)
+    nb = qattn_decode_workspace_bytes(hq, d)
+    if workspace is None:
+        workspace = torch.empty(nb, dtype=torch.uint8, device=q.device)
+    _check(lib().qattn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, length, max_len, scale,
+                              _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
 
 
 def qmoe_workspace_bytes(m: int, n_experts: int, top_k: int, hidden: int, inter: int) -> int:

@@ -8,6 +8,7 @@
 // table (CU count, architecture) built once per device.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -305,6 +306,42 @@ qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float*
   return launched(launch_gemm(w->format, static_cast<const uint8_t*>(w->qdata), w->scales, x, y, m, w->n, w->k,
                               d->cu_count, s),
                   "qmatmul_gemm");
+}
+
+qm_status qattn_decode_workspace_bytes(int32_t n_q_heads, int32_t head_dim, size_t* bytes) {
+  if (!bytes) return fail(QM_EINVAL, "qattn_decode_workspace_bytes: null output pointer");
+  if (n_q_heads < 1 || n_q_heads > 1024 || (head_dim != 64 && head_dim != 128))
+    return fail(QM_ESHAPE, "qattn_decode_workspace_bytes: n_q_heads in [1, 1024], head_dim 64 or 128");
+  *bytes = attn_decode_workspace_bytes(n_q_heads, head_dim);
+  return QM_OK;
+}
+
+qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                       int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale, float* o,
+                       void* workspace, size_t ws_bytes, void* stream) {
+  if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "qattn_decode: head_dim=%d must be 64 or 128", head_dim);
+  if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads > 1024 || n_q_heads % n_kv_heads != 0 ||
+      n_q_heads / n_kv_heads > 8)
+    return fail(QM_ESHAPE, "qattn_decode: n_q_heads=%d must be a multiple of n_kv_heads=%d, at most 8 per KV head",
+                n_q_heads, n_kv_heads);
+  if (max_len < 1 || max_len > kAttnMaxLen || len < 1 || len > max_len)
+    return fail(QM_ESHAPE, "qattn_decode: need 1 <= len <= max_len <= %lld (len=%lld, max_len=%lld)",
+                (long long)kAttnMaxLen, (long long)len, (long long)max_len);
+  if (!(scale == scale) || scale == INFINITY || scale == -INFINITY)
+    return fail(QM_EINVAL, "qattn_decode: scale must be finite");
+  if (!q || !k_cache || !v_cache || !o) return fail(QM_EINVAL, "qattn_decode: null pointer");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(o))
+    return fail(QM_EALIGN, "qattn_decode: q, k_cache, v_cache must be 16-byte aligned, o 4-byte aligned");
+  const size_t need = attn_decode_workspace_bytes(n_q_heads, head_dim);
+  if (!workspace || ws_bytes < need)
+    return fail(QM_EWORKSPACE, "qattn_decode: workspace of %zu bytes needed (got %zu)", need, ws_bytes);
+  if (!aligned16(workspace)) return fail(QM_EALIGN, "qattn_decode: workspace must be 16-byte aligned");
+  const DeviceInfo* d;
+  qm_status st;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_attn_decode(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, len, max_len, scale, o,
+                                     static_cast<float*>(workspace), d->cu_count, static_cast<hipStream_t>(stream)),
+                  "qattn_decode");
 }
 
 qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden, int64_t inter,

@@ -112,6 +112,17 @@ hipError_t launch_gemm_group(int32_t fmt, int count, const uint8_t* const* q, co
                              float* const* y, const int64_t* n, const uint16_t* x, int64_t m, int64_t k,
                              int cu_count, hipStream_t st);
 
+// Decode attention: KV rows per workgroup slice and number of slices.
+constexpr int kAttnMaxSplits = 256;
+constexpr int kAttnScoreFloats = 8192;           // LDS floats for the scores of one slice (32 KiB)
+constexpr int64_t kAttnMaxLen = 262144;          // kAttnMaxSplits x (kAttnScoreFloats / 8 heads)
+struct AttnPlan { int tc; int nsplit; };
+AttnPlan attn_decode_plan(int hkv, int group, int64_t len, int cu_count);
+size_t attn_decode_workspace_bytes(int32_t hq, int32_t d);
+hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
+                              int32_t d, int64_t len, int64_t max_len, float scale, float* o, float* ws,
+                              int cu_count, hipStream_t st);
+
 struct MoeArgs {
   const uint8_t* gq; const uint16_t* gs;   // gate [E][inter][hidden], device layout
   const uint8_t* uq; const uint16_t* us;   // up   [E][inter][hidden]

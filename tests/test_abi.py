@@ -237,3 +237,26 @@ def test_gemm_grouped_validation():
     assert call([w], xp=ctypes.c_void_p(0x30004)) == 3                 # x misaligned
     assert call([w], xp=None) == 1                                     # null x
     assert B.qm_last_error()
+
+
+def test_attention_decode_validation():
+    L = B.lib()
+    p = ctypes.c_void_p(0x50000)
+    ws = ctypes.c_void_p(0x60000)
+    need = B.qattn_decode_workspace_bytes(16, 128)
+    assert need == 16 * 256 * 130 * 4
+    call = lambda hq=16, hkv=8, d=128, n=100, mx=4096, scale=0.088, q=p, o=p, w=ws, nb=need: \
+        L.qattn_decode(q, p, p, hq, hkv, d, n, mx, scale, o, w, nb, None)
+    assert call(d=96) == 2                       # head_dim
+    assert call(hq=12, hkv=8) == 2               # not a multiple
+    assert call(hq=72, hkv=8) == 2               # more than 8 query heads per KV head
+    assert call(n=0) == 2 and call(n=5000) == 2  # len outside [1, max_len]
+    assert call(mx=300000, n=10) == 2            # max_len too large
+    assert call(scale=float("inf")) == 1
+    assert call(q=None) == 1
+    assert call(q=ctypes.c_void_p(0x50008)) == 3
+    assert call(nb=need - 1) == 6
+    assert call(w=None) == 6
+    with pytest.raises(B.QmError):
+        B.qattn_decode_workspace_bytes(16, 80)
+    assert B.qm_last_error()
