@@ -345,26 +345,29 @@ def attention_decode(q, k_cache, v_cache, length: int, scale: float) -> np.ndarr
     return out
 
 
-def attention_prefill(q, k, v, scale: float) -> np.ndarray:
-    """Causal grouped-query attention over a prompt, in fp64.
+def attention_prefill(q, k, v, scale: float, p0: int = 0) -> np.ndarray:
+    """Causal grouped-query attention over a prompt chunk, in fp64.
 
-    q: [Hq][M][D]; k, v: [Hkv][M][D].  Row i of head h attends to rows
-    j <= i of KV head h // (Hq / Hkv) with softmax(scale * q_i . k_j).
-    Returns o [Hq][M][D] (fp64).
+    q: [Hq][M][D], the queries at positions p0 .. p0 + M - 1 (a chunk of a
+    prompt processed in bounded chunks, Sec. 3.4); k, v: [Hkv][>= p0 + M][D],
+    the keys and values of positions 0 .. p0 + M - 1.  Query row i of head h
+    attends to positions j <= p0 + i of KV head h // (Hq / Hkv) with
+    softmax(scale * q_i . k_j).  Returns o [Hq][M][D] (fp64).
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
     hq, m, d = q.shape
     hkv = k.shape[0]
-    if hq % hkv or k.shape != (hkv, m, d) or v.shape != k.shape:
+    n = p0 + m
+    if hq % hkv or k.shape[0] != hkv or k.shape[1] < n or k.shape[2] != d or v.shape != k.shape:
         raise ValueError("bad attention shapes")
     group = hq // hkv
     out = np.empty((hq, m, d))
-    mask = np.tril(np.ones((m, m), dtype=bool))
+    mask = np.arange(n)[None, :] <= (p0 + np.arange(m))[:, None]     # [M][n]
     for h in range(hq):
-        sc = scale * (q[h] @ k[h // group].T)                  # [M][M]
+        sc = scale * (q[h] @ k[h // group, :n].T)                     # [M][n]
         sc = np.where(mask, sc, -np.inf)
         p = np.exp(sc - sc.max(axis=1, keepdims=True))
-        out[h] = (p / p.sum(axis=1, keepdims=True)) @ v[h // group]
+        out[h] = (p / p.sum(axis=1, keepdims=True)) @ v[h // group, :n]
     return out

@@ -551,3 +551,18 @@ def test_attention_against_python_loops():
         for r in range(t):
             # row r of causal prefill = decode attention over the first r+1 rows
             assert np.allclose(op[h, r], O.attention_decode(qp[:, r], k, v, r + 1, 0.9)[h], atol=1e-14)
+
+
+def test_attention_prefill_chunk_offset():
+    """A chunk at offset p0 equals the last rows of the whole prompt, and
+    its row i equals decode attention over the first p0 + i + 1 rows."""
+    rng = np.random.default_rng(43)
+    hq, hkv, n, d = 4, 2, 11, 3
+    q = rng.standard_normal((hq, n, d))
+    k = rng.standard_normal((hkv, n, d))
+    v = rng.standard_normal((hkv, n, d))
+    full = O.attention_prefill(q, k, v, 0.8)
+    part = O.attention_prefill(q[:, 6:], k, v, 0.8, p0=6)
+    assert np.allclose(part, full[:, 6:], atol=1e-14)
+    for i in range(5):
+        assert np.allclose(part[:, i], O.attention_decode(q[:, 6 + i], k, v, 7 + i, 0.8), atol=1e-14)
