@@ -459,6 +459,34 @@ def extra_prefill(torch, B, inputs, workloads, steps, warmup, lib):
         del wds
         torch.cuda.empty_cache()
 
+    # Causal prefill attention of one layer (qattn_prefill): Llama-3.2-1B
+    # (32 query / 8 KV heads, head_dim 64) and Qwen3-0.6B (16 / 8, head_dim
+    # 128); FLOPs 2 * 2 * D * Hq * M(M+1)/2 (the causal half of Q K^T and P V).
+    att = {}
+    for tag, hq, hkv, d in (("llama3.2-1b", 32, 8, 64), ("qwen3-0.6b", 16, 8, 128)):
+        for m in model["m_sweep"]:
+            g = torch.Generator(device="cuda").manual_seed(m)
+            q = torch.randn((hq, m, d), generator=g, device="cuda").half()
+            kc = torch.randn((hkv, m, d), generator=g, device="cuda").half()
+            vc = torch.randn((hkv, m, d), generator=g, device="cuda").half()
+            o = torch.empty((hq, m, d), dtype=torch.float32, device="cuda")
+
+            def run_a(st, q=q, kc=kc, vc=vc, o=o, hq=hq, hkv=hkv, d=d, m=m):
+                for _ in range(10):
+                    rc = lib.qattn_prefill(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(kc.data_ptr()),
+                                           ctypes.c_void_p(vc.data_ptr()), hq, hkv, d, m, 0, m,
+                                           ctypes.c_float(d ** -0.5), ctypes.c_void_p(o.data_ptr()), st)
+                    if rc:
+                        raise RuntimeError(lib.qm_last_error().decode())
+            gr = capture(torch, run_a)
+            t, _ = time_graph(torch, gr, reps, warmup)
+            us = t / reps / 10 * 1e6
+            flops = 2.0 * 2.0 * d * hq * m * (m + 1) / 2
+            att[f"{tag}_m{m}"] = {"us": round(us, 2), "TFLOPs": round(flops / us / 1e6, 1),
+                                  "frac_mfma_peak": round(flops / us / 1e6 / MFMA_F16_PEAK_TFLOPS, 4)}
+            del gr
+    out["prefill_attention"] = att
+    log(f"prefill attention: {att}")
     return out
 
 

@@ -207,6 +207,23 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
  * prompts).  Deterministic. */
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream);
 
+/* Causal prefill attention over a prompt chunk (Sec. 3.4: FlashAttention,
+ * tiles with online softmax and running statistics, O(n) memory; chunked
+ * prefill with a bounded chunk):
+ *   o[h][i] = sum_{j <= p0 + i} p_j v[g][j],  p = softmax_j(scale * q[h][i] . k[g][j]),
+ *   g = h / (n_q_heads / n_kv_heads),  i < m.
+ * q: fp16 [n_q_heads][m][head_dim], the chunk's queries at positions p0 ..
+ * p0 + m - 1; k_cache, v_cache: fp16 [n_kv_heads][max_len][head_dim] holding
+ * positions 0 .. p0 + m - 1 (the chunk's own keys and values written
+ * already); o: fp32 [n_q_heads][m][head_dim].  head_dim 64 or 128;
+ * 1 <= m <= 65536; p0 + m <= max_len <= 262144; scale finite and > 0.
+ * fp16 MFMA for q.k and p.v (p rounded toward zero to fp16; the sums use
+ * the fp32 p), fp32 statistics and accumulation.  One launch, no
+ * workspace, deterministic. */
+qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                        int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len, float scale,
+                        float* o, void* stream);
+
 /* Host-only: bytes of the decode-attention workspace for n_q_heads query
  * heads of head_dim (64 or 128): per query head up to 256 slices of
  * (head_dim + 2) floats. */

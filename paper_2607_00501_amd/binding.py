@@ -28,7 +28,8 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmatmul_gemv", "qmatmul_gemv_swiglu", "qmatmul_gemv_grouped", "qmatmul_gemm",
            "qmatmul_gemm_grouped",
            "qmoe_workspace_bytes", "qmoe_route",
-           "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode")
+           "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
+           "qattn_prefill")
 
 
 class QmError(RuntimeError):
@@ -73,6 +74,7 @@ def lib() -> ctypes.CDLL:
             "qm_device_config": [ctypes.c_char_p, sz],
             "qattn_decode_workspace_bytes": [i32, i32, ctypes.POINTER(sz)],
             "qattn_decode": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
+            "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -262,6 +264,22 @@ def qattn_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, 
         workspace = torch.empty(nb, dtype=torch.uint8, device=q.device)
     _check(lib().qattn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, length, max_len, scale,
                               _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
+
+
+def qattn_prefill(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, p0: int, scale: float,
+                  out: Optional[torch.Tensor] = None, stream=None):
+    """q: fp16 [Hq][m][D] at positions p0..p0+m-1; k_cache, v_cache: fp16
+    [Hkv][max_len][D] -> fp32 [Hq][m][D] (causal)."""
+    hq, m, d = q.shape
+    hkv, max_len, d2 = k_cache.shape
+    assert d2 == d and v_cache.shape == k_cache.shape
+    assert q.dtype == k_cache.dtype == v_cache.dtype == torch.float16
+    assert q.is_contiguous() and k_cache.is_contiguous() and v_cache.is_contiguous()
+    if out is None:
+        out = torch.empty((hq, m, d), dtype=torch.float32, device=q.device)
+    _check(lib().qattn_prefill(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, m, p0, max_len, scale,
+                               _ptr(out), _stream(stream)))
     return out
 
 

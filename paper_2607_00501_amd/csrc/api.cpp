@@ -344,6 +344,28 @@ qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_
                   "qattn_decode");
 }
 
+qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                        int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len, float scale,
+                        float* o, void* stream) {
+  if (head_dim != 64 && head_dim != 128)
+    return fail(QM_ESHAPE, "qattn_prefill: head_dim=%d must be 64 or 128", head_dim);
+  if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads > 1024 || n_q_heads % n_kv_heads != 0)
+    return fail(QM_ESHAPE, "qattn_prefill: n_q_heads=%d must be a multiple of n_kv_heads=%d", n_q_heads, n_kv_heads);
+  if (m < 1 || m > 65536 || p0 < 0 || max_len > kAttnMaxLen || p0 + m > max_len)
+    return fail(QM_ESHAPE, "qattn_prefill: need 1 <= m <= 65536, p0 >= 0, p0 + m <= max_len <= %lld",
+                (long long)kAttnMaxLen);
+  if (!(scale > 0.0f) || scale == INFINITY) return fail(QM_EINVAL, "qattn_prefill: scale must be finite and > 0");
+  if (!q || !k_cache || !v_cache || !o) return fail(QM_EINVAL, "qattn_prefill: null pointer");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(o))
+    return fail(QM_EALIGN, "qattn_prefill: q, k_cache, v_cache must be 16-byte aligned, o 4-byte aligned");
+  const DeviceInfo* d;
+  qm_status st;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_attn_prefill(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, m, p0, max_len, scale, o,
+                                      static_cast<hipStream_t>(stream)),
+                  "qattn_prefill");
+}
+
 qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden, int64_t inter,
                                size_t* bytes) {
   if (!bytes) return fail(QM_EINVAL, "qmoe_workspace_bytes: null output pointer");

@@ -270,7 +270,227 @@ hipError_t launch_decode_d(int group, const uint16_t* q, const uint16_t* k, cons
   }
 }
 
+// ------------------------------------------------------------------ prefill
+
+typedef _Float16 half4v __attribute__((ext_vector_type(4)));
+
+// Causal FlashAttention for a prompt chunk (Sec. 3.4: tiled attention with
+// online softmax and running statistics, O(n) memory).  Workgroup = one
+// query head x 128 query rows, four wavefronts of 32 rows.  Per block of 64
+// keys (32 for head_dim 128, to fit 256 VGPRs; K row-major and V transposed
+// in LDS, the next blocks loading into registers meanwhile), each wavefront
+// computes S^T = K Q^T as independent 32-key tiles with v_mfma_f32_32x32x16_f16 (lane l then holds 32
+// keys of query l%32, so the row statistics need one cross-lane step), masks
+// future positions on the diagonal blocks, updates the running maximum and
+// sum in the base-2 domain, rescales its O^T accumulators when the maximum
+// moved and adds V^T P^T.  The k slots of that second product are relabelled
+// to the keys the lane already holds, so P never leaves its lane.
+template <int D>
+__global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* __restrict__ q,
+                                                           const uint16_t* __restrict__ k,
+                                                           const uint16_t* __restrict__ v, int group,
+                                                           int64_t m, int64_t p0, int64_t max_len, float scale_log2,
+                                                           float* __restrict__ o) {
+  constexpr int KB = D == 64 ? 64 : 32;      // keys per block (head_dim 128: 32, to fit 256 VGPRs)
+  constexpr int NT = KB / 32;                // 32-key S tiles per block
+  constexpr int KS = D / 16;                 // k steps of S over the head dimension
+  constexpr int DB = D / 32;                 // 32-wide blocks of the head dimension
+  constexpr int KPAD = D + 8;                // LDS row of K (halves)
+  constexpr int VPAD = KB + 8;               // LDS row of V^T (halves)
+  constexpr int CHUNKS = KB * D / 8;         // 16-byte pieces of a block
+  constexpr int PER_T = CHUNKS / 256;        // pieces per thread
+  __shared__ __attribute__((aligned(16))) _Float16 ks[KB * KPAD];
+  __shared__ __attribute__((aligned(16))) _Float16 vt[D * VPAD];
+
+  const int ntiles = static_cast<int>((m + 127) / 128);
+  const int tile = ntiles - 1 - static_cast<int>(blockIdx.x);     // longest tiles first
+  const int h = blockIdx.y, g = h / group;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, lh = lane >> 5, col = lane & 31;
+  const int64_t q0 = static_cast<int64_t>(tile) * 128;
+  const int64_t qrow = q0 + 32 * wave + col;                      // this lane's query row
+  const int64_t qpos = p0 + min<int64_t>(qrow, m - 1);            // its position
+  const int64_t nkeys = p0 + min<int64_t>(q0 + 128, m);            // keys this workgroup needs
+  const int64_t wave_first = p0 + q0 + 32 * wave;                  // first query position of the wavefront
+  const int64_t wave_last = p0 + min<int64_t>(q0 + 32 * wave + 31, m - 1);
+
+  // Q fragments (B operand of S^T = K Q^T): query col, dims 16 s + 8 lh + 0..7.
+  half8v qf[KS];
+  const uint16_t* qr = q + (static_cast<int64_t>(h) * m + min<int64_t>(qrow, m - 1)) * D;
+#pragma unroll
+  for (int s = 0; s < KS; ++s) qf[s] = *reinterpret_cast<const half8v*>(qr + 16 * s + 8 * lh);
+
+  const uint16_t* kh = k + static_cast<int64_t>(g) * max_len * D;
+  const uint16_t* vh = v + static_cast<int64_t>(g) * max_len * D;
+  // K pieces row-major (consecutive threads along a row); V pieces
+  // key-major (consecutive threads on consecutive keys of one 8-dimension
+  // chunk), so that the transposed LDS writes of a wavefront hit
+  // consecutive halves of a V^T row.
+  // Blocks past the end load clamped (valid) rows and are never used, so
+  // the loads carry no branch and the register sets stay in registers.
+  struct Blk { uint4 k[PER_T], v[PER_T]; };
+  auto load_block = [&](int64_t kb0) __attribute__((always_inline)) {
+    Blk b;
+#pragma unroll
+    for (int c = 0; c < PER_T; ++c) {
+      const int piece = threadIdx.x + 256 * c;
+      const int row = piece / (D / 8), off = (piece % (D / 8)) * 8;
+      b.k[c] = *reinterpret_cast<const uint4*>(kh + min<int64_t>(kb0 + row, nkeys - 1) * D + off);
+      const int vkey = piece % KB, voff = (piece / KB) * 8;
+      b.v[c] = *reinterpret_cast<const uint4*>(vh + min<int64_t>(kb0 + vkey, nkeys - 1) * D + voff);
+    }
+    return b;
+  };
+  auto store_block = [&](const Blk& b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < PER_T; ++c) {
+      const int piece = threadIdx.x + 256 * c;
+      const int row = piece / (D / 8), off = (piece % (D / 8)) * 8;
+      *reinterpret_cast<uint4*>(&ks[row * KPAD + off]) = b.k[c];
+      const int vkey = piece % KB, voff = (piece / KB) * 8;
+      const uint32_t w[4] = {b.v[c].x, b.v[c].y, b.v[c].z, b.v[c].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const half2v hv = __builtin_bit_cast(half2v, w[i]);
+        vt[(voff + 2 * i) * VPAD + vkey] = hv[0];
+        vt[(voff + 2 * i + 1) * VPAD + vkey] = hv[1];
+      }
+    }
+  };
+
+  float16v acc[DB];
+#pragma unroll
+  for (int b = 0; b < DB; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  auto compute = [&](int64_t kb0) __attribute__((always_inline)) {
+    if (kb0 <= wave_last) {
+      // S^T for keys kb0 + 32 t + (lane's rows), query col: two independent tiles.
+      float16v st[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[t][r] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const half8v a = *reinterpret_cast<const half8v*>(&ks[(32 * t + col) * KPAD + 16 * s + 8 * lh]);
+          st[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, qf[s], st[t], 0, 0, 0);
+        }
+      // Causal mask only where the block reaches past the wavefront's first
+      // query, on 32-bit offsets inside the block; the maximum is taken on
+      // the raw scores (scale > 0) and scaled once.
+      float bm = -INFINITY;
+      if (kb0 + KB - 1 > wave_first) {
+        const int lim = static_cast<int>(min<int64_t>(qpos - kb0, KB)) - 4 * lh;   // >= 0: key offset allowed
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float x = 32 * t + 8 * (r >> 2) + (r & 3) <= lim ? st[t][r] : -INFINITY;
+            st[t][r] = x;
+            bm = fmaxf(bm, x);
+          }
+      } else {
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) bm = fmaxf(bm, st[t][r]);
+      }
+      bm = fmaxf(bm, __shfl_xor(bm, 32)) * scale_log2;
+      const float m_new = fmaxf(m_run, bm);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // v_exp_f32 (0 for -inf)
+      float rs = 0.0f;
+      half8v pf[2 * NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          const float p0v = __builtin_amdgcn_exp2f(fmaf(st[t][r], scale_log2, -m_new));
+          const float p1v = __builtin_amdgcn_exp2f(fmaf(st[t][r + 1], scale_log2, -m_new));
+          rs += p0v + p1v;
+          const half2v pp = __builtin_bit_cast(half2v, __builtin_amdgcn_cvt_pkrtz(p0v, p1v));
+          pf[2 * t + (r >> 3)][r & 7] = pp[0];
+          pf[2 * t + (r >> 3)][(r & 7) + 1] = pp[1];
+        }
+      rs += __shfl_xor(rs, 32);
+      l_run = fmaf(l_run, alpha, rs);
+      m_run = m_new;
+      if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {         // the running maximum moved
+#pragma unroll
+        for (int b = 0; b < DB; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[b][r] *= alpha;
+      }
+      // O^T += V^T P^T; k slot (lh, i) of step kk is key 16 kk + 8 (i / 4) + 4 lh + i % 4.
+#pragma unroll
+      for (int kk = 0; kk < KB / 16; ++kk)
+#pragma unroll
+        for (int b = 0; b < DB; ++b) {
+          const _Float16* vrow = &vt[(32 * b + col) * VPAD + 16 * kk + 4 * lh];
+          const half4v lo = *reinterpret_cast<const half4v*>(vrow);
+          const half4v hi = *reinterpret_cast<const half4v*>(vrow + 8);
+          const half8v a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, pf[kk], acc[b], 0, 0, 0);
+        }
+    }
+  };
+
+  // Register sets of block loads: the loads of block b + 2 (head_dim 64) or
+  // b + 1 (head_dim 128) are issued right after block b has gone to LDS, so
+  // they land during the math.
+  if constexpr (D == 64) {
+    Blk b0 = load_block(0), b1 = load_block(KB);
+    for (int64_t kb0 = 0; kb0 < nkeys; kb0 += 2 * KB) {
+      store_block(b0);
+      __syncthreads();
+      b0 = load_block(kb0 + 2 * KB);
+      compute(kb0);
+      __syncthreads();
+      if (kb0 + KB < nkeys) {
+        store_block(b1);
+        __syncthreads();
+        b1 = load_block(kb0 + 3 * KB);
+        compute(kb0 + KB);
+        __syncthreads();
+      }
+    }
+  } else {
+    // head_dim 128: one register set (two would not fit in 256 VGPRs).
+    Blk b0 = load_block(0);
+    for (int64_t kb0 = 0; kb0 < nkeys; kb0 += KB) {
+      store_block(b0);
+      __syncthreads();
+      b0 = load_block(kb0 + KB);
+      compute(kb0);
+      __syncthreads();
+    }
+  }
+  if (qrow < m) {
+    const float inv = 1.0f / l_run;
+    float* orow = o + (static_cast<int64_t>(h) * m + qrow) * D;
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) orow[32 * b + 8 * (r >> 2) + 4 * lh + (r & 3)] = acc[b][r] * inv;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
+                               int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
+                               hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>((m + 127) / 128), static_cast<unsigned>(hq));
+  const float sl2 = scale * 1.4426950408889634f;
+  if (d == 64)
+    hipLaunchKernelGGL((attn_prefill_kernel<64>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o);
+  else
+    hipLaunchKernelGGL((attn_prefill_kernel<128>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o);
+  return hipGetLastError();
+}
 
 // Slices: enough workgroups for about two per CU over the KV heads, at
 // least 32 rows each (a multiple of 32), at most kAttnMaxSplits slices, and

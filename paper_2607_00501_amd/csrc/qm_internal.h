@@ -123,6 +123,10 @@ hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16
                               int32_t d, int64_t len, int64_t max_len, float scale, float* o, float* ws,
                               int cu_count, hipStream_t st);
 
+hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
+                               int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
+                               hipStream_t st);
+
 struct MoeArgs {
   const uint8_t* gq; const uint16_t* gs;   // gate [E][inter][hidden], device layout
   const uint8_t* uq; const uint16_t* us;   // up   [E][inter][hidden]

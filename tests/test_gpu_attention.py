@@ -79,3 +79,61 @@ def test_attn_decode_deterministic_and_workspace_reuse():
     assert torch.equal(a, c)
     ref = O.attention_decode(q.cpu().numpy(), k.cpu().numpy()[:, :17], v.cpu().numpy()[:, :17], 17, np.float32(0.1))
     assert rel_err(b.cpu().numpy(), ref) <= ATTN_TOL
+
+
+PREFILL_TOL = 1e-2     # fp16 MFMA operands (p rounded to fp16)
+
+
+def _prefill_case(hq, hkv, d, m, p0, max_len, seed, scale=None):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((hq, m, d)).astype(np.float16)
+    k = rng.standard_normal((hkv, max_len, d)).astype(np.float16)
+    v = rng.standard_normal((hkv, max_len, d)).astype(np.float16)
+    if p0 + m < max_len:
+        k[:, p0 + m:] = np.float16(np.nan)          # positions past the chunk are not data
+        v[:, p0 + m:] = np.float16(np.nan)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    o = B.qattn_prefill(torch.from_numpy(q).cuda(), torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda(),
+                        p0, scale).cpu().numpy()
+    return o, q, k, v, scale
+
+
+# Llama-3.2-1B (32 / 8 heads, head_dim 64) and Qwen3 / Llama-3.2-3B style
+# (head_dim 128) shapes; ragged chunks, chunks at an offset, one row.
+@pytest.mark.parametrize("hq,hkv,d,m,p0,max_len", [
+    (4, 2, 64, 1, 0, 8), (4, 2, 128, 33, 0, 40), (8, 8, 64, 200, 0, 256), (6, 2, 128, 300, 0, 300),
+    (4, 1, 64, 129, 77, 400), (32, 8, 64, 512, 0, 512), (16, 8, 128, 250, 1000, 1300),
+    (24, 8, 128, 128, 0, 128)])
+def test_attn_prefill_parity(hq, hkv, d, m, p0, max_len):
+    o, q, k, v, scale = _prefill_case(hq, hkv, d, m, p0, max_len, seed=m + p0 + d)
+    ref = O.attention_prefill(q, k[:, :p0 + m], v[:, :p0 + m], np.float32(scale), p0=p0)
+    assert np.all(np.isfinite(o))
+    err = rel_err(o, ref)
+    assert err <= PREFILL_TOL
+    assert err <= 2e-3, err
+
+
+def test_attn_prefill_full_prompt_sampled_rows():
+    """Llama-3.2-1B attention shape at M = 2048: sampled query rows of
+    sampled heads against the oracle, both ends of the causal range."""
+    hq, hkv, d, m = 32, 8, 64, 2048
+    o, q, k, v, scale = _prefill_case(hq, hkv, d, m, 0, m, seed=99)
+    rows = np.array([0, 1, 127, 128, 1000, 2046, 2047])
+    for h in (0, 9, 31):
+        for i in rows:
+            ref = O.attention_decode(q[h:h + 1, i], k[h // 4:h // 4 + 1], v[h // 4:h // 4 + 1], int(i) + 1,
+                                     np.float32(scale))
+            assert rel_err(o[h, i][None], ref) <= PREFILL_TOL
+
+
+def test_attn_prefill_last_row_matches_decode():
+    """The last query of a chunk attends to the whole prefix: it equals the
+    decode kernel's result for that query (within the MFMA tolerance)."""
+    hq, hkv, d, m, p0 = 16, 8, 128, 96, 160
+    o, q, k, v, scale = _prefill_case(hq, hkv, d, m, p0, p0 + m, seed=5)
+    dec = B.qattn_decode(torch.from_numpy(np.ascontiguousarray(q[:, -1])).cuda(), torch.from_numpy(k).cuda(),
+                         torch.from_numpy(v).cuda(), p0 + m, scale).cpu().numpy()
+    assert rel_err(o[:, -1], dec.astype(np.float64)) <= PREFILL_TOL
+    o2 = B.qattn_prefill(torch.from_numpy(q).cuda(), torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda(),
+                         p0, scale).cpu().numpy()
+    assert np.array_equal(o, o2)                     # deterministic
