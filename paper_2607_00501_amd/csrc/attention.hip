@@ -296,7 +296,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* __
   constexpr int KS = D / 16;                 // k steps of S over the head dimension
   constexpr int DB = D / 32;                 // 32-wide blocks of the head dimension
   constexpr int KPAD = D + 8;                // LDS row of K (halves)
-  constexpr int VPAD = KB + 8;               // LDS row of V^T (halves)
+  constexpr int VPAD = KB + 4;               // LDS row of V^T (halves): an even number of dwords, 2 mod 4
   constexpr int CHUNKS = KB * D / 8;         // 16-byte pieces of a block
   constexpr int PER_T = CHUNKS / 256;        // pieces per thread
   __shared__ __attribute__((aligned(16))) _Float16 ks[KB * KPAD];
@@ -321,10 +321,11 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* __
 
   const uint16_t* kh = k + static_cast<int64_t>(g) * max_len * D;
   const uint16_t* vh = v + static_cast<int64_t>(g) * max_len * D;
-  // K pieces row-major (consecutive threads along a row); V pieces
-  // key-major (consecutive threads on consecutive keys of one 8-dimension
-  // chunk), so that the transposed LDS writes of a wavefront hit
-  // consecutive halves of a V^T row.
+  // K pieces row-major (consecutive threads along a row); V in pairs of
+  // keys (consecutive threads on consecutive key pairs of one 8-dimension
+  // chunk), so that each transposed LDS write of a wavefront is a dword of
+  // two keys and the writes of a wavefront fill consecutive dwords of V^T
+  // rows.
   // Blocks past the end load clamped (valid) rows and are never used, so
   // the loads carry no branch and the register sets stay in registers.
   struct Blk { uint4 k[PER_T], v[PER_T]; };
@@ -335,8 +336,13 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* __
       const int piece = threadIdx.x + 256 * c;
       const int row = piece / (D / 8), off = (piece % (D / 8)) * 8;
       b.k[c] = *reinterpret_cast<const uint4*>(kh + min<int64_t>(kb0 + row, nkeys - 1) * D + off);
-      const int vkey = piece % KB, voff = (piece / KB) * 8;
-      b.v[c] = *reinterpret_cast<const uint4*>(vh + min<int64_t>(kb0 + vkey, nkeys - 1) * D + voff);
+    }
+#pragma unroll
+    for (int c = 0; c < PER_T / 2; ++c) {
+      const int pp = threadIdx.x + 256 * c;                      // a pair of keys, 8 dimensions
+      const int kp = pp % (KB / 2), voff = (pp / (KB / 2)) * 8;
+      b.v[2 * c] = *reinterpret_cast<const uint4*>(vh + min<int64_t>(kb0 + 2 * kp, nkeys - 1) * D + voff);
+      b.v[2 * c + 1] = *reinterpret_cast<const uint4*>(vh + min<int64_t>(kb0 + 2 * kp + 1, nkeys - 1) * D + voff);
     }
     return b;
   };
@@ -346,13 +352,19 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* __
       const int piece = threadIdx.x + 256 * c;
       const int row = piece / (D / 8), off = (piece % (D / 8)) * 8;
       *reinterpret_cast<uint4*>(&ks[row * KPAD + off]) = b.k[c];
-      const int vkey = piece % KB, voff = (piece / KB) * 8;
-      const uint32_t w[4] = {b.v[c].x, b.v[c].y, b.v[c].z, b.v[c].w};
+    }
+    // V^T: dimension d of keys 2 kp, 2 kp + 1 as one dword.
+#pragma unroll
+    for (int c = 0; c < PER_T / 2; ++c) {
+      const int pp = threadIdx.x + 256 * c;
+      const int kp = pp % (KB / 2), voff = (pp / (KB / 2)) * 8;
+      const uint32_t w0[4] = {b.v[2 * c].x, b.v[2 * c].y, b.v[2 * c].z, b.v[2 * c].w};
+      const uint32_t w1[4] = {b.v[2 * c + 1].x, b.v[2 * c + 1].y, b.v[2 * c + 1].z, b.v[2 * c + 1].w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const half2v hv = __builtin_bit_cast(half2v, w[i]);
-        vt[(voff + 2 * i) * VPAD + vkey] = hv[0];
-        vt[(voff + 2 * i + 1) * VPAD + vkey] = hv[1];
+        *reinterpret_cast<uint32_t*>(&vt[(voff + 2 * i) * VPAD + 2 * kp]) = __builtin_amdgcn_perm(w1[i], w0[i], 0x05040100u);
+        *reinterpret_cast<uint32_t*>(&vt[(voff + 2 * i + 1) * VPAD + 2 * kp]) =
+            __builtin_amdgcn_perm(w1[i], w0[i], 0x07060302u);
       }
     }
   };
