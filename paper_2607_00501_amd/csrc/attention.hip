@@ -286,7 +286,7 @@ typedef _Float16 half4v __attribute__((ext_vector_type(4)));
 // moved and adds V^T P^T.  The k slots of that second product are relabelled
 // to the keys the lane already holds, so P never leaves its lane.
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_prefill_kernel(const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v, int group,
                                                            int64_t m, int64_t p0, int64_t max_len, float scale_log2,
