@@ -4,11 +4,14 @@
  * The library implements the matrix products of LLM decode and prefill with
  * quantised weights: a fused dequantise+GEMV for batch-1 decode, a
  * dequantise-into-LDS + fp16 MFMA GEMM for prefill, and the top-k-routed
- * grouped expert GEMM of a mixture-of-experts layer (BaseRT, Sec. 3.3
+ * grouped expert GEMM of a mixture-of-experts layer; plus grouped-query
+ * attention over a pre-allocated KV cache for decode and causal
+ * FlashAttention for prefill chunks (BaseRT, Sec. 3.3
  * "Kernel Fusion and Specialisation": one GEMV (M = 1) and one GEMM (M > 1)
  * kernel per quantisation format, dequantisation inside the inner loop and
  * never materialised; Sec. 3.4 "Prefill": tiled GEMM for prompts, bounded
- * chunks; Sec. 4.1: Q4 / Q8 formats and the MoE models).
+ * chunks, FlashAttention; Sec. 3.2: the KV cache; Sec. 4.1: the weight
+ * formats and the MoE models).
  *
  * Conventions shared by every entry point
  *  - Pointers named d_* / device buffers are HIP device pointers; the caller
