@@ -371,3 +371,61 @@ def attention_prefill(q, k, v, scale: float, p0: int = 0) -> np.ndarray:
         p = np.exp(sc - sc.max(axis=1, keepdims=True))
         out[h] = (p / p.sum(axis=1, keepdims=True)) @ v[h // group, :n]
     return out
+
+
+# ---------------------------------------------------------------------------
+# One decode step of a dense decoder             (Sec. 3.2, Sec. 3.3)
+# ---------------------------------------------------------------------------
+
+def rmsnorm(x, w, eps: float) -> np.ndarray:
+    """y = x / sqrt(mean(x^2) + eps) * w, fp64."""
+    x = np.asarray(x, dtype=np.float64)
+    return x / np.sqrt(np.mean(x * x) + eps) * np.asarray(w, dtype=np.float64)
+
+
+def rope(x, pos: int, theta: float) -> np.ndarray:
+    """Rotary position embedding of each head row of x [H][D] at position
+    pos, pairing dimension i with i + D/2 (the Llama / Qwen convention):
+    angle_i = pos * theta^(-2i/D), (a, b) -> (a cos - b sin, b cos + a sin)."""
+    x = np.asarray(x, dtype=np.float64)
+    d = x.shape[-1]
+    i = np.arange(d // 2)
+    ang = pos * theta ** (-2.0 * i / d)
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[..., :d // 2], x[..., d // 2:]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def f16(x) -> np.ndarray:
+    """Round to fp16 (the precision of every activation a kernel hands to
+    the next one) and return the value as fp64."""
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float16).astype(np.float64)
+
+
+def decode_step(model: dict, token: int, pos: int, k_cache: np.ndarray, v_cache: np.ndarray) -> np.ndarray:
+    """Logits of one decode step of a dense grouped-query-attention decoder
+    with SwiGLU feed-forward blocks (the Llama 3.2 / Qwen3 layer), in fp64.
+
+    model: emb [V][H] and the norm weights as fp16 values; per layer the
+    dequantised projections wq, wk, wv, wo, wg, wu, wd ([N][K], fp64) and
+    attn_norm, ffn_norm; norm, lm_head; hq, hkv, d, eps, theta.  The
+    activations handed between kernels are rounded to fp16 where the kernels'
+    interfaces are fp16: the normed inputs of every projection, q after
+    RoPE, the new K / V rows (written into k_cache / v_cache [L][Hkv][T][D]
+    at row pos), the attention output and the SwiGLU output.  The residual
+    stream stays fp32 on the GPU and fp64 here.
+    """
+    hq, hkv, d, eps, theta = model["hq"], model["hkv"], model["d"], model["eps"], model["theta"]
+    x = np.asarray(model["emb"][token], dtype=np.float64)
+    for li, ly in enumerate(model["layers"]):
+        h = f16(rmsnorm(x, ly["attn_norm"], eps))
+        q = rope((ly["wq"] @ h).reshape(hq, d), pos, theta)
+        k = rope((ly["wk"] @ h).reshape(hkv, d), pos, theta)
+        v = (ly["wv"] @ h).reshape(hkv, d)
+        k_cache[li, :, pos] = f16(k)
+        v_cache[li, :, pos] = f16(v)
+        a = attention_decode(f16(q), k_cache[li], v_cache[li], pos + 1, 1.0 / np.sqrt(d))
+        x = x + ly["wo"] @ f16(a.reshape(-1))
+        h = f16(rmsnorm(x, ly["ffn_norm"], eps))
+        x = x + ly["wd"] @ f16(silu(ly["wg"] @ h) * (ly["wu"] @ h))
+    return model["lm_head"] @ f16(rmsnorm(x, model["norm"], eps))

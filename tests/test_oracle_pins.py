@@ -566,3 +566,75 @@ def test_attention_prefill_chunk_offset():
     assert np.allclose(part, full[:, 6:], atol=1e-14)
     for i in range(5):
         assert np.allclose(part[:, i], O.attention_decode(q[:, 6 + i], k, v, 7 + i, 0.8), atol=1e-14)
+
+
+# ---------------------------------------------------------------- decode step
+
+def test_rmsnorm_closed_forms():
+    w = np.array([1.0, 2.0, -1.0, 0.5])
+    assert np.allclose(O.rmsnorm(np.full(4, 3.0), w, 0.0), w)                 # constant vector -> w
+    assert np.allclose(O.rmsnorm(np.array([3.0, 4.0, 0.0, 0.0]), np.ones(4), 0.0),
+                       np.array([3.0, 4.0, 0.0, 0.0]) / 2.5)                    # rms = 5 / 2
+    assert np.allclose(O.rmsnorm(np.zeros(4), w, 1e-6), 0.0)
+
+
+def test_rope_position_zero_rotation_and_relative_angle():
+    rng = np.random.default_rng(44)
+    q = rng.standard_normal((3, 8))
+    k = rng.standard_normal((3, 8))
+    assert np.allclose(O.rope(q, 0, 10000.0), q)                                 # identity at 0
+    assert np.allclose(np.linalg.norm(O.rope(q, 17, 1e6), axis=1), np.linalg.norm(q, axis=1))
+    # scores depend on the relative position only
+    a = np.sum(O.rope(q, 5, 500.0) * O.rope(k, 2, 500.0), axis=1)
+    b = np.sum(O.rope(q, 13, 500.0) * O.rope(k, 10, 500.0), axis=1)
+    assert np.allclose(a, b)
+    # dimension 0 pairs with D/2, rotating by pos radians (theta^0 = 1)
+    e = np.zeros((1, 8)); e[0, 0] = 1.0
+    r = O.rope(e, 1, 10000.0)
+    assert np.allclose(r[0, [0, 4]], [math.cos(1.0), math.sin(1.0)]) and np.allclose(np.delete(r[0], [0, 4]), 0.0)
+
+
+def _tiny_model(rng, layers=2, h=64, hq=4, hkv=2, d=16, inter=96, vocab=50):
+    mk = lambda *sh: rng.standard_normal(sh) * 0.2
+    ly = [dict(wq=mk(hq * d, h), wk=mk(hkv * d, h), wv=mk(hkv * d, h), wo=mk(h, hq * d), wg=mk(inter, h),
+               wu=mk(inter, h), wd=mk(h, inter), attn_norm=1 + mk(h), ffn_norm=1 + mk(h)) for _ in range(layers)]
+    return dict(emb=mk(vocab, h), layers=ly, norm=1 + mk(h), lm_head=mk(vocab, h), hq=hq, hkv=hkv, d=d,
+                eps=1e-6, theta=10000.0)
+
+
+def test_decode_step_zero_layers_and_first_position():
+    """With every projection zero the residual stream is the embedding, so
+    the logits are lm_head . fp16(rmsnorm(emb[token])); at position 0 the
+    attention output is the (fp16) value row itself."""
+    rng = np.random.default_rng(45)
+    m = _tiny_model(rng)
+    z = dict(m)
+    z["layers"] = [dict(l, wo=np.zeros_like(l["wo"]), wd=np.zeros_like(l["wd"])) for l in m["layers"]]
+    kc = np.zeros((2, 2, 8, 16)); vc = np.zeros((2, 2, 8, 16))
+    lg = O.decode_step(z, 7, 0, kc, vc)
+    want = m["lm_head"] @ O.f16(O.rmsnorm(m["emb"][7], m["norm"], 1e-6))
+    assert np.allclose(lg, want, atol=1e-12)
+    # the cache rows written at position 0 are fp16(W x) (k with RoPE at 0 = identity)
+    h = O.f16(O.rmsnorm(m["emb"][7], m["layers"][0]["attn_norm"], 1e-6))
+    assert np.allclose(vc[0, :, 0], O.f16((m["layers"][0]["wv"] @ h).reshape(2, 16)))
+    assert np.allclose(kc[0, :, 0], O.f16((m["layers"][0]["wk"] @ h).reshape(2, 16)))
+
+
+def test_decode_step_matches_prefill_attention_of_the_sequence():
+    """Running decode steps over a sequence fills the cache so that the last
+    step's attention equals causal prefill attention over the same keys."""
+    rng = np.random.default_rng(46)
+    m = _tiny_model(rng, layers=1)
+    kc = np.zeros((1, 2, 8, 16)); vc = np.zeros((1, 2, 8, 16))
+    toks = [3, 9, 1, 4, 4]
+    for p, t in enumerate(toks):
+        O.decode_step(m, t, p, kc, vc)
+    assert np.all(kc[0, :, 5:] == 0) and np.all(kc[0, :, :5] != 0)
+    # the last step's query at position 4 against keys 0..4 equals row 4 of causal prefill
+    ly = m["layers"][0]
+    x = np.asarray(m["emb"][toks[-1]], dtype=np.float64)
+    q = O.f16(O.rope((ly["wq"] @ O.f16(O.rmsnorm(x, ly["attn_norm"], 1e-6))).reshape(4, 16), 4, 10000.0))
+    dec = O.attention_decode(q, kc[0], vc[0], 5, 0.25)
+    qp = np.zeros((4, 5, 16)); qp[:, 4] = q
+    pre = O.attention_prefill(qp, kc[0, :, :5], vc[0, :, :5], 0.25)
+    assert np.allclose(dec, pre[:, 4], atol=1e-14)
