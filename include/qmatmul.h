@@ -249,6 +249,49 @@ qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_
                        int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale, float* o,
                        void* workspace, size_t ws_bytes, void* stream);
 
+/* ---- Glue of one decode step (Sec. 3.2: the normalisation, RoPE,
+ * embedding and sampling kernels between the matmuls and attention of a
+ * dense Llama 3.2 / Qwen3-style decoder).  Activations handed to a matmul or
+ * to attention are fp16; the residual stream is fp32.  None of these entry
+ * points synchronises with the host: with the token id on the device, one
+ * step's argmax feeds the next step's embedding. */
+
+/* x[i] = table[*token][i] (fp16 -> fp32), i < hidden.  table: fp16
+ * [vocab][hidden]; token: one int32 on the device; an id outside
+ * [0, vocab) writes NaNs into x (a host check would need a synchronisation). */
+qm_status qdec_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,
+                     void* stream);
+
+/* RMSNorm of `rows` rows of x (fp32 [rows][hidden], device), with an
+ * optional residual add first:  if residual != NULL, x += residual (written
+ * back into x);  out = fp16_RNE(x / sqrt(mean(x^2) + eps) * w).  w: fp16
+ * [hidden]; out: fp16 [rows][hidden].  Sum of squares in fp32.  rows may be
+ * 0; hidden >= 1; eps finite and >= 0. */
+qm_status qdec_rmsnorm(float* x, const float* residual, const uint16_t* w, int64_t rows, int64_t hidden, float eps,
+                       uint16_t* out, void* stream);
+
+/* Rotary embedding of the new token's queries and keys, fused with the
+ * KV-cache append (rotate-half pairing: element i with i + head_dim/2,
+ * angle pos * theta^(-2i/head_dim), taken in fp64):
+ *   q_out[h] = fp16(rope(q[h]))          h < n_q_heads,
+ *   k_cache[g][pos] = fp16(rope(k[g])),  v_cache[g][pos] = fp16(v[g]).
+ * q: fp32 [n_q_heads][head_dim]; k, v: fp32 [n_kv_heads][head_dim] (the
+ * projection outputs); q_out: fp16 [n_q_heads][head_dim]; caches: fp16
+ * [n_kv_heads][max_len][head_dim], only row pos of each head written.
+ * head_dim 64 or 128; 0 <= pos < max_len <= 262144; theta > 1. */
+qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32_t n_q_heads, int32_t n_kv_heads,
+                           int32_t head_dim, int64_t pos, int64_t max_len, float theta, uint16_t* q_out,
+                           uint16_t* k_cache, uint16_t* v_cache, void* stream);
+
+/* out[i] = fp16_RNE(x[i]), i < n (values beyond the fp16 range become inf).
+ * x: fp32, out: fp16, device; n >= 0. */
+qm_status qdec_cast_f16(const float* x, int64_t n, uint16_t* out, void* stream);
+
+/* Greedy sampling: *token = the index of the largest of logits[0 .. n),
+ * the lowest index among equal maxima; NaNs are never chosen (0 if all
+ * are NaN).  logits: fp32, device; token: one int32, device; n >= 1. */
+qm_status qdec_argmax(const float* logits, int64_t n, int32_t* token, void* stream);
+
 /* Host-only: workspace bytes qmoe_grouped_gemm needs for m tokens. */
 qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden,
                                int64_t inter, size_t* bytes);

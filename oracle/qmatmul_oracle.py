@@ -402,6 +402,16 @@ def f16(x) -> np.ndarray:
     return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float16).astype(np.float64)
 
 
+def greedy_token(logits) -> int:
+    """Greedy sampling: the first index of the largest non-NaN logit (0 when
+    every logit is NaN)."""
+    z = np.asarray(logits, dtype=np.float64)
+    ok = ~np.isnan(z)
+    if not ok.any():
+        return 0
+    return int(np.flatnonzero(ok & (z == z[ok].max()))[0])
+
+
 def decode_step(model: dict, token: int, pos: int, k_cache: np.ndarray, v_cache: np.ndarray) -> np.ndarray:
     """Logits of one decode step of a dense grouped-query-attention decoder
     with SwiGLU feed-forward blocks (the Llama 3.2 / Qwen3 layer), in fp64.

@@ -29,7 +29,8 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmatmul_gemm_grouped",
            "qmoe_workspace_bytes", "qmoe_route",
            "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
-           "qattn_prefill")
+           "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
+           "qdec_argmax")
 
 
 class QmError(RuntimeError):
@@ -75,6 +76,11 @@ def lib() -> ctypes.CDLL:
             "qattn_decode_workspace_bytes": [i32, i32, ctypes.POINTER(sz)],
             "qattn_decode": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp],
+            "qdec_embed": [vp, i64, i64, vp, vp, vp],
+            "qdec_rmsnorm": [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp],
+            "qdec_rope_append": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, vp, vp],
+            "qdec_cast_f16": [vp, i64, vp, vp],
+            "qdec_argmax": [vp, i64, vp, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -280,6 +286,66 @@ def qattn_prefill(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
         out = torch.empty((hq, m, d), dtype=torch.float32, device=q.device)
     _check(lib().qattn_prefill(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, m, p0, max_len, scale,
                                _ptr(out), _stream(stream)))
+    return out
+
+
+def qdec_embed(table: torch.Tensor, token: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """table: fp16 [vocab][hidden]; token: int32 [1] on the device -> fp32 [hidden]."""
+    vocab, hidden = table.shape
+    assert table.dtype == torch.float16 and table.is_contiguous() and token.dtype == torch.int32
+    if out is None:
+        out = torch.empty(hidden, dtype=torch.float32, device=table.device)
+    _check(lib().qdec_embed(_ptr(table), vocab, hidden, _ptr(token), _ptr(out), _stream(stream)))
+    return out
+
+
+def qdec_rmsnorm(x: torch.Tensor, w: torch.Tensor, eps: float, residual: Optional[torch.Tensor] = None,
+                 out: Optional[torch.Tensor] = None, stream=None):
+    """x: fp32 [rows][hidden] or [hidden] (updated in place when residual is
+    given: x += residual); w: fp16 [hidden] -> fp16 like x."""
+    hidden = x.shape[-1]
+    rows = x.numel() // hidden if hidden else 0
+    assert x.dtype == torch.float32 and x.is_contiguous() and w.dtype == torch.float16 and w.numel() == hidden
+    if residual is not None:
+        assert residual.dtype == torch.float32 and residual.shape == x.shape and residual.is_contiguous()
+    if out is None:
+        out = torch.empty(x.shape, dtype=torch.float16, device=x.device)
+    _check(lib().qdec_rmsnorm(_ptr(x), _ptr(residual), _ptr(w), rows, hidden, eps, _ptr(out), _stream(stream)))
+    return out
+
+
+def qdec_rope_append(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: int, theta: float,
+                     k_cache: torch.Tensor, v_cache: torch.Tensor, q_out: Optional[torch.Tensor] = None,
+                     stream=None):
+    """q: fp32 [Hq*D]; k, v: fp32 [Hkv*D]; caches fp16 [Hkv][max_len][D]
+    (row pos written) -> fp16 [Hq][D] rotated queries."""
+    hkv, max_len, d = k_cache.shape
+    hq = q.numel() // d
+    assert q.dtype == k.dtype == v.dtype == torch.float32 and k.numel() == v.numel() == hkv * d
+    assert k_cache.dtype == v_cache.dtype == torch.float16 and v_cache.shape == k_cache.shape
+    assert k_cache.is_contiguous() and v_cache.is_contiguous()
+    if q_out is None:
+        q_out = torch.empty((hq, d), dtype=torch.float16, device=q.device)
+    _check(lib().qdec_rope_append(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, pos, max_len, theta, _ptr(q_out),
+                                  _ptr(k_cache), _ptr(v_cache), _stream(stream)))
+    return q_out
+
+
+def qdec_cast_f16(x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """fp32 -> fp16 (round to nearest even), any shape."""
+    assert x.dtype == torch.float32 and x.is_contiguous()
+    if out is None:
+        out = torch.empty(x.shape, dtype=torch.float16, device=x.device)
+    _check(lib().qdec_cast_f16(_ptr(x), x.numel(), _ptr(out), _stream(stream)))
+    return out
+
+
+def qdec_argmax(logits: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """fp32 [n] -> int32 [1] on the device (lowest index among equal maxima)."""
+    assert logits.dtype == torch.float32 and logits.is_contiguous()
+    if out is None:
+        out = torch.empty(1, dtype=torch.int32, device=logits.device)
+    _check(lib().qdec_argmax(_ptr(logits), logits.numel(), _ptr(out), _stream(stream)))
     return out
 
 

@@ -24,7 +24,7 @@ COMMON = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I" + os.path.join(os.path.dirname(HERE), "include"),
 ]
-SOURCES = ["api.cpp", "format.hip", "gemv.hip", "gemm.hip", "moe.hip", "attention.hip"]
+SOURCES = ["api.cpp", "format.hip", "gemv.hip", "gemm.hip", "moe.hip", "attention.hip", "decode.hip"]
 
 
 def _compile(src: str) -> str:

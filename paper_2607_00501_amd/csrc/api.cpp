@@ -56,6 +56,7 @@ qm_status device_info(const DeviceInfo** out) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+bool aligned2(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 1u) == 0; }
 
 qm_status check_weight(const qm_qweight* w, const char* name) {
   if (!w) return fail(QM_EINVAL, "%s: null weight descriptor", name);
@@ -364,6 +365,60 @@ qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16
   return launched(launch_attn_prefill(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, m, p0, max_len, scale, o,
                                       static_cast<hipStream_t>(stream)),
                   "qattn_prefill");
+}
+
+qm_status qdec_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,
+                     void* stream) {
+  if (vocab < 1 || vocab > INT32_MAX || hidden < 1 || hidden > (int64_t{1} << 20))
+    return fail(QM_ESHAPE, "qdec_embed: need 1 <= vocab <= 2^31-1 and 1 <= hidden <= 2^20");
+  if (!table || !token || !x) return fail(QM_EINVAL, "qdec_embed: null pointer");
+  if (!aligned2(table) || !aligned4(token) || !aligned4(x))
+    return fail(QM_EALIGN, "qdec_embed: table 2-byte, token and x 4-byte aligned");
+  return launched(launch_embed(table, vocab, hidden, token, x, static_cast<hipStream_t>(stream)), "qdec_embed");
+}
+
+qm_status qdec_rmsnorm(float* x, const float* residual, const uint16_t* w, int64_t rows, int64_t hidden, float eps,
+                       uint16_t* out, void* stream) {
+  if (rows < 0 || rows > 65536 || hidden < 1 || hidden > (int64_t{1} << 20))
+    return fail(QM_ESHAPE, "qdec_rmsnorm: need 0 <= rows <= 65536 and 1 <= hidden <= 2^20");
+  if (!(eps >= 0.0f) || eps == INFINITY) return fail(QM_EINVAL, "qdec_rmsnorm: eps must be finite and >= 0");
+  if (rows > 0 && (!x || !w || !out)) return fail(QM_EINVAL, "qdec_rmsnorm: null pointer");
+  if (!aligned4(x) || (residual && !aligned4(residual)) || !aligned2(w) || !aligned2(out))
+    return fail(QM_EALIGN, "qdec_rmsnorm: x and residual 4-byte, w and out 2-byte aligned");
+  return launched(launch_rmsnorm(x, residual, w, rows, hidden, eps, out, static_cast<hipStream_t>(stream)),
+                  "qdec_rmsnorm");
+}
+
+qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32_t n_q_heads, int32_t n_kv_heads,
+                           int32_t head_dim, int64_t pos, int64_t max_len, float theta, uint16_t* q_out,
+                           uint16_t* k_cache, uint16_t* v_cache, void* stream) {
+  if (head_dim != 64 && head_dim != 128)
+    return fail(QM_ESHAPE, "qdec_rope_append: head_dim=%d must be 64 or 128", head_dim);
+  if (n_q_heads < 1 || n_q_heads > 1024 || n_kv_heads < 1 || n_kv_heads > 1024)
+    return fail(QM_ESHAPE, "qdec_rope_append: head counts must be in [1, 1024]");
+  if (max_len < 1 || max_len > kAttnMaxLen || pos < 0 || pos >= max_len)
+    return fail(QM_ESHAPE, "qdec_rope_append: need 0 <= pos < max_len <= %lld", (long long)kAttnMaxLen);
+  if (!(theta > 1.0f) || theta == INFINITY) return fail(QM_EINVAL, "qdec_rope_append: theta must be finite and > 1");
+  if (!q || !k || !v || !q_out || !k_cache || !v_cache) return fail(QM_EINVAL, "qdec_rope_append: null pointer");
+  if (!aligned4(q) || !aligned4(k) || !aligned4(v) || !aligned2(q_out) || !aligned2(k_cache) || !aligned2(v_cache))
+    return fail(QM_EALIGN, "qdec_rope_append: q, k, v 4-byte, q_out and caches 2-byte aligned");
+  return launched(launch_rope_append(q, k, v, n_q_heads, n_kv_heads, head_dim, pos, max_len, theta, q_out, k_cache,
+                                     v_cache, static_cast<hipStream_t>(stream)),
+                  "qdec_rope_append");
+}
+
+qm_status qdec_cast_f16(const float* x, int64_t n, uint16_t* out, void* stream) {
+  if (n < 0) return fail(QM_ESHAPE, "qdec_cast_f16: n=%lld must be >= 0", (long long)n);
+  if (n > 0 && (!x || !out)) return fail(QM_EINVAL, "qdec_cast_f16: null pointer");
+  if (!aligned4(x) || !aligned2(out)) return fail(QM_EALIGN, "qdec_cast_f16: x 4-byte, out 2-byte aligned");
+  return launched(launch_cast_f16(x, n, out, static_cast<hipStream_t>(stream)), "qdec_cast_f16");
+}
+
+qm_status qdec_argmax(const float* logits, int64_t n, int32_t* token, void* stream) {
+  if (n < 1 || n > INT32_MAX - 1) return fail(QM_ESHAPE, "qdec_argmax: need 1 <= n < 2^31-1");
+  if (!logits || !token) return fail(QM_EINVAL, "qdec_argmax: null pointer");
+  if (!aligned4(logits) || !aligned4(token)) return fail(QM_EALIGN, "qdec_argmax: logits and token 4-byte aligned");
+  return launched(launch_argmax(logits, n, token, static_cast<hipStream_t>(stream)), "qdec_argmax");
 }
 
 qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden, int64_t inter,

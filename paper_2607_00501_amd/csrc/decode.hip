@@ -1,0 +1,183 @@
+// The small kernels that join the matmuls and attention of one decode step
+// into a whole token (BaseRT Sec. 3.2: normalisation, RoPE, embedding and
+// sampling kernels beside the matmul and attention ones): embedding gather,
+// RMSNorm with the residual add folded in, rotary embedding fused with the
+// KV-cache append, fp32 -> fp16 conversion of a matmul input, and greedy
+// sampling.  Each moves a few KiB per token; they are latency-bound, so each
+// is one launch sized to the data, with no host synchronisation anywhere, so
+// the token id stays on the device from the argmax to the next embedding.
+#include <cmath>
+
+#include "qm_internal.h"
+
+namespace qm {
+namespace {
+
+__device__ __forceinline__ float h2f(uint16_t b) {
+  _Float16 h;
+  __builtin_memcpy(&h, &b, 2);
+  return static_cast<float>(h);
+}
+__device__ __forceinline__ uint16_t f2h(float f) {
+  const _Float16 h = static_cast<_Float16>(f);   // round to nearest even
+  uint16_t b;
+  __builtin_memcpy(&b, &h, 2);
+  return b;
+}
+
+// Sum over the 256 threads of a workgroup (4 wavefronts).
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  v = red[0] + red[1] + red[2] + red[3];
+  __syncthreads();
+  return v;
+}
+
+__global__ __launch_bounds__(256) void embed_kernel(const uint16_t* __restrict__ table, int64_t vocab,
+                                                    int64_t hidden, const int32_t* __restrict__ token,
+                                                    float* __restrict__ x) {
+  const int32_t t = *token;
+  const bool ok = t >= 0 && t < vocab;
+  const uint16_t* row = table + (ok ? t : 0) * hidden;
+  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < hidden; i += gridDim.x * 256)
+    x[i] = ok ? h2f(row[i]) : __builtin_nanf("");
+}
+
+// One workgroup per row: x += residual (written back), out = fp16(x / rms * w).
+__global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ res,
+                                                      const uint16_t* __restrict__ w, int64_t hidden, float eps,
+                                                      uint16_t* __restrict__ out) {
+  __shared__ float red[4];
+  float* xr = x + blockIdx.x * hidden;
+  const float* rr = res ? res + blockIdx.x * hidden : nullptr;
+  float ss = 0.0f;
+  for (int64_t i = threadIdx.x; i < hidden; i += 256) {
+    float v = xr[i];
+    if (rr) {
+      v += rr[i];
+      xr[i] = v;
+    }
+    ss = fmaf(v, v, ss);
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / static_cast<float>(hidden) + eps);
+  uint16_t* o = out + blockIdx.x * hidden;
+  for (int64_t i = threadIdx.x; i < hidden; i += 256) o[i] = f2h(xr[i] * inv * h2f(w[i]));
+}
+
+// One workgroup of D/2 threads per head: heads [0, hq) are queries (rotated
+// into q_out), [hq, hq + hkv) keys (rotated into the key cache at row pos),
+// the rest values (copied into the value cache at row pos).  Thread i
+// rotates the pair (i, i + D/2) by pos * theta^(-2i/D); the angle and its
+// sine and cosine are taken in fp64 so that they stay exact to fp32 at
+// positions in the hundreds of thousands.
+__global__ void rope_append_kernel(const float* __restrict__ q, const float* __restrict__ k,
+                                   const float* __restrict__ v, int hq, int hkv, int d, int64_t pos,
+                                   int64_t max_len, double log2_theta, uint16_t* __restrict__ q_out,
+                                   uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+  const int h = blockIdx.x, i = threadIdx.x, half = d / 2;
+  if (h >= hq + hkv) {
+    const int kh = h - hq - hkv;
+    uint16_t* dst = vc + (static_cast<int64_t>(kh) * max_len + pos) * d;
+    dst[i] = f2h(v[kh * d + i]);
+    dst[i + half] = f2h(v[kh * d + i + half]);
+    return;
+  }
+  const double ang = static_cast<double>(pos) * exp2(-2.0 * i / d * log2_theta);
+  const float c = static_cast<float>(cos(ang)), s = static_cast<float>(sin(ang));
+  const float* src = h < hq ? q + h * d : k + (h - hq) * d;
+  uint16_t* dst = h < hq ? q_out + h * d : kc + (static_cast<int64_t>(h - hq) * max_len + pos) * d;
+  const float a = src[i], b = src[i + half];
+  dst[i] = f2h(a * c - b * s);
+  dst[i + half] = f2h(b * c + a * s);
+}
+
+__global__ __launch_bounds__(256) void cast_f16_kernel(const float* __restrict__ x, int64_t n,
+                                                       uint16_t* __restrict__ y) {
+  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) y[i] = f2h(x[i]);
+}
+
+// Greedy sampling: index of the largest logit, the lowest index among equal
+// ones; NaNs are never chosen; 0 if every logit is NaN.
+constexpr int kArgmaxThreads = 1024;
+__global__ __launch_bounds__(kArgmaxThreads) void argmax_kernel(const float* __restrict__ x, int64_t n,
+                                                                int32_t* __restrict__ token) {
+  __shared__ float bv[kArgmaxThreads / 64];
+  __shared__ int32_t bi[kArgmaxThreads / 64];
+  float best = -INFINITY;
+  int32_t idx = INT32_MAX;
+  for (int64_t i = threadIdx.x; i < n; i += kArgmaxThreads) {
+    const float v = x[i];
+    if (v > best || (v == best && idx == INT32_MAX)) {
+      best = v;
+      idx = static_cast<int32_t>(i);
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(best, o, 64);
+    const int32_t oi = __shfl_xor(idx, o, 64);
+    if (ov > best || (ov == best && oi < idx)) {
+      best = ov;
+      idx = oi;
+    }
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    bv[w] = best;
+    bi[w] = idx;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int j = 1; j < kArgmaxThreads / 64; ++j)
+      if (bv[j] > best || (bv[j] == best && bi[j] < idx)) {
+        best = bv[j];
+        idx = bi[j];
+      }
+    token[0] = idx == INT32_MAX ? 0 : idx;
+  }
+}
+
+unsigned spread_blocks(int64_t n) {
+  const int64_t b = (n + 255) / 256;
+  return static_cast<unsigned>(b < 1024 ? (b < 1 ? 1 : b) : 1024);
+}
+
+}  // namespace
+
+hipError_t launch_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,
+                        hipStream_t st) {
+  hipLaunchKernelGGL(embed_kernel, dim3(spread_blocks(hidden)), dim3(256), 0, st, table, vocab, hidden, token, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(float* x, const float* res, const uint16_t* w, int64_t rows, int64_t hidden, float eps,
+                          uint16_t* out, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(static_cast<unsigned>(rows)), dim3(256), 0, st, x, res, w, hidden, eps,
+                     out);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_append(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
+                              int64_t pos, int64_t max_len, float theta, uint16_t* q_out, uint16_t* kc,
+                              uint16_t* vc, hipStream_t st) {
+  hipLaunchKernelGGL(rope_append_kernel, dim3(static_cast<unsigned>(hq + 2 * hkv)), dim3(d / 2), 0, st, q, k, v,
+                     hq, hkv, d, pos, max_len, std::log2(static_cast<double>(theta)), q_out, kc, vc);
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(cast_f16_kernel, dim3(spread_blocks(n)), dim3(256), 0, st, x, n, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax(const float* x, int64_t n, int32_t* token, hipStream_t st) {
+  hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(kArgmaxThreads), 0, st, x, n, token);
+  return hipGetLastError();
+}
+
+}  // namespace qm

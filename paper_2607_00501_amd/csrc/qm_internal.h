@@ -127,6 +127,17 @@ hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint1
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
                                hipStream_t st);
 
+// Decode-step glue kernels.
+hipError_t launch_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,
+                        hipStream_t st);
+hipError_t launch_rmsnorm(float* x, const float* res, const uint16_t* w, int64_t rows, int64_t hidden, float eps,
+                          uint16_t* out, hipStream_t st);
+hipError_t launch_rope_append(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
+                              int64_t pos, int64_t max_len, float theta, uint16_t* q_out, uint16_t* kc,
+                              uint16_t* vc, hipStream_t st);
+hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t st);
+hipError_t launch_argmax(const float* x, int64_t n, int32_t* token, hipStream_t st);
+
 struct MoeArgs {
   const uint8_t* gq; const uint16_t* gs;   // gate [E][inter][hidden], device layout
   const uint8_t* uq; const uint16_t* us;   // up   [E][inter][hidden]

@@ -1,0 +1,100 @@
+"""Host sequencing of one decode step of a dense grouped-query-attention
+decoder (the Llama 3.2 / Qwen3 layer) over the library's entry points
+(BaseRT Sec. 3.2: a token is embedding, per layer norm -> q/k/v projections
+-> RoPE and cache append -> attention -> output projection -> residual and
+norm -> SwiGLU feed-forward, then the final norm, the LM head and sampling).
+
+Every arithmetic step runs in the library's kernels; this module owns the
+device buffers and issues the calls in order on one stream, with no host
+synchronisation, so a step (or several) can be captured in a HIP graph and
+the sampled token stays on the device for the next step's embedding.
+"""
+
+import math
+from dataclasses import dataclass
+from typing import List
+
+import torch
+
+from . import binding as B
+
+
+@dataclass
+class DecoderConfig:
+    hidden: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    inter: int
+    vocab: int
+    layers: int
+    eps: float = 1e-6
+    theta: float = 1e6
+
+
+@dataclass
+class LayerWeights:
+    wq: B.QWeight
+    wk: B.QWeight
+    wv: B.QWeight
+    wo: B.QWeight
+    wg: B.QWeight
+    wu: B.QWeight
+    wd: B.QWeight
+    attn_norm: torch.Tensor   # fp16 [hidden]
+    ffn_norm: torch.Tensor    # fp16 [hidden]
+
+
+class DenseDecoder:
+    """Buffers and call order of one decode step.  Weights: device-layout
+    quantised projections, fp16 embedding table and norm weights."""
+
+    def __init__(self, cfg: DecoderConfig, emb: torch.Tensor, layers: List[LayerWeights], norm: torch.Tensor,
+                 lm_head: B.QWeight, max_len: int):
+        self.cfg, self.emb, self.layers, self.norm, self.lm_head = cfg, emb, layers, norm, lm_head
+        self.max_len = max_len
+        dev = emb.device
+        f32 = dict(dtype=torch.float32, device=dev)
+        f16 = dict(dtype=torch.float16, device=dev)
+        c = cfg
+        qd, kvd = c.n_q_heads * c.head_dim, c.n_kv_heads * c.head_dim
+        self.x = torch.zeros(c.hidden, **f32)             # residual stream
+        self.h = torch.zeros(c.hidden, **f16)             # normed input of a projection
+        self.q, self.k, self.v = torch.zeros(qd, **f32), torch.zeros(kvd, **f32), torch.zeros(kvd, **f32)
+        self.q16 = torch.zeros((c.n_q_heads, c.head_dim), **f16)
+        self.attn = torch.zeros((c.n_q_heads, c.head_dim), **f32)
+        self.attn16 = torch.zeros(qd, **f16)
+        self.y_attn = torch.zeros(c.hidden, **f32)
+        self.g = torch.zeros(c.inter, **f32)
+        self.g16 = torch.zeros(c.inter, **f16)
+        self.y_ffn = torch.zeros(c.hidden, **f32)
+        self.logits = torch.zeros(c.vocab, **f32)
+        self.token = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.k_cache = torch.zeros((c.layers, c.n_kv_heads, max_len, c.head_dim), **f16)
+        self.v_cache = torch.zeros((c.layers, c.n_kv_heads, max_len, c.head_dim), **f16)
+        self.ws = torch.empty(B.qattn_decode_workspace_bytes(c.n_q_heads, c.head_dim), dtype=torch.uint8,
+                              device=dev)
+        self.scale = 1.0 / math.sqrt(c.head_dim)
+
+    def step(self, pos: int, stream=None) -> None:
+        """Consumes self.token (the token at position pos), writes row pos of
+        every layer's caches, self.logits, and the greedy next token into
+        self.token."""
+        c, s = self.cfg, stream
+        B.qdec_embed(self.emb, self.token, out=self.x, stream=s)
+        for li, ly in enumerate(self.layers):
+            B.qdec_rmsnorm(self.x, ly.attn_norm, c.eps, residual=self.y_ffn if li else None, out=self.h, stream=s)
+            B.qmatmul_gemv_grouped([ly.wq, ly.wk, ly.wv], [self.h] * 3, [self.q, self.k, self.v], stream=s)
+            B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
+                               q_out=self.q16, stream=s)
+            B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn,
+                           workspace=self.ws, stream=s)
+            B.qdec_cast_f16(self.attn, out=self.attn16, stream=s)
+            B.qmatmul_gemv(ly.wo, self.attn16, out=self.y_attn, stream=s)
+            B.qdec_rmsnorm(self.x, ly.ffn_norm, c.eps, residual=self.y_attn, out=self.h, stream=s)
+            B.qmatmul_gemv_swiglu(ly.wg, ly.wu, self.h, out=self.g, stream=s)
+            B.qdec_cast_f16(self.g, out=self.g16, stream=s)
+            B.qmatmul_gemv(ly.wd, self.g16, out=self.y_ffn, stream=s)
+        B.qdec_rmsnorm(self.x, self.norm, c.eps, residual=self.y_ffn, out=self.h, stream=s)
+        B.qmatmul_gemv(self.lm_head, self.h, out=self.logits, stream=s)
+        B.qdec_argmax(self.logits, out=self.token, stream=s)

@@ -16,7 +16,7 @@ WEIGHT_SIGMA = 0.02
 
 # tensor ids inside a seed (q, k, v, o, gate, up, down, lm_head, x, logits)
 TENSOR_ID = {"q": 0, "k": 1, "v": 2, "o": 3, "gate": 4, "up": 5, "down": 6, "lm_head": 7, "x": 8,
-             "logits": 9}
+             "logits": 9, "emb": 10, "attn_norm": 11, "ffn_norm": 12, "norm": 13, "cache": 14}
 
 
 def seed_for(config: int, layer: int, tensor: str, call: int = 0) -> int:
@@ -35,6 +35,12 @@ def activations_np(seed: int, shape) -> np.ndarray:
     """fp16 activations ~ N(0, 1) (drawn in fp32, rounded to fp16)."""
     rng = np.random.default_rng(seed)
     return rng.standard_normal(shape, dtype=np.float32).astype(np.float16)
+
+
+def norm_weights_np(seed: int, shape) -> np.ndarray:
+    """fp16 norm gains ~ 1 + N(0, 0.1^2) (drawn in fp32, rounded to fp16)."""
+    rng = np.random.default_rng(seed)
+    return (1.0 + 0.1 * rng.standard_normal(shape, dtype=np.float32)).astype(np.float16)
 
 
 def logits_np(seed: int, shape) -> np.ndarray:

@@ -276,3 +276,29 @@ def test_attention_prefill_validation():
     assert call(o=None) == 1
     assert call(q=ctypes.c_void_p(0x50004)) == 3
     assert B.qm_last_error()
+
+
+def test_decode_glue_validation():
+    """Every call stops at argument validation (none reaches a launch)."""
+    L = B.lib()
+    p = ctypes.c_void_p(0x50000)
+    odd = ctypes.c_void_p(0x50001)
+    emb = lambda vocab=1000, hidden=256, t=p, tab=p, x=p: L.qdec_embed(tab, vocab, hidden, t, x, None)
+    assert emb(vocab=0) == 2 and emb(hidden=0) == 2 and emb(vocab=1 << 31) == 2
+    assert emb(t=None) == 1 and emb(tab=odd) == 3 and emb(x=ctypes.c_void_p(0x50002)) == 3
+    norm = lambda rows=1, hidden=256, eps=1e-6, x=p, r=None, w=p, o=p: L.qdec_rmsnorm(x, r, w, rows, hidden, eps, o, None)
+    assert norm(rows=-1) == 2 and norm(hidden=0) == 2 and norm(rows=70000) == 2
+    assert norm(eps=-1.0) == 1 and norm(eps=float("nan")) == 1 and norm(eps=float("inf")) == 1
+    assert norm(w=None) == 1 and norm(o=None) == 1
+    assert norm(w=odd) == 3 and norm(r=ctypes.c_void_p(0x50002)) == 3
+    rope = lambda hq=4, hkv=2, d=64, pos=0, mx=128, theta=1e4, q=p, kc=p: \
+        L.qdec_rope_append(q, p, p, hq, hkv, d, pos, mx, theta, p, kc, p, None)
+    assert rope(d=96) == 2 and rope(hq=0) == 2 and rope(hkv=2000) == 2
+    assert rope(pos=128) == 2 and rope(pos=-1) == 2 and rope(mx=300000, pos=5) == 2
+    assert rope(theta=1.0) == 1 and rope(theta=float("nan")) == 1
+    assert rope(q=None) == 1 and rope(kc=odd) == 3
+    assert L.qdec_cast_f16(p, -1, p, None) == 2 and L.qdec_cast_f16(None, 4, p, None) == 1
+    assert L.qdec_cast_f16(ctypes.c_void_p(0x50002), 4, p, None) == 3
+    assert L.qdec_argmax(p, 0, p, None) == 2 and L.qdec_argmax(None, 4, p, None) == 1
+    assert L.qdec_argmax(p, 4, odd, None) == 3
+    assert B.qm_last_error()

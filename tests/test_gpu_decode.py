@@ -1,0 +1,252 @@
+"""GPU parity of the decode-step glue kernels (embedding, RMSNorm with the
+residual add, RoPE with the cache append, fp16 cast, greedy argmax) and of
+whole decode steps of small dense decoders against the oracle's fp64
+decode step."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import qmatmul_oracle as O
+from paper_2607_00501_amd import binding as B
+from paper_2607_00501_amd import inputs
+from paper_2607_00501_amd.decoder import DecoderConfig, DenseDecoder, LayerWeights
+from tests.helpers import GEMV_TOL, rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _f16_bits(a):
+    return np.asarray(a, dtype=np.float16).view(np.uint16)
+
+
+# ---------------------------------------------------------------- glue kernels
+
+@pytest.mark.parametrize("rows,hidden", [(1, 1), (1, 96), (3, 1000), (1, 1024), (2, 4096), (1, 8192)])
+@pytest.mark.parametrize("with_residual", [False, True])
+def test_rmsnorm_parity(rows, hidden, with_residual):
+    rng = np.random.default_rng(rows * 7 + hidden)
+    x = (rng.standard_normal((rows, hidden)) * 3).astype(np.float32)
+    r = rng.standard_normal((rows, hidden)).astype(np.float32)
+    w = inputs.norm_weights_np(hidden, hidden)
+    xd = torch.from_numpy(x).cuda()
+    out = B.qdec_rmsnorm(xd, torch.from_numpy(w).cuda(), 1e-6,
+                         residual=torch.from_numpy(r).cuda() if with_residual else None).cpu().numpy()
+    xs = x.astype(np.float64) + (r if with_residual else 0.0)
+    assert np.array_equal(xd.cpu().numpy(), (x + r) if with_residual else x)      # fp32 add written back
+    for i in range(rows):
+        ref = O.rmsnorm(xs[i], w, 1e-6)
+        assert rel_err(out[i].astype(np.float64), ref) <= 1e-3                   # one fp16 rounding
+        # at most one fp16 ulp away from the rounded oracle value
+        diff = np.abs(_f16_bits(out[i]).astype(np.int32) - _f16_bits(O.f16(ref)).astype(np.int32))
+        assert diff.max() <= 1
+
+
+def test_rmsnorm_zero_rows_and_zero_vector():
+    x = torch.zeros((1, 64), device="cuda")
+    w = torch.ones(64, dtype=torch.float16, device="cuda")
+    assert torch.all(B.qdec_rmsnorm(x, w, 1e-6) == 0)
+    e = torch.empty((0, 64), device="cuda")
+    assert B.qdec_rmsnorm(e, w, 1e-6).shape == (0, 64)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("pos,theta", [(0, 1e4), (7, 1e4), (1000, 5e5), (200_000, 1e6), (262_143, 1e6)])
+def test_rope_append_parity(d, pos, theta):
+    hq, hkv = 6, 2
+    max_len = max(pos + 1, 16)
+    rng = np.random.default_rng(pos + d)
+    q = rng.standard_normal(hq * d).astype(np.float32)
+    k = rng.standard_normal(hkv * d).astype(np.float32)
+    v = rng.standard_normal(hkv * d).astype(np.float32)
+    kc = torch.full((hkv, max_len, d), 0.5, dtype=torch.float16, device="cuda")
+    vc = torch.full((hkv, max_len, d), -0.25, dtype=torch.float16, device="cuda")
+    qo = B.qdec_rope_append(torch.from_numpy(q).cuda(), torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda(),
+                            pos, theta, kc, vc).cpu().numpy()
+    ref_q = O.f16(O.rope(q.reshape(hq, d), pos, theta))
+    ref_k = O.f16(O.rope(k.reshape(hkv, d), pos, theta))
+    # fp32 rotation vs fp64, then one rounding each: one fp16 ulp (<= 2^-10
+    # relative) plus the fp32 error of a near-cancelling a cos - b sin
+    for got, want in ((qo, ref_q), (kc.cpu().numpy()[:, pos], ref_k)):
+        got = got.astype(np.float64)
+        assert np.all(np.abs(got - want) <= 2.0 ** -10 * np.abs(want) + 1e-6 * np.abs(want).max())
+    kcn, vcn = kc.cpu().numpy(), vc.cpu().numpy()
+    assert np.array_equal(vcn[:, pos], v.reshape(hkv, d).astype(np.float16))
+    other = np.ones(max_len, bool)
+    other[pos] = False
+    assert np.all(kcn[:, other] == 0.5) and np.all(vcn[:, other] == -0.25)     # only row pos written
+
+
+def test_cast_f16_bit_exact():
+    rng = np.random.default_rng(9)
+    x = np.concatenate([rng.standard_normal(1000).astype(np.float32) * 100,
+                        np.array([65504.0, 65520.0, 65519.99, 1e6, -1e6, 6e-8, 3e-8, -2.9e-8, 1e-30, 0.0, -0.0,
+                                  np.inf, -np.inf], np.float32),
+                        # exact ties between neighbouring fp16 values round to even
+                        (np.arange(1024, 1100, dtype=np.float32) + 0.5)])
+    y = B.qdec_cast_f16(torch.from_numpy(x).cuda()).cpu().numpy()
+    with np.errstate(over="ignore"):
+        want = x.astype(np.float16)
+    assert np.array_equal(_f16_bits(y), _f16_bits(want))
+    assert B.qdec_cast_f16(torch.empty(0, device="cuda")).numel() == 0
+
+
+@pytest.mark.parametrize("case", ["random", "ties", "nan", "allnan", "neginf", "one", "vocab"])
+def test_argmax_parity(case):
+    rng = np.random.default_rng(13)
+    if case == "random":
+        z = rng.standard_normal(5000).astype(np.float32)
+    elif case == "ties":
+        z = rng.standard_normal(300_000).astype(np.float32)
+        z[[100_000, 5, 299_999, 1025]] = 50.0                # lowest index wins, across threads
+    elif case == "nan":
+        z = rng.standard_normal(4096).astype(np.float32)
+        z[::3] = np.nan
+    elif case == "allnan":
+        z = np.full(777, np.nan, np.float32)
+    elif case == "neginf":
+        z = np.full(2000, -np.inf, np.float32)
+        z[1999] = -1e30
+    elif case == "one":
+        z = np.array([-7.0], np.float32)
+    else:
+        z = rng.standard_normal(151_936).astype(np.float32)
+    t = B.qdec_argmax(torch.from_numpy(z).cuda()).cpu().numpy()
+    assert t.shape == (1,) and int(t[0]) == O.greedy_token(z)
+
+
+def test_embed_gathers_rows_and_flags_bad_ids():
+    table = inputs.activations_np(5, (1000, 256))
+    td = torch.from_numpy(table).cuda()
+    for t in (0, 999, 314):
+        x = B.qdec_embed(td, torch.tensor([t], dtype=torch.int32, device="cuda")).cpu().numpy()
+        assert np.array_equal(x, table[t].astype(np.float32))
+    for t in (-1, 1000):
+        x = B.qdec_embed(td, torch.tensor([t], dtype=torch.int32, device="cuda")).cpu().numpy()
+        assert np.all(np.isnan(x))
+
+
+# ---------------------------------------------------------------- decode steps
+
+def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32)):
+    """Seeded weights of a dense decoder, quantised on the device (library)
+    and in the oracle from the same fp32 values."""
+    ofmt, bfmt = fmts
+    qd, kvd = cfg.n_q_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
+
+    def proj(name, li, n, k):
+        w = inputs.weights_np(inputs.seed_for(tag, li, name), (n, k), sigma=1.0 / math.sqrt(k))
+        dev = B.qm_repack(B.qm_quantise(torch.from_numpy(w).cuda(), bfmt), B.LAYOUT_DEVICE)
+        q, s = O.quantise(w, ofmt)
+        return dev, O.dequantise(O.pack(q, ofmt), s, ofmt).astype(np.float64)
+
+    dev_layers, ref_layers = [], []
+    for li in range(cfg.layers):
+        shapes = dict(q=(qd, cfg.hidden), k=(kvd, cfg.hidden), v=(kvd, cfg.hidden), o=(cfg.hidden, qd),
+                      gate=(cfg.inter, cfg.hidden), up=(cfg.inter, cfg.hidden), down=(cfg.hidden, cfg.inter))
+        p = {name: proj(name, li, *sh) for name, sh in shapes.items()}
+        an = inputs.norm_weights_np(inputs.seed_for(tag, li, "attn_norm"), cfg.hidden)
+        fn = inputs.norm_weights_np(inputs.seed_for(tag, li, "ffn_norm"), cfg.hidden)
+        dev_layers.append(LayerWeights(p["q"][0], p["k"][0], p["v"][0], p["o"][0], p["gate"][0], p["up"][0],
+                                       p["down"][0], torch.from_numpy(an).cuda(), torch.from_numpy(fn).cuda()))
+        ref_layers.append(dict(wq=p["q"][1], wk=p["k"][1], wv=p["v"][1], wo=p["o"][1], wg=p["gate"][1],
+                               wu=p["up"][1], wd=p["down"][1], attn_norm=an.astype(np.float64),
+                               ffn_norm=fn.astype(np.float64)))
+    emb = inputs.activations_np(inputs.seed_for(tag, 0, "emb"), (cfg.vocab, cfg.hidden))
+    norm = inputs.norm_weights_np(inputs.seed_for(tag, 0, "norm"), cfg.hidden)
+    head_dev, head_ref = proj("lm_head", 0, cfg.vocab, cfg.hidden)
+    ref = dict(emb=emb.astype(np.float64), layers=ref_layers, norm=norm.astype(np.float64), lm_head=head_ref,
+               hq=cfg.n_q_heads, hkv=cfg.n_kv_heads, d=cfg.head_dim, eps=cfg.eps, theta=cfg.theta)
+    return dev_layers, torch.from_numpy(emb).cuda(), torch.from_numpy(norm).cuda(), head_dev, ref
+
+
+def _decoder(cfg, tag, max_len, fmts=(O.Q4, B.Q4_G32)):
+    layers, emb, norm, head, ref = _model(cfg, tag, fmts)
+    dec = DenseDecoder(cfg, emb, layers, norm, head, max_len)
+    kc = np.zeros((cfg.layers, cfg.n_kv_heads, max_len, cfg.head_dim))
+    vc = np.zeros_like(kc)
+    return dec, ref, kc, vc
+
+
+TINY = DecoderConfig(hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, inter=512, vocab=1000, layers=2,
+                     theta=1e4)
+
+
+def test_decode_steps_teacher_forced_tiny():
+    """Ten teacher-forced steps: logits at every step, then the whole caches."""
+    dec, ref, kc, vc = _decoder(TINY, 21, 16)
+    for pos, t in enumerate([5, 17, 999, 0, 42, 42, 7, 300, 1, 2]):
+        dec.token.fill_(t)
+        dec.step(pos)
+        want = O.decode_step(ref, t, pos, kc, vc)
+        assert rel_err(dec.logits.cpu().numpy(), want) <= GEMV_TOL, pos
+    assert rel_err(dec.k_cache.cpu().numpy().astype(np.float64), kc) <= 2e-3
+    assert rel_err(dec.v_cache.cpu().numpy().astype(np.float64), vc) <= 2e-3
+    assert torch.all(dec.k_cache[:, :, 10:] == 0) and torch.all(dec.v_cache[:, :, 10:] == 0)
+
+
+def test_decode_steps_greedy_chain_q8_d128():
+    """Greedy generation with the token kept on the device: every sampled id
+    is the argmax of that step's logits, and the oracle fed the same ids
+    gives the same logits.  head_dim 128, 8 query heads per KV head, Q8."""
+    cfg = DecoderConfig(hidden=512, n_q_heads=16, n_kv_heads=2, head_dim=128, inter=1024, vocab=3001, layers=1)
+    dec, ref, kc, vc = _decoder(cfg, 22, 32, fmts=(O.Q8, B.Q8_G32))
+    dec.token.fill_(3)
+    t = 3
+    for pos in range(6):
+        dec.step(pos)
+        logits = dec.logits.cpu().numpy()
+        want = O.decode_step(ref, t, pos, kc, vc)
+        assert rel_err(logits, want) <= GEMV_TOL, pos
+        t = int(dec.token.item())
+        assert t == O.greedy_token(logits)
+
+
+def test_decode_step_qwen3_widths_long_context():
+    """Qwen3-0.6B layer widths (hidden 1024, 16 / 8 heads of 128, FFN 3072),
+    two layers, a 20000-entry vocabulary, at positions 1000 and 1001 over a
+    cache pre-filled with seeded values (the same on both sides)."""
+    cfg = DecoderConfig(hidden=1024, n_q_heads=16, n_kv_heads=8, head_dim=128, inter=3072, vocab=20000, layers=2)
+    p0 = 1000
+    dec, ref, kc, vc = _decoder(cfg, 23, 1024)
+    pre_k = inputs.activations_np(inputs.seed_for(23, 0, "cache"), kc.shape)
+    pre_v = inputs.activations_np(inputs.seed_for(23, 1, "cache"), kc.shape)
+    pre_k[:, :, p0:] = 0
+    pre_v[:, :, p0:] = 0
+    dec.k_cache.copy_(torch.from_numpy(pre_k))
+    dec.v_cache.copy_(torch.from_numpy(pre_v))
+    kc[:] = pre_k
+    vc[:] = pre_v
+    for pos, t in ((p0, 12345), (p0 + 1, 19999)):
+        dec.token.fill_(t)
+        dec.step(pos)
+        assert rel_err(dec.logits.cpu().numpy(), O.decode_step(ref, t, pos, kc, vc)) <= GEMV_TOL, pos
+
+
+def test_decode_step_graph_replay_matches_eager():
+    """A captured step replayed several times (eager work and
+    synchronisations between replays) gives the eager step's logits and
+    token each time."""
+    dec, _, _, _ = _decoder(TINY, 24, 16)
+    dec.token.fill_(11)
+    dec.step(0)
+    dec.token.fill_(11)
+    dec.step(1)
+    eager_logits, eager_tok = dec.logits.clone(), dec.token.clone()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        dec.token.fill_(11)
+        with torch.cuda.graph(g, stream=s):
+            dec.step(1)
+    torch.cuda.current_stream().wait_stream(s)
+    for _ in range(3):
+        dec.token.fill_(11)
+        dec.logits.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dec.logits, eager_logits) and torch.equal(dec.token, eager_tok)

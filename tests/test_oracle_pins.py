@@ -638,3 +638,13 @@ def test_decode_step_matches_prefill_attention_of_the_sequence():
     qp = np.zeros((4, 5, 16)); qp[:, 4] = q
     pre = O.attention_prefill(qp, kc[0, :, :5], vc[0, :, :5], 0.25)
     assert np.allclose(dec, pre[:, 4], atol=1e-14)
+
+
+def test_greedy_token_ties_nan_and_infinities():
+    assert O.greedy_token([0.5, 2.0, 2.0, -1.0]) == 1                 # first of equal maxima
+    assert O.greedy_token([np.nan, -np.inf, -np.inf]) == 1           # NaN never chosen
+    assert O.greedy_token([np.nan, np.nan]) == 0
+    assert O.greedy_token([1.0, np.inf, np.nan, np.inf]) == 1
+    assert O.greedy_token([-3.0]) == 0
+    z = np.random.default_rng(47).standard_normal(1000)
+    assert O.greedy_token(z) == int(np.argmax(z))
