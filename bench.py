@@ -276,6 +276,58 @@ def extra_workloads(torch, B, inputs, workloads, steps, warmup, which="all"):
     return out
 
 
+def build_decoder(model: dict, cfg_id: int, fmt, max_len, torch, B, inputs):
+    """A dense decoder of the model's geometry with seeded synthetic weights
+    (projections quantised on the device), as DenseDecoder."""
+    from paper_2607_00501_amd.decoder import DecoderConfig, DenseDecoder, LayerWeights
+    cfg = DecoderConfig(**{k: v for k, v in model.items() if k != "name"})
+    qd, kvd = cfg.n_q_heads * cfg.head_dim, cfg.n_kv_heads * cfg.head_dim
+
+    def proj(name, li, n, k):
+        w = inputs.weights_dev(inputs.seed_for(cfg_id, li, name), (n, k))
+        q = B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE)
+        del w
+        return q
+
+    def gain(name, li):
+        return torch.from_numpy(inputs.norm_weights_np(inputs.seed_for(cfg_id, li, name), cfg.hidden)).cuda()
+
+    layers = []
+    for li in range(cfg.layers):
+        layers.append(LayerWeights(proj("q", li, qd, cfg.hidden), proj("k", li, kvd, cfg.hidden),
+                                   proj("v", li, kvd, cfg.hidden), proj("o", li, cfg.hidden, qd),
+                                   proj("gate", li, cfg.inter, cfg.hidden), proj("up", li, cfg.inter, cfg.hidden),
+                                   proj("down", li, cfg.hidden, cfg.inter), gain("attn_norm", li),
+                                   gain("ffn_norm", li)))
+    emb = inputs.activations_dev(inputs.seed_for(cfg_id, 0, "emb"), (cfg.vocab, cfg.hidden))
+    head = proj("lm_head", 0, cfg.vocab, cfg.hidden)
+    torch.cuda.synchronize()
+    return DenseDecoder(cfg, emb, layers, gain("norm", 0), head, max_len)
+
+
+def tg_tokens_per_s(torch, dec, tokens: int, reps: int):
+    """tg-N: N greedy decode steps from an empty cache (positions 0 .. N-1),
+    the sampled token fed back on the device, all N steps captured in one
+    graph (no host synchronisation between tokens).  Returns (tokens/s,
+    replay seconds)."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        dec.token.fill_(1)
+        dec.step(0)                                   # eager warm-up
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for pos in range(tokens):
+            dec.step(pos)
+    torch.cuda.synchronize()
+    dec.token.fill_(1)
+    t, _ = time_graph(torch, g, reps, 1)
+    del g
+    return tokens * reps / t, t / reps
+
+
 def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
     out = {}
 
@@ -311,6 +363,20 @@ def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
             log(f"{tag} {key}: {out[f'{tag}_decode_q4_{key}']}")
             del g, calls
             torch.cuda.empty_cache()
+
+    # End-to-end decode, tg128 (Sec. 4.1): every kernel of a token (embedding,
+    # norms, projections, RoPE and cache append, attention, SwiGLU, LM head,
+    # greedy sampling), 11 launches per layer + 4.
+    for model, cfg_id in ((workloads.QWEN3_06B_DECODER, 1), (workloads.LLAMA32_1B_DECODER, 3),
+                          (workloads.LLAMA32_3B_DECODER, 2)):
+        dec = build_decoder(model, cfg_id, B.Q4_G32, 128, torch, B, inputs)
+        tps, t = tg_tokens_per_s(torch, dec, 128, 3)
+        key = model["name"] + "_tg128_q4"
+        out[key] = {"tokens_per_s": round(tps, 1), "ms_per_token": round(1e3 / tps, 4),
+                    "launches_per_token": 11 * model["layers"] + 4, "ms_per_128_tokens": round(t * 1e3, 3)}
+        log(f"{key}: {out[key]}")
+        del dec
+        torch.cuda.empty_cache()
 
     # Llama-3.2-3B decode stacks, Q4 and Q8
     for fmt, tag in ((B.Q4_G32, "q4"), (B.Q8_G32, "q8")):

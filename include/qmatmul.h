@@ -244,7 +244,8 @@ qm_status qattn_decode_workspace_bytes(int32_t n_q_heads, int32_t head_dim, size
  * v_cache, workspace 16-byte aligned; workspace of at least
  * qattn_decode_workspace_bytes() bytes (caller-owned scratch, contents not
  * preserved).  Scores and sums in fp32, split over the cache length and
- * merged exactly as online softmax does.  Two kernel launches; deterministic. */
+ * merged exactly as online softmax does.  Two kernel launches (one, with no
+ * merge, when len <= 128); deterministic. */
 qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
                        int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale, float* o,
                        void* workspace, size_t ws_bytes, void* stream);
@@ -289,8 +290,14 @@ qm_status qdec_cast_f16(const float* x, int64_t n, uint16_t* out, void* stream);
 
 /* Greedy sampling: *token = the index of the largest of logits[0 .. n),
  * the lowest index among equal maxima; NaNs are never chosen (0 if all
- * are NaN).  logits: fp32, device; token: one int32, device; n >= 1. */
-qm_status qdec_argmax(const float* logits, int64_t n, int32_t* token, void* stream);
+ * are NaN).  logits: fp32, device; token: one int32, device; n >= 1;
+ * workspace: caller-owned device scratch of at least
+ * QDEC_ARGMAX_WORKSPACE_BYTES bytes, 4-byte aligned, contents not
+ * preserved (partial maxima of up to 256 workgroups).  One launch for
+ * n <= 4096, else two. */
+#define QDEC_ARGMAX_WORKSPACE_BYTES 2048
+qm_status qdec_argmax(const float* logits, int64_t n, int32_t* token, void* workspace, size_t ws_bytes,
+                      void* stream);
 
 /* Host-only: workspace bytes qmoe_grouped_gemm needs for m tokens. */
 qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden,

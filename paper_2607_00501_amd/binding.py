@@ -80,7 +80,7 @@ def lib() -> ctypes.CDLL:
             "qdec_rmsnorm": [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp],
             "qdec_rope_append": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, vp, vp],
             "qdec_cast_f16": [vp, i64, vp, vp],
-            "qdec_argmax": [vp, i64, vp, vp],
+            "qdec_argmax": [vp, i64, vp, vp, sz, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -340,12 +340,19 @@ def qdec_cast_f16(x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=No
     return out
 
 
-def qdec_argmax(logits: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+ARGMAX_WORKSPACE_BYTES = 2048
+
+
+def qdec_argmax(logits: torch.Tensor, out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                stream=None):
     """fp32 [n] -> int32 [1] on the device (lowest index among equal maxima)."""
     assert logits.dtype == torch.float32 and logits.is_contiguous()
     if out is None:
         out = torch.empty(1, dtype=torch.int32, device=logits.device)
-    _check(lib().qdec_argmax(_ptr(logits), logits.numel(), _ptr(out), _stream(stream)))
+    if workspace is None:
+        workspace = torch.empty(ARGMAX_WORKSPACE_BYTES, dtype=torch.uint8, device=logits.device)
+    _check(lib().qdec_argmax(_ptr(logits), logits.numel(), _ptr(out), _ptr(workspace), workspace.numel(),
+                             _stream(stream)))
     return out
 
 

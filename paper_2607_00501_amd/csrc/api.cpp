@@ -414,11 +414,16 @@ qm_status qdec_cast_f16(const float* x, int64_t n, uint16_t* out, void* stream) 
   return launched(launch_cast_f16(x, n, out, static_cast<hipStream_t>(stream)), "qdec_cast_f16");
 }
 
-qm_status qdec_argmax(const float* logits, int64_t n, int32_t* token, void* stream) {
+qm_status qdec_argmax(const float* logits, int64_t n, int32_t* token, void* workspace, size_t ws_bytes,
+                      void* stream) {
   if (n < 1 || n > INT32_MAX - 1) return fail(QM_ESHAPE, "qdec_argmax: need 1 <= n < 2^31-1");
   if (!logits || !token) return fail(QM_EINVAL, "qdec_argmax: null pointer");
-  if (!aligned4(logits) || !aligned4(token)) return fail(QM_EALIGN, "qdec_argmax: logits and token 4-byte aligned");
-  return launched(launch_argmax(logits, n, token, static_cast<hipStream_t>(stream)), "qdec_argmax");
+  if (!workspace || ws_bytes < QDEC_ARGMAX_WORKSPACE_BYTES)
+    return fail(QM_EWORKSPACE, "qdec_argmax: workspace of %d bytes needed (got %zu)", QDEC_ARGMAX_WORKSPACE_BYTES,
+                ws_bytes);
+  if (!aligned4(logits) || !aligned4(token) || !aligned4(workspace))
+    return fail(QM_EALIGN, "qdec_argmax: logits, token and workspace 4-byte aligned");
+  return launched(launch_argmax(logits, n, token, workspace, static_cast<hipStream_t>(stream)), "qdec_argmax");
 }
 
 qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden, int64_t inter,

@@ -48,7 +48,8 @@ __device__ __forceinline__ float wave_sum(float v) {
 template <int D, int G>
 __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    int64_t len, int64_t max_len, int tc, int nsplit, float scale_log2, float* __restrict__ ws) {
+    int64_t len, int64_t max_len, int tc, int nsplit, float scale_log2, float* __restrict__ ws,
+    float* __restrict__ o) {
   constexpr int LPR = D / 8;                 // lanes per cache row
   constexpr int RPW = 64 / LPR;              // rows per wavefront load
   constexpr int RPI = kAttnWaves * RPW;      // rows per workgroup load
@@ -179,6 +180,16 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
       for (int i = 0; i < 8; ++i) part[wave][j][sub * 8 + i] = acc[j][i];
   }
   __syncthreads();
+  if (o) {   // a single slice covers the whole cache: normalise and write the output
+    for (int e = threadIdx.x; e < G * D; e += kAttnWaves * 64) {
+      const int j = e / D, d = e % D;
+      float a = part[0][j][d];
+#pragma unroll
+      for (int w2 = 1; w2 < kAttnWaves; ++w2) a += part[w2][j][d];
+      o[(static_cast<int64_t>(g) * G + j) * D + d] = a / stat[j][1];
+    }
+    return;
+  }
   for (int e = threadIdx.x; e < G * D; e += kAttnWaves * 64) {
     const int j = e / D, d = e % D;
     float a = part[0][j][d];
@@ -248,9 +259,9 @@ hipError_t launch_decode_dg(const uint16_t* q, const uint16_t* k, const uint16_t
                             int64_t max_len, float scale, float* o, float* ws, const AttnPlan& p, hipStream_t st) {
   const size_t lds = static_cast<size_t>(G) * p.tc * sizeof(float);
   hipLaunchKernelGGL((attn_decode_split_kernel<D, G>), dim3(p.nsplit, hkv), dim3(kAttnWaves * 64), lds, st, q, k, v,
-                     len, max_len, p.tc, p.nsplit, scale * 1.4426950408889634f, ws);
+                     len, max_len, p.tc, p.nsplit, scale * 1.4426950408889634f, ws, p.nsplit == 1 ? o : nullptr);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || p.nsplit == 1) return e;
   hipLaunchKernelGGL((attn_decode_combine_kernel<D>), dim3(hkv * G), dim3(D), 0, st, ws, p.nsplit, o);
   return hipGetLastError();
 }
@@ -508,6 +519,9 @@ hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint1
 // least 32 rows each (a multiple of 32), at most kAttnMaxSplits slices, and
 // few enough rows that the G x rows scores fit in 32 KiB of LDS.
 AttnPlan attn_decode_plan(int hkv, int group, int64_t len, int cu_count) {
+  // Short caches: one slice per KV head, which writes the output itself (no
+  // merge launch); a few memory round trips cost less than the second launch.
+  if (len <= kAttnDirectLen) return AttnPlan{static_cast<int>((len + 31) / 32 * 32), 1};
   const int64_t want = (2 * static_cast<int64_t>(cu_count) + hkv - 1) / hkv;
   const int64_t tc_max = kAttnScoreFloats / group / 32 * 32;
   int64_t nsplit = std::min<int64_t>(std::min<int64_t>(want, kAttnMaxSplits), (len + 31) / 32);

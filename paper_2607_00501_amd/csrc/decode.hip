@@ -47,6 +47,44 @@ __global__ __launch_bounds__(256) void embed_kernel(const uint16_t* __restrict__
 }
 
 // One workgroup per row: x += residual (written back), out = fp16(x / rms * w).
+// Rows of up to 256 * PER elements stay in registers: the loads of x, the
+// residual and w go out together, so a row costs one memory round trip
+// before the reduction.
+template <int PER>
+__global__ __launch_bounds__(256) void rmsnorm_reg_kernel(float* __restrict__ x, const float* __restrict__ res,
+                                                          const uint16_t* __restrict__ w, int64_t hidden, float eps,
+                                                          uint16_t* __restrict__ out) {
+  __shared__ float red[4];
+  float* xr = x + blockIdx.x * hidden;
+  const float* rr = res ? res + blockIdx.x * hidden : nullptr;
+  float v[PER], g[PER], r[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int i = threadIdx.x + j * 256;
+    v[j] = i < hidden ? xr[i] : 0.0f;
+    g[j] = i < hidden ? h2f(w[i]) : 0.0f;
+    r[j] = rr && i < hidden ? rr[i] : 0.0f;
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    v[j] += r[j];
+    ss = fmaf(v[j], v[j], ss);
+  }
+  if (rr) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      if (threadIdx.x + j * 256 < hidden) xr[threadIdx.x + j * 256] = v[j];
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / static_cast<float>(hidden) + eps);
+  uint16_t* o = out + blockIdx.x * hidden;
+#pragma unroll
+  for (int j = 0; j < PER; ++j)
+    if (threadIdx.x + j * 256 < hidden) o[threadIdx.x + j * 256] = f2h(v[j] * inv * g[j]);
+}
+
+// Rows longer than the register tile: two passes over the row.
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ res,
                                                       const uint16_t* __restrict__ w, int64_t hidden, float eps,
                                                       uint16_t* __restrict__ out) {
@@ -101,43 +139,79 @@ __global__ __launch_bounds__(256) void cast_f16_kernel(const float* __restrict__
 }
 
 // Greedy sampling: index of the largest logit, the lowest index among equal
-// ones; NaNs are never chosen; 0 if every logit is NaN.
-constexpr int kArgmaxThreads = 1024;
-__global__ __launch_bounds__(kArgmaxThreads) void argmax_kernel(const float* __restrict__ x, int64_t n,
-                                                                int32_t* __restrict__ token) {
-  __shared__ float bv[kArgmaxThreads / 64];
-  __shared__ int32_t bi[kArgmaxThreads / 64];
-  float best = -INFINITY;
-  int32_t idx = INT32_MAX;
-  for (int64_t i = threadIdx.x; i < n; i += kArgmaxThreads) {
-    const float v = x[i];
-    if (v > best || (v == best && idx == INT32_MAX)) {
-      best = v;
-      idx = static_cast<int32_t>(i);
-    }
+// ones; NaNs are never chosen; 0 if every logit is NaN.  Pass 1: each of up
+// to kArgmaxBlocks workgroups reduces a strided share of the logits, four
+// independent loads in flight per lane, to one (value, index) pair (a lone
+// workgroup writes the token directly); pass 2 reduces the pairs.
+constexpr int kArgmaxBlocks = 256;
+
+// (value, index) pair order: larger value first, then lower index; the
+// index INT32_MAX marks "nothing seen yet".
+__device__ __forceinline__ void take_better(float& bv, int32_t& bi, float v, int32_t i) {
+  if (v > bv || (v == bv && i < bi)) {
+    bv = v;
+    bi = i;
   }
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(best, o, 64);
-    const int32_t oi = __shfl_xor(idx, o, 64);
-    if (ov > best || (ov == best && oi < idx)) {
-      best = ov;
-      idx = oi;
-    }
-  }
+}
+
+__device__ __forceinline__ void block_best(float& bv, int32_t& bi) {
+  __shared__ float sv[4];
+  __shared__ int32_t si[4];
+  for (int o = 32; o > 0; o >>= 1) take_better(bv, bi, __shfl_xor(bv, o, 64), __shfl_xor(bi, o, 64));
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
-    bv[w] = best;
-    bi[w] = idx;
+    sv[w] = bv;
+    si[w] = bi;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int j = 1; j < kArgmaxThreads / 64; ++j)
-      if (bv[j] > best || (bv[j] == best && bi[j] < idx)) {
-        best = bv[j];
-        idx = bi[j];
+  bv = sv[0];
+  bi = si[0];
+  for (int j = 1; j < 4; ++j) take_better(bv, bi, sv[j], si[j]);
+}
+
+__global__ __launch_bounds__(256) void argmax_partial_kernel(const float* __restrict__ x, int64_t n,
+                                                             float* __restrict__ pv, int32_t* __restrict__ pi,
+                                                             int32_t* __restrict__ token) {
+  float best = -INFINITY;
+  int32_t idx = INT32_MAX;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  for (int64_t base = blockIdx.x * 256 + threadIdx.x; base < n; base += 4 * stride) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t i = base + u * stride;
+      v[u] = i < n ? x[i] : __builtin_nanf("");
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {   // increasing indices: keep the first of equal values
+      if (v[u] > best || (v[u] == best && idx == INT32_MAX)) {
+        best = v[u];
+        idx = static_cast<int32_t>(base + u * stride);
       }
-    token[0] = idx == INT32_MAX ? 0 : idx;
+    }
   }
+  block_best(best, idx);
+  if (threadIdx.x == 0) {
+    if (gridDim.x == 1) {
+      token[0] = idx == INT32_MAX ? 0 : idx;
+    } else {
+      pv[blockIdx.x] = best;
+      pi[blockIdx.x] = idx;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void argmax_final_kernel(const float* __restrict__ pv,
+                                                           const int32_t* __restrict__ pi, int nb,
+                                                           int32_t* __restrict__ token) {
+  float best = -INFINITY;
+  int32_t idx = INT32_MAX;
+  if (static_cast<int>(threadIdx.x) < nb) {
+    best = pv[threadIdx.x];
+    idx = pi[threadIdx.x];
+  }
+  block_best(best, idx);
+  if (threadIdx.x == 0) token[0] = idx == INT32_MAX ? 0 : idx;
 }
 
 unsigned spread_blocks(int64_t n) {
@@ -156,6 +230,19 @@ hipError_t launch_embed(const uint16_t* table, int64_t vocab, int64_t hidden, co
 hipError_t launch_rmsnorm(float* x, const float* res, const uint16_t* w, int64_t rows, int64_t hidden, float eps,
                           uint16_t* out, hipStream_t st) {
   if (rows == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(rows)), block(256);
+  if (hidden <= 256 * 4) {
+    hipLaunchKernelGGL(rmsnorm_reg_kernel<4>, grid, block, 0, st, x, res, w, hidden, eps, out);
+    return hipGetLastError();
+  }
+  if (hidden <= 256 * 8) {
+    hipLaunchKernelGGL(rmsnorm_reg_kernel<8>, grid, block, 0, st, x, res, w, hidden, eps, out);
+    return hipGetLastError();
+  }
+  if (hidden <= 256 * 16) {
+    hipLaunchKernelGGL(rmsnorm_reg_kernel<16>, grid, block, 0, st, x, res, w, hidden, eps, out);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(rmsnorm_kernel, dim3(static_cast<unsigned>(rows)), dim3(256), 0, st, x, res, w, hidden, eps,
                      out);
   return hipGetLastError();
@@ -175,8 +262,16 @@ hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_argmax(const float* x, int64_t n, int32_t* token, hipStream_t st) {
-  hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(kArgmaxThreads), 0, st, x, n, token);
+hipError_t launch_argmax(const float* x, int64_t n, int32_t* token, void* ws, hipStream_t st) {
+  const int64_t want = (n + 4095) / 4096;
+  const int nb = static_cast<int>(want < kArgmaxBlocks ? want : kArgmaxBlocks);
+  float* pv = static_cast<float*>(ws);
+  int32_t* pi = reinterpret_cast<int32_t*>(pv + kArgmaxBlocks);
+  hipLaunchKernelGGL(argmax_partial_kernel, dim3(nb), dim3(256), 0, st, x, n, pv, pi, token);
+  if (nb == 1) return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(argmax_final_kernel, dim3(1), dim3(256), 0, st, pv, pi, nb, token);
   return hipGetLastError();
 }
 

@@ -116,6 +116,7 @@ hipError_t launch_gemm_group(int32_t fmt, int count, const uint8_t* const* q, co
 constexpr int kAttnMaxSplits = 256;
 constexpr int kAttnScoreFloats = 8192;           // LDS floats for the scores of one slice (32 KiB)
 constexpr int64_t kAttnMaxLen = 262144;          // kAttnMaxSplits x (kAttnScoreFloats / 8 heads)
+constexpr int64_t kAttnDirectLen = 128;          // caches up to this length: one slice, no merge
 struct AttnPlan { int tc; int nsplit; };
 AttnPlan attn_decode_plan(int hkv, int group, int64_t len, int cu_count);
 size_t attn_decode_workspace_bytes(int32_t hq, int32_t d);
@@ -136,7 +137,7 @@ hipError_t launch_rope_append(const float* q, const float* k, const float* v, in
                               int64_t pos, int64_t max_len, float theta, uint16_t* q_out, uint16_t* kc,
                               uint16_t* vc, hipStream_t st);
 hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t st);
-hipError_t launch_argmax(const float* x, int64_t n, int32_t* token, hipStream_t st);
+hipError_t launch_argmax(const float* x, int64_t n, int32_t* token, void* ws, hipStream_t st);
 
 struct MoeArgs {
   const uint8_t* gq; const uint16_t* gs;   // gate [E][inter][hidden], device layout

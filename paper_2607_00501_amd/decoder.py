@@ -74,6 +74,7 @@ class DenseDecoder:
         self.v_cache = torch.zeros((c.layers, c.n_kv_heads, max_len, c.head_dim), **f16)
         self.ws = torch.empty(B.qattn_decode_workspace_bytes(c.n_q_heads, c.head_dim), dtype=torch.uint8,
                               device=dev)
+        self.argmax_ws = torch.empty(B.ARGMAX_WORKSPACE_BYTES, dtype=torch.uint8, device=dev)
         self.scale = 1.0 / math.sqrt(c.head_dim)
 
     def step(self, pos: int, stream=None) -> None:
@@ -97,4 +98,4 @@ class DenseDecoder:
             B.qmatmul_gemv(ly.wd, self.g16, out=self.y_ffn, stream=s)
         B.qdec_rmsnorm(self.x, self.norm, c.eps, residual=self.y_ffn, out=self.h, stream=s)
         B.qmatmul_gemv(self.lm_head, self.h, out=self.logits, stream=s)
-        B.qdec_argmax(self.logits, out=self.token, stream=s)
+        B.qdec_argmax(self.logits, out=self.token, workspace=self.argmax_ws, stream=s)

@@ -299,6 +299,13 @@ def test_decode_glue_validation():
     assert rope(q=None) == 1 and rope(kc=odd) == 3
     assert L.qdec_cast_f16(p, -1, p, None) == 2 and L.qdec_cast_f16(None, 4, p, None) == 1
     assert L.qdec_cast_f16(ctypes.c_void_p(0x50002), 4, p, None) == 3
-    assert L.qdec_argmax(p, 0, p, None) == 2 and L.qdec_argmax(None, 4, p, None) == 1
-    assert L.qdec_argmax(p, 4, odd, None) == 3
+    am = lambda n=4, x=p, t=p, w=p, nb=2048: L.qdec_argmax(x, n, t, w, nb, None)
+    assert am(n=0) == 2 and am(x=None) == 1 and am(t=odd) == 3 and am(w=odd) == 3
+    assert am(nb=2047) == 6 and am(w=None) == 6
     assert B.qm_last_error()
+
+
+def test_argmax_workspace_constant_matches_header():
+    import re
+    hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "qmatmul.h")).read()
+    assert int(re.search(r"#define QDEC_ARGMAX_WORKSPACE_BYTES (\d+)", hdr).group(1)) == B.ARGMAX_WORKSPACE_BYTES
