@@ -166,6 +166,12 @@ qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* s
 qm_status qmatmul_gemv_swiglu(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, float* h,
                               void* stream);
 
+/* As qmatmul_gemv_swiglu, with h written as fp16 [n] (round to nearest
+ * even of the same fp32 value; 2-byte aligned), ready to be the input of
+ * the down projection's GEMV. */
+qm_status qmatmul_gemv_swiglu_f16(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, uint16_t* h,
+                                  void* stream);
+
 /* Grouped decode GEMV (Sec. 3.3: fusing a sequence of operators removes a
  * launch each, which matters most in decode; e.g. the q/k/v projections of
  * a layer, which share x, or its gate and up projections):
@@ -249,6 +255,13 @@ qm_status qattn_decode_workspace_bytes(int32_t n_q_heads, int32_t head_dim, size
 qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
                        int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale, float* o,
                        void* workspace, size_t ws_bytes, void* stream);
+
+/* As qattn_decode, with o written as fp16 [n_q_heads][head_dim] (round to
+ * nearest even of the same fp32 value; 2-byte aligned), ready to be the
+ * input of the output projection's GEMV. */
+qm_status qattn_decode_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                           int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale,
+                           uint16_t* o, void* workspace, size_t ws_bytes, void* stream);
 
 /* ---- Glue of one decode step (Sec. 3.2: the normalisation, RoPE,
  * embedding and sampling kernels between the matmuls and attention of a

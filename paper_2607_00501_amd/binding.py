@@ -30,7 +30,7 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmoe_workspace_bytes", "qmoe_route",
            "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
            "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
-           "qdec_argmax")
+           "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16")
 
 
 class QmError(RuntimeError):
@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
             "qattn_decode": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp],
             "qdec_embed": [vp, i64, i64, vp, vp, vp],
+            "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
+            "qattn_decode_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qdec_rmsnorm": [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp],
             "qdec_rope_append": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, vp, vp],
             "qdec_cast_f16": [vp, i64, vp, vp],
@@ -182,12 +184,14 @@ def qmatmul_gemv(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None
 
 def qmatmul_gemv_swiglu(w_gate: QWeight, w_up: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None,
                         stream=None):
-    """x: fp16 [k] -> h = silu(Wg x) * (Wu x), fp32 [n]."""
+    """x: fp16 [k] -> h = silu(Wg x) * (Wu x), fp32 [n] (fp16 when `out` is
+    an fp16 tensor)."""
     assert x.dtype == torch.float16 and x.is_contiguous() and x.numel() == w_gate.k
     if out is None:
         out = torch.empty(w_gate.n, dtype=torch.float32, device=x.device)
-    _check(lib().qmatmul_gemv_swiglu(ctypes.byref(w_gate.c()), ctypes.byref(w_up.c()), _ptr(x), _ptr(out),
-                                     _stream(stream)))
+    fn = lib().qmatmul_gemv_swiglu_f16 if out.dtype == torch.float16 else lib().qmatmul_gemv_swiglu
+    assert out.dtype in (torch.float16, torch.float32) and out.is_contiguous() and out.numel() == w_gate.n
+    _check(fn(ctypes.byref(w_gate.c()), ctypes.byref(w_up.c()), _ptr(x), _ptr(out), _stream(stream)))
     return out
 
 
@@ -257,7 +261,8 @@ def qattn_decode_workspace_bytes(n_q_heads: int, head_dim: int) -> int:
 
 def qattn_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, length: int, scale: float,
                  out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None, stream=None):
-    """q: fp16 [Hq][D]; k_cache, v_cache: fp16 [Hkv][max_len][D] -> fp32 [Hq][D]."""
+    """q: fp16 [Hq][D]; k_cache, v_cache: fp16 [Hkv][max_len][D] -> fp32 [Hq][D]
+    (fp16 when `out` is an fp16 tensor)."""
     hq, d = q.shape
     hkv, max_len, d2 = k_cache.shape
     assert d2 == d and v_cache.shape == k_cache.shape
@@ -268,8 +273,10 @@ def qattn_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, 
     nb = qattn_decode_workspace_bytes(hq, d)
     if workspace is None:
         workspace = torch.empty(nb, dtype=torch.uint8, device=q.device)
-    _check(lib().qattn_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, length, max_len, scale,
-                              _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)))
+    assert out.dtype in (torch.float16, torch.float32) and out.is_contiguous() and out.numel() == hq * d
+    fn = lib().qattn_decode_f16 if out.dtype == torch.float16 else lib().qattn_decode
+    _check(fn(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, length, max_len, scale,
+              _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)))
     return out
 
 

@@ -181,27 +181,48 @@ qm_status qmatmul_gemv(const qm_qweight* w, const uint16_t* x, float* y, void* s
                   "qmatmul_gemv");
 }
 
-qm_status qmatmul_gemv_swiglu(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, float* h,
-                              void* stream) {
-  qm_status st = check_weight(w_gate, "qmatmul_gemv_swiglu(w_gate)");
+}  // extern "C"
+
+namespace {
+
+// Shared checks and launch of the SwiGLU pair; out is h (fp32) or h16 (fp16).
+qm_status swiglu_call(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, float* h, uint16_t* h16,
+                      void* stream, const char* name) {
+  char what[64];
+  std::snprintf(what, sizeof(what), "%s(w_gate)", name);
+  qm_status st = check_weight(w_gate, what);
   if (st != QM_OK) return st;
-  if ((st = check_weight(w_up, "qmatmul_gemv_swiglu(w_up)")) != QM_OK) return st;
+  std::snprintf(what, sizeof(what), "%s(w_up)", name);
+  if ((st = check_weight(w_up, what)) != QM_OK) return st;
   if (w_gate->layout != QM_LAYOUT_DEVICE || w_up->layout != QM_LAYOUT_DEVICE)
-    return fail(QM_ELAYOUT, "qmatmul_gemv_swiglu: weights must be in DEVICE layout");
-  if (w_gate->batch != 1 || w_up->batch != 1) return fail(QM_ESHAPE, "qmatmul_gemv_swiglu: batch must be 1");
-  if (w_up->format != w_gate->format) return fail(QM_EFORMAT, "qmatmul_gemv_swiglu: formats differ");
-  if (w_up->n != w_gate->n || w_up->k != w_gate->k)
-    return fail(QM_ESHAPE, "qmatmul_gemv_swiglu: gate and up shapes differ");
-  if (w_gate->n > INT32_MAX / 2) return fail(QM_ESHAPE, "qmatmul_gemv_swiglu: n too large");
-  if (w_gate->n > 0 && (!x || !h)) return fail(QM_EINVAL, "qmatmul_gemv_swiglu: null x or h");
-  if (!aligned16(x)) return fail(QM_EALIGN, "qmatmul_gemv_swiglu: x must be 16-byte aligned");
-  if (!aligned4(h)) return fail(QM_EALIGN, "qmatmul_gemv_swiglu: h must be 4-byte aligned");
+    return fail(QM_ELAYOUT, "%s: weights must be in DEVICE layout", name);
+  if (w_gate->batch != 1 || w_up->batch != 1) return fail(QM_ESHAPE, "%s: batch must be 1", name);
+  if (w_up->format != w_gate->format) return fail(QM_EFORMAT, "%s: formats differ", name);
+  if (w_up->n != w_gate->n || w_up->k != w_gate->k) return fail(QM_ESHAPE, "%s: gate and up shapes differ", name);
+  if (w_gate->n > INT32_MAX / 2) return fail(QM_ESHAPE, "%s: n too large", name);
+  if (w_gate->n > 0 && (!x || (!h && !h16))) return fail(QM_EINVAL, "%s: null x or h", name);
+  if (!aligned16(x)) return fail(QM_EALIGN, "%s: x must be 16-byte aligned", name);
+  if (!aligned4(h) || !aligned2(h16)) return fail(QM_EALIGN, "%s: h must be 4-byte (fp32) or 2-byte (fp16) aligned", name);
   const DeviceInfo* d;
   if ((st = device_info(&d)) != QM_OK) return st;
   return launched(launch_gemv_swiglu(w_gate->format, static_cast<const uint8_t*>(w_gate->qdata), w_gate->scales,
-                                     static_cast<const uint8_t*>(w_up->qdata), w_up->scales, x, h, w_gate->n,
+                                     static_cast<const uint8_t*>(w_up->qdata), w_up->scales, x, h, h16, w_gate->n,
                                      w_gate->k, d->cu_count, static_cast<hipStream_t>(stream)),
-                  "qmatmul_gemv_swiglu");
+                  name);
+}
+
+}  // namespace
+
+extern "C" {
+
+qm_status qmatmul_gemv_swiglu(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, float* h,
+                              void* stream) {
+  return swiglu_call(w_gate, w_up, x, h, nullptr, stream, "qmatmul_gemv_swiglu");
+}
+
+qm_status qmatmul_gemv_swiglu_f16(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, uint16_t* h,
+                                  void* stream) {
+  return swiglu_call(w_gate, w_up, x, nullptr, h, stream, "qmatmul_gemv_swiglu_f16");
 }
 
 qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_t* const* x, float* const* y,
@@ -317,32 +338,55 @@ qm_status qattn_decode_workspace_bytes(int32_t n_q_heads, int32_t head_dim, size
   return QM_OK;
 }
 
-qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
-                       int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale, float* o,
-                       void* workspace, size_t ws_bytes, void* stream) {
-  if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "qattn_decode: head_dim=%d must be 64 or 128", head_dim);
+}  // extern "C"
+
+namespace {
+
+// Shared checks and launch of decode attention; out is o (fp32) or o16 (fp16).
+qm_status attn_decode_call(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                           int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale, float* o,
+                           uint16_t* o16, void* workspace, size_t ws_bytes, void* stream, const char* name) {
+  if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "%s: head_dim=%d must be 64 or 128", name, head_dim);
   if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads > 1024 || n_q_heads % n_kv_heads != 0 ||
       n_q_heads / n_kv_heads > 8)
-    return fail(QM_ESHAPE, "qattn_decode: n_q_heads=%d must be a multiple of n_kv_heads=%d, at most 8 per KV head",
+    return fail(QM_ESHAPE, "%s: n_q_heads=%d must be a multiple of n_kv_heads=%d, at most 8 per KV head", name,
                 n_q_heads, n_kv_heads);
   if (max_len < 1 || max_len > kAttnMaxLen || len < 1 || len > max_len)
-    return fail(QM_ESHAPE, "qattn_decode: need 1 <= len <= max_len <= %lld (len=%lld, max_len=%lld)",
+    return fail(QM_ESHAPE, "%s: need 1 <= len <= max_len <= %lld (len=%lld, max_len=%lld)", name,
                 (long long)kAttnMaxLen, (long long)len, (long long)max_len);
   if (!(scale == scale) || scale == INFINITY || scale == -INFINITY)
-    return fail(QM_EINVAL, "qattn_decode: scale must be finite");
-  if (!q || !k_cache || !v_cache || !o) return fail(QM_EINVAL, "qattn_decode: null pointer");
-  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(o))
-    return fail(QM_EALIGN, "qattn_decode: q, k_cache, v_cache must be 16-byte aligned, o 4-byte aligned");
+    return fail(QM_EINVAL, "%s: scale must be finite", name);
+  if (!q || !k_cache || !v_cache || (!o && !o16)) return fail(QM_EINVAL, "%s: null pointer", name);
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(o) || !aligned2(o16))
+    return fail(QM_EALIGN, "%s: q, k_cache, v_cache must be 16-byte aligned, o 4-byte aligned", name);
   const size_t need = attn_decode_workspace_bytes(n_q_heads, head_dim);
   if (!workspace || ws_bytes < need)
-    return fail(QM_EWORKSPACE, "qattn_decode: workspace of %zu bytes needed (got %zu)", need, ws_bytes);
-  if (!aligned16(workspace)) return fail(QM_EALIGN, "qattn_decode: workspace must be 16-byte aligned");
+    return fail(QM_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", name, need, ws_bytes);
+  if (!aligned16(workspace)) return fail(QM_EALIGN, "%s: workspace must be 16-byte aligned", name);
   const DeviceInfo* d;
   qm_status st;
   if ((st = device_info(&d)) != QM_OK) return st;
-  return launched(launch_attn_decode(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, len, max_len, scale, o,
+  return launched(launch_attn_decode(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, len, max_len, scale, o, o16,
                                      static_cast<float*>(workspace), d->cu_count, static_cast<hipStream_t>(stream)),
-                  "qattn_decode");
+                  name);
+}
+
+}  // namespace
+
+extern "C" {
+
+qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                       int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale, float* o,
+                       void* workspace, size_t ws_bytes, void* stream) {
+  return attn_decode_call(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, len, max_len, scale, o, nullptr,
+                          workspace, ws_bytes, stream, "qattn_decode");
+}
+
+qm_status qattn_decode_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                           int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale,
+                           uint16_t* o, void* workspace, size_t ws_bytes, void* stream) {
+  return attn_decode_call(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, len, max_len, scale, nullptr, o,
+                          workspace, ws_bytes, stream, "qattn_decode_f16");
 }
 
 qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,

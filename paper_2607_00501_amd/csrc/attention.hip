@@ -45,11 +45,22 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Output element i: fp32 into o, or, when o16 is set, fp16 (round to
+// nearest even) into o16.
+__device__ __forceinline__ void store_out(float* o, uint16_t* o16, int64_t i, float v) {
+  if (o16) {
+    const _Float16 h = static_cast<_Float16>(v);
+    o16[i] = __builtin_bit_cast(uint16_t, h);
+  } else {
+    o[i] = v;
+  }
+}
+
 template <int D, int G>
 __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     int64_t len, int64_t max_len, int tc, int nsplit, float scale_log2, float* __restrict__ ws,
-    float* __restrict__ o) {
+    float* __restrict__ o, uint16_t* __restrict__ o16) {
   constexpr int LPR = D / 8;                 // lanes per cache row
   constexpr int RPW = 64 / LPR;              // rows per wavefront load
   constexpr int RPI = kAttnWaves * RPW;      // rows per workgroup load
@@ -180,13 +191,13 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
       for (int i = 0; i < 8; ++i) part[wave][j][sub * 8 + i] = acc[j][i];
   }
   __syncthreads();
-  if (o) {   // a single slice covers the whole cache: normalise and write the output
+  if (o || o16) {   // a single slice covers the whole cache: normalise and write the output
     for (int e = threadIdx.x; e < G * D; e += kAttnWaves * 64) {
       const int j = e / D, d = e % D;
       float a = part[0][j][d];
 #pragma unroll
       for (int w2 = 1; w2 < kAttnWaves; ++w2) a += part[w2][j][d];
-      o[(static_cast<int64_t>(g) * G + j) * D + d] = a / stat[j][1];
+      store_out(o, o16, (static_cast<int64_t>(g) * G + j) * D + d, a / stat[j][1]);
     }
     return;
   }
@@ -211,7 +222,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
 // slice.
 template <int D>
 __global__ __launch_bounds__(D) void attn_decode_combine_kernel(const float* __restrict__ ws, int nsplit,
-                                                                 float* __restrict__ o) {
+                                                                 float* __restrict__ o, uint16_t* __restrict__ o16) {
   __shared__ float wt[kAttnMaxSplits];
   __shared__ float red[2][D / 64];
   const int h = blockIdx.x, d = threadIdx.x, lane = d & 63, wv = d >> 6;
@@ -251,33 +262,36 @@ __global__ __launch_bounds__(D) void attn_decode_combine_kernel(const float* __r
   float a = 0.0f;
 #pragma unroll 8
   for (int i = 0; i < nsplit; ++i) a = fmaf(wt[i], base[i * (D + 2) + d], a);
-  o[static_cast<int64_t>(h) * D + d] = a / L;
+  store_out(o, o16, static_cast<int64_t>(h) * D + d, a / L);
 }
 
 template <int D, int G>
 hipError_t launch_decode_dg(const uint16_t* q, const uint16_t* k, const uint16_t* v, int hkv, int64_t len,
-                            int64_t max_len, float scale, float* o, float* ws, const AttnPlan& p, hipStream_t st) {
+                            int64_t max_len, float scale, float* o, uint16_t* o16, float* ws, const AttnPlan& p,
+                            hipStream_t st) {
   const size_t lds = static_cast<size_t>(G) * p.tc * sizeof(float);
   hipLaunchKernelGGL((attn_decode_split_kernel<D, G>), dim3(p.nsplit, hkv), dim3(kAttnWaves * 64), lds, st, q, k, v,
-                     len, max_len, p.tc, p.nsplit, scale * 1.4426950408889634f, ws, p.nsplit == 1 ? o : nullptr);
+                     len, max_len, p.tc, p.nsplit, scale * 1.4426950408889634f, ws, p.nsplit == 1 ? o : nullptr,
+                     p.nsplit == 1 ? o16 : nullptr);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.nsplit == 1) return e;
-  hipLaunchKernelGGL((attn_decode_combine_kernel<D>), dim3(hkv * G), dim3(D), 0, st, ws, p.nsplit, o);
+  hipLaunchKernelGGL((attn_decode_combine_kernel<D>), dim3(hkv * G), dim3(D), 0, st, ws, p.nsplit, o, o16);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_decode_d(int group, const uint16_t* q, const uint16_t* k, const uint16_t* v, int hkv, int64_t len,
-                           int64_t max_len, float scale, float* o, float* ws, const AttnPlan& p, hipStream_t st) {
+                           int64_t max_len, float scale, float* o, uint16_t* o16, float* ws, const AttnPlan& p,
+                            hipStream_t st) {
   switch (group) {
-    case 1: return launch_decode_dg<D, 1>(q, k, v, hkv, len, max_len, scale, o, ws, p, st);
-    case 2: return launch_decode_dg<D, 2>(q, k, v, hkv, len, max_len, scale, o, ws, p, st);
-    case 3: return launch_decode_dg<D, 3>(q, k, v, hkv, len, max_len, scale, o, ws, p, st);
-    case 4: return launch_decode_dg<D, 4>(q, k, v, hkv, len, max_len, scale, o, ws, p, st);
-    case 5: return launch_decode_dg<D, 5>(q, k, v, hkv, len, max_len, scale, o, ws, p, st);
-    case 6: return launch_decode_dg<D, 6>(q, k, v, hkv, len, max_len, scale, o, ws, p, st);
-    case 7: return launch_decode_dg<D, 7>(q, k, v, hkv, len, max_len, scale, o, ws, p, st);
-    default: return launch_decode_dg<D, 8>(q, k, v, hkv, len, max_len, scale, o, ws, p, st);
+    case 1: return launch_decode_dg<D, 1>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 2: return launch_decode_dg<D, 2>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 3: return launch_decode_dg<D, 3>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 4: return launch_decode_dg<D, 4>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 5: return launch_decode_dg<D, 5>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 6: return launch_decode_dg<D, 6>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 7: return launch_decode_dg<D, 7>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    default: return launch_decode_dg<D, 8>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
   }
 }
 
@@ -538,12 +552,12 @@ size_t attn_decode_workspace_bytes(int32_t hq, int32_t d) {
 }
 
 hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
-                              int32_t d, int64_t len, int64_t max_len, float scale, float* o, float* ws,
-                              int cu_count, hipStream_t st) {
+                              int32_t d, int64_t len, int64_t max_len, float scale, float* o, uint16_t* o16,
+                              float* ws, int cu_count, hipStream_t st) {
   const int group = hq / hkv;
   const AttnPlan p = attn_decode_plan(hkv, group, len, cu_count);
-  return d == 64 ? launch_decode_d<64>(group, q, k, v, hkv, len, max_len, scale, o, ws, p, st)
-                 : launch_decode_d<128>(group, q, k, v, hkv, len, max_len, scale, o, ws, p, st);
+  return d == 64 ? launch_decode_d<64>(group, q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st)
+                 : launch_decode_d<128>(group, q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
 }
 
 }  // namespace qm

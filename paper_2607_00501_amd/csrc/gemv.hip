@@ -394,7 +394,8 @@ template <int FMT, int SUBR, int WAVES, bool XLDS, bool SWIGLU = false>
 __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
                                               const uint8_t* __restrict__ q2, const uint16_t* __restrict__ s2,
                                               const uint16_t* __restrict__ x, float* __restrict__ y, int n_rows,
-                                              int groups, int64_t block, int64_t nblocks) {
+                                              int groups, int64_t block, int64_t nblocks,
+                                              uint16_t* __restrict__ y16 = nullptr) {
   constexpr int CL = 64 / SUBR;
   constexpr int NM = SWIGLU ? 2 : 1;                  // matrices
   constexpr int U = kSubU<FMT>;
@@ -469,10 +470,18 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
 #pragma unroll
     for (int off = SUBR; off < 64; off <<= 1) acc[m] += __shfl_xor(acc[m], off);
   auto out = [&](float a, float b) { return SWIGLU ? a / (1.0f + expf(-a)) * b : a; };
+  auto store = [&](int64_t n, float v) {   // y16: fp16 output (round to nearest even) instead of y
+    if (y16) {
+      const _Float16 hv = static_cast<_Float16>(v);
+      y16[n] = __builtin_bit_cast(uint16_t, hv);
+    } else {
+      y[n] = v;
+    }
+  };
   if (WAVES == 1) {
     if (lane < SUBR) {
       const int64_t n = panel * 64 + row;
-      if (n < n_rows) y[n] = out(acc[0], acc[NM - 1]);
+      if (n < n_rows) store(n, out(acc[0], acc[NM - 1]));
     }
     return;
   }
@@ -490,7 +499,7 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
       for (int w = 1; w < WAVES; ++w) t[m] += part[m][w][lane];
     }
     const int64_t n = panel * 64 + row;
-    if (n < n_rows) y[n] = out(t[0], t[NM - 1]);
+    if (n < n_rows) store(n, out(t[0], t[NM - 1]));
   }
 }
 
@@ -512,9 +521,10 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_swiglu_kernel(const uint8_t* 
                                                                  const uint8_t* __restrict__ qu,
                                                                  const uint16_t* __restrict__ su,
                                                                  const uint16_t* __restrict__ x,
-                                                                 float* __restrict__ h, int n_rows, int groups) {
-  asm volatile("" ::"s"(qg), "s"(sg), "s"(qu), "s"(su), "s"(x), "s"(h), "s"(n_rows), "s"(groups));
-  gemv_sub_body<FMT, SUBR, WAVES, XLDS, true>(qg, sg, qu, su, x, h, n_rows, groups, blockIdx.x, gridDim.x);
+                                                                 float* __restrict__ h, int n_rows, int groups,
+                                                                 uint16_t* __restrict__ h16) {
+  asm volatile("" ::"s"(qg), "s"(sg), "s"(qu), "s"(su), "s"(x), "s"(h), "s"(n_rows), "s"(groups), "s"(h16));
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS, true>(qg, sg, qu, su, x, h, n_rows, groups, blockIdx.x, gridDim.x, h16);
 }
 
 // A group of independent GEMVs with one K in one launch: the workgroup
@@ -718,27 +728,27 @@ namespace {
 
 template <int FMT, int SUBR, bool XLDS>
 hipError_t launch_swiglu_rows(const uint8_t* qg, const uint16_t* sg, const uint8_t* qu, const uint16_t* su,
-                              const uint16_t* x, float* h, int64_t n, int groups, hipStream_t st) {
+                              const uint16_t* x, float* h, uint16_t* h16, int64_t n, int groups, hipStream_t st) {
   const dim3 grid(static_cast<unsigned>(padded_rows(n) / SUBR));
   const size_t lds = XLDS ? static_cast<size_t>(groups) * 64 : 0;
   hipLaunchKernelGGL((gemv_swiglu_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, qg, sg, qu, su, x, h,
-                     static_cast<int>(n), groups);
+                     static_cast<int>(n), groups, h16);
   return hipGetLastError();
 }
 
 template <int FMT>
 hipError_t launch_swiglu_fmt(const GemvPlan& plan, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
-                             const uint16_t* su, const uint16_t* x, float* h, int64_t n, int groups,
+                             const uint16_t* su, const uint16_t* x, float* h, uint16_t* h16, int64_t n, int groups,
                              hipStream_t st) {
   switch (plan.subr) {
-    case 4: return plan.xlds ? launch_swiglu_rows<FMT, 4, true>(qg, sg, qu, su, x, h, n, groups, st)
-                             : launch_swiglu_rows<FMT, 4, false>(qg, sg, qu, su, x, h, n, groups, st);
-    case 8: return plan.xlds ? launch_swiglu_rows<FMT, 8, true>(qg, sg, qu, su, x, h, n, groups, st)
-                             : launch_swiglu_rows<FMT, 8, false>(qg, sg, qu, su, x, h, n, groups, st);
-    case 16: return plan.xlds ? launch_swiglu_rows<FMT, 16, true>(qg, sg, qu, su, x, h, n, groups, st)
-                              : launch_swiglu_rows<FMT, 16, false>(qg, sg, qu, su, x, h, n, groups, st);
-    default: return plan.xlds ? launch_swiglu_rows<FMT, 32, true>(qg, sg, qu, su, x, h, n, groups, st)
-                              : launch_swiglu_rows<FMT, 32, false>(qg, sg, qu, su, x, h, n, groups, st);
+    case 4: return plan.xlds ? launch_swiglu_rows<FMT, 4, true>(qg, sg, qu, su, x, h, h16, n, groups, st)
+                             : launch_swiglu_rows<FMT, 4, false>(qg, sg, qu, su, x, h, h16, n, groups, st);
+    case 8: return plan.xlds ? launch_swiglu_rows<FMT, 8, true>(qg, sg, qu, su, x, h, h16, n, groups, st)
+                             : launch_swiglu_rows<FMT, 8, false>(qg, sg, qu, su, x, h, h16, n, groups, st);
+    case 16: return plan.xlds ? launch_swiglu_rows<FMT, 16, true>(qg, sg, qu, su, x, h, h16, n, groups, st)
+                              : launch_swiglu_rows<FMT, 16, false>(qg, sg, qu, su, x, h, h16, n, groups, st);
+    default: return plan.xlds ? launch_swiglu_rows<FMT, 32, true>(qg, sg, qu, su, x, h, h16, n, groups, st)
+                              : launch_swiglu_rows<FMT, 32, false>(qg, sg, qu, su, x, h, h16, n, groups, st);
   }
 }
 
@@ -748,7 +758,7 @@ hipError_t launch_swiglu_fmt(const GemvPlan& plan, const uint8_t* qg, const uint
 // of both matrices); matrices large enough for the panel kernel use 32-row
 // workgroups, 8 wavefronts.
 hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
-                              const uint16_t* su, const uint16_t* x, float* h, int64_t n, int64_t k,
+                              const uint16_t* su, const uint16_t* x, float* h, uint16_t* h16, int64_t n, int64_t k,
                               int cu_count, hipStream_t st) {
   if (n == 0) return hipSuccess;
   GemvPlan plan = gemv_plan(fmt, n, k, cu_count);
@@ -758,7 +768,7 @@ hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg
   }
   const int groups = static_cast<int>(k / kGroup);
   return with_format(fmt, [&](auto f) {
-    return launch_swiglu_fmt<decltype(f)::value>(plan, qg, sg, qu, su, x, h, n, groups, st);
+    return launch_swiglu_fmt<decltype(f)::value>(plan, qg, sg, qu, su, x, h, h16, n, groups, st);
   });
 }
 

@@ -100,8 +100,9 @@ struct GemvGroup {
   int count;
   int groups;                     // K / 32
 };
+// h16 != nullptr: fp16 output into h16 (h unused).
 hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
-                              const uint16_t* su, const uint16_t* x, float* h, int64_t n, int64_t k,
+                              const uint16_t* su, const uint16_t* x, float* h, uint16_t* h16, int64_t n, int64_t k,
                               int cu_count, hipStream_t st);
 hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count, hipStream_t st);
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,
@@ -121,8 +122,8 @@ struct AttnPlan { int tc; int nsplit; };
 AttnPlan attn_decode_plan(int hkv, int group, int64_t len, int cu_count);
 size_t attn_decode_workspace_bytes(int32_t hq, int32_t d);
 hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
-                              int32_t d, int64_t len, int64_t max_len, float scale, float* o, float* ws,
-                              int cu_count, hipStream_t st);
+                              int32_t d, int64_t len, int64_t max_len, float scale, float* o, uint16_t* o16,
+                              float* ws, int cu_count, hipStream_t st);   // o16 != nullptr: fp16 output
 
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,

@@ -62,10 +62,8 @@ class DenseDecoder:
         self.h = torch.zeros(c.hidden, **f16)             # normed input of a projection
         self.q, self.k, self.v = torch.zeros(qd, **f32), torch.zeros(kvd, **f32), torch.zeros(kvd, **f32)
         self.q16 = torch.zeros((c.n_q_heads, c.head_dim), **f16)
-        self.attn = torch.zeros((c.n_q_heads, c.head_dim), **f32)
-        self.attn16 = torch.zeros(qd, **f16)
+        self.attn16 = torch.zeros((c.n_q_heads, c.head_dim), **f16)
         self.y_attn = torch.zeros(c.hidden, **f32)
-        self.g = torch.zeros(c.inter, **f32)
         self.g16 = torch.zeros(c.inter, **f16)
         self.y_ffn = torch.zeros(c.hidden, **f32)
         self.logits = torch.zeros(c.vocab, **f32)
@@ -88,13 +86,11 @@ class DenseDecoder:
             B.qmatmul_gemv_grouped([ly.wq, ly.wk, ly.wv], [self.h] * 3, [self.q, self.k, self.v], stream=s)
             B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
                                q_out=self.q16, stream=s)
-            B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn,
+            B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,
                            workspace=self.ws, stream=s)
-            B.qdec_cast_f16(self.attn, out=self.attn16, stream=s)
-            B.qmatmul_gemv(ly.wo, self.attn16, out=self.y_attn, stream=s)
+            B.qmatmul_gemv(ly.wo, self.attn16.view(-1), out=self.y_attn, stream=s)
             B.qdec_rmsnorm(self.x, ly.ffn_norm, c.eps, residual=self.y_attn, out=self.h, stream=s)
-            B.qmatmul_gemv_swiglu(ly.wg, ly.wu, self.h, out=self.g, stream=s)
-            B.qdec_cast_f16(self.g, out=self.g16, stream=s)
+            B.qmatmul_gemv_swiglu(ly.wg, ly.wu, self.h, out=self.g16, stream=s)
             B.qmatmul_gemv(ly.wd, self.g16, out=self.y_ffn, stream=s)
         B.qdec_rmsnorm(self.x, self.norm, c.eps, residual=self.y_ffn, out=self.h, stream=s)
         B.qmatmul_gemv(self.lm_head, self.h, out=self.logits, stream=s)

@@ -309,3 +309,16 @@ def test_argmax_workspace_constant_matches_header():
     import re
     hdr = open(os.path.join(os.path.dirname(__file__), "..", "include", "qmatmul.h")).read()
     assert int(re.search(r"#define QDEC_ARGMAX_WORKSPACE_BYTES (\d+)", hdr).group(1)) == B.ARGMAX_WORKSPACE_BYTES
+
+
+def test_fp16_output_variants_validation():
+    L = B.lib()
+    p = ctypes.c_void_p(0x50000)
+    need = B.qattn_decode_workspace_bytes(16, 128)
+    call = lambda o=p, d=128, n=10: L.qattn_decode_f16(p, p, p, 16, 8, d, n, 64, 0.1, o, p, need, None)
+    assert call(o=None) == 1 and call(o=ctypes.c_void_p(0x50001)) == 3 and call(d=80) == 2 and call(n=65) == 2
+    w = B.empty_qweight(B.Q4_G32, B.LAYOUT_DEVICE, 1, 64, 64, device="cpu")
+    assert L.qmatmul_gemv_swiglu_f16(ctypes.byref(w.c()), ctypes.byref(w.c()), p, None, None) == 1
+    assert L.qmatmul_gemv_swiglu_f16(ctypes.byref(w.c()), ctypes.byref(w.c()), p, ctypes.c_void_p(0x50001),
+                                     None) == 3
+    assert B.qm_last_error()

@@ -250,3 +250,29 @@ def test_decode_step_graph_replay_matches_eager():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(dec.logits, eager_logits) and torch.equal(dec.token, eager_tok)
+
+
+# ---------------------------------------------------------------- fp16 outputs
+
+@pytest.mark.parametrize("fmt", [B.Q4_G32, B.Q8_G32, B.Q3_G32])
+@pytest.mark.parametrize("n,k", [(65, 96), (3072, 1024), (8192, 3072), (16448, 256)])
+def test_gemv_swiglu_f16_is_the_rounded_fp32_output(fmt, n, k):
+    w = [B.qm_repack(B.qm_quantise(inputs.weights_dev(inputs.seed_for(31, n, t), (n, k)), fmt), B.LAYOUT_DEVICE)
+         for t in ("gate", "up")]
+    x = inputs.activations_dev(inputs.seed_for(31, n, "x"), (k,))
+    h32 = B.qmatmul_gemv_swiglu(w[0], w[1], x)
+    h16 = B.qmatmul_gemv_swiglu(w[0], w[1], x, out=torch.empty(n, dtype=torch.float16, device="cuda"))
+    assert torch.equal(h16, h32.half())
+
+
+@pytest.mark.parametrize("d,hq,hkv", [(64, 32, 8), (128, 16, 8), (128, 24, 8)])
+@pytest.mark.parametrize("length", [1, 100, 128, 129, 3000])
+def test_attention_decode_f16_is_the_rounded_fp32_output(d, hq, hkv, length):
+    max_len = 4096
+    q = inputs.activations_dev(inputs.seed_for(32, length, "q"), (hq, d))
+    kc = inputs.activations_dev(inputs.seed_for(32, length, "k"), (hkv, max_len, d))
+    vc = inputs.activations_dev(inputs.seed_for(32, length, "v"), (hkv, max_len, d))
+    o32 = B.qattn_decode(q, kc, vc, length, 1 / math.sqrt(d))
+    o16 = B.qattn_decode(q, kc, vc, length, 1 / math.sqrt(d), out=torch.empty((hq, d), dtype=torch.float16,
+                                                                              device="cuda"))
+    assert torch.equal(o16, o32.half())
