@@ -267,6 +267,8 @@ def cpu_baseline(budget_s: float):
 def extra_workloads(torch, B, inputs, workloads, steps, warmup, which="all"):
     out = {}
     lib = B.lib()
+    if which in ("all", "tg"):
+        out.update(extra_tg(torch, B, inputs, workloads, steps, warmup, lib))
     if which in ("all", "decode"):
         out.update(extra_decode(torch, B, inputs, workloads, steps, warmup, lib))
     if which in ("all", "prefill"):
@@ -328,6 +330,26 @@ def tg_tokens_per_s(torch, dec, tokens: int, reps: int):
     return tokens * reps / t, t / reps
 
 
+def extra_tg(torch, B, inputs, workloads, steps, warmup, lib):
+    out = {}
+    # End-to-end decode, tg128 (Sec. 4.1): every kernel of a token (embedding,
+    # norms, projections, RoPE and cache append, attention, SwiGLU, LM head,
+    # greedy sampling): 8 launches per layer (attention is one launch for
+    # caches of up to 128 rows) + 5.
+    for model, cfg_id in ((workloads.QWEN3_06B_DECODER, 1), (workloads.LLAMA32_1B_DECODER, 3),
+                          (workloads.LLAMA32_3B_DECODER, 2)):
+        dec = build_decoder(model, cfg_id, B.Q4_G32, 128, torch, B, inputs)
+        tps, t = tg_tokens_per_s(torch, dec, 128, 3)
+        key = model["name"] + "_tg128_q4"
+        out[key] = {"tokens_per_s": round(tps, 1), "ms_per_token": round(1e3 / tps, 4),
+                    "launches_per_token": 8 * model["layers"] + 5, "ms_per_128_tokens": round(t * 1e3, 3)}
+        log(f"{key}: {out[key]}")
+        del dec
+        torch.cuda.empty_cache()
+
+    return out
+
+
 def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
     out = {}
 
@@ -363,21 +385,6 @@ def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
             log(f"{tag} {key}: {out[f'{tag}_decode_q4_{key}']}")
             del g, calls
             torch.cuda.empty_cache()
-
-    # End-to-end decode, tg128 (Sec. 4.1): every kernel of a token (embedding,
-    # norms, projections, RoPE and cache append, attention, SwiGLU, LM head,
-    # greedy sampling): 8 launches per layer (attention is one launch for
-    # caches of up to 128 rows) + 5.
-    for model, cfg_id in ((workloads.QWEN3_06B_DECODER, 1), (workloads.LLAMA32_1B_DECODER, 3),
-                          (workloads.LLAMA32_3B_DECODER, 2)):
-        dec = build_decoder(model, cfg_id, B.Q4_G32, 128, torch, B, inputs)
-        tps, t = tg_tokens_per_s(torch, dec, 128, 3)
-        key = model["name"] + "_tg128_q4"
-        out[key] = {"tokens_per_s": round(tps, 1), "ms_per_token": round(1e3 / tps, 4),
-                    "launches_per_token": 8 * model["layers"] + 5, "ms_per_128_tokens": round(t * 1e3, 3)}
-        log(f"{key}: {out[key]}")
-        del dec
-        torch.cuda.empty_cache()
 
     # Llama-3.2-3B decode stacks, Q4 and Q8
     for fmt, tag in ((B.Q4_G32, "q4"), (B.Q8_G32, "q8")):
@@ -663,7 +670,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--extra", choices=["all", "none", "decode", "prefill", "moe"], default="all",
+    ap.add_argument("--extra", choices=["all", "none", "tg", "decode", "prefill", "moe"], default="all",
                     help="other workloads to time after the headline step (subsets for profiling)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     args = ap.parse_args()

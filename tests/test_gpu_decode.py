@@ -24,7 +24,10 @@ def _f16_bits(a):
 
 # ---------------------------------------------------------------- glue kernels
 
-@pytest.mark.parametrize("rows,hidden", [(1, 1), (1, 96), (3, 1000), (1, 1024), (2, 4096), (1, 8192)])
+# 16-byte-load tiles (hidden % 4 == 0, up to 8192), scalar register tiles
+# (1026, 3002), and the two-pass loop (10000 is beyond the tiles, 12290 odd).
+@pytest.mark.parametrize("rows,hidden", [(1, 1), (1, 96), (3, 1000), (1, 1024), (2, 4096), (1, 8192), (1, 1026),
+                                         (2, 3002), (1, 10000), (1, 12290)])
 @pytest.mark.parametrize("with_residual", [False, True])
 def test_rmsnorm_parity(rows, hidden, with_residual):
     rng = np.random.default_rng(rows * 7 + hidden)
@@ -42,6 +45,21 @@ def test_rmsnorm_parity(rows, hidden, with_residual):
         # at most one fp16 ulp away from the rounded oracle value
         diff = np.abs(_f16_bits(out[i]).astype(np.int32) - _f16_bits(O.f16(ref)).astype(np.int32))
         assert diff.max() <= 1
+
+
+def test_rmsnorm_unaligned_row_uses_scalar_loads():
+    """x starting 4 bytes into an allocation (not 16-byte aligned) gives the
+    same result as an aligned copy."""
+    rng = np.random.default_rng(3)
+    big = torch.from_numpy(rng.standard_normal(2049).astype(np.float32)).cuda()
+    res = torch.from_numpy(rng.standard_normal(2048).astype(np.float32)).cuda()
+    w = torch.from_numpy(inputs.norm_weights_np(77, 2048)).cuda()
+    x_un = big[1:]
+    x_al = x_un.clone()
+    a = B.qdec_rmsnorm(x_un, w, 1e-6, residual=res)
+    b = B.qdec_rmsnorm(x_al, w, 1e-6, residual=res)
+    assert torch.equal(x_un, x_al)
+    assert (a.float() - b.float()).abs().max().item() <= 2.0 ** -10 * b.float().abs().max().item()
 
 
 def test_rmsnorm_zero_rows_and_zero_vector():
