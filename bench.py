@@ -334,15 +334,16 @@ def extra_tg(torch, B, inputs, workloads, steps, warmup, lib):
     out = {}
     # End-to-end decode, tg128 (Sec. 4.1): every kernel of a token (embedding,
     # norms, projections, RoPE and cache append, attention, SwiGLU, LM head,
-    # greedy sampling): 8 launches per layer (attention is one launch for
-    # caches of up to 128 rows) + 5.
+    # greedy sampling): 6 launches per layer (the norms run inside the q/k/v
+    # and gate/up GEMVs; attention is one launch for caches of up to 128
+    # rows) + 5.
     for model, cfg_id in ((workloads.QWEN3_06B_DECODER, 1), (workloads.LLAMA32_1B_DECODER, 3),
                           (workloads.LLAMA32_3B_DECODER, 2)):
         dec = build_decoder(model, cfg_id, B.Q4_G32, 128, torch, B, inputs)
         tps, t = tg_tokens_per_s(torch, dec, 128, 3)
         key = model["name"] + "_tg128_q4"
         out[key] = {"tokens_per_s": round(tps, 1), "ms_per_token": round(1e3 / tps, 4),
-                    "launches_per_token": 8 * model["layers"] + 5, "ms_per_128_tokens": round(t * 1e3, 3)}
+                    "launches_per_token": 6 * model["layers"] + 5, "ms_per_128_tokens": round(t * 1e3, 3)}
         log(f"{key}: {out[key]}")
         del dec
         torch.cuda.empty_cache()

@@ -172,6 +172,26 @@ qm_status qmatmul_gemv_swiglu(const qm_qweight* w_gate, const qm_qweight* w_up, 
 qm_status qmatmul_gemv_swiglu_f16(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, uint16_t* h,
                                   void* stream);
 
+/* RMSNorm folded into the GEMVs that read its output (Sec. 3.3: each fusion
+ * removes a launch; Sec. 3.2: normalisation kernels).  With
+ *   v = x + residual (residual may be NULL: v = x),
+ *   n = fp16_RNE(v / sqrt(mean(v^2) + eps) * gain):
+ * qmatmul_gemv_grouped_rmsnorm: y_i = w_i' n for i < count (the q/k/v
+ * projections of a layer), as qmatmul_gemv_grouped with every x_i = n;
+ * qmatmul_gemv_swiglu_rmsnorm_f16: h = fp16_RNE(silu(Wg' n) * (Wu' n)), as
+ * qmatmul_gemv_swiglu_f16.  Both write v to x_out (fp32 [k]), the residual
+ * stream for the next fused call, which must not overlap x or residual.
+ * x, residual, x_out: fp32 [k], 16-byte aligned; gain: fp16 [k], 8-byte
+ * aligned.  Weights: Q4 or Q8, DEVICE layout, batch 1, one k <= 4096, every
+ * n >= 1.  Every workgroup recomputes n into LDS from x and residual (the
+ * sum of squares in fp32, in the same order in every workgroup); workgroup 0
+ * writes x_out.  One launch each. */
+qm_status qmatmul_gemv_grouped_rmsnorm(int32_t count, const qm_qweight* w, const float* x, const float* residual,
+                                       const uint16_t* gain, float eps, float* x_out, float* const* y, void* stream);
+qm_status qmatmul_gemv_swiglu_rmsnorm_f16(const qm_qweight* w_gate, const qm_qweight* w_up, const float* x,
+                                          const float* residual, const uint16_t* gain, float eps, float* x_out,
+                                          uint16_t* h, void* stream);
+
 /* Grouped decode GEMV (Sec. 3.3: fusing a sequence of operators removes a
  * launch each, which matters most in decode; e.g. the q/k/v projections of
  * a layer, which share x, or its gate and up projections):

@@ -30,7 +30,8 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmoe_workspace_bytes", "qmoe_route",
            "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
            "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
-           "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16")
+           "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
+           "qmatmul_gemv_swiglu_rmsnorm_f16")
 
 
 class QmError(RuntimeError):
@@ -78,6 +79,8 @@ def lib() -> ctypes.CDLL:
             "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp],
             "qdec_embed": [vp, i64, i64, vp, vp, vp],
             "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
+            "qmatmul_gemv_grouped_rmsnorm": [i32, W, vp, vp, vp, ctypes.c_float, vp, ctypes.POINTER(vp), vp],
+            "qmatmul_gemv_swiglu_rmsnorm_f16": [W, W, vp, vp, vp, ctypes.c_float, vp, vp, vp],
             "qattn_decode_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qdec_rmsnorm": [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp],
             "qdec_rope_append": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, vp, vp],
@@ -219,6 +222,42 @@ def qmatmul_gemv_grouped(ws, xs, outs=None, stream=None):
     n, descs, xp, yp = gemv_group_args(ws, xs, outs)
     _check(lib().qmatmul_gemv_grouped(n, descs, xp, yp, _stream(stream)))
     return outs
+
+
+def qmatmul_gemv_grouped_rmsnorm(ws, x: torch.Tensor, gain: torch.Tensor, eps: float, x_out: torch.Tensor,
+                                 residual: Optional[torch.Tensor] = None, outs=None, stream=None):
+    """y_i = W_i' fp16(rmsnorm(x + residual) * gain); x_out = x + residual
+    (fp32 [k]).  Returns the list of fp32 outputs."""
+    k = ws[0].k
+    for t in (x, x_out) + ((residual,) if residual is not None else ()):
+        assert t.dtype == torch.float32 and t.is_contiguous() and t.numel() == k
+    assert gain.dtype == torch.float16 and gain.numel() == k
+    if outs is None:
+        outs = [torch.empty(w.n, dtype=torch.float32, device=x.device) for w in ws]
+    n = len(ws)
+    descs = (CQWeight * n)(*[w.c() for w in ws])
+    yp = (ctypes.c_void_p * n)(*[t.data_ptr() for t in outs])
+    _check(lib().qmatmul_gemv_grouped_rmsnorm(n, descs, _ptr(x), _ptr(residual), _ptr(gain), eps, _ptr(x_out), yp,
+                                              _stream(stream)))
+    return outs
+
+
+def qmatmul_gemv_swiglu_rmsnorm_f16(w_gate: QWeight, w_up: QWeight, x: torch.Tensor, gain: torch.Tensor, eps: float,
+                                    x_out: torch.Tensor, residual: Optional[torch.Tensor] = None,
+                                    out: Optional[torch.Tensor] = None, stream=None):
+    """h = fp16(silu(Wg' n) * (Wu' n)), n = fp16(rmsnorm(x + residual) * gain);
+    x_out = x + residual."""
+    k = w_gate.k
+    for t in (x, x_out) + ((residual,) if residual is not None else ()):
+        assert t.dtype == torch.float32 and t.is_contiguous() and t.numel() == k
+    assert gain.dtype == torch.float16 and gain.numel() == k
+    if out is None:
+        out = torch.empty(w_gate.n, dtype=torch.float16, device=x.device)
+    assert out.dtype == torch.float16 and out.numel() == w_gate.n
+    _check(lib().qmatmul_gemv_swiglu_rmsnorm_f16(ctypes.byref(w_gate.c()), ctypes.byref(w_up.c()), _ptr(x),
+                                                 _ptr(residual), _ptr(gain), eps, _ptr(x_out), _ptr(out),
+                                                 _stream(stream)))
+    return out
 
 
 def qmatmul_gemm(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):

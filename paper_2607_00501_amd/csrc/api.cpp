@@ -225,6 +225,93 @@ qm_status qmatmul_gemv_swiglu_f16(const qm_qweight* w_gate, const qm_qweight* w_
   return swiglu_call(w_gate, w_up, x, nullptr, h, stream, "qmatmul_gemv_swiglu_f16");
 }
 
+}  // extern "C"
+
+namespace {
+
+// Checks of the fused-RMSNorm inputs shared by the two fused entry points.
+qm_status check_norm(const float* x, const float* residual, const uint16_t* gain, float eps, const float* x_out,
+                     int64_t k, const char* name) {
+  if (k > kNormGemvMaxK) return fail(QM_ESHAPE, "%s: k=%lld must be <= %lld", name, (long long)k,
+                                     (long long)kNormGemvMaxK);
+  if (!(eps >= 0.0f) || eps == INFINITY) return fail(QM_EINVAL, "%s: eps must be finite and >= 0", name);
+  if (!x || !gain || !x_out) return fail(QM_EINVAL, "%s: null x, gain or x_out", name);
+  if (!aligned16(x) || !aligned16(residual) || !aligned16(x_out) ||
+      (reinterpret_cast<uintptr_t>(gain) & 7u) != 0)
+    return fail(QM_EALIGN, "%s: x, residual and x_out must be 16-byte aligned, gain 8-byte aligned", name);
+  const uintptr_t o0 = reinterpret_cast<uintptr_t>(x_out), o1 = o0 + static_cast<uintptr_t>(k) * 4;
+  auto overlaps = [&](const void* p) {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(p), a1 = a0 + static_cast<uintptr_t>(k) * 4;
+    return p && a0 < o1 && o0 < a1;
+  };
+  if (overlaps(x) || overlaps(residual)) return fail(QM_EINVAL, "%s: x_out must not overlap x or residual", name);
+  return QM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+qm_status qmatmul_gemv_grouped_rmsnorm(int32_t count, const qm_qweight* w, const float* x, const float* residual,
+                                       const uint16_t* gain, float eps, float* x_out, float* const* y,
+                                       void* stream) {
+  const char* name = "qmatmul_gemv_grouped_rmsnorm";
+  if (count < 1 || count > QM_GEMV_GROUP_MAX)
+    return fail(QM_ESHAPE, "%s: count=%d must be in [1, %d]", name, count, QM_GEMV_GROUP_MAX);
+  if (!w || !y) return fail(QM_EINVAL, "%s: null array", name);
+  GemvGroup g{};
+  g.count = count;
+  for (int i = 0; i < count; ++i) {
+    qm_status st = check_weight(&w[i], "qmatmul_gemv_grouped_rmsnorm(w[i])");
+    if (st != QM_OK) return st;
+    if (w[i].format != QM_Q4_G32 && w[i].format != QM_Q8_G32) return fail(QM_EFORMAT, "%s: Q4 or Q8 only", name);
+    if (w[i].layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "%s: w[%d] must be in DEVICE layout", name, i);
+    if (w[i].batch != 1) return fail(QM_ESHAPE, "%s: w[%d] batch must be 1", name, i);
+    if (w[i].format != w[0].format) return fail(QM_EFORMAT, "%s: formats differ", name);
+    if (w[i].k != w[0].k) return fail(QM_ESHAPE, "%s: k differs between entries", name);
+    if (w[i].n < 1 || w[i].n > INT32_MAX / 2) return fail(QM_ESHAPE, "%s: n of w[%d] must be in [1, 2^30]", name, i);
+    if (!y[i]) return fail(QM_EINVAL, "%s: null y[%d]", name, i);
+    if (!aligned4(y[i])) return fail(QM_EALIGN, "%s: y[%d] must be 4-byte aligned", name, i);
+    g.q[i] = static_cast<const uint8_t*>(w[i].qdata);
+    g.s[i] = w[i].scales;
+    g.y[i] = y[i];
+    g.n[i] = static_cast<int>(w[i].n);
+  }
+  qm_status st = check_norm(x, residual, gain, eps, x_out, w[0].k, name);
+  if (st != QM_OK) return st;
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  const NormArgs na{x, residual, gain, x_out, eps};
+  return launched(launch_gemv_group_norm(w[0].format, g, na, w[0].k, d->cu_count, static_cast<hipStream_t>(stream)),
+                  name);
+}
+
+qm_status qmatmul_gemv_swiglu_rmsnorm_f16(const qm_qweight* w_gate, const qm_qweight* w_up, const float* x,
+                                          const float* residual, const uint16_t* gain, float eps, float* x_out,
+                                          uint16_t* h, void* stream) {
+  const char* name = "qmatmul_gemv_swiglu_rmsnorm_f16";
+  qm_status st = check_weight(w_gate, "qmatmul_gemv_swiglu_rmsnorm_f16(w_gate)");
+  if (st != QM_OK) return st;
+  if ((st = check_weight(w_up, "qmatmul_gemv_swiglu_rmsnorm_f16(w_up)")) != QM_OK) return st;
+  if (w_gate->format != QM_Q4_G32 && w_gate->format != QM_Q8_G32) return fail(QM_EFORMAT, "%s: Q4 or Q8 only", name);
+  if (w_gate->layout != QM_LAYOUT_DEVICE || w_up->layout != QM_LAYOUT_DEVICE)
+    return fail(QM_ELAYOUT, "%s: weights must be in DEVICE layout", name);
+  if (w_gate->batch != 1 || w_up->batch != 1) return fail(QM_ESHAPE, "%s: batch must be 1", name);
+  if (w_up->format != w_gate->format) return fail(QM_EFORMAT, "%s: formats differ", name);
+  if (w_up->n != w_gate->n || w_up->k != w_gate->k) return fail(QM_ESHAPE, "%s: gate and up shapes differ", name);
+  if (w_gate->n < 1 || w_gate->n > INT32_MAX / 2) return fail(QM_ESHAPE, "%s: n must be in [1, 2^30]", name);
+  if (!h) return fail(QM_EINVAL, "%s: null h", name);
+  if (!aligned2(h)) return fail(QM_EALIGN, "%s: h must be 2-byte aligned", name);
+  if ((st = check_norm(x, residual, gain, eps, x_out, w_gate->k, name)) != QM_OK) return st;
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  const NormArgs na{x, residual, gain, x_out, eps};
+  return launched(launch_gemv_swiglu_norm(w_gate->format, static_cast<const uint8_t*>(w_gate->qdata), w_gate->scales,
+                                          static_cast<const uint8_t*>(w_up->qdata), w_up->scales, na, nullptr, h,
+                                          w_gate->n, w_gate->k, d->cu_count, static_cast<hipStream_t>(stream)),
+                  name);
+}
+
 qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_t* const* x, float* const* y,
                                void* stream) {
   static_assert(QM_GEMV_GROUP_MAX == kGemvGroupMax, "group size");

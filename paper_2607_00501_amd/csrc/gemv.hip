@@ -390,12 +390,74 @@ template <int FMT> constexpr int kSubU = fmt_float(FMT) ? 4 : 8;
 // SWIGLU: the same rows of a second matrix (q2, s2) go through the same
 // loads-then-dots pass, and the workgroup writes silu(a) * b of the two
 // row sums a, b (the SwiGLU front half of a feed-forward block).
-template <int FMT, int SUBR, int WAVES, bool XLDS, bool SWIGLU = false>
+// The normed activation of a fused RMSNorm, built by every workgroup in LDS
+// (xs, fp16, K = 32 * groups <= 4096): v = x + res with 16-byte loads, the
+// sum of squares reduced over the workgroup in a fixed order (so every
+// workgroup gets the same bits), fp16_RNE(v * inv * w); `write` also stores v
+// to x_out.
+template <int WAVES>
+__device__ __forceinline__ void stage_rmsnorm(const NormArgs& na, int groups, uint4* xs, bool write) {
+  constexpr int T = WAVES * 64;
+  constexpr int P = (static_cast<int>(kNormGemvMaxK) / 4 + T - 1) / T;   // float4s per thread
+  __shared__ float red[WAVES];
+  const int n4 = groups * 8;
+  const float4* x4 = reinterpret_cast<const float4*>(na.x);
+  const float4* r4 = reinterpret_cast<const float4*>(na.res);
+  const uint2* w4 = reinterpret_cast<const uint2*>(na.w);
+  float4 v[P], r[P];
+  uint2 g[P];
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int i = threadIdx.x + j * T;
+    const bool ok = i < n4;
+    v[j] = ok ? x4[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    g[j] = ok ? w4[i] : make_uint2(0u, 0u);
+    r[j] = r4 && ok ? r4[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    v[j].x += r[j].x; v[j].y += r[j].y; v[j].z += r[j].z; v[j].w += r[j].w;
+    ss = fmaf(v[j].x, v[j].x, ss);
+    ss = fmaf(v[j].y, v[j].y, ss);
+    ss = fmaf(v[j].z, v[j].z, ss);
+    ss = fmaf(v[j].w, v[j].w, ss);
+  }
+  if (write) {
+    float4* o4 = reinterpret_cast<float4*>(na.x_out);
+#pragma unroll
+    for (int j = 0; j < P; ++j)
+      if (threadIdx.x + j * T < n4) o4[threadIdx.x + j * T] = v[j];
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  ss = red[0];
+#pragma unroll
+  for (int w = 1; w < WAVES; ++w) ss += red[w];
+  const float inv = 1.0f / sqrtf(ss / static_cast<float>(groups * 32) + na.eps);
+  uint2* xh = reinterpret_cast<uint2*>(xs);
+  auto h = [](float f) { const _Float16 t = static_cast<_Float16>(f); return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, t)); };
+  auto gf = [](uint32_t b) { return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(b))); };
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int i = threadIdx.x + j * T;
+    if (i < n4) {
+      const uint32_t a = h(v[j].x * inv * gf(g[j].x & 0xffffu)) | h(v[j].y * inv * gf(g[j].x >> 16)) << 16;
+      const uint32_t b = h(v[j].z * inv * gf(g[j].y & 0xffffu)) | h(v[j].w * inv * gf(g[j].y >> 16)) << 16;
+      xh[i] = make_uint2(a, b);
+    }
+  }
+}
+
+template <int FMT, int SUBR, int WAVES, bool XLDS, bool SWIGLU = false, bool NORM = false>
 __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
                                               const uint8_t* __restrict__ q2, const uint16_t* __restrict__ s2,
                                               const uint16_t* __restrict__ x, float* __restrict__ y, int n_rows,
                                               int groups, int64_t block, int64_t nblocks,
-                                              uint16_t* __restrict__ y16 = nullptr) {
+                                              uint16_t* __restrict__ y16 = nullptr,
+                                              const NormArgs* na = nullptr) {
   constexpr int CL = 64 / SUBR;
   constexpr int NM = SWIGLU ? 2 : 1;                  // matrices
   constexpr int U = kSubU<FMT>;
@@ -439,7 +501,11 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
       }
     }
     if (XLDS && it == 0) {
-      for (int i = threadIdx.x; i < groups * 4; i += WAVES * 64) xs[i] = xg[i];
+      if constexpr (NORM) {
+        stage_rmsnorm<WAVES>(*na, groups, xs, blockIdx.x == 0);
+      } else {
+        for (int i = threadIdx.x; i < groups * 4; i += WAVES * 64) xs[i] = xg[i];
+      }
       __syncthreads();
     }
 #pragma unroll
@@ -527,6 +593,19 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_swiglu_kernel(const uint8_t* 
   gemv_sub_body<FMT, SUBR, WAVES, XLDS, true>(qg, sg, qu, su, x, h, n_rows, groups, blockIdx.x, gridDim.x, h16);
 }
 
+// The SwiGLU pair with the RMSNorm of its input folded in.
+template <int FMT, int SUBR>
+__global__ __launch_bounds__(512) void gemv_swiglu_norm_kernel(const uint8_t* __restrict__ qg,
+                                                               const uint16_t* __restrict__ sg,
+                                                               const uint8_t* __restrict__ qu,
+                                                               const uint16_t* __restrict__ su, NormArgs na,
+                                                               float* __restrict__ h, uint16_t* __restrict__ h16,
+                                                               int n_rows, int groups) {
+  asm volatile("" ::"s"(qg), "s"(sg), "s"(qu), "s"(su), "s"(h), "s"(n_rows), "s"(groups), "s"(h16));
+  gemv_sub_body<FMT, SUBR, 8, true, true, true>(qg, sg, qu, su, nullptr, h, n_rows, groups, blockIdx.x, gridDim.x,
+                                                h16, &na);
+}
+
 // A group of independent GEMVs with one K in one launch: the workgroup
 // ranges of the matrices follow each other (each but the last rounded up to
 // a multiple of 8, so every matrix starts on XCD 0 and keeps the XCD
@@ -559,6 +638,33 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_sub_group_kernel(GemvGroup g)
   const int64_t nb = padded_rows(n) / SUBR;
   if (local >= nb) return;                             // padding workgroup (whole group exits)
   gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, nullptr, nullptr, x, y, n, groups, local, nb);
+}
+
+// The grouped GEMV with the RMSNorm of the shared input folded in (8
+// wavefronts, activation in LDS).
+template <int FMT, int SUBR>
+__global__ __launch_bounds__(512) void gemv_sub_group_norm_kernel(GemvGroup g, NormArgs na) {
+  const int b = static_cast<int>(blockIdx.x);
+  const uint8_t* q = g.q[0];
+  const uint16_t* s = g.s[0];
+  float* y = g.y[0];
+  int n = g.n[0], first = 0;
+#pragma unroll
+  for (int j = 1; j < kGemvGroupMax; ++j) {
+    const bool in = j < g.count && b >= g.start[j];
+    q = in ? g.q[j] : q;
+    s = in ? g.s[j] : s;
+    y = in ? g.y[j] : y;
+    n = in ? g.n[j] : n;
+    first = in ? g.start[j] : first;
+  }
+  int groups = g.groups;
+  asm volatile("" ::"s"(q), "s"(s), "s"(y), "s"(n), "s"(first), "s"(groups));
+  const int64_t local = b - first;
+  const int64_t nb = padded_rows(n) / SUBR;
+  if (local >= nb) return;                             // padding workgroup (never workgroup 0)
+  gemv_sub_body<FMT, SUBR, 8, true, false, true>(q, s, nullptr, nullptr, nullptr, y, n, groups, local, nb, nullptr,
+                                                 &na);
 }
 
 template <int FMT, int SUBR, bool XLDS>
@@ -770,6 +876,67 @@ hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg
   return with_format(fmt, [&](auto f) {
     return launch_swiglu_fmt<decltype(f)::value>(plan, qg, sg, qu, su, x, h, h16, n, groups, st);
   });
+}
+
+// Fused RMSNorm + GEMVs: the sub-panel plan of the rows (32-row workgroups
+// where the plan would take the panel kernel), always 8 wavefronts with the
+// activation in LDS.
+static int norm_subr(int32_t fmt, int64_t rows, int64_t k, int cu_count) {
+  const GemvPlan plan = gemv_plan(fmt, rows, k, cu_count);
+  return plan.subr == kPanel ? 32 : plan.subr;
+}
+
+hipError_t launch_gemv_group_norm(int32_t fmt, GemvGroup& g, const NormArgs& na, int64_t k, int cu_count,
+                                  hipStream_t st) {
+  int64_t rows = 0;
+  for (int i = 0; i < g.count; ++i) rows += padded_rows(g.n[i]);
+  const int subr = norm_subr(fmt, rows, k, cu_count);
+  g.groups = static_cast<int>(k / kGroup);
+  int start = 0;
+  for (int i = 0; i < g.count; ++i) {
+    g.start[i] = start;
+    const int nb = static_cast<int>(padded_rows(g.n[i]) / subr);
+    start += i + 1 < g.count ? (nb + kXcds - 1) / kXcds * kXcds : nb;
+  }
+  g.start[g.count] = start;
+  const dim3 grid(static_cast<unsigned>(start));
+  const size_t lds = static_cast<size_t>(g.groups) * 64;
+  auto go = [&](auto f) -> hipError_t {
+    constexpr int F = decltype(f)::value;
+    switch (subr) {
+      case 4: hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, 4>), grid, dim3(512), lds, st, g, na); break;
+      case 8: hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, 8>), grid, dim3(512), lds, st, g, na); break;
+      case 16: hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, 16>), grid, dim3(512), lds, st, g, na); break;
+      default: hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, 32>), grid, dim3(512), lds, st, g, na); break;
+    }
+    return hipGetLastError();
+  };
+  if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
+  if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemv_swiglu_norm(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
+                                   const uint16_t* su, const NormArgs& na, float* h, uint16_t* h16, int64_t n,
+                                   int64_t k, int cu_count, hipStream_t st) {
+  const int subr = norm_subr(fmt, n, k, cu_count);
+  const int groups = static_cast<int>(k / kGroup);
+  const dim3 grid(static_cast<unsigned>(padded_rows(n) / subr));
+  const size_t lds = static_cast<size_t>(groups) * 64;
+  const int ni = static_cast<int>(n);
+  auto go = [&](auto f) -> hipError_t {
+    constexpr int F = decltype(f)::value;
+    switch (subr) {
+      case 4: hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, 4>), grid, dim3(512), lds, st, qg, sg, qu, su, na, h, h16, ni, groups); break;
+      case 8: hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, 8>), grid, dim3(512), lds, st, qg, sg, qu, su, na, h, h16, ni, groups); break;
+      case 16: hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, 16>), grid, dim3(512), lds, st, qg, sg, qu, su, na, h, h16, ni, groups); break;
+      default: hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, 32>), grid, dim3(512), lds, st, qg, sg, qu, su, na, h, h16, ni, groups); break;
+    }
+    return hipGetLastError();
+  };
+  if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
+  if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,

@@ -101,6 +101,22 @@ struct GemvGroup {
   int groups;                     // K / 32
 };
 // h16 != nullptr: fp16 output into h16 (h unused).
+// RMSNorm folded into the GEMVs that consume it: every workgroup forms
+// v = x + res (res optional), fp16_RNE(v / rms(v) * w) into LDS as its
+// activation, and workgroup 0 writes v to x_out.  Q4 and Q8, K <= 4096.
+struct NormArgs {
+  const float* x;
+  const float* res;
+  const uint16_t* w;
+  float* x_out;
+  float eps;
+};
+constexpr int64_t kNormGemvMaxK = 4096;
+hipError_t launch_gemv_group_norm(int32_t fmt, GemvGroup& g, const NormArgs& na, int64_t k, int cu_count,
+                                  hipStream_t st);
+hipError_t launch_gemv_swiglu_norm(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
+                                   const uint16_t* su, const NormArgs& na, float* h, uint16_t* h16, int64_t n,
+                                   int64_t k, int cu_count, hipStream_t st);
 hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
                               const uint16_t* su, const uint16_t* x, float* h, uint16_t* h16, int64_t n, int64_t k,
                               int cu_count, hipStream_t st);

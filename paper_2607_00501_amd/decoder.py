@@ -47,10 +47,15 @@ class LayerWeights:
 
 class DenseDecoder:
     """Buffers and call order of one decode step.  Weights: device-layout
-    quantised projections, fp16 embedding table and norm weights."""
+    quantised projections, fp16 embedding table and norm weights.
+
+    fused: the two RMSNorms of a layer run inside the GEMVs that read them
+    (qmatmul_gemv_grouped_rmsnorm, qmatmul_gemv_swiglu_rmsnorm_f16; Q4/Q8
+    weights, hidden <= 4096), with the residual stream alternating between
+    two buffers; otherwise each norm is its own qdec_rmsnorm launch."""
 
     def __init__(self, cfg: DecoderConfig, emb: torch.Tensor, layers: List[LayerWeights], norm: torch.Tensor,
-                 lm_head: B.QWeight, max_len: int):
+                 lm_head: B.QWeight, max_len: int, fused: bool = True):
         self.cfg, self.emb, self.layers, self.norm, self.lm_head = cfg, emb, layers, norm, lm_head
         self.max_len = max_len
         dev = emb.device
@@ -58,7 +63,10 @@ class DenseDecoder:
         f16 = dict(dtype=torch.float16, device=dev)
         c = cfg
         qd, kvd = c.n_q_heads * c.head_dim, c.n_kv_heads * c.head_dim
+        self.fused = fused and c.hidden <= 4096 and all(
+            w.format in (B.Q4_G32, B.Q8_G32) for ly in layers for w in (ly.wq, ly.wk, ly.wv, ly.wg, ly.wu))
         self.x = torch.zeros(c.hidden, **f32)             # residual stream
+        self.x2 = torch.zeros(c.hidden, **f32)            # its other buffer (fused norms)
         self.h = torch.zeros(c.hidden, **f16)             # normed input of a projection
         self.q, self.k, self.v = torch.zeros(qd, **f32), torch.zeros(kvd, **f32), torch.zeros(kvd, **f32)
         self.q16 = torch.zeros((c.n_q_heads, c.head_dim), **f16)
@@ -81,6 +89,23 @@ class DenseDecoder:
         self.token."""
         c, s = self.cfg, stream
         B.qdec_embed(self.emb, self.token, out=self.x, stream=s)
+        if self.fused:
+            for li, ly in enumerate(self.layers):
+                # x2 = x + y_ffn; q, k, v = W . norm(x2)
+                B.qmatmul_gemv_grouped_rmsnorm([ly.wq, ly.wk, ly.wv], self.x, ly.attn_norm, c.eps, self.x2,
+                                               residual=self.y_ffn if li else None, outs=[self.q, self.k, self.v],
+                                               stream=s)
+                B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
+                                   q_out=self.q16, stream=s)
+                B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,
+                               workspace=self.ws, stream=s)
+                B.qmatmul_gemv(ly.wo, self.attn16.view(-1), out=self.y_attn, stream=s)
+                # x = x2 + y_attn; g = swiglu(norm(x))
+                B.qmatmul_gemv_swiglu_rmsnorm_f16(ly.wg, ly.wu, self.x2, ly.ffn_norm, c.eps, self.x,
+                                                  residual=self.y_attn, out=self.g16, stream=s)
+                B.qmatmul_gemv(ly.wd, self.g16, out=self.y_ffn, stream=s)
+            self._head(s)
+            return
         for li, ly in enumerate(self.layers):
             B.qdec_rmsnorm(self.x, ly.attn_norm, c.eps, residual=self.y_ffn if li else None, out=self.h, stream=s)
             B.qmatmul_gemv_grouped([ly.wq, ly.wk, ly.wv], [self.h] * 3, [self.q, self.k, self.v], stream=s)
@@ -92,6 +117,9 @@ class DenseDecoder:
             B.qdec_rmsnorm(self.x, ly.ffn_norm, c.eps, residual=self.y_attn, out=self.h, stream=s)
             B.qmatmul_gemv_swiglu(ly.wg, ly.wu, self.h, out=self.g16, stream=s)
             B.qmatmul_gemv(ly.wd, self.g16, out=self.y_ffn, stream=s)
-        B.qdec_rmsnorm(self.x, self.norm, c.eps, residual=self.y_ffn, out=self.h, stream=s)
+        self._head(s)
+
+    def _head(self, s) -> None:
+        B.qdec_rmsnorm(self.x, self.norm, self.cfg.eps, residual=self.y_ffn, out=self.h, stream=s)
         B.qmatmul_gemv(self.lm_head, self.h, out=self.logits, stream=s)
         B.qdec_argmax(self.logits, out=self.token, workspace=self.argmax_ws, stream=s)

@@ -322,3 +322,26 @@ def test_fp16_output_variants_validation():
     assert L.qmatmul_gemv_swiglu_f16(ctypes.byref(w.c()), ctypes.byref(w.c()), p, ctypes.c_void_p(0x50001),
                                      None) == 3
     assert B.qm_last_error()
+
+
+def test_fused_rmsnorm_gemv_validation():
+    L = B.lib()
+    p = ctypes.c_void_p(0x50000)
+    w = B.empty_qweight(B.Q4_G32, B.LAYOUT_DEVICE, 1, 64, 1024, device="cpu")
+    descs = (B.CQWeight * 1)(w.c())
+    ys = (ctypes.c_void_p * 1)(0x70000)
+    call = lambda x=p, r=None, g=p, eps=1e-6, xo=ctypes.c_void_p(0x90000), d=descs, n=1: \
+        L.qmatmul_gemv_grouped_rmsnorm(n, d, x, r, g, eps, xo, ys, None)
+    assert call(n=0) == 2 and call(n=9) == 2
+    assert call(x=None) == 1 and call(xo=None) == 1 and call(g=None) == 1
+    assert call(eps=-1.0) == 1
+    assert call(x=ctypes.c_void_p(0x50004)) == 3 and call(g=ctypes.c_void_p(0x50002)) == 3
+    assert call(xo=ctypes.c_void_p(0x50000 + 2048)) == 1          # overlaps x
+    big = B.empty_qweight(B.Q4_G32, B.LAYOUT_DEVICE, 1, 64, 8192, device="cpu")
+    assert call(d=(B.CQWeight * 1)(big.c())) == 2                  # k > 4096
+    q2 = B.empty_qweight(B.Q2_G32, B.LAYOUT_DEVICE, 1, 64, 1024, device="cpu")
+    assert call(d=(B.CQWeight * 1)(q2.c())) == 4                   # Q4/Q8 only
+    sw = lambda h=p, xo=ctypes.c_void_p(0x90000): L.qmatmul_gemv_swiglu_rmsnorm_f16(
+        ctypes.byref(w.c()), ctypes.byref(w.c()), p, None, p, 1e-6, xo, h, None)
+    assert sw(h=None) == 1 and sw(h=ctypes.c_void_p(0x50001)) == 3 and sw(xo=p) == 1
+    assert B.qm_last_error()

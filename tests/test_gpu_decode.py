@@ -180,9 +180,10 @@ def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32)):
     return dev_layers, torch.from_numpy(emb).cuda(), torch.from_numpy(norm).cuda(), head_dev, ref
 
 
-def _decoder(cfg, tag, max_len, fmts=(O.Q4, B.Q4_G32)):
+def _decoder(cfg, tag, max_len, fmts=(O.Q4, B.Q4_G32), fused=True):
     layers, emb, norm, head, ref = _model(cfg, tag, fmts)
-    dec = DenseDecoder(cfg, emb, layers, norm, head, max_len)
+    dec = DenseDecoder(cfg, emb, layers, norm, head, max_len, fused=fused)
+    assert dec.fused == fused
     kc = np.zeros((cfg.layers, cfg.n_kv_heads, max_len, cfg.head_dim))
     vc = np.zeros_like(kc)
     return dec, ref, kc, vc
@@ -192,9 +193,11 @@ TINY = DecoderConfig(hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, inter=5
                      theta=1e4)
 
 
-def test_decode_steps_teacher_forced_tiny():
-    """Ten teacher-forced steps: logits at every step, then the whole caches."""
-    dec, ref, kc, vc = _decoder(TINY, 21, 16)
+@pytest.mark.parametrize("fused", [True, False])
+def test_decode_steps_teacher_forced_tiny(fused):
+    """Ten teacher-forced steps: logits at every step, then the whole caches
+    (norms fused into the GEMVs, and as launches of their own)."""
+    dec, ref, kc, vc = _decoder(TINY, 21, 16, fused=fused)
     for pos, t in enumerate([5, 17, 999, 0, 42, 42, 7, 300, 1, 2]):
         dec.token.fill_(t)
         dec.step(pos)
@@ -294,3 +297,56 @@ def test_attention_decode_f16_is_the_rounded_fp32_output(d, hq, hkv, length):
     o16 = B.qattn_decode(q, kc, vc, length, 1 / math.sqrt(d), out=torch.empty((hq, d), dtype=torch.float16,
                                                                               device="cuda"))
     assert torch.equal(o16, o32.half())
+
+
+# ---------------------------------------------------------------- fused norms
+
+def _norm_inputs(k, tag, with_res):
+    rng = np.random.default_rng(tag + k)
+    x = (rng.standard_normal(k) * 2).astype(np.float32)
+    r = rng.standard_normal(k).astype(np.float32) if with_res else None
+    g = inputs.norm_weights_np(tag + k, k)
+    n = O.f16(O.rmsnorm(x.astype(np.float64) + (r if with_res else 0.0), g, 1e-6))
+    dev = lambda a: None if a is None else torch.from_numpy(a).cuda()
+    return dev(x), dev(r), dev(g), n, x, r
+
+
+@pytest.mark.parametrize("fmt", [(O.Q4, B.Q4_G32), (O.Q8, B.Q8_G32)])
+@pytest.mark.parametrize("k,ns", [(256, (64, 32, 32)), (1024, (2048, 1024, 1024)), (1024, (100, 37, 260)),
+                                  (3072, (3072, 1024, 1024)), (4096, (16448,)), (2048, (2048, 512, 512))])
+@pytest.mark.parametrize("with_res", [False, True])
+def test_gemv_grouped_rmsnorm_parity(fmt, k, ns, with_res):
+    ofmt, bfmt = fmt
+    xd, rd, gd, n, x, r = _norm_inputs(k, 41, with_res)
+    ws, refs = [], []
+    for i, nn in enumerate(ns):
+        w = inputs.weights_np(inputs.seed_for(41, nn, "q", i), (nn, k))
+        ws.append(B.qm_repack(B.qm_quantise(torch.from_numpy(w).cuda(), bfmt), B.LAYOUT_DEVICE))
+        q, s = O.quantise(w, ofmt)
+        refs.append(O.gemv(O.pack(q, ofmt), s, ofmt, n))
+    x_out = torch.empty(k, device="cuda")
+    ys = B.qmatmul_gemv_grouped_rmsnorm(ws, xd, gd, 1e-6, x_out, residual=rd)
+    for y, ref in zip(ys, refs):
+        assert rel_err(y.cpu().numpy(), ref) <= GEMV_TOL
+    assert np.array_equal(x_out.cpu().numpy(), x + r if with_res else x)
+    # the composition of the two separate launches agrees to within fp16 rounding of n
+    h = B.qdec_rmsnorm(xd.clone(), gd, 1e-6, residual=rd)
+    two = B.qmatmul_gemv_grouped(ws, [h] * len(ws))
+    for y, t in zip(ys, two):
+        assert rel_err(y.cpu().numpy(), t.cpu().numpy().astype(np.float64)) <= 2e-3
+
+
+@pytest.mark.parametrize("fmt", [(O.Q4, B.Q4_G32), (O.Q8, B.Q8_G32)])
+@pytest.mark.parametrize("n,k", [(65, 96), (3072, 1024), (8192, 3072), (8192, 2048), (16448, 256)])
+def test_gemv_swiglu_rmsnorm_parity(fmt, n, k):
+    ofmt, bfmt = fmt
+    xd, rd, gd, nrm, x, r = _norm_inputs(k, 42, True)
+    wg = inputs.weights_np(inputs.seed_for(42, n, "gate"), (n, k))
+    wu = inputs.weights_np(inputs.seed_for(42, n, "up"), (n, k))
+    dev = [B.qm_repack(B.qm_quantise(torch.from_numpy(w).cuda(), bfmt), B.LAYOUT_DEVICE) for w in (wg, wu)]
+    (gq, gs), (uq, us) = O.quantise(wg, ofmt), O.quantise(wu, ofmt)
+    ref = O.gemv_swiglu(O.pack(gq, ofmt), gs, O.pack(uq, ofmt), us, ofmt, nrm)
+    x_out = torch.empty(k, device="cuda")
+    h = B.qmatmul_gemv_swiglu_rmsnorm_f16(dev[0], dev[1], xd, gd, 1e-6, x_out, residual=rd)
+    assert rel_err(h.float().cpu().numpy(), ref) <= GEMV_TOL
+    assert np.array_equal(x_out.cpu().numpy(), x + r)
