@@ -283,6 +283,23 @@ qm_status qattn_decode_f16(const uint16_t* q, const uint16_t* k_cache, const uin
                            int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale,
                            uint16_t* o, void* workspace, size_t ws_bytes, void* stream);
 
+/* The new token's rotary embedding and KV-cache append folded into decode
+ * attention (Sec. 3.2: RoPE and attention kernels; Sec. 3.3: one launch
+ * fewer per layer): the result of qdec_rope_append followed by
+ * qattn_decode_f16 with len = pos + 1, value rows bit for bit; a rotated
+ * query or key element whose fp32 value lies on an fp16 rounding midpoint
+ * may round to the other neighbour (one fp16 ulp; the two kernels' fp32
+ * rotations can differ in the last bit).  q: fp32
+ * [n_q_heads][head_dim], k, v: fp32 [n_kv_heads][head_dim] (the projection
+ * outputs, 4-byte aligned); row pos of k_cache and v_cache (fp16
+ * [n_kv_heads][max_len][head_dim], 16-byte aligned) is written; o: fp16
+ * [n_q_heads][head_dim].  0 <= pos < max_len <= 262144; theta > 1; other
+ * limits, the workspace and the launches as qattn_decode. */
+qm_status qattn_decode_rope_f16(const float* q, const float* k, const float* v, int32_t n_q_heads,
+                                int32_t n_kv_heads, int32_t head_dim, int64_t pos, int64_t max_len, float theta,
+                                float scale, uint16_t* k_cache, uint16_t* v_cache, uint16_t* o, void* workspace,
+                                size_t ws_bytes, void* stream);
+
 /* ---- Glue of one decode step (Sec. 3.2: the normalisation, RoPE,
  * embedding and sampling kernels between the matmuls and attention of a
  * dense Llama 3.2 / Qwen3-style decoder).  Activations handed to a matmul or

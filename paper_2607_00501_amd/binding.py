@@ -31,7 +31,7 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
            "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
            "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
-           "qmatmul_gemv_swiglu_rmsnorm_f16")
+           "qmatmul_gemv_swiglu_rmsnorm_f16", "qattn_decode_rope_f16")
 
 
 class QmError(RuntimeError):
@@ -79,6 +79,8 @@ def lib() -> ctypes.CDLL:
             "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp],
             "qdec_embed": [vp, i64, i64, vp, vp, vp],
             "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
+            "qattn_decode_rope_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, ctypes.c_float, vp, vp,
+                                      vp, vp, sz, vp],
             "qmatmul_gemv_grouped_rmsnorm": [i32, W, vp, vp, vp, ctypes.c_float, vp, ctypes.POINTER(vp), vp],
             "qmatmul_gemv_swiglu_rmsnorm_f16": [W, W, vp, vp, vp, ctypes.c_float, vp, vp, vp],
             "qattn_decode_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
@@ -316,6 +318,26 @@ def qattn_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, 
     fn = lib().qattn_decode_f16 if out.dtype == torch.float16 else lib().qattn_decode
     _check(fn(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, length, max_len, scale,
               _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
+
+
+def qattn_decode_rope_f16(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: int, theta: float, scale: float,
+                          k_cache: torch.Tensor, v_cache: torch.Tensor, out: Optional[torch.Tensor] = None,
+                          workspace: Optional[torch.Tensor] = None, stream=None):
+    """RoPE + cache append at row pos + decode attention over rows 0..pos:
+    q fp32 [Hq*D], k, v fp32 [Hkv*D] -> fp16 [Hq][D]."""
+    hkv, max_len, d = k_cache.shape
+    hq = q.numel() // d
+    assert q.dtype == k.dtype == v.dtype == torch.float32 and k.numel() == v.numel() == hkv * d
+    assert k_cache.dtype == v_cache.dtype == torch.float16 and v_cache.shape == k_cache.shape
+    assert k_cache.is_contiguous() and v_cache.is_contiguous()
+    if out is None:
+        out = torch.empty((hq, d), dtype=torch.float16, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(qattn_decode_workspace_bytes(hq, d), dtype=torch.uint8, device=q.device)
+    _check(lib().qattn_decode_rope_f16(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, pos, max_len, theta, scale,
+                                       _ptr(k_cache), _ptr(v_cache), _ptr(out), _ptr(workspace), workspace.numel(),
+                                       _stream(stream)))
     return out
 
 

@@ -469,6 +469,37 @@ qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_
                           workspace, ws_bytes, stream, "qattn_decode");
 }
 
+qm_status qattn_decode_rope_f16(const float* q, const float* k, const float* v, int32_t n_q_heads,
+                                int32_t n_kv_heads, int32_t head_dim, int64_t pos, int64_t max_len, float theta,
+                                float scale, uint16_t* k_cache, uint16_t* v_cache, uint16_t* o, void* workspace,
+                                size_t ws_bytes, void* stream) {
+  const char* name = "qattn_decode_rope_f16";
+  if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "%s: head_dim=%d must be 64 or 128", name, head_dim);
+  if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads > 1024 || n_q_heads % n_kv_heads != 0 ||
+      n_q_heads / n_kv_heads > 8)
+    return fail(QM_ESHAPE, "%s: n_q_heads=%d must be a multiple of n_kv_heads=%d, at most 8 per KV head", name,
+                n_q_heads, n_kv_heads);
+  if (max_len < 1 || max_len > kAttnMaxLen || pos < 0 || pos >= max_len)
+    return fail(QM_ESHAPE, "%s: need 0 <= pos < max_len <= %lld", name, (long long)kAttnMaxLen);
+  if (!(scale == scale) || scale == INFINITY || scale == -INFINITY)
+    return fail(QM_EINVAL, "%s: scale must be finite", name);
+  if (!(theta > 1.0f) || theta == INFINITY) return fail(QM_EINVAL, "%s: theta must be finite and > 1", name);
+  if (!q || !k || !v || !k_cache || !v_cache || !o) return fail(QM_EINVAL, "%s: null pointer", name);
+  if (!aligned4(q) || !aligned4(k) || !aligned4(v) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned2(o))
+    return fail(QM_EALIGN, "%s: q, k, v 4-byte, caches 16-byte, o 2-byte aligned", name);
+  const size_t need = attn_decode_workspace_bytes(n_q_heads, head_dim);
+  if (!workspace || ws_bytes < need)
+    return fail(QM_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", name, need, ws_bytes);
+  if (!aligned16(workspace)) return fail(QM_EALIGN, "%s: workspace must be 16-byte aligned", name);
+  const DeviceInfo* d;
+  qm_status st;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  return launched(launch_attn_decode_rope(q, k, v, n_q_heads, n_kv_heads, head_dim, pos, max_len, theta, scale,
+                                          k_cache, v_cache, o, static_cast<float*>(workspace), d->cu_count,
+                                          static_cast<hipStream_t>(stream)),
+                  name);
+}
+
 qm_status qattn_decode_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
                            int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale,
                            uint16_t* o, void* workspace, size_t ws_bytes, void* stream) {

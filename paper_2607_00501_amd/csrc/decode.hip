@@ -9,6 +9,7 @@
 #include <cmath>
 
 #include "qm_internal.h"
+#include "rope.h"
 
 namespace qm {
 namespace {
@@ -177,13 +178,13 @@ __global__ void rope_append_kernel(const float* __restrict__ q, const float* __r
     dst[i + half] = f2h(v[kh * d + i + half]);
     return;
   }
-  const double ang = static_cast<double>(pos) * exp2(-2.0 * i / d * log2_theta);
-  const float c = static_cast<float>(cos(ang)), s = static_cast<float>(sin(ang));
+  const float2 cs = rope_cos_sin(pos, i, d, log2_theta);
+  const float c = cs.x, s = cs.y;
   const float* src = h < hq ? q + h * d : k + (h - hq) * d;
   uint16_t* dst = h < hq ? q_out + h * d : kc + (static_cast<int64_t>(h - hq) * max_len + pos) * d;
   const float a = src[i], b = src[i + half];
-  dst[i] = f2h(a * c - b * s);
-  dst[i + half] = f2h(b * c + a * s);
+  dst[i] = f2h(rope_low(a, b, c, s));
+  dst[i + half] = f2h(rope_high(a, b, c, s));
 }
 
 __global__ __launch_bounds__(256) void cast_f16_kernel(const float* __restrict__ x, int64_t n,

@@ -141,6 +141,13 @@ hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16
                               int32_t d, int64_t len, int64_t max_len, float scale, float* o, uint16_t* o16,
                               float* ws, int cu_count, hipStream_t st);   // o16 != nullptr: fp16 output
 
+// Decode attention with the new token's RoPE and cache append folded in
+// (len = pos + 1; fp16 output).
+hipError_t launch_attn_decode_rope(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv,
+                                   int32_t d, int64_t pos, int64_t max_len, float theta, float scale,
+                                   uint16_t* kc, uint16_t* vc, uint16_t* o16, float* ws, int cu_count,
+                                   hipStream_t st);
+
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
                                hipStream_t st);

@@ -1,0 +1,32 @@
+// Rotary position embedding of one pair (BaseRT Sec. 3.2: the RoPE kernel),
+// shared by the standalone RoPE + cache-append kernel and the decode
+// attention that folds it in, so both give the same bits: element i pairs
+// with i + D/2, angle pos * theta^(-2i/D) in fp64, its sine and cosine
+// rounded to fp32, the rotation in fp32.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qm {
+
+// Returns (cos, sin) in registers.
+__device__ __forceinline__ float2 rope_cos_sin(int64_t pos, int i, int d, double log2_theta) {
+#pragma clang fp contract(off)
+  const double ang = static_cast<double>(pos) * exp2(-2.0 * i / d * log2_theta);
+  return make_float2(static_cast<float>(cos(ang)), static_cast<float>(sin(ang)));
+}
+
+// (a, b) = (x[i], x[i + D/2]) -> the rotated x[i] and x[i + D/2].  The
+// fused multiply-adds are explicit and the compiler may not contract the
+// remaining product into anything else, so every kernel rounds alike.
+__device__ __forceinline__ float rope_low(float a, float b, float c, float s) {
+#pragma clang fp contract(off)
+  return fmaf(a, c, -(b * s));
+}
+__device__ __forceinline__ float rope_high(float a, float b, float c, float s) {
+#pragma clang fp contract(off)
+  return fmaf(b, c, a * s);
+}
+
+}  // namespace qm

@@ -52,7 +52,7 @@ class DenseDecoder:
     fused: the two RMSNorms of a layer run inside the GEMVs that read them
     (qmatmul_gemv_grouped_rmsnorm, qmatmul_gemv_swiglu_rmsnorm_f16; Q4/Q8
     weights, hidden <= 4096), with the residual stream alternating between
-    two buffers; otherwise each norm is its own qdec_rmsnorm launch."""
+    two buffers; otherwise each norm is a launch of its own."""
 
     def __init__(self, cfg: DecoderConfig, emb: torch.Tensor, layers: List[LayerWeights], norm: torch.Tensor,
                  lm_head: B.QWeight, max_len: int, fused: bool = True):
@@ -95,6 +95,9 @@ class DenseDecoder:
                 B.qmatmul_gemv_grouped_rmsnorm([ly.wq, ly.wk, ly.wv], self.x, ly.attn_norm, c.eps, self.x2,
                                                residual=self.y_ffn if li else None, outs=[self.q, self.k, self.v],
                                                stream=s)
+                # RoPE + cache append, then attention (folding the two into one
+                # launch, qattn_decode_rope_f16, measured slower: the fp64
+                # angles then sit ahead of the attention's first loads)
                 B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
                                    q_out=self.q16, stream=s)
                 B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,

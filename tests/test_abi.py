@@ -345,3 +345,16 @@ def test_fused_rmsnorm_gemv_validation():
         ctypes.byref(w.c()), ctypes.byref(w.c()), p, None, p, 1e-6, xo, h, None)
     assert sw(h=None) == 1 and sw(h=ctypes.c_void_p(0x50001)) == 3 and sw(xo=p) == 1
     assert B.qm_last_error()
+
+
+def test_attention_rope_fused_validation():
+    L = B.lib()
+    p = ctypes.c_void_p(0x50000)
+    need = B.qattn_decode_workspace_bytes(16, 128)
+    call = lambda d=128, pos=10, mx=64, theta=1e6, kc=p, o=p, nb=need: L.qattn_decode_rope_f16(
+        p, p, p, 16, 8, d, pos, mx, theta, 0.1, kc, p, o, p, nb, None)
+    assert call(d=96) == 2 and call(pos=64) == 2 and call(pos=-1) == 2 and call(mx=300000) == 2
+    assert call(theta=0.5) == 1 and call(o=None) == 1
+    assert call(kc=ctypes.c_void_p(0x50004)) == 3 and call(o=ctypes.c_void_p(0x50001)) == 3
+    assert call(nb=need - 1) == 6
+    assert B.qm_last_error()

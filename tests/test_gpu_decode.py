@@ -350,3 +350,31 @@ def test_gemv_swiglu_rmsnorm_parity(fmt, n, k):
     h = B.qmatmul_gemv_swiglu_rmsnorm_f16(dev[0], dev[1], xd, gd, 1e-6, x_out, residual=rd)
     assert rel_err(h.float().cpu().numpy(), ref) <= GEMV_TOL
     assert np.array_equal(x_out.cpu().numpy(), x + r)
+
+
+@pytest.mark.parametrize("d,hq,hkv", [(64, 32, 8), (128, 16, 8), (128, 24, 8), (64, 4, 4)])
+@pytest.mark.parametrize("pos", [0, 99, 127, 128, 1000, 5000])
+def test_attention_rope_fused_equals_two_launches(d, hq, hkv, pos):
+    """qattn_decode_rope_f16 against qdec_rope_append followed by
+    qattn_decode_f16 (one slice and split plans, the new row inside and at
+    the end of a slice): value rows bit for bit; key elements equal except
+    rare fp32 rotations on an fp16 midpoint (one ulp: seen once in about
+    10^5 elements); the output within the fp16 output rounding."""
+    max_len, theta, scale = 8192, 1e6, 1 / math.sqrt(d)
+    rng = np.random.default_rng(pos * 3 + d)
+    q = torch.from_numpy(rng.standard_normal(hq * d).astype(np.float32)).cuda()
+    k = torch.from_numpy(rng.standard_normal(hkv * d).astype(np.float32)).cuda()
+    v = torch.from_numpy(rng.standard_normal(hkv * d).astype(np.float32)).cuda()
+    kc1 = inputs.activations_dev(inputs.seed_for(33, pos, "k"), (hkv, max_len, d))
+    vc1 = inputs.activations_dev(inputs.seed_for(33, pos, "v"), (hkv, max_len, d))
+    kc2, vc2 = kc1.clone(), vc1.clone()
+    q16 = B.qdec_rope_append(q, k, v, pos, theta, kc1, vc1)
+    o1 = B.qattn_decode(q16, kc1, vc1, pos + 1, scale, out=torch.empty((hq, d), dtype=torch.float16, device="cuda"))
+    o2 = B.qattn_decode_rope_f16(q, k, v, pos, theta, scale, kc2, vc2)
+    assert torch.equal(vc1, vc2)
+    diff = kc1 != kc2
+    assert int(diff.sum()) <= 2
+    assert torch.all((kc1.float() - kc2.float()).abs() <= 2.0 ** -10 * kc1.float().abs())
+    assert torch.all(diff[:, :pos] == False) and torch.all(diff[:, pos + 1:] == False)    # only row pos written
+    err = (o1.float() - o2.float()).abs().max().item()
+    assert err <= 2e-3 * o1.float().abs().max().item()
