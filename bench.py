@@ -287,6 +287,8 @@ def build_decoder(model: dict, cfg_id: int, fmt, max_len, torch, B, inputs):
 
     def proj(name, li, n, k):
         w = inputs.weights_dev(inputs.seed_for(cfg_id, li, name), (n, k))
+        if name in ("q", "k"):                # row order of the q/k/v GEMV's RoPE epilogue
+            w = B.rope_interleave_rows(w, n // cfg.head_dim, cfg.head_dim)
         q = B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE)
         del w
         return q
@@ -304,7 +306,7 @@ def build_decoder(model: dict, cfg_id: int, fmt, max_len, torch, B, inputs):
     emb = inputs.activations_dev(inputs.seed_for(cfg_id, 0, "emb"), (cfg.vocab, cfg.hidden))
     head = proj("lm_head", 0, cfg.vocab, cfg.hidden)
     torch.cuda.synchronize()
-    return DenseDecoder(cfg, emb, layers, gain("norm", 0), head, max_len)
+    return DenseDecoder(cfg, emb, layers, gain("norm", 0), head, max_len, rope_rows_interleaved=True)
 
 
 def tg_tokens_per_s(torch, dec, tokens: int, reps: int):
@@ -334,16 +336,16 @@ def extra_tg(torch, B, inputs, workloads, steps, warmup, lib):
     out = {}
     # End-to-end decode, tg128 (Sec. 4.1): every kernel of a token (embedding,
     # norms, projections, RoPE and cache append, attention, SwiGLU, LM head,
-    # greedy sampling): 6 launches per layer (the norms run inside the q/k/v
-    # and gate/up GEMVs; attention is one launch for caches of up to 128
-    # rows) + 5.
+    # greedy sampling): 5 launches per layer (the norms run inside the q/k/v
+    # and gate/up GEMVs, RoPE and the cache append in the q/k/v GEMV's
+    # epilogue; attention is one launch for caches of up to 128 rows) + 5.
     for model, cfg_id in ((workloads.QWEN3_06B_DECODER, 1), (workloads.LLAMA32_1B_DECODER, 3),
                           (workloads.LLAMA32_3B_DECODER, 2)):
         dec = build_decoder(model, cfg_id, B.Q4_G32, 128, torch, B, inputs)
         tps, t = tg_tokens_per_s(torch, dec, 128, 3)
         key = model["name"] + "_tg128_q4"
         out[key] = {"tokens_per_s": round(tps, 1), "ms_per_token": round(1e3 / tps, 4),
-                    "launches_per_token": 6 * model["layers"] + 5, "ms_per_128_tokens": round(t * 1e3, 3)}
+                    "launches_per_token": 5 * model["layers"] + 5, "ms_per_128_tokens": round(t * 1e3, 3)}
         log(f"{key}: {out[key]}")
         del dec
         torch.cuda.empty_cache()

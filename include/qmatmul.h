@@ -192,6 +192,31 @@ qm_status qmatmul_gemv_swiglu_rmsnorm_f16(const qm_qweight* w_gate, const qm_qwe
                                           const float* residual, const uint16_t* gain, float eps, float* x_out,
                                           uint16_t* h, void* stream);
 
+/* (cos, sin) table of the rotary embedding for every position of a cache:
+ * table[p][i] = (cos a, sin a), a = p * theta^(-2i/head_dim), i < head_dim/2,
+ * p < max_len, angle in fp64, fp32 entries (the values qdec_rope_append
+ * computes).  table: fp32 [max_len][head_dim/2][2], 8-byte aligned.  Built
+ * once per cache (Sec. 3.2: RoPE). */
+qm_status qdec_rope_table(int64_t max_len, int32_t head_dim, float theta, float* table, void* stream);
+
+/* The q/k/v projections of a decode step in one launch, with the attention
+ * norm folded in (as qmatmul_gemv_grouped_rmsnorm) and RoPE plus the cache
+ * append as the GEMV epilogue (Sec. 3.3: each fusion removes a launch).
+ * w: three descriptors, q [n_q_heads * head_dim][k], k and v
+ * [n_kv_heads * head_dim][k], Q4 or Q8, DEVICE layout; the rows of each
+ * head of w[0] and w[1] are stored interleaved: stored row 2i is the head's
+ * row i and stored row 2i + 1 its row i + head_dim/2 (so a rotation pair is
+ * computed by neighbouring lanes).  Writes q_out (fp16 [n_q_heads][head_dim],
+ * rotated, in the natural order), row pos of k_cache (rotated) and of
+ * v_cache (fp16 [n_kv_heads][max_len][head_dim]) and x_out; rope_table from
+ * qdec_rope_table for this max_len and head_dim.  x, residual, gain, eps,
+ * x_out as qmatmul_gemv_grouped_rmsnorm. */
+qm_status qmatmul_gemv_qkv_rmsnorm_rope(const qm_qweight* w, const float* x, const float* residual,
+                                        const uint16_t* gain, float eps, float* x_out, int32_t n_q_heads,
+                                        int32_t n_kv_heads, int32_t head_dim, int64_t pos, int64_t max_len,
+                                        const float* rope_table, uint16_t* q_out, uint16_t* k_cache,
+                                        uint16_t* v_cache, void* stream);
+
 /* Grouped decode GEMV (Sec. 3.3: fusing a sequence of operators removes a
  * launch each, which matters most in decode; e.g. the q/k/v projections of
  * a layer, which share x, or its gate and up projections):

@@ -31,7 +31,8 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
            "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
            "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
-           "qmatmul_gemv_swiglu_rmsnorm_f16", "qattn_decode_rope_f16")
+           "qmatmul_gemv_swiglu_rmsnorm_f16", "qattn_decode_rope_f16", "qdec_rope_table",
+           "qmatmul_gemv_qkv_rmsnorm_rope")
 
 
 class QmError(RuntimeError):
@@ -79,6 +80,9 @@ def lib() -> ctypes.CDLL:
             "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp],
             "qdec_embed": [vp, i64, i64, vp, vp, vp],
             "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
+            "qdec_rope_table": [i64, i32, ctypes.c_float, vp, vp],
+            "qmatmul_gemv_qkv_rmsnorm_rope": [W, vp, vp, vp, ctypes.c_float, vp, i32, i32, i32, i64, i64, vp, vp, vp,
+                                              vp, vp],
             "qattn_decode_rope_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, ctypes.c_float, vp, vp,
                                       vp, vp, sz, vp],
             "qmatmul_gemv_grouped_rmsnorm": [i32, W, vp, vp, vp, ctypes.c_float, vp, ctypes.POINTER(vp), vp],
@@ -260,6 +264,40 @@ def qmatmul_gemv_swiglu_rmsnorm_f16(w_gate: QWeight, w_up: QWeight, x: torch.Ten
                                                  _ptr(residual), _ptr(gain), eps, _ptr(x_out), _ptr(out),
                                                  _stream(stream)))
     return out
+
+
+def qdec_rope_table(max_len: int, head_dim: int, theta: float, device="cuda", stream=None) -> torch.Tensor:
+    """fp32 [max_len][head_dim/2][2] (cos, sin) table."""
+    t = torch.empty((max_len, head_dim // 2, 2), dtype=torch.float32, device=device)
+    _check(lib().qdec_rope_table(max_len, head_dim, theta, _ptr(t), _stream(stream)))
+    return t
+
+
+def rope_interleave_rows(w: torch.Tensor, n_heads: int, head_dim: int) -> torch.Tensor:
+    """Row order qmatmul_gemv_qkv_rmsnorm_rope expects for W_q / W_k: within
+    each head, stored row 2i = row i and stored row 2i + 1 = row i + D/2."""
+    k = w.shape[-1]
+    return w.reshape(n_heads, 2, head_dim // 2, k).transpose(1, 2).reshape(n_heads * head_dim, k).contiguous()
+
+
+def qmatmul_gemv_qkv_rmsnorm_rope(ws, x: torch.Tensor, gain: torch.Tensor, eps: float, x_out: torch.Tensor,
+                                  pos: int, rope_table: torch.Tensor, q_out: torch.Tensor, k_cache: torch.Tensor,
+                                  v_cache: torch.Tensor, residual: Optional[torch.Tensor] = None, stream=None):
+    """q/k/v GEMV with the norm folded in and RoPE + cache append as the
+    epilogue (ws[0], ws[1] with rope_interleave_rows order)."""
+    hkv, max_len, d = k_cache.shape
+    hq = ws[0].n // d
+    k = ws[0].k
+    for t in (x, x_out) + ((residual,) if residual is not None else ()):
+        assert t.dtype == torch.float32 and t.is_contiguous() and t.numel() == k
+    assert gain.dtype == torch.float16 and gain.numel() == k
+    assert q_out.dtype == k_cache.dtype == v_cache.dtype == torch.float16 and q_out.numel() == hq * d
+    assert rope_table.dtype == torch.float32 and rope_table.shape == (max_len, d // 2, 2)
+    descs = (CQWeight * 3)(*[w.c() for w in ws])
+    _check(lib().qmatmul_gemv_qkv_rmsnorm_rope(descs, _ptr(x), _ptr(residual), _ptr(gain), eps, _ptr(x_out), hq,
+                                               hkv, d, pos, max_len, _ptr(rope_table), _ptr(q_out),
+                                               _ptr(k_cache), _ptr(v_cache), _stream(stream)))
+    return q_out
 
 
 def qmatmul_gemm(w: QWeight, x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):

@@ -286,6 +286,60 @@ qm_status qmatmul_gemv_grouped_rmsnorm(int32_t count, const qm_qweight* w, const
                   name);
 }
 
+qm_status qdec_rope_table(int64_t max_len, int32_t head_dim, float theta, float* table, void* stream) {
+  if ((head_dim != 64 && head_dim != 128) || max_len < 1 || max_len > kAttnMaxLen)
+    return fail(QM_ESHAPE, "qdec_rope_table: head_dim 64 or 128 and 1 <= max_len <= %lld", (long long)kAttnMaxLen);
+  if (!(theta > 1.0f) || theta == INFINITY) return fail(QM_EINVAL, "qdec_rope_table: theta must be finite and > 1");
+  if (!table) return fail(QM_EINVAL, "qdec_rope_table: null table");
+  if ((reinterpret_cast<uintptr_t>(table) & 7u) != 0) return fail(QM_EALIGN, "qdec_rope_table: table 8-byte aligned");
+  return launched(launch_rope_table(max_len, head_dim, theta, table, static_cast<hipStream_t>(stream)),
+                  "qdec_rope_table");
+}
+
+qm_status qmatmul_gemv_qkv_rmsnorm_rope(const qm_qweight* w, const float* x, const float* residual,
+                                        const uint16_t* gain, float eps, float* x_out, int32_t n_q_heads,
+                                        int32_t n_kv_heads, int32_t head_dim, int64_t pos, int64_t max_len,
+                                        const float* rope_table, uint16_t* q_out, uint16_t* k_cache,
+                                        uint16_t* v_cache, void* stream) {
+  const char* name = "qmatmul_gemv_qkv_rmsnorm_rope";
+  if (!w) return fail(QM_EINVAL, "%s: null weights", name);
+  if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "%s: head_dim=%d must be 64 or 128", name, head_dim);
+  if (n_q_heads < 1 || n_q_heads > 1024 || n_kv_heads < 1 || n_kv_heads > 1024)
+    return fail(QM_ESHAPE, "%s: head counts must be in [1, 1024]", name);
+  if (max_len < 1 || max_len > kAttnMaxLen || pos < 0 || pos >= max_len)
+    return fail(QM_ESHAPE, "%s: need 0 <= pos < max_len <= %lld", name, (long long)kAttnMaxLen);
+  const int64_t want[3] = {int64_t{n_q_heads} * head_dim, int64_t{n_kv_heads} * head_dim,
+                           int64_t{n_kv_heads} * head_dim};
+  GemvGroup g{};
+  g.count = 3;
+  for (int i = 0; i < 3; ++i) {
+    qm_status st = check_weight(&w[i], "qmatmul_gemv_qkv_rmsnorm_rope(w[i])");
+    if (st != QM_OK) return st;
+    if (w[i].format != QM_Q4_G32 && w[i].format != QM_Q8_G32) return fail(QM_EFORMAT, "%s: Q4 or Q8 only", name);
+    if (w[i].format != w[0].format) return fail(QM_EFORMAT, "%s: formats differ", name);
+    if (w[i].layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "%s: w[%d] must be in DEVICE layout", name, i);
+    if (w[i].batch != 1) return fail(QM_ESHAPE, "%s: w[%d] batch must be 1", name, i);
+    if (w[i].k != w[0].k) return fail(QM_ESHAPE, "%s: k differs between entries", name);
+    if (w[i].n != want[i]) return fail(QM_ESHAPE, "%s: w[%d] must have %lld rows", name, i, (long long)want[i]);
+    g.q[i] = static_cast<const uint8_t*>(w[i].qdata);
+    g.s[i] = w[i].scales;
+    g.n[i] = static_cast<int>(w[i].n);
+  }
+  qm_status st = check_norm(x, residual, gain, eps, x_out, w[0].k, name);
+  if (st != QM_OK) return st;
+  if (!rope_table || !q_out || !k_cache || !v_cache) return fail(QM_EINVAL, "%s: null pointer", name);
+  if ((reinterpret_cast<uintptr_t>(rope_table) & 7u) != 0 || !aligned2(q_out) || !aligned2(k_cache) ||
+      !aligned2(v_cache))
+    return fail(QM_EALIGN, "%s: rope_table 8-byte, q_out and caches 2-byte aligned", name);
+  const DeviceInfo* d;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  const NormArgs na{x, residual, gain, x_out, eps};
+  const QkvRopeEpi epi{q_out, k_cache, v_cache, rope_table, pos, max_len, head_dim};
+  return launched(launch_gemv_qkv_norm_rope(w[0].format, g, na, epi, w[0].k, d->cu_count,
+                                            static_cast<hipStream_t>(stream)),
+                  name);
+}
+
 qm_status qmatmul_gemv_swiglu_rmsnorm_f16(const qm_qweight* w_gate, const qm_qweight* w_up, const float* x,
                                           const float* residual, const uint16_t* gain, float eps, float* x_out,
                                           uint16_t* h, void* stream) {

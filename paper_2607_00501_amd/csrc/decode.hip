@@ -187,6 +187,15 @@ __global__ void rope_append_kernel(const float* __restrict__ q, const float* __r
   dst[i + half] = f2h(rope_high(a, b, c, s));
 }
 
+// table[p][i] = (cos, sin) of the angle of pair i at position p, for every
+// position of a cache (built once; the same function as the kernels above).
+__global__ __launch_bounds__(256) void rope_table_kernel(int64_t max_len, int d, double log2_theta,
+                                                         float2* __restrict__ table) {
+  const int64_t n = max_len * (d / 2);
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256)
+    table[e] = rope_cos_sin(e / (d / 2), static_cast<int>(e % (d / 2)), d, log2_theta);
+}
+
 __global__ __launch_bounds__(256) void cast_f16_kernel(const float* __restrict__ x, int64_t n,
                                                        uint16_t* __restrict__ y) {
   for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) y[i] = f2h(x[i]);
@@ -322,6 +331,12 @@ hipError_t launch_rope_append(const float* q, const float* k, const float* v, in
                               uint16_t* vc, hipStream_t st) {
   hipLaunchKernelGGL(rope_append_kernel, dim3(static_cast<unsigned>(hq + 2 * hkv)), dim3(d / 2), 0, st, q, k, v,
                      hq, hkv, d, pos, max_len, std::log2(static_cast<double>(theta)), q_out, kc, vc);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(int64_t max_len, int32_t d, float theta, float* table, hipStream_t st) {
+  hipLaunchKernelGGL(rope_table_kernel, dim3(spread_blocks(max_len * (d / 2))), dim3(256), 0, st, max_len, d,
+                     std::log2(static_cast<double>(theta)), reinterpret_cast<float2*>(table));
   return hipGetLastError();
 }
 

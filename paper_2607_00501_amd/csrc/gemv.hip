@@ -24,6 +24,7 @@
 //    upper half of an fp32) goes through fp32 fma with the fp16 activation
 //    (Sec. 4.1: eight formats, one kernel each).
 #include "qm_internal.h"
+#include "rope.h"
 
 #include <hip/hip_fp16.h>
 
@@ -451,13 +452,38 @@ __device__ __forceinline__ void stage_rmsnorm(const NormArgs& na, int groups, ui
   }
 }
 
-template <int FMT, int SUBR, int WAVES, bool XLDS, bool SWIGLU = false, bool NORM = false>
+// Store of the fused q/k/v epilogue: role 0 (q) and 1 (k) rotate the pair
+// held by lanes 2i and 2i + 1 (interleaved rows) and write q in fp16 or the
+// key into cache row pos; role 2 (v) writes the value row.
+__device__ __forceinline__ void qkv_rope_store(const QkvRopeEpi& e, int role, int64_t n, float val, float partner) {
+  auto h = [](float f) { const _Float16 t = static_cast<_Float16>(f); return __builtin_bit_cast(uint16_t, t); };
+  const int d = e.d, h2 = d / 2;
+  const int64_t head = n / d;
+  const int w = static_cast<int>(n % d);
+  if (role == 2) {
+    e.vc[(head * e.max_len + e.pos) * d + w] = h(val);
+    return;
+  }
+  const int i = w >> 1;
+  const bool hi = (w & 1) != 0;
+  const float2 cs = reinterpret_cast<const float2*>(e.table)[e.pos * h2 + i];
+  const float r = hi ? rope_high(partner, val, cs.x, cs.y) : rope_low(val, partner, cs.x, cs.y);
+  const int dd = hi ? i + h2 : i;
+  if (role == 0)
+    e.q16[head * d + dd] = h(r);
+  else
+    e.kc[(head * e.max_len + e.pos) * d + dd] = h(r);
+}
+
+template <int FMT, int SUBR, int WAVES, bool XLDS, bool SWIGLU = false, bool NORM = false, bool QKV_ROPE = false>
 __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
                                               const uint8_t* __restrict__ q2, const uint16_t* __restrict__ s2,
                                               const uint16_t* __restrict__ x, float* __restrict__ y, int n_rows,
                                               int groups, int64_t block, int64_t nblocks,
                                               uint16_t* __restrict__ y16 = nullptr,
-                                              const NormArgs* na = nullptr) {
+                                              const NormArgs* na = nullptr, const QkvRopeEpi* epi = nullptr,
+                                              int role = 0) {
+  static_assert(!QKV_ROPE || WAVES > 1, "the q/k/v epilogue runs in the multi-wavefront store");
   constexpr int CL = 64 / SUBR;
   constexpr int NM = SWIGLU ? 2 : 1;                  // matrices
   constexpr int U = kSubU<FMT>;
@@ -565,7 +591,13 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
       for (int w = 1; w < WAVES; ++w) t[m] += part[m][w][lane];
     }
     const int64_t n = panel * 64 + row;
-    if (n < n_rows) store(n, out(t[0], t[NM - 1]));
+    const float val = out(t[0], t[NM - 1]);
+    if constexpr (QKV_ROPE) {
+      const float partner = __shfl_xor(val, 1, 64);   // lanes 2i, 2i + 1: one rotation pair (both active)
+      if (n < n_rows) qkv_rope_store(*epi, role, n, val, partner);
+    } else {
+      if (n < n_rows) store(n, val);
+    }
   }
 }
 
@@ -665,6 +697,32 @@ __global__ __launch_bounds__(512) void gemv_sub_group_norm_kernel(GemvGroup g, N
   if (local >= nb) return;                             // padding workgroup (never workgroup 0)
   gemv_sub_body<FMT, SUBR, 8, true, false, true>(q, s, nullptr, nullptr, nullptr, y, n, groups, local, nb, nullptr,
                                                  &na);
+}
+
+// The q/k/v projections with the norm folded in and the RoPE / cache
+// epilogue (matrix 0: q, 1: k, 2: v).
+template <int FMT, int SUBR>
+__global__ __launch_bounds__(512) void gemv_qkv_norm_rope_kernel(GemvGroup g, NormArgs na, QkvRopeEpi epi) {
+  const int b = static_cast<int>(blockIdx.x);
+  const uint8_t* q = g.q[0];
+  const uint16_t* s = g.s[0];
+  int n = g.n[0], first = 0, role = 0;
+#pragma unroll
+  for (int j = 1; j < 3; ++j) {
+    const bool in = b >= g.start[j];
+    q = in ? g.q[j] : q;
+    s = in ? g.s[j] : s;
+    n = in ? g.n[j] : n;
+    first = in ? g.start[j] : first;
+    role = in ? j : role;
+  }
+  int groups = g.groups;
+  asm volatile("" ::"s"(q), "s"(s), "s"(n), "s"(first), "s"(groups), "s"(role));
+  const int64_t local = b - first;
+  const int64_t nb = padded_rows(n) / SUBR;
+  if (local >= nb) return;                             // padding workgroup (never workgroup 0)
+  gemv_sub_body<FMT, SUBR, 8, true, false, true, true>(q, s, nullptr, nullptr, nullptr, nullptr, n, groups, local,
+                                                       nb, nullptr, &na, &epi, role);
 }
 
 template <int FMT, int SUBR, bool XLDS>
@@ -884,6 +942,36 @@ hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg
 static int norm_subr(int32_t fmt, int64_t rows, int64_t k, int cu_count) {
   const GemvPlan plan = gemv_plan(fmt, rows, k, cu_count);
   return plan.subr == kPanel ? 32 : plan.subr;
+}
+
+hipError_t launch_gemv_qkv_norm_rope(int32_t fmt, GemvGroup& g, const NormArgs& na, const QkvRopeEpi& epi,
+                                     int64_t k, int cu_count, hipStream_t st) {
+  int64_t rows = 0;
+  for (int i = 0; i < 3; ++i) rows += padded_rows(g.n[i]);
+  const int subr = norm_subr(fmt, rows, k, cu_count);
+  g.groups = static_cast<int>(k / kGroup);
+  int start = 0;
+  for (int i = 0; i < 3; ++i) {
+    g.start[i] = start;
+    const int nb = static_cast<int>(padded_rows(g.n[i]) / subr);
+    start += i + 1 < 3 ? (nb + kXcds - 1) / kXcds * kXcds : nb;
+  }
+  g.start[3] = start;
+  const dim3 grid(static_cast<unsigned>(start));
+  const size_t lds = static_cast<size_t>(g.groups) * 64;
+  auto go = [&](auto f) -> hipError_t {
+    constexpr int F = decltype(f)::value;
+    switch (subr) {
+      case 4: hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, 4>), grid, dim3(512), lds, st, g, na, epi); break;
+      case 8: hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, 8>), grid, dim3(512), lds, st, g, na, epi); break;
+      case 16: hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, 16>), grid, dim3(512), lds, st, g, na, epi); break;
+      default: hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, 32>), grid, dim3(512), lds, st, g, na, epi); break;
+    }
+    return hipGetLastError();
+  };
+  if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
+  if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemv_group_norm(int32_t fmt, GemvGroup& g, const NormArgs& na, int64_t k, int cu_count,

@@ -161,6 +161,22 @@ hipError_t launch_rope_append(const float* q, const float* k, const float* v, in
                               int64_t pos, int64_t max_len, float theta, uint16_t* q_out, uint16_t* kc,
                               uint16_t* vc, hipStream_t st);
 hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t st);
+hipError_t launch_rope_table(int64_t max_len, int32_t d, float theta, float* table, hipStream_t st);
+
+// Epilogue of the fused q/k/v GEMV that applies RoPE and fills the caches:
+// W_q and W_k hold each head's rows interleaved (row 2i = row i, row 2i + 1
+// = row i + D/2 of the head), so a rotation pair sits in adjacent lanes.
+struct QkvRopeEpi {
+  uint16_t* q16;        // [Hq][D] rotated queries
+  uint16_t* kc;         // [Hkv][max_len][D], row pos written
+  uint16_t* vc;
+  const float* table;   // [max_len][D/2] (cos, sin)
+  int64_t pos;
+  int64_t max_len;
+  int d;
+};
+hipError_t launch_gemv_qkv_norm_rope(int32_t fmt, GemvGroup& g, const NormArgs& na, const QkvRopeEpi& epi,
+                                     int64_t k, int cu_count, hipStream_t st);
 hipError_t launch_argmax(const float* x, int64_t n, int32_t* token, void* ws, hipStream_t st);
 
 struct MoeArgs {

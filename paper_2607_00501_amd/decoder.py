@@ -52,10 +52,15 @@ class DenseDecoder:
     fused: the two RMSNorms of a layer run inside the GEMVs that read them
     (qmatmul_gemv_grouped_rmsnorm, qmatmul_gemv_swiglu_rmsnorm_f16; Q4/Q8
     weights, hidden <= 4096), with the residual stream alternating between
-    two buffers; otherwise each norm is a launch of its own."""
+    two buffers; otherwise each norm is a launch of its own.
+
+    rope_rows_interleaved: W_q and W_k were quantised from rows in
+    binding.rope_interleave_rows order; then (with fused) RoPE and the cache
+    append run as the epilogue of the q/k/v GEMV
+    (qmatmul_gemv_qkv_rmsnorm_rope): 5 launches per layer."""
 
     def __init__(self, cfg: DecoderConfig, emb: torch.Tensor, layers: List[LayerWeights], norm: torch.Tensor,
-                 lm_head: B.QWeight, max_len: int, fused: bool = True):
+                 lm_head: B.QWeight, max_len: int, fused: bool = True, rope_rows_interleaved: bool = False):
         self.cfg, self.emb, self.layers, self.norm, self.lm_head = cfg, emb, layers, norm, lm_head
         self.max_len = max_len
         dev = emb.device
@@ -67,6 +72,9 @@ class DenseDecoder:
             w.format in (B.Q4_G32, B.Q8_G32) for ly in layers for w in (ly.wq, ly.wk, ly.wv, ly.wg, ly.wu))
         self.x = torch.zeros(c.hidden, **f32)             # residual stream
         self.x2 = torch.zeros(c.hidden, **f32)            # its other buffer (fused norms)
+        self.rope_epi = rope_rows_interleaved
+        assert not self.rope_epi or self.fused, "the RoPE epilogue runs in the fused q/k/v GEMV"
+        self.rope_tab = B.qdec_rope_table(max_len, c.head_dim, c.theta, device=dev) if self.rope_epi else None
         self.h = torch.zeros(c.hidden, **f16)             # normed input of a projection
         self.q, self.k, self.v = torch.zeros(qd, **f32), torch.zeros(kvd, **f32), torch.zeros(kvd, **f32)
         self.q16 = torch.zeros((c.n_q_heads, c.head_dim), **f16)
@@ -91,15 +99,21 @@ class DenseDecoder:
         B.qdec_embed(self.emb, self.token, out=self.x, stream=s)
         if self.fused:
             for li, ly in enumerate(self.layers):
-                # x2 = x + y_ffn; q, k, v = W . norm(x2)
-                B.qmatmul_gemv_grouped_rmsnorm([ly.wq, ly.wk, ly.wv], self.x, ly.attn_norm, c.eps, self.x2,
-                                               residual=self.y_ffn if li else None, outs=[self.q, self.k, self.v],
-                                               stream=s)
-                # RoPE + cache append, then attention (folding the two into one
-                # launch, qattn_decode_rope_f16, measured slower: the fp64
-                # angles then sit ahead of the attention's first loads)
-                B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
-                                   q_out=self.q16, stream=s)
+                res = self.y_ffn if li else None
+                if self.rope_epi:
+                    # x2 = x + y_ffn; q, k, v = W . norm(x2), rotated, k and v into the caches
+                    B.qmatmul_gemv_qkv_rmsnorm_rope([ly.wq, ly.wk, ly.wv], self.x, ly.attn_norm, c.eps, self.x2, pos,
+                                                    self.rope_tab, self.q16, self.k_cache[li], self.v_cache[li],
+                                                    residual=res, stream=s)
+                else:
+                    # x2 = x + y_ffn; q, k, v = W . norm(x2)
+                    B.qmatmul_gemv_grouped_rmsnorm([ly.wq, ly.wk, ly.wv], self.x, ly.attn_norm, c.eps, self.x2,
+                                                   residual=res, outs=[self.q, self.k, self.v], stream=s)
+                    # RoPE + cache append, then attention (folding the two into one
+                    # launch, qattn_decode_rope_f16, measured slower: the fp64
+                    # angles then sit ahead of the attention's first loads)
+                    B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
+                                       q_out=self.q16, stream=s)
                 B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,
                                workspace=self.ws, stream=s)
                 B.qmatmul_gemv(ly.wo, self.attn16.view(-1), out=self.y_attn, stream=s)

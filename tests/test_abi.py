@@ -358,3 +358,22 @@ def test_attention_rope_fused_validation():
     assert call(kc=ctypes.c_void_p(0x50004)) == 3 and call(o=ctypes.c_void_p(0x50001)) == 3
     assert call(nb=need - 1) == 6
     assert B.qm_last_error()
+
+
+def test_qkv_rope_epilogue_validation():
+    L = B.lib()
+    p = ctypes.c_void_p(0x50000)
+    wq = B.empty_qweight(B.Q4_G32, B.LAYOUT_DEVICE, 1, 256, 256, device="cpu")
+    wk = B.empty_qweight(B.Q4_G32, B.LAYOUT_DEVICE, 1, 128, 256, device="cpu")
+    good = (B.CQWeight * 3)(wq.c(), wk.c(), wk.c())
+    bad = (B.CQWeight * 3)(wq.c(), wq.c(), wk.c())
+    call = lambda w=good, d=64, pos=3, mx=16, tab=p, qo=p, xo=ctypes.c_void_p(0x90000): \
+        L.qmatmul_gemv_qkv_rmsnorm_rope(w, p, None, p, 1e-6, xo, 4, 2, d, pos, mx, tab, qo, p, p, None)
+    assert call(w=bad) == 2                       # k rows != n_kv_heads * head_dim
+    assert call(d=96) == 2 and call(pos=16) == 2 and call(pos=-1) == 2
+    assert call(tab=None) == 1 and call(qo=None) == 1 and call(xo=p) == 1
+    assert call(tab=ctypes.c_void_p(0x50004)) == 3
+    assert L.qdec_rope_table(0, 64, 1e4, p, None) == 2 and L.qdec_rope_table(8, 80, 1e4, p, None) == 2
+    assert L.qdec_rope_table(8, 64, 1.0, p, None) == 1 and L.qdec_rope_table(8, 64, 1e4, None, None) == 1
+    assert L.qdec_rope_table(8, 64, 1e4, ctypes.c_void_p(0x50004), None) == 3
+    assert B.qm_last_error()

@@ -148,7 +148,7 @@ def test_embed_gathers_rows_and_flags_bad_ids():
 
 # ---------------------------------------------------------------- decode steps
 
-def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32)):
+def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32), interleave=False):
     """Seeded weights of a dense decoder, quantised on the device (library)
     and in the oracle from the same fp32 values."""
     ofmt, bfmt = fmts
@@ -156,7 +156,10 @@ def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32)):
 
     def proj(name, li, n, k):
         w = inputs.weights_np(inputs.seed_for(tag, li, name), (n, k), sigma=1.0 / math.sqrt(k))
-        dev = B.qm_repack(B.qm_quantise(torch.from_numpy(w).cuda(), bfmt), B.LAYOUT_DEVICE)
+        wd = torch.from_numpy(w).cuda()
+        if interleave and name in ("q", "k"):
+            wd = B.rope_interleave_rows(wd, n // cfg.head_dim, cfg.head_dim)
+        dev = B.qm_repack(B.qm_quantise(wd, bfmt), B.LAYOUT_DEVICE)
         q, s = O.quantise(w, ofmt)
         return dev, O.dequantise(O.pack(q, ofmt), s, ofmt).astype(np.float64)
 
@@ -180,9 +183,10 @@ def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32)):
     return dev_layers, torch.from_numpy(emb).cuda(), torch.from_numpy(norm).cuda(), head_dev, ref
 
 
-def _decoder(cfg, tag, max_len, fmts=(O.Q4, B.Q4_G32), fused=True):
-    layers, emb, norm, head, ref = _model(cfg, tag, fmts)
-    dec = DenseDecoder(cfg, emb, layers, norm, head, max_len, fused=fused)
+def _decoder(cfg, tag, max_len, fmts=(O.Q4, B.Q4_G32), fused=True, rope_epi=True):
+    rope_epi = rope_epi and fused
+    layers, emb, norm, head, ref = _model(cfg, tag, fmts, interleave=rope_epi)
+    dec = DenseDecoder(cfg, emb, layers, norm, head, max_len, fused=fused, rope_rows_interleaved=rope_epi)
     assert dec.fused == fused
     kc = np.zeros((cfg.layers, cfg.n_kv_heads, max_len, cfg.head_dim))
     vc = np.zeros_like(kc)
@@ -193,11 +197,12 @@ TINY = DecoderConfig(hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, inter=5
                      theta=1e4)
 
 
-@pytest.mark.parametrize("fused", [True, False])
-def test_decode_steps_teacher_forced_tiny(fused):
+@pytest.mark.parametrize("fused,rope_epi", [(True, True), (True, False), (False, False)])
+def test_decode_steps_teacher_forced_tiny(fused, rope_epi):
     """Ten teacher-forced steps: logits at every step, then the whole caches
-    (norms fused into the GEMVs, and as launches of their own)."""
-    dec, ref, kc, vc = _decoder(TINY, 21, 16, fused=fused)
+    (norms and RoPE fused into the q/k/v GEMV; norms fused only; every step
+    a launch of its own)."""
+    dec, ref, kc, vc = _decoder(TINY, 21, 16, fused=fused, rope_epi=rope_epi)
     for pos, t in enumerate([5, 17, 999, 0, 42, 42, 7, 300, 1, 2]):
         dec.token.fill_(t)
         dec.step(pos)
@@ -378,3 +383,43 @@ def test_attention_rope_fused_equals_two_launches(d, hq, hkv, pos):
     assert torch.all(diff[:, :pos] == False) and torch.all(diff[:, pos + 1:] == False)    # only row pos written
     err = (o1.float() - o2.float()).abs().max().item()
     assert err <= 2e-3 * o1.float().abs().max().item()
+
+
+@pytest.mark.parametrize("fmt", [B.Q4_G32, B.Q8_G32])
+@pytest.mark.parametrize("d,hq,hkv,k", [(64, 4, 2, 256), (128, 16, 8, 1024), (64, 32, 8, 2048), (128, 24, 8, 3072)])
+@pytest.mark.parametrize("pos", [0, 5, 1000])
+def test_gemv_qkv_rmsnorm_rope_matches_separate_launches(fmt, d, hq, hkv, k, pos):
+    """The RoPE epilogue on interleaved rows against the grouped norm GEMV on
+    the natural rows followed by qdec_rope_append: caches and q within one
+    fp16 ulp (fp32 rotations of the same products), rows other than pos
+    untouched, x_out bit for bit."""
+    max_len, theta = 1024, 1e6
+    xd, rd, gd, _, _, _ = _norm_inputs(k, 43, True)
+    w = [inputs.weights_dev(inputs.seed_for(43, k, t), (n, k), sigma=1.0 / math.sqrt(k))
+         for t, n in (("q", hq * d), ("k", hkv * d), ("v", hkv * d))]
+    plain = [B.qm_repack(B.qm_quantise(a, fmt), B.LAYOUT_DEVICE) for a in w]
+    inter = [B.qm_repack(B.qm_quantise(B.rope_interleave_rows(a, n // d, d), fmt), B.LAYOUT_DEVICE)
+             for a, n in ((w[0], hq * d), (w[1], hkv * d))] + [plain[2]]
+    kc1 = inputs.activations_dev(inputs.seed_for(43, pos, "k"), (hkv, max_len, d))
+    vc1 = inputs.activations_dev(inputs.seed_for(43, pos, "v"), (hkv, max_len, d))
+    kc2, vc2 = kc1.clone(), vc1.clone()
+    xo1, xo2 = torch.empty(k, device="cuda"), torch.empty(k, device="cuda")
+    ys = B.qmatmul_gemv_grouped_rmsnorm(plain, xd, gd, 1e-6, xo1, residual=rd)
+    q1 = B.qdec_rope_append(ys[0], ys[1], ys[2], pos, theta, kc1, vc1)
+    tab = B.qdec_rope_table(max_len, d, theta)
+    q2 = torch.empty((hq, d), dtype=torch.float16, device="cuda")
+    B.qmatmul_gemv_qkv_rmsnorm_rope(inter, xd, gd, 1e-6, xo2, pos, tab, q2, kc2, vc2, residual=rd)
+    assert torch.equal(xo1, xo2)
+    for a, b in ((q1, q2), (kc1[:, pos], kc2[:, pos]), (vc1[:, pos], vc2[:, pos])):
+        a, b = a.float(), b.float()
+        assert torch.all((a - b).abs() <= 2.0 ** -9 * a.abs() + 1e-6 * a.abs().max()), (a - b).abs().max()
+    other = torch.ones(max_len, dtype=torch.bool)
+    other[pos] = False
+    assert torch.equal(kc1[:, other], kc2[:, other]) and torch.equal(vc1[:, other], vc2[:, other])
+
+
+def test_rope_table_matches_the_rotation_angles():
+    t = B.qdec_rope_table(300, 64, 5e5).cpu().numpy().astype(np.float64)
+    p, i = np.meshgrid(np.arange(300), np.arange(32), indexing="ij")
+    ang = p * 5e5 ** (-2.0 * i / 64)
+    assert np.abs(t[..., 0] - np.cos(ang)).max() <= 1e-7 and np.abs(t[..., 1] - np.sin(ang)).max() <= 1e-7
