@@ -6,7 +6,9 @@
  * dequantise-into-LDS + fp16 MFMA GEMM for prefill, and the top-k-routed
  * grouped expert GEMM of a mixture-of-experts layer; plus grouped-query
  * attention over a pre-allocated KV cache for decode and causal
- * FlashAttention for prefill chunks (BaseRT, Sec. 3.3
+ * FlashAttention for prefill chunks; plus the rest of a dense decode step
+ * (embedding, RMSNorm, RoPE with the cache append, greedy sampling), folded
+ * into the matmuls where that removes a launch (BaseRT, Sec. 3.3
  * "Kernel Fusion and Specialisation": one GEMV (M = 1) and one GEMM (M > 1)
  * kernel per quantisation format, dequantisation inside the inner loop and
  * never materialised; Sec. 3.4 "Prefill": tiled GEMM for prompts, bounded
@@ -15,8 +17,8 @@
  *
  * Conventions shared by every entry point
  *  - Pointers named d_* / device buffers are HIP device pointers; the caller
- *    owns every buffer.  The library never allocates, frees or retains memory
- *    (Sec. 3.2, "Zero-Allocation Decode Loop").
+ *    owns every buffer, workspaces included.  The library never allocates,
+ *    frees or retains memory (Sec. 3.2, "Zero-Allocation Decode Loop").
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *    QM_OK means "validated and enqueued on stream"; nothing is synchronised.
  *  - Arguments are validated on the host before anything is enqueued.  On an
