@@ -341,12 +341,26 @@ def extra_tg(torch, B, inputs, workloads, steps, warmup, lib):
     # epilogue; attention is one launch for caches of up to 128 rows) + 5.
     for model, cfg_id in ((workloads.QWEN3_06B_DECODER, 1), (workloads.LLAMA32_1B_DECODER, 3),
                           (workloads.LLAMA32_3B_DECODER, 2)):
-        dec = build_decoder(model, cfg_id, B.Q4_G32, 128, torch, B, inputs)
+        dec = build_decoder(model, cfg_id, B.Q4_G32, 640, torch, B, inputs)
         tps, t = tg_tokens_per_s(torch, dec, 128, 3)
         key = model["name"] + "_tg128_q4"
         out[key] = {"tokens_per_s": round(tps, 1), "ms_per_token": round(1e3 / tps, 4),
                     "launches_per_token": 5 * model["layers"] + 5, "ms_per_128_tokens": round(t * 1e3, 3)}
         log(f"{key}: {out[key]}")
+        # pp512: a 512-token prompt in one chunk (prefill GEMMs, causal
+        # attention, the last token's logits and greedy id), one graph
+        toks = torch.from_numpy(inputs.np.random.default_rng(cfg_id).integers(
+            0, model["vocab"], 512).astype(inputs.np.int32)).cuda()
+        dec.prefill(toks)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            dec.prefill(toks)
+        t, _ = time_graph(torch, g, 5, 1)
+        key = model["name"] + "_pp512_q4"
+        out[key] = {"tokens_per_s": round(512 * 5 / t, 1), "ms_per_prompt": round(t / 5 * 1e3, 3)}
+        log(f"{key}: {out[key]}")
+        del g
         del dec
         torch.cuda.empty_cache()
 

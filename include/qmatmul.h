@@ -194,6 +194,38 @@ qm_status qmatmul_gemv_swiglu_rmsnorm_f16(const qm_qweight* w_gate, const qm_qwe
                                           const float* residual, const uint16_t* gain, float eps, float* x_out,
                                           uint16_t* h, void* stream);
 
+/* ---- Glue of a prompt (prefill) chunk of m tokens (Sec. 3.4: chunked
+ * prefill; the same operations as a decode step over m rows, with the GEMMs
+ * and qattn_prefill between them). */
+
+/* x[r] = table[tokens[r]] (fp16 -> fp32), r < m; x: fp32 [m][hidden];
+ * tokens: int32 [m] on the device; ids outside [0, vocab) give NaN rows.
+ * 0 <= m <= 32768. */
+qm_status qdec_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* tokens, int64_t m,
+                          float* x, void* stream);
+
+/* RoPE and the cache append for tokens r < m at positions p0 + r:
+ * q: fp32 [m][n_q_heads * head_dim], k, v: fp32 [m][n_kv_heads * head_dim]
+ * (GEMM outputs; with interleaved = 1 each head's dimensions of q and k are
+ * in the interleaved order of qmatmul_gemv_qkv_rmsnorm_rope's weights);
+ * q_out: fp16 [n_q_heads][m][head_dim] (qattn_prefill's layout), rotated;
+ * cache rows p0 .. p0 + m - 1 written (keys rotated).  Rotation as
+ * qdec_rope_append.  head_dim 64 or 128; 1 <= m <= 32768;
+ * p0 + m <= max_len <= 262144; theta > 1. */
+qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, int32_t n_q_heads,
+                                int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len,
+                                float theta, int32_t interleaved, uint16_t* q_out, uint16_t* k_cache,
+                                uint16_t* v_cache, void* stream);
+
+/* out[r][h * head_dim + d] = fp16_RNE(o[h][r][d]): qattn_prefill's output
+ * as the output projection's GEMM input. */
+qm_status qdec_heads_to_rows_f16(const float* o, int32_t n_heads, int64_t m, int32_t head_dim, uint16_t* out,
+                                 void* stream);
+
+/* out[i] = fp16_RNE(silu(gate[i]) * up[i]), i < n (fp32 in): the SwiGLU of
+ * the prompt's gate/up GEMM outputs. */
+qm_status qdec_swiglu_f16(const float* gate, const float* up, int64_t n, uint16_t* out, void* stream);
+
 /* (cos, sin) table of the rotary embedding for every position of a cache:
  * table[p][i] = (cos a, sin a), a = p * theta^(-2i/head_dim), i < head_dim/2,
  * p < max_len, angle in fp64, fp32 entries (the values qdec_rope_append

@@ -32,7 +32,8 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
            "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
            "qmatmul_gemv_swiglu_rmsnorm_f16", "qattn_decode_rope_f16", "qdec_rope_table",
-           "qmatmul_gemv_qkv_rmsnorm_rope")
+           "qmatmul_gemv_qkv_rmsnorm_rope", "qdec_embed_rows", "qdec_rope_append_rows", "qdec_heads_to_rows_f16",
+           "qdec_swiglu_f16")
 
 
 class QmError(RuntimeError):
@@ -81,6 +82,10 @@ def lib() -> ctypes.CDLL:
             "qdec_embed": [vp, i64, i64, vp, vp, vp],
             "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
             "qdec_rope_table": [i64, i32, ctypes.c_float, vp, vp],
+            "qdec_embed_rows": [vp, i64, i64, vp, i64, vp, vp],
+            "qdec_rope_append_rows": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, i32, vp, vp, vp, vp],
+            "qdec_heads_to_rows_f16": [vp, i32, i64, i32, vp, vp],
+            "qdec_swiglu_f16": [vp, vp, i64, vp, vp],
             "qmatmul_gemv_qkv_rmsnorm_rope": [W, vp, vp, vp, ctypes.c_float, vp, i32, i32, i32, i64, i64, vp, vp, vp,
                                               vp, vp],
             "qattn_decode_rope_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, ctypes.c_float, vp, vp,
@@ -263,6 +268,51 @@ def qmatmul_gemv_swiglu_rmsnorm_f16(w_gate: QWeight, w_up: QWeight, x: torch.Ten
     _check(lib().qmatmul_gemv_swiglu_rmsnorm_f16(ctypes.byref(w_gate.c()), ctypes.byref(w_up.c()), _ptr(x),
                                                  _ptr(residual), _ptr(gain), eps, _ptr(x_out), _ptr(out),
                                                  _stream(stream)))
+    return out
+
+
+def qdec_embed_rows(table: torch.Tensor, tokens: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """table fp16 [vocab][hidden], tokens int32 [m] (device) -> fp32 [m][hidden]."""
+    vocab, hidden = table.shape
+    m = tokens.numel()
+    assert tokens.dtype == torch.int32 and table.dtype == torch.float16
+    if out is None:
+        out = torch.empty((m, hidden), dtype=torch.float32, device=table.device)
+    _check(lib().qdec_embed_rows(_ptr(table), vocab, hidden, _ptr(tokens), m, _ptr(out), _stream(stream)))
+    return out
+
+
+def qdec_rope_append_rows(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, p0: int, theta: float,
+                          k_cache: torch.Tensor, v_cache: torch.Tensor, interleaved: bool = False,
+                          q_out: Optional[torch.Tensor] = None, stream=None):
+    """q fp32 [m][Hq*D], k, v fp32 [m][Hkv*D] -> fp16 [Hq][m][D]; cache rows p0..p0+m-1."""
+    hkv, max_len, d = k_cache.shape
+    m = q.shape[0]
+    hq = q.shape[1] // d
+    assert q.dtype == k.dtype == v.dtype == torch.float32 and k.shape == v.shape == (m, hkv * d)
+    if q_out is None:
+        q_out = torch.empty((hq, m, d), dtype=torch.float16, device=q.device)
+    _check(lib().qdec_rope_append_rows(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, m, p0, max_len, theta,
+                                       1 if interleaved else 0, _ptr(q_out), _ptr(k_cache), _ptr(v_cache),
+                                       _stream(stream)))
+    return q_out
+
+
+def qdec_heads_to_rows_f16(o: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """fp32 [H][m][D] -> fp16 [m][H*D]."""
+    h, m, d = o.shape
+    if out is None:
+        out = torch.empty((m, h * d), dtype=torch.float16, device=o.device)
+    _check(lib().qdec_heads_to_rows_f16(_ptr(o), h, m, d, _ptr(out), _stream(stream)))
+    return out
+
+
+def qdec_swiglu_f16(gate: torch.Tensor, up: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    """fp16(silu(gate) * up), elementwise, fp32 in."""
+    assert gate.dtype == up.dtype == torch.float32 and gate.shape == up.shape
+    if out is None:
+        out = torch.empty(gate.shape, dtype=torch.float16, device=gate.device)
+    _check(lib().qdec_swiglu_f16(_ptr(gate), _ptr(up), gate.numel(), _ptr(out), _stream(stream)))
     return out
 
 

@@ -286,6 +286,56 @@ qm_status qmatmul_gemv_grouped_rmsnorm(int32_t count, const qm_qweight* w, const
                   name);
 }
 
+qm_status qdec_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* tokens, int64_t m,
+                          float* x, void* stream) {
+  if (vocab < 1 || vocab > INT32_MAX || hidden < 1 || hidden > (int64_t{1} << 20) || m < 0 || m > 32768)
+    return fail(QM_ESHAPE, "qdec_embed_rows: need 1 <= vocab < 2^31, 1 <= hidden <= 2^20, 0 <= m <= 32768");
+  if (m > 0 && (!table || !tokens || !x)) return fail(QM_EINVAL, "qdec_embed_rows: null pointer");
+  if (!aligned2(table) || !aligned4(tokens) || !aligned4(x))
+    return fail(QM_EALIGN, "qdec_embed_rows: table 2-byte, tokens and x 4-byte aligned");
+  return launched(launch_embed_rows(table, vocab, hidden, tokens, m, x, static_cast<hipStream_t>(stream)),
+                  "qdec_embed_rows");
+}
+
+qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, int32_t n_q_heads,
+                                int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len,
+                                float theta, int32_t interleaved, uint16_t* q_out, uint16_t* k_cache,
+                                uint16_t* v_cache, void* stream) {
+  const char* name = "qdec_rope_append_rows";
+  if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "%s: head_dim=%d must be 64 or 128", name, head_dim);
+  if (n_q_heads < 1 || n_q_heads > 1024 || n_kv_heads < 1 || n_kv_heads > 1024)
+    return fail(QM_ESHAPE, "%s: head counts must be in [1, 1024]", name);
+  if (m < 1 || m > 32768 || p0 < 0 || max_len > kAttnMaxLen || p0 + m > max_len)
+    return fail(QM_ESHAPE, "%s: need 1 <= m <= 32768, p0 >= 0, p0 + m <= max_len <= %lld", name,
+                (long long)kAttnMaxLen);
+  if (!(theta > 1.0f) || theta == INFINITY) return fail(QM_EINVAL, "%s: theta must be finite and > 1", name);
+  if (interleaved != 0 && interleaved != 1) return fail(QM_EINVAL, "%s: interleaved must be 0 or 1", name);
+  if (!q || !k || !v || !q_out || !k_cache || !v_cache) return fail(QM_EINVAL, "%s: null pointer", name);
+  if (!aligned4(q) || !aligned4(k) || !aligned4(v) || !aligned2(q_out) || !aligned2(k_cache) || !aligned2(v_cache))
+    return fail(QM_EALIGN, "%s: q, k, v 4-byte, q_out and caches 2-byte aligned", name);
+  return launched(launch_rope_append_rows(q, k, v, n_q_heads, n_kv_heads, head_dim, m, p0, max_len, theta,
+                                          interleaved, q_out, k_cache, v_cache, static_cast<hipStream_t>(stream)),
+                  name);
+}
+
+qm_status qdec_heads_to_rows_f16(const float* o, int32_t n_heads, int64_t m, int32_t head_dim, uint16_t* out,
+                                 void* stream) {
+  if (n_heads < 1 || n_heads > 1024 || m < 1 || m > 65536 || head_dim < 1 || head_dim > 256)
+    return fail(QM_ESHAPE, "qdec_heads_to_rows_f16: need 1 <= n_heads <= 1024, 1 <= m <= 65536, 1 <= head_dim <= 256");
+  if (!o || !out) return fail(QM_EINVAL, "qdec_heads_to_rows_f16: null pointer");
+  if (!aligned4(o) || !aligned2(out)) return fail(QM_EALIGN, "qdec_heads_to_rows_f16: o 4-byte, out 2-byte aligned");
+  return launched(launch_heads_to_rows(o, n_heads, m, head_dim, out, static_cast<hipStream_t>(stream)),
+                  "qdec_heads_to_rows_f16");
+}
+
+qm_status qdec_swiglu_f16(const float* gate, const float* up, int64_t n, uint16_t* out, void* stream) {
+  if (n < 0) return fail(QM_ESHAPE, "qdec_swiglu_f16: n must be >= 0");
+  if (n > 0 && (!gate || !up || !out)) return fail(QM_EINVAL, "qdec_swiglu_f16: null pointer");
+  if (!aligned4(gate) || !aligned4(up) || !aligned2(out))
+    return fail(QM_EALIGN, "qdec_swiglu_f16: gate and up 4-byte, out 2-byte aligned");
+  return launched(launch_swiglu(gate, up, n, out, static_cast<hipStream_t>(stream)), "qdec_swiglu_f16");
+}
+
 qm_status qdec_rope_table(int64_t max_len, int32_t head_dim, float theta, float* table, void* stream) {
   if ((head_dim != 64 && head_dim != 128) || max_len < 1 || max_len > kAttnMaxLen)
     return fail(QM_ESHAPE, "qdec_rope_table: head_dim 64 or 128 and 1 <= max_len <= %lld", (long long)kAttnMaxLen);

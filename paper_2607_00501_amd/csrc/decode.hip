@@ -196,6 +196,66 @@ __global__ __launch_bounds__(256) void rope_table_kernel(int64_t max_len, int d,
     table[e] = rope_cos_sin(e / (d / 2), static_cast<int>(e % (d / 2)), d, log2_theta);
 }
 
+// Prompt (prefill) glue: the same operations over m tokens.
+// x[r] = table[tokens[r]] (NaN rows for ids outside the vocabulary).
+__global__ __launch_bounds__(256) void embed_rows_kernel(const uint16_t* __restrict__ table, int64_t vocab,
+                                                         int64_t hidden, const int32_t* __restrict__ tokens,
+                                                         float* __restrict__ x) {
+  const int64_t r = blockIdx.x;
+  const int32_t t = tokens[r];
+  const bool ok = t >= 0 && t < vocab;
+  const uint16_t* row = table + (ok ? t : 0) * hidden;
+  for (int64_t i = threadIdx.x; i < hidden; i += 256) x[r * hidden + i] = ok ? h2f(row[i]) : __builtin_nanf("");
+}
+
+// Grid (head, token): token r at position p0 + r.  Inputs are the projection
+// outputs [m][heads * D] (each head's dimensions interleaved when
+// `interleaved`: column 2i = dimension i, 2i + 1 = dimension i + D/2);
+// queries go to q_out [Hq][m][D] (the prefill attention's layout), keys and
+// values to cache rows p0 + r.
+__global__ void rope_append_rows_kernel(const float* __restrict__ q, const float* __restrict__ k,
+                                        const float* __restrict__ v, int hq, int hkv, int d, int64_t m, int64_t p0,
+                                        int64_t max_len, double log2_theta, int interleaved,
+                                        uint16_t* __restrict__ q_out, uint16_t* __restrict__ kc,
+                                        uint16_t* __restrict__ vc) {
+  const int h = blockIdx.x, i = threadIdx.x, half = d / 2;
+  const int64_t r = blockIdx.y, pos = p0 + r;
+  if (h >= hq + hkv) {
+    const int kh = h - hq - hkv;
+    const float* src = v + r * hkv * d + kh * d;
+    uint16_t* dst = vc + (static_cast<int64_t>(kh) * max_len + pos) * d;
+    dst[i] = f2h(src[i]);
+    dst[i + half] = f2h(src[i + half]);
+    return;
+  }
+  const float2 cs = rope_cos_sin(pos, i, d, log2_theta);
+  const float* src = h < hq ? q + r * hq * d + h * d : k + r * hkv * d + (h - hq) * d;
+  uint16_t* dst = h < hq ? q_out + (static_cast<int64_t>(h) * m + r) * d
+                         : kc + (static_cast<int64_t>(h - hq) * max_len + pos) * d;
+  const float a = interleaved ? src[2 * i] : src[i], b = interleaved ? src[2 * i + 1] : src[i + half];
+  dst[i] = f2h(rope_low(a, b, cs.x, cs.y));
+  dst[i + half] = f2h(rope_high(a, b, cs.x, cs.y));
+}
+
+// o [H][m][D] fp32 -> out [m][H * D] fp16 (the output projection's input).
+__global__ __launch_bounds__(256) void heads_to_rows_kernel(const float* __restrict__ o, int h, int64_t m, int d,
+                                                            uint16_t* __restrict__ out) {
+  const int64_t n = static_cast<int64_t>(h) * m * d;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) {
+    const int64_t r = e / (static_cast<int64_t>(h) * d), c = e % (static_cast<int64_t>(h) * d);
+    out[e] = f2h(o[((c / d) * m + r) * d + c % d]);
+  }
+}
+
+// out = fp16(silu(g) * u) elementwise.
+__global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ g, const float* __restrict__ u,
+                                                     int64_t n, uint16_t* __restrict__ out) {
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) {
+    const float a = g[e];
+    out[e] = f2h(a / (1.0f + expf(-a)) * u[e]);
+  }
+}
+
 __global__ __launch_bounds__(256) void cast_f16_kernel(const float* __restrict__ x, int64_t n,
                                                        uint16_t* __restrict__ y) {
   for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) y[i] = f2h(x[i]);
@@ -337,6 +397,35 @@ hipError_t launch_rope_append(const float* q, const float* k, const float* v, in
 hipError_t launch_rope_table(int64_t max_len, int32_t d, float theta, float* table, hipStream_t st) {
   hipLaunchKernelGGL(rope_table_kernel, dim3(spread_blocks(max_len * (d / 2))), dim3(256), 0, st, max_len, d,
                      std::log2(static_cast<double>(theta)), reinterpret_cast<float2*>(table));
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* tokens, int64_t m,
+                             float* x, hipStream_t st) {
+  if (m == 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_rows_kernel, dim3(static_cast<unsigned>(m)), dim3(256), 0, st, table, vocab, hidden, tokens,
+                     x);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_append_rows(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
+                                   int64_t m, int64_t p0, int64_t max_len, float theta, int32_t interleaved,
+                                   uint16_t* q_out, uint16_t* kc, uint16_t* vc, hipStream_t st) {
+  hipLaunchKernelGGL(rope_append_rows_kernel, dim3(static_cast<unsigned>(hq + 2 * hkv), static_cast<unsigned>(m)),
+                     dim3(d / 2), 0, st, q, k, v, hq, hkv, d, m, p0, max_len, std::log2(static_cast<double>(theta)),
+                     interleaved, q_out, kc, vc);
+  return hipGetLastError();
+}
+
+hipError_t launch_heads_to_rows(const float* o, int32_t h, int64_t m, int32_t d, uint16_t* out, hipStream_t st) {
+  hipLaunchKernelGGL(heads_to_rows_kernel, dim3(spread_blocks(static_cast<int64_t>(h) * m * d)), dim3(256), 0, st, o,
+                     h, m, d, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu(const float* g, const float* u, int64_t n, uint16_t* out, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(swiglu_kernel, dim3(spread_blocks(n)), dim3(256), 0, st, g, u, n, out);
   return hipGetLastError();
 }
 

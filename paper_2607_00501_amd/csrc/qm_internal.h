@@ -162,6 +162,13 @@ hipError_t launch_rope_append(const float* q, const float* k, const float* v, in
                               uint16_t* vc, hipStream_t st);
 hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t st);
 hipError_t launch_rope_table(int64_t max_len, int32_t d, float theta, float* table, hipStream_t st);
+hipError_t launch_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* tokens, int64_t m,
+                             float* x, hipStream_t st);
+hipError_t launch_rope_append_rows(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
+                                   int64_t m, int64_t p0, int64_t max_len, float theta, int32_t interleaved,
+                                   uint16_t* q_out, uint16_t* kc, uint16_t* vc, hipStream_t st);
+hipError_t launch_heads_to_rows(const float* o, int32_t h, int64_t m, int32_t d, uint16_t* out, hipStream_t st);
+hipError_t launch_swiglu(const float* g, const float* u, int64_t n, uint16_t* out, hipStream_t st);
 
 // Epilogue of the fused q/k/v GEMV that applies RoPE and fills the caches:
 // W_q and W_k hold each head's rows interleaved (row 2i = row i, row 2i + 1

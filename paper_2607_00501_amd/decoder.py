@@ -140,3 +140,26 @@ class DenseDecoder:
         B.qdec_rmsnorm(self.x, self.norm, self.cfg.eps, residual=self.y_ffn, out=self.h, stream=s)
         B.qmatmul_gemv(self.lm_head, self.h, out=self.logits, stream=s)
         B.qdec_argmax(self.logits, out=self.token, workspace=self.argmax_ws, stream=s)
+
+    def prefill(self, tokens: torch.Tensor, p0: int = 0, stream=None) -> None:
+        """A prompt chunk (Sec. 3.4): tokens (int32 [m], device) at positions
+        p0 .. p0 + m - 1 through every layer with the prefill GEMMs and
+        causal attention; writes those cache rows, the last token's logits
+        and the greedy next token into self.token."""
+        c, s = self.cfg, stream
+        m = tokens.numel()
+        x = B.qdec_embed_rows(self.emb, tokens, stream=s)                 # fp32 [m][H] residual stream
+        y = None
+        for li, ly in enumerate(self.layers):
+            h = B.qdec_rmsnorm(x, ly.attn_norm, c.eps, residual=y, stream=s)
+            q, k, v = B.qmatmul_gemm_grouped([ly.wq, ly.wk, ly.wv], h, stream=s)
+            qh = B.qdec_rope_append_rows(q, k, v, p0, c.theta, self.k_cache[li], self.v_cache[li],
+                                         interleaved=self.rope_epi, stream=s)
+            o = B.qattn_prefill(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, stream=s)
+            ya = B.qmatmul_gemm(ly.wo, B.qdec_heads_to_rows_f16(o, stream=s), stream=s)
+            h = B.qdec_rmsnorm(x, ly.ffn_norm, c.eps, residual=ya, stream=s)
+            g, u = B.qmatmul_gemm_grouped([ly.wg, ly.wu], h, stream=s)
+            y = B.qmatmul_gemm(ly.wd, B.qdec_swiglu_f16(g, u, stream=s), stream=s)
+        B.qdec_rmsnorm(x[m - 1], self.norm, c.eps, residual=y[m - 1], out=self.h, stream=s)
+        B.qmatmul_gemv(self.lm_head, self.h, out=self.logits, stream=s)
+        B.qdec_argmax(self.logits, out=self.token, workspace=self.argmax_ws, stream=s)

@@ -377,3 +377,18 @@ def test_qkv_rope_epilogue_validation():
     assert L.qdec_rope_table(8, 64, 1.0, p, None) == 1 and L.qdec_rope_table(8, 64, 1e4, None, None) == 1
     assert L.qdec_rope_table(8, 64, 1e4, ctypes.c_void_p(0x50004), None) == 3
     assert B.qm_last_error()
+
+
+def test_prefill_glue_validation():
+    L = B.lib()
+    p = ctypes.c_void_p(0x50000)
+    assert L.qdec_embed_rows(p, 100, 64, p, 40000, p, None) == 2 and L.qdec_embed_rows(p, 0, 64, p, 4, p, None) == 2
+    assert L.qdec_embed_rows(None, 100, 64, p, 4, p, None) == 1
+    rr = lambda d=64, m=8, p0=0, mx=64, il=0, theta=1e4, qo=p: L.qdec_rope_append_rows(
+        p, p, p, 4, 2, d, m, p0, mx, theta, il, qo, p, p, None)
+    assert rr(d=80) == 2 and rr(m=0) == 2 and rr(p0=60) == 2 and rr(il=2) == 1 and rr(theta=0.5) == 1
+    assert rr(qo=None) == 1 and rr(qo=ctypes.c_void_p(0x50001)) == 3
+    assert L.qdec_heads_to_rows_f16(p, 0, 4, 64, p, None) == 2 and L.qdec_heads_to_rows_f16(None, 4, 4, 64, p, None) == 1
+    assert L.qdec_swiglu_f16(p, p, -1, p, None) == 2 and L.qdec_swiglu_f16(None, p, 4, p, None) == 1
+    assert L.qdec_swiglu_f16(p, p, 4, ctypes.c_void_p(0x50001), None) == 3
+    assert B.qm_last_error()

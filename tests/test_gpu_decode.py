@@ -423,3 +423,81 @@ def test_rope_table_matches_the_rotation_angles():
     p, i = np.meshgrid(np.arange(300), np.arange(32), indexing="ij")
     ang = p * 5e5 ** (-2.0 * i / 64)
     assert np.abs(t[..., 0] - np.cos(ang)).max() <= 1e-7 and np.abs(t[..., 1] - np.sin(ang)).max() <= 1e-7
+
+
+# ---------------------------------------------------------------- prompt chunks
+
+def test_prefill_glue_kernels():
+    rng = np.random.default_rng(50)
+    # embedding rows
+    table = inputs.activations_np(51, (300, 64))
+    toks = np.array([0, 299, 5, -3, 7], np.int32)
+    x = B.qdec_embed_rows(torch.from_numpy(table).cuda(), torch.from_numpy(toks).cuda()).cpu().numpy()
+    assert np.array_equal(x[[0, 1, 2, 4]], table[[0, 299, 5, 7]].astype(np.float32)) and np.all(np.isnan(x[3]))
+    # heads -> rows
+    o = rng.standard_normal((6, 33, 64)).astype(np.float32)
+    r = B.qdec_heads_to_rows_f16(torch.from_numpy(o).cuda()).cpu().numpy()
+    assert np.array_equal(r, o.transpose(1, 0, 2).reshape(33, 6 * 64).astype(np.float16))
+    # swiglu
+    g = (rng.standard_normal(5000) * 4).astype(np.float32)
+    u = rng.standard_normal(5000).astype(np.float32)
+    h = B.qdec_swiglu_f16(torch.from_numpy(g).cuda(), torch.from_numpy(u).cuda()).float().cpu().numpy()
+    ref = O.silu(g.astype(np.float64)) * u
+    assert np.all(np.abs(h - ref) <= 2.0 ** -10 * np.abs(ref) + 1e-6)
+
+
+@pytest.mark.parametrize("interleaved", [False, True])
+@pytest.mark.parametrize("d,m,p0", [(64, 37, 0), (128, 100, 20)])
+def test_rope_append_rows_matches_one_token_at_a_time(interleaved, d, m, p0):
+    """Every row r equals qdec_rope_append at position p0 + r (same kernel
+    arithmetic), for natural and interleaved projection columns."""
+    hq, hkv, max_len, theta = 4, 2, 256, 1e4
+    rng = np.random.default_rng(d + m)
+    q = torch.from_numpy(rng.standard_normal((m, hq * d)).astype(np.float32)).cuda()
+    k = torch.from_numpy(rng.standard_normal((m, hkv * d)).astype(np.float32)).cuda()
+    v = torch.from_numpy(rng.standard_normal((m, hkv * d)).astype(np.float32)).cuda()
+    kc1 = torch.zeros((hkv, max_len, d), dtype=torch.float16, device="cuda")
+    vc1, kc2, vc2 = kc1.clone(), kc1.clone(), kc1.clone()
+    qi, ki = q, k
+    if interleaved:      # columns of each head in the interleaved order
+        perm = lambda t, heads: t.reshape(m, heads, 2, d // 2).transpose(2, 3).reshape(m, heads * d).contiguous()
+        qi, ki = perm(q, hq), perm(k, hkv)
+    qo = B.qdec_rope_append_rows(qi, ki, v, p0, theta, kc1, vc1, interleaved=interleaved)
+    for r in range(m):
+        q1 = B.qdec_rope_append(q[r].contiguous(), k[r].contiguous(), v[r].contiguous(), p0 + r, theta, kc2, vc2)
+        assert torch.equal(qo[:, r], q1), r
+    assert torch.equal(kc1, kc2) and torch.equal(vc1, vc2)
+
+
+@pytest.mark.parametrize("rope_epi", [False, True])
+def test_prefill_then_decode_matches_oracle(rope_epi):
+    """A prompt of 13 tokens through the prefill path (GEMMs, causal
+    attention), then three decode steps: every step's logits and the caches
+    against the oracle's token-by-token steps (GEMM tier: fp16 MFMA operands)."""
+    dec, ref, kc, vc = _decoder(TINY, 25, 32, rope_epi=rope_epi)
+    toks = [5, 17, 999, 0, 42, 42, 7, 300, 1, 2, 64, 65, 998]
+    for p, t in enumerate(toks):
+        want = O.decode_step(ref, t, p, kc, vc)
+    dec.prefill(torch.tensor(toks, dtype=torch.int32, device="cuda"))
+    assert rel_err(dec.logits.cpu().numpy(), want) <= 1e-2
+    n = len(toks)
+    assert rel_err(dec.k_cache[:, :, :n].cpu().numpy().astype(np.float64), kc[:, :, :n]) <= 1e-2
+    assert rel_err(dec.v_cache[:, :, :n].cpu().numpy().astype(np.float64), vc[:, :, :n]) <= 1e-2
+    for p, t in enumerate([3, 4, 5], start=n):
+        dec.token.fill_(t)
+        dec.step(p)
+        assert rel_err(dec.logits.cpu().numpy(), O.decode_step(ref, t, p, kc, vc)) <= 1e-2, p
+
+
+def test_prefill_chunks_match_one_chunk():
+    """Two chunks (positions 0..19, then 20..44) give the caches and logits
+    of one 45-token chunk, to the GEMM tier."""
+    cfg = DecoderConfig(hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=128, inter=1024, vocab=2000, layers=2)
+    toks = torch.from_numpy(np.random.default_rng(52).integers(0, 2000, 45).astype(np.int32)).cuda()
+    a, _, _, _ = _decoder(cfg, 26, 64)
+    b, _, _, _ = _decoder(cfg, 26, 64)
+    a.prefill(toks)
+    b.prefill(toks[:20].contiguous())
+    b.prefill(toks[20:].contiguous(), p0=20)
+    assert rel_err(b.logits.cpu().numpy(), a.logits.cpu().numpy().astype(np.float64)) <= 1e-2
+    assert rel_err(b.k_cache[:, :, :45].float().cpu().numpy(), a.k_cache[:, :, :45].float().cpu().numpy().astype(np.float64)) <= 1e-2
