@@ -423,14 +423,21 @@ def decode_step(model: dict, token: int, pos: int, k_cache: np.ndarray, v_cache:
     interfaces are fp16: the normed inputs of every projection, q after
     RoPE, the new K / V rows (written into k_cache / v_cache [L][Hkv][T][D]
     at row pos), the attention output and the SwiGLU output.  The residual
-    stream stays fp32 on the GPU and fp64 here.
+    stream stays fp32 on the GPU and fp64 here.  A layer with "q_norm" and
+    "k_norm" gains ([D], the Qwen3 layer) RMS-normalises every query and key
+    head over its D dimensions before RoPE.
     """
     hq, hkv, d, eps, theta = model["hq"], model["hkv"], model["d"], model["eps"], model["theta"]
     x = np.asarray(model["emb"][token], dtype=np.float64)
     for li, ly in enumerate(model["layers"]):
         h = f16(rmsnorm(x, ly["attn_norm"], eps))
-        q = rope((ly["wq"] @ h).reshape(hq, d), pos, theta)
-        k = rope((ly["wk"] @ h).reshape(hkv, d), pos, theta)
+        q = (ly["wq"] @ h).reshape(hq, d)
+        k = (ly["wk"] @ h).reshape(hkv, d)
+        if "q_norm" in ly:
+            q = np.stack([rmsnorm(r, ly["q_norm"], eps) for r in q])
+            k = np.stack([rmsnorm(r, ly["k_norm"], eps) for r in k])
+        q = rope(q, pos, theta)
+        k = rope(k, pos, theta)
         v = (ly["wv"] @ h).reshape(hkv, d)
         k_cache[li, :, pos] = f16(k)
         v_cache[li, :, pos] = f16(v)

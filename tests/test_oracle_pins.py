@@ -648,3 +648,25 @@ def test_greedy_token_ties_nan_and_infinities():
     assert O.greedy_token([-3.0]) == 0
     z = np.random.default_rng(47).standard_normal(1000)
     assert O.greedy_token(z) == int(np.argmax(z))
+
+
+def test_decode_step_qk_norm_makes_unit_rms_heads():
+    """With unit q/k norm gains every cached key row has RMS 1 (RoPE
+    preserves the norm; fp16 rounding aside), whatever W_k's scale; with the
+    norms absent the rows keep W_k's scale."""
+    rng = np.random.default_rng(48)
+    m = _tiny_model(rng, layers=1)
+    m["layers"][0]["wk"] = m["layers"][0]["wk"] * 37.0
+    kc = np.zeros((1, 2, 8, 16)); vc = np.zeros((1, 2, 8, 16))
+    O.decode_step(m, 3, 0, kc, vc)
+    assert np.sqrt(np.mean(kc[0, :, 0] ** 2, axis=1)).min() > 3.0
+    m["layers"][0]["q_norm"] = np.ones(16)
+    m["layers"][0]["k_norm"] = np.ones(16)
+    for p in range(3):
+        O.decode_step(m, 3 + p, p, kc, vc)
+        assert np.allclose(np.sqrt(np.mean(kc[0, :, p] ** 2, axis=1)), 1.0, atol=2e-3)
+    # a gain of 2 on both doubles the key rows (eps negligible)
+    m2 = dict(m); m2["layers"] = [dict(m["layers"][0], k_norm=np.full(16, 2.0))]
+    kc2 = np.zeros_like(kc); vc2 = np.zeros_like(vc)
+    O.decode_step(m2, 3, 0, kc2, vc2)
+    assert np.allclose(kc2[0, :, 0], 2 * kc[0, :, 0], rtol=2e-3, atol=2e-3)
