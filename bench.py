@@ -278,7 +278,7 @@ def extra_workloads(torch, B, inputs, workloads, steps, warmup, which="all"):
     return out
 
 
-def build_decoder(model: dict, cfg_id: int, fmt, max_len, torch, B, inputs):
+def build_decoder(model: dict, cfg_id: int, fmt, max_len, torch, B, inputs, qk_norm: bool = False):
     """A dense decoder of the model's geometry with seeded synthetic weights
     (projections quantised on the device), as DenseDecoder."""
     from paper_2607_00501_amd.decoder import DecoderConfig, DenseDecoder, LayerWeights
@@ -287,7 +287,7 @@ def build_decoder(model: dict, cfg_id: int, fmt, max_len, torch, B, inputs):
 
     def proj(name, li, n, k):
         w = inputs.weights_dev(inputs.seed_for(cfg_id, li, name), (n, k))
-        if name in ("q", "k"):                # row order of the q/k/v GEMV's RoPE epilogue
+        if name in ("q", "k") and not qk_norm:   # row order of the q/k/v GEMV's RoPE epilogue
             w = B.rope_interleave_rows(w, n // cfg.head_dim, cfg.head_dim)
         q = B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE)
         del w
@@ -296,17 +296,21 @@ def build_decoder(model: dict, cfg_id: int, fmt, max_len, torch, B, inputs):
     def gain(name, li):
         return torch.from_numpy(inputs.norm_weights_np(inputs.seed_for(cfg_id, li, name), cfg.hidden)).cuda()
 
+    def hgain(name, li):
+        return torch.from_numpy(inputs.norm_weights_np(inputs.seed_for(cfg_id, li, name), cfg.head_dim)).cuda()
+
     layers = []
     for li in range(cfg.layers):
         layers.append(LayerWeights(proj("q", li, qd, cfg.hidden), proj("k", li, kvd, cfg.hidden),
                                    proj("v", li, kvd, cfg.hidden), proj("o", li, cfg.hidden, qd),
                                    proj("gate", li, cfg.inter, cfg.hidden), proj("up", li, cfg.inter, cfg.hidden),
                                    proj("down", li, cfg.hidden, cfg.inter), gain("attn_norm", li),
-                                   gain("ffn_norm", li)))
+                                   gain("ffn_norm", li),
+                                   *((hgain("q", li), hgain("k", li)) if qk_norm else ())))
     emb = inputs.activations_dev(inputs.seed_for(cfg_id, 0, "emb"), (cfg.vocab, cfg.hidden))
     head = proj("lm_head", 0, cfg.vocab, cfg.hidden)
     torch.cuda.synchronize()
-    return DenseDecoder(cfg, emb, layers, gain("norm", 0), head, max_len, rope_rows_interleaved=True)
+    return DenseDecoder(cfg, emb, layers, gain("norm", 0), head, max_len, rope_rows_interleaved=not qk_norm)
 
 
 def tg_tokens_per_s(torch, dec, tokens: int, reps: int):
@@ -361,6 +365,16 @@ def extra_tg(torch, B, inputs, workloads, steps, warmup, lib):
         out[key] = {"tokens_per_s": round(512 * 5 / t, 1), "ms_per_prompt": round(t / 5 * 1e3, 3)}
         log(f"{key}: {out[key]}")
         del g
+        if model is workloads.QWEN3_06B_DECODER:
+            # the Qwen3 layer proper: per-head q/k norms before RoPE (in the
+            # RoPE kernel, so one launch more per layer than the epilogue path)
+            del dec
+            dec = build_decoder(model, cfg_id, B.Q4_G32, 640, torch, B, inputs, qk_norm=True)
+            tps, t = tg_tokens_per_s(torch, dec, 128, 3)
+            key = model["name"] + "_qknorm_tg128_q4"
+            out[key] = {"tokens_per_s": round(tps, 1), "ms_per_token": round(1e3 / tps, 4),
+                        "launches_per_token": 6 * model["layers"] + 5, "ms_per_128_tokens": round(t * 1e3, 3)}
+            log(f"{key}: {out[key]}")
         del dec
         torch.cuda.empty_cache()
 

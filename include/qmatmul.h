@@ -210,12 +210,12 @@ qm_status qdec_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, 
  * in the interleaved order of qmatmul_gemv_qkv_rmsnorm_rope's weights);
  * q_out: fp16 [n_q_heads][m][head_dim] (qattn_prefill's layout), rotated;
  * cache rows p0 .. p0 + m - 1 written (keys rotated).  Rotation as
- * qdec_rope_append.  head_dim 64 or 128; 1 <= m <= 32768;
- * p0 + m <= max_len <= 262144; theta > 1. */
+ * qdec_rope_append, the per-head norms too.  head_dim 64 or 128;
+ * 1 <= m <= 32768; p0 + m <= max_len <= 262144; theta > 1. */
 qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, int32_t n_q_heads,
                                 int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len,
-                                float theta, int32_t interleaved, uint16_t* q_out, uint16_t* k_cache,
-                                uint16_t* v_cache, void* stream);
+                                float theta, int32_t interleaved, const uint16_t* q_norm, const uint16_t* k_norm,
+                                float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache, void* stream);
 
 /* out[r][h * head_dim + d] = fp16_RNE(o[h][r][d]): qattn_prefill's output
  * as the output projection's GEMM input. */
@@ -388,10 +388,15 @@ qm_status qdec_rmsnorm(float* x, const float* residual, const uint16_t* w, int64
  * q: fp32 [n_q_heads][head_dim]; k, v: fp32 [n_kv_heads][head_dim] (the
  * projection outputs); q_out: fp16 [n_q_heads][head_dim]; caches: fp16
  * [n_kv_heads][max_len][head_dim], only row pos of each head written.
- * head_dim 64 or 128; 0 <= pos < max_len <= 262144; theta > 1. */
+ * head_dim 64 or 128; 0 <= pos < max_len <= 262144; theta > 1.
+ * q_norm, k_norm: fp16 [head_dim] gains of the per-head RMSNorm the Qwen3
+ * layer applies to every query and key head before RoPE
+ * (x / sqrt(mean over the head(x^2) + eps) * gain, sum in fp32); both NULL
+ * for the Llama layer. */
 qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32_t n_q_heads, int32_t n_kv_heads,
-                           int32_t head_dim, int64_t pos, int64_t max_len, float theta, uint16_t* q_out,
-                           uint16_t* k_cache, uint16_t* v_cache, void* stream);
+                           int32_t head_dim, int64_t pos, int64_t max_len, float theta, const uint16_t* q_norm,
+                           const uint16_t* k_norm, float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
+                           void* stream);
 
 /* out[i] = fp16_RNE(x[i]), i < n (values beyond the fp16 range become inf).
  * x: fp32, out: fp16, device; n >= 0. */

@@ -83,7 +83,8 @@ def lib() -> ctypes.CDLL:
             "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
             "qdec_rope_table": [i64, i32, ctypes.c_float, vp, vp],
             "qdec_embed_rows": [vp, i64, i64, vp, i64, vp, vp],
-            "qdec_rope_append_rows": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, i32, vp, vp, vp, vp],
+            "qdec_rope_append_rows": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, i32, vp, vp,
+                                      ctypes.c_float, vp, vp, vp, vp],
             "qdec_heads_to_rows_f16": [vp, i32, i64, i32, vp, vp],
             "qdec_swiglu_f16": [vp, vp, i64, vp, vp],
             "qmatmul_gemv_qkv_rmsnorm_rope": [W, vp, vp, vp, ctypes.c_float, vp, i32, i32, i32, i64, i64, vp, vp, vp,
@@ -94,7 +95,8 @@ def lib() -> ctypes.CDLL:
             "qmatmul_gemv_swiglu_rmsnorm_f16": [W, W, vp, vp, vp, ctypes.c_float, vp, vp, vp],
             "qattn_decode_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qdec_rmsnorm": [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp],
-            "qdec_rope_append": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, vp, vp],
+            "qdec_rope_append": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, ctypes.c_float, vp, vp,
+                                 vp, vp],
             "qdec_cast_f16": [vp, i64, vp, vp],
             "qdec_argmax": [vp, i64, vp, vp, sz, vp],
         }
@@ -284,7 +286,8 @@ def qdec_embed_rows(table: torch.Tensor, tokens: torch.Tensor, out: Optional[tor
 
 def qdec_rope_append_rows(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, p0: int, theta: float,
                           k_cache: torch.Tensor, v_cache: torch.Tensor, interleaved: bool = False,
-                          q_out: Optional[torch.Tensor] = None, stream=None):
+                          q_out: Optional[torch.Tensor] = None, q_norm: Optional[torch.Tensor] = None,
+                          k_norm: Optional[torch.Tensor] = None, eps: float = 1e-6, stream=None):
     """q fp32 [m][Hq*D], k, v fp32 [m][Hkv*D] -> fp16 [Hq][m][D]; cache rows p0..p0+m-1."""
     hkv, max_len, d = k_cache.shape
     m = q.shape[0]
@@ -293,8 +296,8 @@ def qdec_rope_append_rows(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, p0:
     if q_out is None:
         q_out = torch.empty((hq, m, d), dtype=torch.float16, device=q.device)
     _check(lib().qdec_rope_append_rows(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, m, p0, max_len, theta,
-                                       1 if interleaved else 0, _ptr(q_out), _ptr(k_cache), _ptr(v_cache),
-                                       _stream(stream)))
+                                       1 if interleaved else 0, _ptr(q_norm), _ptr(k_norm), eps, _ptr(q_out),
+                                       _ptr(k_cache), _ptr(v_cache), _stream(stream)))
     return q_out
 
 
@@ -472,6 +475,7 @@ def qdec_rmsnorm(x: torch.Tensor, w: torch.Tensor, eps: float, residual: Optiona
 
 def qdec_rope_append(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: int, theta: float,
                      k_cache: torch.Tensor, v_cache: torch.Tensor, q_out: Optional[torch.Tensor] = None,
+                     q_norm: Optional[torch.Tensor] = None, k_norm: Optional[torch.Tensor] = None, eps: float = 1e-6,
                      stream=None):
     """q: fp32 [Hq*D]; k, v: fp32 [Hkv*D]; caches fp16 [Hkv][max_len][D]
     (row pos written) -> fp16 [Hq][D] rotated queries."""
@@ -482,8 +486,8 @@ def qdec_rope_append(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: int
     assert k_cache.is_contiguous() and v_cache.is_contiguous()
     if q_out is None:
         q_out = torch.empty((hq, d), dtype=torch.float16, device=q.device)
-    _check(lib().qdec_rope_append(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, pos, max_len, theta, _ptr(q_out),
-                                  _ptr(k_cache), _ptr(v_cache), _stream(stream)))
+    _check(lib().qdec_rope_append(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, pos, max_len, theta, _ptr(q_norm),
+                                  _ptr(k_norm), eps, _ptr(q_out), _ptr(k_cache), _ptr(v_cache), _stream(stream)))
     return q_out
 
 

@@ -299,9 +299,12 @@ qm_status qdec_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, 
 
 qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, int32_t n_q_heads,
                                 int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len,
-                                float theta, int32_t interleaved, uint16_t* q_out, uint16_t* k_cache,
-                                uint16_t* v_cache, void* stream) {
+                                float theta, int32_t interleaved, const uint16_t* q_norm, const uint16_t* k_norm,
+                                float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache, void* stream) {
   const char* name = "qdec_rope_append_rows";
+  if ((q_norm == nullptr) != (k_norm == nullptr) || !aligned2(q_norm) || !aligned2(k_norm))
+    return fail(QM_EINVAL, "%s: q_norm and k_norm both given (2-byte aligned) or both NULL", name);
+  if (q_norm && (!(eps >= 0.0f) || eps == INFINITY)) return fail(QM_EINVAL, "%s: eps finite and >= 0", name);
   if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "%s: head_dim=%d must be 64 or 128", name, head_dim);
   if (n_q_heads < 1 || n_q_heads > 1024 || n_kv_heads < 1 || n_kv_heads > 1024)
     return fail(QM_ESHAPE, "%s: head counts must be in [1, 1024]", name);
@@ -314,7 +317,8 @@ qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, 
   if (!aligned4(q) || !aligned4(k) || !aligned4(v) || !aligned2(q_out) || !aligned2(k_cache) || !aligned2(v_cache))
     return fail(QM_EALIGN, "%s: q, k, v 4-byte, q_out and caches 2-byte aligned", name);
   return launched(launch_rope_append_rows(q, k, v, n_q_heads, n_kv_heads, head_dim, m, p0, max_len, theta,
-                                          interleaved, q_out, k_cache, v_cache, static_cast<hipStream_t>(stream)),
+                                          interleaved, q_out, k_cache, v_cache, q_norm, k_norm, eps,
+                                          static_cast<hipStream_t>(stream)),
                   name);
 }
 
@@ -656,8 +660,12 @@ qm_status qdec_rmsnorm(float* x, const float* residual, const uint16_t* w, int64
 }
 
 qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32_t n_q_heads, int32_t n_kv_heads,
-                           int32_t head_dim, int64_t pos, int64_t max_len, float theta, uint16_t* q_out,
-                           uint16_t* k_cache, uint16_t* v_cache, void* stream) {
+                           int32_t head_dim, int64_t pos, int64_t max_len, float theta, const uint16_t* q_norm,
+                           const uint16_t* k_norm, float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
+                           void* stream) {
+  if ((q_norm == nullptr) != (k_norm == nullptr) || !aligned2(q_norm) || !aligned2(k_norm))
+    return fail(QM_EINVAL, "qdec_rope_append: q_norm and k_norm both given (2-byte aligned) or both NULL");
+  if (q_norm && (!(eps >= 0.0f) || eps == INFINITY)) return fail(QM_EINVAL, "qdec_rope_append: eps finite and >= 0");
   if (head_dim != 64 && head_dim != 128)
     return fail(QM_ESHAPE, "qdec_rope_append: head_dim=%d must be 64 or 128", head_dim);
   if (n_q_heads < 1 || n_q_heads > 1024 || n_kv_heads < 1 || n_kv_heads > 1024)
@@ -669,7 +677,7 @@ qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32
   if (!aligned4(q) || !aligned4(k) || !aligned4(v) || !aligned2(q_out) || !aligned2(k_cache) || !aligned2(v_cache))
     return fail(QM_EALIGN, "qdec_rope_append: q, k, v 4-byte, q_out and caches 2-byte aligned");
   return launched(launch_rope_append(q, k, v, n_q_heads, n_kv_heads, head_dim, pos, max_len, theta, q_out, k_cache,
-                                     v_cache, static_cast<hipStream_t>(stream)),
+                                     v_cache, q_norm, k_norm, eps, static_cast<hipStream_t>(stream)),
                   "qdec_rope_append");
 }
 

@@ -160,6 +160,17 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, con
   for (int64_t i = threadIdx.x; i < hidden; i += 256) o[i] = f2h(xr[i] * inv * h2f(w[i]));
 }
 
+// Per-head RMSNorm before RoPE (the Qwen3 layer): thread i of the head's
+// D/2 threads holds dimensions i and i + D/2.
+__device__ __forceinline__ void head_rmsnorm(float& a, float& b, int i, int half, const uint16_t* __restrict__ gain,
+                                             float eps) {
+  float ss = fmaf(a, a, b * b);
+  for (int off = half / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, half);
+  const float inv = 1.0f / sqrtf(ss / static_cast<float>(2 * half) + eps);
+  a = a * inv * h2f(gain[i]);
+  b = b * inv * h2f(gain[i + half]);
+}
+
 // One workgroup of D/2 threads per head: heads [0, hq) are queries (rotated
 // into q_out), [hq, hq + hkv) keys (rotated into the key cache at row pos),
 // the rest values (copied into the value cache at row pos).  Thread i
@@ -169,7 +180,9 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x, con
 __global__ void rope_append_kernel(const float* __restrict__ q, const float* __restrict__ k,
                                    const float* __restrict__ v, int hq, int hkv, int d, int64_t pos,
                                    int64_t max_len, double log2_theta, uint16_t* __restrict__ q_out,
-                                   uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+                                   uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
+                                   const uint16_t* __restrict__ q_gain, const uint16_t* __restrict__ k_gain,
+                                   float eps) {
   const int h = blockIdx.x, i = threadIdx.x, half = d / 2;
   if (h >= hq + hkv) {
     const int kh = h - hq - hkv;
@@ -182,7 +195,8 @@ __global__ void rope_append_kernel(const float* __restrict__ q, const float* __r
   const float c = cs.x, s = cs.y;
   const float* src = h < hq ? q + h * d : k + (h - hq) * d;
   uint16_t* dst = h < hq ? q_out + h * d : kc + (static_cast<int64_t>(h - hq) * max_len + pos) * d;
-  const float a = src[i], b = src[i + half];
+  float a = src[i], b = src[i + half];
+  if (q_gain) head_rmsnorm(a, b, i, half, h < hq ? q_gain : k_gain, eps);
   dst[i] = f2h(rope_low(a, b, c, s));
   dst[i + half] = f2h(rope_high(a, b, c, s));
 }
@@ -217,7 +231,8 @@ __global__ void rope_append_rows_kernel(const float* __restrict__ q, const float
                                         const float* __restrict__ v, int hq, int hkv, int d, int64_t m, int64_t p0,
                                         int64_t max_len, double log2_theta, int interleaved,
                                         uint16_t* __restrict__ q_out, uint16_t* __restrict__ kc,
-                                        uint16_t* __restrict__ vc) {
+                                        uint16_t* __restrict__ vc, const uint16_t* __restrict__ q_gain,
+                                        const uint16_t* __restrict__ k_gain, float eps) {
   const int h = blockIdx.x, i = threadIdx.x, half = d / 2;
   const int64_t r = blockIdx.y, pos = p0 + r;
   if (h >= hq + hkv) {
@@ -232,7 +247,8 @@ __global__ void rope_append_rows_kernel(const float* __restrict__ q, const float
   const float* src = h < hq ? q + r * hq * d + h * d : k + r * hkv * d + (h - hq) * d;
   uint16_t* dst = h < hq ? q_out + (static_cast<int64_t>(h) * m + r) * d
                          : kc + (static_cast<int64_t>(h - hq) * max_len + pos) * d;
-  const float a = interleaved ? src[2 * i] : src[i], b = interleaved ? src[2 * i + 1] : src[i + half];
+  float a = interleaved ? src[2 * i] : src[i], b = interleaved ? src[2 * i + 1] : src[i + half];
+  if (q_gain) head_rmsnorm(a, b, i, half, h < hq ? q_gain : k_gain, eps);
   dst[i] = f2h(rope_low(a, b, cs.x, cs.y));
   dst[i + half] = f2h(rope_high(a, b, cs.x, cs.y));
 }
@@ -388,9 +404,11 @@ hipError_t launch_rmsnorm(float* x, const float* res, const uint16_t* w, int64_t
 
 hipError_t launch_rope_append(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
                               int64_t pos, int64_t max_len, float theta, uint16_t* q_out, uint16_t* kc,
-                              uint16_t* vc, hipStream_t st) {
+                              uint16_t* vc, const uint16_t* q_gain, const uint16_t* k_gain, float eps,
+                              hipStream_t st) {
   hipLaunchKernelGGL(rope_append_kernel, dim3(static_cast<unsigned>(hq + 2 * hkv)), dim3(d / 2), 0, st, q, k, v,
-                     hq, hkv, d, pos, max_len, std::log2(static_cast<double>(theta)), q_out, kc, vc);
+                     hq, hkv, d, pos, max_len, std::log2(static_cast<double>(theta)), q_out, kc, vc, q_gain, k_gain,
+                     eps);
   return hipGetLastError();
 }
 
@@ -410,10 +428,11 @@ hipError_t launch_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidde
 
 hipError_t launch_rope_append_rows(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
                                    int64_t m, int64_t p0, int64_t max_len, float theta, int32_t interleaved,
-                                   uint16_t* q_out, uint16_t* kc, uint16_t* vc, hipStream_t st) {
+                                   uint16_t* q_out, uint16_t* kc, uint16_t* vc, const uint16_t* q_gain,
+                                   const uint16_t* k_gain, float eps, hipStream_t st) {
   hipLaunchKernelGGL(rope_append_rows_kernel, dim3(static_cast<unsigned>(hq + 2 * hkv), static_cast<unsigned>(m)),
                      dim3(d / 2), 0, st, q, k, v, hq, hkv, d, m, p0, max_len, std::log2(static_cast<double>(theta)),
-                     interleaved, q_out, kc, vc);
+                     interleaved, q_out, kc, vc, q_gain, k_gain, eps);
   return hipGetLastError();
 }
 

@@ -159,14 +159,16 @@ hipError_t launch_rmsnorm(float* x, const float* res, const uint16_t* w, int64_t
                           uint16_t* out, hipStream_t st);
 hipError_t launch_rope_append(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
                               int64_t pos, int64_t max_len, float theta, uint16_t* q_out, uint16_t* kc,
-                              uint16_t* vc, hipStream_t st);
+                              uint16_t* vc, const uint16_t* q_gain, const uint16_t* k_gain, float eps,
+                              hipStream_t st);
 hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t st);
 hipError_t launch_rope_table(int64_t max_len, int32_t d, float theta, float* table, hipStream_t st);
 hipError_t launch_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* tokens, int64_t m,
                              float* x, hipStream_t st);
 hipError_t launch_rope_append_rows(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
                                    int64_t m, int64_t p0, int64_t max_len, float theta, int32_t interleaved,
-                                   uint16_t* q_out, uint16_t* kc, uint16_t* vc, hipStream_t st);
+                                   uint16_t* q_out, uint16_t* kc, uint16_t* vc, const uint16_t* q_gain,
+                                   const uint16_t* k_gain, float eps, hipStream_t st);
 hipError_t launch_heads_to_rows(const float* o, int32_t h, int64_t m, int32_t d, uint16_t* out, hipStream_t st);
 hipError_t launch_swiglu(const float* g, const float* u, int64_t n, uint16_t* out, hipStream_t st);
 

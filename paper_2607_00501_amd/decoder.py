@@ -12,7 +12,7 @@ the sampled token stays on the device for the next step's embedding.
 
 import math
 from dataclasses import dataclass
-from typing import List
+from typing import List, Optional
 
 import torch
 
@@ -43,6 +43,8 @@ class LayerWeights:
     wd: B.QWeight
     attn_norm: torch.Tensor   # fp16 [hidden]
     ffn_norm: torch.Tensor    # fp16 [hidden]
+    q_norm: Optional[torch.Tensor] = None   # fp16 [head_dim]: per-head q/k RMSNorm (the Qwen3 layer)
+    k_norm: Optional[torch.Tensor] = None
 
 
 class DenseDecoder:
@@ -74,6 +76,8 @@ class DenseDecoder:
         self.x2 = torch.zeros(c.hidden, **f32)            # its other buffer (fused norms)
         self.rope_epi = rope_rows_interleaved
         assert not self.rope_epi or self.fused, "the RoPE epilogue runs in the fused q/k/v GEMV"
+        assert not (self.rope_epi and any(ly.q_norm is not None for ly in layers)), \
+            "per-head q/k norms need whole heads: use the RoPE kernel (rows not interleaved)"
         self.rope_tab = B.qdec_rope_table(max_len, c.head_dim, c.theta, device=dev) if self.rope_epi else None
         self.h = torch.zeros(c.hidden, **f16)             # normed input of a projection
         self.q, self.k, self.v = torch.zeros(qd, **f32), torch.zeros(kvd, **f32), torch.zeros(kvd, **f32)
@@ -113,7 +117,7 @@ class DenseDecoder:
                     # launch, qattn_decode_rope_f16, measured slower: the fp64
                     # angles then sit ahead of the attention's first loads)
                     B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
-                                       q_out=self.q16, stream=s)
+                                       q_out=self.q16, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps, stream=s)
                 B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,
                                workspace=self.ws, stream=s)
                 B.qmatmul_gemv(ly.wo, self.attn16.view(-1), out=self.y_attn, stream=s)
@@ -127,7 +131,7 @@ class DenseDecoder:
             B.qdec_rmsnorm(self.x, ly.attn_norm, c.eps, residual=self.y_ffn if li else None, out=self.h, stream=s)
             B.qmatmul_gemv_grouped([ly.wq, ly.wk, ly.wv], [self.h] * 3, [self.q, self.k, self.v], stream=s)
             B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
-                               q_out=self.q16, stream=s)
+                               q_out=self.q16, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps, stream=s)
             B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,
                            workspace=self.ws, stream=s)
             B.qmatmul_gemv(ly.wo, self.attn16.view(-1), out=self.y_attn, stream=s)
@@ -154,7 +158,8 @@ class DenseDecoder:
             h = B.qdec_rmsnorm(x, ly.attn_norm, c.eps, residual=y, stream=s)
             q, k, v = B.qmatmul_gemm_grouped([ly.wq, ly.wk, ly.wv], h, stream=s)
             qh = B.qdec_rope_append_rows(q, k, v, p0, c.theta, self.k_cache[li], self.v_cache[li],
-                                         interleaved=self.rope_epi, stream=s)
+                                         interleaved=self.rope_epi, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps,
+                                         stream=s)
             o = B.qattn_prefill(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, stream=s)
             ya = B.qmatmul_gemm(ly.wo, B.qdec_heads_to_rows_f16(o, stream=s), stream=s)
             h = B.qdec_rmsnorm(x, ly.ffn_norm, c.eps, residual=ya, stream=s)

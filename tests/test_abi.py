@@ -291,8 +291,9 @@ def test_decode_glue_validation():
     assert norm(eps=-1.0) == 1 and norm(eps=float("nan")) == 1 and norm(eps=float("inf")) == 1
     assert norm(w=None) == 1 and norm(o=None) == 1
     assert norm(w=odd) == 3 and norm(r=ctypes.c_void_p(0x50002)) == 3
-    rope = lambda hq=4, hkv=2, d=64, pos=0, mx=128, theta=1e4, q=p, kc=p: \
-        L.qdec_rope_append(q, p, p, hq, hkv, d, pos, mx, theta, p, kc, p, None)
+    rope = lambda hq=4, hkv=2, d=64, pos=0, mx=128, theta=1e4, q=p, kc=p, qn=None, kn=None: \
+        L.qdec_rope_append(q, p, p, hq, hkv, d, pos, mx, theta, qn, kn, 1e-6, p, kc, p, None)
+    assert rope(qn=p) == 1 and rope(qn=p, kn=ctypes.c_void_p(0x50001)) == 1
     assert rope(d=96) == 2 and rope(hq=0) == 2 and rope(hkv=2000) == 2
     assert rope(pos=128) == 2 and rope(pos=-1) == 2 and rope(mx=300000, pos=5) == 2
     assert rope(theta=1.0) == 1 and rope(theta=float("nan")) == 1
@@ -384,8 +385,9 @@ def test_prefill_glue_validation():
     p = ctypes.c_void_p(0x50000)
     assert L.qdec_embed_rows(p, 100, 64, p, 40000, p, None) == 2 and L.qdec_embed_rows(p, 0, 64, p, 4, p, None) == 2
     assert L.qdec_embed_rows(None, 100, 64, p, 4, p, None) == 1
-    rr = lambda d=64, m=8, p0=0, mx=64, il=0, theta=1e4, qo=p: L.qdec_rope_append_rows(
-        p, p, p, 4, 2, d, m, p0, mx, theta, il, qo, p, p, None)
+    rr = lambda d=64, m=8, p0=0, mx=64, il=0, theta=1e4, qo=p, kn=None: L.qdec_rope_append_rows(
+        p, p, p, 4, 2, d, m, p0, mx, theta, il, None, kn, 1e-6, qo, p, p, None)
+    assert rr(kn=p) == 1
     assert rr(d=80) == 2 and rr(m=0) == 2 and rr(p0=60) == 2 and rr(il=2) == 1 and rr(theta=0.5) == 1
     assert rr(qo=None) == 1 and rr(qo=ctypes.c_void_p(0x50001)) == 3
     assert L.qdec_heads_to_rows_f16(p, 0, 4, 64, p, None) == 2 and L.qdec_heads_to_rows_f16(None, 4, 4, 64, p, None) == 1

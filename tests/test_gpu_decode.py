@@ -148,7 +148,7 @@ def test_embed_gathers_rows_and_flags_bad_ids():
 
 # ---------------------------------------------------------------- decode steps
 
-def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32), interleave=False):
+def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32), interleave=False, qk_norm=False):
     """Seeded weights of a dense decoder, quantised on the device (library)
     and in the oracle from the same fp32 values."""
     ofmt, bfmt = fmts
@@ -170,11 +170,16 @@ def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32), interleave=False
         p = {name: proj(name, li, *sh) for name, sh in shapes.items()}
         an = inputs.norm_weights_np(inputs.seed_for(tag, li, "attn_norm"), cfg.hidden)
         fn = inputs.norm_weights_np(inputs.seed_for(tag, li, "ffn_norm"), cfg.hidden)
+        qn = inputs.norm_weights_np(inputs.seed_for(tag, li, "q"), cfg.head_dim) if qk_norm else None
+        kn = inputs.norm_weights_np(inputs.seed_for(tag, li, "k"), cfg.head_dim) if qk_norm else None
+        cu = lambda a: None if a is None else torch.from_numpy(a).cuda()
         dev_layers.append(LayerWeights(p["q"][0], p["k"][0], p["v"][0], p["o"][0], p["gate"][0], p["up"][0],
-                                       p["down"][0], torch.from_numpy(an).cuda(), torch.from_numpy(fn).cuda()))
+                                       p["down"][0], cu(an), cu(fn), cu(qn), cu(kn)))
         ref_layers.append(dict(wq=p["q"][1], wk=p["k"][1], wv=p["v"][1], wo=p["o"][1], wg=p["gate"][1],
                                wu=p["up"][1], wd=p["down"][1], attn_norm=an.astype(np.float64),
                                ffn_norm=fn.astype(np.float64)))
+        if qk_norm:
+            ref_layers[-1].update(q_norm=qn.astype(np.float64), k_norm=kn.astype(np.float64))
     emb = inputs.activations_np(inputs.seed_for(tag, 0, "emb"), (cfg.vocab, cfg.hidden))
     norm = inputs.norm_weights_np(inputs.seed_for(tag, 0, "norm"), cfg.hidden)
     head_dev, head_ref = proj("lm_head", 0, cfg.vocab, cfg.hidden)
@@ -183,9 +188,9 @@ def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32), interleave=False
     return dev_layers, torch.from_numpy(emb).cuda(), torch.from_numpy(norm).cuda(), head_dev, ref
 
 
-def _decoder(cfg, tag, max_len, fmts=(O.Q4, B.Q4_G32), fused=True, rope_epi=True):
-    rope_epi = rope_epi and fused
-    layers, emb, norm, head, ref = _model(cfg, tag, fmts, interleave=rope_epi)
+def _decoder(cfg, tag, max_len, fmts=(O.Q4, B.Q4_G32), fused=True, rope_epi=True, qk_norm=False):
+    rope_epi = rope_epi and fused and not qk_norm
+    layers, emb, norm, head, ref = _model(cfg, tag, fmts, interleave=rope_epi, qk_norm=qk_norm)
     dec = DenseDecoder(cfg, emb, layers, norm, head, max_len, fused=fused, rope_rows_interleaved=rope_epi)
     assert dec.fused == fused
     kc = np.zeros((cfg.layers, cfg.n_kv_heads, max_len, cfg.head_dim))
@@ -501,3 +506,30 @@ def test_prefill_chunks_match_one_chunk():
     b.prefill(toks[20:].contiguous(), p0=20)
     assert rel_err(b.logits.cpu().numpy(), a.logits.cpu().numpy().astype(np.float64)) <= 1e-2
     assert rel_err(b.k_cache[:, :, :45].float().cpu().numpy(), a.k_cache[:, :, :45].float().cpu().numpy().astype(np.float64)) <= 1e-2
+
+
+
+# ---------------------------------------------------------------- Qwen3 q/k norms
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_decode_steps_with_qk_norm(fused):
+    """The Qwen3 layer (per-head q/k RMSNorm before RoPE): teacher-forced
+    steps against the oracle, head_dim 64 and 128."""
+    for cfg, tag in ((TINY, 27), (DecoderConfig(hidden=512, n_q_heads=8, n_kv_heads=4, head_dim=128, inter=768,
+                                                 vocab=1500, layers=2), 28)):
+        dec, ref, kc, vc = _decoder(cfg, tag, 16, fused=fused, qk_norm=True)
+        for pos, t in enumerate([9, 1, 77, 3, 3]):
+            dec.token.fill_(t)
+            dec.step(pos)
+            assert rel_err(dec.logits.cpu().numpy(), O.decode_step(ref, t, pos, kc, vc)) <= GEMV_TOL, (tag, pos)
+        assert rel_err(dec.k_cache[:, :, :5].cpu().numpy().astype(np.float64), kc[:, :, :5]) <= 2e-3
+
+
+def test_prefill_with_qk_norm_matches_oracle():
+    dec, ref, kc, vc = _decoder(TINY, 29, 32, qk_norm=True)
+    toks = [4, 8, 15, 16, 23, 42, 108, 500, 0]
+    for p, t in enumerate(toks):
+        want = O.decode_step(ref, t, p, kc, vc)
+    dec.prefill(torch.tensor(toks, dtype=torch.int32, device="cuda"))
+    assert rel_err(dec.logits.cpu().numpy(), want) <= 1e-2
+    assert rel_err(dec.k_cache[:, :, :9].cpu().numpy().astype(np.float64), kc[:, :, :9]) <= 1e-2
