@@ -30,8 +30,13 @@ conversions of the weights.
 Pins: every function here is checked by ``tests/test_oracle_pins.py`` against
 values fixed by something other than this file (hand-derived IEEE bit
 patterns, exact rational arithmetic, integer grids with closed-form answers,
-dense-vs-sparse equivalences, brute-force sorting).  No function is
-"parity unpinned".
+dense-vs-sparse equivalences, brute-force sorting).  The decode-step pieces
+are pinned by hand-worked cases: the RoPE angle of every pair against
+cos/sin of p * 10^-i (D = 8, theta = 10^4), a one-layer step whose output
+projection residual, FFN norm and SwiGLU branch each have a written-out
+value, and per-head q/k norms with non-uniform gains checked before RoPE
+through the cached key and the softmax weights.  Each of these fails when
+the schedule, the residuals, the norm order or the SiLU branch is changed.
 """
 
 from __future__ import annotations

@@ -12,7 +12,10 @@ the wrong branch of the SwiGLU) fails at least one of them:
 * routing against an independent repeated-argmax selection and the softmax's
   closed-form ratios, bucketing against Python's stable ``sorted``,
 * the MoE layer against dense evaluation, a top-1 special case, identical
-  experts and a hand-computed scalar example; SiLU against its identities.
+  experts and a hand-computed scalar example; SiLU against its identities,
+* RoPE angles of every pair against hand values, and one-layer decode steps
+  whose residuals, norms, SwiGLU branch and per-head q/k norms have
+  written-out closed forms.
 """
 
 import math
@@ -670,3 +673,118 @@ def test_decode_step_qk_norm_makes_unit_rms_heads():
     kc2 = np.zeros_like(kc); vc2 = np.zeros_like(vc)
     O.decode_step(m2, 3, 0, kc2, vc2)
     assert np.allclose(kc2[0, :, 0], 2 * kc[0, :, 0], rtol=2e-3, atol=2e-3)
+
+
+# ------------------------------------------- RoPE schedule, decode-step halves
+
+def test_rope_frequency_schedule_every_pair():
+    """Angle of pair i at position p is p * theta^(-2i/D).  With D = 8 and
+    theta = 10^4 that is p * 10^-i: at p = 1 the four pairs turn by 1, 0.1,
+    0.01 and 0.001 rad, at p = 3 by 3, 0.3, 0.03 and 0.003 rad.  One-hot
+    inputs read off each (cos, sin) and the pairing i <-> i + D/2 directly."""
+    d = 8
+    for pos in (1, 3):
+        for i in range(d // 2):
+            a = pos * 10.0 ** (-i)
+            e = np.zeros((1, d)); e[0, i] = 1.0
+            want = np.zeros(d); want[i] = math.cos(a); want[i + d // 2] = math.sin(a)
+            assert np.allclose(O.rope(e, pos, 1e4)[0], want, atol=1e-15), (pos, i)
+            e = np.zeros((1, d)); e[0, i + d // 2] = 1.0
+            want = np.zeros(d); want[i] = -math.sin(a); want[i + d // 2] = math.cos(a)
+            assert np.allclose(O.rope(e, pos, 1e4)[0], want, atol=1e-15), (pos, i)
+    # D = 4, theta = 100: angles p and p / 10
+    r = O.rope(np.array([[1.0, 1.0, 0.0, 0.0]]), 2, 100.0)[0]
+    assert np.allclose(r, [math.cos(2.0), math.cos(0.2), math.sin(2.0), math.sin(0.2)], atol=1e-15)
+
+
+def _h(v: float) -> float:
+    """fp16 round to nearest even of a Python float, via struct."""
+    return _half_value_struct(_half_bits_struct(v))
+
+
+def _rms(v, g, eps):
+    r = math.sqrt(sum(t * t for t in v) / len(v) + eps)
+    return [t / r * w for t, w in zip(v, g)]
+
+
+def _one_layer(h, d, inter, vocab, **w):
+    z = lambda *sh: np.zeros(sh)
+    ly = dict(wq=z(d, h), wk=z(d, h), wv=z(d, h), wo=z(h, d), wg=z(inter, h), wu=z(inter, h), wd=z(h, inter),
+              attn_norm=np.ones(h), ffn_norm=np.ones(h))
+    ly.update({k: np.asarray(v, dtype=np.float64) for k, v in w.items()})
+    return ly
+
+
+def test_decode_step_output_projection_and_ffn_half_closed_form():
+    """One layer with zero q/k projections, so position 0 attends to its own
+    value row only, and small exact matrices, so each stage has a value
+    written out by hand:
+      x0 = emb = (1, 1, 1, 1); eps = 0, so h = f16(rmsnorm(x0)) = attn gains
+      g_a = (1, 2, 0.5, 1);  v = Wv h = (1, 1, 1, -1) = attention output a;
+      x1 = x0 + Wo a = (1.25, 1.5, 1, 1.75)         (the o-projection residual);
+      h2 = f16(x1 / rms(x1) * g_f), g_f = (2, 1, 1, 0.5)   (the FFN norm);
+      gate = (h2_0, h2_3), up = (h2_1, h2_2);  s = f16(silu(gate) * up)
+      (SiLU on the gate branch);  x2 = x1 + Wd s = x1 + (s_0, 0, s_1, 0);
+      logits = f16(rmsnorm(x2) * g_n) with an identity LM head.
+    A dropped residual, swapped norms, SiLU on the up branch or a transposed
+    W_d changes the logits by far more than the fp16 rounding tolerance."""
+    g_a, g_f, g_n = [1.0, 2.0, 0.5, 1.0], [2.0, 1.0, 1.0, 0.5], [1.0, 0.5, 2.0, 1.0]
+    wv = np.diag([1.0, 0.5, 2.0, -1.0])
+    wo = np.diag([0.25, 0.5, 0.0, -0.75])
+    wg = np.array([[1.0, 0, 0, 0], [0, 0, 0, 1.0]])
+    wu = np.array([[0, 1.0, 0, 0], [0, 0, 1.0, 0]])
+    wd = np.array([[1.0, 0], [0, 0], [0, 1.0], [0, 0]])
+    ly = _one_layer(4, 4, 2, 4, wv=wv, wo=wo, wg=wg, wu=wu, wd=wd, attn_norm=g_a, ffn_norm=g_f)
+    model = dict(emb=np.ones((3, 4)), layers=[ly], norm=np.asarray(g_n), lm_head=np.eye(4), hq=1, hkv=1, d=4,
+                 eps=0.0, theta=100.0)
+    kc, vc = np.zeros((1, 1, 2, 4)), np.zeros((1, 1, 2, 4))
+    logits = O.decode_step(model, 2, 0, kc, vc)
+
+    x1 = [1.25, 1.5, 1.0, 1.75]
+    h2 = [_h(t) for t in _rms(x1, g_f, 0.0)]
+    gate, up = (h2[0], h2[3]), (h2[1], h2[2])
+    s = [_h(g / (1.0 + math.exp(-g)) * u) for g, u in zip(gate, up)]
+    x2 = [x1[0] + s[0], x1[1], x1[2] + s[1], x1[3]]
+    want = [_h(t) for t in _rms(x2, g_n, 0.0)]
+    assert np.allclose(vc[0, 0, 0], [1.0, 1.0, 1.0, -1.0]) and np.all(kc == 0)
+    assert np.allclose(logits, want, rtol=0, atol=1e-12), (logits, want)
+
+
+def test_decode_step_qk_norm_nonuniform_gains_before_rope():
+    """Per-head q/k RMSNorm with non-uniform gains, applied before RoPE, at
+    position 1 over a cache whose row 0 the test fills by hand.  Hidden 4,
+    one head of D = 4, theta = 100 (angles 1 and 0.1 rad at position 1),
+    eps = 0, x0 = (1, 1, 1, 1) so the normed input is the attention gains
+    g_a = (1, 1, 1, 1); W_q, W_k, W_v are diagonal, so the raw q, k, v are
+    the diagonals.  Expected, by hand:
+      k1 = f16(rope(rmsnorm(k_raw) * k_norm, 1)), v1 = v_raw,
+      q = f16(rope(rmsnorm(q_raw) * q_norm, 1)),
+      p = softmax(0.5 * (q . k0, q . k1)), a = p0 v0 + p1 v1,
+      x1 = x0 + a (W_o = I), logits = f16(rmsnorm(x1)) (identity head).
+    Norm after RoPE, a dropped q_norm or k_norm, or the two gains swapped
+    moves the cached key or the softmax weights."""
+    q_raw, k_raw, v_raw = [3.0, -1.0, 2.0, 0.5], [1.0, 2.0, -2.0, 4.0], [0.0, 1.0, 0.0, 0.0]
+    qn, kn = [1.0, 0.25, 2.0, 0.5], [0.5, 2.0, 1.0, 0.25]
+    ly = _one_layer(4, 4, 1, 4, wq=np.diag(q_raw), wk=np.diag(k_raw), wv=np.diag(v_raw), wo=np.eye(4),
+                    q_norm=qn, k_norm=kn)
+    model = dict(emb=np.ones((2, 4)), layers=[ly], norm=np.ones(4), lm_head=np.eye(4), hq=1, hkv=1, d=4,
+                 eps=0.0, theta=100.0)
+    kc, vc = np.zeros((1, 1, 3, 4)), np.zeros((1, 1, 3, 4))
+    k0, v0 = [0.5, -1.0, 1.0, 0.25], [1.0, 0.0, 0.0, 0.0]
+    kc[0, 0, 0], vc[0, 0, 0] = k0, v0
+    logits = O.decode_step(model, 1, 1, kc, vc)
+
+    def rot(v):                      # rotate-half pairs (0, 2) by 1 rad and (1, 3) by 0.1 rad
+        c0, s0, c1, s1 = math.cos(1.0), math.sin(1.0), math.cos(0.1), math.sin(0.1)
+        return [v[0] * c0 - v[2] * s0, v[1] * c1 - v[3] * s1, v[2] * c0 + v[0] * s0, v[3] * c1 + v[1] * s1]
+    k1 = [_h(t) for t in rot(_rms(k_raw, kn, 0.0))]
+    q = [_h(t) for t in rot(_rms(q_raw, qn, 0.0))]
+    s0 = 0.5 * sum(a * b for a, b in zip(q, k0))
+    s1 = 0.5 * sum(a * b for a, b in zip(q, k1))
+    p0 = 1.0 / (1.0 + math.exp(s1 - s0))
+    a = [_h(p0 * v0[i] + (1.0 - p0) * v_raw[i]) for i in range(4)]
+    x1 = [1.0 + t for t in a]
+    want = [_h(t) for t in _rms(x1, [1.0] * 4, 0.0)]
+    assert np.allclose(kc[0, 0, 1], k1, rtol=0, atol=1e-12) and np.allclose(vc[0, 0, 1], v_raw)
+    assert np.allclose(logits, want, rtol=0, atol=1e-12), (logits, want)
+    assert 0.05 < p0 < 0.95                          # both keys carry weight
