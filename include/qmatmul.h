@@ -123,16 +123,23 @@ typedef struct {
   uint16_t* scales;
 } qm_qweight;
 
-/* Text of the last error on the calling thread ("" if none yet).  The
- * pointer stays valid until the next failing call on the same thread. */
+/* Text of the last error on the calling thread ("" if none yet), kept in a
+ * static thread-local buffer (Sec. 3.2: errors are reported through a static
+ * thread-local buffer, so the error path allocates nothing).  The pointer
+ * stays valid until the next failing call on the same thread. */
 const char* qm_last_error(void);
 
 /* Host-only: bytes of the code buffer and of the scale buffer for a tensor
- * [batch][n][k] in the given format and layout (DEVICE pads n to 64). */
+ * [batch][n][k] in the given format and layout (DEVICE pads n to 64), so the
+ * caller can allocate every buffer up front (Sec. 3.2: nothing is allocated
+ * on the hot path; Sec. 4.1: the weight formats). */
 qm_status qm_weight_bytes(int32_t format, int32_t layout, int64_t batch, int64_t n,
                           int64_t k, size_t* qbytes, size_t* sbytes);
 
-/* Quantise fp32 weights w [batch][n][k] (device, row-major) into `out`, which
+/* Offline conversion of fp32 weights into one of the quantised formats the
+ * runtime executes (Sec. 4.1: Q2 ... Q8, BF16 and FP16 weights; Sec. 3.3:
+ * weights stay quantised and are dequantised inside the matmul kernels).
+ * Quantise fp32 weights w [batch][n][k] (device, row-major) into `out`, which
  * must be in CANONICAL layout with out->format set.  Bit-exact with the
  * format definition above (one thread per group, IEEE fp32 division,
  * round-half-even, fp16 round-to-nearest-even; F16/BF16: one rounding per
@@ -141,11 +148,15 @@ qm_status qm_weight_bytes(int32_t format, int32_t layout, int64_t batch, int64_t
 qm_status qm_quantise(int32_t format, const float* w, const qm_qweight* out, void* stream);
 
 /* Dequantise w (either layout) into fp32 out [batch][n][k] (device):
- * out = s * q, exact. */
+ * out = s * q, exact.  Not on the hot path, where dequantisation happens in
+ * the matmul's inner loop and is never materialised (Sec. 3.3); this is the
+ * reference view of the weights the kernels compute with. */
 qm_status qm_dequantise(const qm_qweight* w, float* out, void* stream);
 
-/* Reorder codes and scales between layouts (CANONICAL <-> DEVICE).  src and
- * dst must agree in format, batch, n, k and differ in layout; the map is a
+/* Reorder codes and scales between layouts (CANONICAL <-> DEVICE), the
+ * device layout being chosen for coalesced access (Sec. 3.2: memory layouts
+ * chosen to maximise coalesced access; Sec. 1.1: memory-aware data layout).
+ * src and dst must agree in format, batch, n, k and differ in layout; the map is a
  * bijection on the real rows, and DEVICE padding rows are written as zero.
  * src and dst buffers must not overlap. */
 qm_status qm_repack(const qm_qweight* src, const qm_qweight* dst, void* stream);
@@ -170,7 +181,8 @@ qm_status qmatmul_gemv_swiglu(const qm_qweight* w_gate, const qm_qweight* w_up, 
 
 /* As qmatmul_gemv_swiglu, with h written as fp16 [n] (round to nearest
  * even of the same fp32 value; 2-byte aligned), ready to be the input of
- * the down projection's GEMV. */
+ * the down projection's GEMV.
+ * (Sec. 3.3: the fp16 conversion fused into the producer.) */
 qm_status qmatmul_gemv_swiglu_f16(const qm_qweight* w_gate, const qm_qweight* w_up, const uint16_t* x, uint16_t* h,
                                   void* stream);
 
@@ -200,7 +212,8 @@ qm_status qmatmul_gemv_swiglu_rmsnorm_f16(const qm_qweight* w_gate, const qm_qwe
 
 /* x[r] = table[tokens[r]] (fp16 -> fp32), r < m; x: fp32 [m][hidden];
  * tokens: int32 [m] on the device; ids outside [0, vocab) give NaN rows.
- * 0 <= m <= 32768. */
+ * 0 <= m <= 32768.
+ * (Sec. 3.4: chunked prefill; Sec. 3.2: embedding kernel.) */
 qm_status qdec_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* tokens, int64_t m,
                           float* x, void* stream);
 
@@ -211,19 +224,22 @@ qm_status qdec_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, 
  * q_out: fp16 [n_q_heads][m][head_dim] (qattn_prefill's layout), rotated;
  * cache rows p0 .. p0 + m - 1 written (keys rotated).  Rotation as
  * qdec_rope_append, the per-head norms too.  head_dim 64 or 128;
- * 1 <= m <= 32768; p0 + m <= max_len <= 262144; theta > 1. */
+ * 1 <= m <= 32768; p0 + m <= max_len <= 262144; theta > 1.
+ * (Sec. 3.4: chunked prefill; Sec. 3.2: RoPE and the KV cache.) */
 qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, int32_t n_q_heads,
                                 int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len,
                                 float theta, int32_t interleaved, const uint16_t* q_norm, const uint16_t* k_norm,
                                 float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache, void* stream);
 
 /* out[r][h * head_dim + d] = fp16_RNE(o[h][r][d]): qattn_prefill's output
- * as the output projection's GEMM input. */
+ * as the output projection's GEMM input.
+ * (Sec. 3.4: chunked prefill, the attention output handed to the next GEMM.) */
 qm_status qdec_heads_to_rows_f16(const float* o, int32_t n_heads, int64_t m, int32_t head_dim, uint16_t* out,
                                  void* stream);
 
 /* out[i] = fp16_RNE(silu(gate[i]) * up[i]), i < n (fp32 in): the SwiGLU of
- * the prompt's gate/up GEMM outputs. */
+ * the prompt's gate/up GEMM outputs.
+ * (Sec. 3.4: chunked prefill; Sec. 3.2: activation kernels.) */
 qm_status qdec_swiglu_f16(const float* gate, const float* up, int64_t n, uint16_t* out, void* stream);
 
 /* (cos, sin) table of the rotary embedding for every position of a cache:
@@ -314,7 +330,8 @@ qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16
 
 /* Host-only: bytes of the decode-attention workspace for n_q_heads query
  * heads of head_dim (64 or 128): per query head up to 256 slices of
- * (head_dim + 2) floats. */
+ * (head_dim + 2) floats.
+ * (Sec. 3.2: caller-owned buffers, nothing allocated on the hot path.) */
 qm_status qattn_decode_workspace_bytes(int32_t n_q_heads, int32_t head_dim, size_t* bytes);
 
 /* Decode attention over a pre-allocated KV cache (Sec. 3.2: the cache is
@@ -337,27 +354,11 @@ qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_
 
 /* As qattn_decode, with o written as fp16 [n_q_heads][head_dim] (round to
  * nearest even of the same fp32 value; 2-byte aligned), ready to be the
- * input of the output projection's GEMV. */
+ * input of the output projection's GEMV.
+ * (Sec. 3.3: the fp16 conversion fused into the producer.) */
 qm_status qattn_decode_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
                            int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale,
                            uint16_t* o, void* workspace, size_t ws_bytes, void* stream);
-
-/* The new token's rotary embedding and KV-cache append folded into decode
- * attention (Sec. 3.2: RoPE and attention kernels; Sec. 3.3: one launch
- * fewer per layer): the result of qdec_rope_append followed by
- * qattn_decode_f16 with len = pos + 1, value rows bit for bit; a rotated
- * query or key element whose fp32 value lies on an fp16 rounding midpoint
- * may round to the other neighbour (one fp16 ulp; the two kernels' fp32
- * rotations can differ in the last bit).  q: fp32
- * [n_q_heads][head_dim], k, v: fp32 [n_kv_heads][head_dim] (the projection
- * outputs, 4-byte aligned); row pos of k_cache and v_cache (fp16
- * [n_kv_heads][max_len][head_dim], 16-byte aligned) is written; o: fp16
- * [n_q_heads][head_dim].  0 <= pos < max_len <= 262144; theta > 1; other
- * limits, the workspace and the launches as qattn_decode. */
-qm_status qattn_decode_rope_f16(const float* q, const float* k, const float* v, int32_t n_q_heads,
-                                int32_t n_kv_heads, int32_t head_dim, int64_t pos, int64_t max_len, float theta,
-                                float scale, uint16_t* k_cache, uint16_t* v_cache, uint16_t* o, void* workspace,
-                                size_t ws_bytes, void* stream);
 
 /* ---- Glue of one decode step (Sec. 3.2: the normalisation, RoPE,
  * embedding and sampling kernels between the matmuls and attention of a
@@ -368,7 +369,8 @@ qm_status qattn_decode_rope_f16(const float* q, const float* k, const float* v, 
 
 /* x[i] = table[*token][i] (fp16 -> fp32), i < hidden.  table: fp16
  * [vocab][hidden]; token: one int32 on the device; an id outside
- * [0, vocab) writes NaNs into x (a host check would need a synchronisation). */
+ * [0, vocab) writes NaNs into x (a host check would need a synchronisation).
+ * (Sec. 3.2: embedding kernel of the decode step.) */
 qm_status qdec_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,
                      void* stream);
 
@@ -376,7 +378,8 @@ qm_status qdec_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const
  * optional residual add first:  if residual != NULL, x += residual (written
  * back into x);  out = fp16_RNE(x / sqrt(mean(x^2) + eps) * w).  w: fp16
  * [hidden]; out: fp16 [rows][hidden].  Sum of squares in fp32.  rows may be
- * 0; hidden >= 1; eps finite and >= 0. */
+ * 0; hidden >= 1; eps finite and >= 0.
+ * (Sec. 3.2: normalisation kernel of the decode step.) */
 qm_status qdec_rmsnorm(float* x, const float* residual, const uint16_t* w, int64_t rows, int64_t hidden, float eps,
                        uint16_t* out, void* stream);
 
@@ -392,14 +395,16 @@ qm_status qdec_rmsnorm(float* x, const float* residual, const uint16_t* w, int64
  * q_norm, k_norm: fp16 [head_dim] gains of the per-head RMSNorm the Qwen3
  * layer applies to every query and key head before RoPE
  * (x / sqrt(mean over the head(x^2) + eps) * gain, sum in fp32); both NULL
- * for the Llama layer. */
+ * for the Llama layer.
+ * (Sec. 3.2: RoPE and the KV cache of the decode step.) */
 qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32_t n_q_heads, int32_t n_kv_heads,
                            int32_t head_dim, int64_t pos, int64_t max_len, float theta, const uint16_t* q_norm,
                            const uint16_t* k_norm, float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
                            void* stream);
 
 /* out[i] = fp16_RNE(x[i]), i < n (values beyond the fp16 range become inf).
- * x: fp32, out: fp16, device; n >= 0. */
+ * x: fp32, out: fp16, device; n >= 0.
+ * (Sec. 3.2: conversion between the kernels of a decode step.) */
 qm_status qdec_cast_f16(const float* x, int64_t n, uint16_t* out, void* stream);
 
 /* Greedy sampling: *token = the index of the largest of logits[0 .. n),
@@ -408,16 +413,23 @@ qm_status qdec_cast_f16(const float* x, int64_t n, uint16_t* out, void* stream);
  * workspace: caller-owned device scratch of at least
  * QDEC_ARGMAX_WORKSPACE_BYTES bytes, 4-byte aligned, contents not
  * preserved (partial maxima of up to 256 workgroups).  One launch for
- * n <= 4096, else two. */
+ * n <= 4096, else two.
+ * (Sec. 3.2: sampling kernel of the decode step.) */
 #define QDEC_ARGMAX_WORKSPACE_BYTES 2048
 qm_status qdec_argmax(const float* logits, int64_t n, int32_t* token, void* workspace, size_t ws_bytes,
                       void* stream);
 
-/* Host-only: workspace bytes qmoe_grouped_gemm needs for m tokens. */
+/* Host-only: workspace bytes qmoe_grouped_gemm needs for m tokens, so the
+ * caller allocates it once for the largest chunk (Sec. 3.2: no allocation on
+ * the hot path; Sec. 3.4: bounded prefill chunks).  Covers h and the
+ * per-assignment outputs. */
 qm_status qmoe_workspace_bytes(int64_t m, int32_t n_experts, int32_t top_k, int64_t hidden,
                                int64_t inter, size_t* bytes);
 
-/* MoE routing and bucketing (device in/out; all int32/fp32):
+/* MoE routing and bucketing for the mixture-of-experts models (Sec. 4.1:
+ * Qwen3-30B-A3B, 128 experts, 8 active per token; the paper gives no routing
+ * formula, so the top-k-then-softmax router of the model family is taken)
+ * (device in/out; all int32/fp32):
  *  logits [m][n_experts] fp32 -> topk_ids [m][top_k]: per token the top_k
  *  experts by logit, descending, equal logits -> lower expert first;
  *  topk_w [m][top_k]: softmax over those top_k logits (fp32);
@@ -430,16 +442,21 @@ qm_status qmoe_route(const float* logits, int64_t m, int32_t n_experts, int32_t 
                      int32_t* topk_ids, float* topk_w, int32_t* counts, int32_t* offsets,
                      int32_t* sorted_assign, void* stream);
 
-/* Routed SwiGLU expert layer (grouped GEMMs + weighted combine):
+/* Routed SwiGLU expert layer (grouped GEMMs + weighted combine) of the MoE
+ * models (Sec. 4.1; Sec. 3.3: the quantised GEMM per format with the
+ * activation fused into the producing kernel; Sec. 4.3: MoE prefill):
  *  for every assignment a = t*top_k + j, with e the expert whose bucket
  *  [offsets[e], offsets[e+1]) of sorted_assign holds a:
  *    h_a = silu(Wg_e x_t) * (Wu_e x_t),  y_a = Wd_e h_a,
  *  y[t] = sum_j topk_w[t][j] * y_{t*top_k+j}, summed in slot order j.
  *  w_gate, w_up: DEVICE layout Q4, batch E, [E][inter][hidden];
  *  w_down: DEVICE layout Q4, batch E, [E][hidden][inter];
- *  x: fp16 [m][hidden]; y: fp32 [m][hidden]; topk_w [m][top_k], counts,
- *  offsets and sorted_assign come from qmoe_route (sorted_assign must be a
- *  permutation of 0 .. m*top_k-1 consistent with counts/offsets).
+ *  x: fp16 [m][hidden]; y: fp32 [m][hidden]; topk_ids, topk_w [m][top_k],
+ *  counts, offsets and sorted_assign come from qmoe_route (sorted_assign
+ *  must be a permutation of 0 .. m*top_k-1 consistent with counts/offsets).
+ *  topk_ids is checked on the device against the buckets: an assignment a
+ *  placed in the bucket of expert e with topk_ids[a] != e makes its token's
+ *  row of y NaN (no host synchronisation, so no status code for it).
  *  hidden % 32 == 0 and inter % 32 == 0.  h and the gate-weighted
  *  per-assignment outputs topk_w * y_a are held in fp16 (summed in fp32);
  *  all GEMMs use fp16 MFMA with fp32 accumulation.  The workspace (device,
@@ -448,14 +465,17 @@ qm_status qmoe_route(const float* logits, int64_t m, int32_t n_experts, int32_t 
  *  device.  Deterministic. */
 qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up,
                             const qm_qweight* w_down, const uint16_t* x, int64_t m,
-                            int32_t top_k, const float* topk_w,
+                            int32_t top_k, const int32_t* topk_ids, const float* topk_w,
                             const int32_t* counts, const int32_t* offsets,
                             const int32_t* sorted_assign, float* y, void* workspace,
                             size_t ws_bytes, void* stream);
 
 /* Writes a one-line description of the per-chip launch table chosen for the
- * current device (arch, CU count, tile choices) into buf (Sec. 3.3: kernel
- * geometry from a per-chip configuration). */
+ * current device into buf (Sec. 3.3: kernel geometry from a per-chip
+ * configuration): arch, CU count, the Q4 GEMV kernel (name with template
+ * arguments) of each projection shape of the benchmark decode stacks as
+ * "gemv_q4(K->N)=name", and the prefill and MoE tile choices.  Truncated
+ * to len - 1 characters (about 1 KiB is enough). */
 qm_status qm_device_config(char* buf, size_t len);
 
 #ifdef __cplusplus

@@ -290,7 +290,19 @@ def dequantise_experts(qbytes, s16, fmt) -> np.ndarray:
 
 def moe_layer(x_f16, logits, top_k,
               gate_q, gate_s, up_q, up_s, down_q, down_s, fmt=Q4):
-    """Routed MoE layer: out[t] = sum_j gates[t][j] * FFN_{ids[t][j]}(x_t).
+    """Routed MoE layer: out[t] = sum_j gates[t][j] * FFN_{ids[t][j]}(x_t),
+    with expert e's weights dequantised from its codes and scales.
+    Returns (out fp64 [M][H], ids, gates, counts, offsets, sorted_assign).
+    """
+    def weights(e):
+        return (dequantise(gate_q[e], gate_s[e], fmt), dequantise(up_q[e], up_s[e], fmt),
+                dequantise(down_q[e], down_s[e], fmt))
+    return moe_layer_dequantised(x_f16, logits, top_k, gate_q.shape[0], weights)
+
+
+def moe_layer_dequantised(x_f16, logits, top_k, n_experts, expert_weights):
+    """The routed MoE layer given the dequantised experts:
+    expert_weights(e) -> (W'_gate [I][H], W'_up [I][H], W'_down [H][I]).
 
     Each expert's FFN is applied to the tokens that the bucketing hands it;
     the weighted sum then runs over the slots of each token in slot order.
@@ -298,21 +310,21 @@ def moe_layer(x_f16, logits, top_k,
     """
     x = np.asarray(x_f16, dtype=np.float16).astype(np.float64)
     m = x.shape[0]
-    n_exp = gate_q.shape[0]
     ids, gates = moe_route(logits, top_k)
-    counts, offsets, sorted_assign = moe_bucket(ids, n_exp)
-    hidden = down_q.shape[1]
-    y_assign = np.zeros((m * top_k, hidden), dtype=np.float64)
-    for e in range(n_exp):
+    counts, offsets, sorted_assign = moe_bucket(ids, n_experts)
+    y_assign = None
+    for e in range(n_experts):
         rows = sorted_assign[offsets[e]:offsets[e + 1]]
         if rows.size == 0:
             continue
         tok = rows // top_k
-        wg = dequantise(gate_q[e], gate_s[e], fmt).astype(np.float64)
-        wu = dequantise(up_q[e], up_s[e], fmt).astype(np.float64)
-        wd = dequantise(down_q[e], down_s[e], fmt).astype(np.float64)
+        wg, wu, wd = (np.asarray(w, dtype=np.float64) for w in expert_weights(e))
+        if y_assign is None:
+            y_assign = np.zeros((m * top_k, wd.shape[0]), dtype=np.float64)
         y_assign[rows] = expert_ffn(x[tok], wg, wu, wd)
-    out = np.zeros((m, hidden), dtype=np.float64)
+    if y_assign is None:                       # no tokens
+        y_assign = np.zeros((0, np.shape(expert_weights(0)[2])[0]), dtype=np.float64)
+    out = np.zeros((m, y_assign.shape[1]), dtype=np.float64)
     for j in range(top_k):
         out += gates[:, j:j + 1] * y_assign[np.arange(m) * top_k + j]
     return out, ids, gates, counts, offsets, sorted_assign

@@ -31,7 +31,7 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
            "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
            "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
-           "qmatmul_gemv_swiglu_rmsnorm_f16", "qattn_decode_rope_f16", "qdec_rope_table",
+           "qmatmul_gemv_swiglu_rmsnorm_f16", "qdec_rope_table",
            "qmatmul_gemv_qkv_rmsnorm_rope", "qdec_embed_rows", "qdec_rope_append_rows", "qdec_heads_to_rows_f16",
            "qdec_swiglu_f16")
 
@@ -74,7 +74,7 @@ def lib() -> ctypes.CDLL:
             "qmatmul_gemm_grouped": [i32, W, vp, i64, ctypes.POINTER(vp), vp],
             "qmoe_workspace_bytes": [i64, i32, i32, i64, i64, ctypes.POINTER(sz)],
             "qmoe_route": [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp],
-            "qmoe_grouped_gemm": [W, W, W, vp, i64, i32, vp, vp, vp, vp, vp, vp, sz, vp],
+            "qmoe_grouped_gemm": [W, W, W, vp, i64, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
             "qm_device_config": [ctypes.c_char_p, sz],
             "qattn_decode_workspace_bytes": [i32, i32, ctypes.POINTER(sz)],
             "qattn_decode": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
@@ -89,8 +89,6 @@ def lib() -> ctypes.CDLL:
             "qdec_swiglu_f16": [vp, vp, i64, vp, vp],
             "qmatmul_gemv_qkv_rmsnorm_rope": [W, vp, vp, vp, ctypes.c_float, vp, i32, i32, i32, i64, i64, vp, vp, vp,
                                               vp, vp],
-            "qattn_decode_rope_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, ctypes.c_float, vp, vp,
-                                      vp, vp, sz, vp],
             "qmatmul_gemv_grouped_rmsnorm": [i32, W, vp, vp, vp, ctypes.c_float, vp, ctypes.POINTER(vp), vp],
             "qmatmul_gemv_swiglu_rmsnorm_f16": [W, W, vp, vp, vp, ctypes.c_float, vp, vp, vp],
             "qattn_decode_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
@@ -284,6 +282,16 @@ def qdec_embed_rows(table: torch.Tensor, tokens: torch.Tensor, out: Optional[tor
     return out
 
 
+def _check_head_gains(q_norm, k_norm, d):
+    """The per-head q/k norm gains: both absent, or fp16 contiguous [D] each
+    (the kernel reads exactly D fp16 values from each pointer)."""
+    assert (q_norm is None) == (k_norm is None), "q_norm and k_norm go together"
+    for g in (q_norm, k_norm):
+        if g is not None:
+            assert g.dtype == torch.float16 and g.is_contiguous() and g.numel() == d, \
+                "q/k norm gains must be fp16, contiguous, head_dim elements"
+
+
 def qdec_rope_append_rows(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, p0: int, theta: float,
                           k_cache: torch.Tensor, v_cache: torch.Tensor, interleaved: bool = False,
                           q_out: Optional[torch.Tensor] = None, q_norm: Optional[torch.Tensor] = None,
@@ -293,6 +301,10 @@ def qdec_rope_append_rows(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, p0:
     m = q.shape[0]
     hq = q.shape[1] // d
     assert q.dtype == k.dtype == v.dtype == torch.float32 and k.shape == v.shape == (m, hkv * d)
+    assert q.is_contiguous() and k.is_contiguous() and v.is_contiguous() and q.shape[1] == hq * d
+    assert k_cache.dtype == v_cache.dtype == torch.float16 and v_cache.shape == k_cache.shape
+    assert k_cache.is_contiguous() and v_cache.is_contiguous()
+    _check_head_gains(q_norm, k_norm, d)
     if q_out is None:
         q_out = torch.empty((hq, m, d), dtype=torch.float16, device=q.device)
     _check(lib().qdec_rope_append_rows(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, m, p0, max_len, theta,
@@ -412,26 +424,6 @@ def qattn_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, 
     return out
 
 
-def qattn_decode_rope_f16(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: int, theta: float, scale: float,
-                          k_cache: torch.Tensor, v_cache: torch.Tensor, out: Optional[torch.Tensor] = None,
-                          workspace: Optional[torch.Tensor] = None, stream=None):
-    """RoPE + cache append at row pos + decode attention over rows 0..pos:
-    q fp32 [Hq*D], k, v fp32 [Hkv*D] -> fp16 [Hq][D]."""
-    hkv, max_len, d = k_cache.shape
-    hq = q.numel() // d
-    assert q.dtype == k.dtype == v.dtype == torch.float32 and k.numel() == v.numel() == hkv * d
-    assert k_cache.dtype == v_cache.dtype == torch.float16 and v_cache.shape == k_cache.shape
-    assert k_cache.is_contiguous() and v_cache.is_contiguous()
-    if out is None:
-        out = torch.empty((hq, d), dtype=torch.float16, device=q.device)
-    if workspace is None:
-        workspace = torch.empty(qattn_decode_workspace_bytes(hq, d), dtype=torch.uint8, device=q.device)
-    _check(lib().qattn_decode_rope_f16(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, pos, max_len, theta, scale,
-                                       _ptr(k_cache), _ptr(v_cache), _ptr(out), _ptr(workspace), workspace.numel(),
-                                       _stream(stream)))
-    return out
-
-
 def qattn_prefill(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, p0: int, scale: float,
                   out: Optional[torch.Tensor] = None, stream=None):
     """q: fp16 [Hq][m][D] at positions p0..p0+m-1; k_cache, v_cache: fp16
@@ -484,6 +476,7 @@ def qdec_rope_append(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: int
     assert q.dtype == k.dtype == v.dtype == torch.float32 and k.numel() == v.numel() == hkv * d
     assert k_cache.dtype == v_cache.dtype == torch.float16 and v_cache.shape == k_cache.shape
     assert k_cache.is_contiguous() and v_cache.is_contiguous()
+    _check_head_gains(q_norm, k_norm, d)
     if q_out is None:
         q_out = torch.empty((hq, d), dtype=torch.float16, device=q.device)
     _check(lib().qdec_rope_append(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, pos, max_len, theta, _ptr(q_norm),
@@ -558,13 +551,13 @@ def qmoe_grouped_gemm(w_gate: QWeight, w_up: QWeight, w_down: QWeight, x: torch.
         nb = qmoe_workspace_bytes(m, w_gate.batch, r.top_k, hidden, w_gate.n)
         workspace = torch.empty(max(nb, 16), dtype=torch.uint8, device=x.device)
     _check(lib().qmoe_grouped_gemm(ctypes.byref(w_gate.c()), ctypes.byref(w_up.c()), ctypes.byref(w_down.c()),
-                                   _ptr(x), m, r.top_k, _ptr(r.gates), _ptr(r.counts), _ptr(r.offsets),
+                                   _ptr(x), m, r.top_k, _ptr(r.ids), _ptr(r.gates), _ptr(r.counts), _ptr(r.offsets),
                                    _ptr(r.sorted_assign), _ptr(out), _ptr(workspace), workspace.numel(),
                                    _stream(stream)))
     return out
 
 
 def qm_device_config() -> str:
-    buf = ctypes.create_string_buffer(512)
-    _check(lib().qm_device_config(buf, 512))
+    buf = ctypes.create_string_buffer(4096)
+    _check(lib().qm_device_config(buf, 4096))
     return buf.value.decode()

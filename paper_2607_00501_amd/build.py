@@ -24,6 +24,10 @@ COMMON = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I" + os.path.join(os.path.dirname(HERE), "include"),
 ]
+# QM_BUILD_TUNING=1 builds a library that honours the QM_*_PLAN launch-plan
+# overrides (for tuning sweeps only; the default build ignores them).
+if os.environ.get("QM_BUILD_TUNING") == "1":
+    COMMON.append("-DQM_TUNING_OVERRIDES")
 SOURCES = ["api.cpp", "format.hip", "gemv.hip", "gemm.hip", "moe.hip", "attention.hip", "decode.hip"]
 
 

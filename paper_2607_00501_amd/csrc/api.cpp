@@ -577,37 +577,6 @@ qm_status qattn_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_
                           workspace, ws_bytes, stream, "qattn_decode");
 }
 
-qm_status qattn_decode_rope_f16(const float* q, const float* k, const float* v, int32_t n_q_heads,
-                                int32_t n_kv_heads, int32_t head_dim, int64_t pos, int64_t max_len, float theta,
-                                float scale, uint16_t* k_cache, uint16_t* v_cache, uint16_t* o, void* workspace,
-                                size_t ws_bytes, void* stream) {
-  const char* name = "qattn_decode_rope_f16";
-  if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "%s: head_dim=%d must be 64 or 128", name, head_dim);
-  if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads > 1024 || n_q_heads % n_kv_heads != 0 ||
-      n_q_heads / n_kv_heads > 8)
-    return fail(QM_ESHAPE, "%s: n_q_heads=%d must be a multiple of n_kv_heads=%d, at most 8 per KV head", name,
-                n_q_heads, n_kv_heads);
-  if (max_len < 1 || max_len > kAttnMaxLen || pos < 0 || pos >= max_len)
-    return fail(QM_ESHAPE, "%s: need 0 <= pos < max_len <= %lld", name, (long long)kAttnMaxLen);
-  if (!(scale == scale) || scale == INFINITY || scale == -INFINITY)
-    return fail(QM_EINVAL, "%s: scale must be finite", name);
-  if (!(theta > 1.0f) || theta == INFINITY) return fail(QM_EINVAL, "%s: theta must be finite and > 1", name);
-  if (!q || !k || !v || !k_cache || !v_cache || !o) return fail(QM_EINVAL, "%s: null pointer", name);
-  if (!aligned4(q) || !aligned4(k) || !aligned4(v) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned2(o))
-    return fail(QM_EALIGN, "%s: q, k, v 4-byte, caches 16-byte, o 2-byte aligned", name);
-  const size_t need = attn_decode_workspace_bytes(n_q_heads, head_dim);
-  if (!workspace || ws_bytes < need)
-    return fail(QM_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", name, need, ws_bytes);
-  if (!aligned16(workspace)) return fail(QM_EALIGN, "%s: workspace must be 16-byte aligned", name);
-  const DeviceInfo* d;
-  qm_status st;
-  if ((st = device_info(&d)) != QM_OK) return st;
-  return launched(launch_attn_decode_rope(q, k, v, n_q_heads, n_kv_heads, head_dim, pos, max_len, theta, scale,
-                                          k_cache, v_cache, o, static_cast<float*>(workspace), d->cu_count,
-                                          static_cast<hipStream_t>(stream)),
-                  name);
-}
-
 qm_status qattn_decode_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
                            int32_t n_kv_heads, int32_t head_dim, int64_t len, int64_t max_len, float scale,
                            uint16_t* o, void* workspace, size_t ws_bytes, void* stream) {
@@ -733,7 +702,8 @@ qm_status qmoe_route(const float* logits, int64_t m, int32_t n_experts, int32_t 
 }
 
 qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up, const qm_qweight* w_down,
-                            const uint16_t* x, int64_t m, int32_t top_k, const float* topk_w, const int32_t* counts, const int32_t* offsets,
+                            const uint16_t* x, int64_t m, int32_t top_k, const int32_t* topk_ids, const float* topk_w,
+                            const int32_t* counts, const int32_t* offsets,
                             const int32_t* sorted_assign, float* y, void* workspace, size_t ws_bytes,
                             void* stream) {
   qm_status st;
@@ -755,7 +725,7 @@ qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up, co
     return fail(QM_ESHAPE, "qmoe_grouped_gemm: top_k=%d must be in [1, min(16, E)]", top_k);
   if (m < 0 || m > 65536) return fail(QM_ESHAPE, "qmoe_grouped_gemm: m must be in [0, 65536]");
   if (m == 0) return QM_OK;
-  if (!x || !topk_w || !counts || !offsets || !sorted_assign || !y)
+  if (!x || !topk_ids || !topk_w || !counts || !offsets || !sorted_assign || !y)
     return fail(QM_EINVAL, "qmoe_grouped_gemm: null pointer");
   if (!aligned16(x) || !aligned16(y)) return fail(QM_EALIGN, "qmoe_grouped_gemm: x and y must be 16-byte aligned");
   const size_t need = moe_workspace_bytes(m, top_k, hidden, inter);
@@ -769,6 +739,7 @@ qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up, co
   a.uq = static_cast<const uint8_t*>(w_up->qdata); a.us = w_up->scales;
   a.dq = static_cast<const uint8_t*>(w_down->qdata); a.ds = w_down->scales;
   a.x = x; a.counts = counts; a.offsets = offsets; a.sorted_assign = sorted_assign; a.topk_w = topk_w;
+  a.topk_ids = topk_ids;
   a.y = y;
   const size_t h_bytes = (static_cast<size_t>(m * top_k * inter) * 2 + 255) / 256 * 256;
   a.h = static_cast<uint16_t*>(workspace);
@@ -783,15 +754,22 @@ qm_status qm_device_config(char* buf, size_t len) {
   const DeviceInfo* d;
   qm_status st;
   if ((st = device_info(&d)) != QM_OK) return st;
-  std::snprintf(buf, len,
-                "arch=%s cu=%d gemv(1024x1024: rows/wg=%d waves=%d) gemv(3072->1024: rows/wg=%d waves=%d) "
-                "gemv(lm_head 1024->151936: rows/wg=%d waves=%d) "
-                "gemm_tile(m=512,n=2048)=%s moe_tile(rows/expert=8)=%s moe_tile(rows/expert=128)=%s",
-                d->arch, d->cu_count, gemv_plan(QM_Q4_G32, 1024, 1024, d->cu_count).subr,
-                gemv_plan(QM_Q4_G32, 1024, 1024, d->cu_count).waves, gemv_plan(QM_Q4_G32, 1024, 3072, d->cu_count).subr,
-                gemv_plan(QM_Q4_G32, 1024, 3072, d->cu_count).waves, gemv_plan(QM_Q4_G32, 151936, 1024, d->cu_count).subr,
-                gemv_plan(QM_Q4_G32, 151936, 1024, d->cu_count).waves, gemm_tile_name(512, 2048),
-                moe_tile_name(8), moe_tile_name(128));
+  // The Q4 GEMV kernel of each projection shape of the decode stacks
+  // (K -> N), then the prefill and MoE tile choices.
+  static const int64_t shapes[][2] = {{1024, 1024}, {1024, 2048}, {2048, 1024}, {1024, 3072}, {3072, 1024},
+                                      {1024, 151936}, {3072, 3072}, {3072, 8192}, {8192, 3072},
+                                      {3072, 128256}};
+  int used = std::snprintf(buf, len, "arch=%s cu=%d", d->arch, d->cu_count);
+  for (const auto& sh : shapes) {
+    if (used < 0 || static_cast<size_t>(used) >= len) break;
+    char name[96];
+    gemv_kernel_name(QM_Q4_G32, sh[1], sh[0], d->cu_count, name, sizeof name);
+    used += std::snprintf(buf + used, len - used, " gemv_q4(%lld->%lld)=%s", static_cast<long long>(sh[0]),
+                          static_cast<long long>(sh[1]), name);
+  }
+  if (used >= 0 && static_cast<size_t>(used) < len)
+    std::snprintf(buf + used, len - used, " gemm_tile(m=512,n=2048)=%s moe_tile(rows/expert=8)=%s "
+                  "moe_tile(rows/expert=128)=%s", gemm_tile_name(512, 2048), moe_tile_name(8), moe_tile_name(128));
   return QM_OK;
 }
 

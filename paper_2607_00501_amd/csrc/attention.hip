@@ -23,7 +23,6 @@
 //    softmax does: M = max m_i, L = sum l_i 2^(m_i - M), o = sum acc_i
 //    2^(m_i - M) / L.
 #include "qm_internal.h"
-#include "rope.h"
 
 #include <hip/hip_fp16.h>
 
@@ -58,31 +57,11 @@ __device__ __forceinline__ void store_out(float* o, uint16_t* o16, int64_t i, fl
   }
 }
 
-// The new token's RoPE and cache append folded into decode attention: fp32
-// projections in, every slice rotates its G query slices itself, and the
-// slice holding row pos = len - 1 rotates the key, writes that row of both
-// caches and uses the row from LDS (its own global writes are never read
-// back by it).
-struct RopeIn {
-  const float* q;       // [Hq][D] fp32
-  const float* k;       // [Hkv][D] fp32
-  const float* v;       // [Hkv][D] fp32
-  uint16_t* kc;         // caches, row pos written
-  uint16_t* vc;
-  double log2_theta;
-};
-
-__device__ __forceinline__ uint32_t pack_h2(float lo, float hi) {
-  const _Float16 a = static_cast<_Float16>(lo), b = static_cast<_Float16>(hi);
-  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
-         static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16;
-}
-
-template <int D, int G, bool ROPE = false>
+template <int D, int G>
 __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     int64_t len, int64_t max_len, int tc, int nsplit, float scale_log2, float* __restrict__ ws,
-    float* __restrict__ o, uint16_t* __restrict__ o16, RopeIn rp = RopeIn{}) {
+    float* __restrict__ o, uint16_t* __restrict__ o16) {
   constexpr int LPR = D / 8;                 // lanes per cache row
   constexpr int RPW = 64 / LPR;              // rows per wavefront load
   constexpr int RPI = kAttnWaves * RPW;      // rows per workgroup load
@@ -98,75 +77,12 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
 
   // Query slices of the G heads: dimensions 8 sub .. 8 sub + 7.
   half2v qf[G][4];
-  const int64_t pos = len - 1;
-  __shared__ uint4 newrow[2][D / 8];           // ROPE: the new K and V rows (fp16)
-  const bool owns_new = ROPE && t0 + nrows > pos;
-  if constexpr (ROPE) {
-    constexpr int H = D / 2;
-    // The D/2 angles once per workgroup (one fp64 sine and cosine per thread).
-    __shared__ float2 cs_tab[H];
-    if (threadIdx.x < H) cs_tab[threadIdx.x] = rope_cos_sin(pos, threadIdx.x, D, rp.log2_theta);
-    __syncthreads();
-    float c[8], s[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float2 cs = cs_tab[(sub * 8 + e) % H];
-      c[e] = cs.x;
-      s[e] = cs.y;
-    }
-    const bool low = sub * 8 < H;               // the lane's 8 dimensions are all below or all above D/2
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-      const float* src = rp.q + (static_cast<int64_t>(g) * G + j) * D;
-      float r[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int dd = sub * 8 + e;
-        const float a = src[low ? dd : dd - H], b = src[low ? dd + H : dd];
-        r[e] = low ? rope_low(a, b, c[e], s[e]) : rope_high(a, b, c[e], s[e]);
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) qf[j][e] = __builtin_bit_cast(half2v, pack_h2(r[2 * e], r[2 * e + 1]));
-    }
-    if (owns_new) {
-      // Threads 0 .. D/8 - 1 build 8 dimensions of the key row, the next D/8
-      // those of the value row; both go to the caches and to LDS.
-      const int t = threadIdx.x;
-      if (t < D / 4) {
-        const bool isk = t < D / 8;
-        const int c8 = isk ? t : t - D / 8;
-        const float* src = (isk ? rp.k : rp.v) + static_cast<int64_t>(g) * D;
-        const bool lo = c8 * 8 < H;
-        float r[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int dd = c8 * 8 + e;
-          if (isk) {
-            const float2 cs = cs_tab[dd % H];
-            const float cc = cs.x, ss = cs.y;
-            const float a = src[lo ? dd : dd - H], b = src[lo ? dd + H : dd];
-            r[e] = lo ? rope_low(a, b, cc, ss) : rope_high(a, b, cc, ss);
-          } else {
-            r[e] = src[dd];
-          }
-        }
-        const uint4 row = make_uint4(pack_h2(r[0], r[1]), pack_h2(r[2], r[3]), pack_h2(r[4], r[5]),
-                                     pack_h2(r[6], r[7]));
-        newrow[isk ? 0 : 1][c8] = row;
-        uint16_t* dst = (isk ? rp.kc : rp.vc) + (static_cast<int64_t>(g) * max_len + pos) * D + c8 * 8;
-        *reinterpret_cast<uint4*>(dst) = row;
-      }
-      __syncthreads();
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-      const uint4 t = *reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(g) * G + j) * D + sub * 8);
-      qf[j][0] = __builtin_bit_cast(half2v, t.x); qf[j][1] = __builtin_bit_cast(half2v, t.y);
-      qf[j][2] = __builtin_bit_cast(half2v, t.z); qf[j][3] = __builtin_bit_cast(half2v, t.w);
-    }
+  for (int j = 0; j < G; ++j) {
+    const uint4 t = *reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(g) * G + j) * D + sub * 8);
+    qf[j][0] = __builtin_bit_cast(half2v, t.x); qf[j][1] = __builtin_bit_cast(half2v, t.y);
+    qf[j][2] = __builtin_bit_cast(half2v, t.z); qf[j][3] = __builtin_bit_cast(half2v, t.w);
   }
-  const int new_r = static_cast<int>(pos - t0);   // the new row inside the slice (owns_new only)
   const int64_t head_row0 = static_cast<int64_t>(g) * max_len + t0;
   const uint16_t* kb = k + head_row0 * D + sub * 8;
   const uint16_t* vb = v + head_row0 * D + sub * 8;
@@ -182,14 +98,12 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
     for (int u = 0; u < kAttnUnroll; ++u) {
       const int r = min(r0 + u * RPI + wave * RPW + rw, nrows - 1);
       kv[u] = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D);
-      if (owns_new && r == new_r) kv[u] = newrow[0][sub];
     }
     if (r0 == 0) {
 #pragma unroll
       for (int u = 0; u < kAttnUnroll; ++u) {
         const int r = min(u * RPI + wave * RPW + rw, nrows - 1);
         vpre[u] = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(r) * D);
-        if (owns_new && r == new_r) vpre[u] = newrow[1][sub];
       }
     }
 #pragma unroll
@@ -242,7 +156,6 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_decode_split_kernel(
     for (int u = 0; u < kAttnUnroll; ++u) {
       const int r = min(r0 + u * RPI + wave * RPW + rw, nrows - 1);
       vv[u] = r0 == 0 ? vpre[u] : *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(r) * D);
-      if (owns_new && r == new_r) vv[u] = newrow[1][sub];
     }
 #pragma unroll
     for (int u = 0; u < kAttnUnroll; ++u) {
@@ -356,17 +269,13 @@ __global__ __launch_bounds__(D) void attn_decode_combine_kernel(const float* __r
 template <int D, int G>
 hipError_t launch_decode_dg(const uint16_t* q, const uint16_t* k, const uint16_t* v, int hkv, int64_t len,
                             int64_t max_len, float scale, float* o, uint16_t* o16, float* ws, const AttnPlan& p,
-                            const RopeIn* rp, hipStream_t st) {
+                            hipStream_t st) {
   const size_t lds = static_cast<size_t>(G) * p.tc * sizeof(float);
   const float sl2 = scale * 1.4426950408889634f;
   float* od = p.nsplit == 1 ? o : nullptr;
   uint16_t* od16 = p.nsplit == 1 ? o16 : nullptr;
-  if (rp)
-    hipLaunchKernelGGL((attn_decode_split_kernel<D, G, true>), dim3(p.nsplit, hkv), dim3(kAttnWaves * 64), lds, st,
-                       q, k, v, len, max_len, p.tc, p.nsplit, sl2, ws, od, od16, *rp);
-  else
-    hipLaunchKernelGGL((attn_decode_split_kernel<D, G, false>), dim3(p.nsplit, hkv), dim3(kAttnWaves * 64), lds, st,
-                       q, k, v, len, max_len, p.tc, p.nsplit, sl2, ws, od, od16, RopeIn{});
+  hipLaunchKernelGGL((attn_decode_split_kernel<D, G>), dim3(p.nsplit, hkv), dim3(kAttnWaves * 64), lds, st,
+                     q, k, v, len, max_len, p.tc, p.nsplit, sl2, ws, od, od16);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.nsplit == 1) return e;
   hipLaunchKernelGGL((attn_decode_combine_kernel<D>), dim3(hkv * G), dim3(D), 0, st, ws, p.nsplit, o, o16);
@@ -376,16 +285,16 @@ hipError_t launch_decode_dg(const uint16_t* q, const uint16_t* k, const uint16_t
 template <int D>
 hipError_t launch_decode_d(int group, const uint16_t* q, const uint16_t* k, const uint16_t* v, int hkv, int64_t len,
                            int64_t max_len, float scale, float* o, uint16_t* o16, float* ws, const AttnPlan& p,
-                           const RopeIn* rp, hipStream_t st) {
+                           hipStream_t st) {
   switch (group) {
-    case 1: return launch_decode_dg<D, 1>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, rp, st);
-    case 2: return launch_decode_dg<D, 2>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, rp, st);
-    case 3: return launch_decode_dg<D, 3>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, rp, st);
-    case 4: return launch_decode_dg<D, 4>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, rp, st);
-    case 5: return launch_decode_dg<D, 5>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, rp, st);
-    case 6: return launch_decode_dg<D, 6>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, rp, st);
-    case 7: return launch_decode_dg<D, 7>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, rp, st);
-    default: return launch_decode_dg<D, 8>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, rp, st);
+    case 1: return launch_decode_dg<D, 1>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 2: return launch_decode_dg<D, 2>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 3: return launch_decode_dg<D, 3>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 4: return launch_decode_dg<D, 4>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 5: return launch_decode_dg<D, 5>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 6: return launch_decode_dg<D, 6>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    case 7: return launch_decode_dg<D, 7>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
+    default: return launch_decode_dg<D, 8>(q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
   }
 }
 
@@ -650,20 +559,8 @@ hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16
                               float* ws, int cu_count, hipStream_t st) {
   const int group = hq / hkv;
   const AttnPlan p = attn_decode_plan(hkv, group, len, cu_count);
-  return d == 64 ? launch_decode_d<64>(group, q, k, v, hkv, len, max_len, scale, o, o16, ws, p, nullptr, st)
-                 : launch_decode_d<128>(group, q, k, v, hkv, len, max_len, scale, o, o16, ws, p, nullptr, st);
-}
-
-hipError_t launch_attn_decode_rope(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv,
-                                   int32_t d, int64_t pos, int64_t max_len, float theta, float scale,
-                                   uint16_t* kc, uint16_t* vc, uint16_t* o16, float* ws, int cu_count,
-                                   hipStream_t st) {
-  const int group = hq / hkv;
-  const int64_t len = pos + 1;
-  const AttnPlan p = attn_decode_plan(hkv, group, len, cu_count);
-  const RopeIn rp{q, k, v, kc, vc, std::log2(static_cast<double>(theta))};
-  return d == 64 ? launch_decode_d<64>(group, kc, kc, vc, hkv, len, max_len, scale, nullptr, o16, ws, p, &rp, st)
-                 : launch_decode_d<128>(group, kc, kc, vc, hkv, len, max_len, scale, nullptr, o16, ws, p, &rp, st);
+  return d == 64 ? launch_decode_d<64>(group, q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st)
+                 : launch_decode_d<128>(group, q, k, v, hkv, len, max_len, scale, o, o16, ws, p, st);
 }
 
 }  // namespace qm

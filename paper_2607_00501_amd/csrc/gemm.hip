@@ -42,7 +42,7 @@ GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count) {
   // instantiated tiles, see launch_args).
   static const GemmPlan forced = [] {
     GemmPlan f{0, 0, 0};
-    if (const char* e = std::getenv("QM_GEMM_PLAN")) std::sscanf(e, "%d,%d,%d", &f.bm, &f.wn, &f.wk);
+    if (const char* e = tuning_override("QM_GEMM_PLAN")) std::sscanf(e, "%d,%d,%d", &f.bm, &f.wn, &f.wk);
     return f;
   }();
   if (forced.bm != 0 && gemm_plan_instantiated(forced)) return forced;

@@ -828,7 +828,7 @@ GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count) {
   // Tuning sweeps only: QM_GEMV_PLAN="rows,waves,x_in_lds" forces the plan.
   static const GemvPlan forced = [] {
     GemvPlan f{0, 0, 1};
-    if (const char* e = std::getenv("QM_GEMV_PLAN")) std::sscanf(e, "%d,%d,%d", &f.subr, &f.waves, &f.xlds);
+    if (const char* e = tuning_override("QM_GEMV_PLAN")) std::sscanf(e, "%d,%d,%d", &f.subr, &f.waves, &f.xlds);
     return f;
   }();
   if (forced.subr == 4 || forced.subr == 8 || forced.subr == 16 || forced.subr == 32 || forced.subr == 64) {
@@ -866,6 +866,15 @@ GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count) {
   p.waves = 8;
   p.xlds = k <= 4096 ? 1 : 0;
   return p;
+}
+
+void gemv_kernel_name(int32_t fmt, int64_t n, int64_t k, int cu_count, char* buf, size_t len) {
+  const GemvPlan p = gemv_plan(fmt, n, k, cu_count);
+  if (p.subr == kPanel)
+    std::snprintf(buf, len, "gemv_kernel<%d, %d, %d>", fmt, p.waves,
+                  fmt == QM_Q4_G32 ? kPanelUnroll<QM_Q4_G32> : fmt == QM_Q8_G32 ? kPanelUnroll<QM_Q8_G32> : 0);
+  else
+    std::snprintf(buf, len, "gemv_sub_kernel<%d, %d, %d, %s>", fmt, p.subr, p.waves, p.xlds ? "true" : "false");
 }
 
 hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count, hipStream_t st) {

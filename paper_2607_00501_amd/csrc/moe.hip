@@ -291,6 +291,7 @@ hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
   auto tiles = [&](int bm) { return static_cast<unsigned>((A + bm - 1) / bm + a.n_experts); };
   QgemmArgs g{};
   g.counts = a.counts; g.offsets = a.offsets; g.sorted_assign = a.sorted_assign; g.topk_w = a.topk_w;
+  g.topk_ids = a.topk_ids;
   g.n_experts = a.n_experts; g.top_k = a.top_k; g.M = A;
   // gate/up + SwiGLU: A = x rows gathered per assignment, N = inter, K = hidden
   g.q = a.gq; g.s = a.gs; g.q2 = a.uq; g.s2 = a.us; g.a = a.x; g.h = a.h; g.N = a.inter; g.K = a.hidden;
@@ -360,7 +361,7 @@ hipError_t launch_moe(const MoeArgs& a, int cu_count, hipStream_t st) {
   // depth_gate_up,depth_down,nontemporal".
   static const std::array<int, 7> forced = [] {
     std::array<int, 7> f{0, 0, 0, 0, 2, 2, 0};
-    if (const char* e = std::getenv("QM_MOE_PLAN"))
+    if (const char* e = tuning_override("QM_MOE_PLAN"))
       std::sscanf(e, "%d,%d,%d,%d,%d,%d,%d", &f[0], &f[1], &f[2], &f[3], &f[4], &f[5], &f[6]);
     return f;
   }();

@@ -67,6 +67,7 @@ struct QgemmArgs {
   const int32_t* offsets;
   const int32_t* sorted_assign;
   const float* topk_w;
+  const int32_t* topk_ids;                 // MoE: expert of each assignment (checked by kMoeDown)
   uint16_t* h;                             // kMoeGateUp output [M][N] fp16 (bucket order)
   uint16_t* yp;                            // kMoeDown output [M][N] fp16 (assignment order)
   int32_t n_experts, top_k;
@@ -391,7 +392,9 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     for (int r = tid; r < BM; r += C::kThreads) {
       const int64_t asg = p.sorted_assign[row0 + min(r, rows - 1)];
       row_asg[r] = asg;
-      row_w[r] = p.topk_w[asg];
+      // An assignment whose bucket is not the expert topk_ids names gets a
+      // NaN weight, so its token's output row is NaN (no host round trip).
+      row_w[r] = p.topk_ids[asg] == expert ? p.topk_w[asg] : __builtin_nanf("");
     }
   }
 

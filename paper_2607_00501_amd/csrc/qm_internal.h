@@ -7,9 +7,24 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <cstdlib>
+
 #include "../../include/qmatmul.h"
 
 namespace qm {
+
+// Launch-plan overrides for tuning sweeps (QM_GEMV_PLAN, QM_GEMM_PLAN,
+// QM_MOE_PLAN) are read only in a library built with -DQM_TUNING_OVERRIDES;
+// the shipped library ignores the environment, so a stray variable cannot
+// change a production launch.
+inline const char* tuning_override(const char* name) {
+#ifdef QM_TUNING_OVERRIDES
+  return std::getenv(name);
+#else
+  (void)name;
+  return nullptr;
+#endif
+}
 
 constexpr int kGroup = 32;   // weights per scale (group along K)
 constexpr int kPanel = 64;   // rows per device-layout panel (one row per lane)
@@ -143,10 +158,6 @@ hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16
 
 // Decode attention with the new token's RoPE and cache append folded in
 // (len = pos + 1; fp16 output).
-hipError_t launch_attn_decode_rope(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv,
-                                   int32_t d, int64_t pos, int64_t max_len, float theta, float scale,
-                                   uint16_t* kc, uint16_t* vc, uint16_t* o16, float* ws, int cu_count,
-                                   hipStream_t st);
 
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
@@ -197,6 +208,7 @@ struct MoeArgs {
   const int32_t* offsets;                  // [E+1]
   const int32_t* sorted_assign;            // [m*top_k]
   const float* topk_w;                     // [m*top_k]
+  const int32_t* topk_ids;                 // [m*top_k]
   float* y;                                // [m][hidden]
   uint16_t* h;                             // workspace: [m*top_k][inter] fp16
   uint16_t* yp;                            // workspace: [m*top_k][hidden] fp16
@@ -214,6 +226,8 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
 // workgroup, and whether activations are staged in LDS (sub-panel kernel).
 struct GemvPlan { int subr; int waves; int xlds; };
 GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count);
+// Name (with template arguments) of the kernel qmatmul_gemv launches for this shape.
+void gemv_kernel_name(int32_t fmt, int64_t n, int64_t k, int cu_count, char* buf, size_t len);
 struct GemmPlan { int bm; int wn; int wk; };   // rows per tile, panels (wavefronts) per K slice, K slices
 GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count);
 bool gemm_plan_instantiated(const GemmPlan& p);   // a prefill GEMM tile exists for p

@@ -62,9 +62,12 @@ class DenseDecoder:
     (qmatmul_gemv_qkv_rmsnorm_rope): 5 launches per layer."""
 
     def __init__(self, cfg: DecoderConfig, emb: torch.Tensor, layers: List[LayerWeights], norm: torch.Tensor,
-                 lm_head: B.QWeight, max_len: int, fused: bool = True, rope_rows_interleaved: bool = False):
+                 lm_head: B.QWeight, max_len: int, fused: bool = True, rope_rows_interleaved: bool = False,
+                 max_chunk: int = 512):
         self.cfg, self.emb, self.layers, self.norm, self.lm_head = cfg, emb, layers, norm, lm_head
         self.max_len = max_len
+        self.max_chunk = max_chunk          # rows of a prompt chunk (prefill)
+        self._chunk = None
         dev = emb.device
         f32 = dict(dtype=torch.float32, device=dev)
         f16 = dict(dtype=torch.float16, device=dev)
@@ -113,9 +116,7 @@ class DenseDecoder:
                     # x2 = x + y_ffn; q, k, v = W . norm(x2)
                     B.qmatmul_gemv_grouped_rmsnorm([ly.wq, ly.wk, ly.wv], self.x, ly.attn_norm, c.eps, self.x2,
                                                    residual=res, outs=[self.q, self.k, self.v], stream=s)
-                    # RoPE + cache append, then attention (folding the two into one
-                    # launch, qattn_decode_rope_f16, measured slower: the fp64
-                    # angles then sit ahead of the attention's first loads)
+                    # RoPE (with the Qwen3 per-head norms) + cache append, then attention
                     B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
                                        q_out=self.q16, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps, stream=s)
                 B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,
@@ -145,26 +146,53 @@ class DenseDecoder:
         B.qmatmul_gemv(self.lm_head, self.h, out=self.logits, stream=s)
         B.qdec_argmax(self.logits, out=self.token, workspace=self.argmax_ws, stream=s)
 
+    def _chunk_buffers(self, m: int) -> dict:
+        """Views of the prompt-chunk buffers for m rows.  The buffers hold
+        max_chunk rows and are allocated on the first prefill only (a decoder
+        that never prefills pays nothing), so later chunks allocate nothing
+        (Sec. 3.2: no allocation in the loop; Sec. 3.4: bounded chunks)."""
+        c = self.cfg
+        qd, kvd = c.n_q_heads * c.head_dim, c.n_kv_heads * c.head_dim
+        shapes = dict(x=((c.hidden,), torch.float32), h=((c.hidden,), torch.float16),
+                      q=((qd,), torch.float32), k=((kvd,), torch.float32), v=((kvd,), torch.float32),
+                      qh=((qd,), torch.float16), o=((qd,), torch.float32), o16=((qd,), torch.float16),
+                      ya=((c.hidden,), torch.float32), g=((c.inter,), torch.float32),
+                      u=((c.inter,), torch.float32), sw=((c.inter,), torch.float16), y=((c.hidden,), torch.float32))
+        if self._chunk is None:
+            dev = self.emb.device
+            self._chunk = {n: torch.empty(self.max_chunk * sh[0], dtype=dt, device=dev)
+                           for n, (sh, dt) in shapes.items()}
+        b = self._chunk
+        rows = lambda n: b[n][:m * shapes[n][0][0]].view(m, shapes[n][0][0])
+        heads = lambda n: b[n][:m * qd].view(c.n_q_heads, m, c.head_dim)
+        out = {n: rows(n) for n in shapes if n not in ("qh", "o")}
+        out.update(qh=heads("qh"), o=heads("o"))
+        return out
+
     def prefill(self, tokens: torch.Tensor, p0: int = 0, stream=None) -> None:
-        """A prompt chunk (Sec. 3.4): tokens (int32 [m], device) at positions
-        p0 .. p0 + m - 1 through every layer with the prefill GEMMs and
-        causal attention; writes those cache rows, the last token's logits
-        and the greedy next token into self.token."""
+        """A prompt chunk (Sec. 3.4): tokens (int32 [m], device, 1 <= m <=
+        max_chunk) at positions p0 .. p0 + m - 1 through every layer with the
+        prefill GEMMs and causal attention; writes those cache rows, the last
+        token's logits and the greedy next token into self.token.  Longer
+        prompts go through in several chunks."""
         c, s = self.cfg, stream
         m = tokens.numel()
-        x = B.qdec_embed_rows(self.emb, tokens, stream=s)                 # fp32 [m][H] residual stream
+        if not 1 <= m <= self.max_chunk:
+            raise ValueError(f"prefill chunk of {m} tokens: must be 1 .. max_chunk={self.max_chunk}")
+        b = self._chunk_buffers(m)
+        x = B.qdec_embed_rows(self.emb, tokens, out=b["x"], stream=s)     # fp32 [m][H] residual stream
         y = None
         for li, ly in enumerate(self.layers):
-            h = B.qdec_rmsnorm(x, ly.attn_norm, c.eps, residual=y, stream=s)
-            q, k, v = B.qmatmul_gemm_grouped([ly.wq, ly.wk, ly.wv], h, stream=s)
+            h = B.qdec_rmsnorm(x, ly.attn_norm, c.eps, residual=y, out=b["h"], stream=s)
+            q, k, v = B.qmatmul_gemm_grouped([ly.wq, ly.wk, ly.wv], h, outs=[b["q"], b["k"], b["v"]], stream=s)
             qh = B.qdec_rope_append_rows(q, k, v, p0, c.theta, self.k_cache[li], self.v_cache[li],
-                                         interleaved=self.rope_epi, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps,
-                                         stream=s)
-            o = B.qattn_prefill(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, stream=s)
-            ya = B.qmatmul_gemm(ly.wo, B.qdec_heads_to_rows_f16(o, stream=s), stream=s)
-            h = B.qdec_rmsnorm(x, ly.ffn_norm, c.eps, residual=ya, stream=s)
-            g, u = B.qmatmul_gemm_grouped([ly.wg, ly.wu], h, stream=s)
-            y = B.qmatmul_gemm(ly.wd, B.qdec_swiglu_f16(g, u, stream=s), stream=s)
+                                         interleaved=self.rope_epi, q_out=b["qh"], q_norm=ly.q_norm,
+                                         k_norm=ly.k_norm, eps=c.eps, stream=s)
+            o = B.qattn_prefill(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, out=b["o"], stream=s)
+            ya = B.qmatmul_gemm(ly.wo, B.qdec_heads_to_rows_f16(o, out=b["o16"], stream=s), out=b["ya"], stream=s)
+            h = B.qdec_rmsnorm(x, ly.ffn_norm, c.eps, residual=ya, out=b["h"], stream=s)
+            g, u = B.qmatmul_gemm_grouped([ly.wg, ly.wu], h, outs=[b["g"], b["u"]], stream=s)
+            y = B.qmatmul_gemm(ly.wd, B.qdec_swiglu_f16(g, u, out=b["sw"], stream=s), out=b["y"], stream=s)
         B.qdec_rmsnorm(x[m - 1], self.norm, c.eps, residual=y[m - 1], out=self.h, stream=s)
         B.qmatmul_gemv(self.lm_head, self.h, out=self.logits, stream=s)
         B.qdec_argmax(self.logits, out=self.token, workspace=self.argmax_ws, stream=s)

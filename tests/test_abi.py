@@ -108,14 +108,15 @@ def test_gemm_and_moe_validation():
     d = _fake_weight(batch=8, n=64, k=96)
     bad = _fake_weight(batch=8, n=64, k=64)
     ws = ctypes.c_void_p(0x60000)
-    args = lambda wg, wu, wd, nbytes: L.qmoe_grouped_gemm(
-        ctypes.byref(wg), ctypes.byref(wu), ctypes.byref(wd), x, 16, 2, p, p, p, p, y, ws, nbytes, None)
+    args = lambda wg, wu, wd, nbytes, ids=p: L.qmoe_grouped_gemm(
+        ctypes.byref(wg), ctypes.byref(wu), ctypes.byref(wd), x, 16, 2, ids, p, p, p, p, y, ws, nbytes, None)
     need = B.qmoe_workspace_bytes(16, 8, 2, 64, 96)
     assert need == 16 * 2 * 96 * 2 + 16 * 2 * 64 * 2              # h and per-assignment outputs, fp16
     assert args(g, g, bad, need) == 2                                  # down shape mismatch
     assert args(g, g, d, need - 1) == 6                                # workspace too small
     g8 = _fake_weight(fmt=2, batch=8, n=96, k=64)
     assert args(g8, g, d, need) == 4                                   # experts must be Q4
+    assert args(g, g, d, need, ids=None) == 1                          # topk_ids required
 
 
 def test_quantise_repack_validation():
@@ -345,19 +346,6 @@ def test_fused_rmsnorm_gemv_validation():
     sw = lambda h=p, xo=ctypes.c_void_p(0x90000): L.qmatmul_gemv_swiglu_rmsnorm_f16(
         ctypes.byref(w.c()), ctypes.byref(w.c()), p, None, p, 1e-6, xo, h, None)
     assert sw(h=None) == 1 and sw(h=ctypes.c_void_p(0x50001)) == 3 and sw(xo=p) == 1
-    assert B.qm_last_error()
-
-
-def test_attention_rope_fused_validation():
-    L = B.lib()
-    p = ctypes.c_void_p(0x50000)
-    need = B.qattn_decode_workspace_bytes(16, 128)
-    call = lambda d=128, pos=10, mx=64, theta=1e6, kc=p, o=p, nb=need: L.qattn_decode_rope_f16(
-        p, p, p, 16, 8, d, pos, mx, theta, 0.1, kc, p, o, p, nb, None)
-    assert call(d=96) == 2 and call(pos=64) == 2 and call(pos=-1) == 2 and call(mx=300000) == 2
-    assert call(theta=0.5) == 1 and call(o=None) == 1
-    assert call(kc=ctypes.c_void_p(0x50004)) == 3 and call(o=ctypes.c_void_p(0x50001)) == 3
-    assert call(nb=need - 1) == 6
     assert B.qm_last_error()
 
 

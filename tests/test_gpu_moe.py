@@ -111,36 +111,94 @@ def test_moe_all_tokens_to_eight_experts_and_determinism():
     assert rel_err(y1.cpu().numpy(), ref) <= MFMA_TOL
 
 
-@pytest.mark.parametrize("m", workloads.QWEN3_30B_A3B_MOE["m_sweep"])
-def test_moe_full_size_sampled_tokens(m):
-    """Qwen3-30B-A3B MoE layer at full size: routing of all m tokens is
-    bit-exact; the outputs of sampled tokens match the oracle (each token's
-    output depends only on its own experts)."""
+@pytest.fixture(scope="module")
+def full_size_experts():
+    """The Qwen3-30B-A3B experts (128 x gate/up 2048 -> 768, down 768 ->
+    2048, Q4) on the device, and the oracle's dequantised copies of the same
+    seeded weights (quantised, packed and dequantised by the oracle, one
+    thread per expert matrix)."""
+    import concurrent.futures as cf
     cfg = workloads.QWEN3_30B_A3B_MOE
-    e, k, hidden, inter = cfg["experts"], cfg["top_k"], cfg["hidden"], cfg["inter"]
-    gw = inputs.weights_dev(inputs.seed_for(4, 0, "gate"), (e, inter, hidden))
-    uw = inputs.weights_dev(inputs.seed_for(4, 0, "up"), (e, inter, hidden))
-    dw = inputs.weights_dev(inputs.seed_for(4, 0, "down"), (e, hidden, inter))
-    dev = lambda w: B.qm_repack(B.qm_quantise(w, B.Q4_G32), B.LAYOUT_DEVICE)
-    wg, wu, wd = dev(gw), dev(uw), dev(dw)
+    e, hidden, inter = cfg["experts"], cfg["hidden"], cfg["inter"]
+    raw = [inputs.weights_dev(inputs.seed_for(4, 0, t), sh) for t, sh in
+           (("gate", (e, inter, hidden)), ("up", (e, inter, hidden)), ("down", (e, hidden, inter)))]
+    dev = [B.qm_repack(B.qm_quantise(w, B.Q4_G32), B.LAYOUT_DEVICE) for w in raw]
+    host = [w.cpu().numpy() for w in raw]
+    del raw
+
+    def deq(w):
+        q, sc = O.quantise(w, O.Q4)
+        return O.dequantise(O.pack(q, O.Q4), sc, O.Q4)
+    with cf.ThreadPoolExecutor(16) as ex:
+        ora = [list(ex.map(deq, list(h))) for h in host]
+    return dev, ora
+
+
+def _full_size_tokens(m, ids, rng):
+    """All tokens for m <= 128; else 128 or more tokens that hit, in each of
+    the three largest experts' buckets, the first, middle and last row of
+    every 16-row block (so every row tile of every tile plan), topped up with
+    random tokens."""
+    if m <= 128:
+        return np.arange(m)
+    k = ids.shape[1]
+    _, _, sorted_assign = O.moe_bucket(ids, int(ids.max()) + 1)
+    counts = np.bincount(ids.ravel())
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    pick = set()
+    for ex in np.argsort(-counts, kind="stable")[:3]:
+        bucket = sorted_assign[offsets[ex]:offsets[ex + 1]]
+        for b0 in range(0, len(bucket), 16):
+            blk = bucket[b0:b0 + 16]
+            pick.update(int(a) // k for a in (blk[0], blk[len(blk) // 2], blk[-1]))
+    rest = np.setdiff1d(np.arange(m), np.array(sorted(pick)))
+    need = max(0, 128 - len(pick))
+    pick.update(int(t) for t in rng.choice(rest, size=need, replace=False))
+    return np.array(sorted(pick))
+
+
+@pytest.mark.parametrize("m", workloads.QWEN3_30B_A3B_MOE["m_sweep"])
+def test_moe_full_size_sampled_tokens(m, full_size_experts):
+    """Qwen3-30B-A3B MoE layer at full size: routing of all m tokens is
+    bit-exact; the output rows of all tokens (m = 128) or of at least 128
+    tokens that cover every row tile of the three largest buckets match the
+    oracle row by row (each token's output depends only on its own
+    experts)."""
+    cfg = workloads.QWEN3_30B_A3B_MOE
+    e, k, hidden = cfg["experts"], cfg["top_k"], cfg["hidden"]
+    (wg, wu, wd), ora = full_size_experts
     x = inputs.activations_dev(inputs.seed_for(4, m, "x"), (m, hidden))
     logits = inputs.logits_dev(inputs.seed_for(4, m, "logits"), (m, e))
-    r = _route_check(logits.cpu().numpy(), k)
+    lg = logits.cpu().numpy()
+    r = _route_check(lg, k)
     y = B.qmoe_grouped_gemm(wg, wu, wd, x, r).cpu().numpy()
-    toks = np.array([0, m // 3, m - 1])
-    lg = logits.cpu().numpy()[toks]
-    ids, _ = O.moe_route(lg, k)
-    used = np.unique(ids)
-    remap = {int(ex): i for i, ex in enumerate(used)}
-    sub = lambda w: w[torch.from_numpy(used).cuda()].cpu().numpy()
-    ora = []
-    for w in (sub(gw), sub(uw), sub(dw)):
-        qs = [O.quantise(w[i], O.Q4) for i in range(len(used))]
-        ora += [np.stack([O.pack(q, O.Q4) for q, _ in qs]), np.stack([s for _, s in qs])]
-    # the oracle layer over just the experts these tokens use: logits of the
-    # other experts are dropped, which leaves each token's top-k unchanged
-    lg_sub = lg[:, used]
-    ref, ids_sub, *_ = O.moe_layer(x.cpu().numpy()[toks], lg_sub, k, *ora)
-    assert np.array_equal(used[ids_sub], ids)
-    assert all(remap[int(a)] == b for a, b in zip(ids.ravel(), ids_sub.ravel()))
-    assert rel_err(y[toks], ref) <= MFMA_TOL
+    ids_all, _ = O.moe_route(lg, k)
+    toks = _full_size_tokens(m, ids_all, np.random.default_rng(m))
+    assert len(toks) >= min(m, 128)
+    ref, ids, *_ = O.moe_layer_dequantised(x.cpu().numpy()[toks], lg[toks], k, e,
+                                           lambda ex: (ora[0][ex], ora[1][ex], ora[2][ex]))
+    assert np.array_equal(ids, ids_all[toks])
+    got = y[toks]
+    assert np.all(np.isfinite(got))
+    per_row = np.abs(got - ref).max(axis=1) / np.abs(ref).max(axis=1)
+    assert per_row.max() <= MFMA_TOL, (per_row.max(), toks[int(per_row.argmax())])
+
+
+def test_moe_topk_ids_checked_against_buckets():
+    """An assignment whose bucket is not the expert topk_ids names turns its
+    token's output row into NaN; every other row is unchanged."""
+    m, e, k, hidden, inter = 48, 16, 4, 128, 96
+    (wg, wu, wd), _ = _experts(4242, e, hidden, inter)
+    x = torch.from_numpy(inputs.activations_np(inputs.seed_for(4, m, "x"), (m, hidden))).cuda()
+    logits = inputs.logits_np(inputs.seed_for(4, m, "logits"), (m, e))
+    r = _route_check(logits, k)
+    y0 = B.qmoe_grouped_gemm(wg, wu, wd, x, r)
+    bad = 17                                   # token 17, slot 2: claim another expert
+    ids = r.ids.clone()
+    ids[bad, 2] = (ids[bad, 2] + 1) % e
+    r2 = B.Routing(ids, r.gates, r.counts, r.offsets, r.sorted_assign, r.top_k)
+    y1 = B.qmoe_grouped_gemm(wg, wu, wd, x, r2)
+    nan_rows = torch.isnan(y1).any(dim=1).cpu().numpy()
+    assert nan_rows[bad] and nan_rows.sum() == 1
+    keep = torch.ones(m, dtype=torch.bool); keep[bad] = False
+    assert torch.equal(y0[keep.cuda()], y1[keep.cuda()])
