@@ -470,6 +470,24 @@ qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up,
                             const int32_t* sorted_assign, float* y, void* workspace,
                             size_t ws_bytes, void* stream);
 
+/* qmoe_grouped_gemm for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * kernels and results, with h and the per-assignment outputs in a scratch
+ * array the library holds in device memory (QMOE_NOALLOC_SCRATCH_BYTES per
+ * device, kept by every device the library runs on until the process ends)
+ * instead of a caller workspace.  Allocates nothing and calls no allocating
+ * routine.  Arguments as qmoe_grouped_gemm; QM_EWORKSPACE when the layer
+ * needs more than QMOE_NOALLOC_SCRATCH_BYTES (qmoe_workspace_bytes tells:
+ * e.g. up to 744 tokens at top-8, hidden 2048, inter 768).  Every call on a
+ * device uses the same scratch: calls that overlap on one device (other
+ * streams, other threads) race; order them on one stream. */
+#define QMOE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+qm_status qmoe_grouped_gemm_noalloc(const qm_qweight* w_gate, const qm_qweight* w_up,
+                                    const qm_qweight* w_down, const uint16_t* x, int64_t m,
+                                    int32_t top_k, const int32_t* topk_ids, const float* topk_w,
+                                    const int32_t* counts, const int32_t* offsets,
+                                    const int32_t* sorted_assign, float* y, void* stream);
+
 /* Writes a one-line description of the per-chip launch table chosen for the
  * current device into buf (Sec. 3.3: kernel geometry from a per-chip
  * configuration): arch, CU count, the Q4 GEMV kernel (name with template

@@ -28,7 +28,7 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmatmul_gemv", "qmatmul_gemv_swiglu", "qmatmul_gemv_grouped", "qmatmul_gemm",
            "qmatmul_gemm_grouped",
            "qmoe_workspace_bytes", "qmoe_route",
-           "qmoe_grouped_gemm", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
+           "qmoe_grouped_gemm", "qmoe_grouped_gemm_noalloc", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
            "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
            "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
            "qmatmul_gemv_swiglu_rmsnorm_f16", "qdec_rope_table",
@@ -75,6 +75,7 @@ def lib() -> ctypes.CDLL:
             "qmoe_workspace_bytes": [i64, i32, i32, i64, i64, ctypes.POINTER(sz)],
             "qmoe_route": [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp],
             "qmoe_grouped_gemm": [W, W, W, vp, i64, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+            "qmoe_grouped_gemm_noalloc": [W, W, W, vp, i64, i32, vp, vp, vp, vp, vp, vp, vp],
             "qm_device_config": [ctypes.c_char_p, sz],
             "qattn_decode_workspace_bytes": [i32, i32, ctypes.POINTER(sz)],
             "qattn_decode": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
@@ -554,6 +555,25 @@ def qmoe_grouped_gemm(w_gate: QWeight, w_up: QWeight, w_down: QWeight, x: torch.
                                    _ptr(x), m, r.top_k, _ptr(r.ids), _ptr(r.gates), _ptr(r.counts), _ptr(r.offsets),
                                    _ptr(r.sorted_assign), _ptr(out), _ptr(workspace), workspace.numel(),
                                    _stream(stream)))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20     # QMOE_NOALLOC_SCRATCH_BYTES
+
+
+def qmoe_grouped_gemm_noalloc(w_gate: QWeight, w_up: QWeight, w_down: QWeight, x: torch.Tensor, r: Routing,
+                              out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """qmoe_grouped_gemm with the library's per-device scratch instead of a
+    caller workspace (the C call allocates nothing; `out` is allocated here
+    only when not given)."""
+    m, hidden = x.shape
+    assert x.dtype == torch.float16 and x.is_contiguous()
+    if out is None:
+        out = torch.empty((m, hidden), dtype=torch.float32, device=x.device)
+    _check(lib().qmoe_grouped_gemm_noalloc(ctypes.byref(w_gate.c()), ctypes.byref(w_up.c()),
+                                           ctypes.byref(w_down.c()), _ptr(x), m, r.top_k, _ptr(r.ids),
+                                           _ptr(r.gates), _ptr(r.counts), _ptr(r.offsets), _ptr(r.sorted_assign),
+                                           _ptr(out), _stream(stream)))
     return out
 
 

@@ -701,39 +701,58 @@ qm_status qmoe_route(const float* logits, int64_t m, int32_t n_experts, int32_t 
                   "qmoe_route");
 }
 
-qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up, const qm_qweight* w_down,
-                            const uint16_t* x, int64_t m, int32_t top_k, const int32_t* topk_ids, const float* topk_w,
-                            const int32_t* counts, const int32_t* offsets,
-                            const int32_t* sorted_assign, float* y, void* workspace, size_t ws_bytes,
-                            void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared body of the two MoE layer entry points: validation first (nothing
+// enqueued on error), then the workspace (the caller's, or the library's
+// per-device scratch when noalloc), then the launches.
+qm_status moe_layer_call(const char* name, const qm_qweight* w_gate, const qm_qweight* w_up,
+                         const qm_qweight* w_down, const uint16_t* x, int64_t m, int32_t top_k,
+                         const int32_t* topk_ids, const float* topk_w, const int32_t* counts,
+                         const int32_t* offsets, const int32_t* sorted_assign, float* y, void* workspace,
+                         size_t ws_bytes, bool noalloc, void* stream) {
   qm_status st;
-  if ((st = check_weight(w_gate, "qmoe_grouped_gemm(w_gate)")) != QM_OK) return st;
-  if ((st = check_weight(w_up, "qmoe_grouped_gemm(w_up)")) != QM_OK) return st;
-  if ((st = check_weight(w_down, "qmoe_grouped_gemm(w_down)")) != QM_OK) return st;
+  if ((st = check_weight(w_gate, name)) != QM_OK) return st;
+  if ((st = check_weight(w_up, name)) != QM_OK) return st;
+  if ((st = check_weight(w_down, name)) != QM_OK) return st;
   const qm_qweight* ws[3] = {w_gate, w_up, w_down};
   for (const qm_qweight* w : ws) {
-    if (w->format != QM_Q4_G32) return fail(QM_EFORMAT, "qmoe_grouped_gemm: experts must be Q4");
-    if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "qmoe_grouped_gemm: experts must be in DEVICE layout");
+    if (w->format != QM_Q4_G32) return fail(QM_EFORMAT, "%s: experts must be Q4", name);
+    if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "%s: experts must be in DEVICE layout", name);
   }
   const int64_t E = w_gate->batch, inter = w_gate->n, hidden = w_gate->k;
   if (w_up->batch != E || w_up->n != inter || w_up->k != hidden || w_down->batch != E ||
       w_down->n != hidden || w_down->k != inter)
-    return fail(QM_ESHAPE, "qmoe_grouped_gemm: expert shapes disagree (gate/up [E][inter][hidden], down [E][hidden][inter])");
-  if (E > 1024) return fail(QM_ESHAPE, "qmoe_grouped_gemm: at most 1024 experts");
-  if (inter == 0 || hidden == 0) return fail(QM_ESHAPE, "qmoe_grouped_gemm: empty expert matrices");
+    return fail(QM_ESHAPE, "%s: expert shapes disagree (gate/up [E][inter][hidden], down [E][hidden][inter])",
+                name);
+  if (E > 1024) return fail(QM_ESHAPE, "%s: at most 1024 experts", name);
+  if (inter == 0 || hidden == 0) return fail(QM_ESHAPE, "%s: empty expert matrices", name);
   if (top_k < 1 || top_k > 16 || top_k > E)
-    return fail(QM_ESHAPE, "qmoe_grouped_gemm: top_k=%d must be in [1, min(16, E)]", top_k);
-  if (m < 0 || m > 65536) return fail(QM_ESHAPE, "qmoe_grouped_gemm: m must be in [0, 65536]");
+    return fail(QM_ESHAPE, "%s: top_k=%d must be in [1, min(16, E)]", name, top_k);
+  if (m < 0 || m > 65536) return fail(QM_ESHAPE, "%s: m must be in [0, 65536]", name);
   if (m == 0) return QM_OK;
   if (!x || !topk_ids || !topk_w || !counts || !offsets || !sorted_assign || !y)
-    return fail(QM_EINVAL, "qmoe_grouped_gemm: null pointer");
-  if (!aligned16(x) || !aligned16(y)) return fail(QM_EALIGN, "qmoe_grouped_gemm: x and y must be 16-byte aligned");
+    return fail(QM_EINVAL, "%s: null pointer", name);
+  if (!aligned16(x) || !aligned16(y)) return fail(QM_EALIGN, "%s: x and y must be 16-byte aligned", name);
   const size_t need = moe_workspace_bytes(m, top_k, hidden, inter);
-  if (!workspace || ws_bytes < need)
-    return fail(QM_EWORKSPACE, "qmoe_grouped_gemm: workspace of %zu bytes needed, %zu given", need, ws_bytes);
-  if (!aligned16(workspace)) return fail(QM_EALIGN, "qmoe_grouped_gemm: workspace must be 16-byte aligned");
+  if (noalloc) {
+    if (need > kMoeScratchBytes)
+      return fail(QM_EWORKSPACE, "%s: this layer needs %zu bytes of scratch, more than the %zu the library "
+                  "holds per device; use qmoe_grouped_gemm with a workspace or a smaller m", name, need,
+                  kMoeScratchBytes);
+  } else {
+    if (!workspace || ws_bytes < need)
+      return fail(QM_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", name, need, ws_bytes);
+    if (!aligned16(workspace)) return fail(QM_EALIGN, "%s: workspace must be 16-byte aligned", name);
+  }
   const DeviceInfo* d;
   if ((st = device_info(&d)) != QM_OK) return st;
+  if (noalloc) {
+    const hipError_t e = moe_scratch(&workspace);
+    if (e != hipSuccess) return fail(QM_EDEVICE, "%s: scratch lookup failed: %s", name, hipGetErrorString(e));
+  }
   MoeArgs a;
   a.gq = static_cast<const uint8_t*>(w_gate->qdata); a.gs = w_gate->scales;
   a.uq = static_cast<const uint8_t*>(w_up->qdata); a.us = w_up->scales;
@@ -746,7 +765,27 @@ qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up, co
   a.yp = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + h_bytes);
   a.m = m; a.hidden = hidden; a.inter = inter;
   a.n_experts = static_cast<int32_t>(E); a.top_k = top_k;
-  return launched(launch_moe(a, d->cu_count, static_cast<hipStream_t>(stream)), "qmoe_grouped_gemm");
+  return launched(launch_moe(a, d->cu_count, static_cast<hipStream_t>(stream)), name);
+}
+
+}  // namespace
+
+extern "C" {
+
+qm_status qmoe_grouped_gemm(const qm_qweight* w_gate, const qm_qweight* w_up, const qm_qweight* w_down,
+                            const uint16_t* x, int64_t m, int32_t top_k, const int32_t* topk_ids, const float* topk_w,
+                            const int32_t* counts, const int32_t* offsets, const int32_t* sorted_assign, float* y,
+                            void* workspace, size_t ws_bytes, void* stream) {
+  return moe_layer_call("qmoe_grouped_gemm", w_gate, w_up, w_down, x, m, top_k, topk_ids, topk_w, counts, offsets,
+                        sorted_assign, y, workspace, ws_bytes, false, stream);
+}
+
+qm_status qmoe_grouped_gemm_noalloc(const qm_qweight* w_gate, const qm_qweight* w_up, const qm_qweight* w_down,
+                                    const uint16_t* x, int64_t m, int32_t top_k, const int32_t* topk_ids,
+                                    const float* topk_w, const int32_t* counts, const int32_t* offsets,
+                                    const int32_t* sorted_assign, float* y, void* stream) {
+  return moe_layer_call("qmoe_grouped_gemm_noalloc", w_gate, w_up, w_down, x, m, top_k, topk_ids, topk_w, counts,
+                        offsets, sorted_assign, y, nullptr, 0, true, stream);
 }
 
 qm_status qm_device_config(char* buf, size_t len) {

@@ -14,6 +14,7 @@
 #include <cstdlib>
 #include <algorithm>
 #include <array>
+#include <mutex>
 #include <utility>
 
 #include "qgemm.h"
@@ -322,6 +323,37 @@ hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
 }
 
 }  // namespace
+
+// Scratch of the allocation-free MoE entry point: h and the per-assignment
+// outputs of one call, kMoeScratchBytes per device, held by every device the
+// library runs on until the process ends.  In host code `scratch` names a
+// host-side stand-in, never the device memory: its device address is looked
+// up once per device (hipGetSymbolAddress, with that device current) and
+// only that address is handed to kernels.  Every call on a device shares the
+// same bytes, so calls that overlap on one device race.
+static __device__ __align__(256) uint8_t scratch[kMoeScratchBytes];
+
+namespace {
+constexpr int kScratchDevices = 64;
+void* g_scratch_ptr[kScratchDevices];
+hipError_t g_scratch_status[kScratchDevices];
+std::once_flag g_scratch_once[kScratchDevices];
+}  // namespace
+
+hipError_t moe_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  std::call_once(g_scratch_once[dev], [dev]() {
+    void* p = nullptr;
+    g_scratch_status[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = g_scratch_status[dev] == hipSuccess ? p : nullptr;
+  });
+  if (g_scratch_status[dev] != hipSuccess) return g_scratch_status[dev];
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 size_t moe_workspace_bytes(int64_t m, int32_t top_k, int64_t hidden, int64_t inter) {
   const size_t A = static_cast<size_t>(m) * top_k;

@@ -216,6 +216,10 @@ struct MoeArgs {
   int32_t n_experts, top_k;
 };
 size_t moe_workspace_bytes(int64_t m, int32_t top_k, int64_t hidden, int64_t inter);
+// Bytes of the per-device scratch of qmoe_grouped_gemm_noalloc, and its
+// device address on the current device (looked up once per device).
+constexpr size_t kMoeScratchBytes = QMOE_NOALLOC_SCRATCH_BYTES;
+hipError_t moe_scratch(void** ptr);
 hipError_t launch_moe(const MoeArgs& a, int cu_count, hipStream_t st);
 hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, int32_t* ids,
                         float* w, int32_t* counts, int32_t* offsets, int32_t* sorted_assign,

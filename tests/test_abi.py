@@ -117,6 +117,17 @@ def test_gemm_and_moe_validation():
     g8 = _fake_weight(fmt=2, batch=8, n=96, k=64)
     assert args(g8, g, d, need) == 4                                   # experts must be Q4
     assert args(g, g, d, need, ids=None) == 1                          # topk_ids required
+    # the allocation-free variant: sizes beyond the library's scratch are
+    # refused before anything touches the device
+    na = lambda wg, wu, wd, m, ids=p: L.qmoe_grouped_gemm_noalloc(
+        ctypes.byref(wg), ctypes.byref(wu), ctypes.byref(wd), x, m, 8, ids, p, p, p, p, y, None)
+    g2 = _fake_weight(batch=16, n=768, k=2048)
+    d2 = _fake_weight(batch=16, n=2048, k=768)
+    assert B.qmoe_workspace_bytes(744, 16, 8, 2048, 768) <= B.NOALLOC_SCRATCH_BYTES
+    assert B.qmoe_workspace_bytes(745, 16, 8, 2048, 768) > B.NOALLOC_SCRATCH_BYTES
+    assert na(g2, g2, d2, 745) == 6 and "scratch" in B.qm_last_error()
+    assert na(g2, g2, d2, 744, ids=None) == 1
+    assert na(g2, g2, bad, 16) == 2
 
 
 def test_quantise_repack_validation():
