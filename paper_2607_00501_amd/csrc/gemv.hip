@@ -145,6 +145,102 @@ __device__ __forceinline__ float dot_q8_half(const uint4 w, const uint32_t* xs) 
   return acc;
 }
 
+// ---- Activations by lane broadcast (Q4 / Q8 sub-panel rows of 16 or 32).
+// Lane l of a 16-lane row holds activation dword l (the fp16 pair
+// x[2l], x[2l + 1]) of the group its row of lanes is working on; the dot
+// product of pair i takes it from lane i with the DPP row_newbcast:i form of
+// v_dot2c_f32_f16, so a chunk needs one 4-byte activation load per lane
+// instead of 64 bytes of LDS reads.
+//
+// The 16 fp16 weight pairs of one chunk, in activation-dword order (pair i
+// multiplies dword i).  Q4: (d & 0x000F000F) | 0x6400_6400 is the pair
+// (1024 + u) for k even / odd; the nibbles at bits 4-7 give 1024 + 16u, so
+// pairs with i % 4 in {1, 3} carry 16q (scaled by 1/16 after the sum).
+template <class DC>
+__device__ __forceinline__ void q4_pairs(const uint32_t* w, uint32_t* qv, const DC& k) {
+  const half2v b1 = {(_Float16)1032.0f, (_Float16)1032.0f};
+  const half2v b16 = {(_Float16)1152.0f, (_Float16)1152.0f};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t d = w[j], d8 = d >> 8;
+    qv[4 * j + 0] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, and_or(d, k.m0, k.magic)) - b1);
+    qv[4 * j + 1] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, and_or(d, k.m1, k.magic)) - b16);
+    qv[4 * j + 2] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, and_or(d8, k.m0, k.magic)) - b1);
+    qv[4 * j + 3] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, and_or(d8, k.m1, k.magic)) - b16);
+  }
+}
+// Q8: bytes of half h, pairs (0,1), (2,2+1) of dword j -> activation dwords
+// 8h + 2j, 8h + 2j + 1.
+__device__ __forceinline__ void q8_pairs(const uint32_t* w, uint32_t* qv) {
+  const half2v bias = {(_Float16)1152.0f, (_Float16)1152.0f};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t lo = __builtin_amdgcn_perm(0x64646464u, w[j], 0x04010400u);
+    const uint32_t hi = __builtin_amdgcn_perm(0x64646464u, w[j], 0x04030402u);
+    qv[2 * j] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, lo) - bias);
+    qv[2 * j + 1] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, hi) - bias);
+  }
+}
+// a[i % 4] += dot(pair i of the lane's own qv, activation dword i of its
+// row of lanes), i = 0..15.  Hand-written because the compiler does not form
+// the DPP variant of v_dot2c itself (it emits a separate v_mov_b32_dpp per
+// pair).  The four accumulators put four instructions between writes of one
+// register; s_nop 1 before the block covers a VALU write of xd feeding DPP,
+// and s_nop 4 after it covers a VALU read of the last results (measured on
+// gfx950: with the compiler's single wait state there the final sums were
+// read stale).
+__device__ __forceinline__ void dpp_dot16(uint32_t xd, const uint32_t* qv, float* a) {
+  asm("s_nop 1\n\t"
+      "v_dot2c_f32_f16_dpp %0, %4, %5 row_newbcast:0 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %1, %4, %6 row_newbcast:1 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %2, %4, %7 row_newbcast:2 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %3, %4, %8 row_newbcast:3 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %0, %4, %9 row_newbcast:4 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %1, %4, %10 row_newbcast:5 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %2, %4, %11 row_newbcast:6 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %3, %4, %12 row_newbcast:7 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %0, %4, %13 row_newbcast:8 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %1, %4, %14 row_newbcast:9 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %2, %4, %15 row_newbcast:10 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %3, %4, %16 row_newbcast:11 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %0, %4, %17 row_newbcast:12 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %1, %4, %18 row_newbcast:13 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %2, %4, %19 row_newbcast:14 row_mask:0xf bank_mask:0xf\n\t"
+      "v_dot2c_f32_f16_dpp %3, %4, %20 row_newbcast:15 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 4"
+      : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3])
+      : "v"(xd), "v"(qv[0]), "v"(qv[1]), "v"(qv[2]), "v"(qv[3]), "v"(qv[4]), "v"(qv[5]), "v"(qv[6]), "v"(qv[7]),
+        "v"(qv[8]), "v"(qv[9]), "v"(qv[10]), "v"(qv[11]), "v"(qv[12]), "v"(qv[13]), "v"(qv[14]), "v"(qv[15]));
+}
+// One chunk's sum of q * x (before the group scale) with the activations by
+// lane broadcast.
+template <int FMT, class DC>
+__device__ __forceinline__ float dot_chunk_bcast(const uint32_t* w, uint32_t xd, const DC& k) {
+  uint32_t qv[16];
+  float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if constexpr (FMT == QM_Q4_G32) {
+    q4_pairs(w, qv, k);
+    dpp_dot16(xd, qv, a);
+    return fmaf(a[1] + a[3], 0.0625f, a[0] + a[2]);
+  } else {
+    q8_pairs(w, qv);
+    dpp_dot16(xd, qv, a);
+    return (a[0] + a[1]) + (a[2] + a[3]);
+  }
+}
+
+// Sum of v over the lanes l, l ^ 16, l ^ 32, l ^ 48 (from = 16) or l, l ^ 32
+// (from = 32), by lane swaps (no LDS); every lane gets the same bits.
+template <int FROM>
+__device__ __forceinline__ float lane_sum_from(float v) {
+  if constexpr (FROM <= 16) {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  }
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
 // Shift left by SH (right for negative SH); SH is a constant after unrolling.
 __device__ __forceinline__ uint32_t shift_by(uint32_t v, int sh) { return sh >= 0 ? v << sh : v >> -sh; }
 
@@ -386,6 +482,9 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_kernel(const uint8_t* __restr
 // lanes, then a fixed-order sum over wavefronts in LDS.
 // Chunks per lane per pass: 8 (F16/BF16: 4, 64 B each).
 template <int FMT> constexpr int kSubU = fmt_float(FMT) ? 4 : 8;
+// Q4 and Q8 sub-panel workgroups of 16 or 32 rows take their activations by
+// lane broadcast (a row of 16 lanes works on one group).
+constexpr bool sub_bcast(int fmt, int subr) { return (fmt == QM_Q4_G32 || fmt == QM_Q8_G32) && subr >= 16; }
 
 // One workgroup's share of one matrix: `block` of `nblocks` = N/SUBR.
 // SWIGLU: the same rows of a second matrix (q2, s2) go through the same
@@ -475,7 +574,8 @@ __device__ __forceinline__ void qkv_rope_store(const QkvRopeEpi& e, int role, in
     e.kc[(head * e.max_len + e.pos) * d + dd] = h(r);
 }
 
-template <int FMT, int SUBR, int WAVES, bool XLDS, bool SWIGLU = false, bool NORM = false, bool QKV_ROPE = false>
+template <int FMT, int SUBR, int WAVES, bool XLDS, bool SWIGLU = false, bool NORM = false, bool QKV_ROPE = false,
+          int UP = 0>
 __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s,
                                               const uint8_t* __restrict__ q2, const uint16_t* __restrict__ s2,
                                               const uint16_t* __restrict__ x, float* __restrict__ y, int n_rows,
@@ -486,7 +586,7 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
   static_assert(!QKV_ROPE || WAVES > 1, "the q/k/v epilogue runs in the multi-wavefront store");
   constexpr int CL = 64 / SUBR;
   constexpr int NM = SWIGLU ? 2 : 1;                  // matrices
-  constexpr int U = kSubU<FMT>;
+  constexpr int U = UP > 0 ? UP : kSubU<FMT>;       // chunks per lane per pass
   extern __shared__ uint4 xs[];                       // groups * 4 uint4 (K halves) if XLDS
   __shared__ float part[NM][WAVES][SUBR];
   const int lane = threadIdx.x & 63;
@@ -504,63 +604,106 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
   const int iters = (groups + U * stride - 1) / (U * stride);
   const DequantConsts<FMT> dk;
   const uint4* xg = reinterpret_cast<const uint4*>(x);
+  // Q4 / Q8 with rows of 16 or 32: activations by lane broadcast, one dword
+  // per lane and chunk, from global memory (or from the normed copy in LDS).
+  constexpr bool kBcast = sub_bcast(FMT, SUBR);
+  const uint32_t* xg32 = reinterpret_cast<const uint32_t*>(x);
+  // With x staged in LDS (and no fused norm, no broadcast), one extra
+  // wavefront, number WAVES, is the producer of the LDS copy; wavefronts
+  // 0 .. WAVES-1 stream the weights.
+  constexpr bool kProducer = XLDS && !NORM && !kBcast;
 
   float acc[NM];
 #pragma unroll
   for (int m = 0; m < NM; ++m) acc[m] = 0.0f;
-  for (int it = 0; it < iters; ++it) {
-    uint32_t wv[U][NM][kWords<FMT>];
-    uint32_t sv[U][NM];
+  uint32_t wv[U][NM][kWords<FMT>];
+  uint32_t sv[U][NM];
+  uint32_t xdv[U];                                     // kBcast: the lane's activation dword per chunk
+  // Every lane issues all U chunk loads of a pass (chunks past the end of
+  // its range re-read the range's last chunk and are discarded by a select):
+  // no lane branches between a load and its use, so each dot product waits
+  // only for its own chunk's load.
+  auto issue = [&](int it) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int c = first + (it * U + u) * stride;
-      if (c < groups) {
-        const int64_t ch = ch0 + c;
+      const int c = min(first + (it * U + u) * stride, groups - 1);
+      const int64_t ch = ch0 + c;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const uint8_t* qm = m == 0 ? q : q2;
+        const uint16_t* sm = m == 0 ? s : s2;
+        load_chunk<FMT, kBcast>(qm + ch * chunk_block_bytes(FMT), row, wv[u][m]);
+        if constexpr (!fmt_float(FMT)) sv[u][m] = sm[ch * 64 + row];
+        else sv[u][m] = 0;
+      }
+      if constexpr (kBcast && !NORM) xdv[u] = xg32[c * 16 + (lane & 15)];
+    }
+  };
+  auto consume = [&](int it) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int craw = first + (it * U + u) * stride;
+      const int c = min(craw, groups - 1);
+      if constexpr (kBcast) {
+        const uint32_t xd = NORM ? reinterpret_cast<const uint32_t*>(xs)[c * 16 + (lane & 15)] : xdv[u];
 #pragma unroll
         for (int m = 0; m < NM; ++m) {
-          const uint8_t* qm = m == 0 ? q : q2;
-          const uint16_t* sm = m == 0 ? s : s2;
-          load_chunk<FMT, false>(qm + ch * chunk_block_bytes(FMT), row, wv[u][m]);
-          if constexpr (!fmt_float(FMT)) sv[u][m] = sm[ch * 64 + row];
-          else sv[u][m] = 0;
+          const float t = scaled_add<FMT>(sv[u][m], dot_chunk_bcast<FMT>(wv[u][m], xd, dk), acc[m]);
+          acc[m] = craw < groups ? t : acc[m];
+        }
+      } else {
+        uint32_t xv[16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint4 t = XLDS ? xs[c * 4 + i] : xg[c * 4 + i];
+          xv[4 * i] = t.x; xv[4 * i + 1] = t.y; xv[4 * i + 2] = t.z; xv[4 * i + 3] = t.w;
+        }
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+          const float t = scaled_add<FMT>(sv[u][m], dot_chunk<FMT>(wv[u][m], xv, dk), acc[m]);
+          acc[m] = craw < groups ? t : acc[m];
         }
       }
     }
-    if (XLDS && it == 0) {
-      if constexpr (NORM) {
-        stage_rmsnorm<WAVES>(*na, groups, xs, blockIdx.x == 0);
-      } else {
-        for (int i = threadIdx.x; i < groups * 4; i += WAVES * 64) xs[i] = xg[i];
-      }
+  };
+  if (kProducer && wave == WAVES) {
+    // The producer wavefront copies x into LDS (8 loads in flight per lane,
+    // clamped indices, duplicates write the same value) and joins the
+    // barrier when its writes are complete.
+    const int x4 = groups * 4;
+    for (int base = 0; base < x4; base += 8 * 64) {
+      uint4 t[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) t[j] = xg[min(base + j * 64 + lane, x4 - 1)];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) xs[min(base + j * 64 + lane, x4 - 1)] = t[j];
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  } else {
+    issue(0);
+    if constexpr (kProducer) {
+      // Wait for x in LDS only: these wavefronts have no LDS writes and their
+      // weight loads stay in flight across the (fence-free) barrier.
+      asm volatile("s_barrier" ::: "memory");
+    } else if constexpr (NORM) {
+      stage_rmsnorm<WAVES>(*na, groups, xs, blockIdx.x == 0);
       __syncthreads();
     }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int c = first + (it * U + u) * stride;
-      if (c < groups) {
-        uint32_t xv[16];
-        if (XLDS) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const uint4 t = xs[c * 4 + i];
-            xv[4 * i] = t.x; xv[4 * i + 1] = t.y; xv[4 * i + 2] = t.z; xv[4 * i + 3] = t.w;
-          }
-        } else {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const uint4 t = xg[c * 4 + i];
-            xv[4 * i] = t.x; xv[4 * i + 1] = t.y; xv[4 * i + 2] = t.z; xv[4 * i + 3] = t.w;
-          }
-        }
-#pragma unroll
-        for (int m = 0; m < NM; ++m) acc[m] = scaled_add<FMT>(sv[u][m], dot_chunk<FMT>(wv[u][m], xv, dk), acc[m]);
-      }
+    consume(0);
+    for (int it = 1; it < iters; ++it) {
+      issue(it);
+      consume(it);
     }
   }
 #pragma unroll
-  for (int m = 0; m < NM; ++m)
+  for (int m = 0; m < NM; ++m) {
+    if constexpr (SUBR >= 16) {
+      acc[m] = lane_sum_from<SUBR>(acc[m]);
+    } else {
 #pragma unroll
-    for (int off = SUBR; off < 64; off <<= 1) acc[m] += __shfl_xor(acc[m], off);
+      for (int off = SUBR; off < 64; off <<= 1) acc[m] += __shfl_xor(acc[m], off);
+    }
+  }
   auto out = [&](float a, float b) { return SWIGLU ? a / (1.0f + expf(-a)) * b : a; };
   auto store = [&](int64_t n, float v) {   // y16: fp16 output (round to nearest even) instead of y
     if (y16) {
@@ -571,13 +714,13 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
     }
   };
   if (WAVES == 1) {
-    if (lane < SUBR) {
+    if (lane < SUBR && wave == 0) {              // (wavefront 1, if any, is the producer)
       const int64_t n = panel * 64 + row;
       if (n < n_rows) store(n, out(acc[0], acc[NM - 1]));
     }
     return;
   }
-  if (cl == 0) {
+  if (cl == 0 && wave < WAVES) {                 // the producer wavefront has no partial sums
 #pragma unroll
     for (int m = 0; m < NM; ++m) part[m][wave][r] = acc[m];
   }
@@ -601,20 +744,26 @@ __device__ __forceinline__ void gemv_sub_body(const uint8_t* __restrict__ q, con
   }
 }
 
+// Threads of a sub-panel workgroup: WAVES weight-streaming wavefronts, plus
+// the producer wavefront of the LDS copy of x when x is staged (no fused norm).
 template <int FMT, int SUBR, int WAVES, bool XLDS>
-__global__ __launch_bounds__(WAVES * 64) void gemv_sub_kernel(const uint8_t* __restrict__ q,
+constexpr int kSubThreads = (WAVES + (XLDS && !sub_bcast(FMT, SUBR) ? 1 : 0)) * 64;
+
+template <int FMT, int SUBR, int WAVES, bool XLDS, int U>
+__global__ __launch_bounds__((kSubThreads<FMT, SUBR, WAVES, XLDS>)) void gemv_sub_kernel(const uint8_t* __restrict__ q,
                                                               const uint16_t* __restrict__ s,
                                                               const uint16_t* __restrict__ x,
                                                               float* __restrict__ y, int n_rows,
                                                               int groups) {
   // All kernel arguments in one batch of scalar loads (one round trip).
   asm volatile("" ::"s"(q), "s"(s), "s"(x), "s"(y), "s"(n_rows), "s"(groups));
-  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, nullptr, nullptr, x, y, n_rows, groups, blockIdx.x, gridDim.x);
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS, false, false, false, U>(q, s, nullptr, nullptr, x, y, n_rows, groups,
+                                                                 blockIdx.x, gridDim.x);
 }
 
 // SwiGLU pair: h = silu(Wg' x) * (Wu' x) over the same rows, one launch.
-template <int FMT, int SUBR, int WAVES, bool XLDS>
-__global__ __launch_bounds__(WAVES * 64) void gemv_swiglu_kernel(const uint8_t* __restrict__ qg,
+template <int FMT, int SUBR, int WAVES, bool XLDS, int U>
+__global__ __launch_bounds__((kSubThreads<FMT, SUBR, WAVES, XLDS>)) void gemv_swiglu_kernel(const uint8_t* __restrict__ qg,
                                                                  const uint16_t* __restrict__ sg,
                                                                  const uint8_t* __restrict__ qu,
                                                                  const uint16_t* __restrict__ su,
@@ -622,11 +771,12 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_swiglu_kernel(const uint8_t* 
                                                                  float* __restrict__ h, int n_rows, int groups,
                                                                  uint16_t* __restrict__ h16) {
   asm volatile("" ::"s"(qg), "s"(sg), "s"(qu), "s"(su), "s"(x), "s"(h), "s"(n_rows), "s"(groups), "s"(h16));
-  gemv_sub_body<FMT, SUBR, WAVES, XLDS, true>(qg, sg, qu, su, x, h, n_rows, groups, blockIdx.x, gridDim.x, h16);
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS, true, false, false, U>(qg, sg, qu, su, x, h, n_rows, groups, blockIdx.x,
+                                                                gridDim.x, h16);
 }
 
 // The SwiGLU pair with the RMSNorm of its input folded in.
-template <int FMT, int SUBR>
+template <int FMT, int SUBR, int U>
 __global__ __launch_bounds__(512) void gemv_swiglu_norm_kernel(const uint8_t* __restrict__ qg,
                                                                const uint16_t* __restrict__ sg,
                                                                const uint8_t* __restrict__ qu,
@@ -634,8 +784,8 @@ __global__ __launch_bounds__(512) void gemv_swiglu_norm_kernel(const uint8_t* __
                                                                float* __restrict__ h, uint16_t* __restrict__ h16,
                                                                int n_rows, int groups) {
   asm volatile("" ::"s"(qg), "s"(sg), "s"(qu), "s"(su), "s"(h), "s"(n_rows), "s"(groups), "s"(h16));
-  gemv_sub_body<FMT, SUBR, 8, true, true, true>(qg, sg, qu, su, nullptr, h, n_rows, groups, blockIdx.x, gridDim.x,
-                                                h16, &na);
+  gemv_sub_body<FMT, SUBR, 8, true, true, true, false, U>(qg, sg, qu, su, nullptr, h, n_rows, groups, blockIdx.x,
+                                                          gridDim.x, h16, &na);
 }
 
 // A group of independent GEMVs with one K in one launch: the workgroup
@@ -644,8 +794,8 @@ __global__ __launch_bounds__(512) void gemv_swiglu_norm_kernel(const uint8_t* __
 // grouping of its panels).  Every field of the group is read with
 // independent scalar loads and the workgroup's entry is picked by selects,
 // so the kernel arguments cost one memory round trip, as for one matrix.
-template <int FMT, int SUBR, int WAVES, bool XLDS>
-__global__ __launch_bounds__(WAVES * 64) void gemv_sub_group_kernel(GemvGroup g) {
+template <int FMT, int SUBR, int WAVES, bool XLDS, int U>
+__global__ __launch_bounds__((kSubThreads<FMT, SUBR, WAVES, XLDS>)) void gemv_sub_group_kernel(GemvGroup g) {
   const int b = static_cast<int>(blockIdx.x);
   const uint8_t* q = g.q[0];
   const uint16_t* s = g.s[0];
@@ -669,12 +819,12 @@ __global__ __launch_bounds__(WAVES * 64) void gemv_sub_group_kernel(GemvGroup g)
   const int64_t local = b - first;
   const int64_t nb = padded_rows(n) / SUBR;
   if (local >= nb) return;                             // padding workgroup (whole group exits)
-  gemv_sub_body<FMT, SUBR, WAVES, XLDS>(q, s, nullptr, nullptr, x, y, n, groups, local, nb);
+  gemv_sub_body<FMT, SUBR, WAVES, XLDS, false, false, false, U>(q, s, nullptr, nullptr, x, y, n, groups, local, nb);
 }
 
 // The grouped GEMV with the RMSNorm of the shared input folded in (8
 // wavefronts, activation in LDS).
-template <int FMT, int SUBR>
+template <int FMT, int SUBR, int U>
 __global__ __launch_bounds__(512) void gemv_sub_group_norm_kernel(GemvGroup g, NormArgs na) {
   const int b = static_cast<int>(blockIdx.x);
   const uint8_t* q = g.q[0];
@@ -695,13 +845,13 @@ __global__ __launch_bounds__(512) void gemv_sub_group_norm_kernel(GemvGroup g, N
   const int64_t local = b - first;
   const int64_t nb = padded_rows(n) / SUBR;
   if (local >= nb) return;                             // padding workgroup (never workgroup 0)
-  gemv_sub_body<FMT, SUBR, 8, true, false, true>(q, s, nullptr, nullptr, nullptr, y, n, groups, local, nb, nullptr,
-                                                 &na);
+  gemv_sub_body<FMT, SUBR, 8, true, false, true, false, U>(q, s, nullptr, nullptr, nullptr, y, n, groups, local, nb,
+                                                           nullptr, &na);
 }
 
 // The q/k/v projections with the norm folded in and the RoPE / cache
 // epilogue (matrix 0: q, 1: k, 2: v).
-template <int FMT, int SUBR>
+template <int FMT, int SUBR, int U>
 __global__ __launch_bounds__(512) void gemv_qkv_norm_rope_kernel(GemvGroup g, NormArgs na, QkvRopeEpi epi) {
   const int b = static_cast<int>(blockIdx.x);
   const uint8_t* q = g.q[0];
@@ -721,41 +871,34 @@ __global__ __launch_bounds__(512) void gemv_qkv_norm_rope_kernel(GemvGroup g, No
   const int64_t local = b - first;
   const int64_t nb = padded_rows(n) / SUBR;
   if (local >= nb) return;                             // padding workgroup (never workgroup 0)
-  gemv_sub_body<FMT, SUBR, 8, true, false, true, true>(q, s, nullptr, nullptr, nullptr, nullptr, n, groups, local,
-                                                       nb, nullptr, &na, &epi, role);
+  gemv_sub_body<FMT, SUBR, 8, true, false, true, true, U>(q, s, nullptr, nullptr, nullptr, nullptr, n, groups, local,
+                                                          nb, nullptr, &na, &epi, role);
 }
 
-template <int FMT, int SUBR, bool XLDS>
-hipError_t launch_sub_waves(int waves, const GemvGroup& g, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>(g.start[g.count]));
-  const size_t lds = XLDS ? static_cast<size_t>(g.groups) * 64 : 0;
-  if constexpr (FMT != QM_Q4_G32 && FMT != QM_Q8_G32) {
-    // The other formats use the plan's 8 wavefronts only.
-    if (g.count == 1)
-      hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, g.q[0], g.s[0], g.x[0],
-                         g.y[0], g.n[0], g.groups);
-    else
-      hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, g);
-    return hipGetLastError();
-  }
-  if (g.count == 1) {
-    const auto q = g.q[0]; const auto s = g.s[0]; const auto x = g.x[0]; const auto y = g.y[0];
-    const int n = g.n[0], gi = g.groups;
-    switch (waves) {
-      case 1: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 1, XLDS>), grid, dim3(64), lds, st, q, s, x, y, n, gi); break;
-      case 2: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 2, XLDS>), grid, dim3(128), lds, st, q, s, x, y, n, gi); break;
-      case 4: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 4, XLDS>), grid, dim3(256), lds, st, q, s, x, y, n, gi); break;
-      default: hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, q, s, x, y, n, gi); break;
+// fn(SUBR, U) with both as integral constants, for the sub-panel plan
+// (rows 4 / 8 / 16 / 32; chunks per lane per pass 1, 2, 3, 4 or 8 for Q4 and
+// Q8, the format's fixed count otherwise).
+template <int FMT, class Fn>
+hipError_t with_sub_plan(int subr, int u, Fn&& fn) {
+  auto by_u = [&](auto sr) -> hipError_t {
+    if constexpr (FMT == QM_Q4_G32 || FMT == QM_Q8_G32) {
+      switch (u) {
+        case 1: return fn(sr, std::integral_constant<int, 1>{});
+        case 2: return fn(sr, std::integral_constant<int, 2>{});
+        case 3: return fn(sr, std::integral_constant<int, 3>{});
+        case 4: return fn(sr, std::integral_constant<int, 4>{});
+        default: return fn(sr, std::integral_constant<int, 8>{});
+      }
+    } else {
+      return fn(sr, std::integral_constant<int, kSubU<FMT>>{});
     }
-    return hipGetLastError();
+  };
+  switch (subr) {
+    case 4: return by_u(std::integral_constant<int, 4>{});
+    case 8: return by_u(std::integral_constant<int, 8>{});
+    case 16: return by_u(std::integral_constant<int, 16>{});
+    default: return by_u(std::integral_constant<int, 32>{});
   }
-  switch (waves) {
-    case 1: hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 1, XLDS>), grid, dim3(64), lds, st, g); break;
-    case 2: hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 2, XLDS>), grid, dim3(128), lds, st, g); break;
-    case 4: hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 4, XLDS>), grid, dim3(256), lds, st, g); break;
-    default: hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, g); break;
-  }
-  return hipGetLastError();
 }
 
 template <int FMT, bool XLDS>
@@ -767,12 +910,18 @@ hipError_t launch_sub(const GemvPlan& plan, GemvGroup& g, hipStream_t st) {
     start += i + 1 < g.count ? (nb + kXcds - 1) / kXcds * kXcds : nb;
   }
   g.start[g.count] = start;
-  switch (plan.subr) {
-    case 4: return launch_sub_waves<FMT, 4, XLDS>(plan.waves, g, st);
-    case 8: return launch_sub_waves<FMT, 8, XLDS>(plan.waves, g, st);
-    case 16: return launch_sub_waves<FMT, 16, XLDS>(plan.waves, g, st);
-    default: return launch_sub_waves<FMT, 32, XLDS>(plan.waves, g, st);
-  }
+  const dim3 grid(static_cast<unsigned>(start));
+  const size_t lds = XLDS ? static_cast<size_t>(g.groups) * 64 : 0;
+  return with_sub_plan<FMT>(plan.subr, plan.u, [&](auto sr, auto uu) {
+    constexpr int SUBR = decltype(sr)::value, U = decltype(uu)::value;
+    const dim3 block(kSubThreads<FMT, SUBR, 8, XLDS>);
+    if (g.count == 1)
+      hipLaunchKernelGGL((gemv_sub_kernel<FMT, SUBR, 8, XLDS, U>), grid, block, lds, st, g.q[0], g.s[0], g.x[0],
+                         g.y[0], g.n[0], g.groups);
+    else
+      hipLaunchKernelGGL((gemv_sub_group_kernel<FMT, SUBR, 8, XLDS, U>), grid, block, lds, st, g);
+    return hipGetLastError();
+  });
 }
 
 template <int FMT>
@@ -824,29 +973,42 @@ hipError_t launch_fmt(const uint8_t* q, const uint16_t* s, const uint16_t* x, fl
 // for N <= 1024 with K >= 2048) that keeps the grid at <= 2 workgroups per
 // CU; activations are staged in LDS for K <= 4096 and read from global
 // memory beyond.
+// Chunks per lane per pass of the sub-panel kernel: enough for one pass over
+// the K groups (the smallest of 1, 2, 3, 4, 8 that covers them; 8 and more
+// passes beyond), for Q4 and Q8; the format's fixed count otherwise.
+static int sub_u(int32_t fmt, int64_t groups, int subr) {
+  if (fmt != QM_Q4_G32 && fmt != QM_Q8_G32) return kSubU<QM_Q4_G32> / (fmt_float(fmt) ? 2 : 1);
+  const int64_t stride = 8 * (kPanel / subr);
+  const int64_t need = (groups + stride - 1) / stride;
+  return need <= 1 ? 1 : need <= 2 ? 2 : need <= 3 ? 3 : need <= 4 ? 4 : 8;
+}
+
 GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count) {
-  // Tuning sweeps only: QM_GEMV_PLAN="rows,waves,x_in_lds" forces the plan.
+  const int64_t groups = k / kGroup;
+  // Tuning sweeps only: QM_GEMV_PLAN="rows,waves,x_in_lds" forces the plan
+  // (waves: of the panel kernel, rows = 64; the sub-panel kernel always has 8).
   static const GemvPlan forced = [] {
-    GemvPlan f{0, 0, 1};
+    GemvPlan f{0, 0, 1, 0};
     if (const char* e = tuning_override("QM_GEMV_PLAN")) std::sscanf(e, "%d,%d,%d", &f.subr, &f.waves, &f.xlds);
     return f;
   }();
   if (forced.subr == 4 || forced.subr == 8 || forced.subr == 16 || forced.subr == 32 || forced.subr == 64) {
     GemvPlan f = forced;
-    if (f.subr < kPanel && k > 16384) f.xlds = 0;
+    if (f.subr < kPanel && k > kXldsMaxK) f.xlds = 0;
     if (f.subr == kPanel) {
       int w = 1;
       while (w < 16 && w < f.waves) w = w == 8 ? 12 : (w == 12 ? 16 : 2 * w);
       f.waves = w;
     } else {
-      f.waves = f.waves <= 1 ? 1 : f.waves <= 2 ? 2 : f.waves <= 4 ? 4 : 8;
+      f.waves = 8;
+      f.u = sub_u(fmt, groups, f.subr);
+      if (sub_bcast(fmt, f.subr)) f.xlds = 0;
     }
     return f;
   }
   const int64_t npad = padded_rows(n);
   const int64_t panels = npad / kPanel;
-  const int64_t groups = k / kGroup;
-  GemvPlan p;
+  GemvPlan p{};
   if (panels >= cu_count) {
     int w = 1;
     if (fmt == QM_Q4_G32) {
@@ -862,9 +1024,14 @@ GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count) {
   }
   int subr = (npad <= 1024 && k >= 2048) ? 4 : 8;
   while (subr < 32 && npad / subr > 2 * cu_count) subr *= 2;
+  // Q4 / Q8: at least 16 rows, so the activations go by lane broadcast
+  // (measured on MI355X: 16-row workgroups also load faster than 8- or 4-row
+  // ones at 3072 -> 3072 and 3072 -> 8192).
+  if (fmt == QM_Q4_G32 || fmt == QM_Q8_G32) subr = subr < 16 ? 16 : subr;
   p.subr = subr;
   p.waves = 8;
-  p.xlds = k <= 4096 ? 1 : 0;
+  p.xlds = sub_bcast(fmt, subr) ? 0 : (k <= kXldsMaxK ? 1 : 0);
+  p.u = sub_u(fmt, groups, subr);
   return p;
 }
 
@@ -874,7 +1041,8 @@ void gemv_kernel_name(int32_t fmt, int64_t n, int64_t k, int cu_count, char* buf
     std::snprintf(buf, len, "gemv_kernel<%d, %d, %d>", fmt, p.waves,
                   fmt == QM_Q4_G32 ? kPanelUnroll<QM_Q4_G32> : fmt == QM_Q8_G32 ? kPanelUnroll<QM_Q8_G32> : 0);
   else
-    std::snprintf(buf, len, "gemv_sub_kernel<%d, %d, %d, %s>", fmt, p.subr, p.waves, p.xlds ? "true" : "false");
+    std::snprintf(buf, len, "gemv_sub_kernel<%d, %d, %d, %s, %d>", fmt, p.subr, p.waves, p.xlds ? "true" : "false",
+                  p.u);
 }
 
 hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count, hipStream_t st) {
@@ -899,30 +1067,22 @@ hipError_t launch_gemv_group(int32_t fmt, GemvGroup& g, int64_t k, int cu_count,
 
 namespace {
 
-template <int FMT, int SUBR, bool XLDS>
-hipError_t launch_swiglu_rows(const uint8_t* qg, const uint16_t* sg, const uint8_t* qu, const uint16_t* su,
-                              const uint16_t* x, float* h, uint16_t* h16, int64_t n, int groups, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>(padded_rows(n) / SUBR));
-  const size_t lds = XLDS ? static_cast<size_t>(groups) * 64 : 0;
-  hipLaunchKernelGGL((gemv_swiglu_kernel<FMT, SUBR, 8, XLDS>), grid, dim3(512), lds, st, qg, sg, qu, su, x, h,
-                     static_cast<int>(n), groups, h16);
-  return hipGetLastError();
-}
-
 template <int FMT>
 hipError_t launch_swiglu_fmt(const GemvPlan& plan, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
                              const uint16_t* su, const uint16_t* x, float* h, uint16_t* h16, int64_t n, int groups,
                              hipStream_t st) {
-  switch (plan.subr) {
-    case 4: return plan.xlds ? launch_swiglu_rows<FMT, 4, true>(qg, sg, qu, su, x, h, h16, n, groups, st)
-                             : launch_swiglu_rows<FMT, 4, false>(qg, sg, qu, su, x, h, h16, n, groups, st);
-    case 8: return plan.xlds ? launch_swiglu_rows<FMT, 8, true>(qg, sg, qu, su, x, h, h16, n, groups, st)
-                             : launch_swiglu_rows<FMT, 8, false>(qg, sg, qu, su, x, h, h16, n, groups, st);
-    case 16: return plan.xlds ? launch_swiglu_rows<FMT, 16, true>(qg, sg, qu, su, x, h, h16, n, groups, st)
-                              : launch_swiglu_rows<FMT, 16, false>(qg, sg, qu, su, x, h, h16, n, groups, st);
-    default: return plan.xlds ? launch_swiglu_rows<FMT, 32, true>(qg, sg, qu, su, x, h, h16, n, groups, st)
-                              : launch_swiglu_rows<FMT, 32, false>(qg, sg, qu, su, x, h, h16, n, groups, st);
-  }
+  const dim3 grid(static_cast<unsigned>(padded_rows(n) / plan.subr));
+  auto go = [&](auto xl) {
+    constexpr bool XLDS = decltype(xl)::value;
+    const size_t lds = XLDS ? static_cast<size_t>(groups) * 64 : 0;
+    return with_sub_plan<FMT>(plan.subr, plan.u, [&](auto sr, auto uu) {
+      constexpr int SUBR = decltype(sr)::value, U = decltype(uu)::value;
+      hipLaunchKernelGGL((gemv_swiglu_kernel<FMT, SUBR, 8, XLDS, U>), grid, dim3(kSubThreads<FMT, SUBR, 8, XLDS>), lds, st, qg,
+                         sg, qu, su, x, h, static_cast<int>(n), groups, h16);
+      return hipGetLastError();
+    });
+  };
+  return plan.xlds ? go(std::true_type{}) : go(std::false_type{});
 }
 
 }  // namespace
@@ -937,7 +1097,8 @@ hipError_t launch_gemv_swiglu(int32_t fmt, const uint8_t* qg, const uint16_t* sg
   GemvPlan plan = gemv_plan(fmt, n, k, cu_count);
   if (plan.subr == kPanel) {
     plan.subr = 32;
-    plan.xlds = k <= 4096 ? 1 : 0;
+    plan.xlds = sub_bcast(fmt, 32) ? 0 : (k <= kXldsMaxK ? 1 : 0);
+    plan.u = sub_u(fmt, k / kGroup, 32);
   }
   const int groups = static_cast<int>(k / kGroup);
   return with_format(fmt, [&](auto f) {
@@ -968,16 +1129,16 @@ hipError_t launch_gemv_qkv_norm_rope(int32_t fmt, GemvGroup& g, const NormArgs& 
   g.start[3] = start;
   const dim3 grid(static_cast<unsigned>(start));
   const size_t lds = static_cast<size_t>(g.groups) * 64;
+  const int u = sub_u(fmt, g.groups, subr);
   auto go = [&](auto f) -> hipError_t {
     constexpr int F = decltype(f)::value;
-    switch (subr) {
-      case 4: hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, 4>), grid, dim3(512), lds, st, g, na, epi); break;
-      case 8: hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, 8>), grid, dim3(512), lds, st, g, na, epi); break;
-      case 16: hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, 16>), grid, dim3(512), lds, st, g, na, epi); break;
-      default: hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, 32>), grid, dim3(512), lds, st, g, na, epi); break;
-    }
-    return hipGetLastError();
+    return with_sub_plan<F>(subr, u, [&](auto sr, auto uu) {
+      hipLaunchKernelGGL((gemv_qkv_norm_rope_kernel<F, decltype(sr)::value, decltype(uu)::value>), grid, dim3(512),
+                         lds, st, g, na, epi);
+      return hipGetLastError();
+    });
   };
+
   if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
   if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
   return hipErrorInvalidValue;
@@ -998,16 +1159,16 @@ hipError_t launch_gemv_group_norm(int32_t fmt, GemvGroup& g, const NormArgs& na,
   g.start[g.count] = start;
   const dim3 grid(static_cast<unsigned>(start));
   const size_t lds = static_cast<size_t>(g.groups) * 64;
+  const int u = sub_u(fmt, g.groups, subr);
   auto go = [&](auto f) -> hipError_t {
     constexpr int F = decltype(f)::value;
-    switch (subr) {
-      case 4: hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, 4>), grid, dim3(512), lds, st, g, na); break;
-      case 8: hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, 8>), grid, dim3(512), lds, st, g, na); break;
-      case 16: hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, 16>), grid, dim3(512), lds, st, g, na); break;
-      default: hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, 32>), grid, dim3(512), lds, st, g, na); break;
-    }
-    return hipGetLastError();
+    return with_sub_plan<F>(subr, u, [&](auto sr, auto uu) {
+      hipLaunchKernelGGL((gemv_sub_group_norm_kernel<F, decltype(sr)::value, decltype(uu)::value>), grid, dim3(512),
+                         lds, st, g, na);
+      return hipGetLastError();
+    });
   };
+
   if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
   if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
   return hipErrorInvalidValue;
@@ -1021,16 +1182,16 @@ hipError_t launch_gemv_swiglu_norm(int32_t fmt, const uint8_t* qg, const uint16_
   const dim3 grid(static_cast<unsigned>(padded_rows(n) / subr));
   const size_t lds = static_cast<size_t>(groups) * 64;
   const int ni = static_cast<int>(n);
+  const int u = sub_u(fmt, groups, subr);
   auto go = [&](auto f) -> hipError_t {
     constexpr int F = decltype(f)::value;
-    switch (subr) {
-      case 4: hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, 4>), grid, dim3(512), lds, st, qg, sg, qu, su, na, h, h16, ni, groups); break;
-      case 8: hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, 8>), grid, dim3(512), lds, st, qg, sg, qu, su, na, h, h16, ni, groups); break;
-      case 16: hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, 16>), grid, dim3(512), lds, st, qg, sg, qu, su, na, h, h16, ni, groups); break;
-      default: hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, 32>), grid, dim3(512), lds, st, qg, sg, qu, su, na, h, h16, ni, groups); break;
-    }
-    return hipGetLastError();
+    return with_sub_plan<F>(subr, u, [&](auto sr, auto uu) {
+      hipLaunchKernelGGL((gemv_swiglu_norm_kernel<F, decltype(sr)::value, decltype(uu)::value>), grid, dim3(512),
+                         lds, st, qg, sg, qu, su, na, h, h16, ni, groups);
+      return hipGetLastError();
+    });
   };
+
   if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
   if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
   return hipErrorInvalidValue;

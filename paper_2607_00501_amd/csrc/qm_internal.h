@@ -127,6 +127,8 @@ struct NormArgs {
   float eps;
 };
 constexpr int64_t kNormGemvMaxK = 4096;
+// Largest K whose activation the sub-panel GEMV stages in LDS (16 KiB).
+constexpr int kXldsMaxK = 8192;
 hipError_t launch_gemv_group_norm(int32_t fmt, GemvGroup& g, const NormArgs& na, int64_t k, int cu_count,
                                   hipStream_t st);
 hipError_t launch_gemv_swiglu_norm(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
@@ -228,7 +230,9 @@ hipError_t launch_route(const float* logits, int64_t m, int32_t e, int32_t k, in
 // Per-chip choices (Sec. 3.3: per-chip configuration table).
 // GEMV launch plan: rows per workgroup (64 = whole panel), wavefronts per
 // workgroup, and whether activations are staged in LDS (sub-panel kernel).
-struct GemvPlan { int subr; int waves; int xlds; };
+// subr: rows per workgroup (64: the panel kernel); waves: wavefronts (panel
+// kernel); xlds: x staged in LDS; u: chunks per lane per pass (sub-panel).
+struct GemvPlan { int subr; int waves; int xlds; int u; };
 GemvPlan gemv_plan(int32_t fmt, int64_t n, int64_t k, int cu_count);
 // Name (with template arguments) of the kernel qmatmul_gemv launches for this shape.
 void gemv_kernel_name(int32_t fmt, int64_t n, int64_t k, int cu_count, char* buf, size_t len);
