@@ -287,7 +287,7 @@ qm_status qmatmul_gemv_grouped(int32_t count, const qm_qweight* w, const uint16_
  * q/k/v projections of a layer, or its gate and up projections, which all
  * read the same X):  Y_i[m][n_i] = sum_k X[m][k] * w_i'[n_i][k]  for
  * i < count, in one launch.  w: host array of `count` descriptors, all of
- * one format (Q4 or Q8; any format when m == 1), DEVICE layout, batch 1,
+ * one format (any of the eight), DEVICE layout, batch 1,
  * one k; n_i may differ.  X: fp16 [m][k] row-major
  * (device, 16-byte aligned), shared by all entries.  y: host array of
  * `count` device pointers to fp32 [m][n_i], 4-byte aligned, not
@@ -300,13 +300,15 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
                                float* const* y, void* stream);
 
 /* Prefill GEMM (Sec. 3.3, Sec. 3.4, M > 1): Y[m][n] = sum_k X[m][k] * w'[n][k].
- * w: DEVICE layout, batch 1, Q4 or Q8 (Sec. 4.1: both formats; the MFMA
- * path is the same, only the in-register unpacking differs); any format
- * when m == 1.  Other formats with m > 1: QM_EFORMAT.
+ * w: DEVICE layout, batch 1, any of the eight formats of Sec. 4.1 (one MFMA
+ * path; only the in-register unpacking differs).
  * X: fp16 [m][k] row-major; Y: fp32 [m][n].
  * X tiles and (for most tile shapes) the raw weight chunks are copied into
- * LDS by DMA; weights are dequantised to fp16 (value fp16_RNE(s*q)) in
- * registers and fed to fp16 MFMA with fp32 accumulation.
+ * LDS by DMA; integer-format weights are dequantised to fp16 (value
+ * fp16_RNE(s*q)) in registers, F16 weights are used as stored and BF16
+ * weights are converted to fp16 (exact for |w| in [2^-14, 65504]; smaller
+ * magnitudes round to fp16 subnormals, larger ones overflow to inf), all fed
+ * to fp16 MFMA with fp32 accumulation.
  * m >= 1 (m == 1 runs the GEMV); m <= 65536 per call (chunk larger
  * prompts).  Deterministic. */
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream);

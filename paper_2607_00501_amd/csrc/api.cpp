@@ -468,8 +468,6 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
       return fail(QM_ELAYOUT, "qmatmul_gemm_grouped: w[%d] must be in DEVICE layout", i);
     if (w[i].batch != 1) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: w[%d] batch must be 1", i);
     if (w[i].format != w[0].format) return fail(QM_EFORMAT, "qmatmul_gemm_grouped: formats differ");
-    if (m > 1 && fmt_float(w[i].format))
-      return fail(QM_EFORMAT, "qmatmul_gemm_grouped: the MFMA GEMM takes the integer formats Q2 .. Q8 (m > 1)");
     if (w[i].k != w[0].k) return fail(QM_ESHAPE, "qmatmul_gemm_grouped: k differs between entries");
     if (w[i].n > 0 && !y[i]) return fail(QM_EINVAL, "qmatmul_gemm_grouped: null y[%d]", i);
     if (!aligned4(y[i])) return fail(QM_EALIGN, "qmatmul_gemm_grouped: y[%d] must be 4-byte aligned", i);
@@ -508,8 +506,6 @@ qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float*
   if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "qmatmul_gemm: weights must be in DEVICE layout");
   if (w->batch != 1) return fail(QM_ESHAPE, "qmatmul_gemm: batch must be 1");
   if (m < 1 || m > 65536) return fail(QM_ESHAPE, "qmatmul_gemm: m=%lld must be in [1, 65536]", (long long)m);
-  if (m > 1 && fmt_float(w->format))
-    return fail(QM_EFORMAT, "qmatmul_gemm: the MFMA GEMM takes the integer formats Q2 .. Q8 (m > 1)");
   if (w->n > 0 && (!x || !y)) return fail(QM_EINVAL, "qmatmul_gemm: null x or y");
   if (!aligned16(x)) return fail(QM_EALIGN, "qmatmul_gemm: x must be 16-byte aligned");
   if (!aligned4(y)) return fail(QM_EALIGN, "qmatmul_gemm: y must be 4-byte aligned");

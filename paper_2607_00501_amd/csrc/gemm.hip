@@ -1,5 +1,6 @@
 // Prefill GEMM  Y[m][n] = sum_k X[m][k] * w'[n][k]  with Q2 .. Q8 weights
-// dequantised inside the kernel and fp16 MFMA (BaseRT Sec. 3.4: tiled GEMM
+// dequantised inside the kernel, or F16 / BF16 weights taken as they are
+// (BF16 converted to fp16 in registers), and fp16 MFMA (BaseRT Sec. 3.4: tiled GEMM
 // for the prompt, tile geometry chosen by sequence-length regime; Sec. 3.3:
 // dequantisation lives inside the GEMM, weights are never materialised).
 // The kernel itself is the shared MFMA core in qgemm.h (dense mode);
@@ -36,7 +37,8 @@ hipError_t launch_tile(const QgemmArgs& a, hipStream_t st) {
 // The other formats use the same plan.  Where their weight stages do not fit
 // in LDS beside the A stages (Q8, Q5, Q6 at 128 x 256) the tile keeps the
 // weights in registers; for Q8 that still beats 64 x 256 tiles by 10-20%
-// where the rule picks it.
+// where the rule picks it.  F16 / BF16 weights always go through registers:
+// each lane's 16-byte quarters are already MFMA B fragments.
 GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count) {
   // Tuning sweeps only: QM_GEMM_PLAN="bm,wn,wk" forces the plan (one of the
   // instantiated tiles, see launch_args).
@@ -68,7 +70,7 @@ const char* gemm_tile_name(int64_t m, int64_t n) {
 namespace {
 
 // The tiles gemm_plan() can choose (QM_GEMM_PLAN may force any of them).
-// Both formats instantiate the same tiles.
+// Every format instantiates the same tiles.
 #define QM_GEMM_TILES(X) \
   X(128, 4, 1) X(64, 4, 1) X(64, 2, 2) \
   X(64, 1, 1) X(64, 1, 2) X(64, 1, 4) X(64, 1, 8) X(32, 1, 1) X(32, 1, 2) X(32, 1, 4) X(32, 1, 8)
@@ -107,6 +109,14 @@ hipError_t launch_args(const QgemmArgs& a, int32_t fmt, int cu_count, hipStream_
   {
     constexpr int F_ = QM_Q6_G32;
     QM_LAUNCH_FMT(QM_Q6_G32)
+  }
+  {
+    constexpr int F_ = QM_F16;
+    QM_LAUNCH_FMT(QM_F16)
+  }
+  {
+    constexpr int F_ = QM_BF16;
+    QM_LAUNCH_FMT(QM_BF16)
   }
 #undef QM_LAUNCH_TILE
 #undef QM_LAUNCH_FMT

@@ -99,6 +99,13 @@ __device__ __forceinline__ void vm_wait() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// vm_wait<BASE + live * PER>() for a wavefront-uniform live in [0, L...]
+// (s_waitcnt takes an immediate: one scalar branch per candidate).
+template <int BASE, int PER, int... L>
+__device__ __forceinline__ void vm_wait_live(int live, std::integer_sequence<int, L...>) {
+  ((live == L ? vm_wait<BASE + L * PER>() : void()), ...);
+}
+
 // 16 bytes per lane from global memory straight into LDS: lane l of the
 // wavefront writes lds_dst + 16 l (lds_dst is wavefront-uniform and goes
 // to M0).  Issued as inline asm so that the compiler's wait-count tracking
@@ -269,8 +276,11 @@ template <int BM, int WN, int WK, QgMode MODE, int DEPTH, int FMT>
 struct Cfg {
   static constexpr bool kQ8 = FMT == QM_Q8_G32;
   static constexpr bool kPlanes = FMT == QM_Q2_G32 || FMT == QM_Q3_G32 || FMT == QM_Q5_G32 || FMT == QM_Q6_G32;
-  static_assert(FMT == QM_Q4_G32 || ((kQ8 || kPlanes) && MODE == QgMode::kDense),
-                "Q2/Q3/Q5/Q6/Q8 weights: dense GEMM only (no F16/BF16)");
+  // F16 / BF16 weights: no codes, no scales; a lane's 8 k of a substep are
+  // one 16-byte quarter of its row (BF16 converted to fp16 in registers).
+  static constexpr bool kFloat = FMT == QM_F16 || FMT == QM_BF16;
+  static_assert(FMT == QM_Q4_G32 || ((kQ8 || kPlanes || kFloat) && MODE == QgMode::kDense),
+                "Q2/Q3/Q5/Q6/Q8/F16/BF16 weights: dense GEMM only");
   static constexpr int kChunkBytes = chunk_block_bytes(FMT);      // one group of a 64-row panel
   // B words a lane holds per group and column half: Q4 two nibble dwords,
   // Q8 four byte dwords, Q5/Q6 two nibble dwords + one high-plane dword,
@@ -297,7 +307,7 @@ struct Cfg {
   static constexpr int kAStageBytes = WK * BM * kBK * 2;
   static constexpr int kBMatBytes = 2 * kChunkBytes + 256;
   static constexpr int kBWaveBytes = kNB * kBMatBytes;
-  static constexpr bool kBLds = WN > 1 && kSlots * (kAStageBytes + WN * WK * kBWaveBytes) <= 80 * 1024;
+  static constexpr bool kBLds = !kFloat && WN > 1 && kSlots * (kAStageBytes + WN * WK * kBWaveBytes) <= 80 * 1024;
   static constexpr int kStageBytes = kAStageBytes + (kBLds ? WN * WK * kBWaveBytes : 0);
   // A LDS stages: DEPTH + 1 (A loaded DEPTH steps ahead, like B) when they
   // fit in 48 KiB or B goes through LDS, else 2 (A loaded one step ahead),
@@ -308,7 +318,8 @@ struct Cfg {
   // per weight matrix either the code chunks in 1 KiB pieces + 1 scale
   // block (LDS DMA) or 2 chunks x 2 column halves of codes and of scales
   // (registers).
-  static constexpr int kBLoads = kBLds ? kNB * (2 * (kPieces16 + kPieces4) + 1) : kNB * 2 * 2 * (kPlaneLoads + 1);
+  static constexpr int kBLoads = kBLds ? kNB * (2 * (kPieces16 + kPieces4) + 1)
+                                : kFloat ? kNB * 2 * 2 * 2 : kNB * 2 * 2 * (kPlaneLoads + 1);
   // Split-K partial sums of slices 1..WK-1, in halves (fp32 = 2 halves).
   static constexpr int kRedHalves = (WK - 1) * WN * kTM * 2 * kNB * 16 * 64 * 2;
   static constexpr int kLdsHalves =
@@ -422,7 +433,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   const uint8_t* b_q[NB];
   const uint16_t* b_s[NB];
   b_q[0] = mq + expert * mat_q + panel * G * CB;
-  b_s[0] = ms + expert * mat_s + panel * G * kPanel;
+  b_s[0] = C::kFloat ? ms : ms + expert * mat_s + panel * G * kPanel;   // float weights: no scales (null)
   if constexpr (NB == 2) {
     b_q[1] = p.q2 + expert * mat_q + panel * G * CB;
     b_s[1] = p.s2 + expert * mat_s + panel * G * kPanel;
@@ -438,6 +449,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   using BVec = std::conditional_t<Q8, u32x4, u32x2>;
   BVec rb[NS][NB][2][2];                                   // [slot][matrix][chunk][column half]
   uint32_t rw[NS][NB][2][2][LW];                           // the same for the bit-plane formats
+  u32x4 rf[C::kFloat ? NS : 1][NB][2][2][2];               // F16/BF16: [..][column half][substep] quarters
   uint32_t rs[NS][NB][2][2];
   char* const lds_b = reinterpret_cast<char*>(lds);
   // A tile of this slice in stage st; B region of this wavefront in stage st.
@@ -487,6 +499,18 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
       for (int c = 0; c < 2; ++c) {
         const int gc = min(2 * kt + c, G - 1);
         const uint8_t* bq = b_q[j] + static_cast<int64_t>(gc) * CB;
+        if constexpr (C::kFloat) {
+          // Row 32h + l%32: quarter 2(l/32) + s holds its k = 16(l/32) + 8s .. + 7.
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int sub = 0; sub < 2; ++sub) {
+              const u32x4* qa = reinterpret_cast<const u32x4*>(bq + (2 * (lane >> 5) + sub) * 1024 +
+                                                               16 * (32 * h + (lane & 31)));
+              rf[C::kFloat ? sl : 0][j][c][h][sub] = NT ? __builtin_nontemporal_load(qa) : *qa;
+            }
+          continue;
+        }
         const uint16_t* bs = b_s[j] + static_cast<int64_t>(gc) * kPanel;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -550,22 +574,35 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   // Issue order: the prologue takes A of steps 0 .. AD-1 and B of steps
   // 0 .. DEPTH-1 (step q's A before its B); step s then issues A of step
   // s + AD and B of step s + DEPTH, A first, also past the last step
-  // (clamped addresses, zero scales, stages never read), so the count of
-  // loads issued after A of step t is the same at every step.
+  // (clamped addresses, zero scales, stages never read).  LDS DMA is never
+  // dropped, so with B through LDS the count of loads issued after A of
+  // step t is the same at every step, and so it is inside the main loop,
+  // where every register load has a consumer (the next iteration).  In the
+  // steps after the loop a B load into registers for a step past the last
+  // one has none, and the compiler may drop it: there the waits count only
+  // the B loads of real steps (t + j < KTs), never less strict than the
+  // schedule needs.
   constexpr int kNA = C::kALoads, kNBl = C::kBLoads, AD = C::kADist, NSA = C::kAStages;
   static_assert(kNBl + (DEPTH - 1) * (kNA + kNBl) <= 63 && 2 * kNBl <= 63, "vmcnt range");
-  auto wait_a = [&](int t) __attribute__((always_inline)) {
+  auto wait_a = [&](int t, auto tail) __attribute__((always_inline)) {
     if constexpr (C::kBLds) {
       // all of step t (A and B): the groups of steps t+1 .. t+DEPTH-1 may remain
       vm_wait<(DEPTH - 1) * (kNA + kNBl)>();
+    } else if constexpr (!decltype(tail)::value) {
+      if constexpr (AD == DEPTH) vm_wait<kNBl + (DEPTH - 1) * (kNA + kNBl)>();
+      else if (t == 0) vm_wait<2 * kNBl>();
+      else vm_wait<kNBl>();
     } else if constexpr (AD == DEPTH) {
-      // after A(t): B(t), then A and B of steps t+1 .. t+DEPTH-1
-      vm_wait<kNBl + (DEPTH - 1) * (kNA + kNBl)>();
+      // after A(t): B(t), then A of steps t+1 .. t+DEPTH-1 and the B of
+      // those that are real steps
+      const int live = min(max(KTs - 1 - t, 0), DEPTH - 1);
+      vm_wait_live<kNBl + (DEPTH - 1) * kNA, kNBl>(live, std::make_integer_sequence<int, DEPTH>{});
     } else {
       // AD = 1, DEPTH = 2: after A(0): B(0), B(1); after A(t), t >= 1
-      // (issued by step t-1): B(t+1)
-      if (t == 0) vm_wait<2 * kNBl>();
-      else vm_wait<kNBl>();
+      // (issued by step t-1): B(t+1); B(1), B(t+1) only if a real step
+      const int live = t + 1 < KTs ? 1 : 0;
+      if (t == 0) vm_wait_live<kNBl, kNBl>(live, std::make_integer_sequence<int, 2>{});
+      else vm_wait_live<0, kNBl>(live, std::make_integer_sequence<int, 2>{});
     }
   };
   auto a_stage = [&](auto slot, int t) __attribute__((always_inline)) {
@@ -586,10 +623,10 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   // t's operands, the slots of steps t+1 .. t+DEPTH-1 are in flight, and the
   // slot of step t-1 is refilled with step t+DEPTH once every wavefront of
   // the slice is past step t-1 (the barrier at the top of the step).
-  auto step = [&](auto slot, int t) __attribute__((always_inline)) {
+  auto step = [&](auto slot, int t, auto tail) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot)::value;
     using Refill = std::integral_constant<int, (sl + DEPTH) % NS>;
-    wait_a(t);
+    wait_a(t, tail);
     slice_sync();
     // [matrix][column half][dword]: substep ks takes dword ks (Q4) or
     // dwords 2ks, 2ks+1 (Q8).
@@ -598,7 +635,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
     half2v sc[NB][2][2];                                   // [matrix][chunk][column half]
     const char* breg = b_region(sl);
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
+    for (int j = 0; j < (C::kFloat ? 0 : NB); ++j)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const bool ok = scale_ok(t, c);
@@ -655,7 +692,25 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
       }
     auto dequant = [&](int j, int h, int ks) __attribute__((always_inline)) {
       const int c = ks >> 1, s = ks & 1;
-      if constexpr (Q8) return dequant_q8(bd[j][h][2 * ks], bd[j][h][2 * ks + 1], sc[j][c][h], dq);
+      if constexpr (C::kFloat) {
+        // Past the last K step (or a padded panel) the clamped quarter is
+        // replaced by zeros: float weights carry no scale to zero it.
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        const u32x4 v = scale_ok(t, c) ? rf[C::kFloat ? sl : 0][j][c][h][s] : z;
+        if constexpr (FMT == QM_F16) {
+          return __builtin_bit_cast(half8v, v);
+        } else {
+          // bf16 -> fp16: exact for every bf16 in fp16's normal range (8
+          // significant bits fit in 11); smaller ones round to fp16 subnormals.
+          half8v o;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            o[2 * i] = static_cast<_Float16>(__uint_as_float(v[i] << 16));
+            o[2 * i + 1] = static_cast<_Float16>(__uint_as_float(v[i] & 0xFFFF0000u));
+          }
+          return o;
+        }
+      } else if constexpr (Q8) return dequant_q8(bd[j][h][2 * ks], bd[j][h][2 * ks + 1], sc[j][c][h], dq);
       else if constexpr (FMT == QM_Q5_G32 || FMT == QM_Q6_G32)
         return dequant_nib_hi<FMT>(bd[j][h][LW * c + s], bd[j][h][LW * c + 2], s, sc[j][c][h], dq);
       else if constexpr (FMT == QM_Q2_G32 || FMT == QM_Q3_G32)
@@ -719,11 +774,11 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   int t = 0;
   for (; t + NS <= KTs; t += NS) {
     [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
-      (step(std::integral_constant<int, I>{}, t + I), ...);
+      (step(std::integral_constant<int, I>{}, t + I, std::false_type{}), ...);
     }(Slots{});
   }
   [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
-    ((t + I < KTs ? step(std::integral_constant<int, I>{}, t + I) : void()), ...);
+    ((t + I < KTs ? step(std::integral_constant<int, I>{}, t + I, std::true_type{}) : void()), ...);
   }(Slots{});
   // No LDS DMA may still be in flight when the LDS is reused or the
   // workgroup ends (the prefetches past the last step included).

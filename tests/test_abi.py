@@ -96,8 +96,9 @@ def test_gemm_and_moe_validation():
     assert L.qmatmul_gemm(ctypes.byref(w), x, 0, y, None) == 2          # m = 0
     assert L.qmatmul_gemm(ctypes.byref(w), x, 70000, y, None) == 2      # m too large
     assert L.qmatmul_gemm(ctypes.byref(_fake_weight(fmt=9)), x, 16, y, None) == 4   # unknown format
-    for f in (B.F16, B.BF16):
-        assert L.qmatmul_gemm(ctypes.byref(_fake_weight(fmt=f)), x, 16, y, None) == 4   # no MFMA GEMM
+    for f in (B.F16, B.BF16):                                           # float formats: same checks
+        assert L.qmatmul_gemm(ctypes.byref(_fake_weight(fmt=f, layout=0)), x, 16, y, None) == 5
+        assert L.qmatmul_gemm(ctypes.byref(_fake_weight(fmt=f)), x, 70000, y, None) == 2
     assert L.qmatmul_gemm(ctypes.byref(_fake_weight(layout=0)), x, 16, y, None) == 5
     p = ctypes.c_void_p(0x50000)
     assert L.qmoe_route(p, 16, 2000, 8, p, p, p, p, p, None) == 2       # too many experts
@@ -242,7 +243,7 @@ def test_gemm_grouped_validation():
     assert call([w], m=0) == 2                                         # m < 1
     assert call([w, _fake_weight(fmt=2)]) == 4                         # formats differ
     assert call([_fake_weight(fmt=9)] * 2) == 4                        # unknown format
-    assert call([_fake_weight(fmt=B.BF16)] * 2) == 4                   # no MFMA GEMM for BF16
+    assert call([_fake_weight(fmt=B.BF16), _fake_weight(fmt=B.F16)]) == 4   # float formats differ
     assert call([w, _fake_weight(k=96)]) == 2                          # k differs
     assert call([w, _fake_weight(layout=0)]) == 5                      # not DEVICE layout
     assert call([w, w], ys=[0x40000, 0x40002]) == 3                    # y[1] misaligned

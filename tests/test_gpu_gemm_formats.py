@@ -1,6 +1,6 @@
-"""GPU parity of the MFMA GEMM with Q2/Q3/Q5/Q6 weights (qmatmul_gemm and
-qmatmul_gemm_grouped) with the oracle; F16/BF16 weights are refused for
-m > 1."""
+"""GPU parity of the MFMA GEMM with Q2/Q3/Q5/Q6 and F16/BF16 weights
+(qmatmul_gemm and qmatmul_gemm_grouped) with the oracle (Sec. 3.3: one GEMM
+per format for M > 1; Sec. 4.1: the eight formats)."""
 
 import ctypes
 
@@ -15,7 +15,8 @@ from tests.helpers import MFMA_TOL, rel_err
 
 pytestmark = pytest.mark.gpu
 
-FMTS = [(O.Q2, B.Q2_G32), (O.Q3, B.Q3_G32), (O.Q5, B.Q5_G32), (O.Q6, B.Q6_G32)]
+FMTS = [(O.Q2, B.Q2_G32), (O.Q3, B.Q3_G32), (O.Q5, B.Q5_G32), (O.Q6, B.Q6_G32),
+        (O.F16, B.F16), (O.BF16, B.BF16)]
 
 
 def _device_weight(w_np, bfmt):
@@ -50,13 +51,29 @@ def test_gemm_formats_parity(ofmt, bfmt, m, n, k):
     assert err <= 2e-3, err
 
 
+# Every output checked (no sampling) on tiles whose K slices end with steps
+# after the main loop, where the loads of a workgroup's last steps must all
+# have landed before their LDS tiles are read: 64 x 64 with 4-way split-K
+# (512 x 2048 x 2048), 64 x 128 with 2-way split-K, 128 x 256, and 64 x 64
+# with 8-way split-K over a ragged K.
+@pytest.mark.parametrize("ofmt,bfmt", [(O.Q4, B.Q4_G32), (O.Q8, B.Q8_G32), (O.F16, B.F16), (O.BF16, B.BF16)])
+@pytest.mark.parametrize("m,n,k", [(512, 2048, 2048), (500, 3000, 2080), (2000, 4100, 64), (200, 4096, 4128)])
+def test_gemm_every_output_last_k_steps(ofmt, bfmt, m, n, k):
+    w = inputs.weights_np(inputs.seed_for(7, n, "up", ofmt), (n, k))
+    x = inputs.activations_np(inputs.seed_for(7, m, "x", ofmt), (m, k))
+    y = B.qmatmul_gemm(_device_weight(w, bfmt), torch.from_numpy(x).cuda()).cpu().numpy()
+    err = rel_err(y, _ref(w, x, ofmt))
+    assert err <= 2e-3, err
+
+
 @pytest.mark.parametrize("ofmt,bfmt", FMTS)
 @pytest.mark.parametrize("m,n,k", [(70, 190, 512), (1100, 2048, 64)])
 def test_gemm_formats_integer_grid_exact(ofmt, bfmt, m, n, k):
-    """Scale-1 integer weights over every code in [-qmax, qmax] and small
-    integer X: the fp32 result is exact (B through registers and LDS)."""
+    """Scale-1 integer weights over every code in [-qmax, qmax] (F16/BF16:
+    integers in [-64, 64], exact in both) and small integer X: the fp32
+    result is exact (B through registers and LDS)."""
     rng = np.random.default_rng(40 + ofmt)
-    qm = O.QMAX[ofmt]
+    qm = O.QMAX.get(ofmt, 64)
     w = rng.integers(-qm, qm + 1, size=(n, k))
     w[:, ::32] = qm
     x = rng.integers(-4, 5, size=(m, k)).astype(np.float16)
@@ -92,11 +109,30 @@ def test_gemm_formats_grouped(ofmt, bfmt):
 
 
 @pytest.mark.parametrize("bfmt", [B.F16, B.BF16])
-def test_gemm_float_formats_refused_beyond_m1(bfmt):
+def test_gemm_float_formats_m1_runs_the_gemv(bfmt):
     w = _device_weight(inputs.weights_np(3, (64, 64)), bfmt)
     x = torch.from_numpy(inputs.activations_np(4, (2, 64))).cuda()
     y = torch.empty((2, 64), device="cuda")
     st = B.lib().qmatmul_gemm(ctypes.byref(w.c()), ctypes.c_void_p(x.data_ptr()), 2, ctypes.c_void_p(y.data_ptr()), None)
-    assert st == 4 and "integer formats" in B.qm_last_error()
+    assert st == 0, B.qm_last_error()
     y1 = B.qmatmul_gemm(w, x[:1])                                        # m = 1 runs the GEMV
     assert torch.equal(y1[0], B.qmatmul_gemv(w, x[0]))
+
+
+def test_gemm_bf16_weights_reach_the_mfma_as_fp16():
+    """BF16 weights over 2^-26 .. 2^15 times the identity: every output is
+    the weight's value rounded to nearest-even fp16, exact where it lies in
+    fp16's normal range, a subnormal (or zero) below it."""
+    n, k = 192, 96
+    rng = np.random.default_rng(77)
+    w = (np.sign(rng.standard_normal((n, k))) * np.exp2(rng.uniform(-26, 15, (n, k)))).astype(np.float32)
+    x = np.eye(k, dtype=np.float16)
+    y = B.qmatmul_gemm(_device_weight(w, B.BF16), torch.from_numpy(x).cuda()).cpu().numpy()
+    bits, _ = O.quantise(w, O.BF16)
+    want = O.fp16_value(O.dequantise_f16_tile_value(O.pack(bits, O.BF16), None, O.BF16))
+    # Compared as values: a weight that rounds to -0 gives +0 once the
+    # other k's zero products are added.
+    assert np.array_equal(y.T.astype(np.float64), want.astype(np.float64))
+    small = np.abs(O.bf16_value(bits)) < 2.0 ** -14
+    assert small.any() and (~small).any()
+    assert np.array_equal(y.T[~small].astype(np.float64), O.bf16_value(bits)[~small].astype(np.float64))
