@@ -17,7 +17,8 @@ The line also carries
                 events on the launch stream over a graph of all its launches
                 of the step back to back; per-shape figures beside it;
   cpu_baseline: the CPU oracle timed on a bounded sample of the same step
-                (whole layers, then a slice of the lm_head);
+                (whole layers, then a slice of the lm_head), and beside it
+                on samples of the prefill GEMM and MoE workloads at M = 128;
   extra:        the other workloads (single 1024x1024 GEMV hot and cold,
                 Qwen3-0.6B Q4 and Llama-3.2-3B Q8 decode stacks, Llama-3.2-1B
                 prefill GEMM stacks and the Qwen3-30B-A3B MoE layer at M = 128
@@ -35,6 +36,8 @@ import json
 import os
 import sys
 import time
+
+import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -278,7 +281,59 @@ def cpu_baseline(budget_s: float):
                       f"0-{rows - 1} of the Llama-3.2-3B Q4 decode step; {nbytes} weight bytes in "
                       f"{spent:.2f} s of oracle time (numpy: canonical codes dequantised, fp64 products "
                       f"and sums; the fp64 matrix-vector product on BLAS threads={info['blas_threads']}, "
-                      f"the dequantisation on one thread)"}
+                      f"the dequantisation on one thread)",
+            "other_workloads": cpu_baseline_gemm_moe()}
+
+
+def cpu_baseline_gemm_moe():
+    """The oracle on bounded samples of the prefill GEMM and MoE workloads
+    (reported beside the headline's baseline): one Llama-3.2-1B layer's seven
+    GEMMs at M = 128, and the Qwen3-30B-A3B MoE layer at M = 128 routed and
+    bucketed in full, with the FFNs of its first 16 experts' buckets.  The
+    oracle's own quantisation and packing is prepared untimed, as above."""
+    from oracle import qmatmul_oracle as O
+    from paper_2607_00501_amd import inputs, workloads
+    out = {}
+    m = 128
+    prepared = []
+    for name, k, n in workloads.LLAMA32_1B_LAYER:
+        q, sc = O.quantise(inputs.weights_np(inputs.seed_for(3, 0, name), (n, k)), O.Q4)
+        prepared.append((O.pack(q, O.Q4), sc, inputs.activations_np(inputs.seed_for(3, m, "x"), (m, k)), k, n))
+    t0 = time.perf_counter()
+    flops = 0
+    for qb, sc, x, k, n in prepared:
+        O.gemm(qb, sc, O.Q4, x)
+        flops += 2 * m * n * k
+    dt = time.perf_counter() - t0
+    out["llama3.2-1b_prefill_m128"] = {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s",
+                                       "sample": f"one layer's 7 GEMMs at M = 128 ({flops} FLOP in {dt:.2f} s)"}
+    cfg = workloads.QWEN3_30B_A3B_MOE
+    E, K, H, I = cfg["experts"], cfg["top_k"], cfg["hidden"], cfg["inter"]
+    sample = 16
+    x = inputs.activations_np(inputs.seed_for(4, m, "x"), (m, H)).astype(np.float64)
+    lg = inputs.logits_np(inputs.seed_for(4, m, "logits"), (m, E))
+    packed = []
+    for e in range(sample):
+        ws = []
+        for t, sh in (("gate", (I, H)), ("up", (I, H)), ("down", (H, I))):
+            q, sc = O.quantise(inputs.weights_np(inputs.seed_for(4, e, t), sh), O.Q4)
+            ws.append((O.pack(q, O.Q4), sc))
+        packed.append(ws)
+    t0 = time.perf_counter()
+    ids, gates = O.moe_route(lg, K)
+    counts, offsets, sorted_assign = O.moe_bucket(ids, E)
+    rows_done = 0
+    for e in range(sample):
+        rows = sorted_assign[offsets[e]:offsets[e + 1]]
+        wg, wu, wd = (O.dequantise(qb, sc, O.Q4) for qb, sc in packed[e])
+        O.expert_ffn(x[rows // K], wg, wu, wd)
+        rows_done += rows.size
+    dt = time.perf_counter() - t0
+    flops = 2 * rows_done * 3 * H * I
+    out["qwen3-30b-a3b_moe_m128"] = {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s",
+                                     "sample": f"route + bucket of all {m} tokens, FFNs of experts 0-{sample - 1} "
+                                               f"({rows_done} assignments, {flops} FLOP in {dt:.2f} s)"}
+    return out
 
 
 # ------------------------------------------------------------ extras
