@@ -795,7 +795,7 @@ def traffic_from_profile(kernel):
             for line in f:
                 if not line.startswith("traffic:"):
                     continue
-                fields = dict(kv.split("=", 1) for kv in line.split("\t")[1:])
+                fields = dict(kv.split("=", 1) for kv in line.rstrip("\n").split("\t")[1:])
                 if fields.get("kernel") == kernel and fields.get("kernel_source_sha256") == kernel_source_hash():
                     return int(float(fields["hbm_bytes_per_launch"]))
     except (OSError, KeyError, ValueError):
