@@ -16,6 +16,8 @@ The line also carries
                 bytes per launch / its mean launch duration, timed with HIP
                 events on the launch stream over a graph of all its launches
                 of the step back to back; per-shape figures beside it;
+  calibration:  achievable rates on this part from torch's own kernels (a
+                streaming copy, a hipBLASLt fp16 matmul), as context;
   cpu_baseline: the CPU oracle timed on a bounded sample of the same step
                 (whole layers, then a slice of the lm_head), and beside it
                 on samples of the prefill GEMM and MoE workloads at M = 128;
@@ -803,6 +805,42 @@ def traffic_from_profile(kernel):
     return None
 
 
+def calibration(torch):
+    """Achievable rates on this part, measured with torch's own kernels (not
+    this library): a streaming copy of 1 GiB (read + write bytes over the
+    time, the best of five passes) and an fp16 matmul 8192 x 8192 x 8192
+    (hipBLASLt).  Context for the roofline fractions, which stay against the
+    spec peaks."""
+    st = torch.cuda.current_stream()
+
+    def best_ms(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            fn()
+            e1.record(st)
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1))
+        return best
+    a = torch.ones(256 * 2**20, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    copy_ms = best_ms(lambda: b.copy_(a), 5)
+    copy_gbs = 2 * a.numel() * 4 / copy_ms / 1e6
+    del a, b
+    n = 8192
+    x = torch.randn((n, n), device="cuda").half()
+    w = torch.randn((n, n), device="cuda").half()
+    mm_ms = best_ms(lambda: torch.matmul(x, w), 5)
+    mm_tf = 2 * n ** 3 / mm_ms / 1e9
+    del x, w
+    torch.cuda.empty_cache()
+    return {"stream_copy_GBps": round(copy_gbs, 1), "f16_matmul_TFLOPs": round(mm_tf, 1),
+            "how": "torch on this GPU: copy of 1 GiB (read + write bytes), fp16 matmul 8192^3 (hipBLASLt); best of 5"}
+
+
 # ---------------------------------------------------------------- main
 
 def gemv_kernel_names(B):
@@ -899,7 +937,10 @@ def main():
     roofline.update({"lm_head_steady_us": round(lm_us, 3),
                      "lm_head_steady_GBps": round(lm_bytes / lm_us / 1e3, 1),
                      "lm_head_steady_frac": round(lm_bytes / lm_us / 1e3 / HBM_PEAK_GBS, 4)})
+    cal = calibration(torch)
+    roofline["frac_of_measured_stream_copy"] = round(achieved / cal["stream_copy_GBps"], 4)
     log(f"roofline: {roofline}")
+    log(f"calibration: {cal}")
 
     extra = {}
     if args.extra != "none":
@@ -924,6 +965,7 @@ def main():
                    "timing": "hip graph replay, HIP events",
                    "arithmetic": "Q4 codes dequantised to fp16 in registers, fp16 products, fp32 accumulation"},
         "roofline": roofline,
+        "calibration": cal,
         "cpu_baseline": cpu,
         "extra": extra,
     }
