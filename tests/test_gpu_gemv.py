@@ -65,7 +65,7 @@ def test_gemv_one_hot_x_gives_column():
 
 
 def test_gemv_deterministic_and_config0():
-    """Config 0: single Q4 GEMV 1024x1024; repeated calls are bitwise equal."""
+    """The single Q4 GEMV 1024 -> 1024: repeated calls are bitwise equal."""
     cfg = workloads.SINGLE_GEMV
     w = inputs.weights_np(inputs.seed_for(0, 0, "q"), (cfg["n"], cfg["k"]))
     x = inputs.activations_np(inputs.seed_for(0, 0, "x"), (cfg["k"],))
