@@ -288,14 +288,33 @@ def cpu_baseline(budget_s: float):
 
 
 def cpu_baseline_gemm_moe():
-    """The oracle on bounded samples of the prefill GEMM and MoE workloads
-    (reported beside the headline's baseline): one Llama-3.2-1B layer's seven
-    GEMMs at M = 128, and the Qwen3-30B-A3B MoE layer at M = 128 routed and
-    bucketed in full, with the FFNs of its first 16 experts' buckets.  The
-    oracle's own quantisation and packing is prepared untimed, as above."""
+    """The oracle on the other workloads (reported beside the headline's
+    baseline): the single 1024 x 1024 GEMV on one thread; one Llama-3.2-1B
+    layer's seven GEMMs at M = 128; the Qwen3-30B-A3B MoE layer at M = 128
+    routed and bucketed in full, with the FFNs of its first 16 experts'
+    buckets.  The oracle's own quantisation and packing is prepared untimed,
+    as above."""
     from oracle import qmatmul_oracle as O
     from paper_2607_00501_amd import inputs, workloads
     out = {}
+    # The single 1024 x 1024 Q4 GEMV on one thread (median of 5 calls).
+    q, sc = O.quantise(inputs.weights_np(inputs.seed_for(0, 0, "q"), (1024, 1024)), O.Q4)
+    qb, xv = O.pack(q, O.Q4), inputs.activations_np(inputs.seed_for(0, 0, "x"), (1024,))
+    try:
+        from threadpoolctl import threadpool_limits
+        limit = threadpool_limits(1)
+    except Exception:
+        limit = None
+    ts = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        O.gemv(qb, sc, O.Q4, xv)
+        ts.append(time.perf_counter() - t0)
+    if limit is not None:
+        limit.unregister()
+    t1 = sorted(ts)[2]
+    out["single_gemv_1024x1024_q4"] = {"value": round(workloads.q4_bytes(1024, 1024) / t1 / 1e9, 4), "unit": "GB/s",
+                                       "threads": 1, "sample": f"the whole GEMV, median of 5 calls ({t1 * 1e3:.2f} ms)"}
     m = 128
     prepared = []
     for name, k, n in workloads.LLAMA32_1B_LAYER:
