@@ -136,3 +136,19 @@ def test_gemm_bf16_weights_reach_the_mfma_as_fp16():
     small = np.abs(O.bf16_value(bits)) < 2.0 ** -14
     assert small.any() and (~small).any()
     assert np.array_equal(y.T[~small].astype(np.float64), O.bf16_value(bits)[~small].astype(np.float64))
+
+
+# F16 / BF16 weights at the Llama-3.2-1B prefill shapes (gate 2048 -> 8192 and
+# down 8192 -> 2048) at M = 512 and 2048: sampled rows and columns against the
+# oracle, every tile kind these sizes get from the plan.
+@pytest.mark.parametrize("ofmt,bfmt", [(O.F16, B.F16), (O.BF16, B.BF16)])
+@pytest.mark.parametrize("m,n,k", [(512, 8192, 2048), (2048, 2048, 8192), (512, 2048, 8192)])
+def test_gemm_float_formats_full_size_sampled(ofmt, bfmt, m, n, k):
+    w = inputs.weights_np(inputs.seed_for(3, 0, "gate" if n == 8192 else "down", ofmt), (n, k))
+    x = inputs.activations_np(inputs.seed_for(3, m, "x", ofmt), (m, k))
+    y = B.qmatmul_gemm(_device_weight(w, bfmt), torch.from_numpy(x).cuda()).cpu().numpy()
+    rng = np.random.default_rng(m + n + ofmt)
+    rows = np.unique(np.concatenate([rng.choice(m, 24, replace=False), [0, 127, 128, m - 1]]))
+    cols = np.unique(np.concatenate([rng.choice(n, 200, replace=False), [0, 63, 64, 255, 256, n - 1]]))
+    err = rel_err(y[np.ix_(rows, cols)], _ref(w[cols], x[rows], ofmt))
+    assert err <= 2e-3, err
