@@ -139,3 +139,22 @@ def test_gemv_grouped_and_swiglu(ofmt, bfmt):
     h = B.qmatmul_gemv_swiglu(wd[0], wd[0], xt).cpu().numpy()          # gate = up = W_0
     ref = O.gemv_swiglu(*refs[0], *refs[0], ofmt, x)
     assert rel_err(h, ref) <= 1e-5
+
+
+# The Llama-3.2-3B decode shapes in every format: gate/up 3072 -> 8192 (all
+# outputs) and the lm_head 3072 -> 128256 (2,048 sampled rows, the rest of
+# the matrix quantised and streamed by the kernel as in a decode step).
+@pytest.mark.parametrize("ofmt,bfmt", FMTS)
+def test_gemv_llama3b_shapes_every_format(ofmt, bfmt):
+    k = 3072
+    w = inputs.weights_np(inputs.seed_for(2, 0, "gate", ofmt), (8192, k))
+    x = inputs.activations_np(inputs.seed_for(2, 0, "x", ofmt), (k,))
+    xt = torch.from_numpy(x).cuda()
+    y = B.qmatmul_gemv(_device(w, bfmt), xt).cpu().numpy()
+    assert rel_err(y, O.gemv(*_ref(w, ofmt), ofmt, x)) <= 1e-5
+    n = 128256
+    wh = inputs.weights_dev(inputs.seed_for(2, 28, "lm_head", ofmt), (n, k))
+    yh = B.qmatmul_gemv(B.qm_repack(B.qm_quantise(wh, bfmt), B.LAYOUT_DEVICE), xt).cpu().numpy()
+    rows = np.unique(np.concatenate([np.random.default_rng(ofmt).choice(n, 2048, replace=False), [0, 63, 64, n - 1]]))
+    wr = wh[torch.from_numpy(rows).cuda()].cpu().numpy()
+    assert rel_err(yh[rows], O.gemv(*_ref(wr, ofmt), ofmt, x)) <= 1e-5
