@@ -695,6 +695,42 @@ def extra_prefill(torch, B, inputs, workloads, steps, warmup, lib):
         del wds
         torch.cuda.empty_cache()
 
+    # The prefill GEMM in every weight format: the Llama-3.2-1B gate
+    # projection 2048 -> 8192 at M = 512 and 2048, 16 distinct weight copies
+    # per graph (134 MB of F16 / BF16 weights, beyond the MALL), back to back.
+    fmts = {"q2": B.Q2_G32, "q3": B.Q3_G32, "q4": B.Q4_G32, "q5": B.Q5_G32, "q6": B.Q6_G32, "q8": B.Q8_G32,
+            "f16": B.F16, "bf16": B.BF16}
+    k, n, copies = 2048, 8192, 16
+    by_fmt = {}
+    w = inputs.weights_dev(inputs.seed_for(3, 0, "gate"), (n, k))
+    for name, fmt in fmts.items():
+        wd = B.qm_repack(B.qm_quantise(w, fmt), B.LAYOUT_DEVICE)
+        ws = [B.QWeight(wd.format, wd.layout, 1, n, k, wd.qdata.clone(),
+                        None if wd.scales is None else wd.scales.clone()) for _ in range(copies)]
+        descs = [wi.c() for wi in ws]
+        for m in (512, 2048):
+            x = inputs.activations_dev(inputs.seed_for(3, m, "x"), (m, k))
+            ys = [torch.empty((m, n), device="cuda") for _ in range(copies)]
+
+            def run_f(s, x=x, ys=ys, descs=descs, m=m):
+                for d, yv in zip(descs, ys):
+                    st = lib.qmatmul_gemm(ctypes.byref(d), ctypes.c_void_p(x.data_ptr()), m,
+                                          ctypes.c_void_p(yv.data_ptr()), s)
+                    if st:
+                        raise RuntimeError(lib.qm_last_error().decode())
+            g = capture(torch, run_f)
+            t, _ = time_graph(torch, g, reps, warmup)
+            us = t / reps / copies * 1e6
+            tf = 2.0 * m * n * k / us / 1e6
+            by_fmt[f"{name}_m{m}"] = {"us": round(us, 2), "TFLOPs": round(tf, 1),
+                                      "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4)}
+            del g, ys, x
+        del ws, descs, wd
+        torch.cuda.empty_cache()
+    del w
+    out["llama3.2-1b_gate_gemm_by_format"] = by_fmt
+    log(f"gemm by format: {by_fmt}")
+
     # Causal prefill attention of one layer (qattn_prefill): Llama-3.2-1B
     # (32 query / 8 KV heads, head_dim 64) and Qwen3-0.6B (16 / 8, head_dim
     # 128); FLOPs 2 * 2 * D * Hq * M(M+1)/2 (the causal half of Q K^T and P V).
