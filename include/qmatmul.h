@@ -196,7 +196,7 @@ qm_status qmatmul_gemv_swiglu_f16(const qm_qweight* w_gate, const qm_qweight* w_
  * qmatmul_gemv_swiglu_f16.  Both write v to x_out (fp32 [k]), the residual
  * stream for the next fused call, which must not overlap x or residual.
  * x, residual, x_out: fp32 [k], 16-byte aligned; gain: fp16 [k], 8-byte
- * aligned.  Weights: Q4 or Q8, DEVICE layout, batch 1, one k <= 4096, every
+ * aligned.  Weights: any of the eight formats (one per call), DEVICE layout, batch 1, one k <= 4096, every
  * n >= 1.  Every workgroup recomputes n into LDS from x and residual (the
  * sum of squares in fp32, in the same order in every workgroup); workgroup 0
  * writes x_out.  One launch each. */
@@ -253,7 +253,7 @@ qm_status qdec_rope_table(int64_t max_len, int32_t head_dim, float theta, float*
  * norm folded in (as qmatmul_gemv_grouped_rmsnorm) and RoPE plus the cache
  * append as the GEMV epilogue (Sec. 3.3: each fusion removes a launch).
  * w: three descriptors, q [n_q_heads * head_dim][k], k and v
- * [n_kv_heads * head_dim][k], Q4 or Q8, DEVICE layout; the rows of each
+ * [n_kv_heads * head_dim][k], one format (any of the eight), DEVICE layout; the rows of each
  * head of w[0] and w[1] are stored interleaved: stored row 2i is the head's
  * row i and stored row 2i + 1 its row i + head_dim/2 (so a rotation pair is
  * computed by neighbouring lanes).  Writes q_out (fp16 [n_q_heads][head_dim],

@@ -264,7 +264,6 @@ qm_status qmatmul_gemv_grouped_rmsnorm(int32_t count, const qm_qweight* w, const
   for (int i = 0; i < count; ++i) {
     qm_status st = check_weight(&w[i], "qmatmul_gemv_grouped_rmsnorm(w[i])");
     if (st != QM_OK) return st;
-    if (w[i].format != QM_Q4_G32 && w[i].format != QM_Q8_G32) return fail(QM_EFORMAT, "%s: Q4 or Q8 only", name);
     if (w[i].layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "%s: w[%d] must be in DEVICE layout", name, i);
     if (w[i].batch != 1) return fail(QM_ESHAPE, "%s: w[%d] batch must be 1", name, i);
     if (w[i].format != w[0].format) return fail(QM_EFORMAT, "%s: formats differ", name);
@@ -369,7 +368,6 @@ qm_status qmatmul_gemv_qkv_rmsnorm_rope(const qm_qweight* w, const float* x, con
   for (int i = 0; i < 3; ++i) {
     qm_status st = check_weight(&w[i], "qmatmul_gemv_qkv_rmsnorm_rope(w[i])");
     if (st != QM_OK) return st;
-    if (w[i].format != QM_Q4_G32 && w[i].format != QM_Q8_G32) return fail(QM_EFORMAT, "%s: Q4 or Q8 only", name);
     if (w[i].format != w[0].format) return fail(QM_EFORMAT, "%s: formats differ", name);
     if (w[i].layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "%s: w[%d] must be in DEVICE layout", name, i);
     if (w[i].batch != 1) return fail(QM_ESHAPE, "%s: w[%d] batch must be 1", name, i);
@@ -401,7 +399,6 @@ qm_status qmatmul_gemv_swiglu_rmsnorm_f16(const qm_qweight* w_gate, const qm_qwe
   qm_status st = check_weight(w_gate, "qmatmul_gemv_swiglu_rmsnorm_f16(w_gate)");
   if (st != QM_OK) return st;
   if ((st = check_weight(w_up, "qmatmul_gemv_swiglu_rmsnorm_f16(w_up)")) != QM_OK) return st;
-  if (w_gate->format != QM_Q4_G32 && w_gate->format != QM_Q8_G32) return fail(QM_EFORMAT, "%s: Q4 or Q8 only", name);
   if (w_gate->layout != QM_LAYOUT_DEVICE || w_up->layout != QM_LAYOUT_DEVICE)
     return fail(QM_ELAYOUT, "%s: weights must be in DEVICE layout", name);
   if (w_gate->batch != 1 || w_up->batch != 1) return fail(QM_ESHAPE, "%s: batch must be 1", name);

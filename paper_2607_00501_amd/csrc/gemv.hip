@@ -1139,9 +1139,7 @@ hipError_t launch_gemv_qkv_norm_rope(int32_t fmt, GemvGroup& g, const NormArgs& 
     });
   };
 
-  if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
-  if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
-  return hipErrorInvalidValue;
+  return with_format(fmt, go);
 }
 
 hipError_t launch_gemv_group_norm(int32_t fmt, GemvGroup& g, const NormArgs& na, int64_t k, int cu_count,
@@ -1169,9 +1167,7 @@ hipError_t launch_gemv_group_norm(int32_t fmt, GemvGroup& g, const NormArgs& na,
     });
   };
 
-  if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
-  if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
-  return hipErrorInvalidValue;
+  return with_format(fmt, go);
 }
 
 hipError_t launch_gemv_swiglu_norm(int32_t fmt, const uint8_t* qg, const uint16_t* sg, const uint8_t* qu,
@@ -1192,9 +1188,7 @@ hipError_t launch_gemv_swiglu_norm(int32_t fmt, const uint8_t* qg, const uint16_
     });
   };
 
-  if (fmt == QM_Q4_G32) return go(std::integral_constant<int, QM_Q4_G32>{});
-  if (fmt == QM_Q8_G32) return go(std::integral_constant<int, QM_Q8_G32>{});
-  return hipErrorInvalidValue;
+  return with_format(fmt, go);
 }
 
 hipError_t launch_gemv(int32_t fmt, const uint8_t* q, const uint16_t* s, const uint16_t* x, float* y,

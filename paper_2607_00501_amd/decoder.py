@@ -52,8 +52,8 @@ class DenseDecoder:
     quantised projections, fp16 embedding table and norm weights.
 
     fused: the two RMSNorms of a layer run inside the GEMVs that read them
-    (qmatmul_gemv_grouped_rmsnorm, qmatmul_gemv_swiglu_rmsnorm_f16; Q4/Q8
-    weights, hidden <= 4096), with the residual stream alternating between
+    (qmatmul_gemv_grouped_rmsnorm, qmatmul_gemv_swiglu_rmsnorm_f16; any
+    weight format, hidden <= 4096), with the residual stream alternating between
     two buffers; otherwise each norm is a launch of its own.
 
     rope_rows_interleaved: W_q and W_k were quantised from rows in
@@ -73,8 +73,7 @@ class DenseDecoder:
         f16 = dict(dtype=torch.float16, device=dev)
         c = cfg
         qd, kvd = c.n_q_heads * c.head_dim, c.n_kv_heads * c.head_dim
-        self.fused = fused and c.hidden <= 4096 and all(
-            w.format in (B.Q4_G32, B.Q8_G32) for ly in layers for w in (ly.wq, ly.wk, ly.wv, ly.wg, ly.wu))
+        self.fused = fused and c.hidden <= 4096
         self.x = torch.zeros(c.hidden, **f32)             # residual stream
         self.x2 = torch.zeros(c.hidden, **f32)            # its other buffer (fused norms)
         self.rope_epi = rope_rows_interleaved

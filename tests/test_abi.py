@@ -354,7 +354,10 @@ def test_fused_rmsnorm_gemv_validation():
     big = B.empty_qweight(B.Q4_G32, B.LAYOUT_DEVICE, 1, 64, 8192, device="cpu")
     assert call(d=(B.CQWeight * 1)(big.c())) == 2                  # k > 4096
     q2 = B.empty_qweight(B.Q2_G32, B.LAYOUT_DEVICE, 1, 64, 1024, device="cpu")
-    assert call(d=(B.CQWeight * 1)(q2.c())) == 4                   # Q4/Q8 only
+    two_ys = (ctypes.c_void_p * 2)(0x70000, 0x78000)
+    mixed = L.qmatmul_gemv_grouped_rmsnorm(2, (B.CQWeight * 2)(w.c(), q2.c()), p, None, p, 1e-6,
+                                           ctypes.c_void_p(0x90000), two_ys, None)
+    assert mixed == 4                                              # one format per call
     sw = lambda h=p, xo=ctypes.c_void_p(0x90000): L.qmatmul_gemv_swiglu_rmsnorm_f16(
         ctypes.byref(w.c()), ctypes.byref(w.c()), p, None, p, 1e-6, xo, h, None)
     assert sw(h=None) == 1 and sw(h=ctypes.c_void_p(0x50001)) == 3 and sw(xo=p) == 1

@@ -218,6 +218,20 @@ def test_decode_steps_teacher_forced_tiny(fused, rope_epi):
     assert torch.all(dec.k_cache[:, :, 10:] == 0) and torch.all(dec.v_cache[:, :, 10:] == 0)
 
 
+@pytest.mark.parametrize("fmts", [(O.Q3, B.Q3_G32), (O.Q6, B.Q6_G32), (O.BF16, B.BF16)])
+def test_decode_steps_fused_other_formats(fmts):
+    """Norms and RoPE fused into the GEMVs with Q3, Q6 and BF16 weights:
+    logits of four teacher-forced steps and the caches against the oracle."""
+    dec, ref, kc, vc = _decoder(TINY, 23, 8, fmts=fmts, fused=True, rope_epi=True)
+    for pos, t in enumerate([5, 999, 0, 42]):
+        dec.token.fill_(t)
+        dec.step(pos)
+        want = O.decode_step(ref, t, pos, kc, vc)
+        assert rel_err(dec.logits.cpu().numpy(), want) <= GEMV_TOL, pos
+    assert rel_err(dec.k_cache.cpu().numpy().astype(np.float64), kc) <= 2e-3
+    assert rel_err(dec.v_cache.cpu().numpy().astype(np.float64), vc) <= 2e-3
+
+
 def test_decode_steps_greedy_chain_q8_d128():
     """Greedy generation with the token kept on the device: every sampled id
     is the argmax of that step's logits, and the oracle fed the same ids
@@ -393,6 +407,30 @@ def test_gemv_qkv_rmsnorm_rope_matches_separate_launches(fmt, d, hq, hkv, k, pos
     other = torch.ones(max_len, dtype=torch.bool)
     other[pos] = False
     assert torch.equal(kc1[:, other], kc2[:, other]) and torch.equal(vc1[:, other], vc2[:, other])
+
+
+OTHER_FMTS = [(O.Q2, B.Q2_G32), (O.Q3, B.Q3_G32), (O.Q5, B.Q5_G32), (O.Q6, B.Q6_G32), (O.F16, B.F16),
+              (O.BF16, B.BF16)]
+
+
+@pytest.mark.parametrize("fmt", OTHER_FMTS)
+@pytest.mark.parametrize("k,ns", [(1024, (100, 37, 260)), (3072, (3072, 1024, 1024)), (2048, (2048, 512, 512))])
+def test_gemv_grouped_rmsnorm_other_formats(fmt, k, ns):
+    """Q2/Q3/Q5/Q6/F16/BF16 weights: the normed activation staged in LDS by
+    the same workgroups (no lane broadcast), against the oracle."""
+    test_gemv_grouped_rmsnorm_parity(fmt, k, ns, True)
+
+
+@pytest.mark.parametrize("fmt", OTHER_FMTS)
+@pytest.mark.parametrize("n,k", [(65, 96), (3072, 1024), (8192, 2048)])
+def test_gemv_swiglu_rmsnorm_other_formats(fmt, n, k):
+    test_gemv_swiglu_rmsnorm_parity(fmt, n, k)
+
+
+@pytest.mark.parametrize("fmt", [b for _, b in OTHER_FMTS])
+@pytest.mark.parametrize("d,hq,hkv,k", [(64, 4, 2, 256), (128, 24, 8, 3072)])
+def test_gemv_qkv_rmsnorm_rope_other_formats(fmt, d, hq, hkv, k):
+    test_gemv_qkv_rmsnorm_rope_matches_separate_launches(fmt, d, hq, hkv, k, 5)
 
 
 def test_rope_table_matches_the_rotation_angles():
