@@ -24,8 +24,9 @@ The line also carries
   extra:        the other workloads (single 1024x1024 GEMV hot and cold,
                 Qwen3-0.6B Q4 and Llama-3.2-3B Q8 decode stacks, Llama-3.2-1B
                 prefill GEMM stacks and the Qwen3-30B-A3B MoE layer at M = 128
-                / 512 / 2048, attention and whole-decoder lines), each timed
-                the same way (omit with --extra none).
+                / 512 / 2048 (and at M = 512 in the six quantised formats),
+                attention and whole-decoder lines), each timed the same way
+                (omit with --extra none).
 
 Run: python bench.py [--gpus 1] [--steps K] [--warmup W] [--extra all|none|...]
 """
@@ -817,6 +818,35 @@ def extra_moe(torch, B, inputs, workloads, steps, warmup, lib):
         log(f"moe m={m}: {out[f'qwen3-30b-a3b_moe_m{m}']}")
         del g
     del flush
+    # The same layer at M = 512 with the experts in the other quantised
+    # formats (graph replay; weight bytes = codes + one fp16 scale per 32).
+    del wg, wu, wdn
+    m = 512
+    x = inputs.activations_dev(inputs.seed_for(4, m, "x"), (m, H))
+    lg = inputs.logits_dev(inputs.seed_for(4, m, "logits"), (m, E))
+    r = B.qmoe_route(lg, K)
+    yv = torch.empty((m, H), device="cuda")
+    ws = torch.empty(B.qmoe_workspace_bytes(m, E, K, H, I), dtype=torch.uint8, device="cuda")
+    by_fmt = {}
+    for name, fmt, bits in (("q2", B.Q2_G32, 2), ("q3", B.Q3_G32, 3), ("q4", B.Q4_G32, 4), ("q5", B.Q5_G32, 5),
+                            ("q6", B.Q6_G32, 6), ("q8", B.Q8_G32, 8)):
+        mkf = lambda t, sh: B.qm_repack(B.qm_quantise(inputs.weights_dev(inputs.seed_for(4, 0, t), sh), fmt),
+                                        B.LAYOUT_DEVICE)
+        fg, fu, fd = mkf("gate", (E, I, H)), mkf("up", (E, I, H)), mkf("down", (E, H, I))
+        def run(s, fg=fg, fu=fu, fd=fd):
+            B.qmoe_route(lg, K, out=r, stream=_Raw(s))
+            B.qmoe_grouped_gemm(fg, fu, fd, x, r, out=yv, workspace=ws, stream=_Raw(s))
+        g = capture(torch, run)
+        n = max(steps // 2, 5)
+        t, _ = time_graph(torch, g, n, warmup)
+        fbytes = 3 * E * H * I * (bits + 0.5) / 8
+        tf = 2.0 * m * K * 3 * H * I * n / t / 1e12
+        by_fmt[name] = {"layer_us": round(t / n * 1e6, 2), "TFLOPs": round(tf, 1),
+                        "frac_mfma_peak": round(tf / MFMA_F16_PEAK_TFLOPS, 4),
+                        "weight_MB": round(fbytes / 1e6, 1), "weight_GBps": round(fbytes * n / t / 1e9, 1)}
+        del g, fg, fu, fd
+    out["qwen3-30b-a3b_moe_m512_by_format"] = by_fmt
+    log(f"moe m=512 by format: {by_fmt}")
     return out
 
 

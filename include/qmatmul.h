@@ -451,8 +451,9 @@ qm_status qmoe_route(const float* logits, int64_t m, int32_t n_experts, int32_t 
  *  [offsets[e], offsets[e+1]) of sorted_assign holds a:
  *    h_a = silu(Wg_e x_t) * (Wu_e x_t),  y_a = Wd_e h_a,
  *  y[t] = sum_j topk_w[t][j] * y_{t*top_k+j}, summed in slot order j.
- *  w_gate, w_up: DEVICE layout Q4, batch E, [E][inter][hidden];
- *  w_down: DEVICE layout Q4, batch E, [E][hidden][inter];
+ *  w_gate, w_up: DEVICE layout, batch E, [E][inter][hidden];
+ *  w_down: DEVICE layout, batch E, [E][hidden][inter]; all three in one of
+ *  Q2, Q3, Q4, Q5, Q6, Q8 (QM_EFORMAT if they differ, or for F16 / BF16);
  *  x: fp16 [m][hidden]; y: fp32 [m][hidden]; topk_ids, topk_w [m][top_k],
  *  counts, offsets and sorted_assign come from qmoe_route (sorted_assign
  *  must be a permutation of 0 .. m*top_k-1 consistent with counts/offsets).

@@ -712,7 +712,9 @@ qm_status moe_layer_call(const char* name, const qm_qweight* w_gate, const qm_qw
   if ((st = check_weight(w_down, name)) != QM_OK) return st;
   const qm_qweight* ws[3] = {w_gate, w_up, w_down};
   for (const qm_qweight* w : ws) {
-    if (w->format != QM_Q4_G32) return fail(QM_EFORMAT, "%s: experts must be Q4", name);
+    if (w->format != w_gate->format) return fail(QM_EFORMAT, "%s: gate, up and down formats differ", name);
+    if (w->format == QM_F16 || w->format == QM_BF16)
+      return fail(QM_EFORMAT, "%s: experts must be Q2, Q3, Q4, Q5, Q6 or Q8", name);
     if (w->layout != QM_LAYOUT_DEVICE) return fail(QM_ELAYOUT, "%s: experts must be in DEVICE layout", name);
   }
   const int64_t E = w_gate->batch, inter = w_gate->n, hidden = w_gate->k;
@@ -757,7 +759,7 @@ qm_status moe_layer_call(const char* name, const qm_qweight* w_gate, const qm_qw
   a.h = static_cast<uint16_t*>(workspace);
   a.yp = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + h_bytes);
   a.m = m; a.hidden = hidden; a.inter = inter;
-  a.n_experts = static_cast<int32_t>(E); a.top_k = top_k;
+  a.n_experts = static_cast<int32_t>(E); a.top_k = top_k; a.format = w_gate->format;
   return launched(launch_moe(a, d->cu_count, static_cast<hipStream_t>(stream)), name);
 }
 

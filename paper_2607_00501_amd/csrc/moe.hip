@@ -284,7 +284,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const uint16_t* __restrict
   dst[1] = make_float4(s[4], s[5], s[6], s[7]);
 }
 
-template <int BMG, int WKG, int BMD, int WKD, int WN, int DG = 2, int DD = 2, bool NT = false>
+template <int BMG, int WKG, int BMD, int WKD, int WN, int DG = 2, int DD = 2, bool NT = false, int FMT = QM_Q4_G32>
 hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
   const int64_t A = a.m * a.top_k;
   // Upper bound on the number of (expert, row tile) pairs: sum of
@@ -305,14 +305,14 @@ hipError_t launch_moe_tiles(const MoeArgs& a, hipStream_t st) {
     return dim3(static_cast<unsigned>((units + round - 1) / round * round));
   };
   g.tiles = tiles(BMG);
-  hipLaunchKernelGGL((qgemm_kernel<BMG, WN, WKG, QgMode::kMoeGateUp, DG, NT>), grid(BMG, a.inter), dim3(WN * WKG * 64), 0,
+  hipLaunchKernelGGL((qgemm_kernel<BMG, WN, WKG, QgMode::kMoeGateUp, DG, NT, FMT>), grid(BMG, a.inter), dim3(WN * WKG * 64), 0,
                      st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // down, scaled by the gate weight and scattered to the assignment slot
   g.q = a.dq; g.s = a.ds; g.q2 = nullptr; g.s2 = nullptr; g.a = a.h; g.yp = a.yp; g.N = a.hidden; g.K = a.inter;
   g.tiles = tiles(BMD);
-  hipLaunchKernelGGL((qgemm_kernel<BMD, WN, WKD, QgMode::kMoeDown, DD, NT>), grid(BMD, a.hidden), dim3(WN * WKD * 64), 0,
+  hipLaunchKernelGGL((qgemm_kernel<BMD, WN, WKD, QgMode::kMoeDown, DD, NT, FMT>), grid(BMD, a.hidden), dim3(WN * WKD * 64), 0,
                      st, g);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -398,20 +398,42 @@ hipError_t launch_moe(const MoeArgs& a, int cu_count, hipStream_t st) {
     return f;
   }();
   using P = std::array<int, 7>;
-  if (forced == P{32, 1, 32, 1, 2, 2, 0}) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2>(a, st);
-  if (forced == P{64, 1, 64, 1, 2, 2, 0}) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2>(a, st);
-  if (forced == P{32, 1, 32, 1, 2, 2, 1}) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2, true>(a, st);
-  if (forced == P{64, 1, 64, 1, 2, 2, 1}) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2, true>(a, st);
+  if (a.format == QM_Q4_G32) {
+    if (forced == P{32, 1, 32, 1, 2, 2, 0}) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2>(a, st);
+    if (forced == P{64, 1, 64, 1, 2, 2, 0}) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2>(a, st);
+    if (forced == P{32, 1, 32, 1, 2, 2, 1}) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2, true>(a, st);
+    if (forced == P{64, 1, 64, 1, 2, 2, 1}) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2, true>(a, st);
+  }
   // Per-chip tile choice by rows per expert: 32-row tiles when buckets are
   // small (decode-like prefill chunks), 64-row tiles otherwise.  While an
   // expert's rows fit one row tile, each weight panel is read by exactly one
   // workgroup: nontemporal weight loads (measured on MI355X with cold caches:
   // 132 -> 102 us at 8 rows per expert, 157 -> 143 us at 32; with several
-  // row tiles per expert they lose the L2 reuse between tiles).
+  // row tiles per expert they lose the L2 reuse between tiles).  Q2 and
+  // Q3 use the Q4 plan.  Q5, Q6 and Q8 keep their weights in registers
+  // (their LDS stages do not fit beside two workgroups' A stages), and the
+  // two-matrix gate/up tile then holds 64 rows only by spilling: their
+  // gate/up tiles stay at 32 rows.
   const int64_t rpe = a.m * a.top_k / a.n_experts;
-  if (rpe <= 24) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2, true>(a, st);
-  if (rpe <= 64) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2, true>(a, st);
-  return launch_moe_tiles<64, 1, 64, 1, 4>(a, st);
+  auto plan = [&](auto f) -> hipError_t {
+    constexpr int F = decltype(f)::value;
+    if (rpe <= 24) return launch_moe_tiles<32, 1, 32, 1, 4, 2, 2, true, F>(a, st);
+    if constexpr (F == QM_Q5_G32 || F == QM_Q6_G32 || F == QM_Q8_G32) {
+      return launch_moe_tiles<32, 1, 64, 1, 4, 2, 2, false, F>(a, st);
+    } else {
+      if (rpe <= 64) return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2, true, F>(a, st);
+      return launch_moe_tiles<64, 1, 64, 1, 4, 2, 2, false, F>(a, st);
+    }
+  };
+  switch (a.format) {
+    case QM_Q4_G32: return plan(std::integral_constant<int, QM_Q4_G32>{});
+    case QM_Q8_G32: return plan(std::integral_constant<int, QM_Q8_G32>{});
+    case QM_Q2_G32: return plan(std::integral_constant<int, QM_Q2_G32>{});
+    case QM_Q3_G32: return plan(std::integral_constant<int, QM_Q3_G32>{});
+    case QM_Q5_G32: return plan(std::integral_constant<int, QM_Q5_G32>{});
+    case QM_Q6_G32: return plan(std::integral_constant<int, QM_Q6_G32>{});
+    default: return hipErrorInvalidValue;   // F16 / BF16 experts are rejected by the API
+  }
 }
 
 }  // namespace qm

@@ -279,8 +279,7 @@ struct Cfg {
   // F16 / BF16 weights: no codes, no scales; a lane's 8 k of a substep are
   // one 16-byte quarter of its row (BF16 converted to fp16 in registers).
   static constexpr bool kFloat = FMT == QM_F16 || FMT == QM_BF16;
-  static_assert(FMT == QM_Q4_G32 || ((kQ8 || kPlanes || kFloat) && MODE == QgMode::kDense),
-                "Q2/Q3/Q5/Q6/Q8/F16/BF16 weights: dense GEMM only");
+  static_assert(FMT == QM_Q4_G32 || kQ8 || kPlanes || kFloat, "one of the eight weight formats");
   static constexpr int kChunkBytes = chunk_block_bytes(FMT);      // one group of a 64-row panel
   // B words a lane holds per group and column half: Q4 two nibble dwords,
   // Q8 four byte dwords, Q5/Q6 two nibble dwords + one high-plane dword,
@@ -429,14 +428,14 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
   // real panel.  The matrix, expert and panel bases are wavefront-uniform;
   // the lane part is a 32-bit offset.
   const int64_t panel = (cols_ok ? n_wave : mnpad - kPanel) / kPanel;
-  const int64_t mat_q = npad * (K / 2), mat_s = npad * G;   // bytes / scales of one matrix (MoE, Q4)
+  const int64_t mat_q = npad / kPanel * G * CB, mat_s = npad * G;   // bytes / scales of one matrix (MoE)
   const uint8_t* b_q[NB];
   const uint16_t* b_s[NB];
   b_q[0] = mq + expert * mat_q + panel * G * CB;
   b_s[0] = C::kFloat ? ms : ms + expert * mat_s + panel * G * kPanel;   // float weights: no scales (null)
   if constexpr (NB == 2) {
     b_q[1] = p.q2 + expert * mat_q + panel * G * CB;
-    b_s[1] = p.s2 + expert * mat_s + panel * G * kPanel;
+    b_s[1] = C::kFloat ? p.s2 : p.s2 + expert * mat_s + panel * G * kPanel;
   }
   const uint32_t bq_lane = Q8 ? (lane & 31) * 16 + (lane >> 5) * 1024 : (lane & 31) * 16 + (lane >> 5) * 8;
   const uint32_t bs_lane = lane & 31;
@@ -845,7 +844,7 @@ __device__ __forceinline__ void qgemm_body(const QgemmArgs& p) {
 // Two workgroups per CU (up to 256 VGPRs per lane) for up to 4 wavefronts
 // per workgroup, one beyond.  NT: weights and scales are read with
 // nontemporal loads (for weights each workgroup streams once and no other
-// workgroup re-reads soon).  FMT: QM_Q4_G32, or QM_Q8_G32 (dense mode).
+// workgroup re-reads soon).  FMT: any of the eight weight formats.
 template <int BM, int WN, int WK, QgMode MODE, int DEPTH = 2, bool NT = false, int FMT = QM_Q4_G32>
 __global__ __launch_bounds__(WN * WK * 64, WN * WK <= 4 ? 2 : 1) void qgemm_kernel(QgemmArgs p) {
   qg::qgemm_body<BM, WN, WK, MODE, DEPTH, NT, FMT>(p);

@@ -216,6 +216,7 @@ struct MoeArgs {
   uint16_t* yp;                            // workspace: [m*top_k][hidden] fp16
   int64_t m, hidden, inter;
   int32_t n_experts, top_k;
+  int32_t format;                          // of all three expert matrices
 };
 size_t moe_workspace_bytes(int64_t m, int32_t top_k, int64_t hidden, int64_t inter);
 // Bytes of the per-device scratch of qmoe_grouped_gemm_noalloc, and its

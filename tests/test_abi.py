@@ -116,7 +116,9 @@ def test_gemm_and_moe_validation():
     assert args(g, g, bad, need) == 2                                  # down shape mismatch
     assert args(g, g, d, need - 1) == 6                                # workspace too small
     g8 = _fake_weight(fmt=2, batch=8, n=96, k=64)
-    assert args(g8, g, d, need) == 4                                   # experts must be Q4
+    assert args(g8, g, d, need) == 4                                   # gate, up and down formats differ
+    gf, df = _fake_weight(fmt=B.F16, batch=8, n=96, k=64), _fake_weight(fmt=B.F16, batch=8, n=64, k=96)
+    assert args(gf, gf, df, need) == 4                                 # float experts are not taken
     assert args(g, g, d, need, ids=None) == 1                          # topk_ids required
     # the allocation-free variant: sizes beyond the library's scratch are
     # refused before anything touches the device

@@ -68,14 +68,15 @@ def test_route_empty():
     del logits
 
 
-def _experts(seed, e, hidden, inter):
+def _experts(seed, e, hidden, inter, fmts=(O.Q4, B.Q4_G32)):
+    ofmt, bfmt = fmts
     gw = inputs.weights_np(seed + 1, (e, inter, hidden))
     uw = inputs.weights_np(seed + 2, (e, inter, hidden))
     dw = inputs.weights_np(seed + 3, (e, hidden, inter))
-    dev = lambda w: B.qm_repack(B.qm_quantise(torch.from_numpy(w).cuda(), B.Q4_G32), B.LAYOUT_DEVICE)
+    dev = lambda w: B.qm_repack(B.qm_quantise(torch.from_numpy(w).cuda(), bfmt), B.LAYOUT_DEVICE)
     def ora(w):
-        qs = [O.quantise(w[i], O.Q4) for i in range(e)]
-        return np.stack([O.pack(q, O.Q4) for q, _ in qs]), np.stack([s for _, s in qs])
+        qs = [O.quantise(w[i], ofmt) for i in range(e)]
+        return np.stack([O.pack(q, ofmt) for q, _ in qs]), np.stack([s for _, s in qs])
     return (dev(gw), dev(uw), dev(dw)), ora(gw) + ora(uw) + ora(dw)
 
 
@@ -93,6 +94,26 @@ def test_moe_layer_parity(m, e, k, hidden, inter):
     r = _route_check(logits, k)
     y = B.qmoe_grouped_gemm(wg, wu, wd, torch.from_numpy(x).cuda(), r).cpu().numpy()
     ref, *_ = O.moe_layer(x, logits, k, *ora)
+    assert rel_err(y, ref) <= MFMA_TOL
+
+
+@pytest.mark.parametrize("fmts", [(O.Q2, B.Q2_G32), (O.Q3, B.Q3_G32), (O.Q5, B.Q5_G32), (O.Q6, B.Q6_G32),
+                                  (O.Q8, B.Q8_G32)], ids=["q2", "q3", "q5", "q6", "q8"])
+@pytest.mark.parametrize("m,e,k,hidden,inter", [
+    (40, 16, 4, 128, 96),       # ragged tiles, some experts empty
+    (100, 128, 8, 256, 192),    # ~6 rows per expert: 32-row tiles, nontemporal weights
+    (200, 32, 8, 128, 96),      # ~50 rows per expert: middle plan
+    (600, 16, 8, 128, 64),      # ~300 rows per expert: several row tiles per expert
+])
+def test_moe_layer_parity_other_formats(fmts, m, e, k, hidden, inter):
+    """Experts in Q2/Q3/Q5/Q6/Q8 through every tile plan, against the
+    oracle's layer on the same codes and scales."""
+    (wg, wu, wd), ora = _experts(2000 + m, e, hidden, inter, fmts)
+    x = inputs.activations_np(inputs.seed_for(5, m, "x"), (m, hidden))
+    logits = inputs.logits_np(inputs.seed_for(5, m, "logits"), (m, e))
+    r = _route_check(logits, k)
+    y = B.qmoe_grouped_gemm(wg, wu, wd, torch.from_numpy(x).cuda(), r).cpu().numpy()
+    ref, *_ = O.moe_layer(x, logits, k, *ora, fmt=fmts[0])
     assert rel_err(y, ref) <= MFMA_TOL
 
 
