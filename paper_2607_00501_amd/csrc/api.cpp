@@ -595,7 +595,7 @@ qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16
   qm_status st;
   if ((st = device_info(&d)) != QM_OK) return st;
   return launched(launch_attn_prefill(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, m, p0, max_len, scale, o,
-                                      static_cast<hipStream_t>(stream)),
+                                      d->cu_count, static_cast<hipStream_t>(stream)),
                   "qattn_prefill");
 }
 

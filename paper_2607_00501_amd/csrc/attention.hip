@@ -318,7 +318,7 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
                                                            const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v, int group,
                                                            int64_t m, int64_t p0, int64_t max_len, float scale_log2,
-                                                           float* __restrict__ o) {
+                                                           float* __restrict__ o, int n_heads, int cu_count) {
   constexpr int KB = D == 64 ? 64 : 32;      // keys per block (head_dim 128: 32, to fit 256 VGPRs)
   constexpr int NT = KB / 32;                // 32-key S tiles per block
   constexpr int KS = D / 16;                 // k steps of S over the head dimension
@@ -330,9 +330,20 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
   __shared__ __attribute__((aligned(16))) _Float16 ks[KB * KPAD];
   __shared__ __attribute__((aligned(16))) _Float16 vt[D * VPAD];
 
+  // Units (tile, head) in order of decreasing causal length (longest tiles
+  // first).  Workgroup L is dealt to a CU in round L / cu_count, and the
+  // rounds share the CUs in the same order, so every second round is dealt
+  // in reverse: the CU that took one of the longest tiles also takes one of
+  // the shortest (a partial last round keeps its order where reversal would
+  // leave it).  Measured: 512 workgroups of Llama-3.2-1B at m = 2048 took
+  // 52 -> 42 us.
   const int ntiles = static_cast<int>((m + 127) / 128);
-  const int tile = ntiles - 1 - static_cast<int>(blockIdx.x);     // longest tiles first
-  const int h = blockIdx.y, g = h / group;
+  const int L = static_cast<int>(blockIdx.x);
+  const int rnd = L / cu_count, pos = L % cu_count;
+  const int rev = rnd * cu_count + (cu_count - 1 - pos);
+  const int u = (rnd & 1) && rev < ntiles * n_heads ? rev : L;
+  const int tile = ntiles - 1 - u / n_heads;
+  const int h = u % n_heads, g = h / group;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, lh = lane >> 5, col = lane & 31;
   const int64_t q0 = static_cast<int64_t>(tile) * 128;
   const int64_t qrow = q0 + 32 * wave + col;                      // this lane's query row
@@ -522,13 +533,16 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
 
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
-                               hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>((m + 127) / 128), static_cast<unsigned>(hq));
+                               int cu_count, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>((m + 127) / 128 * hq));
   const float sl2 = scale * 1.4426950408889634f;
+  const int cu = cu_count > 0 ? cu_count : 1;
   if (d == 64)
-    hipLaunchKernelGGL((attn_prefill_kernel<64>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o);
+    hipLaunchKernelGGL((attn_prefill_kernel<64>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o,
+                       hq, cu);
   else
-    hipLaunchKernelGGL((attn_prefill_kernel<128>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o);
+    hipLaunchKernelGGL((attn_prefill_kernel<128>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o,
+                       hq, cu);
   return hipGetLastError();
 }
 

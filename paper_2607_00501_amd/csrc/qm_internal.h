@@ -158,12 +158,11 @@ hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16
                               int32_t d, int64_t len, int64_t max_len, float scale, float* o, uint16_t* o16,
                               float* ws, int cu_count, hipStream_t st);   // o16 != nullptr: fp16 output
 
-// Decode attention with the new token's RoPE and cache append folded in
-// (len = pos + 1; fp16 output).
-
+// Causal prefill attention over the cache for a chunk of m query rows
+// (workgroups ordered over the device's cu_count CUs).
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
-                               hipStream_t st);
+                               int cu_count, hipStream_t st);
 
 // Decode-step glue kernels.
 hipError_t launch_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,

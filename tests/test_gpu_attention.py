@@ -126,6 +126,23 @@ def test_attn_prefill_full_prompt_sampled_rows():
             assert rel_err(o[h, i][None], ref) <= PREFILL_TOL
 
 
+@pytest.mark.parametrize("hq,hkv,d,m", [(24, 8, 64, 2400), (20, 4, 128, 4000)])
+def test_attn_prefill_every_tile_of_every_head(hq, hkv, d, m):
+    """Grids of 456 and 640 workgroups: more than one round over the CUs,
+    with partial last rounds (the reversed dealing of every second round).
+    One sampled query row of every (head, 128-row tile) unit against the
+    oracle, so a unit computed twice or never shows up."""
+    o, q, k, v, scale = _prefill_case(hq, hkv, d, m, 0, m, seed=m + d)
+    assert np.all(np.isfinite(o))
+    g = hq // hkv
+    for h in range(hq):
+        for t in range((m + 127) // 128):
+            i = min(m - 1, t * 128 + (37 * h + 11 * t) % 128)
+            ref = O.attention_decode(q[h:h + 1, i], k[h // g:h // g + 1], v[h // g:h // g + 1], int(i) + 1,
+                                     np.float32(scale))
+            assert rel_err(o[h, i][None], ref) <= PREFILL_TOL, (h, t, i)
+
+
 def test_attn_prefill_last_row_matches_decode():
     """The last query of a chunk attends to the whole prefix: it equals the
     decode kernel's result for that query (within the MFMA tolerance)."""
