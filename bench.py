@@ -743,12 +743,15 @@ def extra_prefill(torch, B, inputs, workloads, steps, warmup, lib):
             kc = torch.randn((hkv, m, d), generator=g, device="cuda").half()
             vc = torch.randn((hkv, m, d), generator=g, device="cuda").half()
             o = torch.empty((hq, m, d), dtype=torch.float32, device="cuda")
+            nws = B.qattn_prefill_workspace_bytes(hq, d, m, 0)
+            aws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
 
-            def run_a(st, q=q, kc=kc, vc=vc, o=o, hq=hq, hkv=hkv, d=d, m=m):
+            def run_a(st, q=q, kc=kc, vc=vc, o=o, hq=hq, hkv=hkv, d=d, m=m, aws=aws):
                 for _ in range(10):
                     rc = lib.qattn_prefill(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(kc.data_ptr()),
                                            ctypes.c_void_p(vc.data_ptr()), hq, hkv, d, m, 0, m,
-                                           ctypes.c_float(d ** -0.5), ctypes.c_void_p(o.data_ptr()), st)
+                                           ctypes.c_float(d ** -0.5), ctypes.c_void_p(o.data_ptr()),
+                                           ctypes.c_void_p(aws.data_ptr()), aws.numel(), st)
                     if rc:
                         raise RuntimeError(lib.qm_last_error().decode())
             gr = capture(torch, run_a)
@@ -756,8 +759,39 @@ def extra_prefill(torch, B, inputs, workloads, steps, warmup, lib):
             us = t / reps / 10 * 1e6
             flops = 2.0 * 2.0 * d * hq * m * (m + 1) / 2
             att[f"{tag}_m{m}"] = {"us": round(us, 2), "TFLOPs": round(flops / us / 1e6, 1),
-                                  "frac_mfma_peak": round(flops / us / 1e6 / MFMA_F16_PEAK_TFLOPS, 4)}
+                                  "frac_mfma_peak": round(flops / us / 1e6 / MFMA_F16_PEAK_TFLOPS, 4),
+                                  "workspace_MB": round(nws / 1e6, 2)}
             del gr
+    # A prompt chunk far into the cache (Qwen3-0.6B heads, 128 rows at
+    # position 32,768): its 16 query tiles split over key ranges, against
+    # the unsplit single launch.
+    hq, hkv, d, m, p0 = 16, 8, 128, 128, 32768
+    g = torch.Generator(device="cuda").manual_seed(3)
+    q = torch.randn((hq, m, d), generator=g, device="cuda").half()
+    kc = torch.randn((hkv, p0 + m, d), generator=g, device="cuda").half()
+    vc = torch.randn((hkv, p0 + m, d), generator=g, device="cuda").half()
+    o = torch.empty((hq, m, d), dtype=torch.float32, device="cuda")
+    nws = B.qattn_prefill_workspace_bytes(hq, d, m, p0)
+    aws = torch.empty(max(nws, 16), dtype=torch.uint8, device="cuda")
+    chunk = {}
+    for mode in ("split", "unsplit"):
+        def run_c(st, mode=mode):
+            for _ in range(10):
+                wp = ctypes.c_void_p(aws.data_ptr()) if mode == "split" else None
+                rc = lib.qattn_prefill(ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(kc.data_ptr()),
+                                       ctypes.c_void_p(vc.data_ptr()), hq, hkv, d, m, p0, p0 + m,
+                                       ctypes.c_float(d ** -0.5), ctypes.c_void_p(o.data_ptr()), wp,
+                                       aws.numel() if mode == "split" else 0, st)
+                if rc:
+                    raise RuntimeError(lib.qm_last_error().decode())
+        gr = capture(torch, run_c)
+        t, _ = time_graph(torch, gr, reps, warmup)
+        us = t / reps / 10 * 1e6
+        flops = 2.0 * 2.0 * d * hq * m * (p0 + (m + 1) / 2)
+        chunk[mode] = {"us": round(us, 2), "TFLOPs": round(flops / us / 1e6, 1),
+                       "kv_GBps": round(2 * hkv * (p0 + m) * d * 2 / us / 1e3, 1)}
+        del gr
+    att["qwen3-0.6b_m128_at_32768"] = chunk
     out["prefill_attention"] = att
     log(f"prefill attention: {att}")
     return out

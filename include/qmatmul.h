@@ -324,11 +324,24 @@ qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float*
  * already); o: fp32 [n_q_heads][m][head_dim].  head_dim 64 or 128;
  * 1 <= m <= 65536; p0 + m <= max_len <= 262144; scale finite and > 0.
  * fp16 MFMA for q.k and p.v (p rounded toward zero to fp16; the sums use
- * the fp32 p), fp32 statistics and accumulation.  One launch, no
- * workspace, deterministic. */
+ * the fp32 p), fp32 statistics and accumulation.
+ * workspace (device, 16-byte aligned, or NULL): long query tiles of the
+ * causal triangle are split over key ranges whose partial sums, maxima and
+ * denominators go to the workspace and are merged by a second launch (the
+ * online-softmax merge); qattn_prefill_workspace_bytes gives the bytes of
+ * the full split plan on the current device.  A smaller workspace gives
+ * fewer splits, NULL none (one launch).  Deterministic for a given
+ * workspace size; calls sharing a workspace must not overlap. */
 qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
                         int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len, float scale,
-                        float* o, void* stream);
+                        float* o, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of qattn_prefill's workspace for its full key-split plan on the
+ * current device (0 when no tile is split): per split range of a split
+ * tile, n_q_heads x 128 rows x (head_dim + 4) floats.  Same shape limits as
+ * qattn_prefill.  (Sec. 3.4: tiled attention; the key-range split is this
+ * library's load balancing of the causal triangle.) */
+qm_status qattn_prefill_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int64_t m, int64_t p0, size_t* bytes);
 
 /* Host-only: bytes of the decode-attention workspace for n_q_heads query
  * heads of head_dim (64 or 128): per query head up to 256 slices of

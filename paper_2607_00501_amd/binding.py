@@ -33,7 +33,7 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
            "qmatmul_gemv_swiglu_rmsnorm_f16", "qdec_rope_table",
            "qmatmul_gemv_qkv_rmsnorm_rope", "qdec_embed_rows", "qdec_rope_append_rows", "qdec_heads_to_rows_f16",
-           "qdec_swiglu_f16")
+           "qdec_swiglu_f16", "qattn_prefill_workspace_bytes")
 
 
 class QmError(RuntimeError):
@@ -79,7 +79,8 @@ def lib() -> ctypes.CDLL:
             "qm_device_config": [ctypes.c_char_p, sz],
             "qattn_decode_workspace_bytes": [i32, i32, ctypes.POINTER(sz)],
             "qattn_decode": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
-            "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp],
+            "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp, sz, vp],
+            "qattn_prefill_workspace_bytes": [i32, i32, i64, i64, ctypes.POINTER(sz)],
             "qdec_embed": [vp, i64, i64, vp, vp, vp],
             "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
             "qdec_rope_table": [i64, i32, ctypes.c_float, vp, vp],
@@ -425,10 +426,22 @@ def qattn_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, 
     return out
 
 
+def qattn_prefill_workspace_bytes(n_q_heads: int, head_dim: int, m: int, p0: int) -> int:
+    b = ctypes.c_size_t()
+    _check(lib().qattn_prefill_workspace_bytes(n_q_heads, head_dim, m, p0, ctypes.byref(b)))
+    return b.value
+
+
+NO_WORKSPACE = object()   # qattn_prefill without a workspace (no key splits)
+
+
 def qattn_prefill(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, p0: int, scale: float,
-                  out: Optional[torch.Tensor] = None, stream=None):
+                  out: Optional[torch.Tensor] = None, workspace=None, stream=None):
     """q: fp16 [Hq][m][D] at positions p0..p0+m-1; k_cache, v_cache: fp16
-    [Hkv][max_len][D] -> fp32 [Hq][m][D] (causal)."""
+    [Hkv][max_len][D] -> fp32 [Hq][m][D] (causal).  workspace: a uint8
+    device tensor for the key-split partials (allocated at the full plan's
+    size when None; pass binding.NO_WORKSPACE for the single-launch,
+    unsplit form)."""
     hq, m, d = q.shape
     hkv, max_len, d2 = k_cache.shape
     assert d2 == d and v_cache.shape == k_cache.shape
@@ -436,8 +449,17 @@ def qattn_prefill(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
     assert q.is_contiguous() and k_cache.is_contiguous() and v_cache.is_contiguous()
     if out is None:
         out = torch.empty((hq, m, d), dtype=torch.float32, device=q.device)
+    assert out.dtype == torch.float32 and out.is_contiguous() and out.numel() == hq * m * d
+    if workspace is None:
+        nb = qattn_prefill_workspace_bytes(hq, d, m, p0)
+        workspace = torch.empty(max(nb, 16), dtype=torch.uint8, device=q.device)
+    if workspace is NO_WORKSPACE:
+        wp, wn = None, 0
+    else:
+        assert workspace.dtype == torch.uint8 and workspace.is_contiguous()
+        wp, wn = _ptr(workspace), workspace.numel()
     _check(lib().qattn_prefill(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, m, p0, max_len, scale,
-                               _ptr(out), _stream(stream)))
+                               _ptr(out), wp, wn, _stream(stream)))
     return out
 
 

@@ -577,9 +577,22 @@ qm_status qattn_decode_f16(const uint16_t* q, const uint16_t* k_cache, const uin
                           workspace, ws_bytes, stream, "qattn_decode_f16");
 }
 
+qm_status qattn_prefill_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int64_t m, int64_t p0, size_t* bytes) {
+  if (!bytes) return fail(QM_EINVAL, "qattn_prefill_workspace_bytes: null output pointer");
+  if (n_q_heads < 1 || n_q_heads > 1024 || (head_dim != 64 && head_dim != 128) || m < 1 || m > 65536 || p0 < 0 ||
+      p0 + m > kAttnMaxLen)
+    return fail(QM_ESHAPE, "qattn_prefill_workspace_bytes: n_q_heads in [1, 1024], head_dim 64 or 128, "
+                "1 <= m <= 65536, 0 <= p0, p0 + m <= %lld", (long long)kAttnMaxLen);
+  const DeviceInfo* d;
+  qm_status st;
+  if ((st = device_info(&d)) != QM_OK) return st;
+  *bytes = attn_prefill_plan(n_q_heads, head_dim, m, p0, d->cu_count, SIZE_MAX).ws_needed;
+  return QM_OK;
+}
+
 qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
                         int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len, float scale,
-                        float* o, void* stream) {
+                        float* o, void* workspace, size_t workspace_bytes, void* stream) {
   if (head_dim != 64 && head_dim != 128)
     return fail(QM_ESHAPE, "qattn_prefill: head_dim=%d must be 64 or 128", head_dim);
   if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads > 1024 || n_q_heads % n_kv_heads != 0)
@@ -591,11 +604,13 @@ qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16
   if (!q || !k_cache || !v_cache || !o) return fail(QM_EINVAL, "qattn_prefill: null pointer");
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(o))
     return fail(QM_EALIGN, "qattn_prefill: q, k_cache, v_cache must be 16-byte aligned, o 4-byte aligned");
+  if (workspace && !aligned16(workspace)) return fail(QM_EALIGN, "qattn_prefill: workspace must be 16-byte aligned");
   const DeviceInfo* d;
   qm_status st;
   if ((st = device_info(&d)) != QM_OK) return st;
   return launched(launch_attn_prefill(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, m, p0, max_len, scale, o,
-                                      d->cu_count, static_cast<hipStream_t>(stream)),
+                                      workspace, workspace ? workspace_bytes : 0, d->cu_count,
+                                      static_cast<hipStream_t>(stream)),
                   "qattn_prefill");
 }
 

@@ -27,6 +27,7 @@
 #include <hip/hip_fp16.h>
 
 #include <algorithm>
+#include <cfloat>
 #include <cmath>
 
 namespace qm {
@@ -318,7 +319,8 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
                                                            const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v, int group,
                                                            int64_t m, int64_t p0, int64_t max_len, float scale_log2,
-                                                           float* __restrict__ o, int n_heads, int cu_count) {
+                                                           float* __restrict__ o, int n_heads, int cu_count, int bmax,
+                                                           int64_t n_units, float* __restrict__ ws) {
   constexpr int KB = D == 64 ? 64 : 32;      // keys per block (head_dim 128: 32, to fit 256 VGPRs)
   constexpr int NT = KB / 32;                // 32-key S tiles per block
   constexpr int KS = D / 16;                 // k steps of S over the head dimension
@@ -330,31 +332,52 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
   __shared__ __attribute__((aligned(16))) _Float16 ks[KB * KPAD];
   __shared__ __attribute__((aligned(16))) _Float16 vt[D * VPAD];
 
-  // Units (tile, head) in order of decreasing causal length (longest tiles
-  // first).  Workgroup L is dealt to a CU in round L / cu_count, and the
-  // rounds share the CUs in the same order, so every second round is dealt
-  // in reverse: the CU that took one of the longest tiles also takes one of
-  // the shortest (a partial last round keeps its order where reversal would
-  // leave it).  Measured: 512 workgroups of Llama-3.2-1B at m = 2048 took
-  // 52 -> 42 us.
+  // Units (tile, key split, head), tiles in order of decreasing causal
+  // length (longest first); a tile of nb key blocks is split into
+  // ceil(nb / bmax) ranges of at most bmax blocks.  Workgroup L is dealt to a
+  // CU in round L / cu_count, and the rounds share the CUs in the same order,
+  // so every second round is dealt in reverse: the CU that took one of the
+  // longest units also takes one of the shortest (a partial last round keeps
+  // its order where reversal would leave it).  Measured: 512 workgroups of
+  // Llama-3.2-1B at m = 2048 took 52 -> 42 us.
+  // Positions and key counts fit 32 bits (max_len <= 262144, m <= 65536;
+  // units < 2^31), which keeps them out of 64-bit register pairs.
   const int ntiles = static_cast<int>((m + 127) / 128);
+  const int mi = static_cast<int>(m), p0i = static_cast<int>(p0);
   const int L = static_cast<int>(blockIdx.x);
   const int rnd = L / cu_count, pos = L % cu_count;
   const int rev = rnd * cu_count + (cu_count - 1 - pos);
-  const int u = (rnd & 1) && rev < ntiles * n_heads ? rev : L;
-  const int tile = ntiles - 1 - u / n_heads;
-  const int h = u % n_heads, g = h / group;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, lh = lane >> 5, col = lane & 31;
-  const int64_t q0 = static_cast<int64_t>(tile) * 128;
-  const int64_t qrow = q0 + 32 * wave + col;                      // this lane's query row
-  const int64_t qpos = p0 + min<int64_t>(qrow, m - 1);            // its position
-  const int64_t nkeys = p0 + min<int64_t>(q0 + 128, m);            // keys this workgroup needs
-  const int64_t wave_first = p0 + q0 + 32 * wave;                  // first query position of the wavefront
-  const int64_t wave_last = p0 + min<int64_t>(q0 + 32 * wave + 31, m - 1);
+  const int u = (rnd & 1) && rev < n_units ? rev : L;
+  int tile = ntiles - 1, nsplit = 1, cum = 0, slot = 0;           // units / split slots before the tile
+  for (; tile > 0; --tile) {
+    const int nb = (p0i + min(128 * (tile + 1), mi) + KB - 1) / KB;
+    nsplit = (nb + bmax - 1) / bmax;
+    const int nu = nsplit * n_heads;
+    if (u < cum + nu) break;
+    cum += nu;
+    slot += nsplit > 1 ? nsplit : 0;
+  }
+  if (tile == 0) nsplit = ((p0i + min(128, mi) + KB - 1) / KB + bmax - 1) / bmax;
+  const int split = (u - cum) / n_heads;
+  const int h = (u - cum) % n_heads, g = h / group;
+  // Row records of this unit's partial (split tiles only; 128 rows of D + 4
+  // floats: unnormalised sums, maximum, denominator, 2 pad).
+  float* const part =
+      nsplit > 1 ? ws + (static_cast<int64_t>(slot + split) * n_heads + h) * 128 * (D + 4) : nullptr;
+  const int lane = threadIdx.x & 63, lh = lane >> 5, col = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int q0 = tile * 128;
+  const int qrow = q0 + 32 * wave + col;                          // this lane's query row
+  const int qpos = p0i + min(qrow, mi - 1);                       // its position
+  const int nkeys = p0i + min(q0 + 128, mi);                      // keys of the tile
+  const int kb_lo = split * bmax * KB;                            // this unit's key range
+  const int kb_hi = min(nkeys, kb_lo + bmax * KB);
+  const int wave_first = p0i + q0 + 32 * wave;                    // first query position of the wavefront
+  const int wave_last = p0i + min(q0 + 32 * wave + 31, mi - 1);
 
   // Q fragments (B operand of S^T = K Q^T): query col, dims 16 s + 8 lh + 0..7.
   half8v qf[KS];
-  const uint16_t* qr = q + (static_cast<int64_t>(h) * m + min<int64_t>(qrow, m - 1)) * D;
+  const uint16_t* qr = q + (static_cast<int64_t>(h) * m + min(qrow, mi - 1)) * D;
 #pragma unroll
   for (int s = 0; s < KS; ++s) qf[s] = *reinterpret_cast<const half8v*>(qr + 16 * s + 8 * lh);
 
@@ -368,20 +391,20 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
   // Blocks past the end load clamped (valid) rows and are never used, so
   // the loads carry no branch and the register sets stay in registers.
   struct Blk { uint4 k[PER_T], v[PER_T]; };
-  auto load_block = [&](int64_t kb0) __attribute__((always_inline)) {
+  auto load_block = [&](int kb0) __attribute__((always_inline)) {
     Blk b;
 #pragma unroll
     for (int c = 0; c < PER_T; ++c) {
       const int piece = threadIdx.x + 256 * c;
       const int row = piece / (D / 8), off = (piece % (D / 8)) * 8;
-      b.k[c] = *reinterpret_cast<const uint4*>(kh + min<int64_t>(kb0 + row, nkeys - 1) * D + off);
+      b.k[c] = *reinterpret_cast<const uint4*>(kh + min(kb0 + row, nkeys - 1) * D + off);
     }
 #pragma unroll
     for (int c = 0; c < PER_T / 2; ++c) {
       const int pp = threadIdx.x + 256 * c;                      // a pair of keys, 8 dimensions
       const int kp = pp % (KB / 2), voff = (pp / (KB / 2)) * 8;
-      b.v[2 * c] = *reinterpret_cast<const uint4*>(vh + min<int64_t>(kb0 + 2 * kp, nkeys - 1) * D + voff);
-      b.v[2 * c + 1] = *reinterpret_cast<const uint4*>(vh + min<int64_t>(kb0 + 2 * kp + 1, nkeys - 1) * D + voff);
+      b.v[2 * c] = *reinterpret_cast<const uint4*>(vh + min(kb0 + 2 * kp, nkeys - 1) * D + voff);
+      b.v[2 * c + 1] = *reinterpret_cast<const uint4*>(vh + min(kb0 + 2 * kp + 1, nkeys - 1) * D + voff);
     }
     return b;
   };
@@ -413,9 +436,9 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
   for (int b = 0; b < DB; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[b][r] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
+  float m_run = -FLT_MAX, l_run = 0.0f;
 
-  auto compute = [&](int64_t kb0) __attribute__((always_inline)) {
+  auto compute = [&](int kb0) __attribute__((always_inline)) {
     if (kb0 <= wave_last) {
       // S^T for keys kb0 + 32 t + (lane's rows), query col: two independent tiles.
       float16v st[NT];
@@ -435,7 +458,7 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
       // the raw scores (scale > 0) and scaled once.
       float bm = -INFINITY;
       if (kb0 + KB - 1 > wave_first) {
-        const int lim = static_cast<int>(min<int64_t>(qpos - kb0, KB)) - 4 * lh;   // >= 0: key offset allowed
+        const int lim = min(qpos - kb0, KB) - 4 * lh;              // >= 0: key offset allowed
 #pragma unroll
         for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -451,8 +474,11 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
           for (int r = 0; r < 16; ++r) bm = fmaxf(bm, st[t][r]);
       }
       bm = fmaxf(bm, __shfl_xor(bm, 32)) * scale_log2;
+      // m_run starts at -FLT_MAX, not -inf: a row with no key yet in this
+      // unit's range (a later key split) keeps a finite maximum, so its p and
+      // alpha come out 0 instead of NaN; other rows are unchanged.
       const float m_new = fmaxf(m_run, bm);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // v_exp_f32 (0 for -inf)
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // v_exp_f32 (0 on the first block)
       float rs = 0.0f;
       half8v pf[2 * NT];
 #pragma unroll
@@ -493,14 +519,14 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
   // b + 1 (head_dim 128) are issued right after block b has gone to LDS, so
   // they land during the math.
   if constexpr (D == 64) {
-    Blk b0 = load_block(0), b1 = load_block(KB);
-    for (int64_t kb0 = 0; kb0 < nkeys; kb0 += 2 * KB) {
+    Blk b0 = load_block(kb_lo), b1 = load_block(kb_lo + KB);
+    for (int kb0 = kb_lo; kb0 < kb_hi; kb0 += 2 * KB) {
       store_block(b0);
       __syncthreads();
       b0 = load_block(kb0 + 2 * KB);
       compute(kb0);
       __syncthreads();
-      if (kb0 + KB < nkeys) {
+      if (kb0 + KB < kb_hi) {
         store_block(b1);
         __syncthreads();
         b1 = load_block(kb0 + 3 * KB);
@@ -510,8 +536,8 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
     }
   } else {
     // head_dim 128: one register set (two would not fit in 256 VGPRs).
-    Blk b0 = load_block(0);
-    for (int64_t kb0 = 0; kb0 < nkeys; kb0 += KB) {
+    Blk b0 = load_block(kb_lo);
+    for (int kb0 = kb_lo; kb0 < kb_hi; kb0 += KB) {
       store_block(b0);
       __syncthreads();
       b0 = load_block(kb0 + KB);
@@ -519,30 +545,210 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
       __syncthreads();
     }
   }
-  if (qrow < m) {
-    const float inv = 1.0f / l_run;
-    float* orow = o + (static_cast<int64_t>(h) * m + qrow) * D;
+  if (qrow < mi) {
+    if (!part) {
+      const float inv = 1.0f / l_run;
+      float* orow = o + (static_cast<int64_t>(h) * m + qrow) * D;
 #pragma unroll
-    for (int b = 0; b < DB; ++b)
+      for (int b = 0; b < DB; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) orow[32 * b + 8 * (r >> 2) + 4 * lh + (r & 3)] = acc[b][r] * inv;
+        for (int r = 0; r < 16; ++r) orow[32 * b + 8 * (r >> 2) + 4 * lh + (r & 3)] = acc[b][r] * inv;
+    } else {
+      // Partial of this key range: unnormalised sums, running maximum (base
+      // 2) and sum, in a row record of D + 4 floats (16-byte aligned), merged
+      // by attn_prefill_merge_kernel.
+      float* prow = part + (qrow - q0) * (D + 4);
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) prow[32 * b + 8 * (r >> 2) + 4 * lh + (r & 3)] = acc[b][r];
+      if (lh == 0) {
+        prow[D] = m_run;
+        prow[D + 1] = l_run;
+      }
+    }
+  }
+}
+
+// Merge of the key splits of the split tiles (one workgroup per tile and
+// head, in the kernel's tile order): for each row, M = max of the splits'
+// maxima, L = sum of l_s 2^(m_s - M), o = sum of acc_s 2^(m_s - M) / L, the
+// splits summed in order.  The per-row weights 2^(m_s - M) / L go to LDS
+// first (kMergeBatch splits at a time); then each thread accumulates four
+// dimensions of a row, the loads of a batch of splits issued before their use.
+constexpr int kMergeBatch = 8;
+
+template <int D>
+__global__ __launch_bounds__(256) void attn_prefill_merge_kernel(const float* __restrict__ ws, int64_t m, int64_t p0,
+                                                                 int n_heads, int bmax, float* __restrict__ o) {
+  constexpr int KB = D == 64 ? 64 : 32;
+  __shared__ float wgt[kMergeBatch][128];
+  __shared__ float rowm[128], rowl[128];
+  const int ntiles = static_cast<int>((m + 127) / 128);
+  const int c = static_cast<int>(blockIdx.x / n_heads), h = static_cast<int>(blockIdx.x % n_heads);
+  int tile = ntiles - 1, nsplit = 1, seen = 0;
+  int64_t slot = 0;
+  for (; tile >= 0; --tile) {
+    const int64_t nb = (p0 + min<int64_t>(128 * (tile + 1), m) + KB - 1) / KB;
+    nsplit = static_cast<int>((nb + bmax - 1) / bmax);
+    if (nsplit > 1) {
+      if (seen == c) break;
+      ++seen;
+      slot += nsplit;
+    }
+  }
+  if (tile < 0) return;                                           // (never: the grid counts split tiles)
+  const int rows = static_cast<int>(min<int64_t>(128, m - 128 * static_cast<int64_t>(tile)));
+  // Row record: D unnormalised sums, the maximum, the denominator, 2 pad floats.
+  auto stat = [&](int sp, int r) { return ws + (((slot + sp) * n_heads + h) * 128 + r) * (D + 4) + D; };
+  // Per row: the maximum over the splits, then the denominator.
+  const int tid = threadIdx.x;
+  if (tid < rows) {
+    float mx = -FLT_MAX;
+    for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
+      float mv[kMergeBatch];
+#pragma unroll
+      for (int j = 0; j < kMergeBatch; ++j) mv[j] = s0 + j < nsplit ? stat(s0 + j, tid)[0] : -FLT_MAX;
+#pragma unroll
+      for (int j = 0; j < kMergeBatch; ++j) mx = fmaxf(mx, mv[j]);
+    }
+    float l = 0.0f;
+    for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
+      float mv[kMergeBatch], lv[kMergeBatch];
+#pragma unroll
+      for (int j = 0; j < kMergeBatch; ++j) {
+        mv[j] = s0 + j < nsplit ? stat(s0 + j, tid)[0] : -FLT_MAX;
+        lv[j] = s0 + j < nsplit ? stat(s0 + j, tid)[1] : 0.0f;
+      }
+#pragma unroll
+      for (int j = 0; j < kMergeBatch; ++j) l = fmaf(lv[j], exp2f(mv[j] - mx), l);
+    }
+    rowm[tid] = mx;
+    rowl[tid] = 1.0f / l;
+  }
+  // Outputs: thread t takes dimensions 4 (t % (D/4)) .. + 3 of rows t / (D/4), + 256 / (D/4), ...
+  constexpr int TPR = D / 4;                                      // threads per row
+  constexpr int RPP = 256 / TPR;                                  // rows per pass
+  const int d4 = tid % TPR;
+  float4 acc[128 / RPP];
+#pragma unroll
+  for (int i = 0; i < 128 / RPP; ++i) acc[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
+    __syncthreads();                                              // rowm ready / previous weights consumed
+    for (int e = tid; e < kMergeBatch * 128; e += 256) {
+      const int j = e / 128, r = e % 128;
+      wgt[j][r] = s0 + j < nsplit && r < rows ? exp2f(stat(s0 + j, r)[0] - rowm[r]) * rowl[r] : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 128 / RPP; ++i) {
+      const int r = i * RPP + tid / TPR;
+      float4 v[kMergeBatch];
+#pragma unroll
+      for (int j = 0; j < kMergeBatch; ++j) {
+        const int sp = min(s0 + j, nsplit - 1), rc = min(r, rows - 1);
+        v[j] = reinterpret_cast<const float4*>(ws + (((slot + sp) * n_heads + h) * 128 + rc) * (D + 4))[d4];
+      }
+#pragma unroll
+      for (int j = 0; j < kMergeBatch; ++j) {
+        const float w = wgt[j][min(r, 127)];
+        acc[i].x = fmaf(w, v[j].x, acc[i].x);
+        acc[i].y = fmaf(w, v[j].y, acc[i].y);
+        acc[i].z = fmaf(w, v[j].z, acc[i].z);
+        acc[i].w = fmaf(w, v[j].w, acc[i].w);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 128 / RPP; ++i) {
+    const int r = i * RPP + tid / TPR;
+    if (r < rows)
+      reinterpret_cast<float4*>(o + (static_cast<int64_t>(h) * m + 128 * static_cast<int64_t>(tile) + r) * D)[d4] =
+          acc[i];
   }
 }
 
 }  // namespace
 
+// Key splits of the prefill attention: the blocks of all (tile, head) units
+// spread over about two workgroups per CU, at least kPrefillMinSplitBlocks
+// blocks per split; then the smallest split length whose partials fit the
+// workspace (the slots needed fall as the length grows; no workspace: no
+// split).  Tiles are split only when the longest is at least three such
+// lengths: measured on MI355X, a prompt from position 0 (whose tiles the
+// dealing order already balances) gained at most 4% from splits and lost up
+// to 30% at m = 512 / 2048 to the partials' traffic and the merge launch,
+// while a chunk far into the cache (a few tiles, thousands of key blocks
+// each) runs on a handful of CUs without them.
+PrefillPlan attn_prefill_plan(int32_t hq, int32_t d, int64_t m, int64_t p0, int cu_count, size_t ws_bytes) {
+  PrefillPlan p{};
+  const int kb = d == 64 ? 64 : 32;
+  const int64_t ntiles = (m + 127) / 128;
+  auto blocks = [&](int64_t t) { return (p0 + std::min<int64_t>(128 * (t + 1), m) + kb - 1) / kb; };
+  int64_t total = 0, longest = 0;
+  for (int64_t t = 0; t < ntiles; ++t) {
+    total += blocks(t);
+    longest = std::max(longest, blocks(t));
+  }
+  total *= hq;
+  const int64_t target = 2 * static_cast<int64_t>(std::max(cu_count, 1));
+  int64_t bmax = std::max<int64_t>(kPrefillMinSplitBlocks, (total + target - 1) / target);
+  if (longest < 3 * bmax) bmax = longest;               // no split
+  auto slots = [&](int64_t bm) {
+    int64_t sl = 0;
+    for (int64_t t = 0; t < ntiles; ++t) {
+      const int64_t s = (blocks(t) + bm - 1) / bm;
+      sl += s > 1 ? s : 0;
+    }
+    return sl;
+  };
+  const size_t slot_bytes = static_cast<size_t>(hq) * 128 * (d + 4) * sizeof(float);
+  p.ws_needed = static_cast<size_t>(slots(bmax)) * slot_bytes;
+  auto fits = [&](int64_t bm) { return static_cast<size_t>(slots(bm)) * slot_bytes <= ws_bytes; };
+  if (bmax >= longest || !fits(bmax)) {
+    int64_t lo = bmax, hi = longest;                    // !fits(lo) or lo >= longest; fits(longest): no slots
+    if (lo >= hi) {
+      bmax = longest;
+    } else {
+      while (hi - lo > 1) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        (fits(mid) ? hi : lo) = mid;
+      }
+      bmax = hi;
+    }
+  }
+  p.bmax = static_cast<int>(std::max<int64_t>(bmax, 1));
+  p.units = 0;
+  p.split_tiles = 0;
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int64_t s = (blocks(t) + p.bmax - 1) / p.bmax;
+    p.units += s * hq;
+    p.split_tiles += s > 1 ? 1 : 0;
+  }
+  return p;
+}
+
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
-                               int cu_count, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>((m + 127) / 128 * hq));
+                               void* ws, size_t ws_bytes, int cu_count, hipStream_t st) {
+  const PrefillPlan p = attn_prefill_plan(hq, d, m, p0, cu_count, ws ? ws_bytes : 0);
+  const dim3 grid(static_cast<unsigned>(p.units));
   const float sl2 = scale * 1.4426950408889634f;
   const int cu = cu_count > 0 ? cu_count : 1;
+  float* wsf = static_cast<float*>(ws);
   if (d == 64)
     hipLaunchKernelGGL((attn_prefill_kernel<64>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o,
-                       hq, cu);
+                       hq, cu, p.bmax, p.units, wsf);
   else
     hipLaunchKernelGGL((attn_prefill_kernel<128>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o,
-                       hq, cu);
+                       hq, cu, p.bmax, p.units, wsf);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.split_tiles == 0) return e;
+  const dim3 mg(static_cast<unsigned>(p.split_tiles * hq));
+  if (d == 64)
+    hipLaunchKernelGGL((attn_prefill_merge_kernel<64>), mg, dim3(256), 0, st, wsf, m, p0, hq, p.bmax, o);
+  else
+    hipLaunchKernelGGL((attn_prefill_merge_kernel<128>), mg, dim3(256), 0, st, wsf, m, p0, hq, p.bmax, o);
   return hipGetLastError();
 }
 

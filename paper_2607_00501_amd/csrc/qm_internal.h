@@ -159,10 +159,19 @@ hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16
                               float* ws, int cu_count, hipStream_t st);   // o16 != nullptr: fp16 output
 
 // Causal prefill attention over the cache for a chunk of m query rows
-// (workgroups ordered over the device's cu_count CUs).
+// (workgroups ordered over the device's cu_count CUs; long tiles split over
+// key ranges when the workspace holds their partials).
+constexpr int64_t kPrefillMinSplitBlocks = 8;
+struct PrefillPlan {
+  int bmax;            // key blocks per split
+  int64_t units;       // workgroups of the attention kernel
+  int64_t split_tiles; // tiles with more than one split (merge workgroups / heads)
+  size_t ws_needed;    // workspace bytes of the unconstrained plan
+};
+PrefillPlan attn_prefill_plan(int32_t hq, int32_t d, int64_t m, int64_t p0, int cu_count, size_t ws_bytes);
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
-                               int cu_count, hipStream_t st);
+                               void* ws, size_t ws_bytes, int cu_count, hipStream_t st);
 
 // Decode-step glue kernels.
 hipError_t launch_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,

@@ -161,11 +161,16 @@ class DenseDecoder:
             dev = self.emb.device
             self._chunk = {n: torch.empty(self.max_chunk * sh[0], dtype=dt, device=dev)
                            for n, (sh, dt) in shapes.items()}
+            # Key-split partials of the prefill attention, sized for a full
+            # chunk at position 0 (the deepest causal triangle); other chunks
+            # split within it.
+            nb = B.qattn_prefill_workspace_bytes(c.n_q_heads, c.head_dim, self.max_chunk, 0)
+            self._chunk["attn_ws"] = torch.empty(max(nb, 16), dtype=torch.uint8, device=dev)
         b = self._chunk
         rows = lambda n: b[n][:m * shapes[n][0][0]].view(m, shapes[n][0][0])
         heads = lambda n: b[n][:m * qd].view(c.n_q_heads, m, c.head_dim)
         out = {n: rows(n) for n in shapes if n not in ("qh", "o")}
-        out.update(qh=heads("qh"), o=heads("o"))
+        out.update(qh=heads("qh"), o=heads("o"), attn_ws=b["attn_ws"])
         return out
 
     def prefill(self, tokens: torch.Tensor, p0: int = 0, stream=None) -> None:
@@ -187,7 +192,8 @@ class DenseDecoder:
             qh = B.qdec_rope_append_rows(q, k, v, p0, c.theta, self.k_cache[li], self.v_cache[li],
                                          interleaved=self.rope_epi, q_out=b["qh"], q_norm=ly.q_norm,
                                          k_norm=ly.k_norm, eps=c.eps, stream=s)
-            o = B.qattn_prefill(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, out=b["o"], stream=s)
+            o = B.qattn_prefill(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, out=b["o"],
+                                workspace=b["attn_ws"], stream=s)
             ya = B.qmatmul_gemm(ly.wo, B.qdec_heads_to_rows_f16(o, out=b["o16"], stream=s), out=b["ya"], stream=s)
             h = B.qdec_rmsnorm(x, ly.ffn_norm, c.eps, residual=ya, out=b["h"], stream=s)
             g, u = B.qmatmul_gemm_grouped([ly.wg, ly.wu], h, outs=[b["g"], b["u"]], stream=s)

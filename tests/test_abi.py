@@ -280,8 +280,8 @@ def test_attention_decode_validation():
 def test_attention_prefill_validation():
     L = B.lib()
     p = ctypes.c_void_p(0x50000)
-    call = lambda hq=32, hkv=8, d=64, m=128, p0=0, mx=4096, scale=0.125, q=p, o=p: \
-        L.qattn_prefill(q, p, p, hq, hkv, d, m, p0, mx, scale, o, None)
+    call = lambda hq=32, hkv=8, d=64, m=128, p0=0, mx=4096, scale=0.125, q=p, o=p, w=None: \
+        L.qattn_prefill(q, p, p, hq, hkv, d, m, p0, mx, scale, o, w, 1 << 20, None)
     assert call(d=80) == 2
     assert call(hq=12, hkv=8) == 2
     assert call(m=0) == 2 and call(m=70000, mx=200000) == 2
@@ -289,6 +289,11 @@ def test_attention_prefill_validation():
     assert call(p0=-1) == 2
     assert call(scale=float("nan")) == 1 and call(scale=-0.5) == 1 and call(scale=0.0) == 1
     assert call(o=None) == 1
+    assert call(w=ctypes.c_void_p(0x60008)) == 3                     # workspace alignment
+    nb = ctypes.c_size_t()
+    assert L.qattn_prefill_workspace_bytes(32, 80, 128, 0, ctypes.byref(nb)) == 2
+    assert L.qattn_prefill_workspace_bytes(32, 64, 0, 0, ctypes.byref(nb)) == 2
+    assert L.qattn_prefill_workspace_bytes(32, 64, 128, 0, None) == 1
     assert call(q=ctypes.c_void_p(0x50004)) == 3
     assert B.qm_last_error()
 

@@ -143,6 +143,60 @@ def test_attn_prefill_every_tile_of_every_head(hq, hkv, d, m):
             assert rel_err(o[h, i][None], ref) <= PREFILL_TOL, (h, t, i)
 
 
+@pytest.mark.parametrize("hq,hkv,d,m,p0", [(16, 8, 128, 1000, 0), (8, 2, 64, 300, 20000), (12, 4, 128, 700, 300)])
+def test_attn_prefill_key_splits(hq, hkv, d, m, p0):
+    """Long tiles split over key ranges (full workspace), fewer splits (a
+    third of it) and none (no workspace): each against the oracle, each
+    repeatable bit for bit."""
+    max_len = p0 + m
+    rng = np.random.default_rng(m + d)
+    q = rng.standard_normal((hq, m, d)).astype(np.float16)
+    k = rng.standard_normal((hkv, max_len, d)).astype(np.float16)
+    v = rng.standard_normal((hkv, max_len, d)).astype(np.float16)
+    scale = 1.0 / math.sqrt(d)
+    qd, kd, vd = (torch.from_numpy(a).cuda() for a in (q, k, v))
+    need = B.qattn_prefill_workspace_bytes(hq, d, m, p0)
+    assert need > 0                                       # these shapes split on a 256-CU part
+    ref = O.attention_prefill(q, k, v, np.float32(scale), p0=p0)
+    outs = []
+    for ws in (torch.empty(need, dtype=torch.uint8, device="cuda"),
+               torch.empty(need // 3 // 16 * 16, dtype=torch.uint8, device="cuda"), B.NO_WORKSPACE):
+        o1 = B.qattn_prefill(qd, kd, vd, p0, scale, workspace=ws).cpu().numpy()
+        o2 = B.qattn_prefill(qd, kd, vd, p0, scale, workspace=ws).cpu().numpy()
+        assert np.array_equal(o1, o2)
+        assert np.all(np.isfinite(o1))
+        assert rel_err(o1, ref) <= PREFILL_TOL
+        outs.append(o1)
+    # Each split rounds its p to fp16 (toward zero, 2^-10 relative) against
+    # its own running maximum, so the plans differ at that rounding: two
+    # independent 2^-10 perturbations of the weights of an average.
+    assert rel_err(outs[0], outs[2].astype(np.float64)) <= 2.0 ** -9
+    assert rel_err(outs[1], outs[2].astype(np.float64)) <= 2.0 ** -9
+
+
+def test_attn_prefill_chunk_far_into_cache():
+    """A 128-row chunk at position 100,000 (one query tile per head, split
+    over key ranges): sampled rows against the oracle's decode attention over
+    each row's prefix, and the unsplit form within the p rounding."""
+    hq, hkv, d, m, p0 = 16, 8, 128, 128, 100_000
+    max_len = p0 + m
+    g = torch.Generator(device="cuda").manual_seed(7)
+    q = torch.randn((hq, m, d), generator=g, device="cuda").half()
+    k = torch.randn((hkv, max_len, d), generator=g, device="cuda").half()
+    v = torch.randn((hkv, max_len, d), generator=g, device="cuda").half()
+    scale = 1.0 / math.sqrt(d)
+    assert B.qattn_prefill_workspace_bytes(hq, d, m, p0) > 0
+    o = B.qattn_prefill(q, k, v, p0, scale).cpu().numpy()
+    o_none = B.qattn_prefill(q, k, v, p0, scale, workspace=B.NO_WORKSPACE).cpu().numpy()
+    assert rel_err(o, o_none.astype(np.float64)) <= 2.0 ** -9
+    qn, kn, vn = q.cpu().numpy(), k.cpu().numpy(), v.cpu().numpy()
+    for h in (0, 7, 15):
+        for i in (0, 1, 63, 127):
+            ref = O.attention_decode(qn[h:h + 1, i], kn[h // 2:h // 2 + 1], vn[h // 2:h // 2 + 1], p0 + i + 1,
+                                     np.float32(scale))
+            assert rel_err(o[h, i][None], ref) <= PREFILL_TOL, (h, i)
+
+
 def test_attn_prefill_last_row_matches_decode():
     """The last query of a chunk attends to the whole prefix: it equals the
     decode kernel's result for that query (within the MFMA tolerance)."""
