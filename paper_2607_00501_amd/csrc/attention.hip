@@ -570,22 +570,24 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
   }
 }
 
-// Merge of the key splits of the split tiles (one workgroup per tile and
-// head, in the kernel's tile order): for each row, M = max of the splits'
-// maxima, L = sum of l_s 2^(m_s - M), o = sum of acc_s 2^(m_s - M) / L, the
-// splits summed in order.  The per-row weights 2^(m_s - M) / L go to LDS
-// first (kMergeBatch splits at a time); then each thread accumulates four
-// dimensions of a row, the loads of a batch of splits issued before their use.
+// Merge of the key splits of the split tiles: for each row, M = max of the
+// splits' maxima, L = sum of l_s 2^(m_s - M), o = sum of acc_s 2^(m_s - M) / L,
+// the splits summed in order.  Workgroup = (split tile, head, group of
+// 256 / (D/4) rows); thread = (row, 4 dimensions); the loads of kMergeBatch
+// splits are issued before their use.
 constexpr int kMergeBatch = 8;
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_prefill_merge_kernel(const float* __restrict__ ws, int64_t m, int64_t p0,
                                                                  int n_heads, int bmax, float* __restrict__ o) {
   constexpr int KB = D == 64 ? 64 : 32;
-  __shared__ float wgt[kMergeBatch][128];
-  __shared__ float rowm[128], rowl[128];
+  constexpr int C4 = D / 4;                                       // threads per row
+  constexpr int RW = 256 / C4;                                    // rows per workgroup
+  constexpr int GROUPS = 128 / RW;
   const int ntiles = static_cast<int>((m + 127) / 128);
-  const int c = static_cast<int>(blockIdx.x / n_heads), h = static_cast<int>(blockIdx.x % n_heads);
+  const int gi = static_cast<int>(blockIdx.x % GROUPS);
+  const int rest = static_cast<int>(blockIdx.x / GROUPS);
+  const int c = rest / n_heads, h = rest % n_heads;
   int tile = ntiles - 1, nsplit = 1, seen = 0;
   int64_t slot = 0;
   for (; tile >= 0; --tile) {
@@ -599,73 +601,43 @@ __global__ __launch_bounds__(256) void attn_prefill_merge_kernel(const float* __
   }
   if (tile < 0) return;                                           // (never: the grid counts split tiles)
   const int rows = static_cast<int>(min<int64_t>(128, m - 128 * static_cast<int64_t>(tile)));
-  // Row record: D unnormalised sums, the maximum, the denominator, 2 pad floats.
-  auto stat = [&](int sp, int r) { return ws + (((slot + sp) * n_heads + h) * 128 + r) * (D + 4) + D; };
-  // Per row: the maximum over the splits, then the denominator.
-  const int tid = threadIdx.x;
-  if (tid < rows) {
-    float mx = -FLT_MAX;
-    for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
-      float mv[kMergeBatch];
-#pragma unroll
-      for (int j = 0; j < kMergeBatch; ++j) mv[j] = s0 + j < nsplit ? stat(s0 + j, tid)[0] : -FLT_MAX;
-#pragma unroll
-      for (int j = 0; j < kMergeBatch; ++j) mx = fmaxf(mx, mv[j]);
-    }
-    float l = 0.0f;
-    for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
-      float mv[kMergeBatch], lv[kMergeBatch];
-#pragma unroll
-      for (int j = 0; j < kMergeBatch; ++j) {
-        mv[j] = s0 + j < nsplit ? stat(s0 + j, tid)[0] : -FLT_MAX;
-        lv[j] = s0 + j < nsplit ? stat(s0 + j, tid)[1] : 0.0f;
-      }
-#pragma unroll
-      for (int j = 0; j < kMergeBatch; ++j) l = fmaf(lv[j], exp2f(mv[j] - mx), l);
-    }
-    rowm[tid] = mx;
-    rowl[tid] = 1.0f / l;
-  }
-  // Outputs: thread t takes dimensions 4 (t % (D/4)) .. + 3 of rows t / (D/4), + 256 / (D/4), ...
-  constexpr int TPR = D / 4;                                      // threads per row
-  constexpr int RPP = 256 / TPR;                                  // rows per pass
-  const int d4 = tid % TPR;
-  float4 acc[128 / RPP];
-#pragma unroll
-  for (int i = 0; i < 128 / RPP; ++i) acc[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  const int r = gi * RW + static_cast<int>(threadIdx.x) / C4, d4 = static_cast<int>(threadIdx.x) % C4;
+  if (r >= rows) return;                                          // (no barriers below)
+  // Record of row r in split sp: D sums, maximum, denominator, 2 pad floats.
+  auto rec = [&](int sp) { return ws + (((slot + sp) * n_heads + h) * 128 + r) * (D + 4); };
+  float mx = -FLT_MAX;
   for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
-    __syncthreads();                                              // rowm ready / previous weights consumed
-    for (int e = tid; e < kMergeBatch * 128; e += 256) {
-      const int j = e / 128, r = e % 128;
-      wgt[j][r] = s0 + j < nsplit && r < rows ? exp2f(stat(s0 + j, r)[0] - rowm[r]) * rowl[r] : 0.0f;
+    float mv[kMergeBatch];
+#pragma unroll
+    for (int j = 0; j < kMergeBatch; ++j) mv[j] = rec(min(s0 + j, nsplit - 1))[D];
+#pragma unroll
+    for (int j = 0; j < kMergeBatch; ++j) mx = fmaxf(mx, mv[j]);   // clamped duplicates change no maximum
+  }
+  float l = 0.0f;
+  float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
+    float mv[kMergeBatch], lv[kMergeBatch];
+    float4 av[kMergeBatch];
+#pragma unroll
+    for (int j = 0; j < kMergeBatch; ++j) {
+      const float* p = rec(min(s0 + j, nsplit - 1));
+      mv[j] = p[D];
+      lv[j] = p[D + 1];
+      av[j] = reinterpret_cast<const float4*>(p)[d4];
     }
-    __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 128 / RPP; ++i) {
-      const int r = i * RPP + tid / TPR;
-      float4 v[kMergeBatch];
-#pragma unroll
-      for (int j = 0; j < kMergeBatch; ++j) {
-        const int sp = min(s0 + j, nsplit - 1), rc = min(r, rows - 1);
-        v[j] = reinterpret_cast<const float4*>(ws + (((slot + sp) * n_heads + h) * 128 + rc) * (D + 4))[d4];
-      }
-#pragma unroll
-      for (int j = 0; j < kMergeBatch; ++j) {
-        const float w = wgt[j][min(r, 127)];
-        acc[i].x = fmaf(w, v[j].x, acc[i].x);
-        acc[i].y = fmaf(w, v[j].y, acc[i].y);
-        acc[i].z = fmaf(w, v[j].z, acc[i].z);
-        acc[i].w = fmaf(w, v[j].w, acc[i].w);
-      }
+    for (int j = 0; j < kMergeBatch; ++j) {
+      const float w = s0 + j < nsplit ? exp2f(mv[j] - mx) : 0.0f;
+      l = fmaf(lv[j], w, l);
+      a.x = fmaf(w, av[j].x, a.x);
+      a.y = fmaf(w, av[j].y, a.y);
+      a.z = fmaf(w, av[j].z, a.z);
+      a.w = fmaf(w, av[j].w, a.w);
     }
   }
-#pragma unroll
-  for (int i = 0; i < 128 / RPP; ++i) {
-    const int r = i * RPP + tid / TPR;
-    if (r < rows)
-      reinterpret_cast<float4*>(o + (static_cast<int64_t>(h) * m + 128 * static_cast<int64_t>(tile) + r) * D)[d4] =
-          acc[i];
-  }
+  const float inv = 1.0f / l;
+  reinterpret_cast<float4*>(o + (static_cast<int64_t>(h) * m + 128 * static_cast<int64_t>(tile) + r) * D)[d4] =
+      make_float4(a.x * inv, a.y * inv, a.z * inv, a.w * inv);
 }
 
 }  // namespace
@@ -744,7 +716,7 @@ hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint1
                        hq, cu, p.bmax, p.units, wsf);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.split_tiles == 0) return e;
-  const dim3 mg(static_cast<unsigned>(p.split_tiles * hq));
+  const dim3 mg(static_cast<unsigned>(p.split_tiles * hq * (128 / (256 / (d / 4)))));
   if (d == 64)
     hipLaunchKernelGGL((attn_prefill_merge_kernel<64>), mg, dim3(256), 0, st, wsf, m, p0, hq, p.bmax, o);
   else
