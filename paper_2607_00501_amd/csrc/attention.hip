@@ -572,7 +572,8 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
 
 // Merge of the key splits of the split tiles: for each row, M = max of the
 // splits' maxima, L = sum of l_s 2^(m_s - M), o = sum of acc_s 2^(m_s - M) / L,
-// the splits summed in order.  Workgroup = (split tile, head, group of
+// the splits taken in order (in batches, each rescaling the sums so far to
+// the batch's new maximum).  Workgroup = (split tile, head, group of
 // 256 / (D/4) rows); thread = (row, 4 dimensions); the loads of kMergeBatch
 // splits are issued before their use.
 constexpr int kMergeBatch = 8;
@@ -605,15 +606,9 @@ __global__ __launch_bounds__(256) void attn_prefill_merge_kernel(const float* __
   if (r >= rows) return;                                          // (no barriers below)
   // Record of row r in split sp: D sums, maximum, denominator, 2 pad floats.
   auto rec = [&](int sp) { return ws + (((slot + sp) * n_heads + h) * 128 + r) * (D + 4); };
-  float mx = -FLT_MAX;
-  for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
-    float mv[kMergeBatch];
-#pragma unroll
-    for (int j = 0; j < kMergeBatch; ++j) mv[j] = rec(min(s0 + j, nsplit - 1))[D];
-#pragma unroll
-    for (int j = 0; j < kMergeBatch; ++j) mx = fmaxf(mx, mv[j]);   // clamped duplicates change no maximum
-  }
-  float l = 0.0f;
+  // One pass: the running maximum moves per batch and rescales what is
+  // summed so far, as online softmax does (one memory round trip per batch).
+  float mx = -FLT_MAX, l = 0.0f;
   float4 a = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
   for (int s0 = 0; s0 < nsplit; s0 += kMergeBatch) {
     float mv[kMergeBatch], lv[kMergeBatch];
@@ -625,6 +620,13 @@ __global__ __launch_bounds__(256) void attn_prefill_merge_kernel(const float* __
       lv[j] = p[D + 1];
       av[j] = reinterpret_cast<const float4*>(p)[d4];
     }
+    float bm = mx;
+#pragma unroll
+    for (int j = 0; j < kMergeBatch; ++j) bm = fmaxf(bm, mv[j]);    // clamped duplicates change no maximum
+    const float sc = exp2f(mx - bm);
+    mx = bm;
+    l *= sc;
+    a.x *= sc; a.y *= sc; a.z *= sc; a.w *= sc;
 #pragma unroll
     for (int j = 0; j < kMergeBatch; ++j) {
       const float w = s0 + j < nsplit ? exp2f(mv[j] - mx) : 0.0f;
