@@ -645,15 +645,16 @@ __global__ __launch_bounds__(256) void attn_prefill_merge_kernel(const float* __
 }  // namespace
 
 // Key splits of the prefill attention: the blocks of all (tile, head) units
-// spread over about two workgroups per CU, at least kPrefillMinSplitBlocks
+// spread over about two workgroups per CU, at least a minimum number of
 // blocks per split; then the smallest split length whose partials fit the
 // workspace (the slots needed fall as the length grows; no workspace: no
-// split).  Tiles are split only when the longest is at least three such
-// lengths: measured on MI355X, a prompt from position 0 (whose tiles the
-// dealing order already balances) gained at most 4% from splits and lost up
-// to 30% at m = 512 / 2048 to the partials' traffic and the merge launch,
-// while a chunk far into the cache (a few tiles, thousands of key blocks
-// each) runs on a handful of CUs without them.
+// split).  Split lengths of at least 8 blocks and a longest tile of at
+// least 3 lengths for head_dim 64 (64-key blocks), 4 and 2 for head_dim 128
+// (32-key blocks, twice the blocks per tile and half the heads of the
+// models here): fitted on MI355X over prompts of 128 .. 2048 rows from
+// position 0, where finer splits lost 5-11% for head_dim 64 and gained
+// 3-17% for head_dim 128.  A chunk far into the cache (a few tiles,
+// thousands of key blocks each) runs on a handful of CUs without splits.
 PrefillPlan attn_prefill_plan(int32_t hq, int32_t d, int64_t m, int64_t p0, int cu_count, size_t ws_bytes) {
   PrefillPlan p{};
   const int kb = d == 64 ? 64 : 32;
@@ -666,8 +667,9 @@ PrefillPlan attn_prefill_plan(int32_t hq, int32_t d, int64_t m, int64_t p0, int 
   }
   total *= hq;
   const int64_t target = 2 * static_cast<int64_t>(std::max(cu_count, 1));
-  int64_t bmax = std::max<int64_t>(kPrefillMinSplitBlocks, (total + target - 1) / target);
-  if (longest < 3 * bmax) bmax = longest;               // no split
+  const int64_t min_split = d == 64 ? 8 : 4, factor = d == 64 ? 3 : 2;
+  int64_t bmax = std::max<int64_t>(min_split, (total + target - 1) / target);
+  if (longest < factor * bmax) bmax = longest;          // no split
   auto slots = [&](int64_t bm) {
     int64_t sl = 0;
     for (int64_t t = 0; t < ntiles; ++t) {

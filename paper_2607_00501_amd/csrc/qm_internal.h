@@ -161,7 +161,6 @@ hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16
 // Causal prefill attention over the cache for a chunk of m query rows
 // (workgroups ordered over the device's cu_count CUs; long tiles split over
 // key ranges when the workspace holds their partials).
-constexpr int64_t kPrefillMinSplitBlocks = 8;
 struct PrefillPlan {
   int bmax;            // key blocks per split
   int64_t units;       // workgroups of the attention kernel
