@@ -25,15 +25,20 @@ hipError_t launch_tile(const QgemmArgs& a, hipStream_t st) {
 }  // namespace
 
 // Per-chip tile choice by M regime (Sec. 3.4: tiles tuned to sequence
-// length), fitted to a per-shape sweep on MI355X (256 CUs) over the
-// Llama-3.2-1B shapes and their grouped widths at M = 128, 512, 2048:
+// length), fitted to per-shape sweeps on MI355X (256 CUs) over the
+// Llama-3.2-1B, Llama-3.2-3B and Qwen3-0.6B shapes and their grouped widths
+// at M = 128, 512, 2048 (K steps of 64):
 //  * 128 x 256 tiles when they give at least 3/4 workgroup per CU;
-//  * else 64 x 256 tiles when they give at least one per CU;
+//  * else 64 x 256 tiles when they give at least 3/4 per CU;
 //  * else 64 x 128 tiles with 2-way split-K when those give at least 3/4
-//    workgroup per CU and K has >= 32 steps;
+//    workgroup per CU and K has >= 16 steps;
 //  * else one 64-column panel per K slice with split-K over as many
-//    one-wavefront slices as keep >= 8 K steps each (at most 8), in 64-row
-//    tiles if that gives 4 wavefronts per CU, else 32-row tiles.
+//    one-wavefront slices as keep >= 8 K steps each (>= 4 when K has fewer
+//    than 32 steps; at most 8 slices), in 64-row tiles if that gives 4
+//    wavefronts per CU, else 32-row tiles.
+// (The K < 2048 thresholds took the Qwen3-0.6B shapes 1024 -> 4096 / 6144
+// from 301 / 396 to 373 / 443 TFLOP/s at M = 512 and from 142 / 160 to
+// 164 / 178 at M = 128; no plan of the other models changed.)
 // The other formats use the same plan.  Where their weight stages do not fit
 // in LDS beside the A stages (Q8, Q5, Q6 at 128 x 256) the tile keeps the
 // weights in registers; for Q8 that still beats 64 x 256 tiles by 10-20%
@@ -52,10 +57,11 @@ GemmPlan gemm_plan(int64_t m, int64_t n, int64_t k, int cu_count) {
   const int64_t cu = cu_count;
   const int64_t kt = (k / kGroup + 1) / 2;
   if (4 * blocks(128, 4) >= 3 * cu) return GemmPlan{128, 4, 1};
-  if (blocks(64, 4) >= cu) return GemmPlan{64, 4, 1};
-  if (4 * blocks(64, 2) >= 3 * cu && kt >= 32) return GemmPlan{64, 2, 2};
+  if (4 * blocks(64, 4) >= 3 * cu) return GemmPlan{64, 4, 1};
+  if (4 * blocks(64, 2) >= 3 * cu && kt >= 16) return GemmPlan{64, 2, 2};
+  const int64_t min_steps = kt < 32 ? 4 : 8;
   int wk = 1;
-  while (wk < 8 && kt / (2 * wk) >= 8) wk *= 2;
+  while (wk < 8 && kt / (2 * wk) >= min_steps) wk *= 2;
   if (blocks(64, 1) * wk >= 4 * cu) return GemmPlan{64, 1, wk};
   return GemmPlan{32, 1, wk};
 }
