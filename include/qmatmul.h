@@ -321,7 +321,8 @@ qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float*
  * q: fp16 [n_q_heads][m][head_dim], the chunk's queries at positions p0 ..
  * p0 + m - 1; k_cache, v_cache: fp16 [n_kv_heads][max_len][head_dim] holding
  * positions 0 .. p0 + m - 1 (the chunk's own keys and values written
- * already); o: fp32 [n_q_heads][m][head_dim].  head_dim 64 or 128;
+ * already); o: fp32 [n_q_heads][m][head_dim]; q, the caches, o and the
+ * workspace 16-byte aligned.  head_dim 64 or 128;
  * 1 <= m <= 65536; p0 + m <= max_len <= 262144; scale finite and > 0.
  * fp16 MFMA for q.k and p.v (p rounded toward zero to fp16; the sums use
  * the fp32 p), fp32 statistics and accumulation.
@@ -335,6 +336,17 @@ qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float*
 qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
                         int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len, float scale,
                         float* o, void* workspace, size_t workspace_bytes, void* stream);
+
+/* qattn_prefill with its output as the output projection's GEMM input:
+ * out[i][h * head_dim + d] = fp16_RNE(o[h][i][d]), fp16 [m][n_q_heads *
+ * head_dim] (16-byte aligned), the same values qattn_prefill followed by
+ * qdec_heads_to_rows_f16 gives, written by the attention (and the merge)
+ * itself.  (Sec. 3.4: chunked prefill; Sec. 3.3: the conversion fused into
+ * the producing kernel, one launch fewer per layer.) */
+qm_status qattn_prefill_rows_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                 int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0,
+                                 int64_t max_len, float scale, uint16_t* out, void* workspace, size_t workspace_bytes,
+                                 void* stream);
 
 /* Bytes of qattn_prefill's workspace for its full key-split plan on the
  * current device (0 when no tile is split): per split range of a split

@@ -33,7 +33,7 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
            "qmatmul_gemv_swiglu_rmsnorm_f16", "qdec_rope_table",
            "qmatmul_gemv_qkv_rmsnorm_rope", "qdec_embed_rows", "qdec_rope_append_rows", "qdec_heads_to_rows_f16",
-           "qdec_swiglu_f16", "qattn_prefill_workspace_bytes")
+           "qdec_swiglu_f16", "qattn_prefill_workspace_bytes", "qattn_prefill_rows_f16")
 
 
 class QmError(RuntimeError):
@@ -81,6 +81,7 @@ def lib() -> ctypes.CDLL:
             "qattn_decode": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qattn_prefill": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qattn_prefill_workspace_bytes": [i32, i32, i64, i64, ctypes.POINTER(sz)],
+            "qattn_prefill_rows_f16": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qdec_embed": [vp, i64, i64, vp, vp, vp],
             "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
             "qdec_rope_table": [i64, i32, ctypes.c_float, vp, vp],
@@ -460,6 +461,31 @@ def qattn_prefill(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
         wp, wn = _ptr(workspace), workspace.numel()
     _check(lib().qattn_prefill(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, m, p0, max_len, scale,
                                _ptr(out), wp, wn, _stream(stream)))
+    return out
+
+
+def qattn_prefill_rows_f16(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, p0: int, scale: float,
+                           out: Optional[torch.Tensor] = None, workspace=None, stream=None):
+    """qattn_prefill with fp16 rows out: [m][Hq * D] (the o-projection GEMM's
+    input).  workspace as for qattn_prefill."""
+    hq, m, d = q.shape
+    hkv, max_len, d2 = k_cache.shape
+    assert d2 == d and v_cache.shape == k_cache.shape
+    assert q.dtype == k_cache.dtype == v_cache.dtype == torch.float16
+    assert q.is_contiguous() and k_cache.is_contiguous() and v_cache.is_contiguous()
+    if out is None:
+        out = torch.empty((m, hq * d), dtype=torch.float16, device=q.device)
+    assert out.dtype == torch.float16 and out.is_contiguous() and out.numel() == hq * m * d
+    if workspace is None:
+        nb = qattn_prefill_workspace_bytes(hq, d, m, p0)
+        workspace = torch.empty(max(nb, 16), dtype=torch.uint8, device=q.device)
+    if workspace is NO_WORKSPACE:
+        wp, wn = None, 0
+    else:
+        assert workspace.dtype == torch.uint8 and workspace.is_contiguous()
+        wp, wn = _ptr(workspace), workspace.numel()
+    _check(lib().qattn_prefill_rows_f16(_ptr(q), _ptr(k_cache), _ptr(v_cache), hq, hkv, d, m, p0, max_len, scale,
+                                        _ptr(out), wp, wn, _stream(stream)))
     return out
 
 

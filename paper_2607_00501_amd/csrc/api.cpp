@@ -590,28 +590,56 @@ qm_status qattn_prefill_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int
   return QM_OK;
 }
 
-qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
-                        int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len, float scale,
-                        float* o, void* workspace, size_t workspace_bytes, void* stream) {
-  if (head_dim != 64 && head_dim != 128)
-    return fail(QM_ESHAPE, "qattn_prefill: head_dim=%d must be 64 or 128", head_dim);
+}  // extern "C"
+
+namespace {
+
+// Shared body of the two prefill-attention entry points (o: fp32 heads, or
+// o16: fp16 rows).
+qm_status prefill_attention_call(const char* name, const uint16_t* q, const uint16_t* k_cache,
+                                 const uint16_t* v_cache, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                 int64_t m, int64_t p0, int64_t max_len, float scale, float* o, uint16_t* o16,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  if (head_dim != 64 && head_dim != 128) return fail(QM_ESHAPE, "%s: head_dim=%d must be 64 or 128", name, head_dim);
   if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads > 1024 || n_q_heads % n_kv_heads != 0)
-    return fail(QM_ESHAPE, "qattn_prefill: n_q_heads=%d must be a multiple of n_kv_heads=%d", n_q_heads, n_kv_heads);
+    return fail(QM_ESHAPE, "%s: n_q_heads=%d must be a multiple of n_kv_heads=%d", name, n_q_heads, n_kv_heads);
   if (m < 1 || m > 65536 || p0 < 0 || max_len > kAttnMaxLen || p0 + m > max_len)
-    return fail(QM_ESHAPE, "qattn_prefill: need 1 <= m <= 65536, p0 >= 0, p0 + m <= max_len <= %lld",
+    return fail(QM_ESHAPE, "%s: need 1 <= m <= 65536, p0 >= 0, p0 + m <= max_len <= %lld", name,
                 (long long)kAttnMaxLen);
-  if (!(scale > 0.0f) || scale == INFINITY) return fail(QM_EINVAL, "qattn_prefill: scale must be finite and > 0");
-  if (!q || !k_cache || !v_cache || !o) return fail(QM_EINVAL, "qattn_prefill: null pointer");
-  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(o))
-    return fail(QM_EALIGN, "qattn_prefill: q, k_cache, v_cache must be 16-byte aligned, o 4-byte aligned");
-  if (workspace && !aligned16(workspace)) return fail(QM_EALIGN, "qattn_prefill: workspace must be 16-byte aligned");
+  if (!(scale > 0.0f) || scale == INFINITY) return fail(QM_EINVAL, "%s: scale must be finite and > 0", name);
+  if (!q || !k_cache || !v_cache || (!o && !o16)) return fail(QM_EINVAL, "%s: null pointer", name);
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache))
+    return fail(QM_EALIGN, "%s: q, k_cache, v_cache must be 16-byte aligned", name);
+  if ((o && !aligned16(o)) || (o16 && !aligned16(o16))) return fail(QM_EALIGN, "%s: the output must be 16-byte aligned", name);
+  if (workspace && !aligned16(workspace)) return fail(QM_EALIGN, "%s: workspace must be 16-byte aligned", name);
   const DeviceInfo* d;
   qm_status st;
   if ((st = device_info(&d)) != QM_OK) return st;
   return launched(launch_attn_prefill(q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, m, p0, max_len, scale, o,
-                                      workspace, workspace ? workspace_bytes : 0, d->cu_count,
+                                      o16, workspace, workspace ? workspace_bytes : 0, d->cu_count,
                                       static_cast<hipStream_t>(stream)),
-                  "qattn_prefill");
+                  name);
+}
+
+}  // namespace
+
+extern "C" {
+
+qm_status qattn_prefill(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t n_q_heads,
+                        int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len, float scale,
+                        float* o, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!o) return fail(QM_EINVAL, "qattn_prefill: null pointer");
+  return prefill_attention_call("qattn_prefill", q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, m, p0, max_len,
+                                scale, o, nullptr, workspace, workspace_bytes, stream);
+}
+
+qm_status qattn_prefill_rows_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                 int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0,
+                                 int64_t max_len, float scale, uint16_t* out, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  if (!out) return fail(QM_EINVAL, "qattn_prefill_rows_f16: null pointer");
+  return prefill_attention_call("qattn_prefill_rows_f16", q, k_cache, v_cache, n_q_heads, n_kv_heads, head_dim, m,
+                                p0, max_len, scale, nullptr, out, workspace, workspace_bytes, stream);
 }
 
 qm_status qdec_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,

@@ -320,7 +320,8 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
                                                            const uint16_t* __restrict__ v, int group,
                                                            int64_t m, int64_t p0, int64_t max_len, float scale_log2,
                                                            float* __restrict__ o, int n_heads, int cu_count, int bmax,
-                                                           int64_t n_units, float* __restrict__ ws) {
+                                                           int64_t n_units, float* __restrict__ ws,
+                                                           uint16_t* __restrict__ o16) {
   constexpr int KB = D == 64 ? 64 : 32;      // keys per block (head_dim 128: 32, to fit 256 VGPRs)
   constexpr int NT = KB / 32;                // 32-key S tiles per block
   constexpr int KS = D / 16;                 // k steps of S over the head dimension
@@ -546,7 +547,22 @@ __global__ __launch_bounds__(256, 3) void attn_prefill_kernel(const uint16_t* __
     }
   }
   if (qrow < mi) {
-    if (!part) {
+    if (!part && o16) {
+      // fp16 rows [m][n_heads * D] (the output projection's input): the four
+      // consecutive dimensions of r = 4j .. 4j + 3 as one 8-byte store.
+      const float inv = 1.0f / l_run;
+      uint16_t* orow = o16 + (static_cast<int64_t>(qrow) * n_heads + h) * D;
+#pragma unroll
+      for (int b = 0; b < DB; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const half2v lo = {static_cast<_Float16>(acc[b][4 * j] * inv), static_cast<_Float16>(acc[b][4 * j + 1] * inv)};
+          const half2v hi = {static_cast<_Float16>(acc[b][4 * j + 2] * inv),
+                             static_cast<_Float16>(acc[b][4 * j + 3] * inv)};
+          *reinterpret_cast<uint2*>(orow + 32 * b + 8 * j + 4 * lh) =
+              make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        }
+    } else if (!part) {
       const float inv = 1.0f / l_run;
       float* orow = o + (static_cast<int64_t>(h) * m + qrow) * D;
 #pragma unroll
@@ -580,7 +596,8 @@ constexpr int kMergeBatch = 8;
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_prefill_merge_kernel(const float* __restrict__ ws, int64_t m, int64_t p0,
-                                                                 int n_heads, int bmax, float* __restrict__ o) {
+                                                                 int n_heads, int bmax, float* __restrict__ o,
+                                                                 uint16_t* __restrict__ o16) {
   constexpr int KB = D == 64 ? 64 : 32;
   constexpr int C4 = D / 4;                                       // threads per row
   constexpr int RW = 256 / C4;                                    // rows per workgroup
@@ -638,8 +655,16 @@ __global__ __launch_bounds__(256) void attn_prefill_merge_kernel(const float* __
     }
   }
   const float inv = 1.0f / l;
-  reinterpret_cast<float4*>(o + (static_cast<int64_t>(h) * m + 128 * static_cast<int64_t>(tile) + r) * D)[d4] =
-      make_float4(a.x * inv, a.y * inv, a.z * inv, a.w * inv);
+  const int64_t row = 128 * static_cast<int64_t>(tile) + r;
+  if (o16) {
+    const half2v lo = {static_cast<_Float16>(a.x * inv), static_cast<_Float16>(a.y * inv)};
+    const half2v hi = {static_cast<_Float16>(a.z * inv), static_cast<_Float16>(a.w * inv)};
+    reinterpret_cast<uint2*>(o16 + (row * n_heads + h) * D)[d4] =
+        make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+  } else {
+    reinterpret_cast<float4*>(o + (static_cast<int64_t>(h) * m + row) * D)[d4] =
+        make_float4(a.x * inv, a.y * inv, a.z * inv, a.w * inv);
+  }
 }
 
 }  // namespace
@@ -706,7 +731,7 @@ PrefillPlan attn_prefill_plan(int32_t hq, int32_t d, int64_t m, int64_t p0, int 
 
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
-                               void* ws, size_t ws_bytes, int cu_count, hipStream_t st) {
+                               uint16_t* o16, void* ws, size_t ws_bytes, int cu_count, hipStream_t st) {
   const PrefillPlan p = attn_prefill_plan(hq, d, m, p0, cu_count, ws ? ws_bytes : 0);
   const dim3 grid(static_cast<unsigned>(p.units));
   const float sl2 = scale * 1.4426950408889634f;
@@ -714,17 +739,17 @@ hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint1
   float* wsf = static_cast<float*>(ws);
   if (d == 64)
     hipLaunchKernelGGL((attn_prefill_kernel<64>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o,
-                       hq, cu, p.bmax, p.units, wsf);
+                       hq, cu, p.bmax, p.units, wsf, o16);
   else
     hipLaunchKernelGGL((attn_prefill_kernel<128>), grid, dim3(256), 0, st, q, k, v, hq / hkv, m, p0, max_len, sl2, o,
-                       hq, cu, p.bmax, p.units, wsf);
+                       hq, cu, p.bmax, p.units, wsf, o16);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.split_tiles == 0) return e;
   const dim3 mg(static_cast<unsigned>(p.split_tiles * hq * (128 / (256 / (d / 4)))));
   if (d == 64)
-    hipLaunchKernelGGL((attn_prefill_merge_kernel<64>), mg, dim3(256), 0, st, wsf, m, p0, hq, p.bmax, o);
+    hipLaunchKernelGGL((attn_prefill_merge_kernel<64>), mg, dim3(256), 0, st, wsf, m, p0, hq, p.bmax, o, o16);
   else
-    hipLaunchKernelGGL((attn_prefill_merge_kernel<128>), mg, dim3(256), 0, st, wsf, m, p0, hq, p.bmax, o);
+    hipLaunchKernelGGL((attn_prefill_merge_kernel<128>), mg, dim3(256), 0, st, wsf, m, p0, hq, p.bmax, o, o16);
   return hipGetLastError();
 }
 

@@ -160,7 +160,8 @@ hipError_t launch_attn_decode(const uint16_t* q, const uint16_t* k, const uint16
 
 // Causal prefill attention over the cache for a chunk of m query rows
 // (workgroups ordered over the device's cu_count CUs; long tiles split over
-// key ranges when the workspace holds their partials).
+// key ranges when the workspace holds their partials).  Output: fp32
+// [hq][m][d] into o, or, when o16 is set, fp16 rows [m][hq * d] into o16.
 struct PrefillPlan {
   int bmax;            // key blocks per split
   int64_t units;       // workgroups of the attention kernel
@@ -170,7 +171,7 @@ struct PrefillPlan {
 PrefillPlan attn_prefill_plan(int32_t hq, int32_t d, int64_t m, int64_t p0, int cu_count, size_t ws_bytes);
 hipError_t launch_attn_prefill(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t hq, int32_t hkv,
                                int32_t d, int64_t m, int64_t p0, int64_t max_len, float scale, float* o,
-                               void* ws, size_t ws_bytes, int cu_count, hipStream_t st);
+                               uint16_t* o16, void* ws, size_t ws_bytes, int cu_count, hipStream_t st);
 
 // Decode-step glue kernels.
 hipError_t launch_embed(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* token, float* x,

@@ -154,7 +154,7 @@ class DenseDecoder:
         qd, kvd = c.n_q_heads * c.head_dim, c.n_kv_heads * c.head_dim
         shapes = dict(x=((c.hidden,), torch.float32), h=((c.hidden,), torch.float16),
                       q=((qd,), torch.float32), k=((kvd,), torch.float32), v=((kvd,), torch.float32),
-                      qh=((qd,), torch.float16), o=((qd,), torch.float32), o16=((qd,), torch.float16),
+                      qh=((qd,), torch.float16), o16=((qd,), torch.float16),
                       ya=((c.hidden,), torch.float32), g=((c.inter,), torch.float32),
                       u=((c.inter,), torch.float32), sw=((c.inter,), torch.float16), y=((c.hidden,), torch.float32))
         if self._chunk is None:
@@ -169,8 +169,8 @@ class DenseDecoder:
         b = self._chunk
         rows = lambda n: b[n][:m * shapes[n][0][0]].view(m, shapes[n][0][0])
         heads = lambda n: b[n][:m * qd].view(c.n_q_heads, m, c.head_dim)
-        out = {n: rows(n) for n in shapes if n not in ("qh", "o")}
-        out.update(qh=heads("qh"), o=heads("o"), attn_ws=b["attn_ws"])
+        out = {n: rows(n) for n in shapes if n != "qh"}
+        out.update(qh=heads("qh"), attn_ws=b["attn_ws"])
         return out
 
     def prefill(self, tokens: torch.Tensor, p0: int = 0, stream=None) -> None:
@@ -192,9 +192,9 @@ class DenseDecoder:
             qh = B.qdec_rope_append_rows(q, k, v, p0, c.theta, self.k_cache[li], self.v_cache[li],
                                          interleaved=self.rope_epi, q_out=b["qh"], q_norm=ly.q_norm,
                                          k_norm=ly.k_norm, eps=c.eps, stream=s)
-            o = B.qattn_prefill(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, out=b["o"],
-                                workspace=b["attn_ws"], stream=s)
-            ya = B.qmatmul_gemm(ly.wo, B.qdec_heads_to_rows_f16(o, out=b["o16"], stream=s), out=b["ya"], stream=s)
+            o16 = B.qattn_prefill_rows_f16(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, out=b["o16"],
+                                           workspace=b["attn_ws"], stream=s)
+            ya = B.qmatmul_gemm(ly.wo, o16, out=b["ya"], stream=s)
             h = B.qdec_rmsnorm(x, ly.ffn_norm, c.eps, residual=ya, out=b["h"], stream=s)
             g, u = B.qmatmul_gemm_grouped([ly.wg, ly.wu], h, outs=[b["g"], b["u"]], stream=s)
             y = B.qmatmul_gemm(ly.wd, B.qdec_swiglu_f16(g, u, out=b["sw"], stream=s), out=b["y"], stream=s)

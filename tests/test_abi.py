@@ -290,6 +290,9 @@ def test_attention_prefill_validation():
     assert call(scale=float("nan")) == 1 and call(scale=-0.5) == 1 and call(scale=0.0) == 1
     assert call(o=None) == 1
     assert call(w=ctypes.c_void_p(0x60008)) == 3                     # workspace alignment
+    assert call(o=ctypes.c_void_p(0x50004)) == 3                     # output alignment
+    rows = lambda out=p, d=64: L.qattn_prefill_rows_f16(p, p, p, 32, 8, d, 128, 0, 4096, 0.125, out, None, 0, None)
+    assert rows(out=None) == 1 and rows(d=80) == 2 and rows(out=ctypes.c_void_p(0x50008)) == 3
     nb = ctypes.c_size_t()
     assert L.qattn_prefill_workspace_bytes(32, 80, 128, 0, ctypes.byref(nb)) == 2
     assert L.qattn_prefill_workspace_bytes(32, 64, 0, 0, ctypes.byref(nb)) == 2

@@ -197,6 +197,22 @@ def test_attn_prefill_chunk_far_into_cache():
             assert rel_err(o[h, i][None], ref) <= PREFILL_TOL, (h, i)
 
 
+@pytest.mark.parametrize("hq,hkv,d,m,p0", [(8, 2, 64, 300, 0), (16, 8, 128, 1000, 0), (12, 4, 128, 128, 20000)])
+def test_attn_prefill_rows_f16_equals_heads_then_rows(hq, hkv, d, m, p0):
+    """The fp16-rows form (unsplit and key-split) equals qattn_prefill followed
+    by qdec_heads_to_rows_f16, bit for bit."""
+    g = torch.Generator(device="cuda").manual_seed(m + d)
+    q = torch.randn((hq, m, d), generator=g, device="cuda").half()
+    k = torch.randn((hkv, p0 + m, d), generator=g, device="cuda").half()
+    v = torch.randn((hkv, p0 + m, d), generator=g, device="cuda").half()
+    scale = 1.0 / math.sqrt(d)
+    for ws in (None, B.NO_WORKSPACE):
+        o = B.qattn_prefill(q, k, v, p0, scale, workspace=ws)
+        want = B.qdec_heads_to_rows_f16(o)
+        got = B.qattn_prefill_rows_f16(q, k, v, p0, scale, workspace=ws)
+        assert torch.equal(got.view(torch.int16), want.view(torch.int16))
+
+
 def test_attn_prefill_last_row_matches_decode():
     """The last query of a chunk attends to the whole prefix: it equals the
     decode kernel's result for that query (within the MFMA tolerance)."""
