@@ -225,11 +225,17 @@ qm_status qdec_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, 
  * cache rows p0 .. p0 + m - 1 written (keys rotated).  Rotation as
  * qdec_rope_append, the per-head norms too.  head_dim 64 or 128;
  * 1 <= m <= 32768; p0 + m <= max_len <= 262144; theta > 1.
+ * table: NULL, or qdec_rope_table's (cos, sin) pairs for this head_dim and
+ * theta over table_len >= p0 + m positions (8-byte aligned), read instead
+ * of computing each angle (the same values; the kernel then skips the fp64
+ * angle, cosine and sine per element).  A table of another theta gives
+ * other rotations, not an error.
  * (Sec. 3.4: chunked prefill; Sec. 3.2: RoPE and the KV cache.) */
 qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, int32_t n_q_heads,
                                 int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len,
                                 float theta, int32_t interleaved, const uint16_t* q_norm, const uint16_t* k_norm,
-                                float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache, void* stream);
+                                float eps, const float* table, int64_t table_len, uint16_t* q_out,
+                                uint16_t* k_cache, uint16_t* v_cache, void* stream);
 
 /* out[r][h * head_dim + d] = fp16_RNE(o[h][r][d]): qattn_prefill's output
  * as the output projection's GEMM input.

@@ -87,7 +87,7 @@ def lib() -> ctypes.CDLL:
             "qdec_rope_table": [i64, i32, ctypes.c_float, vp, vp],
             "qdec_embed_rows": [vp, i64, i64, vp, i64, vp, vp],
             "qdec_rope_append_rows": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, i32, vp, vp,
-                                      ctypes.c_float, vp, vp, vp, vp],
+                                      ctypes.c_float, vp, i64, vp, vp, vp, vp],
             "qdec_heads_to_rows_f16": [vp, i32, i64, i32, vp, vp],
             "qdec_swiglu_f16": [vp, vp, i64, vp, vp],
             "qmatmul_gemv_qkv_rmsnorm_rope": [W, vp, vp, vp, ctypes.c_float, vp, i32, i32, i32, i64, i64, vp, vp, vp,
@@ -298,8 +298,11 @@ def _check_head_gains(q_norm, k_norm, d):
 def qdec_rope_append_rows(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, p0: int, theta: float,
                           k_cache: torch.Tensor, v_cache: torch.Tensor, interleaved: bool = False,
                           q_out: Optional[torch.Tensor] = None, q_norm: Optional[torch.Tensor] = None,
-                          k_norm: Optional[torch.Tensor] = None, eps: float = 1e-6, stream=None):
-    """q fp32 [m][Hq*D], k, v fp32 [m][Hkv*D] -> fp16 [Hq][m][D]; cache rows p0..p0+m-1."""
+                          k_norm: Optional[torch.Tensor] = None, eps: float = 1e-6,
+                          table: Optional[torch.Tensor] = None, stream=None):
+    """q fp32 [m][Hq*D], k, v fp32 [m][Hkv*D] -> fp16 [Hq][m][D]; cache rows p0..p0+m-1.
+    table: qdec_rope_table's [positions][D/2][2] fp32 for this theta and D
+    (read instead of computing each angle)."""
     hkv, max_len, d = k_cache.shape
     m = q.shape[0]
     hq = q.shape[1] // d
@@ -310,9 +313,13 @@ def qdec_rope_append_rows(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, p0:
     _check_head_gains(q_norm, k_norm, d)
     if q_out is None:
         q_out = torch.empty((hq, m, d), dtype=torch.float16, device=q.device)
+    tlen = 0
+    if table is not None:
+        assert table.dtype == torch.float32 and table.is_contiguous() and table.shape[1:] == (d // 2, 2)
+        tlen = table.shape[0]
     _check(lib().qdec_rope_append_rows(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, m, p0, max_len, theta,
-                                       1 if interleaved else 0, _ptr(q_norm), _ptr(k_norm), eps, _ptr(q_out),
-                                       _ptr(k_cache), _ptr(v_cache), _stream(stream)))
+                                       1 if interleaved else 0, _ptr(q_norm), _ptr(k_norm), eps, _ptr(table), tlen,
+                                       _ptr(q_out), _ptr(k_cache), _ptr(v_cache), _stream(stream)))
     return q_out
 
 

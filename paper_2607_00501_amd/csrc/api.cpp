@@ -56,6 +56,7 @@ qm_status device_info(const DeviceInfo** out) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 bool aligned2(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 1u) == 0; }
 
 qm_status check_weight(const qm_qweight* w, const char* name) {
@@ -299,8 +300,11 @@ qm_status qdec_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, 
 qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, int32_t n_q_heads,
                                 int32_t n_kv_heads, int32_t head_dim, int64_t m, int64_t p0, int64_t max_len,
                                 float theta, int32_t interleaved, const uint16_t* q_norm, const uint16_t* k_norm,
-                                float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache, void* stream) {
+                                float eps, const float* table, int64_t table_len, uint16_t* q_out,
+                                uint16_t* k_cache, uint16_t* v_cache, void* stream) {
   const char* name = "qdec_rope_append_rows";
+  if (table && (!aligned8(table) || table_len < p0 + m))
+    return fail(QM_EINVAL, "%s: the (cos, sin) table must be 8-byte aligned and cover positions < p0 + m", name);
   if ((q_norm == nullptr) != (k_norm == nullptr) || !aligned2(q_norm) || !aligned2(k_norm))
     return fail(QM_EINVAL, "%s: q_norm and k_norm both given (2-byte aligned) or both NULL", name);
   if (q_norm && (!(eps >= 0.0f) || eps == INFINITY)) return fail(QM_EINVAL, "%s: eps finite and >= 0", name);
@@ -316,7 +320,7 @@ qm_status qdec_rope_append_rows(const float* q, const float* k, const float* v, 
   if (!aligned4(q) || !aligned4(k) || !aligned4(v) || !aligned2(q_out) || !aligned2(k_cache) || !aligned2(v_cache))
     return fail(QM_EALIGN, "%s: q, k, v 4-byte, q_out and caches 2-byte aligned", name);
   return launched(launch_rope_append_rows(q, k, v, n_q_heads, n_kv_heads, head_dim, m, p0, max_len, theta,
-                                          interleaved, q_out, k_cache, v_cache, q_norm, k_norm, eps,
+                                          interleaved, q_out, k_cache, v_cache, q_norm, k_norm, eps, table,
                                           static_cast<hipStream_t>(stream)),
                   name);
 }

@@ -232,7 +232,8 @@ __global__ void rope_append_rows_kernel(const float* __restrict__ q, const float
                                         int64_t max_len, double log2_theta, int interleaved,
                                         uint16_t* __restrict__ q_out, uint16_t* __restrict__ kc,
                                         uint16_t* __restrict__ vc, const uint16_t* __restrict__ q_gain,
-                                        const uint16_t* __restrict__ k_gain, float eps) {
+                                        const uint16_t* __restrict__ k_gain, float eps,
+                                        const float2* __restrict__ table) {
   const int h = blockIdx.x, i = threadIdx.x, half = d / 2;
   const int64_t r = blockIdx.y, pos = p0 + r;
   if (h >= hq + hkv) {
@@ -243,7 +244,9 @@ __global__ void rope_append_rows_kernel(const float* __restrict__ q, const float
     dst[i + half] = f2h(src[i + half]);
     return;
   }
-  const float2 cs = rope_cos_sin(pos, i, d, log2_theta);
+  // (cos, sin) from the cache's table when given (the same values, built
+  // once by rope_table_kernel), else computed here.
+  const float2 cs = table ? table[pos * half + i] : rope_cos_sin(pos, i, d, log2_theta);
   const float* src = h < hq ? q + r * hq * d + h * d : k + r * hkv * d + (h - hq) * d;
   uint16_t* dst = h < hq ? q_out + (static_cast<int64_t>(h) * m + r) * d
                          : kc + (static_cast<int64_t>(h - hq) * max_len + pos) * d;
@@ -429,10 +432,10 @@ hipError_t launch_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidde
 hipError_t launch_rope_append_rows(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
                                    int64_t m, int64_t p0, int64_t max_len, float theta, int32_t interleaved,
                                    uint16_t* q_out, uint16_t* kc, uint16_t* vc, const uint16_t* q_gain,
-                                   const uint16_t* k_gain, float eps, hipStream_t st) {
+                                   const uint16_t* k_gain, float eps, const float* table, hipStream_t st) {
   hipLaunchKernelGGL(rope_append_rows_kernel, dim3(static_cast<unsigned>(hq + 2 * hkv), static_cast<unsigned>(m)),
                      dim3(d / 2), 0, st, q, k, v, hq, hkv, d, m, p0, max_len, std::log2(static_cast<double>(theta)),
-                     interleaved, q_out, kc, vc, q_gain, k_gain, eps);
+                     interleaved, q_out, kc, vc, q_gain, k_gain, eps, reinterpret_cast<const float2*>(table));
   return hipGetLastError();
 }
 

@@ -189,7 +189,7 @@ hipError_t launch_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidde
 hipError_t launch_rope_append_rows(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
                                    int64_t m, int64_t p0, int64_t max_len, float theta, int32_t interleaved,
                                    uint16_t* q_out, uint16_t* kc, uint16_t* vc, const uint16_t* q_gain,
-                                   const uint16_t* k_gain, float eps, hipStream_t st);
+                                   const uint16_t* k_gain, float eps, const float* table, hipStream_t st);
 hipError_t launch_heads_to_rows(const float* o, int32_t h, int64_t m, int32_t d, uint16_t* out, hipStream_t st);
 hipError_t launch_swiglu(const float* g, const float* u, int64_t n, uint16_t* out, hipStream_t st);
 

@@ -80,7 +80,9 @@ class DenseDecoder:
         assert not self.rope_epi or self.fused, "the RoPE epilogue runs in the fused q/k/v GEMV"
         assert not (self.rope_epi and any(ly.q_norm is not None for ly in layers)), \
             "per-head q/k norms need whole heads: use the RoPE kernel (rows not interleaved)"
-        self.rope_tab = B.qdec_rope_table(max_len, c.head_dim, c.theta, device=dev) if self.rope_epi else None
+        # (cos, sin) of every cache position, built once: read by the q/k/v
+        # GEMV's RoPE epilogue and by the prompt path's RoPE kernel.
+        self.rope_tab = B.qdec_rope_table(max_len, c.head_dim, c.theta, device=dev)
         self.h = torch.zeros(c.hidden, **f16)             # normed input of a projection
         self.q, self.k, self.v = torch.zeros(qd, **f32), torch.zeros(kvd, **f32), torch.zeros(kvd, **f32)
         self.q16 = torch.zeros((c.n_q_heads, c.head_dim), **f16)
@@ -191,7 +193,7 @@ class DenseDecoder:
             q, k, v = B.qmatmul_gemm_grouped([ly.wq, ly.wk, ly.wv], h, outs=[b["q"], b["k"], b["v"]], stream=s)
             qh = B.qdec_rope_append_rows(q, k, v, p0, c.theta, self.k_cache[li], self.v_cache[li],
                                          interleaved=self.rope_epi, q_out=b["qh"], q_norm=ly.q_norm,
-                                         k_norm=ly.k_norm, eps=c.eps, stream=s)
+                                         k_norm=ly.k_norm, eps=c.eps, table=self.rope_tab, stream=s)
             o16 = B.qattn_prefill_rows_f16(qh, self.k_cache[li], self.v_cache[li], p0, self.scale, out=b["o16"],
                                            workspace=b["attn_ws"], stream=s)
             ya = B.qmatmul_gemm(ly.wo, o16, out=b["ya"], stream=s)

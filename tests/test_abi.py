@@ -398,9 +398,10 @@ def test_prefill_glue_validation():
     p = ctypes.c_void_p(0x50000)
     assert L.qdec_embed_rows(p, 100, 64, p, 40000, p, None) == 2 and L.qdec_embed_rows(p, 0, 64, p, 4, p, None) == 2
     assert L.qdec_embed_rows(None, 100, 64, p, 4, p, None) == 1
-    rr = lambda d=64, m=8, p0=0, mx=64, il=0, theta=1e4, qo=p, kn=None: L.qdec_rope_append_rows(
-        p, p, p, 4, 2, d, m, p0, mx, theta, il, None, kn, 1e-6, qo, p, p, None)
+    rr = lambda d=64, m=8, p0=0, mx=64, il=0, theta=1e4, qo=p, kn=None, tab=None, tl=0: L.qdec_rope_append_rows(
+        p, p, p, 4, 2, d, m, p0, mx, theta, il, None, kn, 1e-6, tab, tl, qo, p, p, None)
     assert rr(kn=p) == 1
+    assert rr(tab=p, tl=7) == 1 and rr(tab=ctypes.c_void_p(0x50004), tl=64) == 1   # table too short / misaligned
     assert rr(d=80) == 2 and rr(m=0) == 2 and rr(p0=60) == 2 and rr(il=2) == 1 and rr(theta=0.5) == 1
     assert rr(qo=None) == 1 and rr(qo=ctypes.c_void_p(0x50001)) == 3
     assert L.qdec_heads_to_rows_f16(p, 0, 4, 64, p, None) == 2 and L.qdec_heads_to_rows_f16(None, 4, 4, 64, p, None) == 1

@@ -482,6 +482,11 @@ def test_rope_append_rows_matches_one_token_at_a_time(interleaved, d, m, p0):
         q1 = B.qdec_rope_append(q[r].contiguous(), k[r].contiguous(), v[r].contiguous(), p0 + r, theta, kc2, vc2)
         assert torch.equal(qo[:, r], q1), r
     assert torch.equal(kc1, kc2) and torch.equal(vc1, vc2)
+    # with the cache's (cos, sin) table: the same bits
+    kc3, vc3 = torch.zeros_like(kc1), torch.zeros_like(vc1)
+    tab = B.qdec_rope_table(max_len, d, theta)
+    qo3 = B.qdec_rope_append_rows(qi, ki, v, p0, theta, kc3, vc3, interleaved=interleaved, table=tab)
+    assert torch.equal(qo3, qo) and torch.equal(kc3, kc1) and torch.equal(vc3, vc1)
 
 
 @pytest.mark.parametrize("rope_epi", [False, True])
