@@ -429,11 +429,14 @@ qm_status qdec_rmsnorm(float* x, const float* residual, const uint16_t* w, int64
  * layer applies to every query and key head before RoPE
  * (x / sqrt(mean over the head(x^2) + eps) * gain, sum in fp32); both NULL
  * for the Llama layer.
+ * table: NULL, or qdec_rope_table's (cos, sin) pairs for this head_dim and
+ * theta over table_len > pos positions (8-byte aligned), read instead of
+ * computing the angles (the same values).
  * (Sec. 3.2: RoPE and the KV cache of the decode step.) */
 qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32_t n_q_heads, int32_t n_kv_heads,
                            int32_t head_dim, int64_t pos, int64_t max_len, float theta, const uint16_t* q_norm,
-                           const uint16_t* k_norm, float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
-                           void* stream);
+                           const uint16_t* k_norm, float eps, const float* table, int64_t table_len,
+                           uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache, void* stream);
 
 /* out[i] = fp16_RNE(x[i]), i < n (values beyond the fp16 range become inf).
  * x: fp32, out: fp16, device; n >= 0.

@@ -96,8 +96,8 @@ def lib() -> ctypes.CDLL:
             "qmatmul_gemv_swiglu_rmsnorm_f16": [W, W, vp, vp, vp, ctypes.c_float, vp, vp, vp],
             "qattn_decode_f16": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, sz, vp],
             "qdec_rmsnorm": [vp, vp, vp, i64, i64, ctypes.c_float, vp, vp],
-            "qdec_rope_append": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, ctypes.c_float, vp, vp,
-                                 vp, vp],
+            "qdec_rope_append": [vp, vp, vp, i32, i32, i32, i64, i64, ctypes.c_float, vp, vp, ctypes.c_float, vp, i64,
+                                 vp, vp, vp, vp],
             "qdec_cast_f16": [vp, i64, vp, vp],
             "qdec_argmax": [vp, i64, vp, vp, sz, vp],
         }
@@ -524,9 +524,10 @@ def qdec_rmsnorm(x: torch.Tensor, w: torch.Tensor, eps: float, residual: Optiona
 def qdec_rope_append(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: int, theta: float,
                      k_cache: torch.Tensor, v_cache: torch.Tensor, q_out: Optional[torch.Tensor] = None,
                      q_norm: Optional[torch.Tensor] = None, k_norm: Optional[torch.Tensor] = None, eps: float = 1e-6,
-                     stream=None):
+                     table: Optional[torch.Tensor] = None, stream=None):
     """q: fp32 [Hq*D]; k, v: fp32 [Hkv*D]; caches fp16 [Hkv][max_len][D]
-    (row pos written) -> fp16 [Hq][D] rotated queries."""
+    (row pos written) -> fp16 [Hq][D] rotated queries.  table: qdec_rope_table's
+    (cos, sin) for this theta and D, read instead of computing the angles."""
     hkv, max_len, d = k_cache.shape
     hq = q.numel() // d
     assert q.dtype == k.dtype == v.dtype == torch.float32 and k.numel() == v.numel() == hkv * d
@@ -535,8 +536,13 @@ def qdec_rope_append(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: int
     _check_head_gains(q_norm, k_norm, d)
     if q_out is None:
         q_out = torch.empty((hq, d), dtype=torch.float16, device=q.device)
+    tlen = 0
+    if table is not None:
+        assert table.dtype == torch.float32 and table.is_contiguous() and table.shape[1:] == (d // 2, 2)
+        tlen = table.shape[0]
     _check(lib().qdec_rope_append(_ptr(q), _ptr(k), _ptr(v), hq, hkv, d, pos, max_len, theta, _ptr(q_norm),
-                                  _ptr(k_norm), eps, _ptr(q_out), _ptr(k_cache), _ptr(v_cache), _stream(stream)))
+                                  _ptr(k_norm), eps, _ptr(table), tlen, _ptr(q_out), _ptr(k_cache), _ptr(v_cache),
+                                  _stream(stream)))
     return q_out
 
 

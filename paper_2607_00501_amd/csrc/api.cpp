@@ -670,8 +670,10 @@ qm_status qdec_rmsnorm(float* x, const float* residual, const uint16_t* w, int64
 
 qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32_t n_q_heads, int32_t n_kv_heads,
                            int32_t head_dim, int64_t pos, int64_t max_len, float theta, const uint16_t* q_norm,
-                           const uint16_t* k_norm, float eps, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
-                           void* stream) {
+                           const uint16_t* k_norm, float eps, const float* table, int64_t table_len,
+                           uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache, void* stream) {
+  if (table && (!aligned8(table) || table_len <= pos))
+    return fail(QM_EINVAL, "qdec_rope_append: the (cos, sin) table must be 8-byte aligned and cover position pos");
   if ((q_norm == nullptr) != (k_norm == nullptr) || !aligned2(q_norm) || !aligned2(k_norm))
     return fail(QM_EINVAL, "qdec_rope_append: q_norm and k_norm both given (2-byte aligned) or both NULL");
   if (q_norm && (!(eps >= 0.0f) || eps == INFINITY)) return fail(QM_EINVAL, "qdec_rope_append: eps finite and >= 0");
@@ -686,7 +688,7 @@ qm_status qdec_rope_append(const float* q, const float* k, const float* v, int32
   if (!aligned4(q) || !aligned4(k) || !aligned4(v) || !aligned2(q_out) || !aligned2(k_cache) || !aligned2(v_cache))
     return fail(QM_EALIGN, "qdec_rope_append: q, k, v 4-byte, q_out and caches 2-byte aligned");
   return launched(launch_rope_append(q, k, v, n_q_heads, n_kv_heads, head_dim, pos, max_len, theta, q_out, k_cache,
-                                     v_cache, q_norm, k_norm, eps, static_cast<hipStream_t>(stream)),
+                                     v_cache, q_norm, k_norm, eps, table, static_cast<hipStream_t>(stream)),
                   "qdec_rope_append");
 }
 

@@ -182,7 +182,7 @@ __global__ void rope_append_kernel(const float* __restrict__ q, const float* __r
                                    int64_t max_len, double log2_theta, uint16_t* __restrict__ q_out,
                                    uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
                                    const uint16_t* __restrict__ q_gain, const uint16_t* __restrict__ k_gain,
-                                   float eps) {
+                                   float eps, const float2* __restrict__ table) {
   const int h = blockIdx.x, i = threadIdx.x, half = d / 2;
   if (h >= hq + hkv) {
     const int kh = h - hq - hkv;
@@ -191,7 +191,7 @@ __global__ void rope_append_kernel(const float* __restrict__ q, const float* __r
     dst[i + half] = f2h(v[kh * d + i + half]);
     return;
   }
-  const float2 cs = rope_cos_sin(pos, i, d, log2_theta);
+  const float2 cs = table ? table[pos * half + i] : rope_cos_sin(pos, i, d, log2_theta);   // same values
   const float c = cs.x, s = cs.y;
   const float* src = h < hq ? q + h * d : k + (h - hq) * d;
   uint16_t* dst = h < hq ? q_out + h * d : kc + (static_cast<int64_t>(h - hq) * max_len + pos) * d;
@@ -408,10 +408,10 @@ hipError_t launch_rmsnorm(float* x, const float* res, const uint16_t* w, int64_t
 hipError_t launch_rope_append(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
                               int64_t pos, int64_t max_len, float theta, uint16_t* q_out, uint16_t* kc,
                               uint16_t* vc, const uint16_t* q_gain, const uint16_t* k_gain, float eps,
-                              hipStream_t st) {
+                              const float* table, hipStream_t st) {
   hipLaunchKernelGGL(rope_append_kernel, dim3(static_cast<unsigned>(hq + 2 * hkv)), dim3(d / 2), 0, st, q, k, v,
                      hq, hkv, d, pos, max_len, std::log2(static_cast<double>(theta)), q_out, kc, vc, q_gain, k_gain,
-                     eps);
+                     eps, reinterpret_cast<const float2*>(table));
   return hipGetLastError();
 }
 

@@ -180,7 +180,7 @@ hipError_t launch_rmsnorm(float* x, const float* res, const uint16_t* w, int64_t
                           uint16_t* out, hipStream_t st);
 hipError_t launch_rope_append(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,
                               int64_t pos, int64_t max_len, float theta, uint16_t* q_out, uint16_t* kc,
-                              uint16_t* vc, const uint16_t* q_gain, const uint16_t* k_gain, float eps,
+                              uint16_t* vc, const uint16_t* q_gain, const uint16_t* k_gain, float eps, const float* table,
                               hipStream_t st);
 hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t st);
 hipError_t launch_rope_table(int64_t max_len, int32_t d, float theta, float* table, hipStream_t st);

@@ -119,7 +119,8 @@ class DenseDecoder:
                                                    residual=res, outs=[self.q, self.k, self.v], stream=s)
                     # RoPE (with the Qwen3 per-head norms) + cache append, then attention
                     B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
-                                       q_out=self.q16, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps, stream=s)
+                                       q_out=self.q16, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps,
+                                       table=self.rope_tab, stream=s)
                 B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,
                                workspace=self.ws, stream=s)
                 B.qmatmul_gemv(ly.wo, self.attn16.view(-1), out=self.y_attn, stream=s)
@@ -133,7 +134,8 @@ class DenseDecoder:
             B.qdec_rmsnorm(self.x, ly.attn_norm, c.eps, residual=self.y_ffn if li else None, out=self.h, stream=s)
             B.qmatmul_gemv_grouped([ly.wq, ly.wk, ly.wv], [self.h] * 3, [self.q, self.k, self.v], stream=s)
             B.qdec_rope_append(self.q, self.k, self.v, pos, c.theta, self.k_cache[li], self.v_cache[li],
-                               q_out=self.q16, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps, stream=s)
+                               q_out=self.q16, q_norm=ly.q_norm, k_norm=ly.k_norm, eps=c.eps,
+                               table=self.rope_tab, stream=s)
             B.qattn_decode(self.q16, self.k_cache[li], self.v_cache[li], pos + 1, self.scale, out=self.attn16,
                            workspace=self.ws, stream=s)
             B.qmatmul_gemv(ly.wo, self.attn16.view(-1), out=self.y_attn, stream=s)

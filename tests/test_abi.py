@@ -314,13 +314,14 @@ def test_decode_glue_validation():
     assert norm(eps=-1.0) == 1 and norm(eps=float("nan")) == 1 and norm(eps=float("inf")) == 1
     assert norm(w=None) == 1 and norm(o=None) == 1
     assert norm(w=odd) == 3 and norm(r=ctypes.c_void_p(0x50002)) == 3
-    rope = lambda hq=4, hkv=2, d=64, pos=0, mx=128, theta=1e4, q=p, kc=p, qn=None, kn=None: \
-        L.qdec_rope_append(q, p, p, hq, hkv, d, pos, mx, theta, qn, kn, 1e-6, p, kc, p, None)
+    rope = lambda hq=4, hkv=2, d=64, pos=0, mx=128, theta=1e4, q=p, kc=p, qn=None, kn=None, tab=None, tl=0: \
+        L.qdec_rope_append(q, p, p, hq, hkv, d, pos, mx, theta, qn, kn, 1e-6, tab, tl, p, kc, p, None)
     assert rope(qn=p) == 1 and rope(qn=p, kn=ctypes.c_void_p(0x50001)) == 1
     assert rope(d=96) == 2 and rope(hq=0) == 2 and rope(hkv=2000) == 2
     assert rope(pos=128) == 2 and rope(pos=-1) == 2 and rope(mx=300000, pos=5) == 2
     assert rope(theta=1.0) == 1 and rope(theta=float("nan")) == 1
     assert rope(q=None) == 1 and rope(kc=odd) == 3
+    assert rope(pos=7, tab=p, tl=7) == 1 and rope(tab=ctypes.c_void_p(0x50004), tl=8) == 1   # table too short / misaligned
     assert L.qdec_cast_f16(p, -1, p, None) == 2 and L.qdec_cast_f16(None, 4, p, None) == 1
     assert L.qdec_cast_f16(ctypes.c_void_p(0x50002), 4, p, None) == 3
     am = lambda n=4, x=p, t=p, w=p, nb=2048: L.qdec_argmax(x, n, t, w, nb, None)

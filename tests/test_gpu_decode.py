@@ -97,6 +97,27 @@ def test_rope_append_parity(d, pos, theta):
     assert np.all(kcn[:, other] == 0.5) and np.all(vcn[:, other] == -0.25)     # only row pos written
 
 
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("norms", [False, True])
+def test_rope_append_table_gives_the_same_bits(d, norms):
+    """qdec_rope_append reading qdec_rope_table's (cos, sin) writes the bits it
+    writes computing each angle, with and without the per-head q/k norms."""
+    hq, hkv, max_len, theta = 6, 2, 40_000, 1e6
+    rng = np.random.default_rng(d + norms)
+    q, k, v = (torch.from_numpy(rng.standard_normal(h * d).astype(np.float32)).cuda() for h in (hq, hkv, hkv))
+    kw = {}
+    if norms:
+        kw = dict(q_norm=torch.from_numpy(rng.uniform(0.5, 1.5, d).astype(np.float16)).cuda(),
+                  k_norm=torch.from_numpy(rng.uniform(0.5, 1.5, d).astype(np.float16)).cuda())
+    tab = B.qdec_rope_table(max_len, d, theta)
+    for pos in (0, 1, 77, 4095, 39_999):
+        kc1 = torch.zeros((hkv, max_len, d), dtype=torch.float16, device="cuda")
+        vc1, kc2, vc2 = torch.zeros_like(kc1), torch.zeros_like(kc1), torch.zeros_like(kc1)
+        qa = B.qdec_rope_append(q, k, v, pos, theta, kc1, vc1, **kw)
+        qb = B.qdec_rope_append(q, k, v, pos, theta, kc2, vc2, table=tab, **kw)
+        assert torch.equal(qa, qb) and torch.equal(kc1, kc2) and torch.equal(vc1, vc2), pos
+
+
 def test_cast_f16_bit_exact():
     rng = np.random.default_rng(9)
     x = np.concatenate([rng.standard_normal(1000).astype(np.float32) * 100,
