@@ -367,6 +367,8 @@ def extra_workloads(torch, B, inputs, workloads, steps, warmup, which="all"):
         out.update(extra_tg(torch, B, inputs, workloads, steps, warmup, lib))
     if which in ("all", "decode"):
         out.update(extra_decode(torch, B, inputs, workloads, steps, warmup, lib))
+    if which == "qwen-stack":                 # the Qwen3-0.6B 197-call stack alone (for kernel traces)
+        out.update(extra_qwen_stack(torch, B, inputs, workloads, steps, warmup))
     if which in ("all", "prefill"):
         out.update(extra_prefill(torch, B, inputs, workloads, steps, warmup, lib))
     if which in ("all", "moe"):
@@ -477,6 +479,26 @@ def extra_tg(torch, B, inputs, workloads, steps, warmup, lib):
     return out
 
 
+def extra_qwen_stack(torch, B, inputs, workloads, steps, warmup):
+    """The Qwen3-0.6B Q4 decode stack: 197 GEMV calls, 335 MB per token."""
+    out = {}
+    calls, nbytes = build_decode_stack(workloads.QWEN3_06B, 1, B.Q4_G32, torch, B, inputs, workloads)
+    g = capture(torch, lambda s: [c(s) for c in calls])
+    t, _ = time_graph(torch, g, steps, warmup)
+    kh, nh = workloads.QWEN3_06B["lm_head"]
+    head_bytes = workloads.q4_bytes(kh, nh)
+    head_us = steady_launch_us(torch, B, calls[-1], copies=4, reps=12)
+    out["qwen3-0.6b_decode_q4"] = {"tokens_per_s": round(steps / t, 2), "ms_per_token": round(t / steps * 1e3, 4),
+                                   "weight_GBps": round(nbytes * steps / t / 1e9, 2),
+                                   "frac_hbm_peak": round(nbytes * steps / t / 1e9 / HBM_PEAK_GBS, 4),
+                                   "lm_head_steady_us": round(head_us, 3),
+                                   "lm_head_steady_GBps": round(head_bytes / head_us / 1e3, 2),
+                                   "lm_head_steady_frac": round(head_bytes / head_us / 1e3 / HBM_PEAK_GBS, 4)}
+    log(f"qwen3 q4 stack: {out['qwen3-0.6b_decode_q4']}")
+    del g, calls
+    return out
+
+
 def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
     out = {}
 
@@ -516,21 +538,7 @@ def extra_decode(torch, B, inputs, workloads, steps, warmup, lib):
     log(f"config single gemv: {out['single_gemv_1024x1024_q4']}")
     del g, gc, qs, ss, cold_descs
 
-    # Qwen3-0.6B Q4 decode stack (197 calls, 335 MB per token)
-    calls, nbytes = build_decode_stack(workloads.QWEN3_06B, 1, B.Q4_G32, torch, B, inputs, workloads)
-    g = capture(torch, lambda s: [c(s) for c in calls])
-    t, _ = time_graph(torch, g, steps, warmup)
-    kh, nh = workloads.QWEN3_06B["lm_head"]
-    head_bytes = workloads.q4_bytes(kh, nh)
-    head_us = steady_launch_us(torch, B, calls[-1], copies=4, reps=12)
-    out["qwen3-0.6b_decode_q4"] = {"tokens_per_s": round(steps / t, 2), "ms_per_token": round(t / steps * 1e3, 4),
-                                   "weight_GBps": round(nbytes * steps / t / 1e9, 2),
-                                   "frac_hbm_peak": round(nbytes * steps / t / 1e9 / HBM_PEAK_GBS, 4),
-                                   "lm_head_steady_us": round(head_us, 3),
-                                   "lm_head_steady_GBps": round(head_bytes / head_us / 1e3, 2),
-                                   "lm_head_steady_frac": round(head_bytes / head_us / 1e3 / HBM_PEAK_GBS, 4)}
-    log(f"qwen3 q4 stack: {out['qwen3-0.6b_decode_q4']}")
-    del g, calls
+    out.update(extra_qwen_stack(torch, B, inputs, workloads, steps, warmup))
     torch.cuda.empty_cache()
 
     # Grouped dispatch (qmatmul_gemv_grouped): the Qwen3-0.6B and Llama-3.2-3B
@@ -975,7 +983,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--extra", choices=["all", "none", "tg", "decode", "prefill", "moe"], default="all",
+    ap.add_argument("--extra", choices=["all", "none", "tg", "decode", "prefill", "moe", "qwen-stack"], default="all",
                     help="other workloads to time after the headline step (subsets for profiling)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     args = ap.parse_args()
