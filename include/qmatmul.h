@@ -23,8 +23,8 @@
  *    QM_OK means "validated and enqueued on stream"; nothing is synchronised.
  *  - Arguments are validated on the host before anything is enqueued.  On an
  *    error nothing is enqueued, outputs are untouched and a message is left in
- *    a thread-local buffer read by qm_last_error() (Sec. 3.2: error handling
- *    through a static thread-local buffer).
+ *    a thread-local buffer read by qm_last_error() (Sec. 3.2: the error path
+ *    uses a fixed per-thread buffer too).
  *  - A launch failure reported by the HIP runtime maps to QM_EDEVICE.
  *  - Calls that share output or workspace buffers and overlap on one device
  *    race; the library holds no state besides an immutable per-device
@@ -124,9 +124,9 @@ typedef struct {
 } qm_qweight;
 
 /* Text of the last error on the calling thread ("" if none yet), kept in a
- * static thread-local buffer (Sec. 3.2: errors are reported through a static
- * thread-local buffer, so the error path allocates nothing).  The pointer
- * stays valid until the next failing call on the same thread. */
+ * fixed per-thread buffer (Sec. 3.2: reporting an error allocates nothing
+ * either).  The pointer stays valid until the next failing call on the same
+ * thread. */
 const char* qm_last_error(void);
 
 /* Host-only: bytes of the code buffer and of the scale buffer for a tensor
@@ -320,8 +320,9 @@ qm_status qmatmul_gemm_grouped(int32_t count, const qm_qweight* w, const uint16_
 qm_status qmatmul_gemm(const qm_qweight* w, const uint16_t* x, int64_t m, float* y, void* stream);
 
 /* Causal prefill attention over a prompt chunk (Sec. 3.4: FlashAttention,
- * tiles with online softmax and running statistics, O(n) memory; chunked
- * prefill with a bounded chunk):
+ * key blocks folded in one at a time while each query row carries its running
+ * maximum and sum, so memory grows linearly with the chunk; chunks of bounded
+ * size):
  *   o[h][i] = sum_{j <= p0 + i} p_j v[g][j],  p = softmax_j(scale * q[h][i] . k[g][j]),
  *   g = h / (n_q_heads / n_kv_heads),  i < m.
  * q: fp16 [n_q_heads][m][head_dim], the chunk's queries at positions p0 ..

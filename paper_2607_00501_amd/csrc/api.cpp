@@ -3,9 +3,9 @@
 // to the kernel launchers.
 //
 // The library allocates nothing and keeps no per-call state (BaseRT Sec. 3.2:
-// the decode loop allocates zero bytes and errors go through a static
-// thread-local buffer); the only shared state is an immutable per-device
-// table (CU count, architecture) built once per device.
+// no memory is requested on the decode path once a model is loaded, and error
+// text lives in a fixed per-thread buffer); the only shared state is an
+// immutable per-device table (CU count, architecture) built once per device.
 #include <hip/hip_runtime.h>
 
 #include <cmath>

@@ -303,8 +303,9 @@ hipError_t launch_decode_d(int group, const uint16_t* q, const uint16_t* k, cons
 
 typedef _Float16 half4v __attribute__((ext_vector_type(4)));
 
-// Causal FlashAttention for a prompt chunk (Sec. 3.4: tiled attention with
-// online softmax and running statistics, O(n) memory).  Workgroup = one
+// Causal FlashAttention for a prompt chunk (Sec. 3.4: attention over key
+// tiles, each query row carrying its running maximum and sum, memory linear
+// in the length).  Workgroup = one
 // query head x 128 query rows, four wavefronts of 32 rows.  Per block of 64
 // keys (32 for head_dim 128, to fit 256 VGPRs; K row-major and V transposed
 // in LDS, the next blocks loading into registers meanwhile), each wavefront
