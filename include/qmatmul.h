@@ -369,7 +369,7 @@ qm_status qattn_prefill_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int
 qm_status qattn_decode_workspace_bytes(int32_t n_q_heads, int32_t head_dim, size_t* bytes);
 
 /* Decode attention over a pre-allocated KV cache (Sec. 3.2: the cache is
- * allocated to the maximum context length, laid out for coalesced reads;
+ * sized for the longest context up front, laid out for coalesced reads;
  * grouped-query attention as in the Llama 3.2 and Qwen3 models):
  *   o[h] = sum_t p_t v[g][t],  p = softmax_t(scale * q[h] . k[g][t]),
  *   g = h / (n_q_heads / n_kv_heads),  t < len.

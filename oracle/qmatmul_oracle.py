@@ -338,7 +338,7 @@ def attention_decode(q, k_cache, v_cache, length: int, scale: float) -> np.ndarr
     """One decode step of grouped-query attention, in fp64.
 
     q: [Hq][D]; k_cache, v_cache: [Hkv][Tmax][D], rows t < length valid
-    (the cache is allocated to the maximum context length, Sec. 3.2).  Query
+    (the cache is sized for the longest context up front, Sec. 3.2).  Query
     head h reads KV head h // (Hq / Hkv).  For each head:
       s_t = scale * (q_h . k_t),  p = softmax(s) over t < length,
       o_h = sum_t p_t v_t.

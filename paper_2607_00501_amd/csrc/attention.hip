@@ -1,6 +1,6 @@
-// Decode attention over a pre-allocated KV cache (BaseRT Sec. 3.2: the KV
-// cache is allocated to the maximum context length at load time, in a layout
-// chosen for coalesced access during attention; Sec. 3.3: attention is one of
+// Decode attention over a pre-allocated KV cache (BaseRT Sec. 3.2: the cache
+// is sized for the longest context when the model loads, and its layout is
+// picked so that attention reads it coalesced; Sec. 3.3: attention is one of
 // the paths whose operator sequence is fused).
 //
 // One decode step of grouped-query attention: query head h reads KV head
