@@ -35,8 +35,11 @@ are pinned by hand-worked cases: the RoPE angle of every pair against
 cos/sin of p * 10^-i (D = 8, theta = 10^4), a one-layer step whose output
 projection residual, FFN norm and SwiGLU branch each have a written-out
 value, and per-head q/k norms with non-uniform gains checked before RoPE
-through the cached key and the softmax weights.  Each of these fails when
-the schedule, the residuals, the norm order or the SiLU branch is changed.
+through the cached key and the softmax weights, and the Llama 3 frequency
+rule by its two outer regimes, the linear blend across its band (edges and
+midpoint) and the position-scaling identity when every frequency is
+stretched.  Each of these fails when the schedule, the residuals, the norm
+order, the SiLU branch or a branch of the frequency rule is changed.
 """
 
 from __future__ import annotations
@@ -400,14 +403,38 @@ def rmsnorm(x, w, eps: float) -> np.ndarray:
     return x / np.sqrt(np.mean(x * x) + eps) * np.asarray(w, dtype=np.float64)
 
 
-def rope(x, pos: int, theta: float) -> np.ndarray:
+def rope_frequencies(d: int, theta: float, scaling=None) -> np.ndarray:
+    """Rotation frequency of each pair i < D/2, fp64: theta^(-2i/D).
+
+    scaling = (factor, low_freq_factor, high_freq_factor, original_len)
+    applies the Llama 3 family's long-context rule to each frequency f with
+    wavelength w = 2 pi / f, taking L = original_len:
+      w < L / high_freq_factor  -> f (short wavelengths kept),
+      w > L / low_freq_factor   -> f / factor (long wavelengths stretched),
+      otherwise                 -> (1 - t) f / factor + t f,
+                                   t = (L / w - low_freq_factor) / (high_freq_factor - low_freq_factor),
+    so the middle band blends linearly in L / w between the two outer rules
+    (t = 0 and t = 1 at its edges).  The paper runs Llama 3.2 models without
+    stating their RoPE; this is the rule those models are published with."""
+    i = np.arange(d // 2)
+    f = float(theta) ** (-2.0 * i / d)
+    if scaling is None:
+        return f
+    factor, lo, hi, orig = (float(v) for v in scaling)
+    w = 2.0 * np.pi / f
+    t = (orig / w - lo) / (hi - lo)
+    mid = (1.0 - t) * f / factor + t * f
+    return np.where(w < orig / hi, f, np.where(w > orig / lo, f / factor, mid))
+
+
+def rope(x, pos: int, theta: float, scaling=None) -> np.ndarray:
     """Rotary position embedding of each head row of x [H][D] at position
     pos, pairing dimension i with i + D/2 (the Llama / Qwen convention):
-    angle_i = pos * theta^(-2i/D), (a, b) -> (a cos - b sin, b cos + a sin)."""
+    angle_i = pos * f_i with f_i from rope_frequencies (theta^(-2i/D) when
+    unscaled), (a, b) -> (a cos - b sin, b cos + a sin)."""
     x = np.asarray(x, dtype=np.float64)
     d = x.shape[-1]
-    i = np.arange(d // 2)
-    ang = pos * theta ** (-2.0 * i / d)
+    ang = pos * rope_frequencies(d, theta, scaling)
     c, s = np.cos(ang), np.sin(ang)
     a, b = x[..., :d // 2], x[..., d // 2:]
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
@@ -442,9 +469,12 @@ def decode_step(model: dict, token: int, pos: int, k_cache: np.ndarray, v_cache:
     at row pos), the attention output and the SwiGLU output.  The residual
     stream stays fp32 on the GPU and fp64 here.  A layer with "q_norm" and
     "k_norm" gains ([D], the Qwen3 layer) RMS-normalises every query and key
-    head over its D dimensions before RoPE.
+    head over its D dimensions before RoPE.  An optional "rope_scaling"
+    (factor, low_freq_factor, high_freq_factor, original_len) selects the
+    Llama 3 frequency rule of rope_frequencies.
     """
     hq, hkv, d, eps, theta = model["hq"], model["hkv"], model["d"], model["eps"], model["theta"]
+    scaling = model.get("rope_scaling")
     x = np.asarray(model["emb"][token], dtype=np.float64)
     for li, ly in enumerate(model["layers"]):
         h = f16(rmsnorm(x, ly["attn_norm"], eps))
@@ -453,8 +483,8 @@ def decode_step(model: dict, token: int, pos: int, k_cache: np.ndarray, v_cache:
         if "q_norm" in ly:
             q = np.stack([rmsnorm(r, ly["q_norm"], eps) for r in q])
             k = np.stack([rmsnorm(r, ly["k_norm"], eps) for r in k])
-        q = rope(q, pos, theta)
-        k = rope(k, pos, theta)
+        q = rope(q, pos, theta, scaling)
+        k = rope(k, pos, theta, scaling)
         v = (ly["wv"] @ h).reshape(hkv, d)
         k_cache[li, :, pos] = f16(k)
         v_cache[li, :, pos] = f16(v)

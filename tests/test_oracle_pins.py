@@ -13,7 +13,8 @@ the wrong branch of the SwiGLU) fails at least one of them:
   closed-form ratios, bucketing against Python's stable ``sorted``,
 * the MoE layer against dense evaluation, a top-1 special case, identical
   experts and a hand-computed scalar example; SiLU against its identities,
-* RoPE angles of every pair against hand values, and one-layer decode steps
+* RoPE angles of every pair against hand values, the Llama 3 frequency rule
+  by its regimes, band edges and blend, and one-layer decode steps
   whose residuals, norms, SwiGLU branch and per-head q/k norms have
   written-out closed forms.
 """
@@ -695,6 +696,59 @@ def test_rope_frequency_schedule_every_pair():
     # D = 4, theta = 100: angles p and p / 10
     r = O.rope(np.array([[1.0, 1.0, 0.0, 0.0]]), 2, 100.0)[0]
     assert np.allclose(r, [math.cos(2.0), math.cos(0.2), math.sin(2.0), math.sin(0.2)], atol=1e-15)
+
+
+def test_rope_llama3_frequency_rule():
+    """The Llama 3 long-context RoPE rule (factor, low, high, L): wavelengths
+    w = 2 pi / f below L / high keep f, above L / low become f / factor, and
+    in between the ratio f' / f runs linearly in L / w from 1 / factor (at
+    L / w = low) to 1 (at L / w = high).
+    D = 8, theta = 10^4: f = 1, 0.1, 0.01, 0.001 (w = 6.28, 62.8, 628, 6283);
+    with factor 4, low 1, high 4, L = 1000 the cut-offs are 250 and 1000, so
+    pairs 0 and 1 keep 1 and 0.1, pair 3 becomes 0.00025 and pair 2 lies in
+    the band."""
+    f = O.rope_frequencies(8, 1e4, (4, 1, 4, 1000))
+    assert f[0] == 1.0 and abs(f[1] - 0.1) <= 1e-17 and abs(f[3] - 0.00025) <= 1e-19
+    assert 0.01 / 4 < f[2] < 0.01
+    # no scaling at factor 1, whatever the band edges
+    assert np.allclose(O.rope_frequencies(64, 5e5, (1, 1, 4, 8192)), O.rope_frequencies(64, 5e5), rtol=1e-15, atol=0)
+    # the band: pick theta so that pair 2's wavelength 2 pi sqrt(theta) gives
+    # L / w = 1 (long edge), 1.5, 2.5 (the middle), 3.5, 4 (short edge)
+    for lw, ratio in ((1.0, 0.25), (1.5, 0.375), (2.5, (0.25 + 1.0) / 2), (3.5, 0.875), (4.0, 1.0)):
+        theta = (1000.0 / lw / (2 * math.pi)) ** 2
+        plain = O.rope_frequencies(8, theta)[2]
+        assert abs(O.rope_frequencies(8, theta, (4, 1, 4, 1000))[2] / plain - ratio) <= 1e-12, lw
+    # every frequency stretched (L tiny): the rotation at position p equals
+    # the unscaled one at p / factor; every frequency kept (L huge): unscaled
+    x = np.arange(1.0, 17.0).reshape(2, 8)
+    assert np.allclose(O.rope(x, 8, 1e4, (4, 1, 4, 1e-3)), O.rope(x, 2, 1e4), atol=1e-13)
+    assert np.array_equal(O.rope(x, 8, 1e4, (4, 1, 4, 1e12)), O.rope(x, 8, 1e4))
+    # the decode step threads the rule through: a one-layer step whose cached
+    # key is the projection rotated with the scaled frequencies
+    model_scaled = _rope_probe_model((4, 1, 4, 1e-3))
+    model_plain = _rope_probe_model(None)
+    kc = [np.zeros((1, 1, 16, 8)) for _ in range(2)]
+    vc = [np.zeros((1, 1, 16, 8)) for _ in range(2)]
+    O.decode_step(model_scaled, 1, 8, kc[0], vc[0])
+    O.decode_step(model_plain, 1, 2, kc[1], vc[1])
+    assert np.allclose(kc[0][0, 0, 8], kc[1][0, 0, 2], atol=1e-3)     # fp16 rows of the same rotation
+    assert not np.allclose(kc[0][0, 0, 8], O.f16(O.rope(model_plain["probe_k"][None], 8, 1e4))[0], atol=1e-3)
+
+
+def _rope_probe_model(scaling):
+    """One layer, head_dim 8, one query and one KV head; the key projection
+    reads a fixed 8-vector out of the normed embedding."""
+    h, d = 8, 8
+    emb = np.zeros((4, h)); emb[1] = np.arange(1.0, 9.0)
+    wk = np.eye(d)
+    z = lambda *sh: np.zeros(sh)
+    ly = dict(wq=z(d, h), wk=wk, wv=z(d, h), wo=z(h, d), wg=z(4, h), wu=z(4, h), wd=z(h, 4),
+              attn_norm=np.ones(h), ffn_norm=np.ones(h))
+    m = dict(emb=emb, layers=[ly], norm=np.ones(h), lm_head=np.zeros((4, h)), hq=1, hkv=1, d=d, eps=1e-6,
+             theta=1e4, probe_k=O.rmsnorm(np.arange(1.0, 9.0), np.ones(h), 1e-6))
+    if scaling is not None:
+        m["rope_scaling"] = scaling
+    return m
 
 
 def _h(v: float) -> float:
