@@ -255,6 +255,20 @@ qm_status qdec_swiglu_f16(const float* gate, const float* up, int64_t n, uint16_
  * once per cache (Sec. 3.2: RoPE). */
 qm_status qdec_rope_table(int64_t max_len, int32_t head_dim, float theta, float* table, void* stream);
 
+/* The same table for the Llama 3 models' long-context RoPE (the Llama 3.2
+ * models of Sec. 4 carry it; the paper does not restate it): each pair's
+ * frequency f = theta^(-2i/head_dim), of wavelength w = 2 pi / f, is kept
+ * while w < original_len / high_freq_factor, divided by factor while
+ * w > original_len / low_freq_factor, and in between blended as
+ * (1 - t) f / factor + t f, t = (original_len / w - low_freq_factor) /
+ * (high_freq_factor - low_freq_factor); a = p * f in fp64.  Needs finite
+ * factor >= 1, 0 < low_freq_factor < high_freq_factor, original_len > 0
+ * (else QM_EINVAL); shapes, alignment and layout as qdec_rope_table.  Every
+ * entry point that takes a (cos, sin) table applies it as given, so a decoder
+ * that passes this table everywhere runs the scaled RoPE. */
+qm_status qdec_rope_table_llama3(int64_t max_len, int32_t head_dim, float theta, float factor, float low_freq_factor,
+                                 float high_freq_factor, float original_len, float* table, void* stream);
+
 /* The q/k/v projections of a decode step in one launch, with the attention
  * norm folded in (as qmatmul_gemv_grouped_rmsnorm) and RoPE plus the cache
  * append as the GEMV epilogue (Sec. 3.3: each fusion removes a launch).

@@ -31,7 +31,7 @@ EXPORTS = ("qm_last_error", "qm_weight_bytes", "qm_quantise", "qm_dequantise", "
            "qmoe_grouped_gemm", "qmoe_grouped_gemm_noalloc", "qm_device_config", "qattn_decode_workspace_bytes", "qattn_decode",
            "qattn_prefill", "qdec_embed", "qdec_rmsnorm", "qdec_rope_append", "qdec_cast_f16",
            "qdec_argmax", "qmatmul_gemv_swiglu_f16", "qattn_decode_f16", "qmatmul_gemv_grouped_rmsnorm",
-           "qmatmul_gemv_swiglu_rmsnorm_f16", "qdec_rope_table",
+           "qmatmul_gemv_swiglu_rmsnorm_f16", "qdec_rope_table", "qdec_rope_table_llama3",
            "qmatmul_gemv_qkv_rmsnorm_rope", "qdec_embed_rows", "qdec_rope_append_rows", "qdec_heads_to_rows_f16",
            "qdec_swiglu_f16", "qattn_prefill_workspace_bytes", "qattn_prefill_rows_f16")
 
@@ -85,6 +85,8 @@ def lib() -> ctypes.CDLL:
             "qdec_embed": [vp, i64, i64, vp, vp, vp],
             "qmatmul_gemv_swiglu_f16": [W, W, vp, vp, vp],
             "qdec_rope_table": [i64, i32, ctypes.c_float, vp, vp],
+            "qdec_rope_table_llama3": [i64, i32, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                       ctypes.c_float, vp, vp],
             "qdec_embed_rows": [vp, i64, i64, vp, i64, vp, vp],
             "qdec_rope_append_rows": [vp, vp, vp, i32, i32, i32, i64, i64, i64, ctypes.c_float, i32, vp, vp,
                                       ctypes.c_float, vp, i64, vp, vp, vp, vp],
@@ -345,6 +347,16 @@ def qdec_rope_table(max_len: int, head_dim: int, theta: float, device="cuda", st
     """fp32 [max_len][head_dim/2][2] (cos, sin) table."""
     t = torch.empty((max_len, head_dim // 2, 2), dtype=torch.float32, device=device)
     _check(lib().qdec_rope_table(max_len, head_dim, theta, _ptr(t), _stream(stream)))
+    return t
+
+
+def qdec_rope_table_llama3(max_len: int, head_dim: int, theta: float, scaling, device="cuda",
+                           stream=None) -> torch.Tensor:
+    """The (cos, sin) table with the Llama 3 long-context frequencies;
+    scaling = (factor, low_freq_factor, high_freq_factor, original_len)."""
+    factor, low, high, orig = (float(v) for v in scaling)
+    t = torch.empty((max_len, head_dim // 2, 2), dtype=torch.float32, device=device)
+    _check(lib().qdec_rope_table_llama3(max_len, head_dim, theta, factor, low, high, orig, _ptr(t), _stream(stream)))
     return t
 
 

@@ -353,6 +353,25 @@ qm_status qdec_rope_table(int64_t max_len, int32_t head_dim, float theta, float*
                   "qdec_rope_table");
 }
 
+qm_status qdec_rope_table_llama3(int64_t max_len, int32_t head_dim, float theta, float factor, float low_freq_factor,
+                                 float high_freq_factor, float original_len, float* table, void* stream) {
+  if ((head_dim != 64 && head_dim != 128) || max_len < 1 || max_len > kAttnMaxLen)
+    return fail(QM_ESHAPE, "qdec_rope_table_llama3: head_dim 64 or 128 and 1 <= max_len <= %lld",
+                (long long)kAttnMaxLen);
+  if (!(theta > 1.0f) || theta == INFINITY) return fail(QM_EINVAL, "qdec_rope_table_llama3: theta must be finite and > 1");
+  if (!(factor >= 1.0f) || factor == INFINITY || !(low_freq_factor > 0.0f) ||
+      !(high_freq_factor > low_freq_factor) || high_freq_factor == INFINITY || !(original_len > 0.0f) ||
+      original_len == INFINITY)
+    return fail(QM_EINVAL, "qdec_rope_table_llama3: need finite factor >= 1, 0 < low_freq_factor < high_freq_factor "
+                           "and original_len > 0");
+  if (!table) return fail(QM_EINVAL, "qdec_rope_table_llama3: null table");
+  if ((reinterpret_cast<uintptr_t>(table) & 7u) != 0)
+    return fail(QM_EALIGN, "qdec_rope_table_llama3: table 8-byte aligned");
+  return launched(launch_rope_table_llama3(max_len, head_dim, theta, factor, low_freq_factor, high_freq_factor,
+                                           original_len, table, static_cast<hipStream_t>(stream)),
+                  "qdec_rope_table_llama3");
+}
+
 qm_status qmatmul_gemv_qkv_rmsnorm_rope(const qm_qweight* w, const float* x, const float* residual,
                                         const uint16_t* gain, float eps, float* x_out, int32_t n_q_heads,
                                         int32_t n_kv_heads, int32_t head_dim, int64_t pos, int64_t max_len,

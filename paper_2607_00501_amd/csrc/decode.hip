@@ -210,6 +210,19 @@ __global__ __launch_bounds__(256) void rope_table_kernel(int64_t max_len, int d,
     table[e] = rope_cos_sin(e / (d / 2), static_cast<int>(e % (d / 2)), d, log2_theta);
 }
 
+// The same table with the frequencies of the Llama 3 long-context rule.
+__global__ __launch_bounds__(256) void rope_table_llama3_kernel(int64_t max_len, int d, double log2_theta,
+                                                                double factor, double low, double high, double orig,
+                                                                float2* __restrict__ table) {
+#pragma clang fp contract(off)
+  const int64_t n = max_len * (d / 2);
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) {
+    const double ang = static_cast<double>(e / (d / 2)) *
+                       rope_freq_llama3(static_cast<int>(e % (d / 2)), d, log2_theta, factor, low, high, orig);
+    table[e] = make_float2(static_cast<float>(cos(ang)), static_cast<float>(sin(ang)));
+  }
+}
+
 // Prompt (prefill) glue: the same operations over m tokens.
 // x[r] = table[tokens[r]] (NaN rows for ids outside the vocabulary).
 __global__ __launch_bounds__(256) void embed_rows_kernel(const uint16_t* __restrict__ table, int64_t vocab,
@@ -418,6 +431,14 @@ hipError_t launch_rope_append(const float* q, const float* k, const float* v, in
 hipError_t launch_rope_table(int64_t max_len, int32_t d, float theta, float* table, hipStream_t st) {
   hipLaunchKernelGGL(rope_table_kernel, dim3(spread_blocks(max_len * (d / 2))), dim3(256), 0, st, max_len, d,
                      std::log2(static_cast<double>(theta)), reinterpret_cast<float2*>(table));
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table_llama3(int64_t max_len, int32_t d, float theta, float factor, float low, float high,
+                                    float orig, float* table, hipStream_t st) {
+  hipLaunchKernelGGL(rope_table_llama3_kernel, dim3(spread_blocks(max_len * (d / 2))), dim3(256), 0, st, max_len, d,
+                     std::log2(static_cast<double>(theta)), static_cast<double>(factor), static_cast<double>(low),
+                     static_cast<double>(high), static_cast<double>(orig), reinterpret_cast<float2*>(table));
   return hipGetLastError();
 }
 

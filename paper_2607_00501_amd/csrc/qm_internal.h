@@ -184,6 +184,8 @@ hipError_t launch_rope_append(const float* q, const float* k, const float* v, in
                               hipStream_t st);
 hipError_t launch_cast_f16(const float* x, int64_t n, uint16_t* y, hipStream_t st);
 hipError_t launch_rope_table(int64_t max_len, int32_t d, float theta, float* table, hipStream_t st);
+hipError_t launch_rope_table_llama3(int64_t max_len, int32_t d, float theta, float factor, float low, float high,
+                                    float orig, float* table, hipStream_t st);
 hipError_t launch_embed_rows(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* tokens, int64_t m,
                              float* x, hipStream_t st);
 hipError_t launch_rope_append_rows(const float* q, const float* k, const float* v, int32_t hq, int32_t hkv, int32_t d,

@@ -30,6 +30,9 @@ class DecoderConfig:
     layers: int
     eps: float = 1e-6
     theta: float = 1e6
+    # (factor, low_freq_factor, high_freq_factor, original_len): the Llama 3
+    # long-context RoPE frequencies (None: plain theta^(-2i/D))
+    rope_scaling: Optional[tuple] = None
 
 
 @dataclass
@@ -82,7 +85,9 @@ class DenseDecoder:
             "per-head q/k norms need whole heads: use the RoPE kernel (rows not interleaved)"
         # (cos, sin) of every cache position, built once: read by the q/k/v
         # GEMV's RoPE epilogue and by the prompt path's RoPE kernel.
-        self.rope_tab = B.qdec_rope_table(max_len, c.head_dim, c.theta, device=dev)
+        # every RoPE of the step and of the prompt path reads this table
+        self.rope_tab = (B.qdec_rope_table(max_len, c.head_dim, c.theta, device=dev) if c.rope_scaling is None else
+                         B.qdec_rope_table_llama3(max_len, c.head_dim, c.theta, c.rope_scaling, device=dev))
         self.h = torch.zeros(c.hidden, **f16)             # normed input of a projection
         self.q, self.k, self.v = torch.zeros(qd, **f32), torch.zeros(kvd, **f32), torch.zeros(kvd, **f32)
         self.q16 = torch.zeros((c.n_q_heads, c.head_dim), **f16)

@@ -28,13 +28,17 @@ QWEN3_30B_A3B_MOE = dict(name="qwen3-30b-a3b moe layer", hidden=2048, inter=768,
 
 # Whole dense decoders (attention geometry, FFN width, vocabulary) for the
 # end-to-end decode benchmark: tg128, 128 greedy tokens from an empty cache
-# (Sec. 4.1).  RoPE uses the plain theta of each model.
+# (Sec. 4.1).  RoPE: each model's theta; the Llama 3.2 models with their
+# long-context frequency rule (factor 32, low / high frequency factors 1 / 4,
+# original length 8192).
 QWEN3_06B_DECODER = dict(name="qwen3-0.6b", hidden=1024, n_q_heads=16, n_kv_heads=8, head_dim=128, inter=3072,
                          vocab=151936, layers=28, theta=1e6)
 LLAMA32_1B_DECODER = dict(name="llama-3.2-1b", hidden=2048, n_q_heads=32, n_kv_heads=8, head_dim=64, inter=8192,
-                          vocab=128256, layers=16, theta=5e5)
+                          vocab=128256, layers=16, theta=5e5,
+                          rope_scaling=(32, 1, 4, 8192))
 LLAMA32_3B_DECODER = dict(name="llama-3.2-3b", hidden=3072, n_q_heads=24, n_kv_heads=8, head_dim=128, inter=8192,
-                          vocab=128256, layers=28, theta=5e5)
+                          vocab=128256, layers=28, theta=5e5,
+                          rope_scaling=(32, 1, 4, 8192))
 
 SINGLE_GEMV = dict(name="single q4 gemv 1024x1024", k=1024, n=1024)
 

@@ -391,6 +391,12 @@ def test_qkv_rope_epilogue_validation():
     assert L.qdec_rope_table(0, 64, 1e4, p, None) == 2 and L.qdec_rope_table(8, 80, 1e4, p, None) == 2
     assert L.qdec_rope_table(8, 64, 1.0, p, None) == 1 and L.qdec_rope_table(8, 64, 1e4, None, None) == 1
     assert L.qdec_rope_table(8, 64, 1e4, ctypes.c_void_p(0x50004), None) == 3
+    rt3 = lambda n=8, d=64, theta=5e5, f=32.0, lo=1.0, hi=4.0, orig=8192.0, t=p: \
+        L.qdec_rope_table_llama3(n, d, theta, f, lo, hi, orig, t, None)
+    assert rt3(n=0) == 2 and rt3(d=96) == 2 and rt3(n=300000) == 2
+    assert rt3(theta=1.0) == 1 and rt3(f=0.5) == 1 and rt3(f=float("inf")) == 1 and rt3(f=float("nan")) == 1
+    assert rt3(lo=0.0) == 1 and rt3(hi=1.0) == 1 and rt3(hi=float("inf")) == 1 and rt3(orig=0.0) == 1
+    assert rt3(orig=float("nan")) == 1 and rt3(t=None) == 1 and rt3(t=ctypes.c_void_p(0x50004)) == 3
     assert B.qm_last_error()
 
 

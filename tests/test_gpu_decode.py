@@ -206,6 +206,8 @@ def _model(cfg: DecoderConfig, tag: int, fmts=(O.Q4, B.Q4_G32), interleave=False
     head_dev, head_ref = proj("lm_head", 0, cfg.vocab, cfg.hidden)
     ref = dict(emb=emb.astype(np.float64), layers=ref_layers, norm=norm.astype(np.float64), lm_head=head_ref,
                hq=cfg.n_q_heads, hkv=cfg.n_kv_heads, d=cfg.head_dim, eps=cfg.eps, theta=cfg.theta)
+    if cfg.rope_scaling is not None:
+        ref["rope_scaling"] = cfg.rope_scaling
     return dev_layers, torch.from_numpy(emb).cuda(), torch.from_numpy(norm).cuda(), head_dev, ref
 
 
@@ -452,6 +454,48 @@ def test_gemv_swiglu_rmsnorm_other_formats(fmt, n, k):
 @pytest.mark.parametrize("d,hq,hkv,k", [(64, 4, 2, 256), (128, 24, 8, 3072)])
 def test_gemv_qkv_rmsnorm_rope_other_formats(fmt, d, hq, hkv, k):
     test_gemv_qkv_rmsnorm_rope_matches_separate_launches(fmt, d, hq, hkv, k, 5)
+
+
+@pytest.mark.parametrize("d,theta,scaling", [(64, 5e5, (32, 1, 4, 8192)), (128, 5e5, (32, 1, 4, 8192)),
+                                              (64, 1e4, (4, 1, 4, 1000)), (128, 1e6, (8, 2, 3, 4096))])
+def test_rope_table_llama3_matches_the_oracle_frequencies(d, theta, scaling):
+    """qdec_rope_table_llama3 against cos/sin of p * f_i with the oracle's
+    scaled frequencies (every regime of the rule occurs in these shapes)."""
+    n = 9000
+    t = B.qdec_rope_table_llama3(n, d, theta, scaling).cpu().numpy().astype(np.float64)
+    f = O.rope_frequencies(d, theta, scaling)
+    w = 2 * np.pi / O.rope_frequencies(d, theta)
+    assert (w < scaling[3] / scaling[2]).any() and (w > scaling[3] / scaling[1]).any()
+    ang = np.arange(n)[:, None] * f[None, :]
+    assert np.abs(t[..., 0] - np.cos(ang)).max() <= 2e-7 and np.abs(t[..., 1] - np.sin(ang)).max() <= 2e-7
+
+
+@pytest.mark.parametrize("fused,rope_epi,qk_norm", [(True, True, False), (False, False, False), (True, False, True)])
+def test_decode_and_prefill_with_llama3_rope(fused, rope_epi, qk_norm):
+    """A decoder with the Llama 3 RoPE frequencies (the table from
+    qdec_rope_table_llama3 read by every RoPE of the step and of the prompt
+    path): a 9-token prompt, then three decode steps, against the oracle's
+    token-by-token steps with the same rule."""
+    cfg = DecoderConfig(hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, inter=512, vocab=1000, layers=2,
+                        theta=5e5, rope_scaling=(32, 1, 4, 64))
+    dec, ref, kc, vc = _decoder(cfg, 31, 32, fused=fused, rope_epi=rope_epi, qk_norm=qk_norm)
+    toks = [5, 17, 999, 0, 42, 42, 7, 300, 1]
+    for p, t in enumerate(toks):
+        want = O.decode_step(ref, t, p, kc, vc)
+    dec.prefill(torch.tensor(toks, dtype=torch.int32, device="cuda"))
+    assert rel_err(dec.logits.cpu().numpy(), want) <= 1e-2
+    for p, t in enumerate([3, 4, 5], start=len(toks)):
+        dec.token.fill_(t)
+        dec.step(p)
+        assert rel_err(dec.logits.cpu().numpy(), O.decode_step(ref, t, p, kc, vc)) <= 1e-2, p
+    n = len(toks) + 3
+    assert rel_err(dec.k_cache[:, :, :n].cpu().numpy().astype(np.float64), kc[:, :, :n]) <= 1e-2
+    # the rule matters at these positions: the plain-RoPE oracle disagrees
+    plain = dict(ref); plain.pop("rope_scaling")
+    kc2, vc2 = np.zeros_like(kc), np.zeros_like(vc)
+    for p, t in enumerate(toks + [3, 4, 5]):
+        O.decode_step(plain, t, p, kc2, vc2)
+    assert rel_err(dec.k_cache[:, :, :n].cpu().numpy().astype(np.float64), kc2[:, :, :n]) > 1e-2
 
 
 def test_rope_table_matches_the_rotation_angles():
