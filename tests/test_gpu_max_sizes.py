@@ -1,7 +1,9 @@
 """GPU parity at the largest sizes the boundary accepts in one call: GEMM
 and prefill attention at m = 65536, routing and bucketing of 65536 tokens,
 the MoE layer at m = 65536, and a 32768-row RoPE/cache append ending at the
-last row of a 262144-row cache.  Outputs are compared on sampled rows that
+last row of a 262144-row cache; and very long or very many weight rows
+(GEMV at K = 131072 and at a million rows, GEMM at K = 65536).  Outputs
+are compared on sampled rows that
 the oracle recomputes one by one (first, last and tile-boundary rows
 included); routing and bucketing are compared whole, bit for bit."""
 
@@ -125,3 +127,34 @@ def test_rope_append_rows_to_the_last_cache_row():
             assert np.all(np.abs(got - want) <= 2.0 ** -10 * np.abs(want) + 1e-6 * np.abs(want).max()), r
     assert np.array_equal(vc1[:, p0:].cpu().numpy(), v.cpu().numpy().reshape(m, hkv, d).transpose(1, 0, 2)
                           .astype(np.float16))
+
+
+@pytest.mark.parametrize("fmt", [(O.Q4, B.Q4_G32), (O.Q8, B.Q8_G32), (O.Q3, B.Q3_G32), (O.BF16, B.BF16)])
+@pytest.mark.parametrize("n,k", [(100, 131072), (1_000_003, 64)])
+def test_gemv_very_long_rows_and_very_many_rows(fmt, n, k):
+    """The decode GEMV with K = 131072 (4096 groups: many passes of every
+    lane over its chunks, activations from global memory) and with a
+    million rows at K = 64 (15,626 panels, a ragged last one); sampled
+    rows against the oracle at the GEMV tier."""
+    ofmt, bfmt = fmt
+    rng = np.random.default_rng(n + k)
+    rows = np.unique(np.concatenate([rng.choice(n, 64, replace=False), [0, 63, 64, n - 1]]))
+    w = inputs.weights_np(inputs.seed_for(5, n % 1000, "down", k), (n, k))
+    x = inputs.activations_np(inputs.seed_for(5, k, "x", 2), (k,))
+    wd = B.qm_repack(B.qm_quantise(torch.from_numpy(w).cuda(), bfmt), B.LAYOUT_DEVICE)
+    y = B.qmatmul_gemv(wd, torch.from_numpy(x).cuda()).cpu().numpy()
+    assert np.all(np.isfinite(y))
+    q, s = O.quantise(w[rows], ofmt)
+    ref = O.gemv(O.pack(q, ofmt), s, ofmt, x)
+    assert rel_err(y[rows], ref) <= 2e-3
+
+
+def test_gemm_very_long_rows():
+    """qmatmul_gemm with K = 65536 at m = 3 (a long split-K), all outputs."""
+    m, n, k = 3, 200, 65536
+    w = inputs.weights_np(inputs.seed_for(5, n, "up", k), (n, k))
+    x = inputs.activations_np(inputs.seed_for(5, m, "x", 3), (m, k))
+    wd = B.qm_repack(B.qm_quantise(torch.from_numpy(w).cuda(), B.Q4_G32), B.LAYOUT_DEVICE)
+    y = B.qmatmul_gemm(wd, torch.from_numpy(x).cuda()).cpu().numpy()
+    q, s = O.quantise(w, O.Q4)
+    assert rel_err(y, O.gemm(O.pack(q, O.Q4), s, O.Q4, x)) <= MFMA_TOL
